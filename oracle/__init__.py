@@ -1,0 +1,189 @@
+"""VarRate CPU oracle -- TEST INFRASTRUCTURE.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s CPU-baseline leg may import
+this package.  The product path (``paper_2607_15498_amd``) never imports it and shares no
+code with it.
+
+Thin ctypes wrapper over ``varrate_oracle.c`` (plain C, fp64, OpenMP over independent
+rows/tokens).  Each wrapper names the passage of the paper its C function follows; the
+readings of open points are documented beside the C functions.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "varrate_oracle.c")
+_LIB = os.path.join(_HERE, "libvarrate_oracle.so")
+
+_f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
+_f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
+_u32p = np.ctypeslib.ndpointer(np.uint32, flags="C_CONTIGUOUS")
+_i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
+_i64 = ctypes.c_int64
+_int = ctypes.c_int
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, no fast-math, no fp contraction, OpenMP)."""
+    if force or not os.path.exists(_LIB):
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+               "-fno-fast-math", "-fvisibility=hidden", "-Wall", "-o", _LIB, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = ctypes.CDLL(_LIB)
+        L.vro_budget.restype = _i64
+        L.vro_budget.argtypes = [_i64, _i64, _i64, _i64]
+        L.vro_threads.restype = _int
+        L.vro_salience.restype = None
+        L.vro_salience.argtypes = [_i64, _int, _int, _int, _int, _f32p, _f32p, _f64p]
+        L.vro_pool.restype = None
+        L.vro_pool.argtypes = [_f64p, _i64, _f32p]
+        L.vro_weights.restype = None
+        L.vro_weights.argtypes = [_f32p, _i64, _u32p]
+        L.vro_allocate.restype = _int
+        L.vro_allocate.argtypes = [_u32p, _i64, _i64, _int, _int, _i32p,
+                                   ctypes.POINTER(_i64), ctypes.POINTER(_i64),
+                                   ctypes.POINTER(_i64)]
+        L.vro_project.restype = None
+        L.vro_project.argtypes = [_i64, _int, _int, _f32p, _f32p, _i32p, _int, _f32p]
+        L.vro_decode.restype = None
+        L.vro_decode.argtypes = [_i64, _i64, _int, _int, _int, _f32p, _f32p, _i32p,
+                                 _f32p, _f32p, _f32p, _f32p, _f32p, _f64p]
+        _lib = L
+    return _lib
+
+
+def threads() -> int:
+    return int(lib().vro_threads())
+
+
+def _c(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+def budget(n: int, d: int, w: int, kappa_pct: int) -> int:
+    """Eq. (3), integer form: floor(kappa n d / 100) - w d."""
+    return int(lib().vro_budget(n, d, w, kappa_pct))
+
+
+def salience(K: np.ndarray, Qw: np.ndarray, H: int) -> np.ndarray:
+    """Eq. (4): s_t for the coded tokens t < n - w.  K [n][G][d], Qw [w][H][d]."""
+    n, G, d = K.shape
+    w = Qw.shape[0]
+    s = np.zeros(max(n - w, 0), np.float64)
+    lib().vro_salience(n, G, H, d, w, _c(K, np.float32), _c(Qw, np.float32), s)
+    return s
+
+
+def pool(s: np.ndarray) -> np.ndarray:
+    """Sec. 3.2 length-5 moving average, rounded to fp32."""
+    s = _c(s, np.float64)
+    out = np.zeros(s.shape[0], np.float32)
+    lib().vro_pool(s, s.shape[0], out)
+    return out
+
+
+def weights(sbar: np.ndarray) -> np.ndarray:
+    """Sec. 3.2 min-max normalisation as exact integer weights u_t in [1, 2^24 + 1]."""
+    sbar = _c(sbar, np.float32)
+    u = np.zeros(sbar.shape[0], np.uint32)
+    lib().vro_weights(sbar, sbar.shape[0], u)
+    return u
+
+
+@dataclass
+class Allocation:
+    rank: np.ndarray   # int32 [N]
+    k: int             # number of tokens capped at R
+    M: int             # B - R k - r_min (N - k)
+    Q: int             # sum of u over uncapped tokens
+
+
+class BudgetError(ValueError):
+    pass
+
+
+def allocate(u: np.ndarray, B: int, r_min: int, R: int) -> Allocation:
+    """Eq. (5) / Algorithm 1 water-filling + largest-remainder integer ranks."""
+    u = _c(u, np.uint32)
+    N = u.shape[0]
+    rank = np.zeros(N, np.int32)
+    k, M, Q = _i64(), _i64(), _i64()
+    rc = lib().vro_allocate(u, N, B, r_min, R, rank, ctypes.byref(k), ctypes.byref(M),
+                            ctypes.byref(Q))
+    if rc != 0:
+        raise BudgetError(f"infeasible budget B={B} for N={N}, r_min={r_min}, R={R}")
+    return Allocation(rank, int(k.value), int(M.value), int(Q.value))
+
+
+def project(X: np.ndarray, P: np.ndarray, rank: np.ndarray, storage: str) -> np.ndarray:
+    """Eq. (6) projection + nested truncation, rounded to the storage type ('bf16'|'f32')."""
+    n, G, d = X.shape
+    out = np.zeros((n, G, d), np.float32)
+    lib().vro_project(n, G, d, _c(X, np.float32), _c(P, np.float32), _c(rank, np.int32),
+                      1 if storage == "bf16" else 0, out)
+    return out
+
+
+def decode(coefK, coefV, rank, Kx, Vx, PK, PV, q, H: int) -> np.ndarray:
+    """Sec. 4.4 reconstruct-in-place decode for one query set q [H][d] -> [H][d] fp64."""
+    N, G, d = coefK.shape
+    n_exact = Kx.shape[0]
+    out = np.zeros((H, d), np.float64)
+    lib().vro_decode(N, n_exact, G, H, d, _c(coefK, np.float32), _c(coefV, np.float32),
+                     _c(rank, np.int32), _c(Kx, np.float32), _c(Vx, np.float32),
+                     _c(PK, np.float32), _c(PV, np.float32), _c(q, np.float32), out)
+    return out
+
+
+@dataclass
+class Compressed:
+    s: np.ndarray        # fp64 salience [N]
+    sbar: np.ndarray     # fp32 pooled salience [N] (allocation input)
+    u: np.ndarray        # uint32 weights [N]
+    alloc: Allocation
+    B: int
+    coefK: np.ndarray    # [N][G][d] float32 holding storage-rounded values
+    coefV: np.ndarray
+    Kx: np.ndarray       # exact tail [w][G][d]
+    Vx: np.ndarray
+
+
+def compress(K, V, Qw, PK, PV, H: int, kappa_pct: int, r_min: int, storage: str,
+             sbar: np.ndarray | None = None) -> Compressed:
+    """Algorithm 1 for one layer (anchor-free, RoPE-free, per-head bases).
+
+    ``sbar`` optionally replaces the salience stage (used to run the allocation on a
+    supplied fp32 signal, e.g. a constant one for the uniform-rank codec)."""
+    n, G, d = K.shape
+    w = Qw.shape[0]
+    N = n - w
+    B = budget(n, d, w, kappa_pct)
+    if sbar is None:
+        s = salience(K, Qw, H)
+        sb = pool(s)
+    else:
+        s = np.full(N, np.nan)
+        sb = _c(sbar, np.float32)
+    u = weights(sb)
+    al = allocate(u, B, r_min, d)
+    cK = project(K[:N], PK, al.rank, storage)
+    cV = project(V[:N], PV, al.rank, storage)
+    return Compressed(s, sb, u, al, B, cK, cV, np.ascontiguousarray(K[N:]),
+                      np.ascontiguousarray(V[N:]))
