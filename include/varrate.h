@@ -1,0 +1,191 @@
+/*
+ * varrate.h -- C ABI of the variable-rank KV codec (VarRate, arXiv 2607.15498) for one
+ * MI355X (gfx950) GPU.
+ *
+ * The codec compresses one layer's prompt KV cache (Algorithm 1) in three steps:
+ *   1. salience   Sec. 3.2 Eq. (4): attention that the last w queries (the observation
+ *                 window) pay each earlier token, averaged over the window and all query
+ *                 heads, then the length-5 moving average;
+ *   2. allocation Sec. 3.2 Eq. (5) + Sec. 3.1 Eq. (3): water-filling of the coded budget B
+ *                 into one integer rank per token, floor r_min, cap R = d, sum = B exactly;
+ *   3. projection Sec. 3.3 Eq. (6): each token's key and value are projected onto per-KV-head
+ *                 orthonormal bases and truncated to the token's rank.
+ * Decode (Sec. 4.4 "Cost" notes a fused kernel is what realises the saving) attends over
+ * the compressed cache directly in rank space: the query is rotated into the key basis,
+ * ragged coefficient rows are streamed, and the rank-space output is rotated back.
+ *
+ * Conventions for every entry point
+ *   - All data pointers are DEVICE pointers (hipMalloc / torch CUDA tensors) owned by the
+ *     caller unless stated otherwise; descriptors (varrate_shape, varrate_cache) are host
+ *     structs.  Tensors are contiguous row-major, base addresses 16-byte aligned.
+ *   - `stream` is a hipStream_t passed as void*; all device work is enqueued on it
+ *     asynchronously.  No entry point synchronises the host, allocates device memory or
+ *     keeps state between calls.
+ *   - Arguments are validated synchronously before anything is enqueued; on error nothing
+ *     is enqueued and a negative status is returned.  varrate_last_error() then returns a
+ *     thread-local message.
+ *   - Token notation: n = cached prompt tokens (window included), w = exact window = the
+ *     observation window (last w tokens), N = n - w coded tokens, G KV heads, H query heads
+ *     (H a multiple of G; query head h reads KV head h / (H/G)), d = 128 head dim.
+ *   - dtype (VARRATE_BF16 or VARRATE_F32) is the storage type of K, V, window queries,
+ *     decode queries, coefficients and decode outputs.  Bases are always fp32.
+ *   - Workspaces are caller-allocated device buffers; their sizes come from the
+ *     *_workspace_bytes functions.  A workspace must be zero-filled once before its first
+ *     use; every call leaves it in that state again on completion (its counters reset
+ *     themselves).  Calls that overlap in time on one workspace race.
+ */
+#ifndef VARRATE_H
+#define VARRATE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define VARRATE_API __attribute__((visibility("default")))
+
+/* ---- status codes -------------------------------------------------------------------- */
+#define VARRATE_OK            0
+#define VARRATE_EINVAL       -1   /* null pointer, bad shape/dtype, misaligned, small buffer */
+#define VARRATE_EBUDGET      -2   /* N r_min > B, B > N R, or nothing to code (N <= 0)       */
+#define VARRATE_EUNSUPPORTED -3   /* d != 128, H not a multiple of G, too many rows          */
+#define VARRATE_EHIP         -4   /* a HIP launch or runtime call failed                      */
+
+#define VARRATE_F32  0
+#define VARRATE_BF16 1
+
+#define VARRATE_HEAD_DIM 128   /* d = R: the bases are square, so full rank is exact        */
+#define VARRATE_CHUNK    256   /* tokens per layout chunk (see varrate_cache)                */
+#define VARRATE_COEF_PAD 64    /* extra elements after B in every coefficient stream         */
+#define VARRATE_MAX_SEQS 64    /* sequences per varrate_decode_attn call                     */
+#define VARRATE_MAX_QROWS 256  /* queries x heads-per-KV-head per sequence in one decode     */
+
+/* One layer's problem statement (Algorithm 1 inputs). */
+typedef struct varrate_shape {
+    int64_t n;          /* cached prompt tokens, window included                            */
+    int32_t G;          /* KV heads                                                         */
+    int32_t H;          /* query heads (multiple of G)                                      */
+    int32_t d;          /* head dim; must be 128                                            */
+    int32_t w;          /* exact window = observation window, 1 <= w < n                    */
+    int32_t r_min;      /* rank floor, 0 <= r_min <= 128                                    */
+    int32_t kappa_pct;  /* KV budget kappa as an integer percent, 1..100                     */
+    int32_t dtype;      /* VARRATE_BF16 or VARRATE_F32                                      */
+    int32_t reserved;
+} varrate_shape;
+
+/*
+ * A compressed layer of one sequence.  The layout is part of the contract:
+ *   - Coded tokens t in [0, N) are split into chunks of VARRATE_CHUNK consecutive tokens
+ *     (the last chunk is ragged); n_chunks = ceil(N / VARRATE_CHUNK).
+ *   - rank[t] (original order) is the integer rank of token t (Eq. 5, sum = B).
+ *   - chunk_off[c] = sum of rank[t] over chunks before c; chunk_off[n_chunks] = B.
+ *   - Inside chunk c the tokens are stored in order of (rank descending, index
+ *     ascending); stored position i (global, i in [0, N)) holds token sidx[i] with rank
+ *     srank[i].  Stored token i's coefficients occupy, in every head stream,
+ *         coef[g * coef_stride + chunk_off[c] + sum_{chunk-mates i' < i} srank[i'] + j],
+ *     j < srank[i]: the leading srank[i] coordinates of its projection onto the basis
+ *     (row j of P = j-th direction).  Coefficients are stored in `dtype`.
+ *   - k_exact/v_exact hold exact rows: slot e < w is token N + e (the window); slots
+ *     e >= w are tokens appended after compression (varrate_append_exact).
+ * All pointers are device memory owned by the caller; sizes come from
+ * varrate_cache_bytes().  n_exact is advanced on the host by varrate_compress (to w) and
+ * varrate_append_exact.
+ */
+typedef struct varrate_cache {
+    void*     coef_k;       /* [G][coef_stride] dtype                                      */
+    void*     coef_v;       /* [G][coef_stride] dtype                                      */
+    uint8_t*  rank;         /* [N]                                                          */
+    uint8_t*  srank;        /* [N] ranks in stored order                                    */
+    uint32_t* sidx;         /* [N] stored position -> original token index                  */
+    uint32_t* chunk_off;    /* [n_chunks + 1]                                               */
+    void*     k_exact;      /* [G][cap][d] dtype                                            */
+    void*     v_exact;      /* [G][cap][d] dtype                                            */
+    int64_t   coef_stride;  /* elements per head stream, >= B + VARRATE_COEF_PAD           */
+    int64_t   cap;          /* exact-slot capacity, >= w                                    */
+    int64_t   n_exact;      /* exact slots in use                                           */
+    int64_t   N;            /* coded tokens                                                 */
+    int64_t   B;            /* coded budget (coefficients per head stream)                  */
+} varrate_cache;
+
+/* Buffer sizes (bytes) a caller must allocate for one varrate_cache. */
+typedef struct varrate_cache_bytes_t {
+    int64_t N, B, n_chunks, coef_stride;
+    size_t coef_k, coef_v, rank, srank, sidx, chunk_off, k_exact, v_exact;
+} varrate_cache_bytes_t;
+
+/* ---- diagnostics ---------------------------------------------------------------------- */
+VARRATE_API const char* varrate_status_string(int status);
+VARRATE_API const char* varrate_last_error(void);   /* thread-local text of the last failure           */
+VARRATE_API int varrate_version(void);               /* ABI version (1)                                 */
+
+/* ---- sizing ----------------------------------------------------------------------------- */
+/* Coded budget of Sec. 3.1 Eq. (3) in per-head coefficient units, with kappa an integer
+ * percent: B = floor(kappa_pct * n * d / 100) - w * d (the exact window costs w d).       */
+VARRATE_API int64_t varrate_coded_budget(int64_t n, int32_t d, int32_t w, int32_t kappa_pct);
+
+/* Validates the shape and budget feasibility (EBUDGET when N r_min > B or B > N d) and
+ * fills the buffer sizes of one cache with exact capacity `cap` (>= w).                     */
+VARRATE_API int varrate_cache_bytes(const varrate_shape* shape, int64_t cap, varrate_cache_bytes_t* out);
+
+/* Workspace for varrate_salience / varrate_allocate / varrate_project / varrate_compress. */
+VARRATE_API size_t varrate_compress_workspace_bytes(const varrate_shape* shape);
+/* Workspace for varrate_decode_attn over S sequences of this shape with Q queries each. */
+VARRATE_API size_t varrate_decode_workspace_bytes(const varrate_shape* shape, int32_t S, int32_t Q);
+
+/* ---- stages ------------------------------------------------------------------------------ */
+/* Sec. 3.2 Eq. (4) + length-5 moving average.
+ * K: [n][G][d] dtype keys; Qw: [w][H][d] dtype observation-window queries (query i sits at
+ * position n - w + i and attends causally to keys 0..n-w+i).  Writes sbar [N] fp32:
+ *   s_t = (1/(w H)) sum_i sum_h softmax_t(<q_{i,h}, k_{t,g(h)}> / sqrt(d)),
+ *   sbar_t = (s_{t-2} + ... + s_{t+2}) / 5 (out-of-range terms zero).                        */
+VARRATE_API int varrate_salience(const varrate_shape* shape, const void* K, const void* Qw, float* sbar,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Sec. 3.2 Eq. (5) water-filling on a given pooled salience sbar [N] fp32 (device).
+ * Min-max normalisation to integer weights u_t = 1 + floor(2^24 (sbar_t - min)/(max - min))
+ * (all equal when max == min), exact-integer water-filling with floor r_min and cap d, and
+ * largest-remainder integer ranks (ties: larger u_t, then lower t) so that sum = B.
+ * Writes cache->rank and cache->chunk_off; sets cache->N and cache->B.  Bit-exact and
+ * deterministic given sbar.                                                                 */
+VARRATE_API int varrate_allocate(const varrate_shape* shape, const float* sbar, varrate_cache* cache,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Sec. 3.3 Eq. (6): projects K[0:N] and V[0:N] ([n][G][d] dtype) onto the bases
+ * P_K, P_V ([G][d][d] fp32, row j = j-th direction, orthonormal rows) and keeps the leading
+ * rank[t] coefficients of every token in the stored layout (needs cache->rank and
+ * cache->chunk_off from varrate_allocate).  Fills srank, sidx, coef_k, coef_v, copies the
+ * window rows K[N:n], V[N:n] into exact slots 0..w-1 and sets cache->n_exact = w.           */
+VARRATE_API int varrate_project(const varrate_shape* shape, const void* K, const void* V,
+                    const float* P_K, const float* P_V, varrate_cache* cache,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Algorithm 1 for one layer: varrate_salience -> varrate_allocate -> varrate_project.
+ * sbar_out ([N] fp32, device) receives the pooled salience when non-NULL.                   */
+VARRATE_API int varrate_compress(const varrate_shape* shape, const void* K, const void* V, const void* Qw,
+                     const float* P_K, const float* P_V, varrate_cache* cache, float* sbar_out,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Appends one decode-time token (k_new, v_new: [G][d] dtype, device) to the exact slots
+ * (tokens generated after compression stay exact).  EINVAL when the capacity is full.       */
+VARRATE_API int varrate_append_exact(const varrate_shape* shape, varrate_cache* cache, const void* k_new,
+                         const void* v_new, void* stream);
+
+/* Rank-space decode attention (the fused decode Sec. 4.4 calls for).
+ * caches: host array of S compressed sequences of this shape (same layer, same bases).
+ * q:   [S][Q][H][d] dtype decode queries (Q queries share each sequence's cache).
+ * out: [S][Q][H][d] dtype.
+ * For every sequence, query and head h (KV head g = h / (H/G)):
+ *   q' = P_K[g] q / sqrt(d);  coded token t scores <q'[0:r_t], c^K_t>, exact slots score
+ *   <q, k_e>/sqrt(d); softmax over all of them; out = P_V[g]^T (sum_t p_t c^V_t) +
+ *   sum_e p_e v_e, which equals attention over the reconstructed cache of Eq. (6).
+ * Constraints: S <= VARRATE_MAX_SEQS, Q * H / G <= VARRATE_MAX_QROWS.                       */
+VARRATE_API int varrate_decode_attn(const varrate_shape* shape, const varrate_cache* caches, int32_t S,
+                        const void* q, int32_t Q, const float* P_K, const float* P_V,
+                        void* out, void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VARRATE_H */

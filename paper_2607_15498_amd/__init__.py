@@ -1,0 +1,246 @@
+"""VarRate variable-rank KV codec on MI355X: Python binding of libvarrate (HIP, gfx950).
+
+Torch supplies device memory and the current stream; every step of the codec runs in the
+HIP kernels behind the C ABI of ``include/varrate.h``.  There is no CPU fallback: the
+functions raise when the library is missing or a call fails.
+
+    shape = Shape(n=32768, G=8, H=32, w=32, r_min=16, kappa_pct=20, dtype="bf16")
+    cache = compress(shape, K, V, Qw, PK, PV)          # Algorithm 1, one layer
+    out = decode(shape, [cache], q, PK, PV)           # rank-space decode attention
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+from typing import List, Optional, Sequence
+
+import torch
+
+from . import _lib
+from ._lib import CHUNK, COEF_PAD, HEAD_DIM  # noqa: F401
+
+__all__ = ["VarRateError", "Shape", "Cache", "new_cache", "coded_budget", "salience", "allocate",
+           "project", "compress", "append_exact", "decode", "library"]
+
+
+class VarRateError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"varrate error {code}: {msg}")
+        self.code = code
+
+
+def library():
+    return _lib.load()
+
+
+def _check(rc: int):
+    if rc != 0:
+        L = library()
+        raise VarRateError(rc, f"{L.varrate_status_string(rc).decode()}: {L.varrate_last_error().decode()}")
+
+
+@dataclasses.dataclass(frozen=True)
+class Shape:
+    n: int
+    G: int
+    H: int
+    w: int
+    r_min: int
+    kappa_pct: int
+    dtype: str = "bf16"
+    d: int = HEAD_DIM
+
+    def c(self) -> _lib.Shape:
+        return _lib.Shape(self.n, self.G, self.H, self.d, self.w, self.r_min, self.kappa_pct,
+                          _lib.VARRATE_BF16 if self.dtype == "bf16" else _lib.VARRATE_F32, 0)
+
+    @property
+    def torch_dtype(self):
+        return torch.bfloat16 if self.dtype == "bf16" else torch.float32
+
+    @property
+    def N(self) -> int:
+        return self.n - self.w
+
+
+@dataclasses.dataclass
+class Cache:
+    coef_k: torch.Tensor
+    coef_v: torch.Tensor
+    rank: torch.Tensor
+    srank: torch.Tensor
+    sidx: torch.Tensor
+    chunk_off: torch.Tensor
+    k_exact: torch.Tensor
+    v_exact: torch.Tensor
+    coef_stride: int
+    cap: int
+    n_exact: int = 0
+    N: int = 0
+    B: int = 0
+
+    def c(self) -> _lib.CacheC:
+        return _lib.CacheC(self.coef_k.data_ptr(), self.coef_v.data_ptr(), self.rank.data_ptr(),
+                           self.srank.data_ptr(), self.sidx.data_ptr(), self.chunk_off.data_ptr(),
+                           self.k_exact.data_ptr(), self.v_exact.data_ptr(), self.coef_stride,
+                           self.cap, self.n_exact, self.N, self.B)
+
+    def _update(self, cc: _lib.CacheC):
+        self.n_exact, self.N, self.B = int(cc.n_exact), int(cc.N), int(cc.B)
+
+
+def coded_budget(n: int, w: int, kappa_pct: int, d: int = HEAD_DIM) -> int:
+    return int(library().varrate_coded_budget(n, d, w, kappa_pct))
+
+
+def cache_bytes(shape: Shape, cap: int) -> _lib.CacheBytes:
+    out = _lib.CacheBytes()
+    _check(library().varrate_cache_bytes(ctypes.byref(shape.c()), cap, ctypes.byref(out)))
+    return out
+
+
+def new_cache(shape: Shape, cap: Optional[int] = None, device="cuda") -> Cache:
+    """Allocate (torch) the device buffers of one compressed layer; `cap` exact slots."""
+    cap = shape.w if cap is None else cap
+    b = cache_bytes(shape, cap)
+    dt = shape.torch_dtype
+    G = shape.G
+    return Cache(
+        coef_k=torch.zeros((G, b.coef_stride), dtype=dt, device=device),
+        coef_v=torch.zeros((G, b.coef_stride), dtype=dt, device=device),
+        rank=torch.zeros(b.rank, dtype=torch.uint8, device=device),
+        srank=torch.zeros(b.srank, dtype=torch.uint8, device=device),
+        sidx=torch.zeros(b.N, dtype=torch.int32, device=device),
+        chunk_off=torch.zeros(b.n_chunks + 1, dtype=torch.int32, device=device),
+        k_exact=torch.zeros((G, cap, HEAD_DIM), dtype=dt, device=device),
+        v_exact=torch.zeros((G, cap, HEAD_DIM), dtype=dt, device=device),
+        coef_stride=int(b.coef_stride), cap=cap, n_exact=0, N=int(b.N), B=int(b.B))
+
+
+class _Workspaces:
+    """Zero-initialised workspaces, one per (device, kind); kernels leave them zeroed."""
+
+    def __init__(self):
+        self._bufs = {}
+
+    def get(self, kind: str, nbytes: int, device) -> torch.Tensor:
+        dev = torch.device(device)
+        key = (dev, kind)
+        buf = self._bufs.get(key)
+        if buf is None or buf.numel() < nbytes:
+            buf = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=dev)
+            self._bufs[key] = buf
+        return buf
+
+
+_WS = _Workspaces()
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev_ptr(t: Optional[torch.Tensor], dtype=None, name="tensor") -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda:
+        raise VarRateError(_lib.VARRATE_EINVAL, f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise VarRateError(_lib.VARRATE_EINVAL, f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise VarRateError(_lib.VARRATE_EINVAL, f"{name} has dtype {t.dtype}, expected {dtype}")
+    return t.data_ptr()
+
+
+def _compress_ws(shape: Shape, device, workspace):
+    need = int(library().varrate_compress_workspace_bytes(ctypes.byref(shape.c())))
+    if need == 0:
+        _check(library().varrate_cache_bytes(ctypes.byref(shape.c()), shape.w, ctypes.byref(_lib.CacheBytes())))
+    ws = workspace if workspace is not None else _WS.get("compress", need, device)
+    return ws, need
+
+
+def salience(shape: Shape, K: torch.Tensor, Qw: torch.Tensor, sbar: Optional[torch.Tensor] = None,
+             workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Sec. 3.2 Eq. (4) + 5-tap pooling: returns sbar [N] fp32 on the device."""
+    if sbar is None:
+        sbar = torch.empty(shape.N, dtype=torch.float32, device=K.device)
+    ws, _ = _compress_ws(shape, K.device, workspace)
+    _check(library().varrate_salience(ctypes.byref(shape.c()), _dev_ptr(K, shape.torch_dtype, "K"),
+                                      _dev_ptr(Qw, shape.torch_dtype, "Qw"),
+                                      _dev_ptr(sbar, torch.float32, "sbar"), ws.data_ptr(), ws.numel(),
+                                      _stream()))
+    return sbar
+
+
+def allocate(shape: Shape, sbar: torch.Tensor, cache: Cache, workspace: Optional[torch.Tensor] = None) -> Cache:
+    """Sec. 3.2 Eq. (5): integer ranks (cache.rank) and chunk offsets from sbar [N] fp32."""
+    ws, _ = _compress_ws(shape, sbar.device, workspace)
+    cc = cache.c()
+    _check(library().varrate_allocate(ctypes.byref(shape.c()), _dev_ptr(sbar, torch.float32, "sbar"),
+                                      ctypes.byref(cc), ws.data_ptr(), ws.numel(), _stream()))
+    cache._update(cc)
+    return cache
+
+
+def project(shape: Shape, K, V, PK, PV, cache: Cache, workspace: Optional[torch.Tensor] = None) -> Cache:
+    """Sec. 3.3 Eq. (6): stored-order layout, truncated coefficients and exact window rows."""
+    ws, _ = _compress_ws(shape, K.device, workspace)
+    cc = cache.c()
+    _check(library().varrate_project(ctypes.byref(shape.c()), _dev_ptr(K, shape.torch_dtype, "K"),
+                                     _dev_ptr(V, shape.torch_dtype, "V"), _dev_ptr(PK, torch.float32, "PK"),
+                                     _dev_ptr(PV, torch.float32, "PV"), ctypes.byref(cc), ws.data_ptr(),
+                                     ws.numel(), _stream()))
+    cache._update(cc)
+    return cache
+
+
+def compress(shape: Shape, K, V, Qw, PK, PV, cache: Optional[Cache] = None, cap: Optional[int] = None,
+             sbar_out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> Cache:
+    """Algorithm 1 for one layer of one sequence (salience -> allocation -> projection)."""
+    if cache is None:
+        cache = new_cache(shape, cap, K.device)
+    ws, _ = _compress_ws(shape, K.device, workspace)
+    cc = cache.c()
+    _check(library().varrate_compress(ctypes.byref(shape.c()), _dev_ptr(K, shape.torch_dtype, "K"),
+                                      _dev_ptr(V, shape.torch_dtype, "V"), _dev_ptr(Qw, shape.torch_dtype, "Qw"),
+                                      _dev_ptr(PK, torch.float32, "PK"), _dev_ptr(PV, torch.float32, "PV"),
+                                      ctypes.byref(cc), _dev_ptr(sbar_out, torch.float32, "sbar_out"),
+                                      ws.data_ptr(), ws.numel(), _stream()))
+    cache._update(cc)
+    return cache
+
+
+def append_exact(shape: Shape, cache: Cache, k_new: torch.Tensor, v_new: torch.Tensor) -> Cache:
+    """Append one decode-time token ([G][d]) to the exact slots."""
+    cc = cache.c()
+    _check(library().varrate_append_exact(ctypes.byref(shape.c()), ctypes.byref(cc),
+                                          _dev_ptr(k_new, shape.torch_dtype, "k_new"),
+                                          _dev_ptr(v_new, shape.torch_dtype, "v_new"), _stream()))
+    cache._update(cc)
+    return cache
+
+
+def decode_workspace(shape: Shape, S: int, Q: int, device="cuda") -> torch.Tensor:
+    need = int(library().varrate_decode_workspace_bytes(ctypes.byref(shape.c()), S, Q))
+    return _WS.get(f"decode", need, device)
+
+
+def decode(shape: Shape, caches: Sequence[Cache], q: torch.Tensor, PK, PV, out: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Rank-space decode attention.  q: [S][Q][H][d] (or [Q][H][d] for one cache)."""
+    single = q.dim() == 3
+    if single:
+        q = q.unsqueeze(0)
+    S, Q = int(q.shape[0]), int(q.shape[1])
+    if len(caches) != S:
+        raise VarRateError(_lib.VARRATE_EINVAL, f"{len(caches)} caches for {S} query sets")
+    if out is None:
+        out = torch.empty_like(q)
+    arr = (_lib.CacheC * S)(*[c.c() for c in caches])
+    ws = workspace if workspace is not None else decode_workspace(shape, S, Q, q.device)
+    _check(library().varrate_decode_attn(ctypes.byref(shape.c()), arr, S, _dev_ptr(q, shape.torch_dtype, "q"), Q,
+                                         _dev_ptr(PK, torch.float32, "PK"), _dev_ptr(PV, torch.float32, "PV"),
+                                         _dev_ptr(out, shape.torch_dtype, "out"), ws.data_ptr(), ws.numel(),
+                                         _stream()))
+    return out[0] if single else out

@@ -1,0 +1,247 @@
+// C ABI of libvarrate: validation, sizing, workspace carving and kernel dispatch.
+// Every check runs on the host before anything is enqueued; no entry point synchronises,
+// allocates device memory or keeps state between calls.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "vr_internal.h"
+
+using namespace vr;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return VARRATE_OK;
+    return fail(VARRATE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+constexpr int64_t MAX_CODED = 1 << 20;   // allocator limits: chunk table in LDS, 24-bit index keys
+
+int check_shape(const varrate_shape* sh) {
+    if (!sh) return fail(VARRATE_EINVAL, "shape is NULL");
+    if (sh->d != VARRATE_HEAD_DIM) return fail(VARRATE_EUNSUPPORTED, "head dim %d != 128", sh->d);
+    if (sh->G < 1 || sh->H < 1) return fail(VARRATE_EINVAL, "G=%d H=%d must be >= 1", sh->G, sh->H);
+    if (sh->H % sh->G != 0) return fail(VARRATE_EUNSUPPORTED, "H=%d is not a multiple of G=%d", sh->H, sh->G);
+    if (sh->w < 1) return fail(VARRATE_EINVAL, "window w=%d must be >= 1", sh->w);
+    if (sh->n <= sh->w) return fail(VARRATE_EBUDGET, "n=%lld leaves no coded tokens (w=%d)", (long long)sh->n, sh->w);
+    if (sh->r_min < 0 || sh->r_min > VARRATE_HEAD_DIM)
+        return fail(VARRATE_EINVAL, "r_min=%d outside [0, 128]", sh->r_min);
+    if (sh->kappa_pct < 1 || sh->kappa_pct > 100) return fail(VARRATE_EINVAL, "kappa_pct=%d outside [1, 100]", sh->kappa_pct);
+    if (sh->dtype != VARRATE_BF16 && sh->dtype != VARRATE_F32) return fail(VARRATE_EINVAL, "unknown dtype %d", sh->dtype);
+    if ((int64_t)(sh->H / sh->G) * sh->w > 256)
+        return fail(VARRATE_EUNSUPPORTED, "(H/G) * w = %lld window rows per KV head exceeds 256",
+                    (long long)(sh->H / sh->G) * sh->w);
+    if (sh->n - sh->w > MAX_CODED)
+        return fail(VARRATE_EUNSUPPORTED, "N=%lld coded tokens exceeds %lld", (long long)(sh->n - sh->w), (long long)MAX_CODED);
+    const int64_t B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    const int64_t N = sh->n - sh->w;
+    if (N * sh->r_min > B || B > N * VARRATE_HEAD_DIM)
+        return fail(VARRATE_EBUDGET, "budget B=%lld infeasible for N=%lld, r_min=%d, R=128", (long long)B,
+                    (long long)N, sh->r_min);
+    return VARRATE_OK;
+}
+
+int check_cache(const varrate_shape* sh, const varrate_cache* c, bool need_layout) {
+    if (!c) return fail(VARRATE_EINVAL, "cache is NULL");
+    const int64_t B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    if (!c->coef_k || !c->coef_v || !c->rank || !c->chunk_off || !c->k_exact || !c->v_exact ||
+        (need_layout && (!c->srank || !c->sidx)))
+        return fail(VARRATE_EINVAL, "cache has a NULL buffer");
+    if (!aligned16(c->coef_k) || !aligned16(c->coef_v) || !aligned16(c->k_exact) || !aligned16(c->v_exact))
+        return fail(VARRATE_EINVAL, "cache buffers must be 16-byte aligned");
+    if (c->coef_stride < B + VARRATE_COEF_PAD || (c->coef_stride % 8) != 0)
+        return fail(VARRATE_EINVAL, "coef_stride=%lld must be a multiple of 8 and >= B + %d = %lld",
+                    (long long)c->coef_stride, VARRATE_COEF_PAD, (long long)(B + VARRATE_COEF_PAD));
+    if (c->cap < sh->w) return fail(VARRATE_EINVAL, "exact capacity %lld < w=%d", (long long)c->cap, sh->w);
+    return VARRATE_OK;
+}
+
+size_t compress_ws(const varrate_shape& sh) {
+    const int64_t N = sh.n - sh.w;
+    return align256(salience_ws_bytes(sh)) + align256(allocate_ws_bytes(sh)) + align256((size_t)N * 4);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* varrate_status_string(int s) {
+    switch (s) {
+        case VARRATE_OK: return "ok";
+        case VARRATE_EINVAL: return "invalid argument";
+        case VARRATE_EBUDGET: return "infeasible budget";
+        case VARRATE_EUNSUPPORTED: return "unsupported shape";
+        case VARRATE_EHIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+const char* varrate_last_error(void) { return g_err.c_str(); }
+
+int varrate_version(void) { return 1; }
+
+int64_t varrate_coded_budget(int64_t n, int32_t d, int32_t w, int32_t kappa_pct) {
+    return ((int64_t)kappa_pct * n * d) / 100 - (int64_t)w * d;
+}
+
+int varrate_cache_bytes(const varrate_shape* sh, int64_t cap, varrate_cache_bytes_t* out) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if (!out) return fail(VARRATE_EINVAL, "out is NULL");
+    if (cap < sh->w) return fail(VARRATE_EINVAL, "exact capacity %lld < w=%d", (long long)cap, sh->w);
+    const size_t es = sh->dtype == VARRATE_BF16 ? 2 : 4;
+    out->N = sh->n - sh->w;
+    out->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    out->n_chunks = (out->N + VARRATE_CHUNK - 1) / VARRATE_CHUNK;
+    out->coef_stride = ((out->B + VARRATE_COEF_PAD + 63) / 64) * 64;
+    out->coef_k = out->coef_v = (size_t)sh->G * out->coef_stride * es;
+    out->rank = out->srank = (size_t)out->N;
+    out->sidx = (size_t)out->N * 4;
+    out->chunk_off = (size_t)(out->n_chunks + 1) * 4;
+    out->k_exact = out->v_exact = (size_t)sh->G * cap * VARRATE_HEAD_DIM * es;
+    return VARRATE_OK;
+}
+
+size_t varrate_compress_workspace_bytes(const varrate_shape* sh) {
+    if (check_shape(sh)) return 0;
+    return compress_ws(*sh);
+}
+
+size_t varrate_decode_workspace_bytes(const varrate_shape* sh, int32_t S, int32_t Q) {
+    if (check_shape(sh) || S < 1 || Q < 1) return 0;
+    return decode_ws_bytes(*sh, S, Q);
+}
+
+static int ws_check(void* ws, size_t have, size_t need) {
+    if (!ws) return fail(VARRATE_EINVAL, "workspace is NULL");
+    if (!aligned16(ws)) return fail(VARRATE_EINVAL, "workspace must be 16-byte aligned");
+    if (have < need) return fail(VARRATE_EINVAL, "workspace %zu bytes < required %zu", have, need);
+    return VARRATE_OK;
+}
+
+int varrate_salience(const varrate_shape* sh, const void* K, const void* Qw, float* sbar, void* ws,
+                     size_t ws_bytes, void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if (!K || !Qw || !sbar) return fail(VARRATE_EINVAL, "K, Qw and sbar must be non-NULL");
+    if (!aligned16(K) || !aligned16(Qw)) return fail(VARRATE_EINVAL, "K and Qw must be 16-byte aligned");
+    if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
+    return hip_status(launch_salience(*sh, K, Qw, sbar, (uint8_t*)ws, (hipStream_t)stream), "salience launch");
+}
+
+int varrate_allocate(const varrate_shape* sh, const float* sbar, varrate_cache* c, void* ws,
+                     size_t ws_bytes, void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if ((rc = check_cache(sh, c, false))) return rc;
+    if (!sbar) return fail(VARRATE_EINVAL, "sbar is NULL");
+    if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
+    c->N = sh->n - sh->w;
+    c->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    uint8_t* w8 = (uint8_t*)ws + align256(salience_ws_bytes(*sh));
+    return hip_status(launch_allocate(*sh, sbar, *c, w8, (hipStream_t)stream), "allocate launch");
+}
+
+int varrate_project(const varrate_shape* sh, const void* K, const void* V, const float* PK,
+                    const float* PV, varrate_cache* c, void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if ((rc = check_cache(sh, c, true))) return rc;
+    if (!K || !V || !PK || !PV) return fail(VARRATE_EINVAL, "K, V, P_K and P_V must be non-NULL");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(PK) || !aligned16(PV))
+        return fail(VARRATE_EINVAL, "K, V, P_K, P_V must be 16-byte aligned");
+    if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
+    c->N = sh->n - sh->w;
+    c->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    hipStream_t st = (hipStream_t)stream;
+    rc = hip_status(launch_layout(*sh, *c, st), "layout launch");
+    if (rc) return rc;
+    rc = hip_status(launch_project(*sh, K, V, PK, PV, *c, st), "project launch");
+    if (rc) return rc;
+    c->n_exact = sh->w;
+    return VARRATE_OK;
+}
+
+int varrate_compress(const varrate_shape* sh, const void* K, const void* V, const void* Qw,
+                     const float* PK, const float* PV, varrate_cache* c, float* sbar_out, void* ws,
+                     size_t ws_bytes, void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if ((rc = check_cache(sh, c, true))) return rc;
+    if (!K || !V || !Qw || !PK || !PV) return fail(VARRATE_EINVAL, "inputs must be non-NULL");
+    if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
+    float* sbar = sbar_out;
+    if (!sbar) {
+        sbar = (float*)((uint8_t*)ws + align256(salience_ws_bytes(*sh)) + align256(allocate_ws_bytes(*sh)));
+    }
+    if ((rc = varrate_salience(sh, K, Qw, sbar, ws, ws_bytes, stream))) return rc;
+    if ((rc = varrate_allocate(sh, sbar, c, ws, ws_bytes, stream))) return rc;
+    return varrate_project(sh, K, V, PK, PV, c, ws, ws_bytes, stream);
+}
+
+int varrate_append_exact(const varrate_shape* sh, varrate_cache* c, const void* k_new, const void* v_new,
+                         void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if ((rc = check_cache(sh, c, false))) return rc;
+    if (!k_new || !v_new) return fail(VARRATE_EINVAL, "k_new and v_new must be non-NULL");
+    if (c->n_exact >= c->cap) return fail(VARRATE_EINVAL, "exact capacity %lld is full", (long long)c->cap);
+    const size_t es = sh->dtype == VARRATE_BF16 ? 2 : 4;
+    const size_t row = VARRATE_HEAD_DIM * es;
+    hipStream_t st = (hipStream_t)stream;
+    for (int kv = 0; kv < 2; ++kv) {
+        uint8_t* dst = (uint8_t*)(kv ? c->v_exact : c->k_exact) + (size_t)c->n_exact * row;
+        const void* src = kv ? v_new : k_new;
+        hipError_t e = hipMemcpy2DAsync(dst, (size_t)c->cap * row, src, row, row, sh->G,
+                                        hipMemcpyDeviceToDevice, st);
+        if ((rc = hip_status(e, "append copy"))) return rc;
+    }
+    c->n_exact += 1;
+    return VARRATE_OK;
+}
+
+int varrate_decode_attn(const varrate_shape* sh, const varrate_cache* caches, int32_t S, const void* q,
+                        int32_t Q, const float* PK, const float* PV, void* out, void* ws, size_t ws_bytes,
+                        void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if (!caches || S < 1 || S > VARRATE_MAX_SEQS) return fail(VARRATE_EINVAL, "S=%d outside [1, %d]", S, VARRATE_MAX_SEQS);
+    if (Q < 1 || (int64_t)Q * (sh->H / sh->G) > VARRATE_MAX_QROWS)
+        return fail(VARRATE_EUNSUPPORTED, "Q=%d query rows per KV head exceed %d", Q, VARRATE_MAX_QROWS);
+    if (!q || !out || !PK || !PV) return fail(VARRATE_EINVAL, "q, out, P_K, P_V must be non-NULL");
+    if (!aligned16(q) || !aligned16(PK) || !aligned16(PV))
+        return fail(VARRATE_EINVAL, "q, P_K, P_V must be 16-byte aligned");
+    for (int s = 0; s < S; ++s) {
+        if ((rc = check_cache(sh, &caches[s], true))) return rc;
+        if (caches[s].N != sh->n - sh->w) return fail(VARRATE_EINVAL, "cache %d was not compressed with this shape", s);
+        if (caches[s].n_exact < 0 || caches[s].n_exact > caches[s].cap)
+            return fail(VARRATE_EINVAL, "cache %d has n_exact outside [0, cap]", s);
+        if (caches[s].coef_stride != caches[0].coef_stride || caches[s].cap != caches[0].cap)
+            return fail(VARRATE_EINVAL, "caches must share coef_stride and cap");
+    }
+    if (decode_units(*sh, S, Q) > 16384)
+        return fail(VARRATE_EUNSUPPORTED, "S * G * ceil(Q H/G / 16) exceeds 16384 merge slots");
+    if ((rc = ws_check(ws, ws_bytes, decode_ws_bytes(*sh, S, Q)))) return rc;
+    return hip_status(launch_decode(*sh, caches, S, q, Q, PK, PV, out, (uint8_t*)ws, (hipStream_t)stream),
+                      "decode launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,89 @@
+// Device helpers shared by the CDNA4 (gfx950) kernels of the variable-rank codec.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vr {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int D = 128;          // head dim = basis rank R
+constexpr int WAVE = 64;
+
+// ---- bf16 <-> fp32 -------------------------------------------------------------------
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (inputs are finite).
+__device__ __forceinline__ uint32_t f32_to_bf16(float x) {
+    uint32_t u = __float_as_uint(x);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+// x = hi + lo to about 2^-17 relative: hi = bf16(x), lo = bf16(x - hi).
+__device__ __forceinline__ void split_bf16(float x, uint32_t& hi, uint32_t& lo) {
+    hi = f32_to_bf16(x);
+    lo = f32_to_bf16(x - __uint_as_float(hi << 16));
+}
+__device__ __forceinline__ uint32_t pack2(uint32_t lo16, uint32_t hi16) { return lo16 | (hi16 << 16); }
+
+// 8 fp32 -> (hi, lo) bf16x8 fragments.
+__device__ __forceinline__ void split8(const float* x, u32x4& hi, u32x4& lo) {
+    uint32_t h[8], l[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) split_bf16(x[e], h[e], l[e]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        hi[k] = pack2(h[2 * k], h[2 * k + 1]);
+        lo[k] = pack2(l[2 * k], l[2 * k + 1]);
+    }
+}
+
+// ---- MFMA -------------------------------------------------------------------------------
+// D(16x16 fp32) += A(16x32 bf16) * B(32x16 bf16).  Operand lane layout (wave64):
+//   A: lane l holds row (l % 16), 8 K-elements of group (l / 16);
+//   B: lane l holds column (l % 16), the same 8 K-elements of group (l / 16);
+//   C: lane l holds column (l % 16), rows 4 (l / 16) + v, v = 0..3.
+// A and B share the K-element assignment, so any fixed mapping of (group, element) to the
+// contraction index gives the same product.
+__device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// ---- loads ---------------------------------------------------------------------------
+// 16 bytes from a 2-byte aligned address (gfx950 serves it with one dwordx4 load).
+__device__ __forceinline__ u32x4 load16_a2(const uint16_t* p) {
+    u32x4 v;
+    __builtin_memcpy(&v, p, 16);
+    return v;
+}
+__device__ __forceinline__ u32x4 load16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// Keep the first nv (0..8) bf16 elements of an 8-element fragment, zero the rest.
+__device__ __forceinline__ u32x4 keep_first(u32x4 v, int nv) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        uint32_t m = nv >= 2 * k + 2 ? 0xFFFFFFFFu : (nv == 2 * k + 1 ? 0x0000FFFFu : 0u);
+        v[k] &= m;
+    }
+    return v;
+}
+
+// ---- wave / block reductions ---------------------------------------------------------
+__device__ __forceinline__ float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, WAVE); }
+
+__device__ __forceinline__ float wave_max16(float v) {   // over lanes sharing l/16 ... l%16
+    v = fmaxf(v, shfl_xor_f(v, 1));
+    v = fmaxf(v, shfl_xor_f(v, 2));
+    v = fmaxf(v, shfl_xor_f(v, 4));
+    v = fmaxf(v, shfl_xor_f(v, 8));
+    return v;
+}
+
+// exp(x) on the hardware exp2 path (x * log2 e); -inf -> 0.
+__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+
+}  // namespace vr

@@ -1,0 +1,113 @@
+"""C-ABI checks that need no GPU: the library loads, exports every declared entry point, and
+host-side validation returns the documented status codes before anything is enqueued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2607_15498_amd import _lib
+    return _lib.load()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "varrate.h")).read()
+    return sorted(set(re.findall(r"VARRATE_API\s+[\w\s\*]+?\b(varrate_\w+)\s*\(", text)))
+
+
+def test_header_and_binding_agree():
+    from paper_2607_15498_amd import _lib
+    assert declared_functions() == sorted(_lib.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_struct_sizes_match_header():
+    from paper_2607_15498_amd import _lib
+    assert ctypes.sizeof(_lib.Shape) == 40
+    assert ctypes.sizeof(_lib.CacheC) == 8 * 8 + 5 * 8
+
+
+def _shape(**kw):
+    from paper_2607_15498_amd import _lib
+    base = dict(n=32768, G=8, H=32, d=128, w=32, r_min=16, kappa_pct=20, dtype=_lib.VARRATE_BF16, reserved=0)
+    base.update(kw)
+    return _lib.Shape(**base)
+
+
+def test_coded_budget_eq3(L, oracle_lib):
+    for n, w, k in [(512, 32, 20), (32768, 32, 20), (16384, 32, 20), (131072, 32, 20), (32768, 32, 40),
+                    (1000, 7, 33)]:
+        assert L.varrate_coded_budget(n, 128, w, k) == oracle_lib.budget(n, 128, w, k)
+
+
+def test_cache_bytes(L):
+    from paper_2607_15498_amd import _lib
+    out = _lib.CacheBytes()
+    assert L.varrate_cache_bytes(ctypes.byref(_shape()), 32 + 256, ctypes.byref(out)) == 0
+    assert out.N == 32736 and out.B == 834764 and out.n_chunks == 128
+    assert out.coef_stride >= out.B + _lib.COEF_PAD and out.coef_stride % 64 == 0
+    assert out.coef_k == 8 * out.coef_stride * 2
+    assert out.k_exact == 8 * 288 * 128 * 2
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d=64), -3), (dict(H=30), -3), (dict(w=0), -1), (dict(n=32), -2), (dict(r_min=-1), -1),
+    (dict(r_min=129), -1), (dict(kappa_pct=0), -1), (dict(kappa_pct=101), -1), (dict(dtype=7), -1),
+    (dict(kappa_pct=10), -2),                        # 10%: N r_min > B at r_min = 16
+    (dict(w=64, H=64, G=4), -3),                     # 16 x 64 window rows per KV head > 256
+    (dict(n=(1 << 20) + 64, w=32), -3),
+])
+def test_shape_validation(L, kw, code):
+    from paper_2607_15498_amd import _lib
+    out = _lib.CacheBytes()
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(**kw)), 64, ctypes.byref(out)) == code
+    assert L.varrate_last_error()
+
+
+def test_budget_feasibility_edges(L):
+    from paper_2607_15498_amd import _lib
+    out = _lib.CacheBytes()
+    # kappa 100 -> B = N * 128 exactly (every token full rank): feasible
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(kappa_pct=100)), 64, ctypes.byref(out)) == 0
+    assert out.B == out.N * 128
+    # 10% budget is feasible once the floor drops to 8
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(kappa_pct=10, r_min=8)), 64, ctypes.byref(out)) == 0
+
+
+def test_entry_points_reject_bad_arguments_before_launch(L):
+    from paper_2607_15498_amd import _lib
+    sh = _shape()
+    cc = _lib.CacheC()
+    # NULL inputs / NULL cache buffers are rejected on the host
+    assert L.varrate_salience(ctypes.byref(sh), None, None, None, None, 0, None) == -1
+    assert L.varrate_compress(ctypes.byref(sh), None, None, None, None, None, ctypes.byref(cc), None,
+                              None, 0, None) == -1
+    assert L.varrate_allocate(ctypes.byref(sh), None, ctypes.byref(cc), None, 0, None) == -1
+    assert L.varrate_decode_attn(ctypes.byref(sh), ctypes.byref(cc), 0, None, 1, None, None, None,
+                                 None, 0, None) == -1
+    assert L.varrate_decode_attn(ctypes.byref(sh), ctypes.byref(cc), 1, None, 100, None, None, None,
+                                 None, 0, None) == -3
+    assert b"NULL" in L.varrate_last_error() or b"outside" in L.varrate_last_error() \
+        or b"exceed" in L.varrate_last_error()
+
+
+def test_workspace_sizes_positive(L):
+    sh = _shape()
+    assert L.varrate_compress_workspace_bytes(ctypes.byref(sh)) > 0
+    assert L.varrate_decode_workspace_bytes(ctypes.byref(sh), 1, 1) > 0
+    assert L.varrate_decode_workspace_bytes(ctypes.byref(_shape(d=64)), 1, 1) == 0
+
+
+def test_status_strings(L):
+    assert L.varrate_status_string(0) == b"ok"
+    assert L.varrate_status_string(-2) == b"infeasible budget"
+    assert L.varrate_version() == 1

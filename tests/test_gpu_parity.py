@@ -1,0 +1,371 @@
+"""GPU parity of the HIP codec (through the C ABI) against the fp64 CPU oracle.
+
+Tolerances (from the workload definition): ranks, offsets and layout bit-exact given the
+same fp32 pooled salience; salience within 1e-3 relative (entries below 1e-6 of the max are
+an underflow floor, reported separately); decode within 2e-2 of max |o| per (sequence,
+query, head) in bf16.  The fp32 tiny workload is also held to a tighter decode bound."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+SAL_RTOL = 1e-3
+DEC_TOL_BF16 = 2e-2
+DEC_TOL_F32 = 1e-4
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def vr():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a visible MI355X")
+    import paper_2607_15498_amd as vr
+    vr.library()
+    return vr
+
+
+def dev(a, dt):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dt).cuda()
+
+
+def host(t):
+    import torch
+    if t.dtype == torch.bfloat16:
+        t = t.float()
+    return t.cpu().numpy()
+
+
+def shape_of(vr, cfg, n=None, kappa=None, r_min=None, w=None):
+    return vr.Shape(n=cfg["n"] if n is None else n, G=cfg["G"], H=cfg["H"], w=cfg["w"] if w is None else w,
+                    r_min=cfg["r_min"] if r_min is None else r_min,
+                    kappa_pct=cfg["kappa"] if kappa is None else kappa, dtype=cfg["dtype"])
+
+
+def expected_layout(rank, N):
+    srank = np.empty(N, np.int64)
+    sidx = np.empty(N, np.int64)
+    nch = (N + 255) // 256
+    chunk_off = np.zeros(nch + 1, np.int64)
+    for c in range(nch):
+        t = np.arange(c * 256, min(N, c * 256 + 256))
+        order = np.lexsort((t, -rank[t]))
+        sidx[t] = t[order]
+        srank[t] = rank[t][order]
+        chunk_off[c + 1] = chunk_off[c] + rank[t].sum()
+    return srank, sidx, chunk_off
+
+
+def unpack(coef, srank, sidx, chunk_off, N, d=128):
+    """GPU packed streams [G][stride] -> [N][G][d] (zeros past each rank).  Chunks are
+    contiguous, so stored token i starts at the exclusive prefix sum of srank."""
+    G = coef.shape[0]
+    out = np.zeros((N, G, d), np.float32)
+    B = int(srank.sum())
+    assert B == chunk_off[-1]
+    starts = np.concatenate([[0], np.cumsum(srank)[:-1]])
+    tok = np.repeat(sidx, srank)
+    j = np.arange(B) - np.repeat(starts, srank)
+    for g in range(G):
+        out[tok, g, j] = coef[g, :B]
+    return out
+
+
+def rel_err(got, ref):
+    return np.abs(got - ref).max() / max(np.abs(ref).max(), 1e-30)
+
+
+def decode_err(o_gpu, o_or):
+    """max over heads of ||d||_inf / ||o||_inf."""
+    return max(np.abs(o_gpu[h] - o_or[h]).max() / np.abs(o_or[h]).max() for h in range(o_or.shape[0]))
+
+
+_LAYERS = {}
+
+
+def layer(name, **kw):
+    from workloads import CONFIGS, make_layer
+    key = (name, tuple(sorted(kw.items())))
+    if key not in _LAYERS:
+        _LAYERS[key] = make_layer(CONFIGS[name], **kw)
+    return _LAYERS[key]
+
+
+_ORACLE = {}
+
+
+def oracle_compress(oracle_lib, name, li, kappa, r_min, sbar=None, tag=""):
+    from workloads import CONFIGS
+    cfg = CONFIGS[name]
+    key = (name, kappa, r_min, tag)
+    if key not in _ORACLE:
+        _ORACLE[key] = oracle_lib.compress(li.K, li.V, li.Qw, li.PK, li.PV, cfg["H"], kappa, r_min,
+                                           cfg["dtype"], sbar=sbar)
+    return _ORACLE[key]
+
+
+def gpu_compress(vr, shape, li, sbar=None, cap=None):
+    import torch
+    dt = shape.torch_dtype
+    K, V, Qw = dev(li.K, dt), dev(li.V, dt), dev(li.Qw, dt)
+    PK, PV = dev(li.PK, torch.float32), dev(li.PV, torch.float32)
+    if sbar is None:
+        sb = torch.empty(shape.N, dtype=torch.float32, device="cuda")
+        cache = vr.compress(shape, K, V, Qw, PK, PV, cap=cap, sbar_out=sb)
+    else:
+        sb = dev(sbar, torch.float32)
+        cache = vr.new_cache(shape, cap)
+        vr.allocate(shape, sb, cache)
+        vr.project(shape, K, V, PK, PV, cache)
+    torch.cuda.synchronize()
+    return cache, sb, PK, PV
+
+
+# ---------------------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny", "llama_32k"])
+def test_salience_parity(vr, oracle_lib, name):
+    from workloads import CONFIGS
+    say(f"[salience] {name}")
+    li = layer(name)
+    oc = oracle_compress(oracle_lib, name, li, CONFIGS[name]["kappa"], CONFIGS[name]["r_min"])
+    shape = shape_of(vr, CONFIGS[name])
+    _, sb, _, _ = gpu_compress(vr, shape, li)
+    g = host(sb).astype(np.float64)
+    o = oc.sbar.astype(np.float64)
+    floor = 1e-6 * o.max()
+    big = o >= floor
+    rel = np.abs(g[big] - o[big]) / o[big]
+    say(f"  max rel {rel.max():.3e} over {big.sum()} entries; {(~big).sum()} below floor, "
+        f"max abs there {np.abs(g[~big] - o[~big]).max() if (~big).any() else 0:.3e}")
+    assert rel.max() <= SAL_RTOL
+    assert np.all(np.abs(g[~big] - o[~big]) <= SAL_RTOL * floor)
+
+
+def sbar_cases(N, oracle_sbar):
+    rng = np.random.default_rng(123)
+    cases = {
+        "oracle": oracle_sbar,
+        "constant": np.full(N, 0.37, np.float32),
+        "ties": rng.integers(0, 4, N).astype(np.float32) / 7,
+        "one_hot": np.where(np.arange(N) == N // 3, 1.0, 0.0).astype(np.float32),
+        "random": rng.random(N).astype(np.float32),
+        "spiky": (rng.random(N) ** 12).astype(np.float32),
+    }
+    return cases
+
+
+@pytest.mark.parametrize("name,kappa,r_min", [("tiny", 20, 16), ("tiny", 13, 0), ("tiny", 100, 16),
+                                              ("llama_32k", 20, 16), ("llama_32k", 10, 8),
+                                              ("llama_32k", 40, 16), ("llama_32k", 13, 16)])
+def test_allocation_bit_exact(vr, oracle_lib, name, kappa, r_min):
+    from workloads import CONFIGS
+    cfg = CONFIGS[name]
+    li = layer(name)
+    base = oracle_compress(oracle_lib, name, li, cfg["kappa"], cfg["r_min"])
+    N = cfg["n"] - cfg["w"]
+    shape = shape_of(vr, cfg, kappa=kappa, r_min=r_min)
+    B = oracle_lib.budget(cfg["n"], 128, cfg["w"], kappa)
+    import torch
+    for case, sb in sbar_cases(N, base.sbar).items():
+        say(f"[allocate] {name} kappa={kappa} r_min={r_min} case={case}")
+        want = oracle_lib.allocate(oracle_lib.weights(sb), B, r_min, 128).rank
+        cache = vr.new_cache(shape)
+        vr.allocate(shape, dev(sb, torch.float32), cache)
+        torch.cuda.synchronize()
+        got = host(cache.rank).astype(np.int64)
+        mism = int((got != want).sum())
+        assert mism == 0, f"{case}: {mism} rank mismatches"
+        _, _, chunk_off = expected_layout(want.astype(np.int64), N)
+        assert np.array_equal(host(cache.chunk_off).astype(np.int64), chunk_off), case
+        assert cache.B == B and got.sum() == B
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama_32k"])
+def test_layout_and_projection(vr, oracle_lib, name):
+    from workloads import CONFIGS
+    cfg = CONFIGS[name]
+    say(f"[project] {name}")
+    li = layer(name)
+    oc = oracle_compress(oracle_lib, name, li, cfg["kappa"], cfg["r_min"])
+    shape = shape_of(vr, cfg)
+    cache, _, _, _ = gpu_compress(vr, shape, li, sbar=oc.sbar)
+    N = shape.N
+    rank = oc.alloc.rank.astype(np.int64)
+    srank, sidx, chunk_off = expected_layout(rank, N)
+    assert np.array_equal(host(cache.srank).astype(np.int64), srank)
+    assert np.array_equal(host(cache.sidx).astype(np.int64), sidx)
+    assert np.array_equal(host(cache.chunk_off).astype(np.int64), chunk_off)
+    for kind, ref, X in (("K", oc.coefK, li.K), ("V", oc.coefV, li.V)):
+        got = unpack(host(cache.coef_k if kind == "K" else cache.coef_v), srank, sidx, chunk_off, N)
+        err = np.abs(got - ref)
+        # The kernel forms P x from bf16 hi + lo parts of P (and of x when x is fp32), each
+        # product within 2^-18 |P_ji x_i|, summed in fp32: |error| <= 2^-18 sum_i |P_ji x_i|
+        # <= 2^-18 sqrt(128) ||x_t|| < 2^-12 ||x_t||.  bf16 storage then rounds the kernel's
+        # value, which may land one unit (<= 2^-7 |ref|) from the rounding of the exact value.
+        xnorm = np.linalg.norm(X[:N].astype(np.float64), axis=-1)[:, :, None]
+        if cfg["dtype"] == "bf16":
+            ok = err <= np.abs(ref) * 2.0 ** -7 + 2.0 ** -12 * xnorm
+        else:
+            ok = err <= np.abs(ref) * 2.0 ** -23 + 2.0 ** -12 * xnorm
+        say(f"  {kind}: max rel {rel_err(got, ref):.3e}, beyond-bound {int((~ok).sum())}, "
+            f"identical {float((err == 0).mean()):.4f}")
+        assert ok.all()
+    # exact window rows are copied verbatim
+    w = shape.w
+    assert np.array_equal(host(cache.k_exact)[:, :w].transpose(1, 0, 2), li.K[N:])
+    assert np.array_equal(host(cache.v_exact)[:, :w].transpose(1, 0, 2), li.V[N:])
+    assert cache.n_exact == w
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama_32k"])
+def test_decode_parity_same_ranks(vr, oracle_lib, name):
+    import torch
+    from workloads import CONFIGS
+    cfg = CONFIGS[name]
+    say(f"[decode] {name}")
+    li = layer(name, n_queries=2)
+    oc = oracle_compress(oracle_lib, name, li, cfg["kappa"], cfg["r_min"], tag="q2")
+    shape = shape_of(vr, cfg)
+    cache, _, PK, PV = gpu_compress(vr, shape, li, sbar=oc.sbar)
+    assert np.array_equal(host(cache.rank).astype(np.int64), oc.alloc.rank)
+    q = dev(li.q, shape.torch_dtype)
+    out = vr.decode(shape, [cache], q, PK, PV)
+    torch.cuda.synchronize()
+    o_gpu = host(out)
+    tol = DEC_TOL_F32 if cfg["dtype"] == "f32" else DEC_TOL_BF16
+    for i in range(li.q.shape[0]):
+        o_or = oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[i], cfg["H"])
+        e = decode_err(o_gpu[i], o_or)
+        say(f"  query {i}: decode max rel err {e:.3e}")
+        assert e <= tol
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama_32k"])
+def test_end_to_end(vr, oracle_lib, name):
+    """GPU salience feeds the GPU allocation; the oracle runs independently throughout."""
+    import torch
+    from workloads import CONFIGS
+    cfg = CONFIGS[name]
+    say(f"[end-to-end] {name}")
+    li = layer(name, n_queries=2)
+    oc = oracle_compress(oracle_lib, name, li, cfg["kappa"], cfg["r_min"], tag="q2")
+    shape = shape_of(vr, cfg)
+    cache, _, PK, PV = gpu_compress(vr, shape, li)
+    mism = int((host(cache.rank).astype(np.int64) != oc.alloc.rank).sum())
+    out = host(vr.decode(shape, [cache], dev(li.q, shape.torch_dtype), PK, PV))
+    torch.cuda.synchronize()
+    errs = []
+    for i in range(li.q.shape[0]):
+        o_or = oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[i], cfg["H"])
+        errs.append(decode_err(out[i], o_or))
+    say(f"  rank mismatches {mism} of {shape.N}; decode max rel err {max(errs):.3e}")
+    assert mism <= max(8, shape.N // 1000)
+    assert max(errs) <= DEC_TOL_BF16
+
+
+def test_decode_multi_sequence_many_queries_appended(vr, oracle_lib):
+    """S = 3 independent sequences, Q = 5 queries each (20 query rows per KV head: two row
+    tiles), ragged last chunk, and 3 exact tokens appended after compression."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = dict(CONFIGS["llama_32k"])
+    cfg.update(n=1300, G=2, H=8, seed=77)
+    shape = vr.Shape(n=1300, G=2, H=8, w=32, r_min=16, kappa_pct=20, dtype="bf16")
+    Q, extra = 5, 3
+    caches, qs, refs = [], [], []
+    for s in range(3):
+        li = make_layer(cfg, seq=s, n_queries=Q, n=1300 + extra)
+        Kc, Vc = li.K[:1300], li.V[:1300]
+        oc = oracle_lib.compress(Kc, Vc, li.Qw, li.PK, li.PV, 8, 20, 16, "bf16")
+        li2 = type(li)(Kc, Vc, li.Qw, li.q, li.PK, li.PV, li.planted, cfg)
+        cache, _, PK, PV = gpu_compress(vr, shape, li2, sbar=oc.sbar, cap=32 + extra)
+        for e in range(extra):
+            vr.append_exact(shape, cache, dev(li.K[1300 + e], torch.bfloat16), dev(li.V[1300 + e], torch.bfloat16))
+        caches.append(cache)
+        qs.append(li.q)
+        Kx = np.concatenate([oc.Kx, li.K[1300:]])
+        Vx = np.concatenate([oc.Vx, li.V[1300:]])
+        refs.append([oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, Kx, Vx, li.PK, li.PV, li.q[i], 8)
+                     for i in range(Q)])
+    q = dev(np.stack(qs), torch.bfloat16)
+    out = host(vr.decode(shape, caches, q, PK, PV))
+    torch.cuda.synchronize()
+    worst = max(decode_err(out[s][i], refs[s][i]) for s in range(3) for i in range(Q))
+    say(f"[multi] worst decode rel err {worst:.3e}")
+    assert caches[0].n_exact == 32 + extra
+    assert worst <= DEC_TOL_BF16
+
+
+@pytest.mark.parametrize("n,w,kappa,r_min", [(33, 32, 100, 16), (40, 32, 90, 0), (287, 32, 50, 16),
+                                             (289, 32, 25, 4), (600, 1, 30, 16), (2080, 32, 100, 16)])
+def test_ragged_and_degenerate(vr, oracle_lib, n, w, kappa, r_min):
+    """One coded token, chunks of 255 / 1 tokens, window of 1, floor 0, full budget."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = dict(CONFIGS["llama_32k"])
+    cfg.update(n=n, w=w, G=2, H=4, seed=91)
+    say(f"[ragged] n={n} w={w} kappa={kappa} r_min={r_min}")
+    li = make_layer(cfg, n_queries=1)
+    shape = vr.Shape(n=n, G=2, H=4, w=w, r_min=r_min, kappa_pct=kappa, dtype="bf16")
+    B = oracle_lib.budget(n, 128, w, kappa)
+    if B < (n - w) * r_min or B > (n - w) * 128:
+        pytest.skip("infeasible budget for this shape")
+    oc = oracle_lib.compress(li.K, li.V, li.Qw, li.PK, li.PV, 4, kappa, r_min, "bf16")
+    cache, sb, PK, PV = gpu_compress(vr, shape, li)
+    s = host(sb)
+    got_rank = host(cache.rank).astype(np.int64)
+    cache2, _, _, _ = gpu_compress(vr, shape, li, sbar=oc.sbar)
+    assert np.array_equal(host(cache2.rank).astype(np.int64), oc.alloc.rank)
+    out = host(vr.decode(shape, [cache2], dev(li.q, torch.bfloat16), PK, PV))
+    torch.cuda.synchronize()
+    o_or = oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[0], 4)
+    e = decode_err(out[0], o_or)
+    say(f"  decode err {e:.3e}; e2e rank mismatches {int((got_rank != oc.alloc.rank).sum())}; "
+        f"salience max rel {np.max(np.abs(s - oc.sbar) / np.maximum(oc.sbar, 1e-30)):.2e}")
+    assert e <= DEC_TOL_BF16
+
+
+def test_full_budget_is_attention(vr):
+    """kappa = 100 keeps every token at full rank: decode equals attention over the bf16
+    cache up to coefficient storage rounding."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = dict(CONFIGS["llama_32k"])
+    cfg.update(n=3000, G=2, H=8, seed=5)
+    li = make_layer(cfg, n_queries=1)
+    shape = vr.Shape(n=3000, G=2, H=8, w=32, r_min=16, kappa_pct=100, dtype="bf16")
+    cache, _, PK, PV = gpu_compress(vr, shape, li)
+    assert int(host(cache.rank).min()) == 128
+    out = host(vr.decode(shape, [cache], dev(li.q, torch.bfloat16), PK, PV))[0]
+    ref = np.zeros((8, 128))
+    for h in range(8):
+        g = h // 4
+        x = li.K[:, g, :].astype(np.float64) @ li.q[0, h].astype(np.float64) / math.sqrt(128)
+        a = np.exp(x - x.max())
+        a /= a.sum()
+        ref[h] = a @ li.V[:, g, :]
+    e = decode_err(out, ref)
+    say(f"[full budget] err vs attention {e:.3e}")
+    assert e <= DEC_TOL_BF16
+
+
+def test_run_twice_bitwise_identical(vr):
+    import torch
+    li = layer("llama_32k", n_queries=2)
+    from workloads import CONFIGS
+    shape = shape_of(vr, CONFIGS["llama_32k"])
+    outs = []
+    for _ in range(2):
+        cache, sb, PK, PV = gpu_compress(vr, shape, li)
+        o = vr.decode(shape, [cache], dev(li.q, torch.bfloat16), PK, PV)
+        torch.cuda.synchronize()
+        outs.append((host(sb), host(cache.rank), host(cache.coef_k), host(cache.coef_v), host(o)))
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
