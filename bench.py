@@ -1,0 +1,193 @@
+"""Benchmark of the variable-rank KV codec's hot path on one MI355X.
+
+A step is one pass of the whole path over one synthetic layer of the Llama-3.1-8B-shaped
+workload (8 KV heads x 32 query heads, d 128, 32768 cached tokens, bf16, budget 20%,
+floor 16, window 32): salience -> allocation -> projection (compress), then one decode
+query in rank space.  Inputs are device-resident before timing.  To keep the 256 MB
+Infinity Cache from serving repeated reads, steps rotate over several copies of the
+layer's K/V (compress reads) and over many cache slots: a step decodes the slot that
+was compressed half a rotation earlier, so decode never reads what it just wrote.
+
+Prints one JSON line.  `value` is the decode attention throughput (algorithmic decode
+bytes / decode time); compress time per 32K tokens, per-stage times, the decode kernel's
+roofline and the CPU oracle baseline are reported beside it.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+N_INPUT_COPIES = 3             # 3 x 134 MB of K/V
+N_CACHE_SLOTS = 24             # 24 x 28 MB of compressed caches
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="llama_32k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def decode_bytes(shape, cache, n_queries=1):
+    """Algorithmic bytes one decode must move: packed coefficients, exact slots, the stored
+    ranks and chunk offsets, both fp32 bases, queries and outputs."""
+    es = 2 if shape.dtype == "bf16" else 4
+    G, H, d = shape.G, shape.H, 128
+    coef = 2 * G * cache.B * es
+    exact = 2 * G * cache.n_exact * d * es
+    meta = cache.N + (cache.chunk_off.numel()) * 4
+    bases = 2 * G * d * d * 4
+    qo = 2 * n_queries * H * d * es
+    return coef + exact + meta + bases + qo
+
+
+def compress_bytes(shape, cache):
+    """Minimum bytes of one compress: K and V read once, window queries and bases read,
+    packed coefficients, ranks, layout tables and exact rows written."""
+    es = 2 if shape.dtype == "bf16" else 4
+    G, H, d, n, w = shape.G, shape.H, 128, shape.n, shape.w
+    read = 2 * n * G * d * es + w * H * d * es + 2 * G * d * d * 4
+    write = 2 * G * cache.B * es + 2 * G * w * d * es + cache.N * (1 + 1 + 4) + cache.chunk_off.numel() * 4
+    return read + write
+
+
+def cpu_baseline(cfg, li, shape, dbytes):
+    import oracle
+    t0 = time.perf_counter()
+    oc = oracle.compress(li.K, li.V, li.Qw, li.PK, li.PV, cfg["H"], cfg["kappa"], cfg["r_min"], cfg["dtype"])
+    t1 = time.perf_counter()
+    oracle.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[0], cfg["H"])
+    t2 = time.perf_counter()
+    return {
+        "value": round(dbytes / (t2 - t1) / 1e9, 4),
+        "unit": "GB/s",
+        "cores": oracle.threads(),
+        "kind": "oracle",
+        "sample": f"one full {cfg['n']}-token layer of this workload: fp64 compress "
+                  f"({t1 - t0:.2f} s) then one decode query ({t2 - t1:.2f} s, reconstruct-in-place)",
+        "compress_ms_per_32k_tokens": round((t1 - t0) * 1e3 * 32768 / cfg["n"], 1),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this codec has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2607_15498_amd as vr
+    from workloads import CONFIGS, make_layer
+
+    cfg = CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    li = make_layer(cfg, n_queries=1)
+    shape = vr.Shape(n=cfg["n"], G=cfg["G"], H=cfg["H"], w=cfg["w"], r_min=cfg["r_min"],
+                     kappa_pct=cfg["kappa"], dtype=cfg["dtype"])
+    dt = shape.torch_dtype
+    up = lambda a, t=dt: torch.from_numpy(np.ascontiguousarray(a)).to(t).to(dev)
+    Ks = [up(li.K) for _ in range(N_INPUT_COPIES)]
+    Vs = [up(li.V) for _ in range(N_INPUT_COPIES)]
+    Qw, q = up(li.Qw), up(li.q)
+    PK, PV = up(li.PK, torch.float32), up(li.PV, torch.float32)
+    slots = [vr.new_cache(shape, device=dev) for _ in range(N_CACHE_SLOTS)]
+    sbars = [torch.empty(shape.N, dtype=torch.float32, device=dev) for _ in range(N_INPUT_COPIES)]
+    out = torch.empty_like(q)
+    ws_c = torch.zeros(vr.library().varrate_compress_workspace_bytes(__import__("ctypes").byref(shape.c())),
+                       dtype=torch.uint8, device=dev)
+    ws_d = vr.decode_workspace(shape, 1, 1, dev)
+
+    # fill every slot once (untimed) so each decode reads a real compressed cache
+    for i, c in enumerate(slots):
+        j = i % N_INPUT_COPIES
+        vr.compress(shape, Ks[j], Vs[j], Qw, PK, PV, cache=c, sbar_out=sbars[j], workspace=ws_c)
+    torch.cuda.synchronize()
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    n_ev = args.steps
+    E = {k: [ev() for _ in range(n_ev + 1)] for k in ("sal", "alloc", "proj", "dec")}
+
+    def step(i, rec=None):
+        j = i % N_INPUT_COPIES
+        c = slots[i % N_CACHE_SLOTS]
+        d = slots[(i + N_CACHE_SLOTS // 2) % N_CACHE_SLOTS]
+        if rec is not None: E["sal"][rec].record()
+        vr.salience(shape, Ks[j], Qw, sbars[j], workspace=ws_c)
+        if rec is not None: E["alloc"][rec].record()
+        vr.allocate(shape, sbars[j], c, workspace=ws_c)
+        if rec is not None: E["proj"][rec].record()
+        vr.project(shape, Ks[j], Vs[j], PK, PV, c, workspace=ws_c)
+        if rec is not None: E["dec"][rec].record()
+        vr.decode(shape, [d], q, PK, PV, out=out, workspace=ws_d)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    end_ev = [ev() for _ in range(n_ev)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, rec=i)
+        end_ev[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    def span(a, b):
+        return [a[i].elapsed_time(b[i]) for i in range(n_ev)]
+
+    t_sal = span(E["sal"], E["alloc"])
+    t_alloc = span(E["alloc"], E["proj"])
+    t_proj = span(E["proj"], E["dec"])
+    t_dec = span(E["dec"], end_ev)
+    ms_dec = float(np.mean(t_dec))
+    ms_comp = float(np.mean(t_sal) + np.mean(t_alloc) + np.mean(t_proj))
+    dbytes = decode_bytes(shape, slots[0])
+    cbytes = compress_bytes(shape, slots[0])
+    dec_gbs = dbytes * n_ev / (float(np.sum(t_dec)) * 1e-3) / 1e9
+    result = {
+        "metric": "compressed decode attn GB/s (% HBM peak) + compress ms per 32K tokens, 1 GPU",
+        "value": round(dec_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg["dtype"] == "bf16" else "f32",
+        "data": "synthetic (seeded keys/values/queries with planted salient tokens; "
+                "offline PCA bases from disjoint calibration draws)",
+        "config": {"workload": f"{args.config}: 1 layer, {cfg['G']} KV x {cfg['H']} q heads, d 128, "
+                               f"n {cfg['n']}, w {cfg['w']}, budget {cfg['kappa']}%, r_min {cfg['r_min']}",
+                   "decode_batch": 1, "coded_budget_B": slots[0].B},
+        "pct_hbm_peak": round(100 * dec_gbs / HBM_PEAK_GBS, 2),
+        "compress_ms_per_32k_tokens": round(ms_comp * 32768 / cfg["n"], 4),
+        "compress_GBps_algorithmic": round(cbytes / (ms_comp * 1e-3) / 1e9, 1),
+        "stage_ms": {"salience": round(float(np.mean(t_sal)), 4), "allocate": round(float(np.mean(t_alloc)), 4),
+                     "project": round(float(np.mean(t_proj)), 4), "decode": round(ms_dec, 4)},
+        "roofline": {"kernel": "decode_kernel (rank-space decode attention)", "bound": "hbm",
+                     "achieved": round(dbytes / (ms_dec * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(dbytes / (ms_dec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": int(dbytes)},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(cfg, li, shape, dbytes)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
