@@ -96,8 +96,8 @@ typedef struct varrate_shape {
 typedef struct varrate_cache {
     void*     coef_k;       /* [G][coef_stride] dtype                                      */
     void*     coef_v;       /* [G][coef_stride] dtype                                      */
-    uint8_t*  rank;         /* [N]                                                          */
-    uint8_t*  srank;        /* [N] ranks in stored order                                    */
+    uint8_t*  rank;         /* [N], allocation padded to a multiple of 64 bytes             */
+    uint8_t*  srank;        /* [N] ranks in stored order, allocation padded likewise        */
     uint32_t* sidx;         /* [N] stored position -> original token index                  */
     uint32_t* chunk_off;    /* [n_chunks + 1]                                               */
     void*     k_exact;      /* [G][cap][d] dtype                                            */

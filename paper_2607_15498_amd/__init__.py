@@ -108,8 +108,8 @@ def new_cache(shape: Shape, cap: Optional[int] = None, device="cuda") -> Cache:
     return Cache(
         coef_k=torch.zeros((G, b.coef_stride), dtype=dt, device=device),
         coef_v=torch.zeros((G, b.coef_stride), dtype=dt, device=device),
-        rank=torch.zeros(b.rank, dtype=torch.uint8, device=device),
-        srank=torch.zeros(b.srank, dtype=torch.uint8, device=device),
+        rank=torch.zeros(b.rank, dtype=torch.uint8, device=device)[: b.N],
+        srank=torch.zeros(b.srank, dtype=torch.uint8, device=device)[: b.N],
         sidx=torch.zeros(b.N, dtype=torch.int32, device=device),
         chunk_off=torch.zeros(b.n_chunks + 1, dtype=torch.int32, device=device),
         k_exact=torch.zeros((G, cap, HEAD_DIM), dtype=dt, device=device),

@@ -18,8 +18,9 @@
 // most-significant-digit radix select (11-bit digits, common-prefix skipping) over the
 // 2 x 64-bit key.  All arithmetic is integer: the ranks are bit-exact and deterministic.
 //
-// Layout.  A second kernel sorts every chunk of 256 tokens by (rank desc, index asc) with
-// one wave per chunk (counting sort + ballot matching), writing srank / sidx.
+// Every pass over the N tokens keeps eight independent loads in flight per thread.  The
+// selection's first digit comes from phi < Q directly; when the chosen bucket holds at most
+// 2048 candidates they are gathered into LDS and the remaining digits never touch memory.
 #include "vr_internal.h"
 
 namespace vr {
@@ -97,11 +98,120 @@ struct SelState {
     int64_t need;
     int phase;         // 0: narrowing phi, 1: narrowing (u, ~t)
     int done;
+    int ncand;         // candidates gathered into LDS
 };
 
 __device__ __forceinline__ uint64_t lo_key(uint32_t u, int64_t t) {
     return ((uint64_t)u << 24) | (uint64_t)(0xFFFFFFu - (uint32_t)t);
 }
+
+// Visit tokens t = tid, tid + AL_T, ... with U independent loads in flight per thread.
+template <int U, class Load, class Proc>
+__device__ __forceinline__ void sweep(int64_t N, Load load, Proc proc) {
+    for (int64_t b = 0; b < N; b += (int64_t)U * AL_T) {
+        decltype(load((int64_t)0)) v[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t t = b + (int64_t)k * AL_T + threadIdx.x;
+            if (t < N) v[k] = load(t);
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t t = b + (int64_t)k * AL_T + threadIdx.x;
+            if (t < N) proc(t, v[k]);
+        }
+    }
+}
+
+struct PhiU {
+    uint64_t phi;
+    uint32_t u;
+};
+
+struct Fin {
+    uint64_t phi;
+    uint32_t u;
+    uint32_t r;
+};
+
+// Most-significant-digit radix narrowing of the selection threshold over the candidates
+// enumerated by visit(f) (f(hi, lo) per uncapped candidate), starting from `sel`.
+template <class Visit>
+__device__ void radix_narrow(Visit visit, SelState& sel, uint32_t* cnt, uint32_t* wtot32,
+                             unsigned long long* wtot64) {
+    const int tid = threadIdx.x;
+    while (!sel.done) {
+        const int phase = sel.phase;
+        const uint64_t pv = sel.pv, pm = sel.pm, T_hi = sel.T_hi;
+        auto field = [&](uint64_t hi, uint64_t lo, uint64_t& f) -> bool {
+            if (phase == 0) {
+                f = hi;
+            } else {
+                if (hi != T_hi) return false;
+                f = lo;
+            }
+            return (f & pm) == pv;
+        };
+        uint64_t fmn = ~0ull, fmx = 0;
+        visit([&](uint64_t hi, uint64_t lo) {
+            uint64_t f;
+            if (field(hi, lo, f)) {
+                fmn = f < fmn ? f : fmn;
+                fmx = f > fmx ? f : fmx;
+            }
+        });
+        fmn = block_reduce<unsigned long long>(fmn, wtot64, [](unsigned long long a, unsigned long long b) { return a < b ? a : b; });
+        fmx = block_reduce<unsigned long long>(fmx, wtot64, [](unsigned long long a, unsigned long long b) { return a > b ? a : b; });
+        if (fmn == fmx) {
+            if (tid == 0) {
+                if (phase == 0) {
+                    sel.T_hi = fmn; sel.phase = 1; sel.pv = 0; sel.pm = 0;
+                } else {
+                    sel.T_lo = fmn; sel.done = 1;   // keys are unique: a single candidate
+                }
+            }
+            __syncthreads();
+            continue;
+        }
+        const int p = 63 - __clzll((long long)(fmn ^ fmx));
+        const int sh = p > 10 ? p - 10 : 0;
+        const uint64_t dmask = (1ull << (p - sh + 1)) - 1;
+        const uint64_t above_mask = (p == 63) ? 0ull : ~((2ull << p) - 1);
+        for (int i = tid; i < 2048; i += AL_T) cnt[i] = 0;
+        __syncthreads();
+        visit([&](uint64_t hi, uint64_t lo) {
+            uint64_t f;
+            if (field(hi, lo, f)) atomicAdd(&cnt[(f >> sh) & dmask], 1u);
+        });
+        __syncthreads();
+        const int d0 = 2047 - 2 * tid, d1 = d0 - 1;
+        const uint32_t c0 = cnt[d0], c1 = cnt[d1];
+        uint32_t tot;
+        const uint32_t above0 = block_exscan<uint32_t>(c0 + c1, wtot32, tot);
+        const int64_t need = sel.need;
+        __syncthreads();
+        int hit = -1;
+        uint32_t hit_above = 0, hit_cnt = 0;
+        if ((int64_t)above0 < need && need <= (int64_t)(above0 + c0)) { hit = d0; hit_above = above0; hit_cnt = c0; }
+        const uint32_t above1 = above0 + c0;
+        if ((int64_t)above1 < need && need <= (int64_t)(above1 + c1)) { hit = d1; hit_above = above1; hit_cnt = c1; }
+        if (hit >= 0) {
+            const int64_t nn = need - (int64_t)hit_above;
+            const uint64_t npv = (fmn & above_mask) | ((uint64_t)hit << sh);
+            sel.need = nn;
+            sel.pv = npv;
+            sel.pm = ~((1ull << sh) - 1);
+            if ((int64_t)hit_cnt == nn) {
+                if (phase == 0) { sel.T_hi = npv; sel.T_lo = 0; }
+                else { sel.T_lo = npv; }
+                sel.done = 1;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+constexpr int SEL_CAP = 2048;    // candidates the selection can finish in LDS
 
 __global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ sbar, int64_t N,
                                                       int64_t B, int r_min, int R,
@@ -115,17 +225,16 @@ __global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ s
     __shared__ unsigned long long wtot64[AL_W];
     __shared__ uint32_t wtot32[AL_W];
     __shared__ float redf[AL_W];
-    __shared__ unsigned long long bc[8];
     __shared__ SelState sel;
     const int tid = threadIdx.x;
+    constexpr int U = 8;
 
     // ---- 1. min / max of the pooled salience
     float mn = INFINITY, mx = -INFINITY;
-    for (int64_t t = tid; t < N; t += AL_T) {
-        const float s = sbar[t];
+    sweep<U>(N, [&](int64_t t) { return sbar[t]; }, [&](int64_t, float s) {
         mn = fminf(mn, s);
         mx = fmaxf(mx, s);
-    }
+    });
     mn = block_reduce<float>(mn, redf, [](float a, float b) { return fminf(a, b); });
     mx = block_reduce<float>(mx, redf, [](float a, float b) { return fmaxf(a, b); });
 
@@ -136,12 +245,12 @@ __global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ s
     const double lo = (double)mn;
     const double range = (double)mx - lo;
     uint32_t umax = 0;
-    for (int64_t t = tid; t < N; t += AL_T) {
+    sweep<U>(N, [&](int64_t t) { return sbar[t]; }, [&](int64_t t, float s) {
         uint32_t u;
         if (flat) {
             u = (1u << 24) + 1u;
         } else {
-            const double num = (double)sbar[t] - lo;
+            const double num = (double)s - lo;
             double shat = num / range;
             // non-finite inputs cannot index past the histograms
             shat = shat >= 0.0 ? (shat <= 1.0 ? shat : 1.0) : 0.0;
@@ -151,7 +260,7 @@ __global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ s
         umax = u > umax ? u : umax;
         atomicAdd(&cnt[u >> CBITS], 1u);
         atomicAdd(&sm[u >> CBITS], (unsigned long long)u);
-    }
+    });
     umax = block_reduce<uint32_t>(umax, wtot32, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
     __syncthreads();
 
@@ -178,13 +287,12 @@ __global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ s
     // ---- 3. fine histogram of the low 12 bits inside bin bbest
     for (int i = tid; i <= NBIN; i += AL_T) { cnt[i] = 0; sm[i] = 0; }
     __syncthreads();
-    for (int64_t t = tid; t < N; t += AL_T) {
-        const uint32_t u = u_ws[t];
+    sweep<U>(N, [&](int64_t t) { return u_ws[t]; }, [&](int64_t, uint32_t u) {
         if ((int)(u >> CBITS) == bbest) {
             atomicAdd(&cnt[u & ((1u << CBITS) - 1)], 1u);
             atomicAdd(&sm[u & ((1u << CBITS) - 1)], (unsigned long long)u);
         }
-    }
+    });
     __syncthreads();
     const int nf = 1 << CBITS;
     lds_exscan<uint32_t>(cnt, nf + 1, wtot32);
@@ -207,114 +315,101 @@ __global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ s
     const int64_t kcap = (int64_t)(cge_next + fc_total - cnt[fbest + 1]);
     const uint64_t Q = slt_b + sm[fbest + 1];
     const int64_t M = B - (int64_t)R * kcap - (int64_t)r_min * (N - kcap);
+    const double invQ = 1.0 / (double)Q;
     __syncthreads();
 
     // ---- 4. floors and fractional keys
     unsigned long long fsum = 0;
-    for (int64_t t = tid; t < N; t += AL_T) {
-        const uint32_t u = u_ws[t];
+    sweep<U>(N, [&](int64_t t) { return u_ws[t]; }, [&](int64_t t, uint32_t u) {
         uint32_t base;
         uint64_t phi;
         if (u > tau_lo) {
             base = (uint32_t)R;
             phi = CAPPED;
         } else {
+            // num < 2^52 and Q < 2^45 are exact in fp64; the reciprocal quotient is within
+            // one unit of floor(num / Q) and the integer remainder corrects it exactly
             const uint64_t num = (uint64_t)u * (uint64_t)M;
-            const uint64_t f = num / Q;
-            phi = num - f * Q;
-            base = (uint32_t)(r_min + (int64_t)f);
+            int64_t f = (int64_t)((double)num * invQ);
+            int64_t rem = (int64_t)num - f * (int64_t)Q;
+            if (rem < 0) { f -= 1; rem += (int64_t)Q; }
+            if (rem >= (int64_t)Q) { f += 1; rem -= (int64_t)Q; }
+            phi = (uint64_t)rem;
+            base = (uint32_t)(r_min + f);
         }
         rank[t] = (uint8_t)base;
         phi_ws[t] = phi;
         fsum += base;
-    }
+    });
     fsum = block_reduce<unsigned long long>(fsum, wtot64,
                                             [](unsigned long long a, unsigned long long b) { return a + b; });
     const int64_t rho = B - (int64_t)fsum;
 
-    // ---- 5. radix select of the rho largest (phi, u, -t) keys among uncapped tokens
+    // ---- 5. select the rho largest (phi, u, -t) keys among uncapped tokens
+    auto load_pu = [&](int64_t t) { return PhiU{phi_ws[t], u_ws[t]}; };
     if (tid == 0) {
         sel.pv = 0; sel.pm = 0; sel.T_hi = ~0ull; sel.T_lo = ~0ull;
-        sel.need = rho; sel.phase = 0; sel.done = rho <= 0;
+        sel.need = rho; sel.phase = 0; sel.done = rho <= 0; sel.ncand = 0;
     }
     __syncthreads();
-    while (!sel.done) {
-        const int phase = sel.phase;
-        const uint64_t pv = sel.pv, pm = sel.pm, T_hi = sel.T_hi;
-        // min / max of the field over the current candidates
-        uint64_t fmn = ~0ull, fmx = 0;
-        for (int64_t t = tid; t < N; t += AL_T) {
-            const uint64_t phi = phi_ws[t];
-            if (phi == CAPPED) continue;
-            uint64_t f;
-            if (phase == 0) {
-                f = phi;
-            } else {
-                if (phi != T_hi) continue;
-                f = lo_key(u_ws[t], t);
-            }
-            if ((f & pm) != pv) continue;
-            fmn = f < fmn ? f : fmn;
-            fmx = f > fmx ? f : fmx;
-        }
-        fmn = block_reduce<unsigned long long>(fmn, wtot64, [](unsigned long long a, unsigned long long b) { return a < b ? a : b; });
-        fmx = block_reduce<unsigned long long>(fmx, wtot64, [](unsigned long long a, unsigned long long b) { return a > b ? a : b; });
-        if (fmn == fmx) {
-            if (tid == 0) {
-                if (phase == 0) {
-                    sel.T_hi = fmn; sel.phase = 1; sel.pv = 0; sel.pm = 0;
-                } else {
-                    sel.T_lo = fmn; sel.done = 1;   // keys are unique: a single candidate
-                }
-            }
-            __syncthreads();
-            continue;
-        }
-        const int p = 63 - __clzll((long long)(fmn ^ fmx));
-        const int sh = p > 10 ? p - 10 : 0;
-        const uint64_t dmask = (1ull << (p - sh + 1)) - 1;
-        const uint64_t above_mask = (p == 63) ? 0ull : ~((2ull << p) - 1);
+    if (!sel.done) {
+        // first digit: phi < Q, so its top 11 significant bits need no range pass
+        const uint64_t qm1 = Q > 1 ? Q - 1 : 1;
+        const int qb = 64 - __clzll((long long)qm1);
+        const int sh0 = qb > 11 ? qb - 11 : 0;
         for (int i = tid; i < 2048; i += AL_T) cnt[i] = 0;
         __syncthreads();
-        for (int64_t t = tid; t < N; t += AL_T) {
-            const uint64_t phi = phi_ws[t];
-            if (phi == CAPPED) continue;
-            uint64_t f;
-            if (phase == 0) {
-                f = phi;
-            } else {
-                if (phi != T_hi) continue;
-                f = lo_key(u_ws[t], t);
-            }
-            if ((f & pm) != pv) continue;
-            atomicAdd(&cnt[(f >> sh) & dmask], 1u);
-        }
+        sweep<U>(N, [&](int64_t t) { return phi_ws[t]; }, [&](int64_t, uint64_t phi) {
+            if (phi != CAPPED) atomicAdd(&cnt[(phi >> sh0) & 2047], 1u);
+        });
         __syncthreads();
-        // suffix counts from the top digit down: thread k owns digits 2047-2k, 2046-2k
         const int d0 = 2047 - 2 * tid, d1 = d0 - 1;
         const uint32_t c0 = cnt[d0], c1 = cnt[d1];
         uint32_t tot;
         const uint32_t above0 = block_exscan<uint32_t>(c0 + c1, wtot32, tot);
         const int64_t need = sel.need;
         __syncthreads();
+        const uint32_t above1 = above0 + c0;
         int hit = -1;
         uint32_t hit_above = 0, hit_cnt = 0;
         if ((int64_t)above0 < need && need <= (int64_t)(above0 + c0)) { hit = d0; hit_above = above0; hit_cnt = c0; }
-        const uint32_t above1 = above0 + c0;
         if ((int64_t)above1 < need && need <= (int64_t)(above1 + c1)) { hit = d1; hit_above = above1; hit_cnt = c1; }
         if (hit >= 0) {
             const int64_t nn = need - (int64_t)hit_above;
-            const uint64_t npv = (fmn & above_mask) | ((uint64_t)hit << sh);
             sel.need = nn;
-            sel.pv = npv;
-            sel.pm = ~((1ull << sh) - 1);
-            if ((int64_t)hit_cnt == nn) {
-                if (phase == 0) { sel.T_hi = npv; sel.T_lo = 0; }
-                else { sel.T_lo = npv; }
-                sel.done = 1;
-            }
+            sel.pv = (uint64_t)hit << sh0;
+            sel.pm = ~((1ull << sh0) - 1);
+            if ((int64_t)hit_cnt == nn) { sel.T_hi = sel.pv; sel.T_lo = 0; sel.done = 1; }
+            sel.ncand = (int)hit_cnt;
         }
         __syncthreads();
+        if (!sel.done && sel.ncand <= SEL_CAP) {
+            // gather the bucket's candidates into LDS and finish there
+            unsigned long long* chi = sm;
+            unsigned long long* clo = sm + SEL_CAP;
+            const uint64_t pv = sel.pv, pm = sel.pm;
+            __syncthreads();
+            if (tid == 0) sel.ncand = 0;
+            __syncthreads();
+            sweep<U>(N, load_pu, [&](int64_t t, PhiU x) {
+                if (x.phi != CAPPED && (x.phi & pm) == pv) {
+                    const int slot = atomicAdd(&sel.ncand, 1);
+                    chi[slot] = x.phi;
+                    clo[slot] = lo_key(x.u, t);
+                }
+            });
+            __syncthreads();
+            const int nc = sel.ncand;
+            radix_narrow([&](auto f) {
+                for (int i = tid; i < nc; i += AL_T) f(chi[i], clo[i]);
+            }, sel, cnt, wtot32, wtot64);
+        } else if (!sel.done) {
+            radix_narrow([&](auto f) {
+                sweep<U>(N, load_pu, [&](int64_t t, PhiU x) {
+                    if (x.phi != CAPPED) f(x.phi, lo_key(x.u, t));
+                });
+            }, sel, cnt, wtot32, wtot64);
+        }
     }
     const uint64_t T_hi = sel.T_hi, T_lo = sel.T_lo;
     const bool any = rho > 0;
@@ -322,89 +417,37 @@ __global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ s
     // ---- 6. final ranks and chunk sums
     for (int i = tid; i < n_chunks; i += AL_T) cnt[i] = 0;
     __syncthreads();
-    for (int64_t t = tid; t < N; t += AL_T) {
-        const uint64_t phi = phi_ws[t];
-        uint32_t r = rank[t];
-        if (any && phi != CAPPED) {
-            const bool take = phi > T_hi || (phi == T_hi && lo_key(u_ws[t], t) >= T_lo);
-            if (take) {
-                r += 1;
-                rank[t] = (uint8_t)r;
-            }
+    for (int64_t b = 0; b < N; b += (int64_t)U * AL_T) {
+        Fin v[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t t = b + (int64_t)k * AL_T + tid;
+            if (t < N) v[k] = Fin{phi_ws[t], u_ws[t], rank[t]};
         }
-        atomicAdd(&cnt[t >> 8], r);
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t t = b + (int64_t)k * AL_T + tid;
+            uint32_t r = 0;
+            if (t < N) {
+                r = v[k].r;
+                if (any && v[k].phi != CAPPED) {
+                    const bool take = v[k].phi > T_hi || (v[k].phi == T_hi && lo_key(v[k].u, t) >= T_lo);
+                    if (take) {
+                        r += 1;
+                        rank[t] = (uint8_t)r;
+                    }
+                }
+            }
+            // a wave covers 64 consecutive tokens, all inside one 256-token chunk
+            const uint32_t ws = wave_sum(r);
+            const int64_t tw = b + (int64_t)k * AL_T + (tid & ~63);
+            if ((tid & 63) == 0 && tw < N) atomicAdd(&cnt[tw >> 8], ws);
+        }
     }
     __syncthreads();
     const uint32_t total = lds_exscan<uint32_t>(cnt, n_chunks, wtot32);
     for (int i = tid; i < n_chunks; i += AL_T) chunk_off[i] = cnt[i];
     if (tid == 0) chunk_off[n_chunks] = total;
-}
-
-// ----------------------------------------------------------------------------------------
-// Chunk-local storage order: one wave per chunk of 256 tokens, stable by (rank desc, t asc).
-__global__ __launch_bounds__(64) void layout_kernel(const uint8_t* __restrict__ rank, int64_t N,
-                                                    uint8_t* __restrict__ srank,
-                                                    uint32_t* __restrict__ sidx) {
-    __shared__ uint32_t hist[192];
-    __shared__ uint32_t start[192];
-    __shared__ uint32_t run[192];
-    const int lane = threadIdx.x;
-    const int64_t t0 = (int64_t)blockIdx.x * CHUNK;
-    const int T = (int)((N - t0) < CHUNK ? (N - t0) : CHUNK);
-    for (int i = lane; i < 192; i += 64) { hist[i] = 0; run[i] = 0; }
-    __syncthreads();
-    int r[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int idx = k * 64 + lane;
-        r[k] = idx < T ? (int)rank[t0 + idx] : -1;
-        if (r[k] >= 0) atomicAdd(&hist[r[k]], 1u);
-    }
-    __syncthreads();
-    // start[v] = number of tokens with rank > v.  Lane handles descending slots 3l..3l+2
-    // (slot k <-> rank 128 - k).
-    uint32_t h[3], loc = 0;
-#pragma unroll
-    for (int e = 0; e < 3; ++e) {
-        const int k = 3 * lane + e;
-        h[e] = k <= 128 ? hist[128 - k] : 0;
-        loc += h[e];
-    }
-    uint32_t x = loc;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        uint32_t y = __shfl_up(x, off, 64);
-        if (lane >= off) x += y;
-    }
-    uint32_t pre = x - loc;
-#pragma unroll
-    for (int e = 0; e < 3; ++e) {
-        const int k = 3 * lane + e;
-        if (k <= 128) start[128 - k] = pre;
-        pre += h[e];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int idx = k * 64 + lane;
-        const int v = r[k];
-        uint64_t pending = __ballot(v >= 0);
-        while (pending) {
-            const int leader = __ffsll((unsigned long long)pending) - 1;
-            const int rv = __shfl(v, leader, 64);
-            const uint64_t mask = __ballot(v == rv);
-            if (v == rv) {
-                const uint64_t below = mask & ((1ull << lane) - 1);
-                const uint32_t pos = start[rv] + run[rv] + (uint32_t)__popcll(below);
-                srank[t0 + pos] = (uint8_t)rv;
-                sidx[t0 + pos] = (uint32_t)(t0 + idx);
-            }
-            __syncthreads();
-            if (lane == leader) run[rv] += (uint32_t)__popcll(mask);
-            __syncthreads();
-            pending &= ~mask;
-        }
-    }
 }
 
 size_t allocate_ws_bytes(const varrate_shape& sh) {
@@ -420,13 +463,6 @@ hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_c
     const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
     alloc_kernel<<<1, AL_T, 0, st>>>(sbar, N, c.B, sh.r_min, D, u_ws, phi_ws, c.rank, c.chunk_off,
                                      n_chunks);
-    return hipGetLastError();
-}
-
-hipError_t launch_layout(const varrate_shape& sh, varrate_cache& c, hipStream_t st) {
-    const int64_t N = sh.n - sh.w;
-    const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
-    layout_kernel<<<n_chunks, 64, 0, st>>>(c.rank, N, c.srank, c.sidx);
     return hipGetLastError();
 }
 

@@ -113,7 +113,7 @@ int varrate_cache_bytes(const varrate_shape* sh, int64_t cap, varrate_cache_byte
     out->n_chunks = (out->N + VARRATE_CHUNK - 1) / VARRATE_CHUNK;
     out->coef_stride = ((out->B + VARRATE_COEF_PAD + 63) / 64) * 64;
     out->coef_k = out->coef_v = (size_t)sh->G * out->coef_stride * es;
-    out->rank = out->srank = (size_t)out->N;
+    out->rank = out->srank = (size_t)((out->N + 63) / 64) * 64;   // padded for 16-byte loads
     out->sidx = (size_t)out->N * 4;
     out->chunk_off = (size_t)(out->n_chunks + 1) * 4;
     out->k_exact = out->v_exact = (size_t)sh->G * cap * VARRATE_HEAD_DIM * es;
@@ -172,8 +172,6 @@ int varrate_project(const varrate_shape* sh, const void* K, const void* V, const
     c->N = sh->n - sh->w;
     c->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
     hipStream_t st = (hipStream_t)stream;
-    rc = hip_status(launch_layout(*sh, *c, st), "layout launch");
-    if (rc) return rc;
     rc = hip_status(launch_project(*sh, K, V, PK, PV, *c, st), "project launch");
     if (rc) return rc;
     c->n_exact = sh->w;
@@ -237,7 +235,7 @@ int varrate_decode_attn(const varrate_shape* sh, const varrate_cache* caches, in
         if (caches[s].coef_stride != caches[0].coef_stride || caches[s].cap != caches[0].cap)
             return fail(VARRATE_EINVAL, "caches must share coef_stride and cap");
     }
-    if (decode_units(*sh, S, Q) > 16384)
+    if (!decode_supported(*sh, S, Q))
         return fail(VARRATE_EUNSUPPORTED, "S * G * ceil(Q H/G / 16) exceeds 16384 merge slots");
     if ((rc = ws_check(ws, ws_bytes, decode_ws_bytes(*sh, S, Q)))) return rc;
     return hip_status(launch_decode(*sh, caches, S, q, Q, PK, PV, out, (uint8_t*)ws, (hipStream_t)stream),

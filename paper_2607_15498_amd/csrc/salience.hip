@@ -33,30 +33,43 @@ template <> struct KTile<true> {
     static constexpr int ROW_U32 = 136;
 };
 
-// Stage SAL_KSUB keys of KV head g starting at key k0 into LDS (zero rows past n).
+// Keys of one staging step: SAL_KSUB keys x 16 pieces of 8 elements; each thread holds
+// 4 pieces (bf16: 16 bytes each; fp32: 32 bytes each, split into hi/lo when stored).
+template <bool F32> struct KRegs { u32x4 a[4]; u32x4 b[4]; };
+
 template <bool F32>
-__device__ __forceinline__ void stage_keys(uint32_t* lds, const void* K, int64_t n, int G, int g,
-                                           int64_t k0) {
-    constexpr int RU = KTile<F32>::ROW_U32;
-    if constexpr (!F32) {
-        // 64 keys x 16 chunks of 16 B
-        for (int idx = threadIdx.x; idx < SAL_KSUB * 16; idx += SAL_THREADS) {
-            int key = idx >> 4, ch = idx & 15;
-            int64_t t = k0 + key;
-            u32x4 v = {0, 0, 0, 0};
-            if (t < n) v = load16((const uint16_t*)K + ((t * G + g) * D + ch * 8));
-            *reinterpret_cast<u32x4*>(lds + key * RU + ch * 4) = v;
-        }
-    } else {
-        for (int idx = threadIdx.x; idx < SAL_KSUB * 16; idx += SAL_THREADS) {
-            int key = idx >> 4, ch = idx & 15;
-            int64_t t = k0 + key;
-            float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-            if (t < n) {
+__device__ __forceinline__ void load_keys(KRegs<F32>& r, const void* K, int64_t n, int G, int g, int64_t k0) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int idx = threadIdx.x + k * SAL_THREADS;
+        const int key = idx >> 4, ch = idx & 15;
+        const int64_t t = k0 + key;
+        r.a[k] = r.b[k] = u32x4{0, 0, 0, 0};
+        if (t < n) {
+            if constexpr (!F32) {
+                r.a[k] = load16((const uint16_t*)K + ((t * G + g) * D + ch * 8));
+            } else {
                 const float* src = (const float*)K + ((t * G + g) * D + ch * 8);
-                u32x4 a = load16(src), b = load16(src + 4);
-                for (int e = 0; e < 4; ++e) { x[e] = __uint_as_float(a[e]); x[4 + e] = __uint_as_float(b[e]); }
+                r.a[k] = load16(src);
+                r.b[k] = load16(src + 4);
             }
+        }
+    }
+}
+
+template <bool F32>
+__device__ __forceinline__ void store_keys(uint32_t* lds, const KRegs<F32>& r) {
+    constexpr int RU = KTile<F32>::ROW_U32;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int idx = threadIdx.x + k * SAL_THREADS;
+        const int key = idx >> 4, ch = idx & 15;
+        if constexpr (!F32) {
+            *reinterpret_cast<u32x4*>(lds + key * RU + ch * 4) = r.a[k];
+        } else {
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { x[e] = __uint_as_float(r.a[k][e]); x[4 + e] = __uint_as_float(r.b[k][e]); }
             u32x4 hi, lo;
             split8(x, hi, lo);
             *reinterpret_cast<u32x4*>(lds + key * RU + ch * 4) = hi;
@@ -140,10 +153,13 @@ __global__ __launch_bounds__(SAL_THREADS) void sal_rowstats(const void* __restri
     }
     const float scale = 0.08838834764831845f;  // 1/sqrt(128)
 
+    KRegs<F32> kr;
+    load_keys<F32>(kr, K, n, G, g, kbeg);
     for (int64_t k0 = kbeg; k0 < kend; k0 += SAL_KSUB) {
         __syncthreads();
-        stage_keys<F32>(lds, K, n, G, g, k0);
+        store_keys<F32>(lds, kr);
         __syncthreads();
+        if (k0 + SAL_KSUB < kend) load_keys<F32>(kr, K, n, G, g, k0 + SAL_KSUB);
 #pragma unroll
         for (int j = 0; j < SAL_MAX_RT; ++j) {
             const int rt = wave + 4 * j;
@@ -195,18 +211,32 @@ __global__ __launch_bounds__(SAL_THREADS) void sal_rowstats(const void* __restri
     }
 }
 
-// merge: ML[g * rows + rho] = (M, 1/L).  One thread per (g, row).
-__global__ void sal_merge(const float2* __restrict__ stats, int nkb, int total_rows,
-                          float2* __restrict__ ML) {
-    const int r = blockIdx.x * blockDim.x + threadIdx.x;
-    if (r >= total_rows) return;
-    const float2* s = stats + (int64_t)r * nkb;
-    float M = -INFINITY;
-    for (int b = 0; b < nkb; ++b) M = fmaxf(M, s[b].x);
-    float L = 0.f;
-    for (int b = 0; b < nkb; ++b)
-        if (s[b].x != -INFINITY) L += s[b].y * fast_exp(s[b].x - M);
-    ML[r] = make_float2(M, 1.f / L);
+// merge: ML[g * rows + rho] = (M, 1/L).  16 threads per row read its block partials in
+// parallel and combine them with shuffles.
+__global__ __launch_bounds__(256) void sal_merge(const float2* __restrict__ stats, int nkb,
+                                                 int total_rows, float2* __restrict__ ML) {
+    const int r = blockIdx.x * 16 + (threadIdx.x >> 4), k = threadIdx.x & 15;
+    float m = -INFINITY, l = 0.f;
+    if (r < total_rows) {
+        const float2* s = stats + (int64_t)r * nkb;
+        for (int b = k; b < nkb; b += 16) {
+            const float2 v = s[b];
+            if (v.x == -INFINITY) continue;
+            const float mn = fmaxf(m, v.x);
+            l = (m == -INFINITY ? 0.f : l * fast_exp(m - mn)) + v.y * fast_exp(v.x - mn);
+            m = mn;
+        }
+    }
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+        const float mo = shfl_xor_f(m, off), lo = shfl_xor_f(l, off);
+        const float mn = fmaxf(m, mo);
+        const float a = m == -INFINITY ? 0.f : l * fast_exp(m - mn);
+        const float b = mo == -INFINITY ? 0.f : lo * fast_exp(mo - mn);
+        m = mn;
+        l = a + b;
+    }
+    if (k == 0 && r < total_rows) ML[r] = make_float2(m, 1.f / l);
 }
 
 // pass 2: s_part[g * N + t] = sum over the group's rows of exp(x - M) / L, t < N.
@@ -242,10 +272,13 @@ __global__ __launch_bounds__(SAL_THREADS) void sal_colsum(const void* __restrict
     }
     const float scale = 0.08838834764831845f;
 
+    KRegs<F32> kr;
+    load_keys<F32>(kr, K, n, G, g, kbeg);
     for (int64_t k0 = kbeg; k0 < kend; k0 += SAL_KSUB) {
         __syncthreads();
-        stage_keys<F32>(lds, K, n, G, g, k0);
+        store_keys<F32>(lds, kr);
         __syncthreads();
+        if (k0 + SAL_KSUB < kend) load_keys<F32>(kr, K, n, G, g, k0 + SAL_KSUB);
         for (int kt = 0; kt < SAL_KSUB / 16; ++kt) {
             float acc = 0.f;   // this lane's key column: sum over the wave's rows
 #pragma unroll
@@ -310,11 +343,11 @@ hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Q
     const int tr = sh.G * rows;
     if (sh.dtype == VARRATE_BF16) {
         sal_rowstats<false><<<g1, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, nkb);
-        sal_merge<<<(tr + 255) / 256, 256, 0, st>>>(stats, nkb, tr, ML);
+        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, nkb, tr, ML);
         sal_colsum<false><<<g2, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part);
     } else {
         sal_rowstats<true><<<g1, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, nkb);
-        sal_merge<<<(tr + 255) / 256, 256, 0, st>>>(stats, nkb, tr, ML);
+        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, nkb, tr, ML);
         sal_colsum<true><<<g2, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part);
     }
     sal_pool<<<(unsigned)((N + 255) / 256), 256, 0, st>>>(s_part, N, sh.G,

@@ -4,7 +4,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/varrate.h"
+#include "varrate.h"
 #include "vr_device.h"
 
 namespace vr {
@@ -17,12 +17,12 @@ size_t salience_ws_bytes(const varrate_shape& sh);
 size_t allocate_ws_bytes(const varrate_shape& sh);
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q);
 size_t decode_units(const varrate_shape& sh, int S, int Q);   // sequences x KV heads x row tiles
+bool decode_supported(const varrate_shape& sh, int S, int Q);
 
 hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Qw, float* sbar,
                            uint8_t* ws, hipStream_t st);
 hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_cache& c,
                            uint8_t* ws, hipStream_t st);
-hipError_t launch_layout(const varrate_shape& sh, varrate_cache& c, hipStream_t st);
 hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V, const float* PK,
                           const float* PV, varrate_cache& c, hipStream_t st);
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
