@@ -35,6 +35,7 @@ constexpr int DC_MAX_REC = 512;            // partial records per (sequence, hea
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 __device__ __forceinline__ f32x4 mfma16(u32x2 a, u32x2 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a),
@@ -66,28 +67,6 @@ template <bool F32> struct Elem;
 template <> struct Elem<false> { typedef uint16_t T; };
 template <> struct Elem<true> { typedef float T; };
 
-// 8 consecutive elements at p (nv of them valid) as bf16 (hi, lo) fragments.
-template <bool F32>
-__device__ __forceinline__ void load_row8(const typename Elem<F32>::T* p, int nv, u32x4& hi, u32x4& lo) {
-    if constexpr (!F32) {
-        hi = nv > 0 ? keep_first(load16_a2(p), nv) : u32x4{0, 0, 0, 0};
-        lo = u32x4{0, 0, 0, 0};
-    } else {
-        float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        if (nv > 0) {
-            u32x4 a, b;
-            __builtin_memcpy(&a, p, 16);
-            __builtin_memcpy(&b, p + 4, 16);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                x[e] = e < nv ? __uint_as_float(a[e]) : 0.f;
-                x[4 + e] = 4 + e < nv ? __uint_as_float(b[e]) : 0.f;
-            }
-        }
-        split8(x, hi, lo);
-    }
-}
-
 // 4 fp32 -> bf16x4 (hi, lo)
 __device__ __forceinline__ void split4(const float* x, u32x2& hi, u32x2& lo) {
     uint32_t h[4], l[4];
@@ -97,49 +76,70 @@ __device__ __forceinline__ void split4(const float* x, u32x2& hi, u32x2& lo) {
     lo = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
 }
 
+// Staging: each round copies a contiguous coefficient range of both streams (K and V share
+// one layout) into LDS with one 16-byte load per unit, every unit of the round in flight
+// at once; the waves then run their tiles from LDS.
+constexpr int DC_STAGE_BYTES = 32768;                         // per stream and round
+constexpr int DC_UNITS = 2 * DC_STAGE_BYTES / 16 / DC_THREADS; // 16-byte units per thread
+constexpr int DC_STAGE_PAD = 64;                              // over-read slack of row gathers
+constexpr int DC_TB = 17;                                     // tile bases per chunk (16 + end)
+
 struct DecSmem {
-    float* qp;        // [16][128] query rows (rotated or scaled); merge: partial lanes
+    uint8_t* stK;     // [DC_STAGE_BYTES + pad] staged K coefficients of the round; after the
+    uint8_t* stV;     //   tiles: per-wave partial sums comb [4][nr4][128] f32 (spans both)
+    float* comb;
     u32x4* qf;        // [4 steps][hi, lo][64 lanes] score B-operand fragments
-    float* comb;      // [4][nr4][128]; merge: accR [nr4][128], accE [nr4][128]
     float* cm;        // [8][16]
     float* cl;        // [8][16]
     float* mrow;      // [16]
     float* lrow;      // [16]
-    uint32_t* cb;     // [DC_MAX_CPW]
-    int* cT;          // [DC_MAX_CPW]
-    int* flag;        // [4]
-    uint8_t* sr;      // [cpw][256]
-    uint16_t* so;     // [cpw][256]
+    int* cT;          // [DC_MAX_CPW] valid tokens per chunk
+    uint32_t* cb;     // [DC_MAX_CPW] chunk bases (chunk_off)
+    uint32_t* tb;     // [cpw][17] element offset of each 16-token tile start (+ chunk end)
+    uint8_t* sr;      // [cpw][256] stored ranks (0 past the chunk's end)
 };
 
-__device__ __forceinline__ DecSmem carve(uint8_t* smem, int nr4, int cpw) {
+__device__ __forceinline__ DecSmem carve(uint8_t* smem, int cpw) {
     DecSmem s;
-    float* f = reinterpret_cast<float*>(smem);
-    s.qp = f; f += 16 * D;
-    s.qf = reinterpret_cast<u32x4*>(f); f += 4 * 2 * 64 * 4;
-    s.comb = f; f += 4 * nr4 * D;
+    uint8_t* b = smem;
+    s.stK = b; b += DC_STAGE_BYTES + DC_STAGE_PAD;
+    s.stV = b; b += DC_STAGE_BYTES + DC_STAGE_PAD;
+    s.comb = reinterpret_cast<float*>(s.stK);
+    s.qf = reinterpret_cast<u32x4*>(b); b += 4 * 2 * 64 * 16;
+    float* f = reinterpret_cast<float*>(b);
     s.cm = f; f += DC_WAVES * 16;
     s.cl = f; f += DC_WAVES * 16;
     s.mrow = f; f += 16;
     s.lrow = f; f += 16;
-    uint32_t* u = reinterpret_cast<uint32_t*>(f);
-    s.cb = u; u += DC_MAX_CPW;
-    s.cT = reinterpret_cast<int*>(u); u += DC_MAX_CPW;
-    u += DC_MAX_CPW + 4;
-    s.flag = reinterpret_cast<int*>(u); u += 4;
-    s.sr = reinterpret_cast<uint8_t*>(u);                 // 16-byte aligned (sizes above)
-    s.so = reinterpret_cast<uint16_t*>(s.sr + cpw * CHUNK);
+    s.cT = reinterpret_cast<int*>(f); f += DC_MAX_CPW;
+    s.cb = reinterpret_cast<uint32_t*>(f); f += DC_MAX_CPW;
+    s.tb = reinterpret_cast<uint32_t*>(f);
+    uint8_t* e = reinterpret_cast<uint8_t*>(s.tb + ((cpw * DC_TB + 3) & ~3));
+    s.sr = e;                                               // 16-byte aligned
     return s;
 }
 
-static inline size_t decode_smem_bytes(int nr4, int cpw) {
-    return (size_t)(16 * D + 4 * 2 * 64 * 4 + 4 * nr4 * D + 2 * DC_WAVES * 16 + 32) * 4 +
-           (size_t)(3 * DC_MAX_CPW + 8) * 4 + (size_t)cpw * CHUNK * 3;
+static inline size_t decode_smem_bytes(int cpw) {
+    return 2 * (size_t)(DC_STAGE_BYTES + DC_STAGE_PAD) + 4 * 2 * 64 * 16 +
+           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW) * 4 + (size_t)((cpw * DC_TB + 3) & ~3) * 4 +
+           (size_t)cpw * CHUNK;
+}
+
+// 8 consecutive bf16 at element index a of an LDS array (any 2-byte alignment): five dword
+// reads realigned by a funnel shift.
+__device__ __forceinline__ u32x4 lds_row8_bf16(const uint32_t* w, int a) {
+    const int w0 = a >> 1;
+    const uint32_t sh = (uint32_t)(a & 1) * 16u;
+    const uint32_t d0 = w[w0], d1 = w[w0 + 1], d2 = w[w0 + 2], d3 = w[w0 + 3], d4 = w[w0 + 4];
+    return u32x4{__builtin_amdgcn_alignbit(d1, d0, sh), __builtin_amdgcn_alignbit(d2, d1, sh),
+                 __builtin_amdgcn_alignbit(d3, d2, sh), __builtin_amdgcn_alignbit(d4, d3, sh)};
 }
 
 template <bool F32>
 __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecParams p) {
     typedef typename Elem<F32>::T ET;
+    constexpr int EPU = 16 / (int)sizeof(ET);               // elements per 16-byte unit
+    constexpr int SE = DC_STAGE_BYTES / (int)sizeof(ET);     // staged elements per stream
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     const int x = blockIdx.x, gq = blockIdx.y, sq = blockIdx.z;
     const int g = gq / p.nqt, qt = gq % p.nqt;
@@ -147,11 +147,11 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     const int rows = min(16, p.rows_total - 16 * qt);
     const int nr4 = (rows + 3) & ~3;
     const bool exact = x == 0;          // dispatched first; the coded groups follow
-    const int xc = x - 1;               // coded chunk group
+    const int xc = x - 1;               // coded tile range
     const int cpw = p.cpw;
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int grp = lane >> 4, col = lane & 15;
-    DecSmem sm = carve(smem, nr4, cpw);
+    DecSmem sm = carve(smem, cpw);
     const float scale = 0.08838834764831845f;  // 1/sqrt(128)
     const ET* qsrc = reinterpret_cast<const ET*>(S.q);
 
@@ -161,39 +161,62 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     const bool q_ok = qrow_l < p.rows_total;
     const int query_l = q_ok ? qrow_l / p.hpg : 0, hh_l = q_ok ? qrow_l % p.hpg : 0;
     const ET* qv = qsrc + ((int64_t)query_l * p.H + g * p.hpg + hh_l) * D;
+    // Raw loads only (row 0 of the head stands in for a missing query row): nothing here may
+    // wait, so that the rank loads below issue right behind them; masking happens after.
     u32x4 pa[4][2];
-    u32x4 qb[4][2];
+    u32x4 qr[4][2];
+    const int qs_ = tid >> 7, qpart = (tid >> 6) & 1;   // exact: 4 steps x {hi, lo} x 64 lanes
     if (!exact) {
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             const float* src = P + (16 * wave + col) * D + 32 * s + 8 * grp;
             pa[s][0] = load16(src);
             pa[s][1] = load16(src + 4);
-            load_row8<F32>(qv + 32 * s + 8 * grp, q_ok ? 8 : 0, qb[s][0], qb[s][1]);
+            const ET* qsrc8 = qv + 32 * s + 8 * grp;
+            if constexpr (F32) { qr[s][0] = load16(qsrc8); qr[s][1] = load16(qsrc8 + 4); }
+            else qr[s][0] = load16_a2(qsrc8);
         }
+    } else {
+        const ET* src = qv + 32 * qs_ + 8 * grp;
+        if constexpr (F32) { qr[0][0] = load16(src); qr[0][1] = load16(src + 4); }
+        else qr[0][0] = load16_a2(src);
     }
     // ---- 1b. stored ranks and chunk bases of the chunks this tile range touches
     const int tau0 = exact ? 0 : xc * p.tpw;
     const int tau1 = exact ? 0 : min(tau0 + p.tpw, p.total_tiles);
     const int c_lo = tau0 >> 4;
     const int ncl = exact ? 0 : ((tau1 - 1) >> 4) - c_lo + 1;
+    // (ncl <= DC_MAX_CPW = 16 chunks: at most 256 rank vectors, one per thread)
+    u32x4 rv = {0, 0, 0, 0};
+    uint32_t cbv = 0;
+    const int64_t t_r = (int64_t)c_lo * CHUNK + (int64_t)tid * 16;
     if (!exact) {
-        const int64_t t_beg = (int64_t)c_lo * CHUNK;
-        for (int idx = tid; idx < ncl * (CHUNK / 16); idx += DC_THREADS) {
-            const int64_t t = t_beg + (int64_t)idx * 16;
-            u32x4 v = {0, 0, 0, 0};
-            if (t < p.N) v = load16(S.srank + t);      // srank is padded to a multiple of 64
-            *reinterpret_cast<u32x4*>(sm.sr + idx * 16) = v;
-        }
-        if (tid < ncl) {
-            const int c = c_lo + tid;
-            const int64_t t0 = (int64_t)c * CHUNK;
-            sm.cT[tid] = (int)((p.N - t0) < CHUNK ? (p.N - t0) : CHUNK);
-            sm.cb[tid] = S.chunk_off[c];
-        }
+        if (tid < ncl * (CHUNK / 16) && t_r < p.N) rv = load16(S.srank + t_r);   // srank padded to 64
+        if (tid < ncl) cbv = S.chunk_off[c_lo + tid];
     }
-    // ---- 1c. query rows: rotated into the key basis (coded) or as is (exact)
     if (!exact) {
+        if (tid < ncl * (CHUNK / 16)) *reinterpret_cast<u32x4*>(sm.sr + tid * 16) = rv;
+        if (tid < ncl) sm.cb[tid] = cbv;
+    }
+    __syncthreads();
+    // ---- 1c. score-operand fragments of the query rows (lane -> query row col, K group
+    //          grp; bf16 hi and lo parts), before any direct-to-LDS load is in flight
+    uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf);
+    if (!exact) {
+        // q' = P_K q / sqrt(d) by MFMA; C lane -> query row col, directions 16 wave + 4 grp + v
+        u32x4 qb[4][2];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if constexpr (F32) {
+                float x8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x8[e] = q_ok ? __uint_as_float(qr[s][e >> 2][e & 3]) : 0.f;
+                split8(x8, qb[s][0], qb[s][1]);
+            } else {
+                qb[s][0] = q_ok ? qr[s][0] : u32x4{0, 0, 0, 0};
+                qb[s][1] = u32x4{0, 0, 0, 0};
+            }
+        }
         f32x4 c = {0, 0, 0, 0};
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
@@ -206,30 +229,41 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
             c = mfma(al, qb[s][0], c);
             if constexpr (F32) c = mfma(ah, qb[s][1], c);
         }
+        // direction j = 16 wave + 4 grp + v is element (j & 7) of K group ((j & 31) >> 3) of
+        // step j >> 5: two bf16 pairs per lane, for the hi and the lo fragment
+        uint32_t h[4], l[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) sm.qp[col * D + 16 * wave + 4 * grp + v] = c[v] * scale;
+        for (int v = 0; v < 4; ++v) split_bf16(c[v] * scale, h[v], l[v]);
+        const int s = wave >> 1, gp = 2 * (wave & 1) + (grp >> 1), dw = 2 * (grp & 1);
+        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 0) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 1) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
     } else {
-        for (int idx = tid; idx < 16 * D; idx += DC_THREADS) {
-            const int r = idx / D, i = idx % D;
-            const int qrow = 16 * qt + r;
-            float val = 0.f;
-            if (qrow < p.rows_total) {
-                const int query = qrow / p.hpg, hh = qrow % p.hpg;
-                const ET e = qsrc[((int64_t)query * p.H + g * p.hpg + hh) * D + i];
-                if constexpr (F32) val = e; else val = bf16_to_f32(e);
-            }
-            sm.qp[idx] = val * scale;
+        // exact slots: the query rows as they are, scaled
+        float v8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float val;
+            if constexpr (F32) val = __uint_as_float(qr[0][e >> 2][e & 3]);
+            else val = (e & 1) ? bf_hi(qr[0][0][e >> 1]) : bf_lo(qr[0][0][e >> 1]);
+            v8[e] = q_ok ? val * scale : 0.f;
         }
+        u32x4 hh, ll;
+        split8(v8, hh, ll);
+        sm.qf[(qs_ * 2 + qpart) * 64 + lane] = qpart ? ll : hh;
     }
-    __syncthreads();
-    // ---- 1d. local offsets (exclusive scan of the stored ranks inside each chunk)
+    // ---- 1d. tile bases: element offset of every 16-token tile inside the head stream
     for (int cc = wave; cc < ncl; cc += DC_WAVES) {
-        uint32_t r[4], loc = 0;
-        const int T = sm.cT[cc];
+        const int c = c_lo + cc;
+        const int64_t t0 = (int64_t)c * CHUNK;
+        const int T = (int)((p.N - t0) < CHUNK ? (p.N - t0) : CHUNK);
+        const uint32_t cbase = sm.cb[cc];
+        uint32_t loc = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            r[e] = 4 * lane + e < T ? sm.sr[cc * CHUNK + 4 * lane + e] : 0;
-            loc += r[e];
+            const int i = 4 * lane + e;
+            uint32_t r = i < T ? sm.sr[cc * CHUNK + i] : 0u;
+            if (i >= T) sm.sr[cc * CHUNK + i] = 0;
+            loc += r;
         }
         uint32_t xs = loc;
 #pragma unroll
@@ -237,150 +271,228 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
             uint32_t y = __shfl_up(xs, off, 64);
             if (lane >= off) xs += y;
         }
-        uint32_t pre = xs - loc;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) { sm.so[cc * CHUNK + 4 * lane + e] = (uint16_t)pre; pre += r[e]; }
-    }
-    // ---- 2. score-operand fragments (shared by all waves): lane -> query row col, K group grp
-    {
-        const int s = tid >> 7, part = (tid >> 6) & 1;   // 512 threads <-> 4 steps x {hi, lo} x 64 lanes
-        float v8[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v8[e] = sm.qp[col * D + 32 * s + 8 * grp + e];
-        u32x4 h, l;
-        split8(v8, h, l);
-        sm.qf[(s * 2 + part) * 64 + lane] = part ? l : h;
+        if ((lane & 3) == 0) sm.tb[cc * DC_TB + (lane >> 2)] = cbase + xs - loc;
+        if (lane == 63) { sm.tb[cc * DC_TB + 16] = cbase + xs; sm.cT[cc] = T; }
     }
     __syncthreads();
 
     const int t_first = exact ? 0 : tau0;
     const int t_end = exact ? (int)((S.n_exact + 15) / 16) : tau1;
-    const ET* kbase_all = reinterpret_cast<const ET*>(exact ? S.k_exact : S.coef_k);
-    const ET* vbase_all = reinterpret_cast<const ET*>(exact ? S.v_exact : S.coef_v);
+    const int nexact = (int)S.n_exact;
+    const uint8_t* kg = reinterpret_cast<const uint8_t*>(exact ? S.k_exact : S.coef_k) +
+                        (exact ? (int64_t)g * p.cap * D : (int64_t)g * p.coef_stride) * (int64_t)sizeof(ET);
+    const uint8_t* vg = reinterpret_cast<const uint8_t*>(exact ? S.v_exact : S.coef_v) +
+                        (exact ? (int64_t)g * p.cap * D : (int64_t)g * p.coef_stride) * (int64_t)sizeof(ET);
+    // element offsets (in the head stream, or the head's exact rows) of tile tau's first
+    // token and of the end of its last token
+    auto toff = [&](int tau) -> int {
+        if (exact) return tau * 16 * D;
+        return (int)sm.tb[((tau >> 4) - c_lo) * DC_TB + (tau & 15)];
+    };
+    auto tend = [&](int tau) -> int {
+        if (exact) return min(16 * tau + 16, nexact) * D;
+        return (int)sm.tb[((tau >> 4) - c_lo) * DC_TB + (tau & 15) + 1];
+    };
+
     float m_run = -INFINITY, l_part = 0.f;
     f32x4 acc[8];
 #pragma unroll
     for (int b = 0; b < 8; ++b) acc[b] = f32x4{0, 0, 0, 0};
 
-    for (int tile = t_first + wave; tile < t_end; tile += DC_WAVES) {
-        int cc = 0, i0, T, rmax;
-        int64_t base;
-        if (exact) {
-            i0 = tile * 16;
-            T = (int)S.n_exact;
-            rmax = D;
-            base = (int64_t)g * p.cap * D;
-        } else {
-            cc = (tile >> 4) - c_lo;
-            i0 = (tile & 15) * 16;
-            T = sm.cT[cc];
-            rmax = sm.sr[cc * CHUNK + i0];
-            base = (int64_t)g * p.coef_stride + sm.cb[cc];
+    // ---- 2a. round plan (wave-uniform): tiles [ta, tbnd) whose span fits the stage
+    int ta = t_first, tbnd = t_first, s0 = 0, nu = 0;
+    auto plan = [&]() {
+        tbnd = ta;
+        s0 = 0;
+        nu = 0;
+        if (ta < t_end) {
+            s0 = __builtin_amdgcn_readfirstlane(toff(ta) & ~(EPU - 1));
+            for (;;) {
+                const int cand = tbnd + lane;
+                const bool fit = cand < t_end && tend(cand) - s0 <= SE;
+                const uint64_t m = __ballot(fit);
+                const int cnt = m == ~0ull ? 64 : __builtin_ctzll(~m);
+                tbnd += cnt;
+                if (cnt < 64) break;
+            }
+            nu = __builtin_amdgcn_readfirstlane((tend(tbnd - 1) - s0 + EPU - 1) / EPU);
         }
-        const ET* Kb = kbase_all + base;
-        const ET* Vb = vbase_all + base;
-        const int ks = (rmax + 31) >> 5, nb = (rmax + 15) >> 4;
-        // token metadata: rank and offset of stored slot i (0 rank past the chunk's end)
-        auto meta = [&](int i, int& r, int& o) {
-            if (i >= T) { r = 0; o = 0; return; }
-            if (exact) { r = D; o = i * D; }
-            else { r = sm.sr[cc * CHUNK + i]; o = sm.so[cc * CHUNK + i]; }
-        };
-        // score operand: row = token i0 + col, coefficients 32 s + 8 grp .. + 7
-        int rk, ok_;
-        meta(i0 + col, rk, ok_);
-        u32x4 kh[4], kl[4];
+    };
+    // ---- 2b. the round's units go straight to LDS: one load moves 64 lanes x 16 bytes to
+    //          a contiguous 1 KB block of the stage; wave w moves blocks w, w + 8, ..
+    auto issue = [&]() {
+        const uint8_t* kr = kg + (size_t)s0 * sizeof(ET);     // wave-uniform round bases
+        const uint8_t* vr = vg + (size_t)s0 * sizeof(ET);
+        const int wv = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            if (s < ks) {
-                const int c0 = 32 * s + 8 * grp;
-                int nv = rk - c0;
-                nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
-                load_row8<F32>(Kb + ok_ + c0, nv, kh[s], kl[s]);
-            } else {
-                kh[s] = kl[s] = u32x4{0, 0, 0, 0};
+        for (int k = 0; k < DC_STAGE_BYTES / 1024 / DC_WAVES; ++k) {
+            const int m = wv + DC_WAVES * k;
+            const uint32_t u = (uint32_t)(64 * m + lane);
+            if (64 * m < nu) {
+                if ((int)u < nu) {
+                    __builtin_amdgcn_global_load_lds(kr + 16u * u, (lds_void*)(sm.stK + 1024 * m), 16, 0, 0);
+                    __builtin_amdgcn_global_load_lds(vr + 16u * u, (lds_void*)(sm.stV + 1024 * m), 16, 0, 0);
+                }
             }
         }
-        // value operand: column j = 16 b + col, tokens i0 + 4 grp + e
-        int vr_[4], vo_[4];
+    };
+    plan();
+    issue();
+    for (;;) {
+        __builtin_amdgcn_s_waitcnt(0);   // this wave's direct-to-LDS loads have landed
+        __syncthreads();
+
+        // ---- 3. tiles of the round, from LDS
+        const uint32_t* sK32 = reinterpret_cast<const uint32_t*>(sm.stK);
+        const ET* sK = reinterpret_cast<const ET*>(sm.stK);
+        const ET* sV = reinterpret_cast<const ET*>(sm.stV);
+        for (int tile = ta + wave; tile < tbnd; tile += DC_WAVES) {
+            int T, i0, rmax, rk, ok_;
+            int vr_[4], vo_[4];
+            const int base = toff(tile) - s0;
+            if (exact) {
+                i0 = tile * 16;
+                T = nexact;
+                rmax = D;
+                rk = i0 + col < T ? D : 0;
+                ok_ = base + col * D;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) meta(i0 + 4 * grp + e, vr_[e], vo_[e]);
-        u32x2 vh[8], vl[8];
-#pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            if (b < nb) {
-                const int j = 16 * b + col;
-                if constexpr (F32) {
-                    float f4[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) f4[e] = j < vr_[e] ? Vb[vo_[e] + j] : 0.f;
-                    split4(f4, vh[b], vl[b]);
-                } else {
-                    uint32_t h[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) h[e] = j < vr_[e] ? (uint32_t)Vb[vo_[e] + j] : 0u;
-                    vh[b] = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
-                    vl[b] = u32x2{0, 0};
+                for (int e = 0; e < 4; ++e) {
+                    vr_[e] = i0 + 4 * grp + e < T ? D : 0;
+                    vo_[e] = base + (4 * grp + e) * D;
                 }
             } else {
+                const int cc = (tile >> 4) - c_lo;
+                i0 = (tile & 15) * 16;
+                T = sm.cT[cc];
+                const uint8_t* srow = sm.sr + cc * CHUNK + i0;     // ranks are 0 past T
+                rmax = srow[0];
+                rk = srow[col];
+                // offsets of the tile's tokens: exclusive scan of the ranks over 16 lanes
+                int incl = rk;
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) {
+                    const int y = __shfl_up(incl, off, 16);
+                    if (col >= off) incl += y;
+                }
+                ok_ = base + incl - rk;
+                const uint32_t r4 = *reinterpret_cast<const uint32_t*>(srow + 4 * grp);
+                int o = __shfl(ok_, 4 * grp, 16);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    vr_[e] = (int)((r4 >> (8 * e)) & 0xFFu);
+                    vo_[e] = o;
+                    o += vr_[e];
+                }
+            }
+            const int ks = (rmax + 31) >> 5, nb = (rmax + 15) >> 4;
+            // score operand: row = token i0 + col, coefficients 32 s + 8 grp .. + 7
+            u32x4 kh[4], kl[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                kh[s] = kl[s] = u32x4{0, 0, 0, 0};
+                if (s < ks) {
+                    const int c0 = 32 * s + 8 * grp;
+                    int nv = rk - c0;
+                    nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
+                    const int a = nv > 0 ? ok_ + c0 : 0;
+                    if constexpr (!F32) {
+                        kh[s] = keep_first(lds_row8_bf16(sK32, a), nv);
+                    } else {
+                        float x8[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) { const float t = sK[a + e]; x8[e] = e < nv ? t : 0.f; }
+                        split8(x8, kh[s], kl[s]);
+                    }
+                }
+            }
+            // value operand: column j = 16 b + col, tokens i0 + 4 grp + e
+            u32x2 vh[8], vl[8];
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
                 vh[b] = vl[b] = u32x2{0, 0};
-            }
-        }
-        // scores: C lane -> query row col, tokens i0 + 4 grp + v
-        f32x4 sc = {0, 0, 0, 0};
+                if (b < nb) {
+                    const int j = 16 * b + col;
+                    if constexpr (F32) {
+                        float f4[4];
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            if (s < ks) {
-                const u32x4 qh = sm.qf[(s * 2) * 64 + lane], ql = sm.qf[(s * 2 + 1) * 64 + lane];
-                sc = mfma(kh[s], qh, sc);
-                sc = mfma(kh[s], ql, sc);
-                if constexpr (F32) sc = mfma(kl[s], qh, sc);
-            }
-        }
-        float sv[4];
-        float tmax = -INFINITY;
+                        for (int e = 0; e < 4; ++e) {
+                            const float t = sV[j < vr_[e] ? vo_[e] + j : 0];
+                            f4[e] = j < vr_[e] ? t : 0.f;
+                        }
+                        split4(f4, vh[b], vl[b]);
+                    } else {
+                        uint32_t h[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            sv[v] = i0 + 4 * grp + v < T ? sc[v] : -INFINITY;
-            tmax = fmaxf(tmax, sv[v]);
-        }
-        tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
-        tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
-        const float m_new = fmaxf(m_run, tmax);
-        if (__ballot(m_new > m_run)) {
-            const float alpha = m_new > m_run ? fast_exp(m_run - m_new) : 1.f;
-            l_part *= alpha;
+                        for (int e = 0; e < 4; ++e) {
+                            const uint32_t t = sV[j < vr_[e] ? vo_[e] + j : 0];
+                            h[e] = j < vr_[e] ? t : 0u;
+                        }
+                        vh[b] = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+                    }
+                }
+            }
+            // scores: C lane -> query row col, tokens i0 + 4 grp + v
+            f32x4 sc = {0, 0, 0, 0};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                if (s < ks) {
+                    const u32x4 qh = sm.qf[(s * 2) * 64 + lane], ql = sm.qf[(s * 2 + 1) * 64 + lane];
+                    sc = mfma(kh[s], qh, sc);
+                    sc = mfma(kh[s], ql, sc);
+                    if constexpr (F32) sc = mfma(kl[s], qh, sc);
+                }
+            }
+            float sv[4];
+            float tmax = -INFINITY;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const float av = __shfl(alpha, 4 * grp + v, 64);
-#pragma unroll
-                for (int b = 0; b < 8; ++b) acc[b][v] *= av;
+                sv[v] = i0 + 4 * grp + v < T ? sc[v] : -INFINITY;
+                tmax = fmaxf(tmax, sv[v]);
             }
-            m_run = m_new;
-        }
-        float pv[4];
+            tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
+            tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
+            const float m_new = fmaxf(m_run, tmax);
+            if (__ballot(m_new > m_run)) {
+                const float alpha = m_new > m_run ? fast_exp(m_run - m_new) : 1.f;
+                l_part *= alpha;
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            pv[v] = m_run == -INFINITY ? 0.f : fast_exp(sv[v] - m_run);
-            l_part += pv[v];
-        }
-        u32x2 ph, pl;
-        split4(pv, ph, pl);
+                for (int v = 0; v < 4; ++v) {
+                    const float av = __shfl(alpha, 4 * grp + v, 64);
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            if (b < nb) {
-                acc[b] = mfma16(ph, vh[b], acc[b]);
-                acc[b] = mfma16(pl, vh[b], acc[b]);
-                if constexpr (F32) acc[b] = mfma16(ph, vl[b], acc[b]);
+                    for (int b = 0; b < 8; ++b) acc[b][v] *= av;
+                }
+                m_run = m_new;
+            }
+            float pv[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                pv[v] = m_run == -INFINITY ? 0.f : fast_exp(sv[v] - m_run);
+                l_part += pv[v];
+            }
+            u32x2 ph, pl;
+            split4(pv, ph, pl);
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                if (b < nb) {
+                    acc[b] = mfma16(ph, vh[b], acc[b]);
+                    acc[b] = mfma16(pl, vh[b], acc[b]);
+                    if constexpr (F32) acc[b] = mfma16(ph, vl[b], acc[b]);
+                }
             }
         }
+        ta = tbnd;
+        if (ta >= t_end) break;
+        plan();
+        __syncthreads();   // every wave is done with the stage
+        issue();
     }
 
-    // ---- 3. combine the waves of this workgroup (fixed order)
+    // ---- 4. combine the waves of this workgroup (fixed order)
     float lsum = l_part + shfl_xor_f(l_part, 16);
     lsum += shfl_xor_f(lsum, 32);
     if (lane < 16) { sm.cm[wave * 16 + col] = m_run; sm.cl[wave * 16 + col] = lsum; }
-    __syncthreads();
+    __syncthreads();   // also: every wave is done reading the stage, which comb reuses
     if (tid < 16) {
         float M = -INFINITY;
         for (int w = 0; w < DC_WAVES; ++w) M = fmaxf(M, sm.cm[w * 16 + tid]);
@@ -440,16 +552,17 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         }
         if (tid < 16) { rec[tid] = sm.mrow[tid]; rec[16 + tid] = sm.lrow[tid]; }
     }
-
 }
 
 
 // ----------------------------------------------------------------------------------------
 // Merge of the partial records of one (sequence, KV head, row tile): log-sum-exp over the
-// records (record 0 = exact slots, original space; records 1.. = coded chunk groups, rank
+// records (record 0 = exact slots, original space; records 1.. = coded tile ranges, rank
 // space), back-rotation of the rank-space sum with P_V^T by MFMA, division by the softmax
 // denominator.  A separate launch: the kernel boundary publishes every record, so no
-// workgroup of the streaming kernel needs a device-wide fence.
+// workgroup of the streaming kernel needs a device-wide fence.  Every load (basis
+// columns, record maxima and sums, the first batch of record rows) is issued before the
+// first wait.
 struct MergeParams {
     const float* part;
     const float* PV;
@@ -457,6 +570,8 @@ struct MergeParams {
     int64_t out_seq_stride; // elements per sequence
     int G, H, hpg, nqt, rows_total, n_wg;
 };
+
+constexpr int MG_BATCH = 16;   // record rows per thread in flight
 
 template <bool F32>
 __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p) {
@@ -466,6 +581,7 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
     __shared__ __attribute__((aligned(16))) float lanes[DC_THREADS * 4];
     __shared__ __attribute__((aligned(16))) float accR[16 * D];
     __shared__ __attribute__((aligned(16))) float accE[16 * D];
+    __shared__ float red[2][DC_WAVES][16];
     __shared__ float mrow[16], lrow[16];
     const int unit = blockIdx.x;
     const int units = p.G * p.nqt;
@@ -477,50 +593,90 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
     const int grp = lane >> 4, col = lane & 15;
     const int nrec = p.n_wg + 1;
     const float* recs = p.part + (int64_t)unit * nrec * DC_REC;
+    const int E = nr4 * D / 4;                  // float4s per record
+    const int KL = DC_THREADS / E;              // record lanes
+    const int e4 = tid % E, k4 = tid / E;
+    const int row4 = (e4 * 4) / D;
 
-    // per-record maxima and sums
+    // ---- 1. issue: record maxima / sums, the first batch of coded record rows, basis columns
     for (int idx = tid; idx < nrec * 16; idx += DC_THREADS) {
         const int r = idx >> 4, row = idx & 15;
         wm[idx] = recs[(int64_t)r * DC_REC + row];
         wl[idx] = recs[(int64_t)r * DC_REC + 16 + row];
     }
+    f32x4 a[MG_BATCH];
+#pragma unroll
+    for (int u = 0; u < MG_BATCH; ++u) {
+        const int r = 1 + k4 + u * KL;
+        a[u] = k4 < KL && r < nrec ? reinterpret_cast<const f32x4*>(recs + (int64_t)r * DC_REC + 32)[e4]
+                                   : f32x4{0, 0, 0, 0};
+    }
+    const float* PV = p.PV + (int64_t)g * D * D;
+    float pb[4][8];
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pb[s][i] = PV[(32 * s + 8 * grp + i) * D + 16 * wave + col];
+    const f32x4 ex = tid < E ? reinterpret_cast<const f32x4*>(recs + 32)[tid] : f32x4{0, 0, 0, 0};
+    __syncthreads();
+
+    // ---- 2. row maxima, record weights, row sums (32 threads per row)
+    {
+        const int row = tid & 15, part = tid >> 4;
+        float mx = -INFINITY;
+        for (int r = part; r < nrec; r += 32) mx = fmaxf(mx, wm[r * 16 + row]);
+        mx = fmaxf(mx, shfl_xor_f(mx, 16));
+        mx = fmaxf(mx, shfl_xor_f(mx, 32));
+        if (lane < 16) red[0][wave][row] = mx;
+    }
     __syncthreads();
     if (tid < 16) {
         float M = -INFINITY;
-        for (int r = 0; r < nrec; ++r) M = fmaxf(M, wm[r * 16 + tid]);
+        for (int w = 0; w < DC_WAVES; ++w) M = fmaxf(M, red[0][w][tid]);
         mrow[tid] = M;
     }
     __syncthreads();
-    for (int idx = tid; idx < nrec * 16; idx += DC_THREADS) {
-        const float m = wm[idx];
-        wm[idx] = m == -INFINITY ? 0.f : fast_exp(m - mrow[idx & 15]);
+    {
+        const int row = tid & 15, part = tid >> 4;
+        const float M = mrow[row];
+        float ls = 0.f;
+        for (int r = part; r < nrec; r += 32) {
+            const float m = wm[r * 16 + row];
+            const float wgt = m == -INFINITY ? 0.f : fast_exp(m - M);
+            wm[r * 16 + row] = wgt;
+            ls += wgt * wl[r * 16 + row];
+        }
+        ls += shfl_xor_f(ls, 16);
+        ls += shfl_xor_f(ls, 32);
+        if (lane < 16) red[1][wave][row] = ls;
     }
     __syncthreads();
     if (tid < 16) {
         float L = 0.f;
-        for (int r = 0; r < nrec; ++r) L += wm[r * 16 + tid] * wl[r * 16 + tid];
+        for (int w = 0; w < DC_WAVES; ++w) L += red[1][w][tid];
         lrow[tid] = L;
     }
-    // weighted sum of the coded records: thread -> (float4 e, record lane k)
-    const int E = nr4 * D / 4;                  // float4s per record
-    const int KL = DC_THREADS / E;              // record lanes
+    // ---- 3. weighted sum of the coded records: thread -> (float4 e4, record lane k4)
     {
-        const int e = tid % E, k = tid / E;
-        const int row = (e * 4) / D;
         f32x4 s4 = {0, 0, 0, 0};
-        if (k < KL) {
-            for (int r0 = 1 + k; r0 < nrec; r0 += 8 * KL) {
-                f32x4 a[8];
+        if (k4 < KL) {
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {      // eight independent loads in flight
+            for (int u = 0; u < MG_BATCH; ++u) {
+                const int r = 1 + k4 + u * KL;
+                s4 += (r < nrec ? wm[r * 16 + row4] : 0.f) * a[u];
+            }
+            for (int r0 = 1 + k4 + MG_BATCH * KL; r0 < nrec; r0 += 8 * KL) {
+                f32x4 b8[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
                     const int r = r0 + u * KL;
-                    a[u] = r < nrec ? reinterpret_cast<const f32x4*>(recs + (int64_t)r * DC_REC + 32)[e]
-                                    : f32x4{0, 0, 0, 0};
+                    b8[u] = r < nrec ? reinterpret_cast<const f32x4*>(recs + (int64_t)r * DC_REC + 32)[e4]
+                                     : f32x4{0, 0, 0, 0};
                 }
 #pragma unroll
                 for (int u = 0; u < 8; ++u) {
                     const int r = r0 + u * KL;
-                    s4 += (r < nrec ? wm[r * 16 + row] : 0.f) * a[u];
+                    s4 += (r < nrec ? wm[r * 16 + row4] : 0.f) * b8[u];
                 }
             }
         }
@@ -531,18 +687,11 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
         f32x4 t = reinterpret_cast<const f32x4*>(lanes)[tid];
         for (int kk = 1; kk < KL; ++kk) t += reinterpret_cast<const f32x4*>(lanes)[kk * E + tid];
         reinterpret_cast<f32x4*>(accR)[tid] = t;
-        const f32x4 ex = reinterpret_cast<const f32x4*>(recs + 32)[tid];
         reinterpret_cast<f32x4*>(accE)[tid] = wm[(tid * 4) / D] * ex;
     }
     __syncthreads();
-    // back-rotation by MFMA: C[row][c] = sum_j accR[row][j] P_V[j][c]
+    // ---- 4. back-rotation by MFMA: C[row][c] = sum_j accR[row][j] P_V[j][c]
     // wave -> column block 16 wave.., lane -> column col, K group grp
-    const float* PV = p.PV + (int64_t)g * D * D;
-    float pb[4][8];
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pb[s][i] = PV[(32 * s + 8 * grp + i) * D + 16 * wave + col];
     f32x4 o = {0, 0, 0, 0};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
@@ -638,8 +787,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     float* part = (float*)ws;
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
-    const int nr4 = rows_total >= 16 ? 16 : ((rows_total + 3) & ~3);
-    const size_t lds = decode_smem_bytes(nr4, pl.cpw);
+    const size_t lds = decode_smem_bytes(pl.cpw);
     hipError_t e = sh.dtype == VARRATE_BF16 ? set_smem_attr<false>(lds) : set_smem_attr<true>(lds);
     if (e != hipSuccess) return e;
     for (int s0 = 0; s0 < S; s0 += DC_SEQ) {
