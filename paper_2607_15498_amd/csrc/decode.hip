@@ -60,7 +60,7 @@ struct DecParams {
     const float* PV;
     float* part;
     int64_t N, coef_stride, cap;
-    int G, H, hpg, nqt, rows_total, n_chunks, cpw, n_wg, tpw, total_tiles;
+    int G, H, hpg, nqt, rows_total, n_chunks, cpw, n_wg, tpw, total_tiles, units;
 };
 
 template <bool F32> struct Elem;
@@ -69,20 +69,20 @@ template <> struct Elem<true> { typedef float T; };
 
 // 4 fp32 -> bf16x4 (hi, lo)
 __device__ __forceinline__ void split4(const float* x, u32x2& hi, u32x2& lo) {
-    uint32_t h[4], l[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) split_bf16(x[e], h[e], l[e]);
-    hi = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
-    lo = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
+    uint32_t h0, l0, h1, l1;
+    split2(x[0], x[1], h0, l0);
+    split2(x[2], x[3], h1, l1);
+    hi = u32x2{h0, h1};
+    lo = u32x2{l0, l1};
 }
 
 // Staging: each round copies a contiguous coefficient range of both streams (K and V share
-// one layout) into LDS with one 16-byte load per unit, every unit of the round in flight
+// one layout) into LDS with direct-to-LDS 16-byte loads, every unit of the round in flight
 // at once; the waves then run their tiles from LDS.
-constexpr int DC_STAGE_BYTES = 32768;                         // per stream and round
-constexpr int DC_UNITS = 2 * DC_STAGE_BYTES / 16 / DC_THREADS; // 16-byte units per thread
+constexpr int DC_STAGE_BYTES = 30720;                         // per stream and round
 constexpr int DC_STAGE_PAD = 64;                              // over-read slack of row gathers
-constexpr int DC_TB = 17;                                     // tile bases per chunk (16 + end)
+constexpr int DC_SO = 264;                                    // offsets per chunk: 257, padded
+constexpr int DC_CROW = D + 4;                                // comb row stride (floats)
 
 struct DecSmem {
     uint8_t* stK;     // [DC_STAGE_BYTES + pad] staged K coefficients of the round; after the
@@ -95,11 +95,10 @@ struct DecSmem {
     float* lrow;      // [16]
     int* cT;          // [DC_MAX_CPW] valid tokens per chunk
     uint32_t* cb;     // [DC_MAX_CPW] chunk bases (chunk_off)
-    uint32_t* tb;     // [cpw][17] element offset of each 16-token tile start (+ chunk end)
-    uint8_t* sr;      // [cpw][256] stored ranks (0 past the chunk's end)
+    uint16_t* so;     // [cpw][DC_SO] offset of stored slot i inside its chunk, i = 0..256
 };
 
-__device__ __forceinline__ DecSmem carve(uint8_t* smem, int cpw) {
+__device__ __forceinline__ DecSmem carve(uint8_t* smem) {
     DecSmem s;
     uint8_t* b = smem;
     s.stK = b; b += DC_STAGE_BYTES + DC_STAGE_PAD;
@@ -113,16 +112,13 @@ __device__ __forceinline__ DecSmem carve(uint8_t* smem, int cpw) {
     s.lrow = f; f += 16;
     s.cT = reinterpret_cast<int*>(f); f += DC_MAX_CPW;
     s.cb = reinterpret_cast<uint32_t*>(f); f += DC_MAX_CPW;
-    s.tb = reinterpret_cast<uint32_t*>(f);
-    uint8_t* e = reinterpret_cast<uint8_t*>(s.tb + ((cpw * DC_TB + 3) & ~3));
-    s.sr = e;                                               // 16-byte aligned
+    s.so = reinterpret_cast<uint16_t*>(f);                  // 16-byte aligned
     return s;
 }
 
 static inline size_t decode_smem_bytes(int cpw) {
     return 2 * (size_t)(DC_STAGE_BYTES + DC_STAGE_PAD) + 4 * 2 * 64 * 16 +
-           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW) * 4 + (size_t)((cpw * DC_TB + 3) & ~3) * 4 +
-           (size_t)cpw * CHUNK;
+           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW) * 4 + (size_t)cpw * DC_SO * 2;
 }
 
 // 8 consecutive bf16 at element index a of an LDS array (any 2-byte alignment): five dword
@@ -135,34 +131,180 @@ __device__ __forceinline__ u32x4 lds_row8_bf16(const uint32_t* w, int a) {
                  __builtin_amdgcn_alignbit(d3, d2, sh), __builtin_amdgcn_alignbit(d4, d3, sh)};
 }
 
+// Inclusive prefix sum over the 16 lanes of each DPP row (lanes 16 r .. 16 r + 15).
+__device__ __forceinline__ uint32_t row_scan16(uint32_t x) {
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);   // row_shr:1
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);   // row_shr:2
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);   // row_shr:4
+    x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);   // row_shr:8
+    return x;
+}
+
+// Lane index, recomputed where it is used (two mbcnt ALU ops).  Volatile asm keeps the
+// compiler from merging the instances into one value that would stay live (and be spilled)
+// across the tile loop.
+__device__ __forceinline__ int lane_now() {
+    int l;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+    return l;
+}
+
+// Per-lane view of one 16-token tile in the stage: the lane's score row (token i0 + col:
+// rank rk, stage offset ok) and its four value tokens (i0 + 4 grp + e: ranks vr, offsets vo).
+struct TileMeta {
+    int i0, T, rk, ok;
+    int vr[4], vo[4];
+};
+
+// One tile.  Scores S[token][row] by 16x16x32 MFMA over KS steps of 32 coefficients (A =
+// the tile's key rows, B = the query fragments); the C fragment (lane = query row, tokens
+// 4 grp + v) is the B operand of the value product O^T[j][row] += V^T[j][token] P^T[token][row]
+// (16x16x16 MFMA over NB blocks of 16 rank coordinates), so each lane owns one query row
+// and the online-softmax rescale is lane-local.  KS and NB bound the tile's largest rank,
+// so every LDS read is unconditional (masked by value) and they all issue before the first
+// wait.
+template <bool F32, int KS, int NB>
+__device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, const typename Elem<F32>::T* sK,
+                                          const typename Elem<F32>::T* sV, const u32x4* qf, int lane,
+                                          int grp, float& m_run, float& l_part, f32x4 (&acc)[8]) {
+    const int col = lane & 15;
+    // Row gathers may read up to 127 elements past the stage's valid range (into the pad
+    // and the LDS arrays after it); everything past a token's rank is masked by value.
+    // value operand gather (A of the value product: lane -> rank coordinate 16 b + col,
+    // tokens 4 grp + e)
+    u32x2 vh[NB], vl[NB];
+    auto gather_v = [&]() {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int j = 16 * b + col;
+            if constexpr (F32) {
+                float f4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float t = sV[tm.vo[e] + j];
+                    f4[e] = j < tm.vr[e] ? t : 0.f;
+                }
+                split4(f4, vh[b], vl[b]);
+            } else {
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t t = sV[tm.vo[e] + j];
+                    h[e] = j < tm.vr[e] ? t : 0u;
+                }
+                vh[b] = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+                vl[b] = u32x2{0, 0};
+            }
+        }
+    };
+    // small tiles: every read issues up front; full-rank tiles: the value reads wait until
+    // the scores are done, to keep the register footprint inside two workgroups per CU
+    if constexpr (KS < 4) gather_v();
+    // scores: A = the tile's key rows (lane -> token i0 + col, coefficients 32 s + 8 grp ..),
+    // B = the query fragments; full-rank tiles run in two halves to bound live registers
+    f32x4 sc = {0, 0, 0, 0};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        if (KS >= 4 && s == 2) __builtin_amdgcn_sched_barrier(0);
+        const int c0 = 32 * s + 8 * grp;
+        int nv = tm.rk - c0;
+        nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
+        const int a = tm.ok + c0;
+        u32x4 kh, kl;
+        if constexpr (!F32) {
+            kh = keep_first(lds_row8_bf16(reinterpret_cast<const uint32_t*>(sK), a), nv);
+            kl = u32x4{0, 0, 0, 0};
+        } else {
+            float x8[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) { const float t = sK[a + e]; x8[e] = e < nv ? t : 0.f; }
+            split8(x8, kh, kl);
+        }
+        const u32x4 qh = qf[(s * 2) * 64 + lane], ql = qf[(s * 2 + 1) * 64 + lane];
+        sc = mfma(kh, qh, sc);
+        sc = mfma(kh, ql, sc);
+        if constexpr (F32) sc = mfma(kl, qh, sc);
+    }
+    if constexpr (KS >= 4) {
+        __builtin_amdgcn_sched_barrier(0);
+        gather_v();
+    }
+    float sv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sv[v] = sc[v];
+    if (partial) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sv[v] = tm.i0 + 4 * grp + v < tm.T ? sv[v] : -INFINITY;
+    }
+    float tmax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    tmax = xmax32(xmax16(tmax));
+    // Lazy reference: exponents are taken against m_run, which moves only when a score
+    // exceeds it by more than 8 (so every p stays below e^8); sums and accumulators always
+    // share the reference, so the result is the same softmax.
+    if (tmax > m_run + 8.f) {                // lane-local: this lane's query row
+        const float alpha = fast_exp(m_run - tmax);
+        l_part *= alpha;
+#pragma unroll
+        for (int b = 0; b < 8; ++b) acc[b] *= alpha;
+        m_run = tmax;
+    }
+    float pv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        pv[v] = fast_exp(sv[v] - m_run);      // exp(-inf) = 0 for masked tokens
+        l_part += pv[v];
+    }
+    if constexpr (F32) {
+        u32x2 ph, pl;
+        split4(pv, ph, pl);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            acc[b] = mfma16(vh[b], ph, acc[b]);
+            acc[b] = mfma16(vh[b], pl, acc[b]);
+            acc[b] = mfma16(vl[b], ph, acc[b]);
+        }
+    } else {
+        // bf16 storage: one bf16 rounding of p (relative 2^-9, far inside the output bound)
+        const u32x2 ph = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
+#pragma unroll
+        for (int b = 0; b < NB; ++b) acc[b] = mfma16(vh[b], ph, acc[b]);
+    }
+}
+
 template <bool F32>
 __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecParams p) {
     typedef typename Elem<F32>::T ET;
     constexpr int EPU = 16 / (int)sizeof(ET);               // elements per 16-byte unit
     constexpr int SE = DC_STAGE_BYTES / (int)sizeof(ET);     // staged elements per stream
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    const int x = blockIdx.x, gq = blockIdx.y, sq = blockIdx.z;
+    // Workgroup -> (unit, x): consecutive workgroups take consecutive units, so the
+    // workgroups of one unit (one KV head) land on the same XCD of the round-robin
+    // dispatch and share its L2 copy of the key basis.  x = 0 (dispatched first) is the
+    // exact-slot workgroup; x >= 1 take the coded tile ranges.
+    const int U = p.units;
+    const int L = blockIdx.x;
+    const int unit = L % U, x = L / U;
+    const int sq = unit / (p.G * p.nqt), gq = unit % (p.G * p.nqt);
     const int g = gq / p.nqt, qt = gq % p.nqt;
     const DecSeq& S = p.seq[sq];
     const int rows = min(16, p.rows_total - 16 * qt);
     const int nr4 = (rows + 3) & ~3;
-    const bool exact = x == 0;          // dispatched first; the coded groups follow
-    const int xc = x - 1;               // coded tile range
-    const int cpw = p.cpw;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int grp = lane >> 4, col = lane & 15;
-    DecSmem sm = carve(smem, cpw);
+    const bool exact = x == 0;
+    const int xc = x - 1;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));   // scalar
+    int lane = lane_now(), tid = 64 * wave + lane, grp = lane >> 4, col = lane & 15;
+    DecSmem sm = carve(smem);
     const float scale = 0.08838834764831845f;  // 1/sqrt(128)
     const ET* qsrc = reinterpret_cast<const ET*>(S.q);
 
-    // ---- 1a. issue the basis rows and query rows the rotation needs
+    // ---- 1a. issue the basis rows and query rows (raw loads only: nothing here waits, so
+    //          the rank loads below issue right behind them; a missing query row reads
+    //          row 0 of the head and is masked later)
     const float* P = p.PK + (int64_t)g * D * D;
     const int qrow_l = 16 * qt + col;
     const bool q_ok = qrow_l < p.rows_total;
     const int query_l = q_ok ? qrow_l / p.hpg : 0, hh_l = q_ok ? qrow_l % p.hpg : 0;
     const ET* qv = qsrc + ((int64_t)query_l * p.H + g * p.hpg + hh_l) * D;
-    // Raw loads only (row 0 of the head stands in for a missing query row): nothing here may
-    // wait, so that the rank loads below issue right behind them; masking happens after.
     u32x4 pa[4][2];
     u32x4 qr[4][2];
     const int qs_ = tid >> 7, qpart = (tid >> 6) & 1;   // exact: 4 steps x {hi, lo} x 64 lanes
@@ -181,26 +323,21 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         if constexpr (F32) { qr[0][0] = load16(src); qr[0][1] = load16(src + 4); }
         else qr[0][0] = load16_a2(src);
     }
-    // ---- 1b. stored ranks and chunk bases of the chunks this tile range touches
+    // ---- 1b. stored ranks (16 per thread: thread 16 c + k holds tile k of chunk c) and
+    //          chunk bases of the chunks this tile range touches (at most DC_MAX_CPW)
     const int tau0 = exact ? 0 : xc * p.tpw;
     const int tau1 = exact ? 0 : min(tau0 + p.tpw, p.total_tiles);
     const int c_lo = tau0 >> 4;
     const int ncl = exact ? 0 : ((tau1 - 1) >> 4) - c_lo + 1;
-    // (ncl <= DC_MAX_CPW = 16 chunks: at most 256 rank vectors, one per thread)
     u32x4 rv = {0, 0, 0, 0};
     uint32_t cbv = 0;
     const int64_t t_r = (int64_t)c_lo * CHUNK + (int64_t)tid * 16;
-    if (!exact) {
-        if (tid < ncl * (CHUNK / 16) && t_r < p.N) rv = load16(S.srank + t_r);   // srank padded to 64
-        if (tid < ncl) cbv = S.chunk_off[c_lo + tid];
-    }
-    if (!exact) {
-        if (tid < ncl * (CHUNK / 16)) *reinterpret_cast<u32x4*>(sm.sr + tid * 16) = rv;
-        if (tid < ncl) sm.cb[tid] = cbv;
-    }
-    __syncthreads();
+    const bool r_ok = !exact && tid < ncl * (CHUNK / 16);
+    if (r_ok && t_r < p.N) rv = load16(S.srank + t_r);     // srank is padded to a multiple of 64
+    if (!exact && tid < ncl) cbv = S.chunk_off[c_lo + tid];
+
     // ---- 1c. score-operand fragments of the query rows (lane -> query row col, K group
-    //          grp; bf16 hi and lo parts), before any direct-to-LDS load is in flight
+    //          grp; bf16 hi and lo parts)
     uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf);
     if (!exact) {
         // q' = P_K q / sqrt(d) by MFMA; C lane -> query row col, directions 16 wave + 4 grp + v
@@ -238,7 +375,6 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 0) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
         *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 1) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
     } else {
-        // exact slots: the query rows as they are, scaled
         float v8[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -251,47 +387,60 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         split8(v8, hh, ll);
         sm.qf[(qs_ * 2 + qpart) * 64 + lane] = qpart ? ll : hh;
     }
-    // ---- 1d. tile bases: element offset of every 16-token tile inside the head stream
-    for (int cc = wave; cc < ncl; cc += DC_WAVES) {
-        const int c = c_lo + cc;
-        const int64_t t0 = (int64_t)c * CHUNK;
+
+    lane = lane_now(); tid = 64 * wave + lane; grp = lane >> 4; col = lane & 15;
+    // ---- 1d. offsets of the stored slots inside each chunk: local prefix sums of a
+    //          thread's 16 ranks, then a 16-lane scan of the threads of one chunk (one DPP
+    //          row); ranks past the chunk's end count as 0
+    if (r_ok) {
+        const int cc = tid >> 4, k = tid & 15;
+        const int64_t t0 = (int64_t)(c_lo + cc) * CHUNK;
         const int T = (int)((p.N - t0) < CHUNK ? (p.N - t0) : CHUNK);
-        const uint32_t cbase = sm.cb[cc];
-        uint32_t loc = 0;
+        uint32_t r[16];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int i = 4 * lane + e;
-            uint32_t r = i < T ? sm.sr[cc * CHUNK + i] : 0u;
-            if (i >= T) sm.sr[cc * CHUNK + i] = 0;
-            loc += r;
+        for (int e = 0; e < 16; ++e) {
+            const uint32_t b = (rv[e >> 2] >> (8 * (e & 3))) & 0xFFu;
+            r[e] = 16 * k + e < T ? b : 0u;
         }
-        uint32_t xs = loc;
+        uint32_t tot = 0;
 #pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            uint32_t y = __shfl_up(xs, off, 64);
-            if (lane >= off) xs += y;
+        for (int e = 0; e < 16; ++e) tot += r[e];
+        const uint32_t incl = row_scan16(tot);
+        uint32_t o = incl - tot;
+        uint32_t w[8];
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+            const uint32_t o0 = o;
+            o += r[e];
+            w[e >> 1] = o0 | (o << 16);
+            o += r[e + 1];
         }
-        if ((lane & 3) == 0) sm.tb[cc * DC_TB + (lane >> 2)] = cbase + xs - loc;
-        if (lane == 63) { sm.tb[cc * DC_TB + 16] = cbase + xs; sm.cT[cc] = T; }
+        uint16_t* dst = sm.so + cc * DC_SO + 16 * k;
+        *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
+        *reinterpret_cast<u32x4*>(dst + 8) = u32x4{w[4], w[5], w[6], w[7]};
+        if (k == 15) { sm.so[cc * DC_SO + 256] = (uint16_t)incl; sm.cT[cc] = T; }
     }
+    if (!exact && tid < ncl) sm.cb[tid] = cbv;
     __syncthreads();
 
     const int t_first = exact ? 0 : tau0;
     const int t_end = exact ? (int)((S.n_exact + 15) / 16) : tau1;
     const int nexact = (int)S.n_exact;
-    const uint8_t* kg = reinterpret_cast<const uint8_t*>(exact ? S.k_exact : S.coef_k) +
-                        (exact ? (int64_t)g * p.cap * D : (int64_t)g * p.coef_stride) * (int64_t)sizeof(ET);
-    const uint8_t* vg = reinterpret_cast<const uint8_t*>(exact ? S.v_exact : S.coef_v) +
-                        (exact ? (int64_t)g * p.cap * D : (int64_t)g * p.coef_stride) * (int64_t)sizeof(ET);
+    const int64_t hoff = exact ? (int64_t)g * p.cap * D : (int64_t)g * p.coef_stride;
+    const int limit = exact ? (int)(p.cap * D) : (int)p.coef_stride;   // elements in the head's stream
+    const uint8_t* kg = reinterpret_cast<const uint8_t*>(exact ? S.k_exact : S.coef_k) + hoff * (int64_t)sizeof(ET);
+    const uint8_t* vg = reinterpret_cast<const uint8_t*>(exact ? S.v_exact : S.coef_v) + hoff * (int64_t)sizeof(ET);
     // element offsets (in the head stream, or the head's exact rows) of tile tau's first
     // token and of the end of its last token
     auto toff = [&](int tau) -> int {
         if (exact) return tau * 16 * D;
-        return (int)sm.tb[((tau >> 4) - c_lo) * DC_TB + (tau & 15)];
+        const int cc = (tau >> 4) - c_lo;
+        return (int)sm.cb[cc] + sm.so[cc * DC_SO + 16 * (tau & 15)];
     };
     auto tend = [&](int tau) -> int {
         if (exact) return min(16 * tau + 16, nexact) * D;
-        return (int)sm.tb[((tau >> 4) - c_lo) * DC_TB + (tau & 15) + 1];
+        const int cc = (tau >> 4) - c_lo;
+        return (int)sm.cb[cc] + sm.so[cc * DC_SO + 16 * (tau & 15) + 16];
     };
 
     float m_run = -INFINITY, l_part = 0.f;
@@ -299,7 +448,8 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
 #pragma unroll
     for (int b = 0; b < 8; ++b) acc[b] = f32x4{0, 0, 0, 0};
 
-    // ---- 2a. round plan (wave-uniform): tiles [ta, tbnd) whose span fits the stage
+    // ---- 2a. round plan (wave-uniform): tiles [ta, tbnd) whose span fits the stage.  The
+    //          span is clamped to the head's buffer, so no metadata can send a load past it.
     int ta = t_first, tbnd = t_first, s0 = 0, nu = 0;
     auto plan = [&]() {
         tbnd = ta;
@@ -307,15 +457,20 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         nu = 0;
         if (ta < t_end) {
             s0 = __builtin_amdgcn_readfirstlane(toff(ta) & ~(EPU - 1));
+            const int ln = lane_now();
             for (;;) {
-                const int cand = tbnd + lane;
+                const int cand = tbnd + ln;
                 const bool fit = cand < t_end && tend(cand) - s0 <= SE;
                 const uint64_t m = __ballot(fit);
                 const int cnt = m == ~0ull ? 64 : __builtin_ctzll(~m);
                 tbnd += cnt;
                 if (cnt < 64) break;
             }
-            nu = __builtin_amdgcn_readfirstlane((tend(tbnd - 1) - s0 + EPU - 1) / EPU);
+            int n_ = (tend(tbnd - 1) - s0 + EPU - 1) / EPU;
+            const int room = s0 >= 0 && s0 < limit ? (limit - s0) / EPU : 0;
+            n_ = n_ < 0 ? 0 : (n_ > room ? room : n_);
+            n_ = n_ > SE / EPU ? SE / EPU : n_;
+            nu = __builtin_amdgcn_readfirstlane(n_);
         }
     };
     // ---- 2b. the round's units go straight to LDS: one load moves 64 lanes x 16 bytes to
@@ -325,9 +480,9 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         const uint8_t* vr = vg + (size_t)s0 * sizeof(ET);
         const int wv = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
-        for (int k = 0; k < DC_STAGE_BYTES / 1024 / DC_WAVES; ++k) {
+        for (int k = 0; k < (DC_STAGE_BYTES / 1024 + DC_WAVES - 1) / DC_WAVES; ++k) {
             const int m = wv + DC_WAVES * k;
-            const uint32_t u = (uint32_t)(64 * m + lane);
+            const uint32_t u = (uint32_t)(64 * m + lane_now());
             if (64 * m < nu) {
                 if ((int)u < nu) {
                     __builtin_amdgcn_global_load_lds(kr + 16u * u, (lds_void*)(sm.stK + 1024 * m), 16, 0, 0);
@@ -338,148 +493,61 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     };
     plan();
     issue();
+
     for (;;) {
         __builtin_amdgcn_s_waitcnt(0);   // this wave's direct-to-LDS loads have landed
         __syncthreads();
 
         // ---- 3. tiles of the round, from LDS
-        const uint32_t* sK32 = reinterpret_cast<const uint32_t*>(sm.stK);
         const ET* sK = reinterpret_cast<const ET*>(sm.stK);
         const ET* sV = reinterpret_cast<const ET*>(sm.stV);
-        for (int tile = ta + wave; tile < tbnd; tile += DC_WAVES) {
-            int T, i0, rmax, rk, ok_;
-            int vr_[4], vo_[4];
-            const int base = toff(tile) - s0;
+        for (int tile = ta + __builtin_amdgcn_readfirstlane(wave); tile < tbnd; tile += DC_WAVES) {
+            // lane-derived addresses are recomputed per tile (a few ALU ops) rather than
+            // hoisted out of the loop for all four tile shapes and spilled
+            const int ln = lane_now();
+            const int col = ln & 15, grp = ln >> 4;
+            TileMeta tm;
+            const int base = __builtin_amdgcn_readfirstlane(toff(tile) - s0);
+            int rmax;
             if (exact) {
-                i0 = tile * 16;
-                T = nexact;
+                tm.i0 = tile * 16;
+                tm.T = nexact;
                 rmax = D;
-                rk = i0 + col < T ? D : 0;
-                ok_ = base + col * D;
+                tm.rk = tm.i0 + col < tm.T ? D : 0;
+                tm.ok = base + col * D;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    vr_[e] = i0 + 4 * grp + e < T ? D : 0;
-                    vo_[e] = base + (4 * grp + e) * D;
+                    tm.vr[e] = tm.i0 + 4 * grp + e < tm.T ? D : 0;
+                    tm.vo[e] = base + (4 * grp + e) * D;
                 }
             } else {
                 const int cc = (tile >> 4) - c_lo;
-                i0 = (tile & 15) * 16;
-                T = sm.cT[cc];
-                const uint8_t* srow = sm.sr + cc * CHUNK + i0;     // ranks are 0 past T
-                rmax = srow[0];
-                rk = srow[col];
-                // offsets of the tile's tokens: exclusive scan of the ranks over 16 lanes
-                int incl = rk;
+                tm.i0 = (tile & 15) * 16;
+                tm.T = __builtin_amdgcn_readfirstlane(sm.cT[cc]);
+                const uint16_t* so = sm.so + cc * DC_SO + tm.i0;
+                const int o0 = __builtin_amdgcn_readfirstlane((int)so[0]);
+                const int rel = base - o0;                       // stage offset = rel + so[i]
+                rmax = so[1] - o0;
+                const int oc = so[col];
+                tm.rk = so[col + 1] - oc;
+                tm.ok = rel + oc;
+                int ov[5];
 #pragma unroll
-                for (int off = 1; off < 16; off <<= 1) {
-                    const int y = __shfl_up(incl, off, 16);
-                    if (col >= off) incl += y;
-                }
-                ok_ = base + incl - rk;
-                const uint32_t r4 = *reinterpret_cast<const uint32_t*>(srow + 4 * grp);
-                int o = __shfl(ok_, 4 * grp, 16);
+                for (int e = 0; e < 5; ++e) ov[e] = so[4 * grp + e];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    vr_[e] = (int)((r4 >> (8 * e)) & 0xFFu);
-                    vo_[e] = o;
-                    o += vr_[e];
+                    tm.vr[e] = ov[e + 1] - ov[e];
+                    tm.vo[e] = rel + ov[e];
                 }
             }
-            const int ks = (rmax + 31) >> 5, nb = (rmax + 15) >> 4;
-            // score operand: row = token i0 + col, coefficients 32 s + 8 grp .. + 7
-            u32x4 kh[4], kl[4];
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                kh[s] = kl[s] = u32x4{0, 0, 0, 0};
-                if (s < ks) {
-                    const int c0 = 32 * s + 8 * grp;
-                    int nv = rk - c0;
-                    nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
-                    const int a = nv > 0 ? ok_ + c0 : 0;
-                    if constexpr (!F32) {
-                        kh[s] = keep_first(lds_row8_bf16(sK32, a), nv);
-                    } else {
-                        float x8[8];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) { const float t = sK[a + e]; x8[e] = e < nv ? t : 0.f; }
-                        split8(x8, kh[s], kl[s]);
-                    }
-                }
-            }
-            // value operand: column j = 16 b + col, tokens i0 + 4 grp + e
-            u32x2 vh[8], vl[8];
-#pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                vh[b] = vl[b] = u32x2{0, 0};
-                if (b < nb) {
-                    const int j = 16 * b + col;
-                    if constexpr (F32) {
-                        float f4[4];
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const float t = sV[j < vr_[e] ? vo_[e] + j : 0];
-                            f4[e] = j < vr_[e] ? t : 0.f;
-                        }
-                        split4(f4, vh[b], vl[b]);
-                    } else {
-                        uint32_t h[4];
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            const uint32_t t = sV[j < vr_[e] ? vo_[e] + j : 0];
-                            h[e] = j < vr_[e] ? t : 0u;
-                        }
-                        vh[b] = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
-                    }
-                }
-            }
-            // scores: C lane -> query row col, tokens i0 + 4 grp + v
-            f32x4 sc = {0, 0, 0, 0};
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                if (s < ks) {
-                    const u32x4 qh = sm.qf[(s * 2) * 64 + lane], ql = sm.qf[(s * 2 + 1) * 64 + lane];
-                    sc = mfma(kh[s], qh, sc);
-                    sc = mfma(kh[s], ql, sc);
-                    if constexpr (F32) sc = mfma(kl[s], qh, sc);
-                }
-            }
-            float sv[4];
-            float tmax = -INFINITY;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                sv[v] = i0 + 4 * grp + v < T ? sc[v] : -INFINITY;
-                tmax = fmaxf(tmax, sv[v]);
-            }
-            tmax = fmaxf(tmax, shfl_xor_f(tmax, 16));
-            tmax = fmaxf(tmax, shfl_xor_f(tmax, 32));
-            const float m_new = fmaxf(m_run, tmax);
-            if (__ballot(m_new > m_run)) {
-                const float alpha = m_new > m_run ? fast_exp(m_run - m_new) : 1.f;
-                l_part *= alpha;
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const float av = __shfl(alpha, 4 * grp + v, 64);
-#pragma unroll
-                    for (int b = 0; b < 8; ++b) acc[b][v] *= av;
-                }
-                m_run = m_new;
-            }
-            float pv[4];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                pv[v] = m_run == -INFINITY ? 0.f : fast_exp(sv[v] - m_run);
-                l_part += pv[v];
-            }
-            u32x2 ph, pl;
-            split4(pv, ph, pl);
-#pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                if (b < nb) {
-                    acc[b] = mfma16(ph, vh[b], acc[b]);
-                    acc[b] = mfma16(pl, vh[b], acc[b]);
-                    if constexpr (F32) acc[b] = mfma16(ph, vl[b], acc[b]);
-                }
-            }
+            // a tile's first token has its largest rank: 32-coefficient score steps and
+            // 16-wide value blocks it needs, as compile-time bounds (no branches inside)
+            rmax = __builtin_amdgcn_readfirstlane(rmax);
+            const bool partial = __builtin_amdgcn_readfirstlane(tm.i0 + 16 > tm.T ? 1 : 0) != 0;
+            if (rmax <= 16) tile_step<F32, 1, 1>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
+            else if (rmax <= 32) tile_step<F32, 1, 2>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
+            else if (rmax <= 64) tile_step<F32, 2, 4>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
+            else tile_step<F32, 4, 8>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
         }
         ta = tbnd;
         if (ta >= t_end) break;
@@ -488,66 +556,52 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         issue();
     }
 
-    // ---- 4. combine the waves of this workgroup (fixed order)
-    float lsum = l_part + shfl_xor_f(l_part, 16);
-    lsum += shfl_xor_f(lsum, 32);
+    // ---- 4. combine the waves of this workgroup (fixed order).  Lane (col, grp) holds query
+    //          row col: running max m_run, its share of the sum, O[col][16 b + 4 grp + v].
+    //          comb rows are padded to DC_CROW floats, so the 16 rows' stores hit distinct banks.
+    lane = lane_now(); tid = 64 * wave + lane; grp = lane >> 4; col = lane & 15;
+    const float lsum = xsum32(xsum16(l_part));
     if (lane < 16) { sm.cm[wave * 16 + col] = m_run; sm.cl[wave * 16 + col] = lsum; }
     __syncthreads();   // also: every wave is done reading the stage, which comb reuses
     if (tid < 16) {
         float M = -INFINITY;
         for (int w = 0; w < DC_WAVES; ++w) M = fmaxf(M, sm.cm[w * 16 + tid]);
-        float L = 0.f;
+        float Ls = 0.f;
         for (int w = 0; w < DC_WAVES; ++w) {
             const float mw = sm.cm[w * 16 + tid];
-            L += mw == -INFINITY ? 0.f : sm.cl[w * 16 + tid] * fast_exp(mw - M);
+            Ls += mw == -INFINITY ? 0.f : sm.cl[w * 16 + tid] * fast_exp(mw - M);
         }
         sm.mrow[tid] = M;
-        sm.lrow[tid] = L;
+        sm.lrow[tid] = Ls;
     }
     __syncthreads();
-    float fac[4];
+    const float mrow = sm.mrow[col];
+    const float fac = m_run == -INFINITY ? 0.f : fast_exp(m_run - mrow);
+    if (wave >= 4 && col < nr4) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        const int row = 4 * grp + v;
-        const float mw = sm.cm[wave * 16 + row];
-        fac[v] = mw == -INFINITY ? 0.f : fast_exp(mw - sm.mrow[row]);
+        for (int b = 0; b < 8; ++b)
+            *reinterpret_cast<f32x4*>(&sm.comb[((wave - 4) * nr4 + col) * DC_CROW + 16 * b + 4 * grp]) = acc[b] * fac;
     }
-    if (wave >= 4) {
+    __syncthreads();
+    if (wave < 4 && col < nr4) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int row = 4 * grp + v;
-            if (row < nr4) {
-#pragma unroll
-                for (int b = 0; b < 8; ++b) sm.comb[((wave - 4) * nr4 + row) * D + 16 * b + col] = acc[b][v] * fac[v];
-            }
+        for (int b = 0; b < 8; ++b) {
+            f32x4* dst = reinterpret_cast<f32x4*>(&sm.comb[(wave * nr4 + col) * DC_CROW + 16 * b + 4 * grp]);
+            *dst = acc[b] * fac + *dst;
         }
     }
     __syncthreads();
-    if (wave < 4) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int row = 4 * grp + v;
-            if (row < nr4) {
-#pragma unroll
-                for (int b = 0; b < 8; ++b) {
-                    float* dst = &sm.comb[(wave * nr4 + row) * D + 16 * b + col];
-                    *dst = acc[b][v] * fac[v] + *dst;
-                }
-            }
-        }
-    }
-    __syncthreads();
-    const int units = p.G * p.nqt;
     const int nrec = p.n_wg + 1;
-    float* recs = p.part + ((int64_t)sq * units + gq) * nrec * DC_REC;
+    float* recs = p.part + (int64_t)unit * nrec * DC_REC;
     {
         float* rec = recs + (int64_t)x * DC_REC;
         const int n4 = nr4 * D / 4;
         for (int idx = tid; idx < n4; idx += DC_THREADS) {
-            const f32x4 a = reinterpret_cast<const f32x4*>(sm.comb)[idx];
-            const f32x4 b = reinterpret_cast<const f32x4*>(sm.comb + nr4 * D)[idx];
-            const f32x4 c = reinterpret_cast<const f32x4*>(sm.comb + 2 * nr4 * D)[idx];
-            const f32x4 d = reinterpret_cast<const f32x4*>(sm.comb + 3 * nr4 * D)[idx];
+            const int ci = (idx >> 5) * DC_CROW + 4 * (idx & 31);   // row idx/32, float4 idx%32
+            const f32x4 a = *reinterpret_cast<const f32x4*>(sm.comb + ci);
+            const f32x4 b = *reinterpret_cast<const f32x4*>(sm.comb + nr4 * DC_CROW + ci);
+            const f32x4 c = *reinterpret_cast<const f32x4*>(sm.comb + 2 * nr4 * DC_CROW + ci);
+            const f32x4 d = *reinterpret_cast<const f32x4*>(sm.comb + 3 * nr4 * DC_CROW + ci);
             reinterpret_cast<f32x4*>(rec + 32)[idx] = ((a + b) + c) + d;
         }
         if (tid < 16) { rec[tid] = sm.mrow[tid]; rec[16 + tid] = sm.lrow[tid]; }
@@ -816,9 +870,10 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         prm.n_wg = pl.n_wg;
         prm.tpw = pl.tpw;
         prm.total_tiles = pl.total_tiles;
-        dim3 grid(pl.n_wg + 1, sh.G * pl.nqt, ns);
-        if (sh.dtype == VARRATE_BF16) decode_kernel<false><<<grid, DC_THREADS, lds, st>>>(prm);
-        else decode_kernel<true><<<grid, DC_THREADS, lds, st>>>(prm);
+        prm.units = ns * sh.G * pl.nqt;
+        const unsigned nblk = (unsigned)(prm.units * (pl.n_wg + 1));
+        if (sh.dtype == VARRATE_BF16) decode_kernel<false><<<nblk, DC_THREADS, lds, st>>>(prm);
+        else decode_kernel<true><<<nblk, DC_THREADS, lds, st>>>(prm);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         MergeParams mp;

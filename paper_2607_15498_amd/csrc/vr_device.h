@@ -29,15 +29,27 @@ __device__ __forceinline__ void split_bf16(float x, uint32_t& hi, uint32_t& lo) 
 }
 __device__ __forceinline__ uint32_t pack2(uint32_t lo16, uint32_t hi16) { return lo16 | (hi16 << 16); }
 
+// Two fp32 -> packed bf16x2 (a in the low half), round to nearest even, by the gfx950
+// conversion instruction.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t cvt_bf16x2(float a, float b) {
+    const bf16x2_t v = {(__bf16)a, (__bf16)b};
+    return __builtin_bit_cast(uint32_t, v);
+}
+// (hi, lo) bf16x2 pairs of two fp32 values.
+__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+    hi = cvt_bf16x2(a, b);
+    lo = cvt_bf16x2(a - bf_lo(hi), b - bf_hi(hi));
+}
+
 // 8 fp32 -> (hi, lo) bf16x8 fragments.
 __device__ __forceinline__ void split8(const float* x, u32x4& hi, u32x4& lo) {
-    uint32_t h[8], l[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) split_bf16(x[e], h[e], l[e]);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-        hi[k] = pack2(h[2 * k], h[2 * k + 1]);
-        lo[k] = pack2(l[2 * k], l[2 * k + 1]);
+        uint32_t h, l;
+        split2(x[2 * k], x[2 * k + 1], h, l);
+        hi[k] = h;
+        lo[k] = l;
     }
 }
 
@@ -81,6 +93,26 @@ __device__ __forceinline__ float wave_max16(float v) {   // over lanes sharing l
     v = fmaxf(v, shfl_xor_f(v, 4));
     v = fmaxf(v, shfl_xor_f(v, 8));
     return v;
+}
+
+// Reductions over the lane pairs (l, l ^ 16) and (l, l ^ 32) by the gfx950 permlane swaps
+// (ALU ops, no LDS path, no lane-index arithmetic).  Both lanes of a pair receive the two
+// values in the same order, so both compute bit-identical results.
+__device__ __forceinline__ float xmax16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xmax32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xsum16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xsum32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 // exp(x) on the hardware exp2 path (x * log2 e); -inf -> 0.
