@@ -336,60 +336,8 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     if (r_ok && t_r < p.N) rv = load16(S.srank + t_r);     // srank is padded to a multiple of 64
     if (!exact && tid < ncl) cbv = S.chunk_off[c_lo + tid];
 
-    // ---- 1c. score-operand fragments of the query rows (lane -> query row col, K group
-    //          grp; bf16 hi and lo parts)
-    uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf);
-    if (!exact) {
-        // q' = P_K q / sqrt(d) by MFMA; C lane -> query row col, directions 16 wave + 4 grp + v
-        u32x4 qb[4][2];
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            if constexpr (F32) {
-                float x8[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) x8[e] = q_ok ? __uint_as_float(qr[s][e >> 2][e & 3]) : 0.f;
-                split8(x8, qb[s][0], qb[s][1]);
-            } else {
-                qb[s][0] = q_ok ? qr[s][0] : u32x4{0, 0, 0, 0};
-                qb[s][1] = u32x4{0, 0, 0, 0};
-            }
-        }
-        f32x4 c = {0, 0, 0, 0};
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            float a8[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) { a8[e] = __uint_as_float(pa[s][0][e]); a8[4 + e] = __uint_as_float(pa[s][1][e]); }
-            u32x4 ah, al;
-            split8(a8, ah, al);
-            c = mfma(ah, qb[s][0], c);
-            c = mfma(al, qb[s][0], c);
-            if constexpr (F32) c = mfma(ah, qb[s][1], c);
-        }
-        // direction j = 16 wave + 4 grp + v is element (j & 7) of K group ((j & 31) >> 3) of
-        // step j >> 5: two bf16 pairs per lane, for the hi and the lo fragment
-        uint32_t h[4], l[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) split_bf16(c[v] * scale, h[v], l[v]);
-        const int s = wave >> 1, gp = 2 * (wave & 1) + (grp >> 1), dw = 2 * (grp & 1);
-        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 0) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
-        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 1) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
-    } else {
-        float v8[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float val;
-            if constexpr (F32) val = __uint_as_float(qr[0][e >> 2][e & 3]);
-            else val = (e & 1) ? bf_hi(qr[0][0][e >> 1]) : bf_lo(qr[0][0][e >> 1]);
-            v8[e] = q_ok ? val * scale : 0.f;
-        }
-        u32x4 hh, ll;
-        split8(v8, hh, ll);
-        sm.qf[(qs_ * 2 + qpart) * 64 + lane] = qpart ? ll : hh;
-    }
-
     lane = lane_now(); tid = 64 * wave + lane; grp = lane >> 4; col = lane & 15;
-    // ---- 1d. offsets of the stored slots inside each chunk: local prefix sums of a
+    // ---- 1c. offsets of the stored slots inside each chunk: local prefix sums of a
     //          thread's 16 ranks, then a 16-lane scan of the threads of one chunk (one DPP
     //          row); ranks past the chunk's end count as 0
     if (r_ok) {
@@ -493,6 +441,60 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     };
     plan();
     issue();
+    // ---- 2c. while the round is in flight: score-operand fragments of the query rows
+    //          (lane -> query row col, K group grp; bf16 hi and lo parts).  The basis and
+    //          query loads landed with the rank loads (issued before them), so nothing here
+    //          waits for the direct-to-LDS loads.
+    uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf);
+    if (!exact) {
+        // q' = P_K q / sqrt(d) by MFMA; C lane -> query row col, directions 16 wave + 4 grp + v
+        u32x4 qb[4][2];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            if constexpr (F32) {
+                float x8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x8[e] = q_ok ? __uint_as_float(qr[s][e >> 2][e & 3]) : 0.f;
+                split8(x8, qb[s][0], qb[s][1]);
+            } else {
+                qb[s][0] = q_ok ? qr[s][0] : u32x4{0, 0, 0, 0};
+                qb[s][1] = u32x4{0, 0, 0, 0};
+            }
+        }
+        f32x4 c = {0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            float a8[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { a8[e] = __uint_as_float(pa[s][0][e]); a8[4 + e] = __uint_as_float(pa[s][1][e]); }
+            u32x4 ah, al;
+            split8(a8, ah, al);
+            c = mfma(ah, qb[s][0], c);
+            c = mfma(al, qb[s][0], c);
+            if constexpr (F32) c = mfma(ah, qb[s][1], c);
+        }
+        // direction j = 16 wave + 4 grp + v is element (j & 7) of K group ((j & 31) >> 3) of
+        // step j >> 5: two bf16 pairs per lane, for the hi and the lo fragment
+        uint32_t h[4], l[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) split_bf16(c[v] * scale, h[v], l[v]);
+        const int s = wave >> 1, gp = 2 * (wave & 1) + (grp >> 1), dw = 2 * (grp & 1);
+        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 0) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 1) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
+    } else {
+        float v8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            float val;
+            if constexpr (F32) val = __uint_as_float(qr[0][e >> 2][e & 3]);
+            else val = (e & 1) ? bf_hi(qr[0][0][e >> 1]) : bf_lo(qr[0][0][e >> 1]);
+            v8[e] = q_ok ? val * scale : 0.f;
+        }
+        u32x4 hh, ll;
+        split8(v8, hh, ll);
+        sm.qf[(qs_ * 2 + qpart) * 64 + lane] = qpart ? ll : hh;
+    }
+
 
     for (;;) {
         __builtin_amdgcn_s_waitcnt(0);   // this wave's direct-to-LDS loads have landed
@@ -630,11 +632,11 @@ constexpr int MG_BATCH = 16;   // record rows per thread in flight
 template <bool F32>
 __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p) {
     typedef typename Elem<F32>::T ET;
-    __shared__ float wm[DC_MAX_REC * 16];
-    __shared__ float wl[DC_MAX_REC * 16];
+    __shared__ float wm[DC_MAX_REC * 16 + DC_THREADS];   // + a dummy slot per thread
+    __shared__ float wl[DC_MAX_REC * 16 + DC_THREADS];
     __shared__ __attribute__((aligned(16))) float lanes[DC_THREADS * 4];
-    __shared__ __attribute__((aligned(16))) float accR[16 * D];
-    __shared__ __attribute__((aligned(16))) float accE[16 * D];
+    __shared__ __attribute__((aligned(16))) float accR[16 * DC_CROW];   // rows padded: no bank conflicts
+    __shared__ __attribute__((aligned(16))) float accE[16 * DC_CROW];
     __shared__ float red[2][DC_WAVES][16];
     __shared__ float mrow[16], lrow[16];
     const int unit = blockIdx.x;
@@ -652,12 +654,9 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
     const int e4 = tid % E, k4 = tid / E;
     const int row4 = (e4 * 4) / D;
 
-    // ---- 1. issue: record maxima / sums, the first batch of coded record rows, basis columns
-    for (int idx = tid; idx < nrec * 16; idx += DC_THREADS) {
-        const int r = idx >> 4, row = idx & 15;
-        wm[idx] = recs[(int64_t)r * DC_REC + row];
-        wl[idx] = recs[(int64_t)r * DC_REC + 16 + row];
-    }
+    // ---- 1. issue the first batch of coded record rows, the basis columns and the record
+    //          maxima / sums (the first 1024 of each held in registers), then store the
+    //          maxima / sums to LDS: one memory round trip
     f32x4 a[MG_BATCH];
 #pragma unroll
     for (int u = 0; u < MG_BATCH; ++u) {
@@ -672,6 +671,27 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
 #pragma unroll
         for (int i = 0; i < 8; ++i) pb[s][i] = PV[(32 * s + 8 * grp + i) * D + 16 * wave + col];
     const f32x4 ex = tid < E ? reinterpret_cast<const f32x4*>(recs + 32)[tid] : f32x4{0, 0, 0, 0};
+    float ml[2][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        int idx = tid + h * DC_THREADS;
+        idx = idx < nrec * 16 ? idx : nrec * 16 - 1;          // clamped: unconditional loads
+        const int r = idx >> 4, row = idx & 15;
+        ml[h][0] = recs[(int64_t)r * DC_REC + row];
+        ml[h][1] = recs[(int64_t)r * DC_REC + 16 + row];
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {      // unconditional stores (past the records: dummy slot)
+        const int idx = tid + h * DC_THREADS;
+        const int dst = idx < nrec * 16 ? idx : DC_MAX_REC * 16 + tid;
+        wm[dst] = ml[h][0];
+        wl[dst] = ml[h][1];
+    }
+    for (int idx = tid + 2 * DC_THREADS; idx < nrec * 16; idx += DC_THREADS) {
+        const int r = idx >> 4, row = idx & 15;
+        wm[idx] = recs[(int64_t)r * DC_REC + row];
+        wl[idx] = recs[(int64_t)r * DC_REC + 16 + row];
+    }
     __syncthreads();
 
     // ---- 2. row maxima, record weights, row sums (32 threads per row)
@@ -740,8 +760,9 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
     if (tid < E) {
         f32x4 t = reinterpret_cast<const f32x4*>(lanes)[tid];
         for (int kk = 1; kk < KL; ++kk) t += reinterpret_cast<const f32x4*>(lanes)[kk * E + tid];
-        reinterpret_cast<f32x4*>(accR)[tid] = t;
-        reinterpret_cast<f32x4*>(accE)[tid] = wm[(tid * 4) / D] * ex;
+        const int ci = (tid >> 5) * DC_CROW + 4 * (tid & 31);     // row tid/32, float4 tid%32
+        *reinterpret_cast<f32x4*>(accR + ci) = t;
+        *reinterpret_cast<f32x4*>(accE + ci) = wm[(tid * 4) / D] * ex;
     }
     __syncthreads();
     // ---- 4. back-rotation by MFMA: C[row][c] = sum_j accR[row][j] P_V[j][c]
@@ -751,7 +772,7 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
     for (int s = 0; s < 4; ++s) {
         float a8[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) a8[i] = col < nr4 ? accR[col * D + 32 * s + 8 * grp + i] : 0.f;
+        for (int i = 0; i < 8; ++i) a8[i] = col < nr4 ? accR[col * DC_CROW + 32 * s + 8 * grp + i] : 0.f;
         u32x4 ah, al, bh, bl;
         split8(a8, ah, al);
         split8(pb[s], bh, bl);
@@ -766,7 +787,7 @@ __global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p)
     for (int v = 0; v < 4; ++v) {
         const int row = 4 * grp + v;
         if (row < rows) {
-            const float val = (o[v] + accE[row * D + c]) / lrow[row];
+            const float val = (o[v] + accE[row * DC_CROW + c]) / lrow[row];
             const int qrow = 16 * qt + row;
             const int query = qrow / p.hpg, hh = qrow % p.hpg;
             const int64_t oi = ((int64_t)query * p.H + g * p.hpg + hh) * D + c;
