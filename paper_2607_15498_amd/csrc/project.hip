@@ -230,7 +230,7 @@ __global__ __launch_bounds__(PJ_THREADS, F32 ? 2 : 4) void project_kernel(
             load_x<F32>(nxt, X, sm, ncc, ni0, s_T[ncc], (int64_t)(c0 + ncc) * CHUNK, G, g, grp, col);
             const int T = s_T[cc];
             const int rmax = sm.s_rank[cc * CHUNK + i0];
-            const int na = (rmax + 15) >> 4;
+            const int na = rmax < D ? (rmax + 15) >> 4 : D / 16;
             u32x4 xh[2][4], xl[2][4];
 #pragma unroll
             for (int hb = 0; hb < 2; ++hb)
@@ -255,6 +255,9 @@ __global__ __launch_bounds__(PJ_THREADS, F32 ? 2 : 4) void project_kernel(
                 const int i = i0 + 16 * hb + col;
                 r_of[hb] = i < T ? sm.s_rank[cc * CHUNK + i] : 0;
                 o_of[hb] = i < T ? sm.s_off[cc * CHUNK + i] : 0;
+                // stores stay inside the head's stream whatever the layout tables hold
+                const int64_t room = coef_stride - ((int64_t)s_base[cc] + o_of[hb]);
+                r_of[hb] = room < r_of[hb] ? (room > 0 ? (int)room : 0) : r_of[hb];
             }
             const int64_t out0 = (int64_t)g * coef_stride + s_base[cc];
             for (int a = 0; a < na; ++a) {

@@ -1,87 +1,79 @@
-// Observation-window salience (Sec. 3.2 Eq. (4)) and SnapKV pooling, gfx950.
+// Observation-window salience (Sec. 3.2 Eq. (4)) and the length-5 moving average, gfx950.
 //
 // For KV head g the window queries of its H/G query heads form `rows` = (H/G) * w query
 // rows (row rho = hh * w + i: query head g*(H/G)+hh, window query i at position n-w+i).
 // Logits x = <q_rho, k_t> / sqrt(d) come from bf16 MFMA tiles (16 rows x 16 keys x 32 d);
 // fp32 inputs are split into bf16 hi + lo parts (three products), keeping ~2^-16 accuracy.
 //
-//   pass 1 (sal_rowstats): per (row, key block) online max / sum of exp over the causal
-//            range, from key tiles staged through LDS;
+//   pass 1 (sal_rowstats): per (row, key block) running max / sum of exp over the causal
+//            range;
 //   merge  (sal_merge):    per row, the global max M and 1/L;
 //   pass 2 (sal_colsum):   per coded key t, sum over rows of exp(x - M) / L (every window
 //            query sees every coded key, so no mask), summed over the group's rows in a
 //            fixed order -> s_part[g][t];
 //   pool   (sal_pool):     s_t = sum_g s_part[g][t] / (w H) (fixed order), then the centred
 //            length-5 moving average with zero padding, rounded to fp32.
+//
+// Both passes give each workgroup (8 waves) a contiguous run of 32 KB key blocks of one KV
+// head, double-buffered in LDS: block b + 2 is requested with direct-to-LDS loads into the
+// buffer block b has just vacated, while block b + 1 is computed.  Every wave takes one or
+// two 16-row tiles of the window rows (its query fragments load once per workgroup).  A
+// block sits in LDS in 16-byte pieces, XOR-swizzled inside each key row, so the 16 lanes
+// that read the same piece of 16 consecutive keys hit 16 different bank groups.
 #include "vr_internal.h"
 
 namespace vr {
 
-constexpr int SAL_THREADS = 256;           // 4 waves
-constexpr int SAL_KSUB = 64;               // keys staged in LDS at a time
-constexpr int SAL_KB1 = 512;               // keys per pass-1 workgroup
-constexpr int SAL_KB2 = 256;               // keys per pass-2 workgroup
-constexpr int SAL_MAX_RT = 4;              // row tiles per wave (rows <= 4 * 16 * 4 = 256)
+constexpr int SL_THREADS = 512;            // 8 waves
+constexpr int SL_WAVES = 8;
+constexpr int SL_STAGE = 32768;            // bytes of keys per block (one LDS buffer)
+constexpr int SL_MAX_RT = 2;               // row tiles per wave (rows <= 8 * 16 * 2 = 256)
+constexpr int SL_LPB = SL_STAGE / 1024 / SL_WAVES;   // direct-to-LDS loads per wave per block (4)
+constexpr int SL_SLOTS = 512;              // workgroups per launch: two per CU
 
-template <bool F32> struct KTile;
-// bf16 keys: row of 128 bf16 = 256 B, padded to 272 B to spread LDS banks.
-template <> struct KTile<false> {
-    static constexpr int ROW_U32 = 68;
-};
-// fp32 keys are staged as split hi/lo bf16 rows (2 x 272 B).
-template <> struct KTile<true> {
-    static constexpr int ROW_U32 = 136;
-};
-
-// Keys of one staging step: SAL_KSUB keys x 16 pieces of 8 elements; each thread holds
-// 4 pieces (bf16: 16 bytes each; fp32: 32 bytes each, split into hi/lo when stored).
-template <bool F32> struct KRegs { u32x4 a[4]; u32x4 b[4]; };
-
-template <bool F32>
-__device__ __forceinline__ void load_keys(KRegs<F32>& r, const void* K, int64_t n, int G, int g, int64_t k0) {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int idx = threadIdx.x + k * SAL_THREADS;
-        const int key = idx >> 4, ch = idx & 15;
-        const int64_t t = k0 + key;
-        r.a[k] = r.b[k] = u32x4{0, 0, 0, 0};
-        if (t < n) {
-            if constexpr (!F32) {
-                r.a[k] = load16((const uint16_t*)K + ((t * G + g) * D + ch * 8));
-            } else {
-                const float* src = (const float*)K + ((t * G + g) * D + ch * 8);
-                r.a[k] = load16(src);
-                r.b[k] = load16(src + 4);
-            }
-        }
-    }
+// Wait until at most `left` of this wave's memory loads are outstanding (vmcnt; the export
+// and LDS counters are left alone).  Loads complete in order for this counter.
+template <int left>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(left >= 0 && left < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((left & 15) | (7 << 4) | (15 << 8) | ((left >> 4) << 14));
 }
 
+template <bool B> struct SlTag { static constexpr bool value = B; };
+
+template <bool F32> __host__ __device__ constexpr int sl_keys() { return SL_STAGE / (D * (F32 ? 4 : 2)); }
+template <bool F32> __host__ __device__ constexpr int sl_pieces() { return D * (F32 ? 4 : 2) / 16; }
+
+// Issue the block's keys k0 .. k0 + KB - 1 of head g into the stage.  Slot s (16 bytes)
+// holds piece (s % P) ^ (k % P) of key k = s / P; keys past n read key n - 1 (masked later).
 template <bool F32>
-__device__ __forceinline__ void store_keys(uint32_t* lds, const KRegs<F32>& r) {
-    constexpr int RU = KTile<F32>::ROW_U32;
+__device__ __forceinline__ void sl_issue(uint8_t* stage, const void* K, int64_t n, int G, int g, int64_t k0) {
+    constexpr int P = sl_pieces<F32>();
+    constexpr int BLOCKS = SL_STAGE / 1024;             // 64 slots (1 KB) per load
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const size_t row_bytes = (size_t)D * (F32 ? 4 : 2);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int idx = threadIdx.x + k * SAL_THREADS;
-        const int key = idx >> 4, ch = idx & 15;
-        if constexpr (!F32) {
-            *reinterpret_cast<u32x4*>(lds + key * RU + ch * 4) = r.a[k];
-        } else {
-            float x[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) { x[e] = __uint_as_float(r.a[k][e]); x[4 + e] = __uint_as_float(r.b[k][e]); }
-            u32x4 hi, lo;
-            split8(x, hi, lo);
-            *reinterpret_cast<u32x4*>(lds + key * RU + ch * 4) = hi;
-            *reinterpret_cast<u32x4*>(lds + key * RU + 68 + ch * 4) = lo;
-        }
+    for (int b = 0; b < BLOCKS / SL_WAVES; ++b) {
+        const int m = wave + SL_WAVES * b;
+        const int s = 64 * m + lane;
+        const int k = s / P, piece = (s % P) ^ (k % P);
+        int64_t t = k0 + k;
+        t = t < n ? t : n - 1;
+        const uint8_t* src = (const uint8_t*)K + ((size_t)t * G + g) * row_bytes + 16 * piece;
+        const uint32_t dst = __builtin_amdgcn_readfirstlane(
+            (uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)(stage + 1024 * m));
+        // issued in asm so the compiler does not add its own wait for all of these loads
+        // before the first LDS read; the stage waits below (vmcnt + barrier) order them
+        asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                     :: "v"(src), "s"(dst) : "memory", "m0");
     }
 }
 
 // Query fragments (A operand) for row tile rt: lane row = 16 rt + l%16, K group l/16.
 template <bool F32>
-__device__ __forceinline__ void load_qfrag(const void* Qw, int H, int w, int hpg, int g, int rows,
-                                           int rt, u32x4 (&qh)[4], u32x4 (&ql)[4]) {
+__device__ __forceinline__ void sl_qfrag(const void* Qw, int H, int w, int hpg, int g, int rows,
+                                         int rt, u32x4 (&qh)[4], u32x4 (&ql)[4]) {
     const int lane = threadIdx.x & 63;
     const int rho = rt * 16 + (lane & 15);
     const int grp = lane >> 4;
@@ -92,34 +84,49 @@ __device__ __forceinline__ void load_qfrag(const void* Qw, int H, int w, int hpg
     for (int s = 0; s < 4; ++s) {
         const int c0 = 32 * s + 8 * grp;
         if constexpr (!F32) {
-            qh[s] = ok ? load16((const uint16_t*)Qw + base + c0) : u32x4{0, 0, 0, 0};
+            // rows past `rows` read row 0: their logits are never used (pass 1 writes only
+            // real rows; pass 2 weighs them by 1/L = 0), and no mask waits for the load
+            qh[s] = load16((const uint16_t*)Qw + base + c0);
             ql[s] = u32x4{0, 0, 0, 0};
         } else {
-            float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-            if (ok) {
-                const float* src = (const float*)Qw + base + c0;
-                u32x4 a = load16(src), b = load16(src + 4);
-                for (int e = 0; e < 4; ++e) { x[e] = __uint_as_float(a[e]); x[4 + e] = __uint_as_float(b[e]); }
+            const float* src = (const float*)Qw + base + c0;
+            const u32x4 a = load16(src), b = load16(src + 4);
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                x[e] = ok ? __uint_as_float(a[e]) : 0.f;
+                x[4 + e] = ok ? __uint_as_float(b[e]) : 0.f;
             }
             split8(x, qh[s], ql[s]);
         }
     }
 }
 
-// Logit tile: rows 16 rt.., keys kt*16.. of the staged block (C layout: lane col = key).
+// Logit tile: rows 16 rt.. (the fragments) x keys 16 kt.. of the stage (C lane col = key).
 template <bool F32>
-__device__ __forceinline__ f32x4 logit_tile(const uint32_t* lds, int kt, const u32x4 (&qh)[4],
-                                            const u32x4 (&ql)[4]) {
-    constexpr int RU = KTile<F32>::ROW_U32;
+__device__ __forceinline__ f32x4 sl_logits(const uint8_t* stage, int kt, const u32x4 (&qh)[4],
+                                           const u32x4 (&ql)[4]) {
+    constexpr int P = sl_pieces<F32>();
     const int lane = threadIdx.x & 63;
-    const uint32_t* row = lds + (kt * 16 + (lane & 15)) * RU + (lane >> 4) * 4;
+    const int k = kt * 16 + (lane & 15), grp = lane >> 4;
+    const uint8_t* row = stage + (size_t)k * P * 16;
     f32x4 c = {0, 0, 0, 0};
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-        u32x4 kh = *reinterpret_cast<const u32x4*>(row + s * 16);
-        c = mfma(qh[s], kh, c);
-        if constexpr (F32) {
-            u32x4 kl = *reinterpret_cast<const u32x4*>(row + 68 + s * 16);
+        if constexpr (!F32) {
+            const int piece = 4 * s + grp;
+            const u32x4 kh = *reinterpret_cast<const u32x4*>(row + 16 * (piece ^ (k % P)));
+            c = mfma(qh[s], kh, c);
+        } else {
+            const int p0 = 2 * (4 * s + grp);
+            const u32x4 a = *reinterpret_cast<const u32x4*>(row + 16 * (p0 ^ (k % P)));
+            const u32x4 b = *reinterpret_cast<const u32x4*>(row + 16 * ((p0 + 1) ^ (k % P)));
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { x[e] = __uint_as_float(a[e]); x[4 + e] = __uint_as_float(b[e]); }
+            u32x4 kh, kl;
+            split8(x, kh, kl);
+            c = mfma(qh[s], kh, c);
             c = mfma(ql[s], kh, c);
             c = mfma(qh[s], kl, c);
         }
@@ -128,73 +135,129 @@ __device__ __forceinline__ f32x4 logit_tile(const uint32_t* lds, int kt, const u
 }
 
 // ----------------------------------------------------------------------------------------
-// pass 1: stats[(g * rows + rho) * nkb + kb] = (max, sum exp(x - max)) over this block's
-// causal keys.  Grid (nkb, G).
+// Block pipeline shared by both passes: buffers 0/1 hold blocks b0, b0+1, ..; `step(b, buf)`
+// computes block b from its buffer.
+template <bool F32, class Step>
+__device__ __forceinline__ void sl_pipeline(uint8_t* lds, const void* K, int64_t n, int G, int g,
+                                            int b0, int b1, Step step) {
+    constexpr int KB = sl_keys<F32>();
+    sl_issue<F32>(lds, K, n, G, g, (int64_t)b0 * KB);
+    if (b0 + 1 < b1) sl_issue<F32>(lds + SL_STAGE, K, n, G, g, (int64_t)(b0 + 1) * KB);
+    for (int b = b0; b < b1; ++b) {
+        uint8_t* buf = lds + ((b - b0) & 1) * SL_STAGE;
+        if (b + 1 < b1) wait_vm<SL_LPB>();       // block b landed; block b + 1 may be in flight
+        else wait_vm<0>();
+        __syncthreads();
+        step(b, buf);
+        __syncthreads();                          // every wave is done with this buffer
+        if (b + 2 < b1) sl_issue<F32>(buf, K, n, G, g, (int64_t)(b + 2) * KB);
+    }
+}
+
+// pass 1: stats[(g * rows + rho) * nw + wgi] = (max, sum exp(x - max)) over the causal keys
+// of the blocks [wgi * bpw, ..) of head g.  Grid (nw, G).
 template <bool F32>
-__global__ __launch_bounds__(SAL_THREADS) void sal_rowstats(const void* __restrict__ K,
-                                                            const void* __restrict__ Qw,
-                                                            int64_t n, int G, int H, int w,
-                                                            float2* __restrict__ stats, int nkb) {
-    __shared__ __attribute__((aligned(16))) uint32_t lds[SAL_KSUB * KTile<F32>::ROW_U32];
-    const int kb = blockIdx.x, g = blockIdx.y;
+__global__ __launch_bounds__(SL_THREADS, 4) void sal_rowstats(const void* __restrict__ K,
+                                                              const void* __restrict__ Qw,
+                                                              int64_t n, int G, int H, int w,
+                                                              float2* __restrict__ stats, int nw, int bpw) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    constexpr int KB = sl_keys<F32>();
+    constexpr int TPB = KB / 16;                  // key tiles per block
+    constexpr int TPS = TPB < 4 ? TPB : 4;        // key tiles per rescale
+    const int wgi = blockIdx.x, g = blockIdx.y;
     const int hpg = H / G, rows = hpg * w, nrt = (rows + 15) / 16;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t kbeg = (int64_t)kb * SAL_KB1;
-    const int64_t kend = kbeg + SAL_KB1 < n ? kbeg + SAL_KB1 : n;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const int64_t N = n - w;
+    const int nblk = (int)((n + KB - 1) / KB);
+    const int b0 = wgi * bpw, b1 = b0 + bpw < nblk ? b0 + bpw : nblk;
 
-    u32x4 qh[SAL_MAX_RT][4], ql[SAL_MAX_RT][4];
-    float m[SAL_MAX_RT][4], l[SAL_MAX_RT][4];
+    u32x4 qh[SL_MAX_RT][4], ql[SL_MAX_RT][4];
 #pragma unroll
-    for (int j = 0; j < SAL_MAX_RT; ++j) {
-        const int rt = wave + 4 * j;
-        if (rt < nrt) load_qfrag<F32>(Qw, H, w, hpg, g, rows, rt, qh[j], ql[j]);
-#pragma unroll
-        for (int v = 0; v < 4; ++v) { m[j][v] = -INFINITY; l[j][v] = 0.f; }
+    for (int j = 0; j < SL_MAX_RT; ++j) {
+        const int rt = wave + SL_WAVES * j;
+        if (rt < nrt) sl_qfrag<F32>(Qw, H, w, hpg, g, rows, rt, qh[j], ql[j]);
     }
-    const float scale = 0.08838834764831845f;  // 1/sqrt(128)
-
-    KRegs<F32> kr;
-    load_keys<F32>(kr, K, n, G, g, kbeg);
-    for (int64_t k0 = kbeg; k0 < kend; k0 += SAL_KSUB) {
-        __syncthreads();
-        store_keys<F32>(lds, kr);
-        __syncthreads();
-        if (k0 + SAL_KSUB < kend) load_keys<F32>(kr, K, n, G, g, k0 + SAL_KSUB);
+    // last visible key of each of this lane's rows (n - w + i for window query i); rows past
+    // `rows` see nothing
+    int tlast[SL_MAX_RT][4];                       // n < 2^31 (checked by the library)
 #pragma unroll
-        for (int j = 0; j < SAL_MAX_RT; ++j) {
-            const int rt = wave + 4 * j;
-            if (rt >= nrt) continue;
-            for (int kt = 0; kt < SAL_KSUB / 16; ++kt) {
-                const int64_t t = k0 + kt * 16 + (lane & 15);
-                if (k0 + kt * 16 >= kend) break;
-                f32x4 c = logit_tile<F32>(lds, kt, qh[j], ql[j]);
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int rho = rt * 16 + (lane >> 4) * 4 + v;
-                    const int i = rho % w;
-                    const bool vis = rho < rows && t < kend && t <= n - w + i;
-                    const float x = c[v] * scale;
-                    if (vis) {
-                        // online max/sum; rescale only when the max moves up
-                        if (x > m[j][v]) {
-                            l[j][v] = l[j][v] * fast_exp(m[j][v] - x) + 1.f;
-                            m[j][v] = x;
-                        } else {
-                            l[j][v] += fast_exp(x - m[j][v]);
-                        }
-                    }
-                }
-            }
-        }
-    }
-    // combine the 16 lanes that share a row (lane bits 0..3)
-#pragma unroll
-    for (int j = 0; j < SAL_MAX_RT; ++j) {
-        const int rt = wave + 4 * j;
-        if (rt >= nrt) continue;
+    for (int j = 0; j < SL_MAX_RT; ++j)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            float mm = m[j][v], ll = l[j][v];
+            const int rho = (wave + SL_WAVES * j) * 16 + (lane >> 4) * 4 + v;
+            tlast[j][v] = rho < rows ? (int)N + rho % w : -1;
+        }
+    // The block loads are issued in asm, unseen by the compiler's wait bookkeeping: every
+    // load it knows of must land before them, or its own waits would drain the pipeline.
+    wait_vm<0>();
+
+    const float sl2 = 0.08838834764831845f * 1.4426950408889634f;   // log2(e) / sqrt(128)
+    // Per lane and row: running max m and sum l of exp2 over this lane's keys, in log2
+    // units, rescaled once per TPS key tiles (no per-element branches).
+    float m[SL_MAX_RT][4], l[SL_MAX_RT][4];
+#pragma unroll
+    for (int j = 0; j < SL_MAX_RT; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) { m[j][v] = -INFINITY; l[j][v] = 0.f; }
+
+    auto tiles = [&](const uint8_t* buf, int64_t k0, int64_t kend, int tq0, auto masked) {
+#pragma unroll
+        for (int j = 0; j < SL_MAX_RT; ++j) {
+            const int rt = wave + SL_WAVES * j;
+            if (rt >= nrt) continue;
+            float x[TPS][4];
+#pragma unroll
+            for (int q = 0; q < TPS; ++q) {
+                const int kt = tq0 + q;
+                const f32x4 c = sl_logits<F32>(buf, kt, qh[j], ql[j]);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) x[q][v] = c[v] * sl2;
+                if constexpr (decltype(masked)::value) {
+                    const int t = (int)k0 + kt * 16 + (lane & 15);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        if (!(t < (int)kend && t <= tlast[j][v])) x[q][v] = -INFINITY;
+                }
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                float mx = m[j][v];
+#pragma unroll
+                for (int q = 0; q < TPS; ++q) mx = fmaxf(mx, x[q][v]);
+                if constexpr (decltype(masked)::value) {
+                    if (mx == -INFINITY) continue;            // nothing visible yet here
+                }
+                float sum = l[j][v] * __builtin_amdgcn_exp2f(m[j][v] - mx);
+#pragma unroll
+                for (int q = 0; q < TPS; ++q) sum += __builtin_amdgcn_exp2f(x[q][v] - mx);
+                l[j][v] = sum;
+                m[j][v] = mx;
+            }
+        }
+    };
+    sl_pipeline<F32>(lds, K, n, G, g, b0, b1, [&](int b, const uint8_t* buf) {
+        const int64_t k0 = (int64_t)b * KB;
+        const int64_t kend = k0 + KB < n ? k0 + KB : n;
+        // every key of a full block that ends before the window is visible to every row
+        if (kend - k0 == KB && kend <= N) {
+#pragma unroll
+            for (int tq = 0; tq < TPB; tq += TPS) tiles(buf, k0, kend, tq, SlTag<false>{});
+        } else {
+#pragma unroll
+            for (int tq = 0; tq < TPB; tq += TPS) tiles(buf, k0, kend, tq, SlTag<true>{});
+        }
+    });
+
+#pragma unroll
+    for (int j = 0; j < SL_MAX_RT; ++j) {
+        const int rt = wave + SL_WAVES * j;
+        if (rt >= nrt) continue;
+        // combine the 16 lanes (keys) that share a row (lane bits 0..3), in natural-log units
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            float mm = m[j][v] * 0.6931471805599453f, ll = l[j][v];
 #pragma unroll
             for (int off = 1; off < 16; off <<= 1) {
                 const float mo = shfl_xor_f(mm, off), lo = shfl_xor_f(ll, off);
@@ -206,152 +269,200 @@ __global__ __launch_bounds__(SAL_THREADS) void sal_rowstats(const void* __restri
             }
             const int rho = rt * 16 + (lane >> 4) * 4 + v;
             if ((lane & 15) == 0 && rho < rows)
-                stats[((int64_t)g * rows + rho) * nkb + kb] = make_float2(mm, ll);
+                stats[((int64_t)g * rows + rho) * nw + wgi] = make_float2(mm, ll);
         }
     }
 }
 
 // merge: ML[g * rows + rho] = (M, 1/L).  16 threads per row read its block partials in
-// parallel and combine them with shuffles.
+// parallel: the row maximum first, then the rescaled sums.
 __global__ __launch_bounds__(256) void sal_merge(const float2* __restrict__ stats, int nkb,
                                                  int total_rows, float2* __restrict__ ML) {
     const int r = blockIdx.x * 16 + (threadIdx.x >> 4), k = threadIdx.x & 15;
-    float m = -INFINITY, l = 0.f;
-    if (r < total_rows) {
-        const float2* s = stats + (int64_t)r * nkb;
+    const int rr = r < total_rows ? r : total_rows - 1;
+    const float2* s = stats + (int64_t)rr * nkb;
+    // max over this thread's partials (their loads all issue first), then the 16-lane max
+    float m = -INFINITY;
+#pragma unroll 8
+    for (int b = k; b < nkb; b += 16) m = fmaxf(m, s[b].x);
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, shfl_xor_f(m, off));
+    // sums rescaled to the row max (the partials are L1/L2 hits now)
+    float l = 0.f;
+    if (m != -INFINITY) {
+#pragma unroll 8
         for (int b = k; b < nkb; b += 16) {
             const float2 v = s[b];
-            if (v.x == -INFINITY) continue;
-            const float mn = fmaxf(m, v.x);
-            l = (m == -INFINITY ? 0.f : l * fast_exp(m - mn)) + v.y * fast_exp(v.x - mn);
-            m = mn;
+            l += v.x == -INFINITY ? 0.f : v.y * fast_exp(v.x - m);
         }
     }
 #pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-        const float mo = shfl_xor_f(m, off), lo = shfl_xor_f(l, off);
-        const float mn = fmaxf(m, mo);
-        const float a = m == -INFINITY ? 0.f : l * fast_exp(m - mn);
-        const float b = mo == -INFINITY ? 0.f : lo * fast_exp(mo - mn);
-        m = mn;
-        l = a + b;
-    }
+    for (int off = 1; off < 16; off <<= 1) l += shfl_xor_f(l, off);
     if (k == 0 && r < total_rows) ML[r] = make_float2(m, 1.f / l);
 }
 
-// pass 2: s_part[g * N + t] = sum over the group's rows of exp(x - M) / L, t < N.
-// Grid (ceil(N / SAL_KB2), G).
+// pass 2: s_part[g * N + t] = sum over the group's rows of exp(x - M) / L, t < N, for the
+// blocks [wgi * bpw, ..) of the coded keys of head g.  Grid (nw, G).
 template <bool F32>
-__global__ __launch_bounds__(SAL_THREADS) void sal_colsum(const void* __restrict__ K,
-                                                          const void* __restrict__ Qw,
-                                                          int64_t n, int G, int H, int w,
-                                                          const float2* __restrict__ ML,
-                                                          float* __restrict__ s_part) {
-    __shared__ __attribute__((aligned(16))) uint32_t lds[SAL_KSUB * KTile<F32>::ROW_U32];
-    __shared__ float colsum[4][SAL_KSUB];
-    const int g = blockIdx.y;
+__global__ __launch_bounds__(SL_THREADS, 4) void sal_colsum(const void* __restrict__ K,
+                                                            const void* __restrict__ Qw,
+                                                            int64_t n, int G, int H, int w,
+                                                            const float2* __restrict__ ML,
+                                                            float* __restrict__ s_part, int bpw) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    constexpr int KB = sl_keys<F32>();
+    constexpr int TPB = KB / 16;
+    __shared__ float colsum[SL_WAVES][KB];
+    const int wgi = blockIdx.x, g = blockIdx.y;
     const int64_t N = n - w;
     const int hpg = H / G, rows = hpg * w, nrt = (rows + 15) / 16;
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int64_t kbeg = (int64_t)blockIdx.x * SAL_KB2;
-    const int64_t kend = kbeg + SAL_KB2 < N ? kbeg + SAL_KB2 : N;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = threadIdx.x & 63;
+    const int nblk = (int)((N + KB - 1) / KB);
+    const int b0 = wgi * bpw, b1 = b0 + bpw < nblk ? b0 + bpw : nblk;
 
-    u32x4 qh[SAL_MAX_RT][4], ql[SAL_MAX_RT][4];
-    float rm[SAL_MAX_RT][4], rinv[SAL_MAX_RT][4];
+    u32x4 qh[SL_MAX_RT][4], ql[SL_MAX_RT][4];
+    float rm[SL_MAX_RT][4], rinv[SL_MAX_RT][4];
 #pragma unroll
-    for (int j = 0; j < SAL_MAX_RT; ++j) {
-        const int rt = wave + 4 * j;
-        if (rt < nrt) load_qfrag<F32>(Qw, H, w, hpg, g, rows, rt, qh[j], ql[j]);
+    for (int j = 0; j < SL_MAX_RT; ++j) {
+        const int rt = wave + SL_WAVES * j;
+        if (rt < nrt) sl_qfrag<F32>(Qw, H, w, hpg, g, rows, rt, qh[j], ql[j]);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int rho = rt * 16 + (lane >> 4) * 4 + v;
-            float2 mlv = (rt < nrt && rho < rows) ? ML[(int64_t)g * rows + rho] : make_float2(INFINITY, 0.f);
-            rm[j][v] = mlv.x;
-            rinv[j][v] = mlv.y;
+            const bool ok = rt < nrt && rho < rows;
+            const float2 mlv = ML[(int64_t)g * rows + (ok ? rho : 0)];   // unconditional load
+            rm[j][v] = mlv.x * 1.4426950408889634f;          // log2 units
+            rinv[j][v] = ok ? mlv.y : 0.f;                   // rows past `rows` weigh nothing
         }
     }
-    const float scale = 0.08838834764831845f;
+    // (see pass 1) every compiler-visible load lands before the asm-issued block loads
+    wait_vm<0>();
+    const float sl2 = 0.08838834764831845f * 1.4426950408889634f;   // log2(e) / sqrt(128)
 
-    KRegs<F32> kr;
-    load_keys<F32>(kr, K, n, G, g, kbeg);
-    for (int64_t k0 = kbeg; k0 < kend; k0 += SAL_KSUB) {
-        __syncthreads();
-        store_keys<F32>(lds, kr);
-        __syncthreads();
-        if (k0 + SAL_KSUB < kend) load_keys<F32>(kr, K, n, G, g, k0 + SAL_KSUB);
-        for (int kt = 0; kt < SAL_KSUB / 16; ++kt) {
+    sl_pipeline<F32>(lds, K, n, G, g, b0, b1, [&](int b, const uint8_t* buf) {
+        const int64_t k0 = (int64_t)b * KB;
+        const int64_t kend = k0 + KB < N ? k0 + KB : N;
+        const int ntile = (int)((kend - k0 + 15) / 16);
+#pragma unroll
+        for (int kt = 0; kt < TPB; ++kt) {
+            if (kt >= ntile) break;
             float acc = 0.f;   // this lane's key column: sum over the wave's rows
 #pragma unroll
-            for (int j = 0; j < SAL_MAX_RT; ++j) {
-                const int rt = wave + 4 * j;
+            for (int j = 0; j < SL_MAX_RT; ++j) {
+                const int rt = wave + SL_WAVES * j;
                 if (rt >= nrt) continue;
-                f32x4 c = logit_tile<F32>(lds, kt, qh[j], ql[j]);
+                const f32x4 c = sl_logits<F32>(buf, kt, qh[j], ql[j]);
 #pragma unroll
-                for (int v = 0; v < 4; ++v) acc += fast_exp(c[v] * scale - rm[j][v]) * rinv[j][v];
+                for (int v = 0; v < 4; ++v) acc += __builtin_amdgcn_exp2f(c[v] * sl2 - rm[j][v]) * rinv[j][v];
             }
-            acc += shfl_xor_f(acc, 16);
-            acc += shfl_xor_f(acc, 32);
+            acc = xsum32(xsum16(acc));
             if (lane < 16) colsum[wave][kt * 16 + lane] = acc;
         }
         __syncthreads();
-        if (threadIdx.x < SAL_KSUB) {
-            const int64_t t = k0 + threadIdx.x;
+        for (int kk = threadIdx.x; kk < ntile * 16; kk += SL_THREADS) {
+            const int64_t t = k0 + kk;
             if (t < kend) {
-                const int kk = threadIdx.x;
-                s_part[(int64_t)g * N + t] = ((colsum[0][kk] + colsum[1][kk]) + colsum[2][kk]) + colsum[3][kk];
+                float s = 0.f;
+#pragma unroll
+                for (int ww = 0; ww < SL_WAVES; ++ww) s += colsum[ww][kk];
+                s_part[(int64_t)g * N + t] = s;
             }
         }
-    }
+    });
 }
 
-// pool: sbar[t] = (s_{t-2} + ... + s_{t+2}) / 5 with s_k = sum_g s_part[g][k] / (w H).
-__global__ void sal_pool(const float* __restrict__ s_part, int64_t N, int G, float inv_wh,
-                         float* __restrict__ sbar) {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= N) return;
-    double acc = 0.0;
-    for (int64_t k = t - 2; k <= t + 2; ++k) {
-        if (k < 0 || k >= N) continue;
-        float s = 0.f;
-        for (int g = 0; g < G; ++g) s += s_part[(int64_t)g * N + k];
-        acc += (double)(s * inv_wh);
+// pool: sbar[t] = (s_{t-2} + ... + s_{t+2}) / 5 with s_k = sum_g s_part[g][k] / (w H).  A
+// block of 256 tokens first forms s for its tokens and a 2-token halo on each side.
+constexpr int SP_T = 256;
+__global__ __launch_bounds__(SP_T) void sal_pool(const float* __restrict__ s_part, int64_t N, int G,
+                                                 float inv_wh, float* __restrict__ sbar) {
+    __shared__ double sv[SP_T + 4];
+    const int64_t t0 = (int64_t)blockIdx.x * SP_T;
+    for (int i = threadIdx.x; i < SP_T + 4; i += SP_T) {
+        const int64_t k = t0 - 2 + i;
+        double v = 0.0;
+        if (k >= 0 && k < N) {
+            float s = 0.f;
+            for (int gg = 0; gg < G; ++gg) s += s_part[(int64_t)gg * N + k];
+            v = (double)(s * inv_wh);
+        }
+        sv[i] = v;
     }
+    __syncthreads();
+    const int64_t t = t0 + threadIdx.x;
+    if (t >= N) return;
+    const int i = threadIdx.x + 2;
+    const double acc = (((sv[i - 2] + sv[i - 1]) + sv[i]) + sv[i + 1]) + sv[i + 2];
     sbar[t] = (float)(acc / 5.0);
 }
 
 // ----------------------------------------------------------------------------------------
+// Work split: a pass over nblk blocks of each of the G heads uses about SL_SLOTS workgroups,
+// each taking bpw consecutive blocks of one head.
+struct SalPlan {
+    int nw, bpw;
+};
+static SalPlan sal_plan(int64_t nblk, int G) {
+    int per_head = SL_SLOTS / G;
+    per_head = per_head < 1 ? 1 : per_head;
+    SalPlan p;
+    p.bpw = (int)((nblk + per_head - 1) / per_head);
+    p.bpw = p.bpw < 1 ? 1 : p.bpw;
+    p.nw = (int)((nblk + p.bpw - 1) / p.bpw);
+    return p;
+}
+static int sal_kb(const varrate_shape& sh) { return sh.dtype == VARRATE_BF16 ? sl_keys<false>() : sl_keys<true>(); }
+
 size_t salience_ws_bytes(const varrate_shape& sh) {
     const int rows = (sh.H / sh.G) * sh.w;
-    const int64_t nkb = (sh.n + SAL_KB1 - 1) / SAL_KB1;
+    const int KB = sal_kb(sh);
+    const SalPlan p1 = sal_plan((sh.n + KB - 1) / KB, sh.G);
     const int64_t N = sh.n - sh.w;
-    return align256((size_t)sh.G * rows * nkb * sizeof(float2)) +
+    return align256((size_t)sh.G * rows * p1.nw * sizeof(float2)) +
            align256((size_t)sh.G * rows * sizeof(float2)) + align256((size_t)sh.G * N * sizeof(float));
+}
+
+template <bool F32>
+static hipError_t sal_attr() {
+    static bool done = false;
+    if (done) return hipSuccess;
+    hipError_t e = hipFuncSetAttribute((const void*)sal_rowstats<F32>, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * SL_STAGE);
+    if (e == hipSuccess)
+        e = hipFuncSetAttribute((const void*)sal_colsum<F32>, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * SL_STAGE);
+    if (e == hipSuccess) done = true;
+    return e;
 }
 
 hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Qw, float* sbar,
                            uint8_t* ws, hipStream_t st) {
     const int rows = (sh.H / sh.G) * sh.w;
-    const int nkb = (int)((sh.n + SAL_KB1 - 1) / SAL_KB1);
     const int64_t N = sh.n - sh.w;
+    const int KB = sal_kb(sh);
+    const SalPlan p1 = sal_plan((sh.n + KB - 1) / KB, sh.G);
+    const SalPlan p2 = sal_plan((N + KB - 1) / KB, sh.G);
     float2* stats = (float2*)ws;
-    ws += align256((size_t)sh.G * rows * nkb * sizeof(float2));
+    ws += align256((size_t)sh.G * rows * p1.nw * sizeof(float2));
     float2* ML = (float2*)ws;
     ws += align256((size_t)sh.G * rows * sizeof(float2));
     float* s_part = (float*)ws;
-
-    dim3 g1(nkb, sh.G), g2((unsigned)((N + SAL_KB2 - 1) / SAL_KB2), sh.G);
     const int tr = sh.G * rows;
-    if (sh.dtype == VARRATE_BF16) {
-        sal_rowstats<false><<<g1, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, nkb);
-        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, nkb, tr, ML);
-        sal_colsum<false><<<g2, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part);
+    const bool bf = sh.dtype == VARRATE_BF16;
+    hipError_t e = bf ? sal_attr<false>() : sal_attr<true>();
+    if (e != hipSuccess) return e;
+    dim3 g1(p1.nw, sh.G), g2(p2.nw, sh.G);
+    const size_t lds = 2 * SL_STAGE;
+    if (bf) {
+        sal_rowstats<false><<<g1, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, p1.bpw);
+        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, p1.nw, tr, ML);
+        sal_colsum<false><<<g2, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part, p2.bpw);
     } else {
-        sal_rowstats<true><<<g1, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, nkb);
-        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, nkb, tr, ML);
-        sal_colsum<true><<<g2, SAL_THREADS, 0, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part);
+        sal_rowstats<true><<<g1, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, p1.bpw);
+        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, p1.nw, tr, ML);
+        sal_colsum<true><<<g2, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part, p2.bpw);
     }
-    sal_pool<<<(unsigned)((N + 255) / 256), 256, 0, st>>>(s_part, N, sh.G,
-                                                           1.0f / ((float)sh.w * (float)sh.H), sbar);
+    sal_pool<<<(unsigned)((N + SP_T - 1) / SP_T), SP_T, 0, st>>>(s_part, N, sh.G,
+                                                                   1.0f / ((float)sh.w * (float)sh.H), sbar);
     return hipGetLastError();
 }
 
