@@ -7,8 +7,9 @@
 //
 //   pass 1 (sal_rowstats): per (row, key block) running max / sum of exp over the causal
 //            range;
-//   merge  (sal_merge):    per row, the global max M and 1/L;
-//   pass 2 (sal_colsum):   per coded key t, sum over rows of exp(x - M) / L (every window
+//   pass 2 (sal_colsum):   per row, the global max M and 1/L from the pass-1 partials (every
+//            workgroup for its own head), then per coded key t, the sum over rows of
+//            exp(x - M) / L (every window
 //            query sees every coded key, so no mask), summed over the group's rows in a
 //            fixed order -> s_part[g][t];
 //   pool   (sal_pool):     s_t = sum_g s_part[g][t] / (w H) (fixed order), then the centred
@@ -30,6 +31,7 @@ constexpr int SL_STAGE = 32768;            // bytes of keys per block (one LDS b
 constexpr int SL_MAX_RT = 2;               // row tiles per wave (rows <= 8 * 16 * 2 = 256)
 constexpr int SL_LPB = SL_STAGE / 1024 / SL_WAVES;   // direct-to-LDS loads per wave per block (4)
 constexpr int SL_SLOTS = 512;              // workgroups per launch: two per CU
+constexpr int SL_MERGE_REG = 16;           // pass-1 partials per thread loaded at once in pass 2
 
 // Wait until at most `left` of this wave's memory loads are outstanding (vmcnt; the export
 // and LDS counters are left alone).  Loads complete in order for this counter.
@@ -137,12 +139,17 @@ __device__ __forceinline__ f32x4 sl_logits(const uint8_t* stage, int kt, const u
 // ----------------------------------------------------------------------------------------
 // Block pipeline shared by both passes: buffers 0/1 hold blocks b0, b0+1, ..; `step(b, buf)`
 // computes block b from its buffer.
+// sl_prime requests the first two blocks; sl_pipeline then runs the loop.
+template <bool F32>
+__device__ __forceinline__ void sl_prime(uint8_t* lds, const void* K, int64_t n, int G, int g, int b0, int b1) {
+    constexpr int KB = sl_keys<F32>();
+    sl_issue<F32>(lds, K, n, G, g, (int64_t)b0 * KB);
+    if (b0 + 1 < b1) sl_issue<F32>(lds + SL_STAGE, K, n, G, g, (int64_t)(b0 + 1) * KB);
+}
 template <bool F32, class Step>
 __device__ __forceinline__ void sl_pipeline(uint8_t* lds, const void* K, int64_t n, int G, int g,
                                             int b0, int b1, Step step) {
     constexpr int KB = sl_keys<F32>();
-    sl_issue<F32>(lds, K, n, G, g, (int64_t)b0 * KB);
-    if (b0 + 1 < b1) sl_issue<F32>(lds + SL_STAGE, K, n, G, g, (int64_t)(b0 + 1) * KB);
     for (int b = b0; b < b1; ++b) {
         uint8_t* buf = lds + ((b - b0) & 1) * SL_STAGE;
         if (b + 1 < b1) wait_vm<SL_LPB>();       // block b landed; block b + 1 may be in flight
@@ -237,6 +244,7 @@ __global__ __launch_bounds__(SL_THREADS, 4) void sal_rowstats(const void* __rest
             }
         }
     };
+    sl_prime<F32>(lds, K, n, G, g, b0, b1);
     sl_pipeline<F32>(lds, K, n, G, g, b0, b1, [&](int b, const uint8_t* buf) {
         const int64_t k0 = (int64_t)b * KB;
         const int64_t kend = k0 + KB < n ? k0 + KB : n;
@@ -274,45 +282,20 @@ __global__ __launch_bounds__(SL_THREADS, 4) void sal_rowstats(const void* __rest
     }
 }
 
-// merge: ML[g * rows + rho] = (M, 1/L).  16 threads per row read its block partials in
-// parallel: the row maximum first, then the rescaled sums.
-__global__ __launch_bounds__(256) void sal_merge(const float2* __restrict__ stats, int nkb,
-                                                 int total_rows, float2* __restrict__ ML) {
-    const int r = blockIdx.x * 16 + (threadIdx.x >> 4), k = threadIdx.x & 15;
-    const int rr = r < total_rows ? r : total_rows - 1;
-    const float2* s = stats + (int64_t)rr * nkb;
-    // max over this thread's partials (their loads all issue first), then the 16-lane max
-    float m = -INFINITY;
-#pragma unroll 8
-    for (int b = k; b < nkb; b += 16) m = fmaxf(m, s[b].x);
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, shfl_xor_f(m, off));
-    // sums rescaled to the row max (the partials are L1/L2 hits now)
-    float l = 0.f;
-    if (m != -INFINITY) {
-#pragma unroll 8
-        for (int b = k; b < nkb; b += 16) {
-            const float2 v = s[b];
-            l += v.x == -INFINITY ? 0.f : v.y * fast_exp(v.x - m);
-        }
-    }
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) l += shfl_xor_f(l, off);
-    if (k == 0 && r < total_rows) ML[r] = make_float2(m, 1.f / l);
-}
-
 // pass 2: s_part[g * N + t] = sum over the group's rows of exp(x - M) / L, t < N, for the
-// blocks [wgi * bpw, ..) of the coded keys of head g.  Grid (nw, G).
+// blocks [wgi * bpw, ..) of the coded keys of head g; (M, L) per row from the nw1 pass-1
+// partials.  Grid (nw, G).
 template <bool F32>
 __global__ __launch_bounds__(SL_THREADS, 4) void sal_colsum(const void* __restrict__ K,
                                                             const void* __restrict__ Qw,
                                                             int64_t n, int G, int H, int w,
-                                                            const float2* __restrict__ ML,
+                                                            const float2* __restrict__ stats, int nw1,
                                                             float* __restrict__ s_part, int bpw) {
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     constexpr int KB = sl_keys<F32>();
     constexpr int TPB = KB / 16;
     __shared__ float colsum[SL_WAVES][KB];
+    __shared__ float2 rowml[SL_WAVES * SL_MAX_RT * 16];   // (M, 1/L) of the head's rows
     const int wgi = blockIdx.x, g = blockIdx.y;
     const int64_t N = n - w;
     const int hpg = H / G, rows = hpg * w, nrt = (rows + 15) / 16;
@@ -327,17 +310,57 @@ __global__ __launch_bounds__(SL_THREADS, 4) void sal_colsum(const void* __restri
     for (int j = 0; j < SL_MAX_RT; ++j) {
         const int rt = wave + SL_WAVES * j;
         if (rt < nrt) sl_qfrag<F32>(Qw, H, w, hpg, g, rows, rt, qh[j], ql[j]);
+    }
+    // Row statistics of head g from the pass-1 partials (every workgroup of the head forms
+    // them): tpr threads per row, each over every tpr-th partial.  The partial loads issue
+    // together, before the first two key blocks are requested, so the two round trips overlap.
+    int tpr = 2;
+    while (tpr * 2 * rows <= SL_THREADS && tpr < 64) tpr *= 2;
+    const int r = threadIdx.x / tpr, h = threadIdx.x % tpr;
+    const bool live = r < rows;
+    const float2* st = stats + ((int64_t)g * rows + (live ? r : 0)) * nw1;
+    float2 part[SL_MERGE_REG];
+#pragma unroll
+    for (int i = 0; i < SL_MERGE_REG; ++i) {
+        const int b = h + tpr * i;
+        part[i] = st[b < nw1 ? b : 0];
+        if (!(b < nw1)) part[i].x = -INFINITY;
+    }
+    // The block loads are issued in asm after every compiler-visible load, so the compiler's
+    // waits for the partials (counted over its own loads only) can only over-wait.
+    sl_prime<F32>(lds, K, n, G, g, b0, b1);
+    {
+        float mm = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < SL_MERGE_REG; ++i) mm = fmaxf(mm, part[i].x);
+        for (int b = h + tpr * SL_MERGE_REG; b < nw1; b += tpr) mm = fmaxf(mm, st[b].x);
+        for (int off = 1; off < tpr; off <<= 1) mm = fmaxf(mm, shfl_xor_f(mm, off));
+        float ll = 0.f;
+        if (mm != -INFINITY) {
+#pragma unroll
+            for (int i = 0; i < SL_MERGE_REG; ++i)
+                ll += part[i].x == -INFINITY ? 0.f : part[i].y * fast_exp(part[i].x - mm);
+            for (int b = h + tpr * SL_MERGE_REG; b < nw1; b += tpr) {
+                const float2 v = st[b];
+                ll += v.x == -INFINITY ? 0.f : v.y * fast_exp(v.x - mm);
+            }
+        }
+        for (int off = 1; off < tpr; off <<= 1) ll += shfl_xor_f(ll, off);
+        if (live && h == 0) rowml[r] = make_float2(mm, 1.f / ll);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < SL_MAX_RT; ++j) {
+        const int rt = wave + SL_WAVES * j;
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const int rho = rt * 16 + (lane >> 4) * 4 + v;
             const bool ok = rt < nrt && rho < rows;
-            const float2 mlv = ML[(int64_t)g * rows + (ok ? rho : 0)];   // unconditional load
+            const float2 mlv = rowml[ok ? rho : 0];
             rm[j][v] = mlv.x * 1.4426950408889634f;          // log2 units
             rinv[j][v] = ok ? mlv.y : 0.f;                   // rows past `rows` weigh nothing
         }
     }
-    // (see pass 1) every compiler-visible load lands before the asm-issued block loads
-    wait_vm<0>();
     const float sl2 = 0.08838834764831845f * 1.4426950408889634f;   // log2(e) / sqrt(128)
 
     sl_pipeline<F32>(lds, K, n, G, g, b0, b1, [&](int b, const uint8_t* buf) {
@@ -375,6 +398,7 @@ __global__ __launch_bounds__(SL_THREADS, 4) void sal_colsum(const void* __restri
 // pool: sbar[t] = (s_{t-2} + ... + s_{t+2}) / 5 with s_k = sum_g s_part[g][k] / (w H).  A
 // block of 256 tokens first forms s for its tokens and a 2-token halo on each side.
 constexpr int SP_T = 256;
+constexpr int SP_MAXG = 16;      // heads whose loads issue together
 __global__ __launch_bounds__(SP_T) void sal_pool(const float* __restrict__ s_part, int64_t N, int G,
                                                  float inv_wh, float* __restrict__ sbar) {
     __shared__ double sv[SP_T + 4];
@@ -383,8 +407,15 @@ __global__ __launch_bounds__(SP_T) void sal_pool(const float* __restrict__ s_par
         const int64_t k = t0 - 2 + i;
         double v = 0.0;
         if (k >= 0 && k < N) {
+            // the heads' loads all issue before the (fixed-order) sum
+            float part[SP_MAXG];
+#pragma unroll
+            for (int gg = 0; gg < SP_MAXG; ++gg) part[gg] = gg < G ? s_part[(int64_t)gg * N + k] : 0.f;
             float s = 0.f;
-            for (int gg = 0; gg < G; ++gg) s += s_part[(int64_t)gg * N + k];
+#pragma unroll
+            for (int gg = 0; gg < SP_MAXG; ++gg)
+                if (gg < G) s += part[gg];
+            for (int gg = SP_MAXG; gg < G; ++gg) s += s_part[(int64_t)gg * N + k];
             v = (double)(s * inv_wh);
         }
         sv[i] = v;
@@ -420,7 +451,7 @@ size_t salience_ws_bytes(const varrate_shape& sh) {
     const SalPlan p1 = sal_plan((sh.n + KB - 1) / KB, sh.G);
     const int64_t N = sh.n - sh.w;
     return align256((size_t)sh.G * rows * p1.nw * sizeof(float2)) +
-           align256((size_t)sh.G * rows * sizeof(float2)) + align256((size_t)sh.G * N * sizeof(float));
+           align256((size_t)sh.G * N * sizeof(float));
 }
 
 template <bool F32>
@@ -443,10 +474,7 @@ hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Q
     const SalPlan p2 = sal_plan((N + KB - 1) / KB, sh.G);
     float2* stats = (float2*)ws;
     ws += align256((size_t)sh.G * rows * p1.nw * sizeof(float2));
-    float2* ML = (float2*)ws;
-    ws += align256((size_t)sh.G * rows * sizeof(float2));
     float* s_part = (float*)ws;
-    const int tr = sh.G * rows;
     const bool bf = sh.dtype == VARRATE_BF16;
     hipError_t e = bf ? sal_attr<false>() : sal_attr<true>();
     if (e != hipSuccess) return e;
@@ -454,12 +482,10 @@ hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Q
     const size_t lds = 2 * SL_STAGE;
     if (bf) {
         sal_rowstats<false><<<g1, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, p1.bpw);
-        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, p1.nw, tr, ML);
-        sal_colsum<false><<<g2, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part, p2.bpw);
+        sal_colsum<false><<<g2, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, s_part, p2.bpw);
     } else {
         sal_rowstats<true><<<g1, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, p1.bpw);
-        sal_merge<<<(tr + 15) / 16, 256, 0, st>>>(stats, p1.nw, tr, ML);
-        sal_colsum<true><<<g2, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, ML, s_part, p2.bpw);
+        sal_colsum<true><<<g2, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, s_part, p2.bpw);
     }
     sal_pool<<<(unsigned)((N + SP_T - 1) / SP_T), SP_T, 0, st>>>(s_part, N, sh.G,
                                                                    1.0f / ((float)sh.w * (float)sh.H), sbar);
