@@ -1,5 +1,5 @@
 // Budgeted rank allocation (Sec. 3.2 Eq. (5), Algorithm 1 water-filling, integer ranks),
-// exact integer arithmetic in a single workgroup, plus the chunk-local storage order.
+// exact integer arithmetic, plus the chunk-local storage order.
 //
 // Weights.  u_t = 1 + floor(2^24 (sbar_t - min) / (max - min)) with each fp64 operation
 // rounded once (all equal when max == min), so the ranks are a function of the fp32 input.
@@ -18,27 +18,107 @@
 // most-significant-digit radix select (11-bit digits, common-prefix skipping) over the
 // 2 x 64-bit key.  All arithmetic is integer: the ranks are bit-exact and deterministic.
 //
-// Every pass over the N tokens keeps eight independent loads in flight per thread.  The
-// selection's first digit comes from phi < Q directly; when the chosen bucket holds at most
-// 2048 candidates they are gathered into LDS and the remaining digits never touch memory.
+// Kernel chain.  Every pass over the tokens is a grid of 256-thread workgroups holding 1024
+// consecutive tokens each (wave w: the 256 tokens of one storage chunk, four coalesced loads
+// per lane).  The small scans between passes (4097 coarse bins, 4096 fine bins, 2048 digit
+// bins) are repeated by every workgroup of the pass that needs them, which costs less than
+// a launch of their own; workgroup 0 records the results for the later kernels.
+//   al_minmax   per-workgroup min / max of sbar; clears the histograms and counters
+//   al_weights  u, coarse histogram of u >> 12 (count, sum of the low bits), max u
+//   al_fine     coarse scan -> the bin holding tau_lo; counts of the low bits inside it
+//   al_floors   fine scan -> tau_lo, k, Q, M; floors, keys phi, sum of floors, histogram
+//               of phi's top 11 significant bits
+//   al_gather   rho; the digit bucket holding the rho-th largest key; its candidates
+//   al_select   (one workgroup) radix narrowing of the candidates to the exact threshold
+//   al_final    final ranks and per-chunk sums
+//   al_scan     (one workgroup) chunk offsets
 #include "vr_internal.h"
 
 namespace vr {
 
-constexpr int AL_T = 1024;
-constexpr int AL_W = AL_T / 64;
+constexpr int AK_T = 256;                  // threads per workgroup of a token pass
+constexpr int AK_PER = CHUNK / 64;         // tokens per lane (a wave holds one chunk)
+constexpr int AK_TOK = AK_T * AK_PER;      // tokens per workgroup
+constexpr int AL_T = 1024;                 // threads of the one-workgroup kernels
 constexpr int CBITS = 12;
-constexpr int NBIN = (1 << CBITS) + 1;     // coarse bins of u (u <= 2^24 + 1)
+constexpr int NCB = (1 << CBITS) + 1;      // coarse bins of u (u <= 2^24 + 1)
+constexpr int NFB = 1 << CBITS;            // fine bins
+constexpr int NDB = 2048;                  // selection digit bins (11 bits)
+constexpr int SEL_CAP = 2048;              // candidates the selection finishes in LDS
 constexpr uint64_t CAPPED = 1ull << 63;
+static_assert(AK_PER * 64 == CHUNK, "a wave holds one storage chunk");
 
+// Device-side state of one allocation (in the workspace, cleared by al_minmax).
+struct AlCtl {
+    unsigned long long fsum;     // sum of the floors (atomic)
+    uint32_t umax;               // (atomic max)
+    uint32_t ncand;              // gathered candidates (atomic)
+    // water level (coarse: al_fine, fine: al_floors)
+    int bbest, pad0;
+    unsigned long long cge_next, slt_b;
+    unsigned long long Q;
+    long long M, kcap;
+    uint32_t tau_lo;
+    int sh0;                     // shift of the first selection digit
+    // selection (al_gather, then al_select)
+    unsigned long long pv, pm, T_hi, T_lo;
+    long long need;
+    int done, any;
+};
+
+// Workspace: [coarse low sums (u64) | coarse counts | fine counts | digit counts | ctl]
+// (the cleared region), then partial min/max, u, phi, candidates.
+struct AlWs {
+    unsigned long long* c_low;
+    uint32_t* c_cnt;
+    uint32_t* f_cnt;
+    uint32_t* d_cnt;
+    AlCtl* ctl;
+    uint32_t* clear;             // start of the cleared region, clear_words 32-bit words
+    int clear_words;
+    float2* mm;
+    uint32_t* u;
+    uint64_t* phi;
+    uint64_t* cand;              // 2 x u64 per candidate (hi = phi, lo = (u, ~t))
+};
+constexpr int NCB_PAD = (NCB + 3) & ~3;
+
+static AlWs al_ws(uint8_t* ws, int64_t N) {
+    AlWs w;
+    const int64_t nwg = (N + AK_TOK - 1) / AK_TOK;
+    uint8_t* p = ws;
+    w.clear = (uint32_t*)p;
+    w.c_low = (unsigned long long*)p; p += NCB_PAD * 8;
+    w.c_cnt = (uint32_t*)p;           p += NCB_PAD * 4;
+    w.f_cnt = (uint32_t*)p;           p += NFB * 4;
+    w.d_cnt = (uint32_t*)p;           p += NDB * 4;
+    w.ctl = (AlCtl*)p;                p += (sizeof(AlCtl) + 15) & ~(size_t)15;
+    w.clear_words = (int)((p - ws) / 4);
+    p = ws + align256(p - ws);
+    w.mm = (float2*)p;                p += align256((size_t)nwg * sizeof(float2));
+    w.u = (uint32_t*)p;               p += align256((size_t)N * 4);
+    w.phi = (uint64_t*)p;             p += align256((size_t)N * 8);
+    w.cand = (uint64_t*)p;
+    return w;
+}
+
+size_t allocate_ws_bytes(const varrate_shape& sh) {
+    const int64_t N = sh.n - sh.w;
+    const int64_t nwg = (N + AK_TOK - 1) / AK_TOK;
+    size_t b = align256(NCB_PAD * 12 + NFB * 4 + NDB * 4 + ((sizeof(AlCtl) + 15) & ~(size_t)15));
+    b += align256((size_t)nwg * sizeof(float2)) + align256((size_t)N * 4) + align256((size_t)N * 8);
+    return b + align256((size_t)N * 16);
+}
+
+// ---- workgroup primitives ----------------------------------------------------------------
 template <typename T> __device__ __forceinline__ T wave_sum(T v) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
     return v;
 }
 
-// Block exclusive scan of one value per thread; `tot` receives the block total.
-template <typename T>
+// Exclusive scan of one value per thread over NT threads; `tot` receives the total.
+template <int NT, typename T>
 __device__ T block_exscan(T v, T* wtot, T& tot) {
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     T x = v;
@@ -50,7 +130,8 @@ __device__ T block_exscan(T v, T* wtot, T& tot) {
     if (lane == 63) wtot[wid] = x;
     __syncthreads();
     T pre = 0, all = 0;
-    for (int i = 0; i < AL_W; ++i) {
+#pragma unroll
+    for (int i = 0; i < NT / 64; ++i) {
         T wv = wtot[i];
         if (i < wid) pre += wv;
         all += wv;
@@ -60,28 +141,29 @@ __device__ T block_exscan(T v, T* wtot, T& tot) {
     return pre + x - v;
 }
 
-template <typename T, typename Op>
+template <int NT, typename T, typename Op>
 __device__ T block_reduce(T v, T* scratch, Op op) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) v = op(v, __shfl_xor(v, off, 64));
     if ((threadIdx.x & 63) == 0) scratch[threadIdx.x >> 6] = v;
     __syncthreads();
     T r = scratch[0];
-    for (int i = 1; i < AL_W; ++i) r = op(r, scratch[i]);
+#pragma unroll
+    for (int i = 1; i < NT / 64; ++i) r = op(r, scratch[i]);
     __syncthreads();
     return r;
 }
 
-// In-place exclusive scan of n (<= 4 * AL_T + 4) entries held in LDS; returns the total.
-template <typename T>
+// In-place exclusive scan of n entries held in LDS; returns the total.
+template <int NT, typename T>
 __device__ T lds_exscan(T* a, int n, T* wtot) {
-    const int per = (n + AL_T - 1) / AL_T;
+    const int per = (n + NT - 1) / NT;
     const int b = threadIdx.x * per;
     T loc = 0;
     for (int i = 0; i < per; ++i)
         if (b + i < n) loc += a[b + i];
     T tot;
-    T pre = block_exscan<T>(loc, wtot, tot);
+    T pre = block_exscan<NT, T>(loc, wtot, tot);
     for (int i = 0; i < per; ++i)
         if (b + i < n) {
             T v = a[b + i];
@@ -92,55 +174,349 @@ __device__ T lds_exscan(T* a, int n, T* wtot) {
     return tot;
 }
 
+__device__ __forceinline__ uint64_t lo_key(uint32_t u, int64_t t) {
+    return ((uint64_t)u << 24) | (uint64_t)(0xFFFFFFu - (uint32_t)t);
+}
+
+// Token of lane slot k in this workgroup: wave w holds tokens [256 w, 256 w + 256).
+__device__ __forceinline__ int64_t al_tok(int k) {
+    return (int64_t)blockIdx.x * AK_TOK + (threadIdx.x >> 6) * CHUNK + 64 * k + (threadIdx.x & 63);
+}
+
+// The u of one token (see the header); lo = min, range = max - min.
+__device__ __forceinline__ uint32_t weight_of(float s, bool flat, double lo, double range) {
+    if (flat) return (1u << 24) + 1u;
+    const double num = (double)s - lo;
+    double shat = num / range;
+    // non-finite inputs cannot index past the histograms
+    shat = shat >= 0.0 ? (shat <= 1.0 ? shat : 1.0) : 0.0;
+    return 1u + (uint32_t)floor(shat * 16777216.0);
+}
+
+// ---- 1. min / max; clear the histograms and counters --------------------------------------
+__global__ __launch_bounds__(AK_T) void al_minmax(const float* __restrict__ sbar, int64_t N,
+                                                  float2* __restrict__ mm, uint32_t* __restrict__ clear,
+                                                  int clear_words) {
+    __shared__ float red[AK_T / 64];
+    const int per = (clear_words + gridDim.x - 1) / gridDim.x;
+    const int c0 = blockIdx.x * per, c1 = c0 + per < clear_words ? c0 + per : clear_words;
+    for (int i = c0 + threadIdx.x; i < c1; i += AK_T) clear[i] = 0;
+    float v[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        v[k] = sbar[t < N ? t : N - 1];
+    }
+    float mn = v[0], mx = v[0];
+#pragma unroll
+    for (int k = 1; k < AK_PER; ++k) { mn = fminf(mn, v[k]); mx = fmaxf(mx, v[k]); }
+    mn = block_reduce<AK_T>(mn, red, [](float a, float b) { return fminf(a, b); });
+    mx = block_reduce<AK_T>(mx, red, [](float a, float b) { return fmaxf(a, b); });
+    if (threadIdx.x == 0) mm[blockIdx.x] = make_float2(mn, mx);
+}
+
+// Global min / max from the per-workgroup partials (exact, so any order gives the same).
+__device__ __forceinline__ float2 al_range(const float2* __restrict__ mm, int nwg, float* red) {
+    float mn = INFINITY, mx = -INFINITY;
+    for (int i = threadIdx.x; i < nwg; i += AK_T) {
+        const float2 p = mm[i];
+        mn = fminf(mn, p.x);
+        mx = fmaxf(mx, p.y);
+    }
+    mn = block_reduce<AK_T>(mn, red, [](float a, float b) { return fminf(a, b); });
+    mx = block_reduce<AK_T>(mx, red, [](float a, float b) { return fmaxf(a, b); });
+    return make_float2(mn, mx);
+}
+
+// ---- 2. weights and the coarse histogram ----------------------------------------------------
+__global__ __launch_bounds__(AK_T) void al_weights(const float* __restrict__ sbar, int64_t N,
+                                                   const float2* __restrict__ mm, int nwg,
+                                                   uint32_t* __restrict__ u_ws,
+                                                   unsigned long long* __restrict__ c_low,
+                                                   uint32_t* __restrict__ c_cnt, AlCtl* __restrict__ ctl) {
+    __shared__ uint32_t cnt[NCB_PAD], low[NCB_PAD];
+    __shared__ float red[AK_T / 64];
+    __shared__ uint32_t redu[AK_T / 64];
+    float s[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        s[k] = sbar[t < N ? t : N - 1];
+    }
+    for (int i = threadIdx.x; i < NCB_PAD; i += AK_T) { cnt[i] = 0; low[i] = 0; }
+    const float2 r = al_range(mm, nwg, red);     // (its barriers also order the clearing)
+    const bool flat = !(r.y > r.x);
+    const double lo = (double)r.x, range = (double)r.y - lo;
+    uint32_t umax = 0;
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        if (t < N) {
+            const uint32_t u = weight_of(s[k], flat, lo, range);
+            u_ws[t] = u;
+            umax = u > umax ? u : umax;
+            atomicAdd(&cnt[u >> CBITS], 1u);
+            atomicAdd(&low[u >> CBITS], u & ((1u << CBITS) - 1));
+        }
+    }
+    umax = block_reduce<AK_T>(umax, redu, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+    if (threadIdx.x == 0) atomicMax(&ctl->umax, umax);
+    for (int i = threadIdx.x; i < NCB; i += AK_T) {
+        const uint32_t c = cnt[i];
+        if (c) {
+            atomicAdd(&c_cnt[i], c);
+            atomicAdd(&c_low[i], (unsigned long long)low[i]);
+        }
+    }
+}
+
+// ---- 3. coarse level; fine histogram ----------------------------------------------------------
+__global__ __launch_bounds__(AK_T) void al_fine(int64_t N, int64_t B, int r_min, int R,
+                                                const uint32_t* __restrict__ u_ws,
+                                                const unsigned long long* __restrict__ c_low,
+                                                const uint32_t* __restrict__ c_cnt,
+                                                uint32_t* __restrict__ f_cnt, AlCtl* __restrict__ ctl) {
+    __shared__ uint32_t cnt[NCB_PAD];
+    __shared__ unsigned long long sm[NCB_PAD];
+    __shared__ uint32_t wt32[AK_T / 64];
+    __shared__ unsigned long long wt64[AK_T / 64];
+    uint32_t u[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        u[k] = u_ws[t < N ? t : N - 1];
+    }
+    const uint32_t umax = ctl->umax;
+    const int nb = (int)(umax >> CBITS) + 1;
+    for (int i = threadIdx.x; i <= nb; i += AK_T) {
+        const uint32_t c = i < nb ? c_cnt[i] : 0u;
+        cnt[i] = c;
+        sm[i] = i < nb ? (unsigned long long)c * ((uint64_t)i << CBITS) + c_low[i] : 0ull;
+    }
+    __syncthreads();
+    // exclusive prefixes over bins 0..nb (entry nb = totals)
+    lds_exscan<AK_T, uint32_t>(cnt, nb + 1, wt32);
+    lds_exscan<AK_T, unsigned long long>(sm, nb + 1, wt64);
+    const uint64_t Dr = (uint64_t)(R - r_min);
+    const uint64_t E = (uint64_t)(B - N * (int64_t)r_min);
+    // the predicate at coarse edges tau_b = max(1, b << 12): c_ge = N - cnt_ex[b], s_lt = sm_ex[b]
+    int bbest = 0;
+    for (int b = threadIdx.x; b < nb; b += AK_T) {
+        const uint64_t tau = b == 0 ? 1 : ((uint64_t)b << CBITS);
+        const uint64_t cge = (uint64_t)N - cnt[b];
+        const uint64_t slt = sm[b];
+        if (Dr * (tau * cge + slt) >= E * tau) bbest = b > bbest ? b : bbest;
+    }
+    bbest = (int)block_reduce<AK_T, uint32_t>((uint32_t)bbest, wt32,
+                                              [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        ctl->bbest = bbest;
+        ctl->cge_next = (uint64_t)N - cnt[bbest + 1];   // tokens in bins above bbest
+        ctl->slt_b = sm[bbest];                         // sum of u in bins below bbest
+    }
+    __syncthreads();
+    // fine counts of the low 12 bits inside bin bbest (every u there is (bbest << 12) + f)
+    for (int i = threadIdx.x; i < NFB; i += AK_T) cnt[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k)
+        if (al_tok(k) < N && (int)(u[k] >> CBITS) == bbest) atomicAdd(&cnt[u[k] & (NFB - 1)], 1u);
+    __syncthreads();
+    for (int i = threadIdx.x; i < NFB; i += AK_T) {
+        const uint32_t c = cnt[i];
+        if (c) atomicAdd(&f_cnt[i], c);
+    }
+}
+
+// ---- 4. fine level; floors, keys and the first selection digit --------------------------------
+__global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_min, int R,
+                                                  const uint32_t* __restrict__ u_ws,
+                                                  const uint32_t* __restrict__ f_cnt,
+                                                  uint8_t* __restrict__ rank, uint64_t* __restrict__ phi_ws,
+                                                  uint32_t* __restrict__ d_cnt, AlCtl* __restrict__ ctl) {
+    __shared__ uint32_t cnt[NFB + 1];
+    __shared__ unsigned long long sm[NFB + 1];
+    __shared__ uint32_t wt32[AK_T / 64];
+    __shared__ unsigned long long wt64[AK_T / 64];
+    uint32_t u[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        u[k] = u_ws[t < N ? t : N - 1];
+    }
+    const uint32_t umax = ctl->umax;
+    const int bbest = ctl->bbest;
+    const uint64_t cge_next = ctl->cge_next, slt_b = ctl->slt_b;
+    const uint64_t base_tau = (uint64_t)bbest << CBITS;
+    for (int i = threadIdx.x; i <= NFB; i += AK_T) {
+        const uint32_t c = i < NFB ? f_cnt[i] : 0u;
+        cnt[i] = c;
+        sm[i] = (unsigned long long)c * (base_tau + (uint64_t)i);
+    }
+    __syncthreads();
+    lds_exscan<AK_T, uint32_t>(cnt, NFB + 1, wt32);
+    lds_exscan<AK_T, unsigned long long>(sm, NFB + 1, wt64);
+    const uint64_t Dr = (uint64_t)(R - r_min);
+    const uint64_t E = (uint64_t)(B - N * (int64_t)r_min);
+    const uint64_t fc_total = cnt[NFB];
+    const int f_lo = bbest == 0 ? 1 : 0;
+    const int f_hi = (int)(((uint64_t)umax - base_tau) < (uint64_t)(NFB - 1) ? (umax - base_tau) : (NFB - 1));
+    int fbest = f_lo;
+    for (int f = threadIdx.x; f <= f_hi; f += AK_T) {
+        if (f < f_lo) continue;
+        const uint64_t tau = base_tau + f;
+        const uint64_t cge = cge_next + fc_total - cnt[f];
+        const uint64_t slt = slt_b + sm[f];
+        if (Dr * (tau * cge + slt) >= E * tau) fbest = f > fbest ? f : fbest;
+    }
+    fbest = (int)block_reduce<AK_T, uint32_t>((uint32_t)fbest, wt32,
+                                              [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+    const uint32_t tau_lo = (uint32_t)(base_tau + fbest);
+    const int64_t kcap = (int64_t)(cge_next + fc_total - cnt[fbest + 1]);
+    const uint64_t Q = slt_b + sm[fbest + 1];
+    const int64_t M = B - (int64_t)R * kcap - (int64_t)r_min * (N - kcap);
+    const double invQ = 1.0 / (double)Q;
+    // first selection digit: phi < Q, so its top 11 significant bits need no range pass
+    const uint64_t qm1 = Q > 1 ? Q - 1 : 1;
+    const int qb = 64 - __clzll((long long)qm1);
+    const int sh0 = qb > 11 ? qb - 11 : 0;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        ctl->tau_lo = tau_lo;
+        ctl->kcap = kcap;
+        ctl->Q = Q;
+        ctl->M = M;
+        ctl->sh0 = sh0;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < NDB; i += AK_T) cnt[i] = 0;
+    __syncthreads();
+
+    unsigned long long fsum = 0;
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        if (t >= N) continue;
+        uint32_t base;
+        uint64_t phi;
+        if (u[k] > tau_lo) {
+            base = (uint32_t)R;
+            phi = CAPPED;
+        } else {
+            // num < 2^52 and Q < 2^45 are exact in fp64; the reciprocal quotient is within
+            // one unit of floor(num / Q) and the integer remainder corrects it exactly
+            const uint64_t num = (uint64_t)u[k] * (uint64_t)M;
+            int64_t f = (int64_t)((double)num * invQ);
+            int64_t rem = (int64_t)num - f * (int64_t)Q;
+            if (rem < 0) { f -= 1; rem += (int64_t)Q; }
+            if (rem >= (int64_t)Q) { f += 1; rem -= (int64_t)Q; }
+            phi = (uint64_t)rem;
+            base = (uint32_t)(r_min + f);
+            atomicAdd(&cnt[(phi >> sh0) & (NDB - 1)], 1u);
+        }
+        rank[t] = (uint8_t)base;
+        phi_ws[t] = phi;
+        fsum += base;
+    }
+    fsum = block_reduce<AK_T, unsigned long long>(fsum, wt64,
+                                                  [](unsigned long long a, unsigned long long b) { return a + b; });
+    if (threadIdx.x == 0) atomicAdd(&ctl->fsum, fsum);
+    for (int i = threadIdx.x; i < NDB; i += AK_T) {
+        const uint32_t c = cnt[i];
+        if (c) atomicAdd(&d_cnt[i], c);
+    }
+}
+
+// ---- 5. the digit bucket holding the rho-th largest key; gather its candidates -------------------
+__global__ __launch_bounds__(AK_T) void al_gather(int64_t N, int64_t B, const uint32_t* __restrict__ u_ws,
+                                                  const uint64_t* __restrict__ phi_ws,
+                                                  const uint32_t* __restrict__ d_cnt,
+                                                  uint64_t* __restrict__ cand, AlCtl* __restrict__ ctl) {
+    __shared__ uint32_t wt32[AK_T / 64];
+    __shared__ int s_hit;
+    __shared__ uint32_t s_above, s_hcnt, s_n, s_base;
+    uint64_t phi[AK_PER];
+    uint32_t u[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        phi[k] = phi_ws[t < N ? t : N - 1];
+        u[k] = u_ws[t < N ? t : N - 1];
+    }
+    const int64_t rho = B - (int64_t)ctl->fsum;
+    const int sh0 = ctl->sh0;
+    if (threadIdx.x == 0) { s_hit = -1; s_n = 0; }
+    // descending digit order: thread i holds digits 2047 - 8 i .. 2040 - 8 i
+    constexpr int DPT = NDB / AK_T;
+    uint32_t c[DPT], loc = 0;
+#pragma unroll
+    for (int j = 0; j < DPT; ++j) { c[j] = d_cnt[NDB - 1 - DPT * threadIdx.x - j]; loc += c[j]; }
+    uint32_t tot;
+    uint32_t above = block_exscan<AK_T, uint32_t>(loc, wt32, tot);
+    if (rho > 0) {
+#pragma unroll
+        for (int j = 0; j < DPT; ++j) {
+            if ((int64_t)above < rho && rho <= (int64_t)(above + c[j])) {
+                s_hit = NDB - 1 - DPT * threadIdx.x - j;
+                s_above = above;
+                s_hcnt = c[j];
+            }
+            above += c[j];
+        }
+    }
+    __syncthreads();
+    const int hit = s_hit;
+    // rho <= 0 selects nothing; rho > 0 always lands in a bucket (rho < uncapped count)
+    const bool done0 = hit < 0 || (int64_t)s_hcnt == rho - (int64_t)s_above;
+    const uint64_t pv = hit < 0 ? 0 : (uint64_t)hit << sh0;
+    const uint64_t pm = ~((1ull << sh0) - 1);
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        ctl->any = rho > 0 && hit >= 0;
+        ctl->need = hit < 0 ? 0 : rho - (int64_t)s_above;
+        ctl->pv = pv;
+        ctl->pm = pm;
+        ctl->done = done0;
+        ctl->T_hi = hit < 0 ? ~0ull : pv;      // the whole bucket is taken when done here
+        ctl->T_lo = 0;
+    }
+    if (done0) return;
+    // candidates of the bucket: a workgroup-local slot first, then one global reservation
+    uint32_t slot[AK_PER];
+    bool mine[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        mine[k] = al_tok(k) < N && phi[k] != CAPPED && (phi[k] & pm) == pv;
+        if (mine[k]) slot[k] = atomicAdd(&s_n, 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0 && s_n) s_base = atomicAdd(&ctl->ncand, s_n);
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k)
+        if (mine[k]) {
+            const uint64_t i = (uint64_t)(s_base + slot[k]);
+            cand[2 * i] = phi[k];
+            cand[2 * i + 1] = lo_key(u[k], al_tok(k));
+        }
+}
+
+// ---- 6. radix narrowing of the candidates (one workgroup) ----------------------------------------
 struct SelState {
     uint64_t pv, pm;   // fixed prefix value / mask of the field being narrowed
     uint64_t T_hi, T_lo;
     int64_t need;
     int phase;         // 0: narrowing phi, 1: narrowing (u, ~t)
     int done;
-    int ncand;         // candidates gathered into LDS
 };
 
-__device__ __forceinline__ uint64_t lo_key(uint32_t u, int64_t t) {
-    return ((uint64_t)u << 24) | (uint64_t)(0xFFFFFFu - (uint32_t)t);
-}
-
-// Visit tokens t = tid, tid + AL_T, ... with U independent loads in flight per thread.
-template <int U, class Load, class Proc>
-__device__ __forceinline__ void sweep(int64_t N, Load load, Proc proc) {
-    for (int64_t b = 0; b < N; b += (int64_t)U * AL_T) {
-        decltype(load((int64_t)0)) v[U];
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t t = b + (int64_t)k * AL_T + threadIdx.x;
-            if (t < N) v[k] = load(t);
-        }
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t t = b + (int64_t)k * AL_T + threadIdx.x;
-            if (t < N) proc(t, v[k]);
-        }
-    }
-}
-
-struct PhiU {
-    uint64_t phi;
-    uint32_t u;
-};
-
-struct Fin {
-    uint64_t phi;
-    uint32_t u;
-    uint32_t r;
-};
-
-// Most-significant-digit radix narrowing of the selection threshold over the candidates
-// enumerated by visit(f) (f(hi, lo) per uncapped candidate), starting from `sel`.
+// Most-significant-digit narrowing of the threshold over the candidates enumerated by
+// visit(f) (f(hi, lo) per candidate), starting from `sel`.
 template <class Visit>
 __device__ void radix_narrow(Visit visit, SelState& sel, uint32_t* cnt, uint32_t* wtot32,
                              unsigned long long* wtot64) {
     const int tid = threadIdx.x;
-    while (!sel.done) {
+    // every round fixes at least one more bit of the field or ends the phase, so two 64-bit
+    // fields finish within 2 * 65 rounds; the bound only guards against a broken invariant
+    for (int round = 0; round < 2 * 65 && !sel.done; ++round) {
         const int phase = sel.phase;
         const uint64_t pv = sel.pv, pm = sel.pm, T_hi = sel.T_hi;
         auto field = [&](uint64_t hi, uint64_t lo, uint64_t& f) -> bool {
@@ -160,8 +536,8 @@ __device__ void radix_narrow(Visit visit, SelState& sel, uint32_t* cnt, uint32_t
                 fmx = f > fmx ? f : fmx;
             }
         });
-        fmn = block_reduce<unsigned long long>(fmn, wtot64, [](unsigned long long a, unsigned long long b) { return a < b ? a : b; });
-        fmx = block_reduce<unsigned long long>(fmx, wtot64, [](unsigned long long a, unsigned long long b) { return a > b ? a : b; });
+        fmn = block_reduce<AL_T, unsigned long long>(fmn, wtot64, [](unsigned long long a, unsigned long long b) { return a < b ? a : b; });
+        fmx = block_reduce<AL_T, unsigned long long>(fmx, wtot64, [](unsigned long long a, unsigned long long b) { return a > b ? a : b; });
         if (fmn == fmx) {
             if (tid == 0) {
                 if (phase == 0) {
@@ -187,7 +563,7 @@ __device__ void radix_narrow(Visit visit, SelState& sel, uint32_t* cnt, uint32_t
         const int d0 = 2047 - 2 * tid, d1 = d0 - 1;
         const uint32_t c0 = cnt[d0], c1 = cnt[d1];
         uint32_t tot;
-        const uint32_t above0 = block_exscan<uint32_t>(c0 + c1, wtot32, tot);
+        const uint32_t above0 = block_exscan<AL_T, uint32_t>(c0 + c1, wtot32, tot);
         const int64_t need = sel.need;
         __syncthreads();
         int hit = -1;
@@ -211,258 +587,107 @@ __device__ void radix_narrow(Visit visit, SelState& sel, uint32_t* cnt, uint32_t
     }
 }
 
-constexpr int SEL_CAP = 2048;    // candidates the selection can finish in LDS
-
-__global__ __launch_bounds__(AL_T) void alloc_kernel(const float* __restrict__ sbar, int64_t N,
-                                                      int64_t B, int r_min, int R,
-                                                      uint32_t* __restrict__ u_ws,
-                                                      uint64_t* __restrict__ phi_ws,
-                                                      uint8_t* __restrict__ rank,
-                                                      uint32_t* __restrict__ chunk_off,
-                                                      int n_chunks) {
-    __shared__ uint32_t cnt[NBIN + 1];
-    __shared__ unsigned long long sm[NBIN + 1];
-    __shared__ unsigned long long wtot64[AL_W];
-    __shared__ uint32_t wtot32[AL_W];
-    __shared__ float redf[AL_W];
+__global__ __launch_bounds__(AL_T) void al_select(const uint64_t* __restrict__ cand, AlCtl* __restrict__ ctl) {
+    __shared__ uint32_t cnt[2048];
+    __shared__ unsigned long long chi[SEL_CAP], clo[SEL_CAP];
+    __shared__ unsigned long long wtot64[AL_T / 64];
+    __shared__ uint32_t wtot32[AL_T / 64];
     __shared__ SelState sel;
+    if (ctl->done) return;
     const int tid = threadIdx.x;
-    constexpr int U = 8;
-
-    // ---- 1. min / max of the pooled salience
-    float mn = INFINITY, mx = -INFINITY;
-    sweep<U>(N, [&](int64_t t) { return sbar[t]; }, [&](int64_t, float s) {
-        mn = fminf(mn, s);
-        mx = fmaxf(mx, s);
-    });
-    mn = block_reduce<float>(mn, redf, [](float a, float b) { return fminf(a, b); });
-    mx = block_reduce<float>(mx, redf, [](float a, float b) { return fmaxf(a, b); });
-
-    // ---- 2. integer weights + coarse histogram (count, sum) of u >> 12
-    for (int i = tid; i <= NBIN; i += AL_T) { cnt[i] = 0; sm[i] = 0; }
-    __syncthreads();
-    const bool flat = !(mx > mn);
-    const double lo = (double)mn;
-    const double range = (double)mx - lo;
-    uint32_t umax = 0;
-    sweep<U>(N, [&](int64_t t) { return sbar[t]; }, [&](int64_t t, float s) {
-        uint32_t u;
-        if (flat) {
-            u = (1u << 24) + 1u;
-        } else {
-            const double num = (double)s - lo;
-            double shat = num / range;
-            // non-finite inputs cannot index past the histograms
-            shat = shat >= 0.0 ? (shat <= 1.0 ? shat : 1.0) : 0.0;
-            u = 1u + (uint32_t)floor(shat * 16777216.0);
-        }
-        u_ws[t] = u;
-        umax = u > umax ? u : umax;
-        atomicAdd(&cnt[u >> CBITS], 1u);
-        atomicAdd(&sm[u >> CBITS], (unsigned long long)u);
-    });
-    umax = block_reduce<uint32_t>(umax, wtot32, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
-    __syncthreads();
-
-    const uint64_t Dr = (uint64_t)(R - r_min);
-    const uint64_t E = (uint64_t)(B - N * (int64_t)r_min);
-    const int nb = (int)(umax >> CBITS) + 1;
-    // exclusive prefixes over bins 0..nb (entry nb = totals)
-    lds_exscan<uint32_t>(cnt, nb + 1, wtot32);
-    lds_exscan<unsigned long long>(sm, nb + 1, wtot64);
-    // P'(tau) at coarse edges tau_b = max(1, b << 12): c_ge = N - cnt_ex[b], s_lt = sm_ex[b]
-    int bbest = 0;
-    for (int b = tid; b < nb; b += AL_T) {
-        const uint64_t tau = b == 0 ? 1 : ((uint64_t)b << CBITS);
-        const uint64_t cge = (uint64_t)N - cnt[b];
-        const uint64_t slt = sm[b];
-        if (Dr * (tau * cge + slt) >= E * tau) bbest = b > bbest ? b : bbest;
-    }
-    bbest = (int)block_reduce<uint32_t>((uint32_t)bbest, wtot32,
-                                        [](uint32_t a, uint32_t b) { return a > b ? a : b; });
-    const uint64_t cge_next = (uint64_t)N - cnt[bbest + 1];   // tokens in bins above bbest
-    const uint64_t slt_b = sm[bbest];                          // sum of u in bins below bbest
-    __syncthreads();
-
-    // ---- 3. fine histogram of the low 12 bits inside bin bbest
-    for (int i = tid; i <= NBIN; i += AL_T) { cnt[i] = 0; sm[i] = 0; }
-    __syncthreads();
-    sweep<U>(N, [&](int64_t t) { return u_ws[t]; }, [&](int64_t, uint32_t u) {
-        if ((int)(u >> CBITS) == bbest) {
-            atomicAdd(&cnt[u & ((1u << CBITS) - 1)], 1u);
-            atomicAdd(&sm[u & ((1u << CBITS) - 1)], (unsigned long long)u);
-        }
-    });
-    __syncthreads();
-    const int nf = 1 << CBITS;
-    lds_exscan<uint32_t>(cnt, nf + 1, wtot32);
-    lds_exscan<unsigned long long>(sm, nf + 1, wtot64);
-    const uint64_t fc_total = cnt[nf];
-    const uint64_t base_tau = (uint64_t)bbest << CBITS;
-    const int f_lo = bbest == 0 ? 1 : 0;
-    const int f_hi = (int)(((uint64_t)umax - base_tau) < (uint64_t)(nf - 1) ? (umax - base_tau) : (nf - 1));
-    int fbest = f_lo;
-    for (int f = tid; f <= f_hi; f += AL_T) {
-        if (f < f_lo) continue;
-        const uint64_t tau = base_tau + f;
-        const uint64_t cge = cge_next + fc_total - cnt[f];
-        const uint64_t slt = slt_b + sm[f];
-        if (Dr * (tau * cge + slt) >= E * tau) fbest = f > fbest ? f : fbest;
-    }
-    fbest = (int)block_reduce<uint32_t>((uint32_t)fbest, wtot32,
-                                        [](uint32_t a, uint32_t b) { return a > b ? a : b; });
-    const uint32_t tau_lo = (uint32_t)(base_tau + fbest);
-    const int64_t kcap = (int64_t)(cge_next + fc_total - cnt[fbest + 1]);
-    const uint64_t Q = slt_b + sm[fbest + 1];
-    const int64_t M = B - (int64_t)R * kcap - (int64_t)r_min * (N - kcap);
-    const double invQ = 1.0 / (double)Q;
-    __syncthreads();
-
-    // ---- 4. floors and fractional keys
-    unsigned long long fsum = 0;
-    sweep<U>(N, [&](int64_t t) { return u_ws[t]; }, [&](int64_t t, uint32_t u) {
-        uint32_t base;
-        uint64_t phi;
-        if (u > tau_lo) {
-            base = (uint32_t)R;
-            phi = CAPPED;
-        } else {
-            // num < 2^52 and Q < 2^45 are exact in fp64; the reciprocal quotient is within
-            // one unit of floor(num / Q) and the integer remainder corrects it exactly
-            const uint64_t num = (uint64_t)u * (uint64_t)M;
-            int64_t f = (int64_t)((double)num * invQ);
-            int64_t rem = (int64_t)num - f * (int64_t)Q;
-            if (rem < 0) { f -= 1; rem += (int64_t)Q; }
-            if (rem >= (int64_t)Q) { f += 1; rem -= (int64_t)Q; }
-            phi = (uint64_t)rem;
-            base = (uint32_t)(r_min + f);
-        }
-        rank[t] = (uint8_t)base;
-        phi_ws[t] = phi;
-        fsum += base;
-    });
-    fsum = block_reduce<unsigned long long>(fsum, wtot64,
-                                            [](unsigned long long a, unsigned long long b) { return a + b; });
-    const int64_t rho = B - (int64_t)fsum;
-
-    // ---- 5. select the rho largest (phi, u, -t) keys among uncapped tokens
-    auto load_pu = [&](int64_t t) { return PhiU{phi_ws[t], u_ws[t]}; };
     if (tid == 0) {
-        sel.pv = 0; sel.pm = 0; sel.T_hi = ~0ull; sel.T_lo = ~0ull;
-        sel.need = rho; sel.phase = 0; sel.done = rho <= 0; sel.ncand = 0;
+        sel.pv = ctl->pv; sel.pm = ctl->pm; sel.need = ctl->need;
+        sel.T_hi = ~0ull; sel.T_lo = ~0ull; sel.phase = 0; sel.done = 0;
     }
-    __syncthreads();
-    if (!sel.done) {
-        // first digit: phi < Q, so its top 11 significant bits need no range pass
-        const uint64_t qm1 = Q > 1 ? Q - 1 : 1;
-        const int qb = 64 - __clzll((long long)qm1);
-        const int sh0 = qb > 11 ? qb - 11 : 0;
-        for (int i = tid; i < 2048; i += AL_T) cnt[i] = 0;
+    const int nc = (int)ctl->ncand;
+    if (nc <= SEL_CAP) {
+        for (int i = tid; i < nc; i += AL_T) { chi[i] = cand[2 * i]; clo[i] = cand[2 * i + 1]; }
         __syncthreads();
-        sweep<U>(N, [&](int64_t t) { return phi_ws[t]; }, [&](int64_t, uint64_t phi) {
-            if (phi != CAPPED) atomicAdd(&cnt[(phi >> sh0) & 2047], 1u);
-        });
+        radix_narrow([&](auto f) {
+            for (int i = tid; i < nc; i += AL_T) f(chi[i], clo[i]);
+        }, sel, cnt, wtot32, wtot64);
+    } else {
         __syncthreads();
-        const int d0 = 2047 - 2 * tid, d1 = d0 - 1;
-        const uint32_t c0 = cnt[d0], c1 = cnt[d1];
-        uint32_t tot;
-        const uint32_t above0 = block_exscan<uint32_t>(c0 + c1, wtot32, tot);
-        const int64_t need = sel.need;
-        __syncthreads();
-        const uint32_t above1 = above0 + c0;
-        int hit = -1;
-        uint32_t hit_above = 0, hit_cnt = 0;
-        if ((int64_t)above0 < need && need <= (int64_t)(above0 + c0)) { hit = d0; hit_above = above0; hit_cnt = c0; }
-        if ((int64_t)above1 < need && need <= (int64_t)(above1 + c1)) { hit = d1; hit_above = above1; hit_cnt = c1; }
-        if (hit >= 0) {
-            const int64_t nn = need - (int64_t)hit_above;
-            sel.need = nn;
-            sel.pv = (uint64_t)hit << sh0;
-            sel.pm = ~((1ull << sh0) - 1);
-            if ((int64_t)hit_cnt == nn) { sel.T_hi = sel.pv; sel.T_lo = 0; sel.done = 1; }
-            sel.ncand = (int)hit_cnt;
-        }
-        __syncthreads();
-        if (!sel.done && sel.ncand <= SEL_CAP) {
-            // gather the bucket's candidates into LDS and finish there
-            unsigned long long* chi = sm;
-            unsigned long long* clo = sm + SEL_CAP;
-            const uint64_t pv = sel.pv, pm = sel.pm;
-            __syncthreads();
-            if (tid == 0) sel.ncand = 0;
-            __syncthreads();
-            sweep<U>(N, load_pu, [&](int64_t t, PhiU x) {
-                if (x.phi != CAPPED && (x.phi & pm) == pv) {
-                    const int slot = atomicAdd(&sel.ncand, 1);
-                    chi[slot] = x.phi;
-                    clo[slot] = lo_key(x.u, t);
-                }
-            });
-            __syncthreads();
-            const int nc = sel.ncand;
-            radix_narrow([&](auto f) {
-                for (int i = tid; i < nc; i += AL_T) f(chi[i], clo[i]);
-            }, sel, cnt, wtot32, wtot64);
-        } else if (!sel.done) {
-            radix_narrow([&](auto f) {
-                sweep<U>(N, load_pu, [&](int64_t t, PhiU x) {
-                    if (x.phi != CAPPED) f(x.phi, lo_key(x.u, t));
-                });
-            }, sel, cnt, wtot32, wtot64);
-        }
-    }
-    const uint64_t T_hi = sel.T_hi, T_lo = sel.T_lo;
-    const bool any = rho > 0;
-
-    // ---- 6. final ranks and chunk sums
-    for (int i = tid; i < n_chunks; i += AL_T) cnt[i] = 0;
-    __syncthreads();
-    for (int64_t b = 0; b < N; b += (int64_t)U * AL_T) {
-        Fin v[U];
+        radix_narrow([&](auto f) {
+            for (int i0 = 0; i0 < nc; i0 += 4 * AL_T) {
+                uint64_t h[4], l[4];
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t t = b + (int64_t)k * AL_T + tid;
-            if (t < N) v[k] = Fin{phi_ws[t], u_ws[t], rank[t]};
-        }
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            const int64_t t = b + (int64_t)k * AL_T + tid;
-            uint32_t r = 0;
-            if (t < N) {
-                r = v[k].r;
-                if (any && v[k].phi != CAPPED) {
-                    const bool take = v[k].phi > T_hi || (v[k].phi == T_hi && lo_key(v[k].u, t) >= T_lo);
-                    if (take) {
-                        r += 1;
-                        rank[t] = (uint8_t)r;
-                    }
+                for (int k = 0; k < 4; ++k) {
+                    const int i = i0 + k * AL_T + tid;
+                    if (i < nc) { h[k] = cand[2 * i]; l[k] = cand[2 * i + 1]; }
                 }
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (i0 + k * AL_T + tid < nc) f(h[k], l[k]);
             }
-            // a wave covers 64 consecutive tokens, all inside one 256-token chunk
-            const uint32_t ws = wave_sum(r);
-            const int64_t tw = b + (int64_t)k * AL_T + (tid & ~63);
-            if ((tid & 63) == 0 && tw < N) atomicAdd(&cnt[tw >> 8], ws);
-        }
+        }, sel, cnt, wtot32, wtot64);
     }
-    __syncthreads();
-    const uint32_t total = lds_exscan<uint32_t>(cnt, n_chunks, wtot32);
-    for (int i = tid; i < n_chunks; i += AL_T) chunk_off[i] = cnt[i];
-    if (tid == 0) chunk_off[n_chunks] = total;
+    if (tid == 0) { ctl->T_hi = sel.T_hi; ctl->T_lo = sel.T_lo; }
 }
 
-size_t allocate_ws_bytes(const varrate_shape& sh) {
-    const int64_t N = sh.n - sh.w;
-    return align256((size_t)N * sizeof(uint32_t)) + align256((size_t)N * sizeof(uint64_t));
+// ---- 7. final ranks and chunk sums ------------------------------------------------------------
+__global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __restrict__ u_ws,
+                                                 const uint64_t* __restrict__ phi_ws,
+                                                 uint8_t* __restrict__ rank, uint32_t* __restrict__ csum,
+                                                 const AlCtl* __restrict__ ctl) {
+    uint64_t phi[AK_PER];
+    uint32_t u[AK_PER], r[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k), tt = t < N ? t : N - 1;
+        phi[k] = phi_ws[tt];
+        u[k] = u_ws[tt];
+        r[k] = rank[tt];
+    }
+    const uint64_t T_hi = ctl->T_hi, T_lo = ctl->T_lo;
+    const bool any = ctl->any;
+    uint32_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        if (t >= N) continue;
+        if (any && phi[k] != CAPPED) {
+            const bool take = phi[k] > T_hi || (phi[k] == T_hi && lo_key(u[k], t) >= T_lo);
+            if (take) {
+                r[k] += 1;
+                rank[t] = (uint8_t)r[k];
+            }
+        }
+        sum += r[k];
+    }
+    sum = wave_sum(sum);
+    const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + (threadIdx.x >> 6);
+    if ((threadIdx.x & 63) == 0 && c * CHUNK < N) csum[c] = sum;
+}
+
+// ---- 8. chunk offsets (in place: chunk sums -> exclusive prefix, total at [n_chunks]) --------
+__global__ __launch_bounds__(AL_T) void al_scan(uint32_t* __restrict__ chunk_off, int n_chunks) {
+    __shared__ uint32_t a[MAX_CODED_CHUNKS];
+    __shared__ uint32_t wtot32[AL_T / 64];
+    for (int i = threadIdx.x; i < n_chunks; i += AL_T) a[i] = chunk_off[i];
+    __syncthreads();
+    const uint32_t total = lds_exscan<AL_T, uint32_t>(a, n_chunks, wtot32);
+    for (int i = threadIdx.x; i < n_chunks; i += AL_T) chunk_off[i] = a[i];
+    if (threadIdx.x == 0) chunk_off[n_chunks] = total;
 }
 
 hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_cache& c,
                            uint8_t* ws, hipStream_t st) {
     const int64_t N = sh.n - sh.w;
-    uint32_t* u_ws = (uint32_t*)ws;
-    uint64_t* phi_ws = (uint64_t*)(ws + align256((size_t)N * sizeof(uint32_t)));
+    const int R = D, r_min = sh.r_min;
+    const int64_t B = c.B;
+    const int nwg = (int)((N + AK_TOK - 1) / AK_TOK);
     const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
-    alloc_kernel<<<1, AL_T, 0, st>>>(sbar, N, c.B, sh.r_min, D, u_ws, phi_ws, c.rank, c.chunk_off,
-                                     n_chunks);
+    if (n_chunks > MAX_CODED_CHUNKS) return hipErrorInvalidValue;
+    const AlWs w = al_ws(ws, N);
+    al_minmax<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, w.clear, w.clear_words);
+    al_weights<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_low, w.c_cnt, w.ctl);
+    al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
+    al_floors<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
+    al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
+    al_select<<<1, AL_T, 0, st>>>(w.cand, w.ctl);
+    al_final<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, c.rank, c.chunk_off, w.ctl);
+    al_scan<<<1, AL_T, 0, st>>>(c.chunk_off, n_chunks);
     return hipGetLastError();
 }
 

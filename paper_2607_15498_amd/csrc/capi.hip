@@ -33,7 +33,6 @@ int hip_status(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-constexpr int64_t MAX_CODED = 1 << 20;   // allocator limits: chunk table in LDS, 24-bit index keys
 
 int check_shape(const varrate_shape* sh) {
     if (!sh) return fail(VARRATE_EINVAL, "shape is NULL");

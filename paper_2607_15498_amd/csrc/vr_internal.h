@@ -10,6 +10,8 @@
 namespace vr {
 
 constexpr int CHUNK = VARRATE_CHUNK;
+constexpr int64_t MAX_CODED = 1 << 20;   // allocator limits: chunk table in LDS, 24-bit index keys
+constexpr int MAX_CODED_CHUNKS = (int)(MAX_CODED / CHUNK);
 
 inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
