@@ -29,7 +29,7 @@
 //   al_floors   fine scan -> tau_lo, k, Q, M; floors, keys phi, sum of floors, histogram
 //               of phi's top 11 significant bits
 //   al_gather   rho; the digit bucket holding the rho-th largest key; its candidates
-//   al_select   (one workgroup) radix narrowing of the candidates to the exact threshold
+//   al_select   (one workgroup) the exact threshold among the candidates
 //   al_final    final ranks and per-chunk sums
 //   al_scan     (one workgroup) chunk offsets
 #include "vr_internal.h"
@@ -39,7 +39,6 @@ namespace vr {
 constexpr int AK_T = 256;                  // threads per workgroup of a token pass
 constexpr int AK_PER = CHUNK / 64;         // tokens per lane (a wave holds one chunk)
 constexpr int AK_TOK = AK_T * AK_PER;      // tokens per workgroup
-constexpr int AL_T = 1024;                 // threads of the one-workgroup kernels
 constexpr int CBITS = 12;
 constexpr int NCB = (1 << CBITS) + 1;      // coarse bins of u (u <= 2^24 + 1)
 constexpr int NFB = 1 << CBITS;            // fine bins
@@ -62,7 +61,7 @@ struct AlCtl {
     int sh0;                     // shift of the first selection digit
     // selection (al_gather, then al_select)
     unsigned long long pv, pm, T_hi, T_lo;
-    long long need;
+    long long need;              // rank of the threshold inside the bucket
     int done, any;
 };
 
@@ -271,60 +270,98 @@ __global__ __launch_bounds__(AK_T) void al_weights(const float* __restrict__ sba
 }
 
 // ---- 3. coarse level; fine histogram ----------------------------------------------------------
+// Thread i holds bins [CPT i, CPT i + CPT) of a scan in registers (one batch of loads).
+constexpr int CPT = (NCB + AK_T - 1) / AK_T;    // 17 coarse bins per thread
+constexpr int FPT = NFB / AK_T;                 // 16 fine bins per thread
+
 __global__ __launch_bounds__(AK_T) void al_fine(int64_t N, int64_t B, int r_min, int R,
                                                 const uint32_t* __restrict__ u_ws,
                                                 const unsigned long long* __restrict__ c_low,
                                                 const uint32_t* __restrict__ c_cnt,
                                                 uint32_t* __restrict__ f_cnt, AlCtl* __restrict__ ctl) {
-    __shared__ uint32_t cnt[NCB_PAD];
-    __shared__ unsigned long long sm[NCB_PAD];
+    __shared__ uint32_t cnt[NFB];
     __shared__ uint32_t wt32[AK_T / 64];
     __shared__ unsigned long long wt64[AK_T / 64];
+    __shared__ unsigned long long s_edge[2];
     uint32_t u[AK_PER];
 #pragma unroll
     for (int k = 0; k < AK_PER; ++k) {
         const int64_t t = al_tok(k);
         u[k] = u_ws[t < N ? t : N - 1];
     }
+    const int b0 = CPT * threadIdx.x;
+    uint32_t c[CPT];
+    unsigned long long l[CPT];
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+        const int b = b0 + j < NCB ? b0 + j : NCB - 1;
+        c[j] = c_cnt[b];
+        l[j] = c_low[b];
+    }
+    for (int i = threadIdx.x; i < NFB; i += AK_T) cnt[i] = 0;
     const uint32_t umax = ctl->umax;
     const int nb = (int)(umax >> CBITS) + 1;
-    for (int i = threadIdx.x; i <= nb; i += AK_T) {
-        const uint32_t c = i < nb ? c_cnt[i] : 0u;
-        cnt[i] = c;
-        sm[i] = i < nb ? (unsigned long long)c * ((uint64_t)i << CBITS) + c_low[i] : 0ull;
+    // bin sums and this thread's totals (bins >= nb are empty: u <= umax)
+    uint32_t lc = 0;
+    unsigned long long ls = 0;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) {
+        const int b = b0 + j;
+        if (b >= nb) { c[j] = 0; l[j] = 0; }
+        l[j] += (unsigned long long)c[j] * ((uint64_t)b << CBITS);    // sum of u in bin b
+        lc += c[j];
+        ls += l[j];
     }
-    __syncthreads();
-    // exclusive prefixes over bins 0..nb (entry nb = totals)
-    lds_exscan<AK_T, uint32_t>(cnt, nb + 1, wt32);
-    lds_exscan<AK_T, unsigned long long>(sm, nb + 1, wt64);
+    uint32_t tc;
+    unsigned long long ts;
+    uint32_t pc = block_exscan<AK_T, uint32_t>(lc, wt32, tc);
+    unsigned long long ps = block_exscan<AK_T, unsigned long long>(ls, wt64, ts);
     const uint64_t Dr = (uint64_t)(R - r_min);
     const uint64_t E = (uint64_t)(B - N * (int64_t)r_min);
     // the predicate at coarse edges tau_b = max(1, b << 12): c_ge = N - cnt_ex[b], s_lt = sm_ex[b]
     int bbest = 0;
-    for (int b = threadIdx.x; b < nb; b += AK_T) {
-        const uint64_t tau = b == 0 ? 1 : ((uint64_t)b << CBITS);
-        const uint64_t cge = (uint64_t)N - cnt[b];
-        const uint64_t slt = sm[b];
-        if (Dr * (tau * cge + slt) >= E * tau) bbest = b > bbest ? b : bbest;
+    {
+        uint32_t rc = pc;
+        unsigned long long rs = ps;
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) {
+            const int b = b0 + j;
+            const uint64_t tau = b == 0 ? 1 : ((uint64_t)b << CBITS);
+            const uint64_t cge = (uint64_t)N - rc;
+            if (b < nb && Dr * (tau * cge + rs) >= E * tau) bbest = b;
+            rc += c[j];
+            rs += l[j];
+        }
     }
     bbest = (int)block_reduce<AK_T, uint32_t>((uint32_t)bbest, wt32,
                                               [](uint32_t a, uint32_t b) { return a > b ? a : b; });
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        ctl->bbest = bbest;
-        ctl->cge_next = (uint64_t)N - cnt[bbest + 1];   // tokens in bins above bbest
-        ctl->slt_b = sm[bbest];                         // sum of u in bins below bbest
+    {
+        uint32_t rc = pc;
+        unsigned long long rs = ps;
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) {
+            if (b0 + j == bbest) {
+                s_edge[0] = (uint64_t)N - (rc + c[j]);   // tokens in bins above bbest
+                s_edge[1] = rs;                          // sum of u in bins below bbest
+            }
+            rc += c[j];
+            rs += l[j];
+        }
     }
     __syncthreads();
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        ctl->bbest = bbest;
+        ctl->cge_next = s_edge[0];
+        ctl->slt_b = s_edge[1];
+    }
     // fine counts of the low 12 bits inside bin bbest (every u there is (bbest << 12) + f)
-    for (int i = threadIdx.x; i < NFB; i += AK_T) cnt[i] = 0;
-    __syncthreads();
 #pragma unroll
     for (int k = 0; k < AK_PER; ++k)
         if (al_tok(k) < N && (int)(u[k] >> CBITS) == bbest) atomicAdd(&cnt[u[k] & (NFB - 1)], 1u);
     __syncthreads();
     for (int i = threadIdx.x; i < NFB; i += AK_T) {
-        const uint32_t c = cnt[i];
-        if (c) atomicAdd(&f_cnt[i], c);
+        const uint32_t cc = cnt[i];
+        if (cc) atomicAdd(&f_cnt[i], cc);
     }
 }
 
@@ -334,46 +371,75 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
                                                   const uint32_t* __restrict__ f_cnt,
                                                   uint8_t* __restrict__ rank, uint64_t* __restrict__ phi_ws,
                                                   uint32_t* __restrict__ d_cnt, AlCtl* __restrict__ ctl) {
-    __shared__ uint32_t cnt[NFB + 1];
-    __shared__ unsigned long long sm[NFB + 1];
+    __shared__ uint32_t cnt[NDB];
     __shared__ uint32_t wt32[AK_T / 64];
     __shared__ unsigned long long wt64[AK_T / 64];
+    __shared__ unsigned long long s_edge[2];
     uint32_t u[AK_PER];
 #pragma unroll
     for (int k = 0; k < AK_PER; ++k) {
         const int64_t t = al_tok(k);
         u[k] = u_ws[t < N ? t : N - 1];
     }
+    const int f0 = FPT * threadIdx.x;
+    uint32_t c[FPT];
+#pragma unroll
+    for (int j = 0; j < FPT; j += 4) {
+        const uint4 v = *reinterpret_cast<const uint4*>(f_cnt + f0 + j);
+        c[j] = v.x; c[j + 1] = v.y; c[j + 2] = v.z; c[j + 3] = v.w;
+    }
+    for (int i = threadIdx.x; i < NDB; i += AK_T) cnt[i] = 0;
     const uint32_t umax = ctl->umax;
     const int bbest = ctl->bbest;
     const uint64_t cge_next = ctl->cge_next, slt_b = ctl->slt_b;
     const uint64_t base_tau = (uint64_t)bbest << CBITS;
-    for (int i = threadIdx.x; i <= NFB; i += AK_T) {
-        const uint32_t c = i < NFB ? f_cnt[i] : 0u;
-        cnt[i] = c;
-        sm[i] = (unsigned long long)c * (base_tau + (uint64_t)i);
+    uint32_t lc = 0;
+    unsigned long long ls = 0;
+#pragma unroll
+    for (int j = 0; j < FPT; ++j) {
+        lc += c[j];
+        ls += (unsigned long long)c[j] * (base_tau + (uint64_t)(f0 + j));
     }
-    __syncthreads();
-    lds_exscan<AK_T, uint32_t>(cnt, NFB + 1, wt32);
-    lds_exscan<AK_T, unsigned long long>(sm, NFB + 1, wt64);
+    uint32_t tc;
+    unsigned long long ts;
+    const uint32_t pc = block_exscan<AK_T, uint32_t>(lc, wt32, tc);
+    const unsigned long long ps = block_exscan<AK_T, unsigned long long>(ls, wt64, ts);
     const uint64_t Dr = (uint64_t)(R - r_min);
     const uint64_t E = (uint64_t)(B - N * (int64_t)r_min);
-    const uint64_t fc_total = cnt[NFB];
+    const uint64_t fc_total = tc;
     const int f_lo = bbest == 0 ? 1 : 0;
     const int f_hi = (int)(((uint64_t)umax - base_tau) < (uint64_t)(NFB - 1) ? (umax - base_tau) : (NFB - 1));
     int fbest = f_lo;
-    for (int f = threadIdx.x; f <= f_hi; f += AK_T) {
-        if (f < f_lo) continue;
-        const uint64_t tau = base_tau + f;
-        const uint64_t cge = cge_next + fc_total - cnt[f];
-        const uint64_t slt = slt_b + sm[f];
-        if (Dr * (tau * cge + slt) >= E * tau) fbest = f > fbest ? f : fbest;
+    {
+        uint32_t rc = pc;
+        unsigned long long rs = ps;
+#pragma unroll
+        for (int j = 0; j < FPT; ++j) {
+            const int f = f0 + j;
+            const uint64_t tau = base_tau + f;
+            const uint64_t cge = cge_next + fc_total - rc;
+            const uint64_t slt = slt_b + rs;
+            if (f >= f_lo && f <= f_hi && Dr * (tau * cge + slt) >= E * tau) fbest = f;
+            rc += c[j];
+            rs += (unsigned long long)c[j] * (base_tau + (uint64_t)f);
+        }
     }
     fbest = (int)block_reduce<AK_T, uint32_t>((uint32_t)fbest, wt32,
                                               [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+    {
+        uint32_t rc = pc;
+        unsigned long long rs = ps;
+#pragma unroll
+        for (int j = 0; j < FPT; ++j) {
+            rc += c[j];
+            rs += (unsigned long long)c[j] * (base_tau + (uint64_t)(f0 + j));
+            if (f0 + j == fbest) { s_edge[0] = rc; s_edge[1] = rs; }   // inclusive of fbest
+        }
+    }
+    __syncthreads();
     const uint32_t tau_lo = (uint32_t)(base_tau + fbest);
-    const int64_t kcap = (int64_t)(cge_next + fc_total - cnt[fbest + 1]);
-    const uint64_t Q = slt_b + sm[fbest + 1];
+    const int64_t kcap = (int64_t)(cge_next + fc_total - s_edge[0]);
+    const uint64_t Q = slt_b + s_edge[1];
     const int64_t M = B - (int64_t)R * kcap - (int64_t)r_min * (N - kcap);
     const double invQ = 1.0 / (double)Q;
     // first selection digit: phi < Q, so its top 11 significant bits need no range pass
@@ -387,9 +453,6 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
         ctl->M = M;
         ctl->sh0 = sh0;
     }
-    __syncthreads();
-    for (int i = threadIdx.x; i < NDB; i += AK_T) cnt[i] = 0;
-    __syncthreads();
 
     unsigned long long fsum = 0;
 #pragma unroll
@@ -426,7 +489,98 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
     }
 }
 
-// ---- 5. the digit bucket holding the rho-th largest key; gather its candidates -------------------
+// ---- 5. selection ------------------------------------------------------------------------------
+struct SelState {
+    uint64_t pv, pm;   // fixed prefix value / mask of the field being narrowed
+    uint64_t T_hi, T_lo;
+    int64_t need;
+    int phase;         // 0: narrowing phi, 1: narrowing (u, ~t)
+    int done;
+};
+
+// Most-significant-digit narrowing of the threshold over the candidates enumerated by
+// visit(f) (f(hi, lo) per candidate) by NT threads, starting from `sel`.
+template <int NT, class Visit>
+__device__ void radix_narrow(Visit visit, SelState& sel, uint32_t* cnt, uint32_t* wtot32,
+                             unsigned long long* wtot64) {
+    constexpr int DPT = NDB / NT;       // digits per thread, in descending order
+    const int tid = threadIdx.x;
+    // every round fixes at least one more bit of the field or ends the phase, so two 64-bit
+    // fields finish within 2 * 65 rounds; the bound only guards against a broken invariant
+    for (int round = 0; round < 2 * 65 && !sel.done; ++round) {
+        const int phase = sel.phase;
+        const uint64_t pv = sel.pv, pm = sel.pm, T_hi = sel.T_hi;
+        auto field = [&](uint64_t hi, uint64_t lo, uint64_t& f) -> bool {
+            if (phase == 0) {
+                f = hi;
+            } else {
+                if (hi != T_hi) return false;
+                f = lo;
+            }
+            return (f & pm) == pv;
+        };
+        uint64_t fmn = ~0ull, fmx = 0;
+        visit([&](uint64_t hi, uint64_t lo) {
+            uint64_t f;
+            if (field(hi, lo, f)) {
+                fmn = f < fmn ? f : fmn;
+                fmx = f > fmx ? f : fmx;
+            }
+        });
+        fmn = block_reduce<NT, unsigned long long>(fmn, wtot64, [](unsigned long long a, unsigned long long b) { return a < b ? a : b; });
+        fmx = block_reduce<NT, unsigned long long>(fmx, wtot64, [](unsigned long long a, unsigned long long b) { return a > b ? a : b; });
+        if (fmn == fmx) {
+            if (tid == 0) {
+                if (phase == 0) {
+                    sel.T_hi = fmn; sel.phase = 1; sel.pv = 0; sel.pm = 0;
+                } else {
+                    sel.T_lo = fmn; sel.done = 1;   // keys are unique: a single candidate
+                }
+            }
+            __syncthreads();
+            continue;
+        }
+        const int p = 63 - __clzll((long long)(fmn ^ fmx));
+        const int sh = p > 10 ? p - 10 : 0;
+        const uint64_t dmask = (1ull << (p - sh + 1)) - 1;
+        const uint64_t above_mask = (p == 63) ? 0ull : ~((2ull << p) - 1);
+        for (int i = tid; i < NDB; i += NT) cnt[i] = 0;
+        __syncthreads();
+        visit([&](uint64_t hi, uint64_t lo) {
+            uint64_t f;
+            if (field(hi, lo, f)) atomicAdd(&cnt[(f >> sh) & dmask], 1u);
+        });
+        __syncthreads();
+        uint32_t c[DPT], loc = 0;
+#pragma unroll
+        for (int j = 0; j < DPT; ++j) { c[j] = cnt[NDB - 1 - DPT * tid - j]; loc += c[j]; }
+        uint32_t tot;
+        uint32_t above = block_exscan<NT, uint32_t>(loc, wtot32, tot);
+        const int64_t need = sel.need;
+        __syncthreads();                          // every thread has read sel before it changes
+#pragma unroll
+        for (int j = 0; j < DPT; ++j) {
+            if ((int64_t)above < need && need <= (int64_t)(above + c[j])) {
+                const int hit = NDB - 1 - DPT * tid - j;
+                const int64_t nn = need - (int64_t)above;
+                const uint64_t npv = (fmn & above_mask) | ((uint64_t)hit << sh);
+                sel.need = nn;
+                sel.pv = npv;
+                sel.pm = ~((1ull << sh) - 1);
+                if ((int64_t)c[j] == nn) {
+                    if (phase == 0) { sel.T_hi = npv; sel.T_lo = 0; }
+                    else { sel.T_lo = npv; }
+                    sel.done = 1;
+                }
+            }
+            above += c[j];
+        }
+        __syncthreads();
+    }
+}
+
+// The digit bucket holding the rho-th largest key (every workgroup), and its candidates
+// into a list.
 __global__ __launch_bounds__(AK_T) void al_gather(int64_t N, int64_t B, const uint32_t* __restrict__ u_ws,
                                                   const uint64_t* __restrict__ phi_ws,
                                                   const uint32_t* __restrict__ d_cnt,
@@ -466,19 +620,20 @@ __global__ __launch_bounds__(AK_T) void al_gather(int64_t N, int64_t B, const ui
     __syncthreads();
     const int hit = s_hit;
     // rho <= 0 selects nothing; rho > 0 always lands in a bucket (rho < uncapped count)
-    const bool done0 = hit < 0 || (int64_t)s_hcnt == rho - (int64_t)s_above;
+    const int64_t need = hit < 0 ? 0 : rho - (int64_t)s_above;
+    const bool done0 = hit < 0 || (int64_t)s_hcnt == need;
     const uint64_t pv = hit < 0 ? 0 : (uint64_t)hit << sh0;
     const uint64_t pm = ~((1ull << sh0) - 1);
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         ctl->any = rho > 0 && hit >= 0;
-        ctl->need = hit < 0 ? 0 : rho - (int64_t)s_above;
-        ctl->pv = pv;
-        ctl->pm = pm;
-        ctl->done = done0;
         ctl->T_hi = hit < 0 ? ~0ull : pv;      // the whole bucket is taken when done here
         ctl->T_lo = 0;
+        ctl->pv = pv;
+        ctl->pm = pm;
+        ctl->need = need;
+        ctl->done = done0;
     }
-    if (done0) return;
+    if (done0) return;                         // (the same in every workgroup)
     // candidates of the bucket: a workgroup-local slot first, then one global reservation
     uint32_t slot[AK_PER];
     bool mine[AK_PER];
@@ -497,138 +652,77 @@ __global__ __launch_bounds__(AK_T) void al_gather(int64_t N, int64_t B, const ui
             cand[2 * i] = phi[k];
             cand[2 * i + 1] = lo_key(u[k], al_tok(k));
         }
+
 }
 
-// ---- 6. radix narrowing of the candidates (one workgroup) ----------------------------------------
-struct SelState {
-    uint64_t pv, pm;   // fixed prefix value / mask of the field being narrowed
-    uint64_t T_hi, T_lo;
-    int64_t need;
-    int phase;         // 0: narrowing phi, 1: narrowing (u, ~t)
-    int done;
-};
+// The exact threshold among the bucket's candidates (one workgroup).  Up to AS_T candidates
+// (the usual case: a bucket holds about 2^-11 of the uncapped tokens) each find their
+// rank among the others directly; more go through the radix narrowing.
+constexpr int AS_T = 1024;
 
-// Most-significant-digit narrowing of the threshold over the candidates enumerated by
-// visit(f) (f(hi, lo) per candidate), starting from `sel`.
-template <class Visit>
-__device__ void radix_narrow(Visit visit, SelState& sel, uint32_t* cnt, uint32_t* wtot32,
-                             unsigned long long* wtot64) {
-    const int tid = threadIdx.x;
-    // every round fixes at least one more bit of the field or ends the phase, so two 64-bit
-    // fields finish within 2 * 65 rounds; the bound only guards against a broken invariant
-    for (int round = 0; round < 2 * 65 && !sel.done; ++round) {
-        const int phase = sel.phase;
-        const uint64_t pv = sel.pv, pm = sel.pm, T_hi = sel.T_hi;
-        auto field = [&](uint64_t hi, uint64_t lo, uint64_t& f) -> bool {
-            if (phase == 0) {
-                f = hi;
-            } else {
-                if (hi != T_hi) return false;
-                f = lo;
-            }
-            return (f & pm) == pv;
-        };
-        uint64_t fmn = ~0ull, fmx = 0;
-        visit([&](uint64_t hi, uint64_t lo) {
-            uint64_t f;
-            if (field(hi, lo, f)) {
-                fmn = f < fmn ? f : fmn;
-                fmx = f > fmx ? f : fmx;
-            }
-        });
-        fmn = block_reduce<AL_T, unsigned long long>(fmn, wtot64, [](unsigned long long a, unsigned long long b) { return a < b ? a : b; });
-        fmx = block_reduce<AL_T, unsigned long long>(fmx, wtot64, [](unsigned long long a, unsigned long long b) { return a > b ? a : b; });
-        if (fmn == fmx) {
-            if (tid == 0) {
-                if (phase == 0) {
-                    sel.T_hi = fmn; sel.phase = 1; sel.pv = 0; sel.pm = 0;
-                } else {
-                    sel.T_lo = fmn; sel.done = 1;   // keys are unique: a single candidate
-                }
-            }
-            __syncthreads();
-            continue;
-        }
-        const int p = 63 - __clzll((long long)(fmn ^ fmx));
-        const int sh = p > 10 ? p - 10 : 0;
-        const uint64_t dmask = (1ull << (p - sh + 1)) - 1;
-        const uint64_t above_mask = (p == 63) ? 0ull : ~((2ull << p) - 1);
-        for (int i = tid; i < 2048; i += AL_T) cnt[i] = 0;
-        __syncthreads();
-        visit([&](uint64_t hi, uint64_t lo) {
-            uint64_t f;
-            if (field(hi, lo, f)) atomicAdd(&cnt[(f >> sh) & dmask], 1u);
-        });
-        __syncthreads();
-        const int d0 = 2047 - 2 * tid, d1 = d0 - 1;
-        const uint32_t c0 = cnt[d0], c1 = cnt[d1];
-        uint32_t tot;
-        const uint32_t above0 = block_exscan<AL_T, uint32_t>(c0 + c1, wtot32, tot);
-        const int64_t need = sel.need;
-        __syncthreads();
-        int hit = -1;
-        uint32_t hit_above = 0, hit_cnt = 0;
-        if ((int64_t)above0 < need && need <= (int64_t)(above0 + c0)) { hit = d0; hit_above = above0; hit_cnt = c0; }
-        const uint32_t above1 = above0 + c0;
-        if ((int64_t)above1 < need && need <= (int64_t)(above1 + c1)) { hit = d1; hit_above = above1; hit_cnt = c1; }
-        if (hit >= 0) {
-            const int64_t nn = need - (int64_t)hit_above;
-            const uint64_t npv = (fmn & above_mask) | ((uint64_t)hit << sh);
-            sel.need = nn;
-            sel.pv = npv;
-            sel.pm = ~((1ull << sh) - 1);
-            if ((int64_t)hit_cnt == nn) {
-                if (phase == 0) { sel.T_hi = npv; sel.T_lo = 0; }
-                else { sel.T_lo = npv; }
-                sel.done = 1;
-            }
-        }
-        __syncthreads();
-    }
-}
-
-__global__ __launch_bounds__(AL_T) void al_select(const uint64_t* __restrict__ cand, AlCtl* __restrict__ ctl) {
-    __shared__ uint32_t cnt[2048];
+__global__ __launch_bounds__(AS_T) void al_select(int64_t N, const uint64_t* __restrict__ cand,
+                                                  AlCtl* __restrict__ ctl) {
+    __shared__ uint32_t cnt[NDB];
     __shared__ unsigned long long chi[SEL_CAP], clo[SEL_CAP];
-    __shared__ unsigned long long wtot64[AL_T / 64];
-    __shared__ uint32_t wtot32[AL_T / 64];
+    __shared__ unsigned long long wtot64[AS_T / 64];
+    __shared__ uint32_t wtot32[AS_T / 64];
     __shared__ SelState sel;
-    if (ctl->done) return;
     const int tid = threadIdx.x;
+    // the candidates' loads issue with the state's (slots past the list hold stale keys and
+    // are not used)
+    const int64_t ti = tid < N ? tid : N - 1;
+    const uint64_t my_hi = cand[2 * ti], my_lo = cand[2 * ti + 1];
+    if (ctl->done) return;
+    const int nc = (int)ctl->ncand;
+    const int64_t need = ctl->need;
+    if (nc <= AS_T) {
+        if (tid < nc) { chi[tid] = my_hi; clo[tid] = my_lo; }
+        __syncthreads();
+        if (tid < nc) {
+            // keys are unique: exactly one candidate has need - 1 larger ones
+            int above = 0;
+            for (int j = 0; j < nc; ++j) {
+                const uint64_t h = chi[j], l = clo[j];
+                above += (h > my_hi || (h == my_hi && l > my_lo)) ? 1 : 0;
+            }
+            if (above == need - 1) { ctl->T_hi = my_hi; ctl->T_lo = my_lo; }
+        }
+        return;
+    }
     if (tid == 0) {
-        sel.pv = ctl->pv; sel.pm = ctl->pm; sel.need = ctl->need;
+        sel.pv = ctl->pv; sel.pm = ctl->pm; sel.need = need;
         sel.T_hi = ~0ull; sel.T_lo = ~0ull; sel.phase = 0; sel.done = 0;
     }
-    const int nc = (int)ctl->ncand;
     if (nc <= SEL_CAP) {
-        for (int i = tid; i < nc; i += AL_T) { chi[i] = cand[2 * i]; clo[i] = cand[2 * i + 1]; }
+        for (int i = tid; i < nc; i += AS_T) { chi[i] = cand[2 * i]; clo[i] = cand[2 * i + 1]; }
         __syncthreads();
-        radix_narrow([&](auto f) {
-            for (int i = tid; i < nc; i += AL_T) f(chi[i], clo[i]);
+        radix_narrow<AS_T>([&](auto f) {
+            for (int i = tid; i < nc; i += AS_T) f(chi[i], clo[i]);
         }, sel, cnt, wtot32, wtot64);
     } else {
         __syncthreads();
-        radix_narrow([&](auto f) {
-            for (int i0 = 0; i0 < nc; i0 += 4 * AL_T) {
+        radix_narrow<AS_T>([&](auto f) {
+            for (int i0 = 0; i0 < nc; i0 += 4 * AS_T) {
                 uint64_t h[4], l[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    const int i = i0 + k * AL_T + tid;
+                    const int i = i0 + k * AS_T + tid;
                     if (i < nc) { h[k] = cand[2 * i]; l[k] = cand[2 * i + 1]; }
                 }
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
-                    if (i0 + k * AL_T + tid < nc) f(h[k], l[k]);
+                    if (i0 + k * AS_T + tid < nc) f(h[k], l[k]);
             }
         }, sel, cnt, wtot32, wtot64);
     }
     if (tid == 0) { ctl->T_hi = sel.T_hi; ctl->T_lo = sel.T_lo; }
 }
 
-// ---- 7. final ranks and chunk sums ------------------------------------------------------------
+// ---- 6. final ranks and chunk sums ------------------------------------------------------------
+
 __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __restrict__ u_ws,
                                                  const uint64_t* __restrict__ phi_ws,
-                                                 uint8_t* __restrict__ rank, uint32_t* __restrict__ csum,
+                                                 uint8_t* __restrict__ rank, uint32_t* __restrict__ chunk_off,
                                                  const AlCtl* __restrict__ ctl) {
     uint64_t phi[AK_PER];
     uint32_t u[AK_PER], r[AK_PER];
@@ -657,17 +751,32 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
     }
     sum = wave_sum(sum);
     const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + (threadIdx.x >> 6);
-    if ((threadIdx.x & 63) == 0 && c * CHUNK < N) csum[c] = sum;
+    if ((threadIdx.x & 63) == 0 && c * CHUNK < N) chunk_off[c] = sum;
+
 }
 
-// ---- 8. chunk offsets (in place: chunk sums -> exclusive prefix, total at [n_chunks]) --------
-__global__ __launch_bounds__(AL_T) void al_scan(uint32_t* __restrict__ chunk_off, int n_chunks) {
-    __shared__ uint32_t a[MAX_CODED_CHUNKS];
-    __shared__ uint32_t wtot32[AL_T / 64];
-    for (int i = threadIdx.x; i < n_chunks; i += AL_T) a[i] = chunk_off[i];
-    __syncthreads();
-    const uint32_t total = lds_exscan<AL_T, uint32_t>(a, n_chunks, wtot32);
-    for (int i = threadIdx.x; i < n_chunks; i += AL_T) chunk_off[i] = a[i];
+// ---- 7. chunk offsets (in place: chunk sums -> exclusive prefix, total at [n_chunks]) --------
+constexpr int SCAN_T = 1024;
+constexpr int SCAN_PT = MAX_CODED_CHUNKS / SCAN_T;   // chunk sums per thread
+
+__global__ __launch_bounds__(SCAN_T) void al_scan(uint32_t* __restrict__ chunk_off, int n_chunks) {
+    __shared__ uint32_t wt32[SCAN_T / 64];
+    const int per = (n_chunks + SCAN_T - 1) / SCAN_T;
+    const int i0 = per * threadIdx.x;
+    uint32_t v[SCAN_PT], loc = 0;
+#pragma unroll
+    for (int j = 0; j < SCAN_PT; ++j) {
+        v[j] = j < per && i0 + j < n_chunks ? chunk_off[i0 + j] : 0u;
+        loc += v[j];
+    }
+    uint32_t total;
+    uint32_t pre = block_exscan<SCAN_T, uint32_t>(loc, wt32, total);
+#pragma unroll
+    for (int j = 0; j < SCAN_PT; ++j)
+        if (j < per && i0 + j < n_chunks) {
+            chunk_off[i0 + j] = pre;
+            pre += v[j];
+        }
     if (threadIdx.x == 0) chunk_off[n_chunks] = total;
 }
 
@@ -685,9 +794,9 @@ hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_c
     al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
     al_floors<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
     al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
-    al_select<<<1, AL_T, 0, st>>>(w.cand, w.ctl);
+    al_select<<<1, AS_T, 0, st>>>(N, w.cand, w.ctl);
     al_final<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, c.rank, c.chunk_off, w.ctl);
-    al_scan<<<1, AL_T, 0, st>>>(c.chunk_off, n_chunks);
+    al_scan<<<1, SCAN_T, 0, st>>>(c.chunk_off, n_chunks);
     return hipGetLastError();
 }
 
