@@ -276,15 +276,31 @@ __global__ __launch_bounds__(PJ_THREADS, F32 ? 2 : 4) void project_kernel(
                         c = mfma(pl[s], xh[hb][s], c);
                         if constexpr (F32) c = mfma(ph[s], xl[hb][s], c);
                     }
-                    // C: lane -> token column (slot i0 + 16hb + col), rows j = 16a + 4grp + v
+                    // C: lane -> token column (slot i0 + 16hb + col), rows j0 .. j0 + 3 with
+                    // j0 = 16a + 4grp: four consecutive coefficients of one packed row, stored
+                    // at once unless the row ends inside them
                     const int r = r_of[hb];
-                    const int64_t dst = out0 + o_of[hb];
+                    const int j0 = 16 * a + 4 * grp;
+                    const int64_t dst = out0 + o_of[hb] + j0;
+                    if constexpr (F32) {
+                        float* o = (float*)(kv ? coef_v : coef_k) + dst;
+                        if (j0 + 4 <= r) {
+                            __builtin_memcpy(o, &c, 16);
+                        } else {
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int j = 16 * a + 4 * grp + v;
-                        if (j < r) {
-                            if constexpr (F32) ((float*)(kv ? coef_v : coef_k))[dst + j] = c[v];
-                            else ((uint16_t*)(kv ? coef_v : coef_k))[dst + j] = (uint16_t)f32_to_bf16(c[v]);
+                            for (int v = 0; v < 3; ++v)
+                                if (j0 + v < r) o[v] = c[v];
+                        }
+                    } else {
+                        uint16_t* o = (uint16_t*)(kv ? coef_v : coef_k) + dst;
+                        const uint32_t p01 = cvt_bf16x2(c[0], c[1]), p23 = cvt_bf16x2(c[2], c[3]);
+                        if (j0 + 4 <= r) {
+                            const uint2 pk = make_uint2(p01, p23);
+                            __builtin_memcpy(o, &pk, 8);
+                        } else {
+                            if (j0 < r) o[0] = (uint16_t)p01;
+                            if (j0 + 1 < r) o[1] = (uint16_t)(p01 >> 16);
+                            if (j0 + 2 < r) o[2] = (uint16_t)p23;
                         }
                     }
                 }
