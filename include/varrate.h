@@ -147,16 +147,17 @@ VARRATE_API int varrate_salience(const varrate_shape* shape, const void* K, cons
  * Min-max normalisation to integer weights u_t = 1 + floor(2^24 (sbar_t - min)/(max - min))
  * (all equal when max == min), exact-integer water-filling with floor r_min and cap d, and
  * largest-remainder integer ranks (ties: larger u_t, then lower t) so that sum = B.
- * Writes cache->rank and cache->chunk_off; sets cache->N and cache->B.  Bit-exact and
- * deterministic given sbar.                                                                 */
+ * Writes cache->rank, the storage order cache->srank / cache->sidx (each chunk's tokens by
+ * rank descending, index ascending) and cache->chunk_off; sets cache->N and cache->B.
+ * Bit-exact and deterministic given sbar.                                                   */
 VARRATE_API int varrate_allocate(const varrate_shape* shape, const float* sbar, varrate_cache* cache,
                      void* workspace, size_t workspace_bytes, void* stream);
 
 /* Sec. 3.3 Eq. (6): projects K[0:N] and V[0:N] ([n][G][d] dtype) onto the bases
  * P_K, P_V ([G][d][d] fp32, row j = j-th direction, orthonormal rows) and keeps the leading
- * rank[t] coefficients of every token in the stored layout (needs cache->rank and
- * cache->chunk_off from varrate_allocate).  Fills srank, sidx, coef_k, coef_v, copies the
- * window rows K[N:n], V[N:n] into exact slots 0..w-1 and sets cache->n_exact = w.           */
+ * rank[t] coefficients of every token in the stored layout (needs cache->srank, cache->sidx
+ * and cache->chunk_off from varrate_allocate).  Fills coef_k, coef_v, copies the window rows
+ * K[N:n], V[N:n] into exact slots 0..w-1 and sets cache->n_exact = w.                       */
 VARRATE_API int varrate_project(const varrate_shape* shape, const void* K, const void* V,
                     const float* P_K, const float* P_V, varrate_cache* cache,
                     void* workspace, size_t workspace_bytes, void* stream);

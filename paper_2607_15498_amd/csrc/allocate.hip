@@ -30,7 +30,7 @@
 //               of phi's top 11 significant bits
 //   al_gather   rho; the digit bucket holding the rho-th largest key; its candidates
 //   al_select   (one workgroup) the exact threshold among the candidates
-//   al_final    final ranks and per-chunk sums
+//   al_final    final ranks, per-chunk sums and each chunk's storage order (srank, sidx)
 //   al_scan     (one workgroup) chunk offsets
 #include "vr_internal.h"
 
@@ -45,6 +45,7 @@ constexpr int NFB = 1 << CBITS;            // fine bins
 constexpr int NDB = 2048;                  // selection digit bins (11 bits)
 constexpr int SEL_CAP = 2048;              // candidates the selection finishes in LDS
 constexpr uint64_t CAPPED = 1ull << 63;
+constexpr int NRV = D + 1;                 // rank values 0..128
 static_assert(AK_PER * 64 == CHUNK, "a wave holds one storage chunk");
 
 // Device-side state of one allocation (in the workspace, cleared by al_minmax).
@@ -718,12 +719,17 @@ __global__ __launch_bounds__(AS_T) void al_select(int64_t N, const uint64_t* __r
     if (tid == 0) { ctl->T_hi = sel.T_hi; ctl->T_lo = sel.T_lo; }
 }
 
-// ---- 6. final ranks and chunk sums ------------------------------------------------------------
+// ---- 6. final ranks, chunk sums, storage order ----------------------------------------------------
 
 __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __restrict__ u_ws,
                                                  const uint64_t* __restrict__ phi_ws,
-                                                 uint8_t* __restrict__ rank, uint32_t* __restrict__ chunk_off,
+                                                 uint8_t* __restrict__ rank, uint8_t* __restrict__ srank,
+                                                 uint32_t* __restrict__ sidx, uint32_t* __restrict__ chunk_off,
                                                  const AlCtl* __restrict__ ctl) {
+    // storage order of each wave's chunk: per-rank 256-bit token masks, and the count of
+    // tokens of higher rank per rank value
+    __shared__ unsigned long long msk[AK_T / 64][NRV][4];
+    __shared__ uint16_t above_r[AK_T / 64][NRV];
     uint64_t phi[AK_PER];
     uint32_t u[AK_PER], r[AK_PER];
 #pragma unroll
@@ -750,9 +756,61 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
         sum += r[k];
     }
     sum = wave_sum(sum);
-    const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + (threadIdx.x >> 6);
-    if ((threadIdx.x & 63) == 0 && c * CHUNK < N) chunk_off[c] = sum;
+    const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + wv;
+    if (lane == 0 && c * CHUNK < N) chunk_off[c] = sum;
 
+    // Stored order of the chunk: rank descending, token index ascending (a stable counting
+    // sort).  Token lane + 64 k of the chunk is bit `lane` of word k of its rank's mask, so a
+    // token's place is (#tokens of higher rank) + (#earlier tokens of its rank).
+    unsigned long long (*m)[4] = msk[wv];
+    for (int i = lane; i < NRV * 4; i += 64) (&m[0][0])[i] = 0ull;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k)
+        if (al_tok(k) < N) atomicOr(&m[r[k]][k], 1ull << lane);
+    __syncthreads();
+    {
+        // lane covers rank values 128 - 3 lane - e (descending), then a wave exclusive scan
+        uint32_t h[3], loc = 0;
+#pragma unroll
+        for (int e = 0; e < 3; ++e) {
+            const int q = 3 * lane + e;
+            h[e] = 0;
+            if (q < NRV) {
+                const unsigned long long* mm = m[NRV - 1 - q];
+                h[e] = __popcll(mm[0]) + __popcll(mm[1]) + __popcll(mm[2]) + __popcll(mm[3]);
+            }
+            loc += h[e];
+        }
+        uint32_t x = loc;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        uint32_t pre = x - loc;
+#pragma unroll
+        for (int e = 0; e < 3; ++e) {
+            const int q = 3 * lane + e;
+            if (q < NRV) above_r[wv][NRV - 1 - q] = (uint16_t)pre;
+            pre += h[e];
+        }
+    }
+    __syncthreads();
+    const int64_t t0 = c * CHUNK;
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        if (t >= N) continue;
+        const unsigned long long* mm = m[r[k]];
+        uint32_t pos = above_r[wv][r[k]] + __popcll(mm[k] & ((1ull << lane) - 1ull));
+#pragma unroll
+        for (int j = 0; j < AK_PER - 1; ++j)
+            if (j < k) pos += __popcll(mm[j]);
+        srank[t0 + pos] = (uint8_t)r[k];
+        sidx[t0 + pos] = (uint32_t)t;
+    }
 }
 
 // ---- 7. chunk offsets (in place: chunk sums -> exclusive prefix, total at [n_chunks]) --------
@@ -795,7 +853,7 @@ hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_c
     al_floors<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
     al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
     al_select<<<1, AS_T, 0, st>>>(N, w.cand, w.ctl);
-    al_final<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, c.rank, c.chunk_off, w.ctl);
+    al_final<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, c.rank, c.srank, c.sidx, c.chunk_off, w.ctl);
     al_scan<<<1, SCAN_T, 0, st>>>(c.chunk_off, n_chunks);
     return hipGetLastError();
 }
