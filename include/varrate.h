@@ -80,13 +80,19 @@ typedef struct varrate_shape {
  *   - Coded tokens t in [0, N) are split into chunks of VARRATE_CHUNK consecutive tokens
  *     (the last chunk is ragged); n_chunks = ceil(N / VARRATE_CHUNK).
  *   - rank[t] (original order) is the integer rank of token t (Eq. 5, sum = B).
- *   - chunk_off[c] = sum of rank[t] over chunks before c; chunk_off[n_chunks] = B.
  *   - Inside chunk c the tokens are stored in order of (rank descending, index
  *     ascending); stored position i (global, i in [0, N)) holds token sidx[i] with rank
- *     srank[i].  Stored token i's coefficients occupy, in every head stream,
- *         coef[g * coef_stride + chunk_off[c] + sum_{chunk-mates i' < i} srank[i'] + j],
- *     j < srank[i]: the leading srank[i] coordinates of its projection onto the basis
- *     (row j of P = j-th direction).  Coefficients are stored in `dtype`.
+ *     srank[i].
+ *   - Tile h of chunk c is its stored positions 16h .. 16h + 15 (positions past the chunk's
+ *     end are absent, rank 0).  Its size m_h is the rank of its first position (the largest
+ *     in the tile), and it takes 16 * m_h elements of every head stream at
+ *         coef[g * coef_stride + chunk_off[c] + 16 * sum_{h' < h} m_h'],
+ *     with chunk_off[c] = sum of 16 * m_h over the tiles of earlier chunks.  The K block is
+ *     16 rows of m_h coordinates (row i: position 16h + i); the V block is m_h rows of 16
+ *     positions (coordinate-major).  An entry (position, coordinate j) holds the position's
+ *     projection onto basis row j (row j of P = j-th direction) when j < its rank, and 0
+ *     otherwise.  Coefficients are stored in `dtype`.  chunk_off[n_chunks] <= B + 8 *
+ *     VARRATE_CHUNK * n_chunks (a tile's size is bounded by the ranks of the tile before it).
  *   - k_exact/v_exact hold exact rows: slot e < w is token N + e (the window); slots
  *     e >= w are tokens appended after compression (varrate_append_exact).
  * All pointers are device memory owned by the caller; sizes come from
@@ -102,7 +108,7 @@ typedef struct varrate_cache {
     uint32_t* chunk_off;    /* [n_chunks + 1]                                               */
     void*     k_exact;      /* [G][cap][d] dtype                                            */
     void*     v_exact;      /* [G][cap][d] dtype                                            */
-    int64_t   coef_stride;  /* elements per head stream, >= B + VARRATE_COEF_PAD           */
+    int64_t   coef_stride;  /* elements per head stream, >= B + 2048 n_chunks + COEF_PAD    */
     int64_t   cap;          /* exact-slot capacity, >= w                                    */
     int64_t   n_exact;      /* exact slots in use                                           */
     int64_t   N;            /* coded tokens                                                 */

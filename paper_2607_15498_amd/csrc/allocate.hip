@@ -30,7 +30,8 @@
 //               of phi's top 11 significant bits
 //   al_gather   rho; the digit bucket holding the rho-th largest key; its candidates
 //   al_select   (one workgroup) the exact threshold among the candidates
-//   al_final    final ranks, per-chunk sums and each chunk's storage order (srank, sidx)
+//   al_final    final ranks, each chunk's storage order (srank, sidx) and its size in tile
+//               rectangles (16 x the largest rank of each 16-position tile)
 //   al_scan     (one workgroup) chunk offsets
 #include "vr_internal.h"
 
@@ -741,7 +742,6 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
     }
     const uint64_t T_hi = ctl->T_hi, T_lo = ctl->T_lo;
     const bool any = ctl->any;
-    uint32_t sum = 0;
 #pragma unroll
     for (int k = 0; k < AK_PER; ++k) {
         const int64_t t = al_tok(k);
@@ -753,12 +753,9 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
                 rank[t] = (uint8_t)r[k];
             }
         }
-        sum += r[k];
     }
-    sum = wave_sum(sum);
     const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + wv;
-    if (lane == 0 && c * CHUNK < N) chunk_off[c] = sum;
 
     // Stored order of the chunk: rank descending, token index ascending (a stable counting
     // sort).  Token lane + 64 k of the chunk is bit `lane` of word k of its rank's mask, so a
@@ -799,6 +796,7 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
     }
     __syncthreads();
     const int64_t t0 = c * CHUNK;
+    uint32_t tile_sum = 0;
 #pragma unroll
     for (int k = 0; k < AK_PER; ++k) {
         const int64_t t = al_tok(k);
@@ -810,7 +808,11 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
             if (j < k) pos += __popcll(mm[j]);
         srank[t0 + pos] = (uint8_t)r[k];
         sidx[t0 + pos] = (uint32_t)t;
+        // the chunk's storage: each tile of 16 positions takes 16 x its first (largest) rank
+        if ((pos & 15) == 0) tile_sum += 16u * r[k];
     }
+    tile_sum = wave_sum(tile_sum);
+    if (lane == 0 && c * CHUNK < N) chunk_off[c] = tile_sum;
 }
 
 // ---- 7. chunk offsets (in place: chunk sums -> exclusive prefix, total at [n_chunks]) --------

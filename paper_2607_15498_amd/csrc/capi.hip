@@ -66,9 +66,11 @@ int check_cache(const varrate_shape* sh, const varrate_cache* c, bool need_layou
         return fail(VARRATE_EINVAL, "cache has a NULL buffer");
     if (!aligned16(c->coef_k) || !aligned16(c->coef_v) || !aligned16(c->k_exact) || !aligned16(c->v_exact))
         return fail(VARRATE_EINVAL, "cache buffers must be 16-byte aligned");
-    if (c->coef_stride < B + VARRATE_COEF_PAD || (c->coef_stride % 8) != 0)
-        return fail(VARRATE_EINVAL, "coef_stride=%lld must be a multiple of 8 and >= B + %d = %lld",
-                    (long long)c->coef_stride, VARRATE_COEF_PAD, (long long)(B + VARRATE_COEF_PAD));
+    const int64_t N = sh->n - sh->w;
+    const int64_t need = B + (int64_t)8 * VARRATE_CHUNK * ((N + VARRATE_CHUNK - 1) / VARRATE_CHUNK) + VARRATE_COEF_PAD;
+    if (c->coef_stride < need || (c->coef_stride % 8) != 0)
+        return fail(VARRATE_EINVAL, "coef_stride=%lld must be a multiple of 8 and >= %lld (B + 2048 per chunk + %d)",
+                    (long long)c->coef_stride, (long long)need, VARRATE_COEF_PAD);
     if (c->cap < sh->w) return fail(VARRATE_EINVAL, "exact capacity %lld < w=%d", (long long)c->cap, sh->w);
     return VARRATE_OK;
 }
@@ -110,7 +112,9 @@ int varrate_cache_bytes(const varrate_shape* sh, int64_t cap, varrate_cache_byte
     out->N = sh->n - sh->w;
     out->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
     out->n_chunks = (out->N + VARRATE_CHUNK - 1) / VARRATE_CHUNK;
-    out->coef_stride = ((out->B + VARRATE_COEF_PAD + 63) / 64) * 64;
+    // tile rectangles: a chunk's 16 tiles take at most its ranks + 16 x 128 elements
+    const int64_t bound = out->B + (int64_t)8 * VARRATE_CHUNK * out->n_chunks;
+    out->coef_stride = ((bound + VARRATE_COEF_PAD + 63) / 64) * 64;
     out->coef_k = out->coef_v = (size_t)sh->G * out->coef_stride * es;
     out->rank = out->srank = (size_t)((out->N + 63) / 64) * 64;   // padded for 16-byte loads
     out->sidx = (size_t)out->N * 4;

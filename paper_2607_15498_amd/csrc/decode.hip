@@ -81,8 +81,10 @@ __device__ __forceinline__ void split4(const float* x, u32x2& hi, u32x2& lo) {
 // at once; the waves then run their tiles from LDS.
 constexpr int DC_STAGE_BYTES = 30720;                         // per stream and round
 constexpr int DC_STAGE_PAD = 64;                              // over-read slack of row gathers
-constexpr int DC_SO = 264;                                    // offsets per chunk: 257, padded
+constexpr int DC_TO = 18;                                     // tile offsets per chunk: 17, padded
 constexpr int DC_CROW = D + 4;                                // comb row stride (floats)
+constexpr int DC_ZERO_BF16 = DC_STAGE_BYTES / 2;               // V stage element in the zeroed pad
+typedef unsigned short us2 __attribute__((ext_vector_type(2)));
 
 struct DecSmem {
     uint8_t* stK;     // [DC_STAGE_BYTES + pad] staged K coefficients of the round; after the
@@ -95,7 +97,8 @@ struct DecSmem {
     float* lrow;      // [16]
     int* cT;          // [DC_MAX_CPW] valid tokens per chunk
     uint32_t* cb;     // [DC_MAX_CPW] chunk bases (chunk_off)
-    uint16_t* so;     // [cpw][DC_SO] offset of stored slot i inside its chunk, i = 0..256
+    u32x4* kmask;     // [9] bf16 masks keeping the first nv elements of an 8-element row piece
+    uint16_t* to;     // [cpw][DC_TO] element offset of tile h inside its chunk, h = 0..16
 };
 
 __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
@@ -112,13 +115,14 @@ __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
     s.lrow = f; f += 16;
     s.cT = reinterpret_cast<int*>(f); f += DC_MAX_CPW;
     s.cb = reinterpret_cast<uint32_t*>(f); f += DC_MAX_CPW;
-    s.so = reinterpret_cast<uint16_t*>(f);                  // 16-byte aligned
+    s.kmask = reinterpret_cast<u32x4*>(f); f += 9 * 4;
+    s.to = reinterpret_cast<uint16_t*>(f);
     return s;
 }
 
 static inline size_t decode_smem_bytes(int cpw) {
     return 2 * (size_t)(DC_STAGE_BYTES + DC_STAGE_PAD) + 4 * 2 * 64 * 16 +
-           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW) * 4 + (size_t)cpw * DC_SO * 2;
+           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW + 9 * 4) * 4 + (size_t)cpw * DC_TO * 2;
 }
 
 // 8 consecutive bf16 at element index a of an LDS array (any 2-byte alignment): five dword
@@ -149,11 +153,11 @@ __device__ __forceinline__ int lane_now() {
     return l;
 }
 
-// Per-lane view of one 16-token tile in the stage: the lane's score row (token i0 + col:
-// rank rk, stage offset ok) and its four value tokens (i0 + 4 grp + e: ranks vr, offsets vo).
+// One 16-position tile in the stage (wave-uniform): its first position i0 inside the chunk
+// (or the exact rows), the chunk's valid positions T, the stage offset of its first element
+// and its size m (coded: the largest rank of the tile; exact rows: 128).
 struct TileMeta {
-    int i0, T, rk, ok;
-    int vr[4], vo[4];
+    int i0, T, base, m;
 };
 
 // One tile.  Scores S[token][row] by 16x16x32 MFMA over KS steps of 32 coefficients (A =
@@ -163,37 +167,55 @@ struct TileMeta {
 // and the online-softmax rescale is lane-local.  KS and NB bound the tile's largest rank,
 // so every LDS read is unconditional (masked by value) and they all issue before the first
 // wait.
-template <bool F32, int KS, int NB>
+template <bool F32, bool EXACT, int KS, int NB>
 __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, const typename Elem<F32>::T* sK,
-                                          const typename Elem<F32>::T* sV, const u32x4* qf, int lane,
-                                          int grp, float& m_run, float& l_part, f32x4 (&acc)[8]) {
+                                          const typename Elem<F32>::T* sV, const u32x4* qf,
+                                          const u32x4* kmask, int lane, int grp, float& m_run,
+                                          float& l_part, f32x4 (&acc)[8]) {
     const int col = lane & 15;
-    // Row gathers may read up to 127 elements past the stage's valid range (into the pad
-    // and the LDS arrays after it); everything past a token's rank is masked by value.
-    // value operand gather (A of the value product: lane -> rank coordinate 16 b + col,
-    // tokens 4 grp + e)
+    // K rows of a coded tile are m coordinates apart (exact rows: 128) with zeros past each
+    // position's rank; a row piece past the row's end (into the next row, the pad or the LDS
+    // arrays after the stage) is masked.  V blocks are coordinate-major (coded) or row-major
+    // exact rows.  Value operand (A of the value product): lane -> coordinate 16 b + col,
+    // positions 4 grp .. 4 grp + 3.
     u32x2 vh[NB], vl[NB];
     auto gather_v = [&]() {
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
             const int j = 16 * b + col;
-            if constexpr (F32) {
-                float f4[4];
+            if constexpr (EXACT) {
+                // rows past the exact slots in use hold no data: masked
+                if constexpr (F32) {
+                    float f4[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float t = sV[tm.vo[e] + j];
-                    f4[e] = j < tm.vr[e] ? t : 0.f;
+                    for (int e = 0; e < 4; ++e) {
+                        const float t = sV[tm.base + (4 * grp + e) * D + j];
+                        f4[e] = tm.i0 + 4 * grp + e < tm.T ? t : 0.f;
+                    }
+                    split4(f4, vh[b], vl[b]);
+                } else {
+                    us2 h[2];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int a = tm.i0 + 4 * grp + e < tm.T ? tm.base + (4 * grp + e) * D + j : DC_ZERO_BF16;
+                        h[e >> 1][e & 1] = sV[a];
+                    }
+                    vh[b] = u32x2{__builtin_bit_cast(uint32_t, h[0]), __builtin_bit_cast(uint32_t, h[1])};
+                    vl[b] = u32x2{0, 0};
                 }
-                split4(f4, vh[b], vl[b]);
             } else {
-                uint32_t h[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t t = sV[tm.vo[e] + j];
-                    h[e] = j < tm.vr[e] ? t : 0u;
+                // four consecutive positions at coordinate j; past the tile's size: the zeros
+                // after the stage
+                if constexpr (F32) {
+                    const int a = j < tm.m ? tm.base + 16 * j + 4 * grp : DC_STAGE_BYTES / 4;
+                    const f32x4 t = *reinterpret_cast<const f32x4*>(sV + a);
+                    const float f4[4] = {t[0], t[1], t[2], t[3]};
+                    split4(f4, vh[b], vl[b]);
+                } else {
+                    const int a = j < tm.m ? tm.base + 16 * j + 4 * grp : DC_ZERO_BF16;
+                    vh[b] = *reinterpret_cast<const u32x2*>(sV + a);
+                    vl[b] = u32x2{0, 0};
                 }
-                vh[b] = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
-                vl[b] = u32x2{0, 0};
             }
         }
     };
@@ -207,12 +229,12 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
     for (int s = 0; s < KS; ++s) {
         if (KS >= 4 && s == 2) __builtin_amdgcn_sched_barrier(0);
         const int c0 = 32 * s + 8 * grp;
-        int nv = tm.rk - c0;
+        int nv = tm.m - c0;
         nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
-        const int a = tm.ok + c0;
+        const int a = tm.base + col * (EXACT ? D : tm.m) + c0;
         u32x4 kh, kl;
         if constexpr (!F32) {
-            kh = keep_first(lds_row8_bf16(reinterpret_cast<const uint32_t*>(sK), a), nv);
+            kh = lds_row8_bf16(reinterpret_cast<const uint32_t*>(sK), a) & kmask[nv];
             kl = u32x4{0, 0, 0, 0};
         } else {
             float x8[8];
@@ -241,12 +263,16 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
     // Lazy reference: exponents are taken against m_run, which moves only when a score
     // exceeds it by more than 8 (so every p stays below e^8); sums and accumulators always
     // share the reference, so the result is the same softmax.
-    if (tmax > m_run + 8.f) {                // lane-local: this lane's query row
-        const float alpha = fast_exp(m_run - tmax);
+    // The reference moves for every lane at once, so the (rare) rescale is a wave-uniform
+    // branch; lanes whose maximum did not jump scale by 1.
+    const bool jump = tmax > m_run + 8.f;                // lane-local: this lane's query row
+    if (__builtin_amdgcn_ballot_w64(jump) != 0) {
+        const float m_new = jump ? tmax : m_run;
+        const float alpha = fast_exp(m_run - m_new);
         l_part *= alpha;
 #pragma unroll
         for (int b = 0; b < 8; ++b) acc[b] *= alpha;
-        m_run = tmax;
+        m_run = m_new;
     }
     float pv[4];
 #pragma unroll
@@ -341,34 +367,26 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     //          thread's 16 ranks, then a 16-lane scan of the threads of one chunk (one DPP
     //          row); ranks past the chunk's end count as 0
     if (r_ok) {
+        // tile k's size m_k = its first rank; offsets inside the chunk by a 16-lane scan
         const int cc = tid >> 4, k = tid & 15;
         const int64_t t0 = (int64_t)(c_lo + cc) * CHUNK;
         const int T = (int)((p.N - t0) < CHUNK ? (p.N - t0) : CHUNK);
-        uint32_t r[16];
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const uint32_t b = (rv[e >> 2] >> (8 * (e & 3))) & 0xFFu;
-            r[e] = 16 * k + e < T ? b : 0u;
-        }
-        uint32_t tot = 0;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) tot += r[e];
-        const uint32_t incl = row_scan16(tot);
-        uint32_t o = incl - tot;
-        uint32_t w[8];
-#pragma unroll
-        for (int e = 0; e < 16; e += 2) {
-            const uint32_t o0 = o;
-            o += r[e];
-            w[e >> 1] = o0 | (o << 16);
-            o += r[e + 1];
-        }
-        uint16_t* dst = sm.so + cc * DC_SO + 16 * k;
-        *reinterpret_cast<u32x4*>(dst) = u32x4{w[0], w[1], w[2], w[3]};
-        *reinterpret_cast<u32x4*>(dst + 8) = u32x4{w[4], w[5], w[6], w[7]};
-        if (k == 15) { sm.so[cc * DC_SO + 256] = (uint16_t)incl; sm.cT[cc] = T; }
+        const uint32_t mk = 16 * k < T ? (rv[0] & 0xFFu) : 0u;
+        const uint32_t incl = row_scan16(16u * mk);
+        sm.to[cc * DC_TO + k] = (uint16_t)(incl - 16u * mk);
+        if (k == 15) { sm.to[cc * DC_TO + 16] = (uint16_t)incl; sm.cT[cc] = T; }
     }
     if (!exact && tid < ncl) sm.cb[tid] = cbv;
+    // the V stage's pad holds zeros (coordinates past a token's rank read them), and the
+    // K-row masks: entry nv keeps the first nv bf16 elements of an 8-element piece
+    if (tid < DC_STAGE_PAD / 4) reinterpret_cast<uint32_t*>(sm.stV + DC_STAGE_BYTES)[tid] = 0u;
+    if (tid >= 64 && tid < 64 + 9) {
+        const int nv = tid - 64;
+        u32x4 mk;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) mk[k] = nv >= 2 * k + 2 ? 0xFFFFFFFFu : (nv == 2 * k + 1 ? 0x0000FFFFu : 0u);
+        sm.kmask[nv] = mk;
+    }
     __syncthreads();
 
     const int t_first = exact ? 0 : tau0;
@@ -383,12 +401,12 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     auto toff = [&](int tau) -> int {
         if (exact) return tau * 16 * D;
         const int cc = (tau >> 4) - c_lo;
-        return (int)sm.cb[cc] + sm.so[cc * DC_SO + 16 * (tau & 15)];
+        return (int)sm.cb[cc] + sm.to[cc * DC_TO + (tau & 15)];
     };
     auto tend = [&](int tau) -> int {
         if (exact) return min(16 * tau + 16, nexact) * D;
         const int cc = (tau >> 4) - c_lo;
-        return (int)sm.cb[cc] + sm.so[cc * DC_SO + 16 * (tau & 15) + 16];
+        return (int)sm.cb[cc] + sm.to[cc * DC_TO + (tau & 15) + 1];
     };
 
     float m_run = -INFINITY, l_part = 0.f;
@@ -509,47 +527,27 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
             const int ln = lane_now();
             const int col = ln & 15, grp = ln >> 4;
             TileMeta tm;
-            const int base = __builtin_amdgcn_readfirstlane(toff(tile) - s0);
-            int rmax;
+            tm.base = __builtin_amdgcn_readfirstlane(toff(tile) - s0);
             if (exact) {
                 tm.i0 = tile * 16;
                 tm.T = nexact;
-                rmax = D;
-                tm.rk = tm.i0 + col < tm.T ? D : 0;
-                tm.ok = base + col * D;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    tm.vr[e] = tm.i0 + 4 * grp + e < tm.T ? D : 0;
-                    tm.vo[e] = base + (4 * grp + e) * D;
-                }
+                tm.m = D;
+                const bool partial = tm.i0 + 16 > tm.T;
+                tile_step<F32, true, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
             } else {
                 const int cc = (tile >> 4) - c_lo;
                 tm.i0 = (tile & 15) * 16;
                 tm.T = __builtin_amdgcn_readfirstlane(sm.cT[cc]);
-                const uint16_t* so = sm.so + cc * DC_SO + tm.i0;
-                const int o0 = __builtin_amdgcn_readfirstlane((int)so[0]);
-                const int rel = base - o0;                       // stage offset = rel + so[i]
-                rmax = so[1] - o0;
-                const int oc = so[col];
-                tm.rk = so[col + 1] - oc;
-                tm.ok = rel + oc;
-                int ov[5];
-#pragma unroll
-                for (int e = 0; e < 5; ++e) ov[e] = so[4 * grp + e];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    tm.vr[e] = ov[e + 1] - ov[e];
-                    tm.vo[e] = rel + ov[e];
-                }
+                const uint16_t* to = sm.to + cc * DC_TO + (tile & 15);
+                tm.m = __builtin_amdgcn_readfirstlane(((int)to[1] - (int)to[0]) >> 4);
+                // a tile's size bounds its 32-coefficient score steps and 16-wide value
+                // blocks, as compile-time bounds (no branches inside)
+                const bool partial = __builtin_amdgcn_readfirstlane(tm.i0 + 16 > tm.T ? 1 : 0) != 0;
+                if (tm.m <= 16) tile_step<F32, false, 1, 1>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
+                else if (tm.m <= 32) tile_step<F32, false, 1, 2>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
+                else if (tm.m <= 64) tile_step<F32, false, 2, 4>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
+                else tile_step<F32, false, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
             }
-            // a tile's first token has its largest rank: 32-coefficient score steps and
-            // 16-wide value blocks it needs, as compile-time bounds (no branches inside)
-            rmax = __builtin_amdgcn_readfirstlane(rmax);
-            const bool partial = __builtin_amdgcn_readfirstlane(tm.i0 + 16 > tm.T ? 1 : 0) != 0;
-            if (rmax <= 16) tile_step<F32, 1, 1>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
-            else if (rmax <= 32) tile_step<F32, 1, 2>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
-            else if (rmax <= 64) tile_step<F32, 2, 4>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
-            else tile_step<F32, 4, 8>(tm, partial, sK, sV, sm.qf, ln, grp, m_run, l_part, acc);
         }
         ta = tbnd;
         if (ta >= t_end) break;

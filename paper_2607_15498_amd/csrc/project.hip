@@ -6,10 +6,12 @@
 //   1. The basis P (fp32) is split into bf16 hi + lo parts once per workgroup and kept in
 //      LDS in MFMA-fragment order (64 KB), so every product is P_hi x + P_lo x with exact
 //      bf16 x (fp32 x adds P_hi x_lo): about 2^-16 relative error before storage rounding.
-//   2. A wave takes 16-token tiles of the stored order (the tiles of a chunk rotate over the
-//      waves from chunk to chunk) and computes only the 16-row coefficient blocks below the
-//      tile's largest rank (its first token's).  The C tile (16 coefficients x 16 tokens)
-//      gives each lane four consecutive coefficients of one token's packed row.
+//   2. A wave takes 16-position tiles of the stored order (the tiles of a chunk rotate over
+//      the waves from chunk to chunk) and computes only the 16-row coefficient blocks below
+//      the tile's size m (its largest rank, its first position's).  The tile is stored as
+//      a rectangle with zeros past each position's rank: K as 16 rows of m coordinates (the
+//      C tile gives each lane four consecutive coordinates of one position), V as m rows of
+//      16 positions (C^T by swapped operands: four consecutive positions at one coordinate).
 //   3. The tile loop is fully unrolled with a fixed number of loads per tile: the layout rows
 //      of tile k + 4 and the token rows of tile k + 3 are requested while tile k is computed,
 //      and tile k's coefficients stay in registers until the data of tile k + 1 has landed.
@@ -28,8 +30,9 @@ constexpr int PJ_HT = 16;                             // tokens per tile
 constexpr int PJ_TPC = CHUNK / PJ_HT;                 // tiles per chunk
 constexpr int PJ_ITERS = PJ_CPW * PJ_TPC / PJ_WAVES;  // tiles per wave
 constexpr int PJ_FRAGS = 8 * 4;                       // (16-row block a, 32-col step s) pairs
-constexpr int PJ_XD = 3;                              // token rows requested this many tiles ahead
-constexpr int PJ_MD = PJ_XD + 1;                      // layout rows one tile further
+// token rows are requested XD tiles ahead (fp32 rows are twice as large: one tile less),
+// layout rows one tile further
+template <bool F32> __host__ __device__ constexpr int pj_xd() { return F32 ? 2 : 3; }
 static_assert(PJ_CPW * PJ_TPC % PJ_WAVES == 0, "whole tiles per wave");
 
 static inline size_t project_smem_bytes() { return (size_t)PJ_FRAGS * 64 * 16 * 2; }
@@ -47,13 +50,15 @@ struct PjX {                                           // B fragments of the til
     u32x4 b[F32 ? 4 : 1];                              // fp32: second half of each 8-element run
 };
 
-// Coefficients of one tile held for the late store, and where they go.
+// Coefficients of one tile held for the late store, and where they go.  K lanes hold four
+// consecutive coordinates of one position, V lanes four consecutive positions at one
+// coordinate; entries past a position's rank are already zero.
 template <bool F32>
 struct PjOut {
     uint32_t v[8][F32 ? 4 : 2];                        // per 16-row block: 4 values (packed bf16)
     int na;                                            // blocks computed (uniform)
-    int r;                                             // this lane's token rank (clamped)
-    int64_t dst;                                       // element index of the token's row
+    int m;                                             // the tile's size: its largest rank (uniform)
+    uint32_t off;                                      // the tile's first element in the head stream
 };
 
 __device__ __forceinline__ void pj_tile_of(int k, int wave, int c0, int& c, int& h) {
@@ -110,48 +115,47 @@ __device__ __forceinline__ void pj_load_x(PjX<F32>& x, const void* X, uint32_t t
     }
 }
 
-// Tile k: ranks / offsets from the layout rows, then the coefficient blocks into `o`.
+// Tile k: its size and place from the layout rows, then the coefficient blocks into `o`:
+// C = P x (K: lane -> position col, coordinates 16 a + 4 grp ..) or C^T = x^T P^T (V: lane
+// -> coordinate 16 a + col, positions 4 grp ..), with zeros past each position's rank.
 template <bool F32>
 __device__ __forceinline__ void pj_compute(PjOut<F32>& o, const PjMeta& m, const PjX<F32>& x, int k,
-                                           int wave, int c0, int n_chunks, int64_t N,
-                                           const uint32_t* __restrict__ chunk_off, int g,
+                                           int wave, int c0, int n_chunks, int64_t N, bool is_v,
+                                           const uint32_t* __restrict__ chunk_off,
                                            int64_t coef_stride, const u32x4* frag_hi,
                                            const u32x4* frag_lo) {
-    const int lane = threadIdx.x & 63, col = lane & 15;
+    const int lane = threadIdx.x & 63, col = lane & 15, grp = lane >> 4;
     int c, h;
     pj_tile_of(k, wave, c0, c, h);
     const bool live = c < n_chunks;
     const int64_t t0 = (int64_t)c * CHUNK;
     const int T = live ? (int)(N - t0 < CHUNK ? N - t0 : CHUNK) : 0;
-    // bytes past the chunk's end weigh nothing
+    // bytes past the chunk's end weigh nothing (absent positions: rank 0)
     uint32_t quad = m.quad;
     const int nv = T - 4 * lane;
     quad = nv >= 4 ? quad : (nv <= 0 ? 0u : quad & ((1u << (8 * nv)) - 1u));
-    const uint32_t qs = (quad & 0xFF) + ((quad >> 8) & 0xFF) + ((quad >> 16) & 0xFF) + (quad >> 24);
-    uint32_t incl = qs;
+    // tile sizes: the first rank of every 16 positions (byte 0 of quads 0, 4, 8, ..), and
+    // their prefix up to tile h
+    uint32_t incl = (lane & 3) == 0 ? (quad & 0xFF) : 0u;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
         const uint32_t y = __shfl_up(incl, off, 64);
         if (lane >= off) incl += y;
     }
-    // this lane's token: slot 16 h + col = byte (col % 4) of quad (4 h + col / 4)
-    const int src = 4 * h + (col >> 2), byte = col & 3;
-    const uint32_t q_i = __shfl(quad, src, 64);
-    const uint32_t e_i = __shfl(incl - qs, src, 64);
-    uint32_t below = 0;
-#pragma unroll
-    for (int b = 0; b < 3; ++b)
-        if (b < byte) below += (q_i >> (8 * b)) & 0xFF;
-    const int r_i = (int)((q_i >> (8 * byte)) & 0xFF);
-    const int rmax = (int)(__shfl(quad, 4 * h, 64) & 0xFF);   // the tile's first token
+    const int mt = __builtin_amdgcn_readfirstlane((int)(__shfl(quad, 4 * h, 64) & 0xFF));
+    const uint32_t before = __builtin_amdgcn_readfirstlane(__shfl(incl, 4 * h, 64)) - (uint32_t)mt;
     const uint32_t base = live ? chunk_off[c] : 0u;
-    // stores stay inside the head's stream whatever the layout tables hold
-    const int64_t room = coef_stride - ((int64_t)base + e_i + below);
-    o.r = live ? (room < r_i ? (room > 0 ? (int)room : 0) : r_i) : 0;
-    o.dst = (int64_t)g * coef_stride + base + e_i + below;
-    int na = (rmax + 15) >> 4;
-    na = live ? (na < D / 16 ? na : D / 16) : 0;
+    o.off = __builtin_amdgcn_readfirstlane(base + 16u * before);
+    o.m = mt;
+    // the tile stays inside the head's stream whatever the layout tables hold
+    const bool fits = (int64_t)o.off + 16 * (int64_t)mt <= coef_stride;
+    int na = (mt + 15) >> 4;
+    na = live && fits ? (na < D / 16 ? na : D / 16) : 0;
     o.na = __builtin_amdgcn_readfirstlane(na);
+    // ranks: K -> this lane's position 16 h + col; V -> positions 16 h + 4 grp .. + 3
+    const uint32_t qk = __shfl(quad, 4 * h + (col >> 2), 64);
+    const int rk = (int)((qk >> (8 * (col & 3))) & 0xFF);
+    const uint32_t qv = __shfl(quad, 4 * h + grp, 64);
 
     u32x4 xh[4], xl[4];
 #pragma unroll
@@ -177,71 +181,101 @@ __device__ __forceinline__ void pj_compute(PjOut<F32>& o, const PjMeta& m, const
         for (int s = 0; s < 4; ++s) {
             const u32x4 ph = frag_hi[(a * 4 + s) * 64 + lane];
             const u32x4 pl = frag_lo[(a * 4 + s) * 64 + lane];
-            acc = mfma(ph, xh[s], acc);
-            acc = mfma(pl, xh[s], acc);
-            if constexpr (F32) acc = mfma(ph, xl[s], acc);
+            if (!is_v) {
+                acc = mfma(ph, xh[s], acc);
+                acc = mfma(pl, xh[s], acc);
+                if constexpr (F32) acc = mfma(ph, xl[s], acc);
+            } else {
+                acc = mfma(xh[s], ph, acc);
+                acc = mfma(xh[s], pl, acc);
+                if constexpr (F32) acc = mfma(xl[s], ph, acc);
+            }
+        }
+        // zeros past each position's rank
+        float val[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = is_v ? 16 * a + col : 16 * a + 4 * grp + v;
+            const int r = is_v ? (int)((qv >> (8 * v)) & 0xFF) : rk;
+            val[v] = j < r ? acc[v] : 0.f;
         }
         if constexpr (F32) {
 #pragma unroll
-            for (int v = 0; v < 4; ++v) o.v[a][v] = __float_as_uint(acc[v]);
+            for (int v = 0; v < 4; ++v) o.v[a][v] = __float_as_uint(val[v]);
         } else {
-            o.v[a][0] = cvt_bf16x2(acc[0], acc[1]);
-            o.v[a][1] = cvt_bf16x2(acc[2], acc[3]);
+            o.v[a][0] = cvt_bf16x2(val[0], val[1]);
+            o.v[a][1] = cvt_bf16x2(val[2], val[3]);
         }
     }
 }
 
-// Store a computed tile: rows j0 .. j0 + 3 (j0 = 16 a + 4 grp) of this lane's token, at once
-// unless the row ends inside them.
+// Store a computed tile.  K: rows of m coordinates, the lane's four coordinates at once
+// unless the row ends inside them.  V: coordinate rows of 16 positions, the lane's four
+// positions at once (aligned: tiles start at multiples of 16 elements).
 template <bool F32>
-__device__ __forceinline__ void pj_store(const PjOut<F32>& o, void* __restrict__ coef) {
-    const int grp = (threadIdx.x & 63) >> 4;
+__device__ __forceinline__ void pj_store(const PjOut<F32>& o, bool is_v, void* __restrict__ coef) {
+    const int lane = threadIdx.x & 63, col = lane & 15, grp = lane >> 4;
 #pragma unroll
     for (int a = 0; a < D / 16; ++a) {
         if (a >= o.na) break;
-        const int j0 = 16 * a + 4 * grp;
-        if constexpr (F32) {
-            float* p = (float*)coef + o.dst + j0;
-            if (j0 + 4 <= o.r) {
-                __builtin_memcpy(p, &o.v[a][0], 16);
-            } else {
-#pragma unroll
-                for (int v = 0; v < 3; ++v)
-                    if (j0 + v < o.r) p[v] = __uint_as_float(o.v[a][v]);
+        if (is_v) {
+            const int j = 16 * a + col;
+            if (j < o.m) {
+                const int64_t e = (int64_t)o.off + 16 * j + 4 * grp;
+                if constexpr (F32) __builtin_memcpy((float*)coef + e, &o.v[a][0], 16);
+                else {
+                    const uint2 pk = make_uint2(o.v[a][0], o.v[a][1]);
+                    *reinterpret_cast<uint2*>((uint16_t*)coef + e) = pk;
+                }
             }
         } else {
-            uint16_t* p = (uint16_t*)coef + o.dst + j0;
-            if (j0 + 4 <= o.r) {
-                const uint2 pk = make_uint2(o.v[a][0], o.v[a][1]);
-                __builtin_memcpy(p, &pk, 8);
+            const int j0 = 16 * a + 4 * grp;
+            const int64_t e = (int64_t)o.off + (int64_t)col * o.m + j0;
+            if constexpr (F32) {
+                float* p = (float*)coef + e;
+                if (j0 + 4 <= o.m) {
+                    __builtin_memcpy(p, &o.v[a][0], 16);
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 3; ++v)
+                        if (j0 + v < o.m) p[v] = __uint_as_float(o.v[a][v]);
+                }
             } else {
-                if (j0 < o.r) p[0] = (uint16_t)o.v[a][0];
-                if (j0 + 1 < o.r) p[1] = (uint16_t)(o.v[a][0] >> 16);
-                if (j0 + 2 < o.r) p[2] = (uint16_t)o.v[a][1];
+                uint16_t* p = (uint16_t*)coef + e;
+                if (j0 + 4 <= o.m) {
+                    const uint2 pk = make_uint2(o.v[a][0], o.v[a][1]);
+                    __builtin_memcpy(p, &pk, 8);
+                } else {
+                    if (j0 < o.m) p[0] = (uint16_t)o.v[a][0];
+                    if (j0 + 1 < o.m) p[1] = (uint16_t)(o.v[a][0] >> 16);
+                    if (j0 + 2 < o.m) p[2] = (uint16_t)o.v[a][1];
+                }
             }
         }
     }
 }
 
-template <bool F32>
-__global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
+template <bool F32, bool IS_V>
+__device__ __forceinline__ void project_body(
     const void* __restrict__ K, const void* __restrict__ V, const float* __restrict__ PK,
     const float* __restrict__ PV, int64_t N, int G, int w, const uint8_t* __restrict__ srank,
     const uint32_t* __restrict__ sidx, const uint32_t* __restrict__ chunk_off, int n_chunks,
     void* __restrict__ coef_k, void* __restrict__ coef_v, int64_t coef_stride,
-    void* __restrict__ k_exact, void* __restrict__ v_exact, int64_t cap) {
-    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    void* __restrict__ k_exact, void* __restrict__ v_exact, int64_t cap, uint8_t* smem) {
     u32x4* frag_hi = reinterpret_cast<u32x4*>(smem);
     u32x4* frag_lo = frag_hi + PJ_FRAGS * 64;
 
-    const int g = blockIdx.y, kv = blockIdx.z;
+    const int g = blockIdx.y, kv = IS_V ? 1 : 0;
     const void* X = kv ? V : K;
-    void* coef = kv ? coef_v : coef_k;
+    // this head's stream
+    void* coef = (uint8_t*)(kv ? coef_v : coef_k) + (int64_t)g * coef_stride * (F32 ? 4 : 2);
+    constexpr bool is_v = IS_V;
     const float* P = (kv ? PV : PK) + (int64_t)g * D * D;
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c0 = blockIdx.x * PJ_CPW;
 
+    constexpr int PJ_XD = pj_xd<F32>(), PJ_MD = PJ_XD + 1;
     // ---- layout rows of the first PJ_MD tiles and the basis, all requested at once
     PjMeta m[PJ_ITERS];
     PjX<F32> x[PJ_ITERS];
@@ -279,13 +313,13 @@ __global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
     for (int k = 0; k < PJ_ITERS; ++k) {
         pj_ready(x[k]);
         if (k + PJ_XD < PJ_ITERS) pj_ready(m[k + PJ_XD].tok);
-        if (k > 0) pj_store<F32>(o, coef);                               // tile k - 1, late
+        if (k > 0) pj_store<F32>(o, is_v, coef);                         // tile k - 1, late
         if (k + PJ_MD < PJ_ITERS) m[k + PJ_MD] = pj_load_meta(k + PJ_MD, wave, c0, n_chunks, N, srank, sidx);
         if (k + PJ_XD < PJ_ITERS) pj_load_x<F32>(x[k + PJ_XD], X, m[k + PJ_XD].tok, N, G, g);
-        pj_compute<F32>(o, m[k], x[k], k, wave, c0, n_chunks, N, chunk_off, g, coef_stride,
+        pj_compute<F32>(o, m[k], x[k], k, wave, c0, n_chunks, N, is_v, chunk_off, coef_stride,
                         frag_hi, frag_lo);
     }
-    pj_store<F32>(o, coef);
+    pj_store<F32>(o, is_v, coef);
 
     // ---- exact window rows (chunk group 0 only)
     if (blockIdx.x == 0) {
@@ -300,6 +334,24 @@ __global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
             *reinterpret_cast<u32x4*>(dst + d0) = *reinterpret_cast<const u32x4*>(src + so);
         }
     }
+}
+
+// K (blockIdx.z = 0) and V (blockIdx.z = 1) in one launch; their stores differ, so each
+// half runs its own instance of the body.
+template <bool F32>
+__global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
+    const void* __restrict__ K, const void* __restrict__ V, const float* __restrict__ PK,
+    const float* __restrict__ PV, int64_t N, int G, int w, const uint8_t* __restrict__ srank,
+    const uint32_t* __restrict__ sidx, const uint32_t* __restrict__ chunk_off, int n_chunks,
+    void* __restrict__ coef_k, void* __restrict__ coef_v, int64_t coef_stride,
+    void* __restrict__ k_exact, void* __restrict__ v_exact, int64_t cap) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    if (blockIdx.z == 0)
+        project_body<F32, false>(K, V, PK, PV, N, G, w, srank, sidx, chunk_off, n_chunks, coef_k, coef_v,
+                                 coef_stride, k_exact, v_exact, cap, smem);
+    else
+        project_body<F32, true>(K, V, PK, PV, N, G, w, srank, sidx, chunk_off, n_chunks, coef_k, coef_v,
+                                coef_stride, k_exact, v_exact, cap, smem);
 }
 
 template <bool F32>

@@ -50,6 +50,9 @@ def shape_of(vr, cfg, n=None, kappa=None, r_min=None, w=None):
 
 
 def expected_layout(rank, N):
+    """Storage order and chunk offsets of the tile-rectangle layout (the header's contract):
+    chunks of 256 tokens stored by (rank descending, index ascending); tile h of a chunk (its
+    stored slots 16h .. 16h + 15) takes 16 * m_h elements, m_h = its first slot's rank."""
     srank = np.empty(N, np.int64)
     sidx = np.empty(N, np.int64)
     nch = (N + 255) // 256
@@ -59,22 +62,36 @@ def expected_layout(rank, N):
         order = np.lexsort((t, -rank[t]))
         sidx[t] = t[order]
         srank[t] = rank[t][order]
-        chunk_off[c + 1] = chunk_off[c] + rank[t].sum()
+        chunk_off[c + 1] = chunk_off[c] + 16 * srank[t][::16].sum()
     return srank, sidx, chunk_off
 
 
-def unpack(coef, srank, sidx, chunk_off, N, d=128):
-    """GPU packed streams [G][stride] -> [N][G][d] (zeros past each rank).  Chunks are
-    contiguous, so stored token i starts at the exclusive prefix sum of srank."""
+def unpack(coef, srank, sidx, chunk_off, N, kind, d=128):
+    """GPU streams [G][stride] -> [N][G][d] (zeros past each rank).  Tile h of chunk c sits at
+    chunk_off[c] + 16 * (sum of the chunk's earlier tile maxima): for K, 16 rows of m_h
+    coordinates; for V, m_h coordinate rows of 16 slots.  Asserts that every element past a
+    slot's rank (and every element of an absent slot) is zero."""
     G = coef.shape[0]
     out = np.zeros((N, G, d), np.float32)
-    B = int(srank.sum())
-    assert B == chunk_off[-1]
-    starts = np.concatenate([[0], np.cumsum(srank)[:-1]])
-    tok = np.repeat(sidx, srank)
-    j = np.arange(B) - np.repeat(starts, srank)
-    for g in range(G):
-        out[tok, g, j] = coef[g, :B]
+    nch = (N + 255) // 256
+    for c in range(nch):
+        t0 = c * 256
+        T = min(256, N - t0)
+        base = int(chunk_off[c])
+        for h in range(16):
+            if 16 * h >= T:
+                break
+            m = int(srank[t0 + 16 * h])
+            blk = coef[:, base:base + 16 * m].astype(np.float32)
+            blk = blk.reshape(G, 16, m) if kind == "K" else blk.reshape(G, m, 16).transpose(0, 2, 1)
+            for i in range(16):
+                slot = t0 + 16 * h + i
+                r = int(srank[slot]) if 16 * h + i < T else 0
+                assert np.all(blk[:, i, r:] == 0), (kind, c, h, i)
+                if r:
+                    out[sidx[slot], :, :r] = blk[:, i, :r]
+            base += 16 * m
+        assert base == chunk_off[c + 1]
     return out
 
 
@@ -203,7 +220,7 @@ def test_layout_and_projection(vr, oracle_lib, name):
     assert np.array_equal(host(cache.sidx).astype(np.int64), sidx)
     assert np.array_equal(host(cache.chunk_off).astype(np.int64), chunk_off)
     for kind, ref, X in (("K", oc.coefK, li.K), ("V", oc.coefV, li.V)):
-        got = unpack(host(cache.coef_k if kind == "K" else cache.coef_v), srank, sidx, chunk_off, N)
+        got = unpack(host(cache.coef_k if kind == "K" else cache.coef_v), srank, sidx, chunk_off, N, kind)
         err = np.abs(got - ref)
         # The kernel forms P x from bf16 hi + lo parts of P (and of x when x is fp32), each
         # product within 2^-18 |P_ji x_i|, summed in fp32: |error| <= 2^-18 sum_i |P_ji x_i|
