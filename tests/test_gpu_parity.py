@@ -264,6 +264,34 @@ def test_decode_parity_same_ranks(vr, oracle_lib, name):
         assert e <= tol
 
 
+@pytest.mark.parametrize("name,Q,law,check", [("llama_32k", 1, "aware", 1),       # 4 rows per KV head
+                                                ("qwen_16k_stack", 1, "aware", 1),  # 7 rows
+                                                ("llama_32k", 4, "aware", 4),       # 16 rows
+                                                ("agnostic_32k", 64, "agnostic", 6)])  # 256 rows
+def test_decode_row_tiles(vr, oracle_lib, name, Q, law, check):
+    """Decode at full size in each query-row grouping the kernel has: row tiles of at most
+    4 rows (four 16-position tiles per MFMA group), at most 8 (two), and 16-row tiles (one
+    each; 16 row tiles for 64 queries).  `check` queries, spread over the batch, are compared
+    with the oracle one by one."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = CONFIGS[name]
+    say(f"[decode rows] {name} Q={Q} ({law})")
+    li = make_layer(cfg, n_queries=Q, query_law=law)
+    oc = oracle_compress(oracle_lib, name, li, cfg["kappa"], cfg["r_min"], tag=f"rows{Q}{law}")
+    shape = shape_of(vr, cfg)
+    cache, _, PK, PV = gpu_compress(vr, shape, li, sbar=oc.sbar)
+    assert np.array_equal(host(cache.rank).astype(np.int64), oc.alloc.rank)
+    out = host(vr.decode(shape, [cache], dev(li.q, shape.torch_dtype), PK, PV))
+    torch.cuda.synchronize()
+    worst = 0.0
+    for i in np.linspace(0, Q - 1, check).astype(int):
+        o_or = oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[i], cfg["H"])
+        worst = max(worst, decode_err(out[i], o_or))
+    say(f"  worst decode rel err {worst:.3e} over {check} queries")
+    assert worst <= DEC_TOL_BF16
+
+
 @pytest.mark.parametrize("name", ["tiny", "llama_32k"])
 def test_end_to_end(vr, oracle_lib, name):
     """GPU salience feeds the GPU allocation; the oracle runs independently throughout."""
