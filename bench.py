@@ -39,7 +39,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=48)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="llama_32k")
+    ap.add_argument("--config", default="llama_32k",
+                    choices=("llama_32k", "llama_128k_stack", "qwen_16k_stack", "agnostic_32k"),
+                    help="llama_32k: the headline layer (default).  The others are the model-stack "
+                         "and query-agnostic workloads, reported in their own JSON line")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=("bench", "pmc"), default="bench",
                     help="pmc: a short run for hardware-counter passes (eager decodes on distinct "
@@ -123,6 +126,10 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this codec has no "
               "multi-GPU path", file=sys.stderr)
         sys.exit(2)
+    if args.config in ("llama_128k_stack", "qwen_16k_stack"):
+        return bench_stack(args)
+    if args.config == "agnostic_32k":
+        return bench_agnostic(args)
     import torch
 
     import paper_2607_15498_amd as vr
@@ -268,6 +275,197 @@ def main():
     }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, li, shape, dbytes)
+    print(json.dumps(result), flush=True)
+
+
+def _graph_ms(g_, reps):
+    """Average ms of one replay of a captured graph (events on the current stream)."""
+    import torch
+    g_.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g_.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def bench_stack(args):
+    """Whole model stack: every layer (and sequence) drawn on the device, compressed, then
+    decode steps of one query per sequence over all layers (one decode call per layer, the
+    batch's caches in that call).  Compress and decode are timed from captured graphs.  The
+    Qwen batch decodes with 128 tokens appended to every exact tail (the middle of its 256
+    steps); the Llama 128K stack decodes right after the prompt."""
+    import torch
+
+    import paper_2607_15498_amd as vr
+    from workloads import CONFIGS, make_head_model
+    from workloads.synth_gpu import make_layer_device
+
+    cfg = CONFIGS[args.config]
+    L, S, n, w = cfg["layers"], cfg["batch"], cfg["n"], cfg["w"]
+    extra = 128 if S > 1 else 0
+    dev = torch.device("cuda:0")
+    shape = vr.Shape(n=n, G=cfg["G"], H=cfg["H"], w=w, r_min=cfg["r_min"], kappa_pct=cfg["kappa"],
+                     dtype=cfg["dtype"])
+    dt = shape.torch_dtype
+    up = lambda a, t=dt: torch.from_numpy(np.ascontiguousarray(a)).to(t).to(dev)
+    t0 = time.perf_counter()
+    inputs, caches, bases, qs = [], [], [], []
+    for l in range(L):
+        hms = [make_head_model(cfg["seed"], l, g, cfg["d"]) for g in range(cfg["G"])]
+        row, qrow = [], []
+        for sq in range(S):
+            dl = make_layer_device(cfg, layer=l, seq=sq, head_models=hms, with_basis=(sq == 0), device=dev)
+            if sq == 0:
+                bases.append((up(dl.PK, torch.float32), up(dl.PV, torch.float32)))
+            row.append((dl.K, dl.V, up(dl.Qw)))
+            qrow.append(dl.q)
+        inputs.append(row)
+        caches.append([vr.new_cache(shape, cap=w + 2 * extra + 8, device=dev) for _ in range(S)])
+        qs.append(up(np.stack(qrow)))
+    torch.cuda.synchronize()
+    t_draw = time.perf_counter() - t0
+    ws_c = torch.zeros(vr.library().varrate_compress_workspace_bytes(__import__("ctypes").byref(shape.c())),
+                       dtype=torch.uint8, device=dev)
+    ws_d = vr.decode_workspace(shape, S, 1, dev)
+
+    def compress_all():
+        for l in range(L):
+            for sq in range(S):
+                K, V, Qw = inputs[l][sq]
+                vr.compress(shape, K, V, Qw, bases[l][0], bases[l][1], cache=caches[l][sq], workspace=ws_c)
+    compress_all()
+    torch.cuda.synchronize()
+    if extra:
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(cfg["seed"])
+        for l in range(L):
+            for sq in range(S):
+                for _ in range(extra):
+                    kv = torch.randn((2, cfg["G"], cfg["d"]), generator=gen, device=dev).to(dt)
+                    vr.append_exact(shape, caches[l][sq], kv[0], kv[1])
+        torch.cuda.synchronize()
+    outs = [torch.empty_like(qs[l]) for l in range(L)]
+
+    def step():
+        for l in range(L):
+            vr.decode(shape, caches[l], qs[l], bases[l][0], bases[l][1], out=outs[l], workspace=ws_d)
+    step()
+    torch.cuda.synchronize()
+    cap = torch.cuda.Stream()
+    g_step, g_comp = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_step, stream=cap):
+        step()
+    if extra == 0:   # re-compressing resets the exact tails, so only without appended tokens
+        with torch.cuda.graph(g_comp, stream=cap):
+            compress_all()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        g_step.replay()
+    torch.cuda.synchronize()
+    ms_step = _graph_ms(g_step, max(args.steps, 1))
+    ms_comp = _graph_ms(g_comp, 2) if extra == 0 else None
+    if ms_comp is None:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        compress_all()
+        e1.record()
+        torch.cuda.synchronize()
+        ms_comp_eager = e0.elapsed_time(e1)
+    dbytes = sum(decode_bytes(shape, c) for row in caches for c in row)
+    gbs = dbytes / (ms_step * 1e-3) / 1e9
+    result = {
+        "metric": "compressed decode attn GB/s (% HBM peak) + compress ms per 32K tokens, 1 GPU",
+        "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg["dtype"], "data": "synthetic, drawn on the device (same recipe as the parity inputs, "
+                                        "device Philox draws per layer/head/sequence)",
+        "config": {"workload": f"{args.config}: {L} layers, {cfg['G']} KV x {cfg['H']} q heads, d 128, "
+                               f"n {n}, w {w}, budget {cfg['kappa']}%, r_min {cfg['r_min']}, "
+                               f"batch {S} independent sequences, decode exact tail w + {extra}",
+                   "decode_calls_per_step": L},
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "decode_tokens_per_s": round(S / (ms_step * 1e-3), 1),
+        "decode_bytes_per_step": int(dbytes),
+        "compress_ms_per_32k_tokens": round((ms_comp if ms_comp is not None else ms_comp_eager)
+                                            * 32768 / (n * S), 4),
+        "compress_timing": "graph replay" if ms_comp is not None else "eager (events around all calls)",
+        "compress_ms_total": round(ms_comp if ms_comp is not None else ms_comp_eager, 3),
+        "draw_s": round(t_draw, 1),
+    }
+    print(json.dumps(result), flush=True)
+
+
+def bench_agnostic(args):
+    """Query-agnostic reuse: one 32K prefix compressed once per budget (10/20/40%; r_min 8 at
+    10%, where 16 is infeasible in per-head units), then 64 fresh Gaussian queries decoded as
+    one batch.  Reports decode GB/s per budget and the error of VarRate and of the uniform
+    ("flat") allocation at the same budget against full-KV attention over the uncompressed
+    bf16 cache (fp32 reference on the device)."""
+    import torch
+
+    import paper_2607_15498_amd as vr
+    from workloads import CONFIGS
+    from workloads.synth_gpu import make_layer_device
+
+    cfg = CONFIGS[args.config]
+    Qn, n, w, G, H = cfg["queries"], cfg["n"], cfg["w"], cfg["G"], cfg["H"]
+    dev = torch.device("cuda:0")
+    dl = make_layer_device(cfg, n_queries=Qn, query_law="agnostic", device=dev)
+    up = lambda a, t=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(t).to(dev)
+    PK, PV, Qw, q = up(dl.PK, torch.float32), up(dl.PV, torch.float32), up(dl.Qw), up(dl.q)
+    # full-KV attention reference (fp32), [Q][H][d]
+    hpg = H // G
+    ref = torch.empty((Qn, H, 128), dtype=torch.float32, device=dev)
+    for h in range(H):
+        g = h // hpg
+        sc = (q[:, h].float() @ dl.K[:, g].float().T) / np.sqrt(128.0)
+        ref[:, h] = torch.softmax(sc, dim=-1) @ dl.V[:, g].float()
+
+    def rel_l2(out):
+        e = (out.float() - ref).norm(dim=-1) / ref.norm(dim=-1)
+        e = e.flatten().cpu().numpy()
+        return {"mean": round(float(e.mean()), 5), "p95": round(float(np.percentile(e, 95)), 5),
+                "max": round(float(e.max()), 5)}
+
+    rows = []
+    for kappa, r_min in cfg["budgets"]:
+        shape = vr.Shape(n=n, G=G, H=H, w=w, r_min=r_min, kappa_pct=kappa, dtype="bf16")
+        cache = vr.compress(shape, dl.K, dl.V, Qw, PK, PV)
+        flat = vr.new_cache(shape, device=dev)
+        vr.allocate(shape, torch.full((shape.N,), 0.5, dtype=torch.float32, device=dev), flat)
+        vr.project(shape, dl.K, dl.V, PK, PV, flat)
+        ws = vr.decode_workspace(shape, 1, Qn, dev)
+        out = torch.empty_like(q)
+        vr.decode(shape, [cache], q, PK, PV, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        err_v = rel_l2(out)
+        vr.decode(shape, [flat], q, PK, PV, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        err_f = rel_l2(out)
+        g_ = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        with torch.cuda.graph(g_, stream=cap):
+            vr.decode(shape, [cache], q, PK, PV, out=out, workspace=ws)
+        ms = _graph_ms(g_, 20)
+        by = decode_bytes(shape, cache, Qn)
+        rows.append({"budget_pct": kappa, "r_min": r_min, "decode_ms": round(ms, 4),
+                     "decode_GBps": round(by / (ms * 1e-3) / 1e9, 1), "decode_bytes": int(by),
+                     "rel_l2_err_varrate": err_v, "rel_l2_err_flat": err_f})
+    main_row = next(r for r in rows if r["budget_pct"] == 20)
+    result = {
+        "metric": "compressed decode attn GB/s (% HBM peak), batch of 64 query-agnostic queries, 1 GPU",
+        "value": main_row["decode_GBps"], "unit": "GB/s", "n_gpus": 1, "steps": 20, "warmup": 1,
+        "ms_per_step": main_row["decode_ms"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (device draws, fresh Gaussian decode queries independent of the window)",
+        "config": {"workload": f"agnostic_32k: 1 layer, {G} KV x {H} q heads, d 128, n {n}, w {w}, "
+                               f"{Qn} queries per call"},
+        "budgets": rows,
+    }
     print(json.dumps(result), flush=True)
 
 

@@ -292,6 +292,57 @@ def test_decode_row_tiles(vr, oracle_lib, name, Q, law, check):
     assert worst <= DEC_TOL_BF16
 
 
+def test_llama_128k_layer(vr, oracle_lib):
+    """One layer of the Llama-3.1-8B-shaped 128K stack at full size (n = 131072, 8 KV x 32
+    query heads): salience, bit-exact ranks on the oracle's pooled salience, and decode."""
+    import torch
+    from workloads import CONFIGS
+    name = "llama_128k_stack"
+    cfg = CONFIGS[name]
+    say(f"[128k] drawing layer 0 (n={cfg['n']})")
+    li = layer(name, n_queries=1)
+    oc = oracle_compress(oracle_lib, name, li, cfg["kappa"], cfg["r_min"])
+    shape = shape_of(vr, cfg)
+    _, sb, _, _ = gpu_compress(vr, shape, li)
+    g, o = host(sb).astype(np.float64), oc.sbar.astype(np.float64)
+    big = o >= 1e-6 * o.max()
+    sal = float((np.abs(g[big] - o[big]) / o[big]).max())
+    cache, _, PK, PV = gpu_compress(vr, shape, li, sbar=oc.sbar)
+    mism = int((host(cache.rank).astype(np.int64) != oc.alloc.rank).sum())
+    out = host(vr.decode(shape, [cache], dev(li.q, shape.torch_dtype), PK, PV))
+    torch.cuda.synchronize()
+    o_or = oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[0], cfg["H"])
+    e = decode_err(out[0], o_or)
+    say(f"  salience max rel {sal:.2e}; rank mismatches {mism}; decode err {e:.3e}")
+    assert sal <= SAL_RTOL and mism == 0 and e <= DEC_TOL_BF16
+
+
+def test_qwen_stack_batch8(vr, oracle_lib):
+    """Qwen2.5-7B-shaped stack (4 KV x 28 query heads, n = 16384): the first and last of its
+    28 layers for all 8 independent sequences, decoded as one batch of 8 caches per layer
+    (7 query rows per KV head), every sequence against the oracle."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = CONFIGS["qwen_16k_stack"]
+    shape = shape_of(vr, cfg)
+    for lyr in (0, cfg["layers"] - 1):
+        caches, qs, refs = [], [], []
+        for sq in range(cfg["batch"]):
+            li = make_layer(cfg, layer=lyr, seq=sq, n_queries=1)
+            oc = oracle_lib.compress(li.K, li.V, li.Qw, li.PK, li.PV, cfg["H"], cfg["kappa"], cfg["r_min"], "bf16")
+            cache, _, PK, PV = gpu_compress(vr, shape, li, sbar=oc.sbar)
+            assert np.array_equal(host(cache.rank).astype(np.int64), oc.alloc.rank), (lyr, sq)
+            caches.append(cache)
+            qs.append(li.q)
+            refs.append(oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV,
+                                          li.q[0], cfg["H"]))
+        out = host(vr.decode(shape, caches, dev(np.stack(qs), torch.bfloat16), PK, PV))
+        torch.cuda.synchronize()
+        worst = max(decode_err(out[sq][0], refs[sq]) for sq in range(cfg["batch"]))
+        say(f"[qwen stack] layer {lyr}: worst decode err over {cfg['batch']} sequences {worst:.3e}")
+        assert worst <= DEC_TOL_BF16
+
+
 @pytest.mark.parametrize("name", ["tiny", "llama_32k"])
 def test_end_to_end(vr, oracle_lib, name):
     """GPU salience feeds the GPU allocation; the oracle runs independently throughout."""
