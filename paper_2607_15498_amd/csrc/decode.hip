@@ -4,22 +4,27 @@
 // orthonormal key basis <q, P_K^T (m . c)> = <P_K q, m . c>, and the value side is linear,
 // so  o = P_V^T (sum_t p_t m_t . c^V_t) + sum_e p_e v_e.
 //
-// Grid (n_wg + 1, G * nqt, S).  Workgroup x = 0 attends to the exact slots (window +
-// appended tokens) in the original space; workgroup x >= 1 streams the 16-token tiles
-// [(x-1) tpw, x tpw) of KV head g's stored tokens (tile t = chunk t/16, slots 16 (t%16)..),
-// for one sequence and one tile of up to 16 query rows (row = query * H/G + head).  Per workgroup (8 waves, two workgroups per CU):
-//   1. q' = P_K[g] q / sqrt(d) by MFMA (basis split into bf16 hi + lo parts, ~2^-16 error),
-//      while the chunks' stored ranks are fetched with one vector load per 16 tokens;
-//   2. waves take 16-token tiles of the rank-sorted storage.  Each lane gathers its MFMA
-//      operands straight from the packed ragged rows: 16-byte row segments for the score
-//      tile (16 tokens x 32 coefficients per step, masked past each token's rank) and, for
-//      the value tile, 4 tokens' coefficients at one rank index.  The score C fragment
-//      (lane = query row, 4 tokens) is exactly the A fragment of the 16x16x16 value MFMA,
-//      so the online softmax needs no shuffles; p is split into bf16 hi + lo parts;
-//   3. the waves' (max, sum, acc) are combined in a fixed order into one partial record;
-//   4. a second launch (one workgroup per sequence, head and row tile) loads every partial
-//      with coalesced vector loads, merges them by log-sum-exp, rotates the rank-space sum
-//      back with P_V^T (MFMA) and adds the exact part.
+// Grid: (n_wg + 1) workgroups per unit (sequence, KV head, tile of up to 16 query rows,
+// row = query * H/G + head), on a 1D grid in which consecutive workgroups take consecutive
+// units.  Workgroup x = 0 attends to the exact slots (window + appended tokens) in the
+// original space; workgroup x >= 1 streams the 16-token tiles [(x-1) tpw, x tpw) of KV head
+// g's stored tokens (tile t = chunk t/16, slots 16 (t%16)..).  Per workgroup (8 waves, two
+// workgroups per CU):
+//   1. the chunks' stored ranks are fetched with one vector load per 16 tokens and turned
+//      into tile offsets; q' = P_K[g] q / sqrt(d) by MFMA (basis split into bf16 hi + lo
+//      parts, ~2^-16 error);
+//   2. the tile range is cut into rounds that fit one 16 KB buffer per stream; two rounds
+//      are in flight at a time (double-buffered direct-to-LDS loads, a fixed number per
+//      wave and round), so a round's tiles run while the next round lands;
+//   3. waves take 16-token tiles of the rank-sorted storage and gather their MFMA operands
+//      from the tile rectangles in LDS: 16-byte row pieces for the score tile (16 tokens x
+//      32 coefficients per step) and, for the value tile, 4 positions at one coordinate.
+//      The score C fragment (lane = query row, 4 tokens) is the B operand of the transposed
+//      16x16x16 value MFMA, so the online softmax is lane-local;
+//   4. the waves' (max, sum, acc) are combined in a fixed order into one partial record;
+//   5. a second launch (one workgroup per unit) loads every partial with coalesced vector
+//      loads, merges them by log-sum-exp, rotates the rank-space sum back with P_V^T (MFMA)
+//      and adds the exact part.
 // A tile's first token has the largest rank (storage is rank-descending per chunk), which
 // bounds its MFMA steps: ceil(r_max/32) score steps and ceil(r_max/16) value blocks.
 #include "vr_internal.h"
@@ -36,6 +41,7 @@ constexpr int DC_MAX_REC = 512;            // partial records per (sequence, hea
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
 __device__ __forceinline__ f32x4 mfma16(u32x2 a, u32x2 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, a),
@@ -79,16 +85,17 @@ __device__ __forceinline__ void split4(const float* x, u32x2& hi, u32x2& lo) {
 // Staging: each round copies a contiguous coefficient range of both streams (K and V share
 // one layout) into LDS with direct-to-LDS 16-byte loads, every unit of the round in flight
 // at once; the waves then run their tiles from LDS.
-constexpr int DC_STAGE_BYTES = 30720;                         // per stream and round
+constexpr int DC_STAGE_BYTES = 16384;                         // per stream, round and buffer
 constexpr int DC_STAGE_PAD = 64;                              // over-read slack of row gathers
+constexpr int DC_LPR = 2 * DC_STAGE_BYTES / 1024 / DC_WAVES;  // loads per wave per round (K and V)
 constexpr int DC_TO = 18;                                     // tile offsets per chunk: 17, padded
 constexpr int DC_CROW = D + 4;                                // comb row stride (floats)
 constexpr int DC_ZERO_BF16 = DC_STAGE_BYTES / 2;               // V stage element in the zeroed pad
 typedef unsigned short us2 __attribute__((ext_vector_type(2)));
 
 struct DecSmem {
-    uint8_t* stK;     // [DC_STAGE_BYTES + pad] staged K coefficients of the round; after the
-    uint8_t* stV;     //   tiles: per-wave partial sums comb [4][nr4][128] f32 (spans both)
+    uint8_t* stK;     // [2][DC_STAGE_BYTES + pad] staged K coefficients, two rounds in flight;
+    uint8_t* stV;     //   [2][..] V; after the tiles: per-wave partial sums comb [4][nr4][128] f32
     float* comb;
     u32x4* qf;        // [4 steps][hi, lo][64 lanes] score B-operand fragments
     float* cm;        // [8][16]
@@ -104,8 +111,8 @@ struct DecSmem {
 __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
     DecSmem s;
     uint8_t* b = smem;
-    s.stK = b; b += DC_STAGE_BYTES + DC_STAGE_PAD;
-    s.stV = b; b += DC_STAGE_BYTES + DC_STAGE_PAD;
+    s.stK = b; b += 2 * (DC_STAGE_BYTES + DC_STAGE_PAD);
+    s.stV = b; b += 2 * (DC_STAGE_BYTES + DC_STAGE_PAD);
     s.comb = reinterpret_cast<float*>(s.stK);
     s.qf = reinterpret_cast<u32x4*>(b); b += 4 * 2 * 64 * 16;
     float* f = reinterpret_cast<float*>(b);
@@ -121,7 +128,7 @@ __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
 }
 
 static inline size_t decode_smem_bytes(int cpw) {
-    return 2 * (size_t)(DC_STAGE_BYTES + DC_STAGE_PAD) + 4 * 2 * 64 * 16 +
+    return 4 * (size_t)(DC_STAGE_BYTES + DC_STAGE_PAD) + 4 * 2 * 64 * 16 +
            (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW + 9 * 4) * 4 + (size_t)cpw * DC_TO * 2;
 }
 
@@ -379,7 +386,8 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     if (!exact && tid < ncl) sm.cb[tid] = cbv;
     // the V stage's pad holds zeros (coordinates past a token's rank read them), and the
     // K-row masks: entry nv keeps the first nv bf16 elements of an 8-element piece
-    if (tid < DC_STAGE_PAD / 4) reinterpret_cast<uint32_t*>(sm.stV + DC_STAGE_BYTES)[tid] = 0u;
+    if (tid < DC_STAGE_PAD / 2)     // the zeroed pad after each V buffer
+        reinterpret_cast<uint32_t*>(sm.stV + (tid >> 4) * (DC_STAGE_BYTES + DC_STAGE_PAD) + DC_STAGE_BYTES)[tid & 15] = 0u;
     if (tid >= 64 && tid < 64 + 9) {
         const int nv = tid - 64;
         u32x4 mk;
@@ -414,51 +422,61 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
 #pragma unroll
     for (int b = 0; b < 8; ++b) acc[b] = f32x4{0, 0, 0, 0};
 
-    // ---- 2a. round plan (wave-uniform): tiles [ta, tbnd) whose span fits the stage.  The
+    // ---- 2a. round plans (wave-uniform): tiles [ta, tb) whose span fits one buffer.  The
     //          span is clamped to the head's buffer, so no metadata can send a load past it.
-    int ta = t_first, tbnd = t_first, s0 = 0, nu = 0;
-    auto plan = [&]() {
-        tbnd = ta;
-        s0 = 0;
-        nu = 0;
+    struct Round { int ta, tb, s0, nu; };
+    auto plan = [&](int ta) -> Round {
+        Round r{ta, ta, 0, 0};
         if (ta < t_end) {
-            s0 = __builtin_amdgcn_readfirstlane(toff(ta) & ~(EPU - 1));
+            r.s0 = __builtin_amdgcn_readfirstlane(toff(ta) & ~(EPU - 1));
             const int ln = lane_now();
             for (;;) {
-                const int cand = tbnd + ln;
-                const bool fit = cand < t_end && tend(cand) - s0 <= SE;
+                const int cand = r.tb + ln;
+                const bool fit = cand < t_end && tend(cand) - r.s0 <= SE;
                 const uint64_t m = __ballot(fit);
                 const int cnt = m == ~0ull ? 64 : __builtin_ctzll(~m);
-                tbnd += cnt;
+                r.tb += cnt;
                 if (cnt < 64) break;
             }
-            int n_ = (tend(tbnd - 1) - s0 + EPU - 1) / EPU;
-            const int room = s0 >= 0 && s0 < limit ? (limit - s0) / EPU : 0;
+            int n_ = (tend(r.tb - 1) - r.s0 + EPU - 1) / EPU;
+            const int room = r.s0 >= 0 && r.s0 < limit ? (limit - r.s0) / EPU : 0;
             n_ = n_ < 0 ? 0 : (n_ > room ? room : n_);
             n_ = n_ > SE / EPU ? SE / EPU : n_;
-            nu = __builtin_amdgcn_readfirstlane(n_);
+            r.nu = __builtin_amdgcn_readfirstlane(n_);
         }
+        return r;
     };
-    // ---- 2b. the round's units go straight to LDS: one load moves 64 lanes x 16 bytes to
-    //          a contiguous 1 KB block of the stage; wave w moves blocks w, w + 8, ..
-    auto issue = [&]() {
-        const uint8_t* kr = kg + (size_t)s0 * sizeof(ET);     // wave-uniform round bases
-        const uint8_t* vr = vg + (size_t)s0 * sizeof(ET);
+    // ---- 2b. a round's units go straight to LDS buffer `buf`: one load moves 64 lanes x 16
+    //          bytes to a contiguous 1 KB block; wave w moves blocks w and w + 8 of K and of
+    //          V.  Every wave issues exactly DC_LPR loads per round, whatever the round holds
+    //          (lanes and blocks past its units reload its first unit into the unused tail of
+    //          the buffer), so a wait for "all but the next round's DC_LPR loads" is exact.
+    //          Issued in asm, so the compiler adds no wait of its own for them.
+    auto issue = [&](const Round& r, int buf) {
+        const uint8_t* kr = kg + (size_t)r.s0 * sizeof(ET);     // wave-uniform round bases
+        const uint8_t* vr = vg + (size_t)r.s0 * sizeof(ET);
         const int wv = __builtin_amdgcn_readfirstlane(wave);
+        uint8_t* bk = sm.stK + buf * (DC_STAGE_BYTES + DC_STAGE_PAD);
+        uint8_t* bv = sm.stV + buf * (DC_STAGE_BYTES + DC_STAGE_PAD);
 #pragma unroll
-        for (int k = 0; k < (DC_STAGE_BYTES / 1024 + DC_WAVES - 1) / DC_WAVES; ++k) {
+        for (int k = 0; k < DC_STAGE_BYTES / 1024 / DC_WAVES; ++k) {
             const int m = wv + DC_WAVES * k;
             const uint32_t u = (uint32_t)(64 * m + lane_now());
-            if (64 * m < nu) {
-                if ((int)u < nu) {
-                    __builtin_amdgcn_global_load_lds(kr + 16u * u, (lds_void*)(sm.stK + 1024 * m), 16, 0, 0);
-                    __builtin_amdgcn_global_load_lds(vr + 16u * u, (lds_void*)(sm.stV + 1024 * m), 16, 0, 0);
-                }
-            }
+            const uint32_t uu = (int)u < r.nu ? u : 0u;
+            const uint8_t* srck = kr + 16u * uu;
+            const uint8_t* srcv = vr + 16u * uu;
+            const uint32_t dk = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_u8*)(bk + 1024 * m));
+            const uint32_t dv = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_u8*)(bv + 1024 * m));
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(srck), "s"(dk) : "memory", "m0");
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(srcv), "s"(dv) : "memory", "m0");
         }
     };
-    plan();
-    issue();
+    Round cur = plan(t_first);
+    issue(cur, 0);
+    Round nxt = plan(cur.tb);
+    issue(nxt, 1);
     // ---- 2c. while the round is in flight: score-operand fragments of the query rows
     //          (lane -> query row col, K group grp; bf16 hi and lo parts).  The basis and
     //          query loads landed with the rank loads (issued before them), so nothing here
@@ -514,13 +532,17 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     }
 
 
-    for (;;) {
-        __builtin_amdgcn_s_waitcnt(0);   // this wave's direct-to-LDS loads have landed
+    for (int rd = 0;; ++rd) {
+        // this wave's loads of round rd have landed (only the next round's are younger),
+        // then every wave's
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"(DC_LPR) : "memory");
         __syncthreads();
 
-        // ---- 3. tiles of the round, from LDS
-        const ET* sK = reinterpret_cast<const ET*>(sm.stK);
-        const ET* sV = reinterpret_cast<const ET*>(sm.stV);
+        // ---- 3. tiles of the round, from LDS buffer rd & 1
+        const int buf = rd & 1;
+        const ET* sK = reinterpret_cast<const ET*>(sm.stK + buf * (DC_STAGE_BYTES + DC_STAGE_PAD));
+        const ET* sV = reinterpret_cast<const ET*>(sm.stV + buf * (DC_STAGE_BYTES + DC_STAGE_PAD));
+        const int ta = cur.ta, tbnd = cur.tb, s0 = cur.s0;
         for (int tile = ta + __builtin_amdgcn_readfirstlane(wave); tile < tbnd; tile += DC_WAVES) {
             // lane-derived addresses are recomputed per tile (a few ALU ops) rather than
             // hoisted out of the loop for all four tile shapes and spilled
@@ -549,12 +571,15 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
                 else tile_step<F32, false, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
             }
         }
-        ta = tbnd;
-        if (ta >= t_end) break;
-        plan();
-        __syncthreads();   // every wave is done with the stage
-        issue();
+        if (tbnd >= t_end) break;
+        __syncthreads();   // every wave is done with buffer rd & 1
+        cur = nxt;
+        nxt = plan(cur.tb);
+        issue(nxt, buf);
     }
+    // the loads past the last round (into the idle buffer) land before the buffers are reused
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
 
     // ---- 4. combine the waves of this workgroup (fixed order).  Lane (col, grp) holds query
     //          row col: running max m_run, its share of the sum, O[col][16 b + 4 grp + v].
