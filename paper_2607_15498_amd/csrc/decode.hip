@@ -449,7 +449,7 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     // ---- 2b. a round's units go straight to LDS buffer `buf`: one load moves 64 lanes x 16
     //          bytes to a contiguous 1 KB block; wave w moves blocks w and w + 8 of K and of
     //          V.  Every wave issues exactly DC_LPR loads per round, whatever the round holds
-    //          (lanes and blocks past its units reload its first unit into the unused tail of
+    //          (lanes and blocks past its units reload its last unit into the unused tail of
     //          the buffer), so a wait for "all but the next round's DC_LPR loads" is exact.
     //          Issued in asm, so the compiler adds no wait of its own for them.
     auto issue = [&](const Round& r, int buf) {
@@ -462,7 +462,8 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         for (int k = 0; k < DC_STAGE_BYTES / 1024 / DC_WAVES; ++k) {
             const int m = wv + DC_WAVES * k;
             const uint32_t u = (uint32_t)(64 * m + lane_now());
-            const uint32_t uu = (int)u < r.nu ? u : 0u;
+            // past the round's end: the round's last unit, a line this load already fetches
+            const uint32_t uu = (int)u < r.nu ? u : (r.nu > 0 ? (uint32_t)(r.nu - 1) : 0u);
             const uint8_t* srck = kr + 16u * uu;
             const uint8_t* srcv = vr + 16u * uu;
             const uint32_t dk = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_u8*)(bk + 1024 * m));
