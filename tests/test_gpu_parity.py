@@ -399,6 +399,29 @@ def test_decode_multi_sequence_many_queries_appended(vr, oracle_lib):
     assert worst <= DEC_TOL_BF16
 
 
+def test_decode_more_sequences_than_one_launch(vr, oracle_lib):
+    """S = 20 sequences in one call: more than the 16 a launch carries, so the call splits
+    into two launch pairs with their own records; every sequence against the oracle."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = dict(CONFIGS["llama_32k"])
+    cfg.update(n=700, G=2, H=8, seed=19)
+    shape = vr.Shape(n=700, G=2, H=8, w=32, r_min=16, kappa_pct=25, dtype="bf16")
+    caches, qs, refs = [], [], []
+    for sq in range(20):
+        li = make_layer(cfg, seq=sq, n_queries=1)
+        oc = oracle_lib.compress(li.K, li.V, li.Qw, li.PK, li.PV, 8, 25, 16, "bf16")
+        cache, _, PK, PV = gpu_compress(vr, shape, li, sbar=oc.sbar)
+        caches.append(cache)
+        qs.append(li.q)
+        refs.append(oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[0], 8))
+    out = host(vr.decode(shape, caches, dev(np.stack(qs), torch.bfloat16), PK, PV))
+    torch.cuda.synchronize()
+    worst = max(decode_err(out[sq][0], refs[sq]) for sq in range(20))
+    say(f"[20 sequences] worst decode rel err {worst:.3e}")
+    assert worst <= DEC_TOL_BF16
+
+
 @pytest.mark.parametrize("n,w,kappa,r_min", [(33, 32, 100, 16), (40, 32, 90, 0), (287, 32, 50, 16),
                                              (289, 32, 25, 4), (600, 1, 30, 16), (2080, 32, 100, 16)])
 def test_ragged_and_degenerate(vr, oracle_lib, n, w, kappa, r_min):
