@@ -160,6 +160,54 @@ __device__ __forceinline__ int lane_now() {
     return l;
 }
 
+// The value-product accumulators O^T (8 blocks of 16 rank coordinates x 16 query rows, one
+// f32x4 per lane per block) live in AGPRs a0..a31 for the whole tile loop: block b in
+// a[4b .. 4b + 3].  The MFMAs that update them, their rare rescale and the final read-out
+// are inline asm naming those registers, so the compiler never moves them between
+// registers at the joins of the tile loop (which it otherwise does with a copy of all 32
+// accumulators per tile).  Every statement lists them as clobbered, so the kernel's
+// register allocation counts them and the compiler keeps nothing of its own there.
+// Hazards are padded by hand: 2 wait states from a VALU write of an operand to the first
+// MFMA, 24 from the last MFMA to a VALU read of its result, 5 from an AGPR write by VALU to
+// an MFMA that accumulates into it.
+#define ACC_AGPRS "a0", "a1", "a2", "a3", "a4", "a5", "a6", "a7", "a8", "a9", "a10", "a11", "a12", "a13", "a14", "a15", "a16", "a17", "a18", "a19", "a20", "a21", "a22", "a23", "a24", "a25", "a26", "a27", "a28", "a29", "a30", "a31"
+__device__ __forceinline__ void acc_zero() {
+    asm volatile("v_accvgpr_write_b32 a0, 0\n\t" "v_accvgpr_write_b32 a1, 0\n\t" "v_accvgpr_write_b32 a2, 0\n\t" "v_accvgpr_write_b32 a3, 0\n\t" "v_accvgpr_write_b32 a4, 0\n\t" "v_accvgpr_write_b32 a5, 0\n\t" "v_accvgpr_write_b32 a6, 0\n\t" "v_accvgpr_write_b32 a7, 0\n\t" "v_accvgpr_write_b32 a8, 0\n\t" "v_accvgpr_write_b32 a9, 0\n\t" "v_accvgpr_write_b32 a10, 0\n\t" "v_accvgpr_write_b32 a11, 0\n\t" "v_accvgpr_write_b32 a12, 0\n\t" "v_accvgpr_write_b32 a13, 0\n\t" "v_accvgpr_write_b32 a14, 0\n\t" "v_accvgpr_write_b32 a15, 0\n\t" "v_accvgpr_write_b32 a16, 0\n\t" "v_accvgpr_write_b32 a17, 0\n\t" "v_accvgpr_write_b32 a18, 0\n\t" "v_accvgpr_write_b32 a19, 0\n\t" "v_accvgpr_write_b32 a20, 0\n\t" "v_accvgpr_write_b32 a21, 0\n\t" "v_accvgpr_write_b32 a22, 0\n\t" "v_accvgpr_write_b32 a23, 0\n\t" "v_accvgpr_write_b32 a24, 0\n\t" "v_accvgpr_write_b32 a25, 0\n\t" "v_accvgpr_write_b32 a26, 0\n\t" "v_accvgpr_write_b32 a27, 0\n\t" "v_accvgpr_write_b32 a28, 0\n\t" "v_accvgpr_write_b32 a29, 0\n\t" "v_accvgpr_write_b32 a30, 0\n\t" "v_accvgpr_write_b32 a31, 0\n\t" "s_nop 4\n\t" ::: ACC_AGPRS);
+}
+template <int NB> __device__ __forceinline__ void acc_mfma_bf16(const u32x2* vh, u32x2 ph);
+template <> __device__ __forceinline__ void acc_mfma_bf16<1>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %1, a[0:3]\n\t" :: "v"(vh[0]), "v"(ph) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_bf16<2>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %2, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %2, a[4:7]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(ph) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_bf16<4>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %4, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %4, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %4, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %4, a[12:15]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(ph) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_bf16<8>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %8, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %8, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %8, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %8, a[12:15]\n\t" "v_mfma_f32_16x16x16_bf16 a[16:19], %4, %8, a[16:19]\n\t" "v_mfma_f32_16x16x16_bf16 a[20:23], %5, %8, a[20:23]\n\t" "v_mfma_f32_16x16x16_bf16 a[24:27], %6, %8, a[24:27]\n\t" "v_mfma_f32_16x16x16_bf16 a[28:31], %7, %8, a[28:31]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(vh[4]), "v"(vh[5]), "v"(vh[6]), "v"(vh[7]), "v"(ph) : ACC_AGPRS);
+}
+template <int NB> __device__ __forceinline__ void acc_mfma_f32(const u32x2* vh, const u32x2* vl, u32x2 ph, u32x2 pl);
+template <> __device__ __forceinline__ void acc_mfma_f32<1>(const u32x2* vh, const u32x2* vl, u32x2 ph, u32x2 pl) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %2, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %3, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %1, %2, a[0:3]\n\t" :: "v"(vh[0]), "v"(vl[0]), "v"(ph), "v"(pl) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_f32<2>(const u32x2* vh, const u32x2* vl, u32x2 ph, u32x2 pl) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %4, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %5, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %2, %4, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %4, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %5, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %3, %4, a[4:7]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vl[0]), "v"(vl[1]), "v"(ph), "v"(pl) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_f32<4>(const u32x2* vh, const u32x2* vl, u32x2 ph, u32x2 pl) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %8, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %9, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %4, %8, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %8, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %9, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %5, %8, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %8, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %9, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %6, %8, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %8, a[12:15]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %9, a[12:15]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %7, %8, a[12:15]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(vl[0]), "v"(vl[1]), "v"(vl[2]), "v"(vl[3]), "v"(ph), "v"(pl) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_f32<8>(const u32x2* vh, const u32x2* vl, u32x2 ph, u32x2 pl) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %16, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %17, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %8, %16, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %16, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %17, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %9, %16, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %16, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %17, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %10, %16, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %16, a[12:15]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %17, a[12:15]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %11, %16, a[12:15]\n\t" "v_mfma_f32_16x16x16_bf16 a[16:19], %4, %16, a[16:19]\n\t" "v_mfma_f32_16x16x16_bf16 a[16:19], %4, %17, a[16:19]\n\t" "v_mfma_f32_16x16x16_bf16 a[16:19], %12, %16, a[16:19]\n\t" "v_mfma_f32_16x16x16_bf16 a[20:23], %5, %16, a[20:23]\n\t" "v_mfma_f32_16x16x16_bf16 a[20:23], %5, %17, a[20:23]\n\t" "v_mfma_f32_16x16x16_bf16 a[20:23], %13, %16, a[20:23]\n\t" "v_mfma_f32_16x16x16_bf16 a[24:27], %6, %16, a[24:27]\n\t" "v_mfma_f32_16x16x16_bf16 a[24:27], %6, %17, a[24:27]\n\t" "v_mfma_f32_16x16x16_bf16 a[24:27], %14, %16, a[24:27]\n\t" "v_mfma_f32_16x16x16_bf16 a[28:31], %7, %16, a[28:31]\n\t" "v_mfma_f32_16x16x16_bf16 a[28:31], %7, %17, a[28:31]\n\t" "v_mfma_f32_16x16x16_bf16 a[28:31], %15, %16, a[28:31]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(vh[4]), "v"(vh[5]), "v"(vh[6]), "v"(vh[7]), "v"(vl[0]), "v"(vl[1]), "v"(vl[2]), "v"(vl[3]), "v"(vl[4]), "v"(vl[5]), "v"(vl[6]), "v"(vl[7]), "v"(ph), "v"(pl) : ACC_AGPRS);
+}
+__device__ __forceinline__ void acc_scale(float alpha) {
+    float t0, t1, t2, t3;
+    asm volatile("s_nop 15\n\ts_nop 7\n\t" "v_accvgpr_read_b32 %0, a0\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a0, %0\n\t" "v_accvgpr_read_b32 %1, a1\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a1, %1\n\t" "v_accvgpr_read_b32 %2, a2\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a2, %2\n\t" "v_accvgpr_read_b32 %3, a3\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a3, %3\n\t" "v_accvgpr_read_b32 %0, a4\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a4, %0\n\t" "v_accvgpr_read_b32 %1, a5\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a5, %1\n\t" "v_accvgpr_read_b32 %2, a6\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a6, %2\n\t" "v_accvgpr_read_b32 %3, a7\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a7, %3\n\t" "v_accvgpr_read_b32 %0, a8\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a8, %0\n\t" "v_accvgpr_read_b32 %1, a9\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a9, %1\n\t" "v_accvgpr_read_b32 %2, a10\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a10, %2\n\t" "v_accvgpr_read_b32 %3, a11\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a11, %3\n\t" "v_accvgpr_read_b32 %0, a12\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a12, %0\n\t" "v_accvgpr_read_b32 %1, a13\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a13, %1\n\t" "v_accvgpr_read_b32 %2, a14\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a14, %2\n\t" "v_accvgpr_read_b32 %3, a15\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a15, %3\n\t" "v_accvgpr_read_b32 %0, a16\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a16, %0\n\t" "v_accvgpr_read_b32 %1, a17\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a17, %1\n\t" "v_accvgpr_read_b32 %2, a18\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a18, %2\n\t" "v_accvgpr_read_b32 %3, a19\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a19, %3\n\t" "v_accvgpr_read_b32 %0, a20\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a20, %0\n\t" "v_accvgpr_read_b32 %1, a21\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a21, %1\n\t" "v_accvgpr_read_b32 %2, a22\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a22, %2\n\t" "v_accvgpr_read_b32 %3, a23\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a23, %3\n\t" "v_accvgpr_read_b32 %0, a24\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a24, %0\n\t" "v_accvgpr_read_b32 %1, a25\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a25, %1\n\t" "v_accvgpr_read_b32 %2, a26\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a26, %2\n\t" "v_accvgpr_read_b32 %3, a27\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a27, %3\n\t" "v_accvgpr_read_b32 %0, a28\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a28, %0\n\t" "v_accvgpr_read_b32 %1, a29\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a29, %1\n\t" "v_accvgpr_read_b32 %2, a30\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a30, %2\n\t" "v_accvgpr_read_b32 %3, a31\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a31, %3\n\t" "s_nop 4\n\t" : "=&v"(t0), "=&v"(t1), "=&v"(t2), "=&v"(t3) : "v"(alpha) : ACC_AGPRS);
+}
+__device__ __forceinline__ void acc_read(f32x4 (&acc)[8]) {
+    asm volatile("s_nop 15\n\ts_nop 7\n\t" "v_accvgpr_read_b32 %0, a0\n\t" "v_accvgpr_read_b32 %1, a1\n\t" "v_accvgpr_read_b32 %2, a2\n\t" "v_accvgpr_read_b32 %3, a3\n\t" "v_accvgpr_read_b32 %4, a4\n\t" "v_accvgpr_read_b32 %5, a5\n\t" "v_accvgpr_read_b32 %6, a6\n\t" "v_accvgpr_read_b32 %7, a7\n\t" "v_accvgpr_read_b32 %8, a8\n\t" "v_accvgpr_read_b32 %9, a9\n\t" "v_accvgpr_read_b32 %10, a10\n\t" "v_accvgpr_read_b32 %11, a11\n\t" "v_accvgpr_read_b32 %12, a12\n\t" "v_accvgpr_read_b32 %13, a13\n\t" "v_accvgpr_read_b32 %14, a14\n\t" "v_accvgpr_read_b32 %15, a15\n\t" "v_accvgpr_read_b32 %16, a16\n\t" "v_accvgpr_read_b32 %17, a17\n\t" "v_accvgpr_read_b32 %18, a18\n\t" "v_accvgpr_read_b32 %19, a19\n\t" "v_accvgpr_read_b32 %20, a20\n\t" "v_accvgpr_read_b32 %21, a21\n\t" "v_accvgpr_read_b32 %22, a22\n\t" "v_accvgpr_read_b32 %23, a23\n\t" "v_accvgpr_read_b32 %24, a24\n\t" "v_accvgpr_read_b32 %25, a25\n\t" "v_accvgpr_read_b32 %26, a26\n\t" "v_accvgpr_read_b32 %27, a27\n\t" "v_accvgpr_read_b32 %28, a28\n\t" "v_accvgpr_read_b32 %29, a29\n\t" "v_accvgpr_read_b32 %30, a30\n\t" "v_accvgpr_read_b32 %31, a31\n\t" : "=v"(acc[0][0]), "=v"(acc[0][1]), "=v"(acc[0][2]), "=v"(acc[0][3]), "=v"(acc[1][0]), "=v"(acc[1][1]), "=v"(acc[1][2]), "=v"(acc[1][3]), "=v"(acc[2][0]), "=v"(acc[2][1]), "=v"(acc[2][2]), "=v"(acc[2][3]), "=v"(acc[3][0]), "=v"(acc[3][1]), "=v"(acc[3][2]), "=v"(acc[3][3]), "=v"(acc[4][0]), "=v"(acc[4][1]), "=v"(acc[4][2]), "=v"(acc[4][3]), "=v"(acc[5][0]), "=v"(acc[5][1]), "=v"(acc[5][2]), "=v"(acc[5][3]), "=v"(acc[6][0]), "=v"(acc[6][1]), "=v"(acc[6][2]), "=v"(acc[6][3]), "=v"(acc[7][0]), "=v"(acc[7][1]), "=v"(acc[7][2]), "=v"(acc[7][3]) :: ACC_AGPRS);
+}
+
 // One 16-position tile in the stage (wave-uniform): its first position i0 inside the chunk
 // (or the exact rows), the chunk's valid positions T, the stage offset of its first element
 // and its size m (coded: the largest rank of the tile; exact rows: 128).
@@ -178,7 +226,7 @@ template <bool F32, bool EXACT, int KS, int NB>
 __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, const typename Elem<F32>::T* sK,
                                           const typename Elem<F32>::T* sV, const u32x4* qf,
                                           const u32x4* kmask, int lane, int grp, float& m_run,
-                                          float& l_part, f32x4 (&acc)[8]) {
+                                          float& l_part) {
     const int col = lane & 15;
     // K rows of a coded tile are m coordinates apart (exact rows: 128) with zeros past each
     // position's rank; a row piece past the row's end (into the next row, the pad or the LDS
@@ -277,8 +325,7 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
         const float m_new = jump ? tmax : m_run;
         const float alpha = fast_exp(m_run - m_new);
         l_part *= alpha;
-#pragma unroll
-        for (int b = 0; b < 8; ++b) acc[b] *= alpha;
+        acc_scale(alpha);
         m_run = m_new;
     }
     float pv[4];
@@ -290,17 +337,11 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
     if constexpr (F32) {
         u32x2 ph, pl;
         split4(pv, ph, pl);
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            acc[b] = mfma16(vh[b], ph, acc[b]);
-            acc[b] = mfma16(vh[b], pl, acc[b]);
-            acc[b] = mfma16(vl[b], ph, acc[b]);
-        }
+        acc_mfma_f32<NB>(vh, vl, ph, pl);
     } else {
         // bf16 storage: one bf16 rounding of p (relative 2^-9, far inside the output bound)
         const u32x2 ph = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
-#pragma unroll
-        for (int b = 0; b < NB; ++b) acc[b] = mfma16(vh[b], ph, acc[b]);
+        acc_mfma_bf16<NB>(vh, ph);
     }
 }
 
@@ -323,6 +364,9 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     const int rows = min(16, p.rows_total - 16 * qt);
     const int nr4 = (rows + 3) & ~3;
     const bool exact = x == 0;
+    // the later-dispatched half of the grid shares CUs with the earlier half; give its waves
+    // the higher issue priority so both workgroups on a CU progress alike
+    if (L >= (int)(gridDim.x >> 1)) __builtin_amdgcn_s_setprio(1);
     const int xc = x - 1;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));   // scalar
     int lane = lane_now(), tid = 64 * wave + lane, grp = lane >> 4, col = lane & 15;
@@ -418,9 +462,7 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     };
 
     float m_run = -INFINITY, l_part = 0.f;
-    f32x4 acc[8];
-#pragma unroll
-    for (int b = 0; b < 8; ++b) acc[b] = f32x4{0, 0, 0, 0};
+    acc_zero();
 
     // ---- 2a. round plans (wave-uniform): tiles [ta, tb) whose span fits one buffer.  The
     //          span is clamped to the head's buffer, so no metadata can send a load past it.
@@ -556,7 +598,7 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
                 tm.T = nexact;
                 tm.m = D;
                 const bool partial = tm.i0 + 16 > tm.T;
-                tile_step<F32, true, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
+                tile_step<F32, true, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
             } else {
                 const int cc = (tile >> 4) - c_lo;
                 tm.i0 = (tile & 15) * 16;
@@ -566,10 +608,10 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
                 // a tile's size bounds its 32-coefficient score steps and 16-wide value
                 // blocks, as compile-time bounds (no branches inside)
                 const bool partial = __builtin_amdgcn_readfirstlane(tm.i0 + 16 > tm.T ? 1 : 0) != 0;
-                if (tm.m <= 16) tile_step<F32, false, 1, 1>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
-                else if (tm.m <= 32) tile_step<F32, false, 1, 2>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
-                else if (tm.m <= 64) tile_step<F32, false, 2, 4>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
-                else tile_step<F32, false, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part, acc);
+                if (tm.m <= 16) tile_step<F32, false, 1, 1>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                else if (tm.m <= 32) tile_step<F32, false, 1, 2>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                else if (tm.m <= 64) tile_step<F32, false, 2, 4>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                else tile_step<F32, false, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
             }
         }
         if (tbnd >= t_end) break;
@@ -578,6 +620,8 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         nxt = plan(cur.tb);
         issue(nxt, buf);
     }
+    f32x4 acc[8];
+    acc_read(acc);
     // the loads past the last round (into the idle buffer) land before the buffers are reused
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();

@@ -112,3 +112,41 @@ def test_status_strings(L):
     assert L.varrate_status_string(0) == b"ok"
     assert L.varrate_status_string(-2) == b"infeasible budget"
     assert L.varrate_version() == 1
+
+
+def test_decode_accumulator_agprs_are_private():
+    """The decode kernel keeps its value-product accumulators in AGPRs a0..a31 named by inline
+    asm.  That is only sound if the compiler itself never places a value in an AGPR: check
+    the generated gfx950 code of both decode kernels (outside the inline asm blocks) for any
+    AGPR operand, and that every kernel that uses AGPRs declares exactly the 32."""
+    import shutil
+    import subprocess
+    import tempfile
+    from paper_2607_15498_amd import build as B
+    if shutil.which("hipcc") is None:
+        pytest.skip("hipcc not available")
+    src = os.path.join(B.CSRC, "decode.hip")
+    with tempfile.TemporaryDirectory() as td:
+        out = os.path.join(td, "decode.s")
+        cmd = ["hipcc", *B.FLAGS, *B.SOURCE_FLAGS.get("decode.hip", []), "-S", "--offload-device-only",
+               src, "-o", out]
+        r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+        assert r.returncode == 0, r.stdout[-2000:]
+        text = open(out).read()
+    agpr = re.compile(r"\ba\d+\b|\ba\[\d+:\d+\]|v_accvgpr")
+    kernels = re.findall(r"^(_ZN2vr13decode_kernelILb[01]EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm", text, re.S | re.M)
+    assert len(kernels) == 2
+    for name, body in kernels:
+        inside = False
+        for line in body.splitlines():
+            if ";;#ASMSTART" in line:
+                inside = True
+                continue
+            if ";;#ASMEND" in line:
+                inside = False
+                continue
+            code = line.split(";")[0]
+            assert inside or not agpr.search(code), f"{name}: compiler-placed AGPR use: {line.strip()}"
+        m = re.search(r"\.set " + re.escape(name) + r"\.num_agpr, (\d+)", text)
+        if m:
+            assert int(m.group(1)) == 32
