@@ -185,19 +185,24 @@ def main():
             "salience": lambda: vr.salience(shape, Ks[j], Qw, sbars[j], workspace=ws_c),
             "allocate": lambda: vr.allocate(shape, sbars[j], c, workspace=ws_c),
             "project": lambda: vr.project(shape, Ks[j], Vs[j], PK, PV, c, workspace=ws_c),
+            "compress": lambda: vr.compress(shape, Ks[j], Vs[j], Qw, PK, PV, cache=c, sbar_out=sbars[j],
+                                            workspace=ws_c),
             "decode": lambda: vr.decode(shape, [d], q, PK, PV, out=out, workspace=ws_d),
         }
 
     def step(i):
-        for f in stage_fns(i).values():
-            f()
+        # one pass of the hot path as a caller runs it: compress (the single entry point),
+        # then decode
+        fns = stage_fns(i)
+        fns["compress"]()
+        fns["decode"]()
 
     for i in range(max(args.warmup, 1)):
         step(i)
     torch.cuda.synchronize()
     cap_stream = torch.cuda.Stream()
     graphs = {}
-    for name in ("salience", "allocate", "project", "decode"):
+    for name in ("salience", "allocate", "project", "compress", "decode"):
         g_ = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g_, stream=cap_stream):
             for i in range(N_CACHE_SLOTS):
@@ -242,7 +247,7 @@ def main():
     ms_step_events = e0.elapsed_time(e1) / steps
 
     ms_dec = stage["decode"]
-    ms_comp = stage["salience"] + stage["allocate"] + stage["project"]
+    ms_comp = stage["compress"]
     dbytes = decode_bytes(shape, slots[0])
     cbytes = compress_bytes(shape, slots[0])
     dec_gbs = dbytes / (ms_dec * 1e-3) / 1e9

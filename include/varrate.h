@@ -168,8 +168,10 @@ VARRATE_API int varrate_project(const varrate_shape* shape, const void* K, const
                     const float* P_K, const float* P_V, varrate_cache* cache,
                     void* workspace, size_t workspace_bytes, void* stream);
 
-/* Algorithm 1 for one layer: varrate_salience -> varrate_allocate -> varrate_project.
- * sbar_out ([N] fp32, device) receives the pooled salience when non-NULL.                   */
+/* Algorithm 1 for one layer: the results of varrate_salience -> varrate_allocate ->
+ * varrate_project, bit for bit (the pooling of the salience runs inside the allocation's
+ * first pass, one launch fewer).  sbar_out ([N] fp32, device) receives the pooled salience
+ * when non-NULL.  EINVAL for NULL inputs or inputs not 16-byte aligned.                      */
 VARRATE_API int varrate_compress(const varrate_shape* shape, const void* K, const void* V, const void* Qw,
                      const float* P_K, const float* P_V, varrate_cache* cache, float* sbar_out,
                      void* workspace, size_t workspace_bytes, void* stream);

@@ -216,6 +216,37 @@ __global__ __launch_bounds__(AK_T) void al_minmax(const float* __restrict__ sbar
     if (threadIdx.x == 0) mm[blockIdx.x] = make_float2(mn, mx);
 }
 
+// ---- 1'. (compress path) the same pass forming sbar from the salience column sums: the
+//          pooled value of each of its tokens (the pooling kernel's arithmetic), written out
+//          for the later passes, then min / max as above
+__global__ __launch_bounds__(AK_T) void al_pool_minmax(const float* __restrict__ s_part, int64_t N, int G,
+                                                       float inv_wh, float* __restrict__ sbar,
+                                                       float2* __restrict__ mm, uint32_t* __restrict__ clear,
+                                                       int clear_words) {
+    __shared__ float red[AK_T / 64];
+    __shared__ double sv[AK_TOK + 4];
+    const int per = (clear_words + gridDim.x - 1) / gridDim.x;
+    const int c0 = blockIdx.x * per, c1 = c0 + per < clear_words ? c0 + per : clear_words;
+    for (int i = c0 + threadIdx.x; i < c1; i += AK_T) clear[i] = 0;
+    const int64_t t0 = (int64_t)blockIdx.x * AK_TOK;
+    for (int i = threadIdx.x; i < AK_TOK + 4; i += AK_T) sv[i] = pool_term(s_part, N, G, inv_wh, t0 - 2 + i);
+    __syncthreads();
+    float v[AK_PER];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        // tokens past N take token N - 1's value (inside this workgroup: t0 < N)
+        v[k] = pool5(sv, (int)((t < N ? t : N - 1) - t0) + 2);
+        if (t < N) sbar[t] = v[k];
+    }
+    float mn = v[0], mx = v[0];
+#pragma unroll
+    for (int k = 1; k < AK_PER; ++k) { mn = fminf(mn, v[k]); mx = fmaxf(mx, v[k]); }
+    mn = block_reduce<AK_T>(mn, red, [](float a, float b) { return fminf(a, b); });
+    mx = block_reduce<AK_T>(mx, red, [](float a, float b) { return fmaxf(a, b); });
+    if (threadIdx.x == 0) mm[blockIdx.x] = make_float2(mn, mx);
+}
+
 // Global min / max from the per-workgroup partials (exact, so any order gives the same).
 __device__ __forceinline__ float2 al_range(const float2* __restrict__ mm, int nwg, float* red) {
     float mn = INFINITY, mx = -INFINITY;
@@ -841,7 +872,7 @@ __global__ __launch_bounds__(SCAN_T) void al_scan(uint32_t* __restrict__ chunk_o
 }
 
 hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_cache& c,
-                           uint8_t* ws, hipStream_t st) {
+                           uint8_t* ws, hipStream_t st, const float* s_part) {
     const int64_t N = sh.n - sh.w;
     const int R = D, r_min = sh.r_min;
     const int64_t B = c.B;
@@ -849,7 +880,11 @@ hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_c
     const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
     if (n_chunks > MAX_CODED_CHUNKS) return hipErrorInvalidValue;
     const AlWs w = al_ws(ws, N);
-    al_minmax<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, w.clear, w.clear_words);
+    if (s_part)
+        al_pool_minmax<<<nwg, AK_T, 0, st>>>(s_part, N, sh.G, salience_pool_scale(sh), const_cast<float*>(sbar),
+                                             w.mm, w.clear, w.clear_words);
+    else
+        al_minmax<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, w.clear, w.clear_words);
     al_weights<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_low, w.c_cnt, w.ctl);
     al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
     al_floors<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);

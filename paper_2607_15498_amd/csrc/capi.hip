@@ -189,13 +189,26 @@ int varrate_compress(const varrate_shape* sh, const void* K, const void* V, cons
     if ((rc = check_cache(sh, c, true))) return rc;
     if (!K || !V || !Qw || !PK || !PV) return fail(VARRATE_EINVAL, "inputs must be non-NULL");
     if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
+    if (!aligned16(K) || !aligned16(V) || !aligned16(Qw) || !aligned16(PK) || !aligned16(PV))
+        return fail(VARRATE_EINVAL, "K, V, Qw, P_K, P_V must be 16-byte aligned");
     float* sbar = sbar_out;
     if (!sbar) {
         sbar = (float*)((uint8_t*)ws + align256(salience_ws_bytes(*sh)) + align256(allocate_ws_bytes(*sh)));
     }
-    if ((rc = varrate_salience(sh, K, Qw, sbar, ws, ws_bytes, stream))) return rc;
-    if ((rc = varrate_allocate(sh, sbar, c, ws, ws_bytes, stream))) return rc;
-    return varrate_project(sh, K, V, PK, PV, c, ws, ws_bytes, stream);
+    // salience passes, then the allocation's first pass pools sbar from the column sums
+    // itself (the separate pooling launch is skipped), then the rest of the allocation and
+    // the projection: the same results as the three entry points in turn
+    hipStream_t st = (hipStream_t)stream;
+    uint8_t* w0 = (uint8_t*)ws;
+    if ((rc = hip_status(launch_salience(*sh, K, Qw, sbar, w0, st, false), "salience launch"))) return rc;
+    c->N = sh->n - sh->w;
+    c->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    uint8_t* w8 = w0 + align256(salience_ws_bytes(*sh));
+    if ((rc = hip_status(launch_allocate(*sh, sbar, *c, w8, st, salience_part(*sh, w0)), "allocate launch")))
+        return rc;
+    if ((rc = hip_status(launch_project(*sh, K, V, PK, PV, *c, st), "project launch"))) return rc;
+    c->n_exact = sh->w;
+    return VARRATE_OK;
 }
 
 int varrate_append_exact(const varrate_shape* sh, varrate_cache* c, const void* k_new, const void* v_new,

@@ -398,34 +398,15 @@ __global__ __launch_bounds__(SL_THREADS, 4) void sal_colsum(const void* __restri
 // pool: sbar[t] = (s_{t-2} + ... + s_{t+2}) / 5 with s_k = sum_g s_part[g][k] / (w H).  A
 // block of 256 tokens first forms s for its tokens and a 2-token halo on each side.
 constexpr int SP_T = 256;
-constexpr int SP_MAXG = 16;      // heads whose loads issue together
 __global__ __launch_bounds__(SP_T) void sal_pool(const float* __restrict__ s_part, int64_t N, int G,
                                                  float inv_wh, float* __restrict__ sbar) {
     __shared__ double sv[SP_T + 4];
     const int64_t t0 = (int64_t)blockIdx.x * SP_T;
-    for (int i = threadIdx.x; i < SP_T + 4; i += SP_T) {
-        const int64_t k = t0 - 2 + i;
-        double v = 0.0;
-        if (k >= 0 && k < N) {
-            // the heads' loads all issue before the (fixed-order) sum
-            float part[SP_MAXG];
-#pragma unroll
-            for (int gg = 0; gg < SP_MAXG; ++gg) part[gg] = gg < G ? s_part[(int64_t)gg * N + k] : 0.f;
-            float s = 0.f;
-#pragma unroll
-            for (int gg = 0; gg < SP_MAXG; ++gg)
-                if (gg < G) s += part[gg];
-            for (int gg = SP_MAXG; gg < G; ++gg) s += s_part[(int64_t)gg * N + k];
-            v = (double)(s * inv_wh);
-        }
-        sv[i] = v;
-    }
+    for (int i = threadIdx.x; i < SP_T + 4; i += SP_T) sv[i] = pool_term(s_part, N, G, inv_wh, t0 - 2 + i);
     __syncthreads();
     const int64_t t = t0 + threadIdx.x;
     if (t >= N) return;
-    const int i = threadIdx.x + 2;
-    const double acc = (((sv[i - 2] + sv[i - 1]) + sv[i]) + sv[i + 1]) + sv[i + 2];
-    sbar[t] = (float)(acc / 5.0);
+    sbar[t] = pool5(sv, threadIdx.x + 2);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -465,8 +446,16 @@ static hipError_t sal_attr() {
     return e;
 }
 
+const float* salience_part(const varrate_shape& sh, const uint8_t* ws) {
+    const int rows = (sh.H / sh.G) * sh.w;
+    const SalPlan p1 = sal_plan((sh.n + sal_kb(sh) - 1) / sal_kb(sh), sh.G);
+    return (const float*)(ws + align256((size_t)sh.G * rows * p1.nw * sizeof(float2)));
+}
+
+float salience_pool_scale(const varrate_shape& sh) { return 1.0f / ((float)sh.w * (float)sh.H); }
+
 hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Qw, float* sbar,
-                           uint8_t* ws, hipStream_t st) {
+                           uint8_t* ws, hipStream_t st, bool pool) {
     const int rows = (sh.H / sh.G) * sh.w;
     const int64_t N = sh.n - sh.w;
     const int KB = sal_kb(sh);
@@ -487,8 +476,8 @@ hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Q
         sal_rowstats<true><<<g1, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, p1.bpw);
         sal_colsum<true><<<g2, SL_THREADS, lds, st>>>(K, Qw, sh.n, sh.G, sh.H, sh.w, stats, p1.nw, s_part, p2.bpw);
     }
-    sal_pool<<<(unsigned)((N + SP_T - 1) / SP_T), SP_T, 0, st>>>(s_part, N, sh.G,
-                                                                   1.0f / ((float)sh.w * (float)sh.H), sbar);
+    if (pool)
+        sal_pool<<<(unsigned)((N + SP_T - 1) / SP_T), SP_T, 0, st>>>(s_part, N, sh.G, salience_pool_scale(sh), sbar);
     return hipGetLastError();
 }
 

@@ -118,4 +118,29 @@ __device__ __forceinline__ float xsum32(float v) {
 // exp(x) on the hardware exp2 path (x * log2 e); -inf -> 0.
 __device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
 
+// Salience pooling terms (Sec. 3.2, after Eq. (4)): s_k = (sum over the G heads of the
+// per-head column sums, fp32 in head order) / (w H), carried in fp64; the pooled value of a
+// token is the centred 5-term sum of s in fixed order, divided by 5 and rounded to fp32.
+// Used by the pooling kernel and by the compress path's fused pooling + range pass, so both
+// produce the same bits.
+constexpr int POOL_MAXG = 16;      // heads whose loads issue together
+__device__ __forceinline__ double pool_term(const float* __restrict__ s_part, int64_t N, int G,
+                                            float inv_wh, int64_t k) {
+    if (k < 0 || k >= N) return 0.0;
+    float part[POOL_MAXG];
+#pragma unroll
+    for (int gg = 0; gg < POOL_MAXG; ++gg) part[gg] = gg < G ? s_part[(int64_t)gg * N + k] : 0.f;
+    float s = 0.f;
+#pragma unroll
+    for (int gg = 0; gg < POOL_MAXG; ++gg)
+        if (gg < G) s += part[gg];
+    for (int gg = POOL_MAXG; gg < G; ++gg) s += s_part[(int64_t)gg * N + k];
+    return (double)(s * inv_wh);
+}
+// sv[i - 2 .. i + 2] are the terms around the token
+__device__ __forceinline__ float pool5(const double* sv, int i) {
+    const double acc = (((sv[i - 2] + sv[i - 1]) + sv[i]) + sv[i + 1]) + sv[i + 2];
+    return (float)(acc / 5.0);
+}
+
 }  // namespace vr

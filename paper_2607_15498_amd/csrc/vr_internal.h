@@ -21,10 +21,15 @@ size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q);
 size_t decode_units(const varrate_shape& sh, int S, int Q);   // sequences x KV heads x row tiles
 bool decode_supported(const varrate_shape& sh, int S, int Q);
 
+// pool = false leaves the per-head column sums in the workspace (salience_part) for
+// launch_allocate to pool (compress path: one launch fewer)
 hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Qw, float* sbar,
-                           uint8_t* ws, hipStream_t st);
+                           uint8_t* ws, hipStream_t st, bool pool = true);
+const float* salience_part(const varrate_shape& sh, const uint8_t* ws);
+float salience_pool_scale(const varrate_shape& sh);
+// s_part non-NULL: the first pass pools sbar from the column sums (and writes it) itself
 hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_cache& c,
-                           uint8_t* ws, hipStream_t st);
+                           uint8_t* ws, hipStream_t st, const float* s_part = nullptr);
 hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V, const float* PK,
                           const float* PV, varrate_cache& c, hipStream_t st);
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,

@@ -422,6 +422,30 @@ def test_decode_more_sequences_than_one_launch(vr, oracle_lib):
     assert worst <= DEC_TOL_BF16
 
 
+@pytest.mark.parametrize("name", ["tiny", "qwen_16k_stack", "llama_32k"])
+def test_compress_equals_the_three_entry_points(vr, name):
+    """varrate_compress pools the salience inside the allocation's first pass; its outputs
+    must equal those of varrate_salience -> varrate_allocate -> varrate_project bit for bit."""
+    import torch
+    from workloads import CONFIGS
+    say(f"[compress = steps] {name}")
+    li = layer(name)
+    shape = shape_of(vr, CONFIGS[name])
+    dt = shape.torch_dtype
+    K, V, Qw = dev(li.K, dt), dev(li.V, dt), dev(li.Qw, dt)
+    PK, PV = dev(li.PK, torch.float32), dev(li.PV, torch.float32)
+    sb1 = vr.salience(shape, K, Qw)
+    c1 = vr.new_cache(shape)
+    vr.allocate(shape, sb1, c1)
+    vr.project(shape, K, V, PK, PV, c1)
+    sb2 = torch.empty(shape.N, dtype=torch.float32, device="cuda")
+    c2 = vr.compress(shape, K, V, Qw, PK, PV, sbar_out=sb2)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(sb1), host(sb2))
+    for f in ("rank", "srank", "sidx", "chunk_off", "coef_k", "coef_v", "k_exact", "v_exact"):
+        assert np.array_equal(host(getattr(c1, f)), host(getattr(c2, f))), f
+
+
 @pytest.mark.parametrize("n,w,kappa,r_min", [(33, 32, 100, 16), (40, 32, 90, 0), (287, 32, 50, 16),
                                              (289, 32, 25, 4), (600, 1, 30, 16), (2080, 32, 100, 16)])
 def test_ragged_and_degenerate(vr, oracle_lib, n, w, kappa, r_min):
