@@ -751,6 +751,69 @@ __global__ __launch_bounds__(AS_T) void al_select(int64_t N, const uint64_t* __r
     if (tid == 0) { ctl->T_hi = sel.T_hi; ctl->T_lo = sel.T_lo; }
 }
 
+// Stored order of one chunk per wave: rank descending, token index ascending (a stable
+// counting sort).  Lane `lane` holds the ranks r[k] of tokens t0 + 64 k + lane (tokens past N
+// take no part); token lane + 64 k is bit `lane` of word k of its rank's mask, so a token's
+// place is (#tokens of higher rank) + (#earlier tokens of its rank).  Writes srank / sidx at
+// the chunk's positions and returns the chunk's size in tile rectangles (16 x the first,
+// largest rank of each 16-position tile), summed over the wave.  m and above are the wave's
+// own LDS scratch; the function holds workgroup barriers, so every wave calls it together.
+__device__ uint32_t chunk_order(unsigned long long (*m)[4], uint16_t* above, const uint32_t (&r)[AK_PER],
+                                int64_t t0, int64_t N, uint8_t* __restrict__ srank,
+                                uint32_t* __restrict__ sidx) {
+    const int lane = threadIdx.x & 63;
+    for (int i = lane; i < NRV * 4; i += 64) (&m[0][0])[i] = 0ull;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k)
+        if (t0 + 64 * k + lane < N) atomicOr(&m[r[k]][k], 1ull << lane);
+    __syncthreads();
+    {
+        // lane covers rank values 128 - 3 lane - e (descending), then a wave exclusive scan
+        uint32_t h[3], loc = 0;
+#pragma unroll
+        for (int e = 0; e < 3; ++e) {
+            const int q = 3 * lane + e;
+            h[e] = 0;
+            if (q < NRV) {
+                const unsigned long long* mm = m[NRV - 1 - q];
+                h[e] = __popcll(mm[0]) + __popcll(mm[1]) + __popcll(mm[2]) + __popcll(mm[3]);
+            }
+            loc += h[e];
+        }
+        uint32_t x = loc;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        uint32_t pre = x - loc;
+#pragma unroll
+        for (int e = 0; e < 3; ++e) {
+            const int q = 3 * lane + e;
+            if (q < NRV) above[NRV - 1 - q] = (uint16_t)pre;
+            pre += h[e];
+        }
+    }
+    __syncthreads();
+    uint32_t tile_sum = 0;
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = t0 + 64 * k + lane;
+        if (t >= N) continue;
+        const unsigned long long* mm = m[r[k]];
+        uint32_t pos = above[r[k]] + __popcll(mm[k] & ((1ull << lane) - 1ull));
+#pragma unroll
+        for (int j = 0; j < AK_PER - 1; ++j)
+            if (j < k) pos += __popcll(mm[j]);
+        srank[t0 + pos] = (uint8_t)r[k];
+        sidx[t0 + pos] = (uint32_t)t;
+        // the chunk's storage: each tile of 16 positions takes 16 x its first (largest) rank
+        if ((pos & 15) == 0) tile_sum += 16u * r[k];
+    }
+    return wave_sum(tile_sum);
+}
+
 // ---- 6. final ranks, chunk sums, storage order ----------------------------------------------------
 
 __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __restrict__ u_ws,
@@ -787,62 +850,7 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
     }
     const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + wv;
-
-    // Stored order of the chunk: rank descending, token index ascending (a stable counting
-    // sort).  Token lane + 64 k of the chunk is bit `lane` of word k of its rank's mask, so a
-    // token's place is (#tokens of higher rank) + (#earlier tokens of its rank).
-    unsigned long long (*m)[4] = msk[wv];
-    for (int i = lane; i < NRV * 4; i += 64) (&m[0][0])[i] = 0ull;
-    __syncthreads();
-#pragma unroll
-    for (int k = 0; k < AK_PER; ++k)
-        if (al_tok(k) < N) atomicOr(&m[r[k]][k], 1ull << lane);
-    __syncthreads();
-    {
-        // lane covers rank values 128 - 3 lane - e (descending), then a wave exclusive scan
-        uint32_t h[3], loc = 0;
-#pragma unroll
-        for (int e = 0; e < 3; ++e) {
-            const int q = 3 * lane + e;
-            h[e] = 0;
-            if (q < NRV) {
-                const unsigned long long* mm = m[NRV - 1 - q];
-                h[e] = __popcll(mm[0]) + __popcll(mm[1]) + __popcll(mm[2]) + __popcll(mm[3]);
-            }
-            loc += h[e];
-        }
-        uint32_t x = loc;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const uint32_t y = __shfl_up(x, off, 64);
-            if (lane >= off) x += y;
-        }
-        uint32_t pre = x - loc;
-#pragma unroll
-        for (int e = 0; e < 3; ++e) {
-            const int q = 3 * lane + e;
-            if (q < NRV) above_r[wv][NRV - 1 - q] = (uint16_t)pre;
-            pre += h[e];
-        }
-    }
-    __syncthreads();
-    const int64_t t0 = c * CHUNK;
-    uint32_t tile_sum = 0;
-#pragma unroll
-    for (int k = 0; k < AK_PER; ++k) {
-        const int64_t t = al_tok(k);
-        if (t >= N) continue;
-        const unsigned long long* mm = m[r[k]];
-        uint32_t pos = above_r[wv][r[k]] + __popcll(mm[k] & ((1ull << lane) - 1ull));
-#pragma unroll
-        for (int j = 0; j < AK_PER - 1; ++j)
-            if (j < k) pos += __popcll(mm[j]);
-        srank[t0 + pos] = (uint8_t)r[k];
-        sidx[t0 + pos] = (uint32_t)t;
-        // the chunk's storage: each tile of 16 positions takes 16 x its first (largest) rank
-        if ((pos & 15) == 0) tile_sum += 16u * r[k];
-    }
-    tile_sum = wave_sum(tile_sum);
+    const uint32_t tile_sum = chunk_order(msk[wv], above_r[wv], r, c * CHUNK, N, srank, sidx);
     if (lane == 0 && c * CHUNK < N) chunk_off[c] = tile_sum;
 }
 

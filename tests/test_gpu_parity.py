@@ -199,9 +199,40 @@ def test_allocation_bit_exact(vr, oracle_lib, name, kappa, r_min):
         got = host(cache.rank).astype(np.int64)
         mism = int((got != want).sum())
         assert mism == 0, f"{case}: {mism} rank mismatches"
-        _, _, chunk_off = expected_layout(want.astype(np.int64), N)
+        srank, sidx, chunk_off = expected_layout(want.astype(np.int64), N)
         assert np.array_equal(host(cache.chunk_off).astype(np.int64), chunk_off), case
+        assert np.array_equal(host(cache.srank).astype(np.int64), srank), case
+        assert np.array_equal(host(cache.sidx).astype(np.int64), sidx), case
         assert cache.B == B and got.sum() == B
+
+
+@pytest.mark.parametrize("n,kappa,r_min", [(40000, 20, 16), (40000, 10, 8), (32800, 40, 16)])
+def test_allocation_bit_exact_grid_passes(vr, oracle_lib, n, kappa, r_min):
+    """Coded lengths other than the workloads' (39968 tokens: 40 workgroups of 1024 with a
+    ragged last one; 32768: exactly 32): the synthetic sbar cases, ranks, storage order and
+    chunk table bit-exact against the oracle."""
+    import torch
+    from workloads import CONFIGS
+    cfg = CONFIGS["llama_32k"]
+    N = n - cfg["w"]
+    shape = shape_of(vr, cfg, n=n, kappa=kappa, r_min=r_min)
+    B = oracle_lib.budget(n, 128, cfg["w"], kappa)
+    for case, sb in sbar_cases(N, None).items():
+        if sb is None:
+            continue
+        say(f"[allocate] n={n} kappa={kappa} r_min={r_min} case={case}")
+        want = oracle_lib.allocate(oracle_lib.weights(sb), B, r_min, 128).rank
+        cache = vr.new_cache(shape)
+        vr.allocate(shape, dev(sb, torch.float32), cache)
+        torch.cuda.synchronize()
+        got = host(cache.rank).astype(np.int64)
+        mism = int((got != want).sum())
+        assert mism == 0, f"{case}: {mism} rank mismatches"
+        srank, sidx, chunk_off = expected_layout(want.astype(np.int64), N)
+        assert np.array_equal(host(cache.chunk_off).astype(np.int64), chunk_off), case
+        assert np.array_equal(host(cache.srank).astype(np.int64), srank), case
+        assert np.array_equal(host(cache.sidx).astype(np.int64), sidx), case
+        assert got.sum() == B
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama_32k"])
