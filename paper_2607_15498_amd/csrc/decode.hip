@@ -364,8 +364,9 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     const int rows = min(16, p.rows_total - 16 * qt);
     const int nr4 = (rows + 3) & ~3;
     const bool exact = x == 0;
-    // the later-dispatched half of the grid shares CUs with the earlier half; give its waves
-    // the higher issue priority so both workgroups on a CU progress alike
+    // the later-dispatched half of the grid shares CUs with the earlier half: its waves take
+    // the higher issue priority through the prologue, so its metadata and first rounds are not
+    // queued behind the earlier half's
     if (L >= (int)(gridDim.x >> 1)) __builtin_amdgcn_s_setprio(1);
     const int xc = x - 1;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));   // scalar
@@ -575,6 +576,9 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     }
 
 
+    // the raised priority of the later half only speeds its prologue up (its first loads go
+    // out with the earlier half's); in the round loop both halves issue at the same priority
+    __builtin_amdgcn_s_setprio(0);
     for (int rd = 0;; ++rd) {
         // this wave's loads of round rd have landed (only the next round's are younger),
         // then every wave's
