@@ -19,8 +19,10 @@
  *     caller unless stated otherwise; descriptors (varrate_shape, varrate_cache) are host
  *     structs.  Tensors are contiguous row-major, base addresses 16-byte aligned.
  *   - `stream` is a hipStream_t passed as void*; all device work is enqueued on it
- *     asynchronously.  No entry point synchronises the host, allocates device memory or
- *     keeps state between calls.
+ *     asynchronously.  No entry point synchronises the host or allocates device memory.
+ *     The only state kept between calls is, per (kernel, device), the dynamic-LDS limit
+ *     already raised with hipFuncSetAttribute (guarded by a lock, so calls from several
+ *     host threads and on several devices are safe).
  *   - Arguments are validated synchronously before anything is enqueued; on error nothing
  *     is enqueued and a negative status is returned.  varrate_last_error() then returns a
  *     thread-local message.

@@ -1,15 +1,37 @@
 // C ABI of libvarrate: validation, sizing, workspace carving and kernel dispatch.
-// Every check runs on the host before anything is enqueued; no entry point synchronises,
-// allocates device memory or keeps state between calls.
+// Every check runs on the host before anything is enqueued; no entry point synchronises or
+// allocates device memory.  The one piece of state kept across calls is the per (kernel,
+// device) record of raised dynamic-LDS limits (ensure_lds_limit, under a lock).
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
 
+#include <map>
+#include <mutex>
 #include <string>
+#include <utility>
 
 #include "vr_internal.h"
 
 using namespace vr;
+
+namespace vr {
+
+hipError_t ensure_lds_limit(const void* fn, size_t bytes) {
+    static std::mutex mu;
+    static std::map<std::pair<const void*, int>, size_t> raised;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(mu);
+    size_t& have = raised[{fn, dev}];
+    if (bytes <= have) return hipSuccess;
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e == hipSuccess) have = bytes;
+    return e;
+}
+
+}  // namespace vr
 
 namespace {
 
@@ -232,9 +254,8 @@ int varrate_append_exact(const varrate_shape* sh, varrate_cache* c, const void* 
     return VARRATE_OK;
 }
 
-int varrate_decode_attn(const varrate_shape* sh, const varrate_cache* caches, int32_t S, const void* q,
-                        int32_t Q, const float* PK, const float* PV, void* out, void* ws, size_t ws_bytes,
-                        void* stream) {
+static int check_decode(const varrate_shape* sh, const varrate_cache* caches, int32_t S, const void* q,
+                        int32_t Q, const float* PK, const float* PV, void* out) {
     int rc = check_shape(sh);
     if (rc) return rc;
     if (!caches || S < 1 || S > VARRATE_MAX_SEQS) return fail(VARRATE_EINVAL, "S=%d outside [1, %d]", S, VARRATE_MAX_SEQS);
@@ -253,6 +274,14 @@ int varrate_decode_attn(const varrate_shape* sh, const varrate_cache* caches, in
     }
     if (!decode_supported(*sh, S, Q))
         return fail(VARRATE_EUNSUPPORTED, "S * G * ceil(Q H/G / 16) exceeds 16384 merge slots");
+    return VARRATE_OK;
+}
+
+int varrate_decode_attn(const varrate_shape* sh, const varrate_cache* caches, int32_t S, const void* q,
+                        int32_t Q, const float* PK, const float* PV, void* out, void* ws, size_t ws_bytes,
+                        void* stream) {
+    int rc = check_decode(sh, caches, S, q, Q, PK, PV, out);
+    if (rc) return rc;
     if ((rc = ws_check(ws, ws_bytes, decode_ws_bytes(*sh, S, Q)))) return rc;
     return hip_status(launch_decode(*sh, caches, S, q, Q, PK, PV, out, (uint8_t*)ws, (hipStream_t)stream),
                       "decode launch");

@@ -912,16 +912,6 @@ size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
     return align256(units * (pl.n_wg + 1) * DC_REC * sizeof(float));
 }
 
-template <bool F32>
-static hipError_t set_smem_attr(size_t bytes) {
-    static size_t done = 0;
-    if (bytes <= done) return hipSuccess;
-    hipError_t e = hipFuncSetAttribute((const void*)decode_kernel<F32>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e == hipSuccess) done = bytes;
-    return e;
-}
-
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
                          int Q, const float* PK, const float* PV, void* out, uint8_t* ws,
                          hipStream_t st) {
@@ -935,7 +925,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
     const size_t lds = decode_smem_bytes(pl.cpw);
-    hipError_t e = sh.dtype == VARRATE_BF16 ? set_smem_attr<false>(lds) : set_smem_attr<true>(lds);
+    hipError_t e = sh.dtype == VARRATE_BF16 ? ensure_lds_limit((const void*)decode_kernel<false>, lds)
+                                             : ensure_lds_limit((const void*)decode_kernel<true>, lds);
     if (e != hipSuccess) return e;
     for (int s0 = 0; s0 < S; s0 += DC_SEQ) {
         const int ns = S - s0 < DC_SEQ ? S - s0 : DC_SEQ;
@@ -988,5 +979,6 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     }
     return hipSuccess;
 }
+
 
 }  // namespace vr

@@ -354,16 +354,6 @@ __global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
                                 coef_stride, k_exact, v_exact, cap, smem);
 }
 
-template <bool F32>
-static hipError_t pj_attr(size_t bytes) {
-    static size_t done = 0;
-    if (bytes <= done) return hipSuccess;
-    hipError_t e = hipFuncSetAttribute((const void*)project_kernel<F32>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e == hipSuccess) done = bytes;
-    return e;
-}
-
 hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V, const float* PK,
                           const float* PV, varrate_cache& c, hipStream_t st) {
     const int64_t N = sh.n - sh.w;
@@ -371,13 +361,13 @@ hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V,
     dim3 grid((n_chunks + PJ_CPW - 1) / PJ_CPW, sh.G, 2);
     const size_t lds = project_smem_bytes();
     if (sh.dtype == VARRATE_BF16) {
-        hipError_t e = pj_attr<false>(lds);
+        hipError_t e = ensure_lds_limit((const void*)project_kernel<false>, lds);
         if (e != hipSuccess) return e;
         project_kernel<false><<<grid, PJ_THREADS, lds, st>>>(
             K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
             c.coef_stride, c.k_exact, c.v_exact, c.cap);
     } else {
-        hipError_t e = pj_attr<true>(lds);
+        hipError_t e = ensure_lds_limit((const void*)project_kernel<true>, lds);
         if (e != hipSuccess) return e;
         project_kernel<true><<<grid, PJ_THREADS, lds, st>>>(
             K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, c.chunk_off, n_chunks, c.coef_k, c.coef_v,

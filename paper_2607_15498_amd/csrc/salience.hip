@@ -437,12 +437,8 @@ size_t salience_ws_bytes(const varrate_shape& sh) {
 
 template <bool F32>
 static hipError_t sal_attr() {
-    static bool done = false;
-    if (done) return hipSuccess;
-    hipError_t e = hipFuncSetAttribute((const void*)sal_rowstats<F32>, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * SL_STAGE);
-    if (e == hipSuccess)
-        e = hipFuncSetAttribute((const void*)sal_colsum<F32>, hipFuncAttributeMaxDynamicSharedMemorySize, 2 * SL_STAGE);
-    if (e == hipSuccess) done = true;
+    hipError_t e = ensure_lds_limit((const void*)sal_rowstats<F32>, 2 * SL_STAGE);
+    if (e == hipSuccess) e = ensure_lds_limit((const void*)sal_colsum<F32>, 2 * SL_STAGE);
     return e;
 }
 

@@ -15,6 +15,11 @@ constexpr int MAX_CODED_CHUNKS = (int)(MAX_CODED / CHUNK);
 
 inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
+// Raises kernel `fn`'s dynamic-LDS limit to at least `bytes` on the current device.  The
+// raised limit is remembered per (kernel, device) under a lock, so concurrent callers and
+// several devices are safe; this is the only state the library keeps across calls.
+hipError_t ensure_lds_limit(const void* fn, size_t bytes);
+
 size_t salience_ws_bytes(const varrate_shape& sh);
 size_t allocate_ws_bytes(const varrate_shape& sh);
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q);

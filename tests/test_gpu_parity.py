@@ -5,6 +5,7 @@ same fp32 pooled salience; salience within 1e-3 relative (entries below 1e-6 of 
 an underflow floor, reported separately); decode within 2e-2 of max |o| per (sequence,
 query, head) in bf16.  The fp32 tiny workload is also held to a tighter decode bound."""
 import math
+import os
 import sys
 
 import numpy as np
@@ -18,7 +19,13 @@ DEC_TOL_F32 = 1e-4
 
 
 def say(*a):
+    """Progress and observed errors: stderr, and appended to the file named by
+    VARRATE_PARITY_LOG when that variable is set (so a run keeps its measured errors)."""
     print(*a, file=sys.stderr, flush=True)
+    path = os.environ.get("VARRATE_PARITY_LOG")
+    if path:
+        with open(path, "a") as fh:
+            print(*a, file=fh)
 
 
 @pytest.fixture(scope="module")
@@ -146,23 +153,53 @@ def gpu_compress(vr, shape, li, sbar=None, cap=None):
 
 
 # ---------------------------------------------------------------------------------------
-@pytest.mark.parametrize("name", ["tiny", "llama_32k"])
-def test_salience_parity(vr, oracle_lib, name):
-    from workloads import CONFIGS
-    say(f"[salience] {name}")
-    li = layer(name)
-    oc = oracle_compress(oracle_lib, name, li, CONFIGS[name]["kappa"], CONFIGS[name]["r_min"])
-    shape = shape_of(vr, CONFIGS[name])
-    _, sb, _, _ = gpu_compress(vr, shape, li)
-    g = host(sb).astype(np.float64)
-    o = oc.sbar.astype(np.float64)
+def check_salience(got, want, label):
+    """Elementwise relative error <= SAL_RTOL on entries at or above 1e-6 of the largest
+    (the underflow floor); below it the absolute error stays under SAL_RTOL x the floor."""
+    g = np.asarray(got, np.float64)
+    o = np.asarray(want, np.float64)
     floor = 1e-6 * o.max()
     big = o >= floor
     rel = np.abs(g[big] - o[big]) / o[big]
-    say(f"  max rel {rel.max():.3e} over {big.sum()} entries; {(~big).sum()} below floor, "
-        f"max abs there {np.abs(g[~big] - o[~big]).max() if (~big).any() else 0:.3e}")
-    assert rel.max() <= SAL_RTOL
-    assert np.all(np.abs(g[~big] - o[~big]) <= SAL_RTOL * floor)
+    small = np.abs(g[~big] - o[~big]).max() if (~big).any() else 0.0
+    say(f"  {label}: salience max rel {rel.max():.3e} over {big.sum()} entries; "
+        f"{(~big).sum()} below floor, max abs there {small:.3e}")
+    assert rel.max() <= SAL_RTOL, label
+    assert small <= SAL_RTOL * floor, label
+
+
+# Window rows per KV head ((H/G) w): tiny 64, llama 128, qwen 224 (the second row tile of
+# waves 0-5), and a small synthetic layer at the 256-row maximum.
+SALIENCE_CASES = {
+    "tiny": None,
+    "llama_32k": None,
+    "qwen_16k_stack": None,
+    "rows256": dict(base="llama_32k", n=3000, G=1, H=8, w=32, seed=31),
+}
+
+
+@pytest.mark.parametrize("name", list(SALIENCE_CASES))
+def test_salience_parity(vr, oracle_lib, name):
+    from workloads import CONFIGS, make_layer
+    over = SALIENCE_CASES[name]
+    if over is None:
+        cfg = CONFIGS[name]
+        li = layer(name)
+    else:
+        cfg = dict(CONFIGS[over["base"]])
+        cfg.update({k: v for k, v in over.items() if k != "base"})
+        li = make_layer(cfg)
+    say(f"[salience] {name}: n={cfg['n']} G={cfg['G']} H={cfg['H']} w={cfg['w']} "
+        f"({cfg['H'] // cfg['G'] * cfg['w']} window rows per KV head)")
+    sbar_or = oracle_lib.pool(oracle_lib.salience(li.K, li.Qw, cfg["H"]))
+    shape = shape_of(vr, cfg)
+    _, sb, _, _ = gpu_compress(vr, shape, li)
+    check_salience(host(sb), sbar_or, name)
+    # the salience entry point alone (pooling launch) gives the same bits as compress
+    import torch
+    sb2 = vr.salience(shape, dev(li.K, shape.torch_dtype), dev(li.Qw, shape.torch_dtype))
+    torch.cuda.synchronize()
+    assert np.array_equal(host(sb2), host(sb)), name
 
 
 def sbar_cases(N, oracle_sbar):
@@ -253,17 +290,25 @@ def test_layout_and_projection(vr, oracle_lib, name):
     for kind, ref, X in (("K", oc.coefK, li.K), ("V", oc.coefV, li.V)):
         got = unpack(host(cache.coef_k if kind == "K" else cache.coef_v), srank, sidx, chunk_off, N, kind)
         err = np.abs(got - ref)
-        # The kernel forms P x from bf16 hi + lo parts of P (and of x when x is fp32), each
-        # product within 2^-18 |P_ji x_i|, summed in fp32: |error| <= 2^-18 sum_i |P_ji x_i|
-        # <= 2^-18 sqrt(128) ||x_t|| < 2^-12 ||x_t||.  bf16 storage then rounds the kernel's
-        # value, which may land one unit (<= 2^-7 |ref|) from the rounding of the exact value.
-        xnorm = np.linalg.norm(X[:N].astype(np.float64), axis=-1)[:, :, None]
+        # The kernel forms P x from bf16 hi + lo parts of P (x too when it is fp32): each
+        # product is within 3 x 2^-18 |P_ji x_i| of exact (the dropped lo x lo term and the
+        # two split residuals), and the fp32 MFMA accumulation of 128 such terms (12 rounded
+        # accumulator updates at most, each <= 2^-24 of the running sum) adds under
+        # 2^-19 sum_i |P_ji x_i|.  So |c_kernel - c| <= 2^-15 S_j with S_j = sum_i |P_ji x_i|
+        # (<= ||x_t||, as basis rows have unit norm).  bf16 storage then rounds the kernel's
+        # value, which lands at most one unit (<= 2^-7 |ref|) from the rounding of the exact
+        # value.  A projection that dropped the basis lo part would err by up to 2^-9 S_j.
+        G = X.shape[1]
+        P = li.PK if kind == "K" else li.PV
+        Xa = np.abs(X[:N].astype(np.float64))
+        S = np.stack([Xa[:, g, :] @ np.abs(P[g].astype(np.float64)).T for g in range(G)], axis=1)
         if cfg["dtype"] == "bf16":
-            ok = err <= np.abs(ref) * 2.0 ** -7 + 2.0 ** -12 * xnorm
+            ok = err <= np.abs(ref) * 2.0 ** -7 + 2.0 ** -15 * S
         else:
-            ok = err <= np.abs(ref) * 2.0 ** -23 + 2.0 ** -12 * xnorm
-        say(f"  {kind}: max rel {rel_err(got, ref):.3e}, beyond-bound {int((~ok).sum())}, "
-            f"identical {float((err == 0).mean()):.4f}")
+            ok = err <= np.abs(ref) * 2.0 ** -23 + 2.0 ** -15 * S
+        frac = float((err / np.maximum(S, 1e-30)).max())
+        say(f"  {kind}: max rel {rel_err(got, ref):.3e}, max err / S_j {frac:.3e}, beyond-bound "
+            f"{int((~ok).sum())}, identical {float((err == 0).mean()):.4f}")
         assert ok.all()
     # exact window rows are copied verbatim
     w = shape.w
@@ -501,8 +546,10 @@ def test_ragged_and_degenerate(vr, oracle_lib, n, w, kappa, r_min):
     torch.cuda.synchronize()
     o_or = oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[0], 4)
     e = decode_err(out[0], o_or)
-    say(f"  decode err {e:.3e}; e2e rank mismatches {int((got_rank != oc.alloc.rank).sum())}; "
-        f"salience max rel {np.max(np.abs(s - oc.sbar) / np.maximum(oc.sbar, 1e-30)):.2e}")
+    mism = int((got_rank != oc.alloc.rank).sum())
+    say(f"  decode err {e:.3e}; e2e rank mismatches {mism} of {n - w}")
+    check_salience(s, oc.sbar, f"ragged n={n} w={w}")
+    assert mism <= max(8, (n - w) // 1000)
     assert e <= DEC_TOL_BF16
 
 

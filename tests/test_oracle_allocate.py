@@ -227,3 +227,83 @@ def test_budget_matches_storage_fraction(oracle_lib, n, w, kappa):
     B = oracle_lib.budget(n, d, w, kappa)
     total = B + w * d
     assert Fraction(total, n * d) <= Fraction(kappa, 100) < Fraction(total + 1, n * d)
+
+
+# ---------------------------------------------------------------------------------------
+# Reading of the all-zero division in Algorithm 1's loop: the oracle water-fills the integer
+# weights u_t = 1 + floor(2^24 s_hat_t) instead of s_hat itself.  As weights w = u / 2^24 =
+# s_hat + delta with 0 < delta_t <= 2^-24, and the water level lambda falls as weights grow,
+# every token's continuous rank moves by at most (N + 1) lambda_w 2^-24, where lambda_w 2^-24
+# = M / Q is the oracle's level per unit of u:
+#   q^s_t - clip(r_min + lambda_w s_hat_t) lies in [0, g(lambda_s) - g(lambda_w)] <= lambda_w N 2^-24,
+#   |q^w_t - clip(r_min + lambda_w s_hat_t)| <= lambda_w delta_t <= lambda_w 2^-24,
+# with g(lambda) = sum_t clip(r_min + lambda s_hat_t), which the budget fixes on both sides.
+def _shat_cases():
+    rng = np.random.default_rng(4242)
+    for i in range(14):
+        N = int(rng.integers(2, 36))
+        R = int(rng.integers(4, 40))
+        r_min = int(rng.integers(0, R // 2 + 1))
+        B = int(rng.integers(N * r_min, N * R + 1))
+        kind = i % 4
+        if kind == 0:
+            s = rng.random(N)
+        elif kind == 1:                     # spiky: one or two hot tokens, the rest near zero
+            s = rng.random(N) ** 16
+        elif kind == 2:                     # exact zeros besides the minimum (Q7's 0/0 risk)
+            s = np.where(rng.random(N) < 0.6, 0.0, rng.random(N))
+        else:                               # heavy ties
+            s = rng.integers(0, 3, N) / 2.0
+        yield N, R, r_min, B, s.astype(np.float32)
+
+
+@pytest.mark.parametrize("case", list(_shat_cases()), ids=lambda c: f"N{c[0]}R{c[1]}m{c[2]}B{c[3]}")
+def test_epsilon_weights_stay_within_bound_of_algorithm1_on_shat(oracle_lib, case):
+    N, R, r_min, B, sbar = case
+    if sbar.max() == sbar.min():
+        pytest.skip("constant signal: both readings give the uniform codec")
+    u = oracle_lib.weights(sbar)
+    lo, hi = float(sbar.min()), float(sbar.max())
+    shat = [Fraction((float(x) - lo)) / Fraction(hi - lo) for x in sbar]
+    if sum(shat) == 0:
+        pytest.skip("all-zero s_hat: Algorithm 1 itself divides 0 / 0")
+    q_s, stalled = alg1_exact_weights(shat, B, r_min, R)
+    al = oracle_lib.allocate(u, B, r_min, R)
+    q_w = continuous_from_oracle(al, u, r_min, R)
+    assert int(al.rank.sum()) == B
+    if stalled:
+        # Algorithm 1 reached 0/0: every remaining token has s_hat = 0 while budget is left.
+        # Under the reading, tokens with s_hat < 2^-24 weigh u = 1 like the zeros: the loop's
+        # capped tokens above that resolution stay capped, and the remainder is spread evenly
+        # over the u = 1 tokens.
+        assert all(q_w[t] == R for t in range(N) if q_s[t] == R and u[t] > 1)
+        ones = [t for t in range(N) if u[t] == 1]
+        assert ones and len({q_w[t] for t in ones}) == 1
+        assert sum(q_w) == B
+        return
+    lam = Fraction(al.M, al.Q) if al.Q else Fraction(0)
+    bound = (N + 1) * lam
+    gap = max(abs(a - b) for a, b in zip(q_w, q_s))
+    assert gap <= bound, (float(gap), float(bound))
+    # the integer ranks stay within one unit (plus the bound) of Algorithm 1 on s_hat
+    assert all(abs(r - q) < 1 + bound for r, q in zip(al.rank.tolist(), q_s))
+
+
+def alg1_exact_weights(w, B, r_min, R):
+    """Algorithm 1's loop in exact rationals with arbitrary non-negative weights w."""
+    N = len(w)
+    r = [Fraction(r_min)] * N
+    U = set(range(N))
+    while True:
+        delta = Fraction(B) - sum(r)
+        tot = sum(w[t] for t in U)
+        if tot == 0:
+            return r, delta > 0
+        for t in U:
+            r[t] += delta * w[t] / tot
+        S = {t for t in U if r[t] > R}
+        for t in S:
+            r[t] = Fraction(R)
+        U -= S
+        if not S:
+            return r, False
