@@ -196,6 +196,22 @@ VARRATE_API int varrate_decode_attn(const varrate_shape* shape, const varrate_ca
                         const void* q, int32_t Q, const float* P_K, const float* P_V,
                         void* out, void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): varrate_decode_attn without a workspace.
+ * The partial records go to a fixed device array of VARRATE_DECODE_SCRATCH_BYTES that the
+ * library holds on every device it runs on until the process ends (its address is looked
+ * up once per device, on the first call there).  Same arguments, results and bits as
+ * varrate_decode_attn; no allocation of any kind.  Returns VARRATE_EUNSUPPORTED when the
+ * call needs more scratch than that (varrate_decode_scratch_need(); typically about
+ * 4.3 MB: 512 partial records of 8320 bytes).  Every call on one device shares that
+ * device's array: calls that overlap in time on one device (two streams, two host
+ * threads) race and must be serialised by the caller.                                      */
+#define VARRATE_DECODE_SCRATCH_BYTES (8u << 20)
+VARRATE_API size_t varrate_decode_scratch_need(const varrate_shape* shape, int32_t S, int32_t Q);
+VARRATE_API int varrate_decode_attn_noalloc(const varrate_shape* shape, const varrate_cache* caches, int32_t S,
+                                const void* q, int32_t Q, const float* P_K, const float* P_V,
+                                void* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

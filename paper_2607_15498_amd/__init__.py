@@ -20,7 +20,7 @@ from . import _lib
 from ._lib import CHUNK, COEF_PAD, HEAD_DIM  # noqa: F401
 
 __all__ = ["VarRateError", "Shape", "Cache", "new_cache", "coded_budget", "salience", "allocate",
-           "project", "compress", "append_exact", "decode", "library"]
+           "project", "compress", "append_exact", "decode", "decode_noalloc", "library"]
 
 
 class VarRateError(RuntimeError):
@@ -243,4 +243,24 @@ def decode(shape: Shape, caches: Sequence[Cache], q: torch.Tensor, PK, PV, out: 
                                          _dev_ptr(PK, torch.float32, "PK"), _dev_ptr(PV, torch.float32, "PV"),
                                          _dev_ptr(out, shape.torch_dtype, "out"), ws.data_ptr(), ws.numel(),
                                          _stream()))
+    return out[0] if single else out
+
+
+def decode_noalloc(shape: Shape, caches: Sequence[Cache], q: torch.Tensor, PK, PV,
+                   out: torch.Tensor) -> torch.Tensor:
+    """Rank-space decode through varrate_decode_attn_noalloc: no workspace, the partial
+    records go to the library's fixed per-device scratch (calls on one device must not
+    overlap).  `out` must be preallocated ([S][Q][H][d] or [Q][H][d])."""
+    single = q.dim() == 3
+    if single:
+        q, out = q.unsqueeze(0), out.unsqueeze(0)
+    S, Q = int(q.shape[0]), int(q.shape[1])
+    if len(caches) != S:
+        raise VarRateError(_lib.VARRATE_EINVAL, f"{len(caches)} caches for {S} query sets")
+    arr = (_lib.CacheC * S)(*[c.c() for c in caches])
+    _check(library().varrate_decode_attn_noalloc(ctypes.byref(shape.c()), arr, S,
+                                                 _dev_ptr(q, shape.torch_dtype, "q"), Q,
+                                                 _dev_ptr(PK, torch.float32, "PK"),
+                                                 _dev_ptr(PV, torch.float32, "PV"),
+                                                 _dev_ptr(out, shape.torch_dtype, "out"), _stream()))
     return out[0] if single else out

@@ -20,8 +20,10 @@ EXPORTS = (
     "varrate_status_string", "varrate_last_error", "varrate_version", "varrate_coded_budget",
     "varrate_cache_bytes", "varrate_compress_workspace_bytes", "varrate_decode_workspace_bytes",
     "varrate_salience", "varrate_allocate", "varrate_project", "varrate_compress",
-    "varrate_append_exact", "varrate_decode_attn",
+    "varrate_append_exact", "varrate_decode_attn", "varrate_decode_scratch_need",
+    "varrate_decode_attn_noalloc",
 )
+DECODE_SCRATCH_BYTES = 8 << 20
 
 
 class Shape(ctypes.Structure):
@@ -72,6 +74,8 @@ def load() -> ctypes.CDLL:
         "varrate_compress": (ctypes.c_int, [P(Shape), vp, vp, vp, vp, vp, P(CacheC), vp, vp, sz, vp]),
         "varrate_append_exact": (ctypes.c_int, [P(Shape), P(CacheC), vp, vp, vp]),
         "varrate_decode_attn": (ctypes.c_int, [P(Shape), P(CacheC), i32, vp, i32, vp, vp, vp, vp, sz, vp]),
+        "varrate_decode_scratch_need": (sz, [P(Shape), i32, i32]),
+        "varrate_decode_attn_noalloc": (ctypes.c_int, [P(Shape), P(CacheC), i32, vp, i32, vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)

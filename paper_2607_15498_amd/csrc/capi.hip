@@ -287,4 +287,27 @@ int varrate_decode_attn(const varrate_shape* sh, const varrate_cache* caches, in
                       "decode launch");
 }
 
+size_t varrate_decode_scratch_need(const varrate_shape* sh, int32_t S, int32_t Q) {
+    if (check_shape(sh) || S < 1 || S > VARRATE_MAX_SEQS || Q < 1 ||
+        (int64_t)Q * (sh->H / sh->G) > VARRATE_MAX_QROWS)
+        return 0;
+    return decode_group_bytes(*sh, S, Q);
+}
+
+int varrate_decode_attn_noalloc(const varrate_shape* sh, const varrate_cache* caches, int32_t S, const void* q,
+                                int32_t Q, const float* PK, const float* PV, void* out, void* stream) {
+    int rc = check_decode(sh, caches, S, q, Q, PK, PV, out);
+    if (rc) return rc;
+    const size_t need = decode_group_bytes(*sh, S, Q);
+    if (need > (size_t)VARRATE_DECODE_SCRATCH_BYTES)
+        return fail(VARRATE_EUNSUPPORTED,
+                    "this decode needs %zu bytes of partial records, more than the fixed %zu-byte scratch; "
+                    "call varrate_decode_attn with a workspace instead",
+                    need, (size_t)VARRATE_DECODE_SCRATCH_BYTES);
+    uint8_t* scratch = nullptr;
+    if ((rc = hip_status(decode_scratch(&scratch), "decode scratch lookup"))) return rc;
+    return hip_status(launch_decode(*sh, caches, S, q, Q, PK, PV, out, scratch, (hipStream_t)stream, true),
+                      "decode launch");
+}
+
 }  // extern "C"

@@ -27,6 +27,8 @@
 //      and adds the exact part.
 // A tile's first token has the largest rank (storage is rank-descending per chunk), which
 // bounds its MFMA steps: ceil(r_max/32) score steps and ceil(r_max/16) value blocks.
+#include <mutex>
+
 #include "vr_internal.h"
 
 namespace vr {
@@ -914,7 +916,7 @@ size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
 
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
                          int Q, const float* PK, const float* PV, void* out, uint8_t* ws,
-                         hipStream_t st) {
+                         hipStream_t st, bool reuse_group_region) {
     DecPlan pl = plan_decode(sh, S, Q);
     const int hpg = sh.H / sh.G;
     const int rows_total = Q * hpg;
@@ -940,7 +942,9 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         for (int i = ns; i < DC_SEQ; ++i) prm.seq[i] = prm.seq[0];
         prm.PK = PK;
         prm.PV = PV;
-        prm.part = part + (size_t)s0 * sh.G * pl.nqt * (pl.n_wg + 1) * DC_REC;
+        // launch groups run in stream order, so with reuse_group_region every group's records
+        // go to the start of the buffer (the previous group's merge has finished reading them)
+        prm.part = reuse_group_region ? part : part + (size_t)s0 * sh.G * pl.nqt * (pl.n_wg + 1) * DC_REC;
         prm.N = sh.n - sh.w;
         prm.coef_stride = caches[s0].coef_stride;
         prm.cap = caches[s0].cap;
@@ -980,5 +984,41 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     return hipSuccess;
 }
 
+
+// ----------------------------------------------------------------------------------------
+// Decode without a caller workspace: the partial records live in a fixed device array.
+// Each device holds its own copy of `scratch` at its own address, looked up once per device
+// with hipGetSymbolAddress; host code only ever passes that address (the array's name is a
+// host-side stand-in).  The launch groups of one call reuse the array in stream order.  The
+// records need no clearing: every record the merge reads is written by the streaming launch
+// of the same group first.
+static __device__ __attribute__((aligned(256))) uint8_t scratch[VARRATE_DECODE_SCRATCH_BYTES];
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+static std::mutex scratch_mu;
+static void* scratch_addr[SCRATCH_MAX_DEVICES];
+
+size_t decode_group_bytes(const varrate_shape& sh, int S, int Q) {
+    DecPlan pl = plan_decode(sh, S, Q);
+    const int ns = S < DC_SEQ ? S : DC_SEQ;
+    return (size_t)ns * sh.G * pl.nqt * (pl.n_wg + 1) * DC_REC * sizeof(float);
+}
+
+hipError_t decode_scratch(uint8_t** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        scratch_addr[dev] = p;
+    }
+    *out = (uint8_t*)scratch_addr[dev];
+    return hipSuccess;
+}
 
 }  // namespace vr

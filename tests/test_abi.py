@@ -150,3 +150,28 @@ def test_decode_accumulator_agprs_are_private():
         m = re.search(r"\.set " + re.escape(name) + r"\.num_agpr, (\d+)", text)
         if m:
             assert int(m.group(1)) == 32
+
+
+def test_noalloc_decode_validates_and_bounds_its_scratch(L):
+    """The no-allocation decode validates like varrate_decode_attn and rejects a call whose
+    partial records exceed the fixed scratch, before touching the device."""
+    from paper_2607_15498_amd import _lib
+    sh = _shape()
+    cc = _lib.CacheC()
+    assert L.varrate_decode_attn_noalloc(ctypes.byref(sh), ctypes.byref(cc), 0, None, 1, None, None,
+                                         None, None) == -1
+    # the bench layer (batch 1) fits: at most 512 records of 8320 bytes
+    need = L.varrate_decode_scratch_need(ctypes.byref(sh), 1, 1)
+    assert 0 < need <= _lib.DECODE_SCRATCH_BYTES
+    assert need % 8320 == 0 and need // 8320 <= 512
+    # 16 sequences x 64 queries x 4 heads per KV head: 2048 units of 2 records, 34 MB > 8 MiB
+    S, Q = 16, 64
+    assert L.varrate_decode_scratch_need(ctypes.byref(sh), S, Q) > _lib.DECODE_SCRATCH_BYTES
+    b = _lib.CacheBytes()
+    assert L.varrate_cache_bytes(ctypes.byref(sh), 32, ctypes.byref(b)) == 0
+    fake = 1 << 20            # never dereferenced: the call fails before any device work
+    arr = (_lib.CacheC * S)(*[_lib.CacheC(fake, fake, fake, fake, fake, fake, fake, fake, b.coef_stride,
+                                          32, 32, b.N, b.B) for _ in range(S)])
+    rc = L.varrate_decode_attn_noalloc(ctypes.byref(sh), arr, S, fake, Q, fake, fake, fake, None)
+    assert rc == -3
+    assert b"scratch" in L.varrate_last_error()
