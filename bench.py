@@ -30,7 +30,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
-N_INPUT_COPIES = 3             # 3 x 134 MB of K/V
+N_INPUT_COPIES = 4             # 4 x 134 MB of K/V (537 MB > the 256 MB Infinity Cache)
 N_CACHE_SLOTS = 24             # 24 x 28 MB of compressed caches
 
 
@@ -44,6 +44,8 @@ def parse():
                     help="llama_32k: the headline layer (default).  The others are the model-stack "
                          "and query-agnostic workloads, reported in their own JSON line")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-stack", action="store_true",
+                    help="default run only: skip the 32-layer 128K stack that the line also reports")
     ap.add_argument("--mode", choices=("bench", "pmc"), default="bench",
                     help="pmc: a short run for hardware-counter passes (eager decodes on distinct "
                          "cache slots, then plain 64 MiB device copies that calibrate the byte counters)")
@@ -73,28 +75,99 @@ def compress_bytes(shape, cache):
     return read + write
 
 
-def cpu_baseline(cfg, li, shape, dbytes, budget_s=8.0, max_decodes=64):
-    """The fp64 oracle on the host cores: one compress of the layer, then repeated decodes of
-    the same query until about `budget_s` seconds of decode work (at most `max_decodes`)."""
+def _median_time(fn, reps):
+    ts, out = [], None
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        out = fn()
+        ts.append(time.perf_counter() - t0)
+    return float(np.median(ts)), out
+
+
+def _oracle_layer(oracle, cfg, li, reps=1, decode_reps=1):
+    """The oracle's stages on one layer, timed one by one (median of `reps` runs each), then
+    `decode_reps` decodes of the first query (median).  Returns seconds per stage."""
+    H, n, w, r_min = cfg["H"], cfg["n"], cfg["w"], cfg["r_min"]
+    N = n - w
+    st = {}
+    st["salience"], s = _median_time(lambda: oracle.salience(li.K, li.Qw, H), reps)
+    st["pool"], sb = _median_time(lambda: oracle.pool(s), reps)
+    st["weights"], u = _median_time(lambda: oracle.weights(sb), reps)
+    B = oracle.budget(n, 128, w, cfg["kappa"])
+    st["allocate"], al = _median_time(lambda: oracle.allocate(u, B, r_min, 128), reps)
+    st["project"], (cK, cV) = _median_time(
+        lambda: (oracle.project(li.K[:N], li.PK, al.rank, cfg["dtype"]),
+                 oracle.project(li.V[:N], li.PV, al.rank, cfg["dtype"])), reps)
+    st["compress"] = sum(st[k] for k in ("salience", "pool", "weights", "allocate", "project"))
+    Kx, Vx = np.ascontiguousarray(li.K[N:]), np.ascontiguousarray(li.V[N:])
+    dec = lambda: oracle.decode(cK, cV, al.rank, Kx, Vx, li.PK, li.PV, li.q[0], H)
+    st["decode"], _ = _median_time(dec, decode_reps)
+    return st, dec
+
+
+def cpu_baseline(cfg, li, dbytes, gpu, decode_reps=24, qwen_layers=4, llama128_layers=2):
+    """The fp64 oracle (as it stands) on the host cores, on bounded samples of the workloads:
+    the Llama 32K layer stage by stage (median of 3 compresses, median of `decode_reps`
+    decodes; one decode again on one thread), `qwen_layers` layers of one of the 8 Qwen
+    sequences scaled to the 28-layer x 8-sequence stack, and `llama128_layers` of the 32
+    layers of the 128K stack scaled to 32.  `gpu` holds the GPU figures for the ratios."""
     import oracle
+    from workloads import CONFIGS, make_layer
+    cores = oracle.threads()
     t0 = time.perf_counter()
-    oc = oracle.compress(li.K, li.V, li.Qw, li.PK, li.PV, cfg["H"], cfg["kappa"], cfg["r_min"], cfg["dtype"])
-    t1 = time.perf_counter()
-    reps = 0
-    while reps < max_decodes and (reps == 0 or time.perf_counter() - t1 < budget_s):
-        oracle.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[0], cfg["H"])
-        reps += 1
-    t2 = time.perf_counter()
-    return {
-        "value": round(dbytes * reps / (t2 - t1) / 1e9, 4),
+    st, dec = _oracle_layer(oracle, cfg, li, reps=3, decode_reps=decode_reps)
+    oracle.set_threads(1)
+    try:
+        t1thr, _ = _median_time(dec, 1)
+    finally:
+        oracle.set_threads(cores)
+    ms = {k: round(v * 1e3, 2) for k, v in st.items()}
+    out = {
+        "value": round(dbytes / st["decode"] / 1e9, 4),
         "unit": "GB/s",
-        "cores": oracle.threads(),
+        "cores": cores,
         "kind": "oracle",
-        "sample": f"one full {cfg['n']}-token layer of this workload: fp64 compress "
-                  f"({t1 - t0:.2f} s), then {reps} decodes of one query ({t2 - t1:.2f} s, "
-                  f"reconstruct-in-place); value = decode bytes / decode time",
-        "compress_ms_per_32k_tokens": round((t1 - t0) * 1e3 * 32768 / cfg["n"], 1),
+        "sample": f"llama_32k: one full layer ({cfg['n']} tokens), fp64 stages timed one by one "
+                  f"(median of 3), decode of one query median of {decode_reps} "
+                  f"(reconstruct-in-place); value = decode bytes / decode time",
+        "stage_ms": ms,
+        "compress_ms_per_32k_tokens": round(st["compress"] * 1e3 * 32768 / cfg["n"], 1),
+        "decode_GBps_1_thread": round(dbytes / t1thr / 1e9, 5),
+        "gpu_over_cpu": {"decode": round(st["decode"] * 1e3 / gpu["decode_ms"], 1),
+                         "compress": round(st["compress"] * 1e3 / gpu["compress_ms"], 1)},
     }
+    # Qwen2.5-7B-shaped stack: `qwen_layers` of 28 layers, sequence 0 of 8, scaled x (28/L) x 8
+    qc = CONFIGS["qwen_16k_stack"]
+    acc = {"compress": 0.0, "decode": 0.0}
+    for lyr in range(qwen_layers):
+        qli = make_layer(qc, layer=lyr, seq=0, n_queries=1)
+        qst, _ = _oracle_layer(oracle, qc, qli)
+        acc["compress"] += qst["compress"]
+        acc["decode"] += qst["decode"]
+    sc = qc["layers"] / qwen_layers * qc["batch"]
+    out["qwen_16k_stack_scaled"] = {
+        "sample": f"layers 0..{qwen_layers - 1} of sequence 0 (of 28 layers x 8 sequences), scaled x{sc:g}",
+        "compress_ms_stack": round(acc["compress"] * 1e3 * sc, 1),
+        "decode_ms_per_step": round(acc["decode"] * 1e3 * sc, 1),
+        "decode_tokens_per_s": round(qc["batch"] / (acc["decode"] * sc), 3),
+    }
+    # Llama-3.1-8B-shaped 128K stack: `llama128_layers` of 32 layers, scaled x 32/L
+    lc = CONFIGS["llama_128k_stack"]
+    acc = {"compress": 0.0, "decode": 0.0}
+    for lyr in range(llama128_layers):
+        lli = make_layer(lc, layer=lyr, n_queries=1)
+        lst, _ = _oracle_layer(oracle, lc, lli)
+        acc["compress"] += lst["compress"]
+        acc["decode"] += lst["decode"]
+    sc = lc["layers"] / llama128_layers
+    out["llama_128k_stack_scaled"] = {
+        "sample": f"layers 0..{llama128_layers - 1} of 32 (host draws), scaled x{sc:g}",
+        "compress_ms_per_32k_tokens": round(acc["compress"] * 1e3 * sc * 32768 / (lc["n"] * lc["layers"]), 1),
+        "decode_ms_per_step": round(acc["decode"] * 1e3 * sc, 1),
+        "decode_tokens_per_s": round(1.0 / (acc["decode"] * sc), 4),
+    }
+    out["wall_s"] = round(time.perf_counter() - t0, 1)
+    return out
 
 
 # HBM bytes of one decode call (both launches), from the FETCH_SIZE and WRITE_SIZE counter
@@ -218,18 +291,9 @@ def main():
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
 
-    def time_graph(g_, reps):
-        g_.replay()
-        torch.cuda.synchronize()
-        a, b = ev(), ev()
-        a.record()
-        for _ in range(reps):
-            g_.replay()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / (reps * N_CACHE_SLOTS)   # ms per launch
-
-    stage = {name: time_graph(g_, 4) for name, g_ in graphs.items()}
+    # per stage: median (p10, p90) over replays of its graph, per launch
+    stage_st = {name: _replay_stats(g_, 8, N_CACHE_SLOTS) for name, g_ in graphs.items()}
+    stage = {name: st["p50"] for name, st in stage_st.items()}
 
     # timed region: exactly `steps` whole steps (compress + decode)
     steps = args.steps
@@ -273,31 +337,65 @@ def main():
         "compress_ms_per_32k_tokens": round(ms_comp * 32768 / cfg["n"], 4),
         "compress_GBps_algorithmic": round(cbytes / (ms_comp * 1e-3) / 1e9, 1),
         "stage_ms": {k: round(v, 4) for k, v in stage.items()},
+        "stage_ms_p10_p90": {k: [round(st["p10"], 4), round(st["p90"], 4)] for k, st in stage_st.items()},
+        "timing": "medians over 8 replays of a graph of 24 launches on distinct inputs/caches "
+                  "(HIP events on the launching stream); p10/p90 beside them",
         "roofline": {"kernel": "decode_kernel (rank-space decode attention)", "bound": "hbm",
                      "achieved": round(dbytes / (ms_dec * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(dbytes / (ms_dec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": decode_traffic(), "bytes_per_launch": int(dbytes)},
     }
+    if not args.no_stack:
+        # the 128K end of the 32K-128K target range: the 32-layer Llama stack, decode at batch 1
+        del graphs, step_graphs, slots, Ks, Vs, sbars
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        stk = bench_stack(args, "llama_128k_stack", emit=False)
+        result["llama_128k_stack"] = {
+            "workload": stk["config"]["workload"],
+            "decode_GBps": stk["value"], "pct_hbm_peak": stk["pct_hbm_peak"],
+            "frac": round(stk["value"] / HBM_PEAK_GBS, 4),
+            "decode_ms_per_step": stk["ms_per_step"], "decode_ms_per_step_p10_p90": stk["ms_per_step_p10_p90"],
+            "decode_us_per_layer": round(stk["ms_per_step"] * 1e3 / 32, 2),
+            "decode_tokens_per_s": stk["decode_tokens_per_s"],
+            "decode_bytes_per_step": stk["decode_bytes_per_step"],
+            "compress_ms_per_32k_tokens": stk["compress_ms_per_32k_tokens"],
+            "compress_ms_per_32k_tokens_all_layers": stk["compress_ms_per_32k_tokens_all_layers"],
+        }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cfg, li, shape, dbytes)
+        result["cpu_baseline"] = cpu_baseline(cfg, li, dbytes, {"decode_ms": ms_dec, "compress_ms": ms_comp})
     print(json.dumps(result), flush=True)
 
 
 def _graph_ms(g_, reps):
-    """Average ms of one replay of a captured graph (events on the current stream)."""
+    """Median ms of one replay of a captured graph over `reps` replays (events on the
+    current stream, which the replays run on)."""
+    return _replay_stats(g_, reps)["p50"]
+
+
+def _replay_stats(g_, reps, per=1):
+    """Per-replay durations of a captured graph (HIP events on the current stream around
+    each replay, back to back), divided by `per` launches per replay: median, p10, p90, mean
+    in ms."""
     import torch
     g_.replay()
     torch.cuda.synchronize()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record()
-    for _ in range(reps):
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+    evs[0].record()
+    for i in range(reps):
         g_.replay()
-    b.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
-    return a.elapsed_time(b) / reps
+    t = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(reps)]) / per
+    return {"p50": float(np.median(t)), "p10": float(np.percentile(t, 10)),
+            "p90": float(np.percentile(t, 90)), "mean": float(t.mean()), "n": int(reps)}
 
 
-def bench_stack(args):
+def _pct(st, nd=4):
+    return {k: (round(v, nd) if isinstance(v, float) else v) for k, v in st.items()}
+
+
+def bench_stack(args, config=None, emit=True):
     """Whole model stack: every layer (and sequence) drawn on the device, compressed, then
     decode steps of one query per sequence over all layers (one decode call per layer, the
     batch's caches in that call).  Compress and decode are timed from captured graphs.  The
@@ -309,7 +407,8 @@ def bench_stack(args):
     from workloads import CONFIGS, make_head_model
     from workloads.synth_gpu import make_layer_device
 
-    cfg = CONFIGS[args.config]
+    name = config or args.config
+    cfg = CONFIGS[name]
     L, S, n, w = cfg["layers"], cfg["batch"], cfg["n"], cfg["w"]
     extra = 128 if S > 1 else 0
     dev = torch.device("cuda:0")
@@ -374,17 +473,19 @@ def bench_stack(args):
     for _ in range(args.warmup):
         g_step.replay()
     torch.cuda.synchronize()
-    ms_step = _graph_ms(g_step, max(args.steps, 1))
-    ms_comp = _graph_ms(g_comp, 2)
+    st_step = _replay_stats(g_step, max(args.steps, 1))
+    ms_step = st_step["p50"]
+    ms_comp = _replay_stats(g_comp, 3)["p50"]
     dbytes = sum(decode_bytes(shape, c) for row in caches for c in row)
     gbs = dbytes / (ms_step * 1e-3) / 1e9
     result = {
         "metric": "compressed decode attn GB/s (% HBM peak) + compress ms per 32K tokens, 1 GPU",
         "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "ms_per_step": round(ms_step, 4), "ms_per_step_p10_p90": [round(st_step["p10"], 4), round(st_step["p90"], 4)],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg["dtype"], "data": "synthetic, drawn on the device (same recipe as the parity inputs, "
                                         "device Philox draws per layer/head/sequence)",
-        "config": {"workload": f"{args.config}: {L} layers, {cfg['G']} KV x {cfg['H']} q heads, d 128, "
+        "config": {"workload": f"{name}: {L} layers, {cfg['G']} KV x {cfg['H']} q heads, d 128, "
                                f"n {n}, w {w}, budget {cfg['kappa']}%, r_min {cfg['r_min']}, "
                                f"batch {S} independent sequences, decode exact tail w + {extra}",
                    "decode_calls_per_step": L},
@@ -398,7 +499,9 @@ def bench_stack(args):
         "compress_ms_total": round(ms_comp, 3),
         "draw_s": round(t_draw, 1),
     }
-    print(json.dumps(result), flush=True)
+    if emit:
+        print(json.dumps(result), flush=True)
+    return result
 
 
 def bench_agnostic(args):

@@ -50,6 +50,8 @@ def lib():
         L.vro_budget.restype = _i64
         L.vro_budget.argtypes = [_i64, _i64, _i64, _i64]
         L.vro_threads.restype = _int
+        L.vro_set_threads.restype = None
+        L.vro_set_threads.argtypes = [_int]
         L.vro_salience.restype = None
         L.vro_salience.argtypes = [_i64, _int, _int, _int, _int, _f32p, _f32p, _f64p]
         L.vro_pool.restype = None
@@ -71,6 +73,11 @@ def lib():
 
 def threads() -> int:
     return int(lib().vro_threads())
+
+
+def set_threads(n: int) -> None:
+    """Thread count of the oracle's OpenMP loops from now on."""
+    lib().vro_set_threads(int(n))
 
 
 def _c(a, dt):

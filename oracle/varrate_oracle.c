@@ -52,6 +52,16 @@ EXPORT int vro_threads(void)
 #endif
 }
 
+/* Thread count of the OpenMP loops that follow (the timing harness's 1-thread baseline). */
+EXPORT void vro_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------------------- */
 /* Sec. 3.1 attention + Sec. 3.2 Eq. (4).
  * Window query i (0 <= i < w) sits at position p = n - w + i and attends causally to keys

@@ -688,186 +688,137 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
 // ----------------------------------------------------------------------------------------
 // Merge of the partial records of one (sequence, KV head, row tile): log-sum-exp over the
 // records (record 0 = exact slots, original space; records 1.. = coded tile ranges, rank
-// space), back-rotation of the rank-space sum with P_V^T by MFMA, division by the softmax
+// space), back-rotation of the rank-space sum with P_V^T, division by the softmax
 // denominator.  A separate launch: the kernel boundary publishes every record, so no
-// workgroup of the streaming kernel needs a device-wide fence.  Every load (basis
-// columns, record maxima and sums, the first batch of record rows) is issued before the
-// first wait.
+// workgroup of the streaming kernel needs a device-wide fence.
+// The merge is spread over one workgroup per (unit, query row, block of 32 output columns),
+// so no workgroup pulls more than one row of every record (512 bytes each) and a 128 x 32
+// slab of the basis; every load is issued before the first wait, and the small per-row
+// reductions are repeated by the column blocks instead of exchanged.
 struct MergeParams {
     const float* part;
     const float* PV;
     void* out;              // [S][Q][H][d] of this launch's sequences
     int64_t out_seq_stride; // elements per sequence
-    int G, H, hpg, nqt, rows_total, n_wg;
+    int G, H, hpg, nqt, rows_total, n_wg, rpu;
 };
 
-constexpr int MG_BATCH = 16;   // record rows per thread in flight
+constexpr int MG_THREADS = 256;
+constexpr int MG_COLS = 32;                       // output columns per workgroup
+constexpr int MG_CB = D / MG_COLS;                // column blocks per row
+constexpr int MG_RPT = 32;                        // coded records per thread in registers
 
 template <bool F32>
-__global__ __launch_bounds__(DC_THREADS) void decode_merge_kernel(MergeParams p) {
+__global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p) {
     typedef typename Elem<F32>::T ET;
-    __shared__ float wm[DC_MAX_REC * 16 + DC_THREADS];   // + a dummy slot per thread
-    __shared__ float wl[DC_MAX_REC * 16 + DC_THREADS];
-    __shared__ __attribute__((aligned(16))) float lanes[DC_THREADS * 4];
-    __shared__ __attribute__((aligned(16))) float accR[16 * DC_CROW];   // rows padded: no bank conflicts
-    __shared__ __attribute__((aligned(16))) float accE[16 * DC_CROW];
-    __shared__ float red[2][DC_WAVES][16];
-    __shared__ float mrow[16], lrow[16];
-    const int unit = blockIdx.x;
+    __shared__ float wr[DC_MAX_REC];              // record weights exp(m_r - M)
+    __shared__ float red[2][MG_THREADS / 64];
+    __shared__ float accR[2][D];
+    __shared__ float part8[8][MG_COLS];
+    const int cb = blockIdx.x % MG_CB;
+    const int row = (blockIdx.x / MG_CB) % p.rpu;
+    const int unit = blockIdx.x / (MG_CB * p.rpu);
     const int units = p.G * p.nqt;
     const int sq = unit / units, gq = unit % units;
     const int g = gq / p.nqt, qt = gq % p.nqt;
     const int rows = min(16, p.rows_total - 16 * qt);
-    const int nr4 = (rows + 3) & ~3;
+    if (row >= rows) return;                      // row tiles with fewer rows (workgroup-uniform)
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int grp = lane >> 4, col = lane & 15;
     const int nrec = p.n_wg + 1;
     const float* recs = p.part + (int64_t)unit * nrec * DC_REC;
-    const int E = nr4 * D / 4;                  // float4s per record
-    const int KL = DC_THREADS / E;              // record lanes
-    const int e4 = tid % E, k4 = tid / E;
-    const int row4 = (e4 * 4) / D;
 
-    // ---- 1. issue the first batch of coded record rows, the basis columns and the record
-    //          maxima / sums (the first 1024 of each held in registers), then store the
-    //          maxima / sums to LDS: one memory round trip
-    f32x4 a[MG_BATCH];
+    // ---- 1. issue every load: this row's max and sum of each record, its rank-space row of
+    //          the coded records (thread -> coordinate j, half h of the records), the basis
+    //          slab rows 16 jg .. 16 jg + 15 at column c, and the exact record's row piece
+    const int j = tid & (D - 1), h = tid >> 7;
+    const int c = tid & (MG_COLS - 1), jg = tid >> 5;
+    float ms[2], ls[2];
 #pragma unroll
-    for (int u = 0; u < MG_BATCH; ++u) {
-        const int r = 1 + k4 + u * KL;
-        a[u] = k4 < KL && r < nrec ? reinterpret_cast<const f32x4*>(recs + (int64_t)r * DC_REC + 32)[e4]
-                                   : f32x4{0, 0, 0, 0};
+    for (int k = 0; k < 2; ++k) {
+        const int r = tid + k * MG_THREADS;
+        const int rr = r < nrec ? r : 0;
+        ms[k] = recs[(int64_t)rr * DC_REC + row];
+        ls[k] = recs[(int64_t)rr * DC_REC + 16 + row];
     }
-    const float* PV = p.PV + (int64_t)g * D * D;
-    float pb[4][8];
+    float a[MG_RPT];
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) pb[s][i] = PV[(32 * s + 8 * grp + i) * D + 16 * wave + col];
-    const f32x4 ex = tid < E ? reinterpret_cast<const f32x4*>(recs + 32)[tid] : f32x4{0, 0, 0, 0};
-    float ml[2][2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        int idx = tid + h * DC_THREADS;
-        idx = idx < nrec * 16 ? idx : nrec * 16 - 1;          // clamped: unconditional loads
-        const int r = idx >> 4, row = idx & 15;
-        ml[h][0] = recs[(int64_t)r * DC_REC + row];
-        ml[h][1] = recs[(int64_t)r * DC_REC + 16 + row];
+    for (int u = 0; u < MG_RPT; ++u) {
+        const int r = 1 + h + 2 * u;
+        a[u] = r < nrec ? recs[(int64_t)r * DC_REC + 32 + row * D + j] : 0.f;
     }
+    const float* PV = p.PV + (int64_t)g * D * D + MG_COLS * cb + c;
+    float pb[16];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {      // unconditional stores (past the records: dummy slot)
-        const int idx = tid + h * DC_THREADS;
-        const int dst = idx < nrec * 16 ? idx : DC_MAX_REC * 16 + tid;
-        wm[dst] = ml[h][0];
-        wl[dst] = ml[h][1];
+    for (int i = 0; i < 16; ++i) pb[i] = PV[(int64_t)(16 * jg + i) * D];
+    const float ex = tid < MG_COLS ? recs[32 + row * D + MG_COLS * cb + tid] : 0.f;
+
+    // ---- 2. row maximum over the records, record weights, softmax denominator
+    float mx = fmaxf(tid < nrec ? ms[0] : -INFINITY, tid + MG_THREADS < nrec ? ms[1] : -INFINITY);
+    for (int r = tid + 2 * MG_THREADS; r < nrec; r += MG_THREADS) mx = fmaxf(mx, recs[(int64_t)r * DC_REC + row]);
+    mx = xmax32(xmax16(wave_max16(mx)));
+    if (lane == 0) red[0][wave] = mx;
+    __syncthreads();
+    float M = red[0][0];
+#pragma unroll
+    for (int w = 1; w < MG_THREADS / 64; ++w) M = fmaxf(M, red[0][w]);
+    float lsum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int r = tid + k * MG_THREADS;
+        if (r < nrec) {
+            const float wgt = ms[k] == -INFINITY ? 0.f : fast_exp(ms[k] - M);
+            wr[r] = wgt;
+            lsum += wgt * ls[k];
+        }
     }
-    for (int idx = tid + 2 * DC_THREADS; idx < nrec * 16; idx += DC_THREADS) {
-        const int r = idx >> 4, row = idx & 15;
-        wm[idx] = recs[(int64_t)r * DC_REC + row];
-        wl[idx] = recs[(int64_t)r * DC_REC + 16 + row];
+    for (int r = tid + 2 * MG_THREADS; r < nrec; r += MG_THREADS) {
+        const float m = recs[(int64_t)r * DC_REC + row];
+        const float wgt = m == -INFINITY ? 0.f : fast_exp(m - M);
+        wr[r] = wgt;
+        lsum += wgt * recs[(int64_t)r * DC_REC + 16 + row];
     }
+    // fixed-order sum: lanes, then waves
+    lsum = xsum32(xsum16(lsum + shfl_xor_f(lsum, 1)));
+    lsum += shfl_xor_f(lsum, 2);
+    lsum += shfl_xor_f(lsum, 4);
+    lsum += shfl_xor_f(lsum, 8);
+    if (lane == 0) red[1][wave] = lsum;
+    __syncthreads();
+    float L = red[1][0];
+#pragma unroll
+    for (int w = 1; w < MG_THREADS / 64; ++w) L += red[1][w];
+
+    // ---- 3. weighted sum of the coded records' rank-space rows (two halves, fixed order)
+    float s = 0.f;
+#pragma unroll
+    for (int u = 0; u < MG_RPT; ++u) {
+        const int r = 1 + h + 2 * u;
+        s += (r < nrec ? wr[r] : 0.f) * a[u];
+    }
+    for (int r = 1 + h + 2 * MG_RPT; r < nrec; r += 2) s += wr[r] * recs[(int64_t)r * DC_REC + 32 + row * D + j];
+    accR[h][j] = s;
     __syncthreads();
 
-    // ---- 2. row maxima, record weights, row sums (32 threads per row)
-    {
-        const int row = tid & 15, part = tid >> 4;
-        float mx = -INFINITY;
-        for (int r = part; r < nrec; r += 32) mx = fmaxf(mx, wm[r * 16 + row]);
-        mx = fmaxf(mx, shfl_xor_f(mx, 16));
-        mx = fmaxf(mx, shfl_xor_f(mx, 32));
-        if (lane < 16) red[0][wave][row] = mx;
+    // ---- 4. back-rotation: out[c] = sum_j accR[j] P_V[j][c], 8 groups of 16 coordinates
+    float o = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        const int jj = 16 * jg + i;
+        o += (accR[0][jj] + accR[1][jj]) * pb[i];
     }
+    part8[jg][c] = o;
     __syncthreads();
-    if (tid < 16) {
-        float M = -INFINITY;
-        for (int w = 0; w < DC_WAVES; ++w) M = fmaxf(M, red[0][w][tid]);
-        mrow[tid] = M;
-    }
-    __syncthreads();
-    {
-        const int row = tid & 15, part = tid >> 4;
-        const float M = mrow[row];
-        float ls = 0.f;
-        for (int r = part; r < nrec; r += 32) {
-            const float m = wm[r * 16 + row];
-            const float wgt = m == -INFINITY ? 0.f : fast_exp(m - M);
-            wm[r * 16 + row] = wgt;
-            ls += wgt * wl[r * 16 + row];
-        }
-        ls += shfl_xor_f(ls, 16);
-        ls += shfl_xor_f(ls, 32);
-        if (lane < 16) red[1][wave][row] = ls;
-    }
-    __syncthreads();
-    if (tid < 16) {
-        float L = 0.f;
-        for (int w = 0; w < DC_WAVES; ++w) L += red[1][w][tid];
-        lrow[tid] = L;
-    }
-    // ---- 3. weighted sum of the coded records: thread -> (float4 e4, record lane k4)
-    {
-        f32x4 s4 = {0, 0, 0, 0};
-        if (k4 < KL) {
+    if (tid < MG_COLS) {
+        float t = part8[0][tid];
 #pragma unroll
-            for (int u = 0; u < MG_BATCH; ++u) {
-                const int r = 1 + k4 + u * KL;
-                s4 += (r < nrec ? wm[r * 16 + row4] : 0.f) * a[u];
-            }
-            for (int r0 = 1 + k4 + MG_BATCH * KL; r0 < nrec; r0 += 8 * KL) {
-                f32x4 b8[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int r = r0 + u * KL;
-                    b8[u] = r < nrec ? reinterpret_cast<const f32x4*>(recs + (int64_t)r * DC_REC + 32)[e4]
-                                     : f32x4{0, 0, 0, 0};
-                }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int r = r0 + u * KL;
-                    s4 += (r < nrec ? wm[r * 16 + row4] : 0.f) * b8[u];
-                }
-            }
-        }
-        reinterpret_cast<f32x4*>(lanes)[tid] = s4;
-    }
-    __syncthreads();
-    if (tid < E) {
-        f32x4 t = reinterpret_cast<const f32x4*>(lanes)[tid];
-        for (int kk = 1; kk < KL; ++kk) t += reinterpret_cast<const f32x4*>(lanes)[kk * E + tid];
-        const int ci = (tid >> 5) * DC_CROW + 4 * (tid & 31);     // row tid/32, float4 tid%32
-        *reinterpret_cast<f32x4*>(accR + ci) = t;
-        *reinterpret_cast<f32x4*>(accE + ci) = wm[(tid * 4) / D] * ex;
-    }
-    __syncthreads();
-    // ---- 4. back-rotation by MFMA: C[row][c] = sum_j accR[row][j] P_V[j][c]
-    // wave -> column block 16 wave.., lane -> column col, K group grp
-    f32x4 o = {0, 0, 0, 0};
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        float a8[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) a8[i] = col < nr4 ? accR[col * DC_CROW + 32 * s + 8 * grp + i] : 0.f;
-        u32x4 ah, al, bh, bl;
-        split8(a8, ah, al);
-        split8(pb[s], bh, bl);
-        o = mfma(ah, bh, o);
-        o = mfma(al, bh, o);
-        o = mfma(ah, bl, o);
-    }
-    // C lane -> column c = 16 wave + col, rows 4 grp + v
-    ET* out = reinterpret_cast<ET*>(p.out) + (int64_t)sq * p.out_seq_stride;
-    const int c = 16 * wave + col;
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        const int row = 4 * grp + v;
-        if (row < rows) {
-            const float val = (o[v] + accE[row * DC_CROW + c]) / lrow[row];
-            const int qrow = 16 * qt + row;
-            const int query = qrow / p.hpg, hh = qrow % p.hpg;
-            const int64_t oi = ((int64_t)query * p.H + g * p.hpg + hh) * D + c;
-            if constexpr (F32) out[oi] = val;
-            else out[oi] = (uint16_t)f32_to_bf16(val);
-        }
+        for (int k = 1; k < 8; ++k) t += part8[k][tid];
+        const float val = (t + wr[0] * ex) / L;
+        const int qrow = 16 * qt + row;
+        const int query = qrow / p.hpg, hh = qrow % p.hpg;
+        ET* out = reinterpret_cast<ET*>(p.out) + (int64_t)sq * p.out_seq_stride;
+        const int64_t oi = ((int64_t)query * p.H + g * p.hpg + hh) * D + MG_COLS * cb + tid;
+        if constexpr (F32) out[oi] = val;
+        else out[oi] = (uint16_t)f32_to_bf16(val);
     }
 }
 // ----------------------------------------------------------------------------------------
@@ -975,9 +926,10 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         mp.nqt = pl.nqt;
         mp.rows_total = rows_total;
         mp.n_wg = pl.n_wg;
-        const unsigned nunits = (unsigned)(ns * sh.G * pl.nqt);
-        if (sh.dtype == VARRATE_BF16) decode_merge_kernel<false><<<nunits, DC_THREADS, 0, st>>>(mp);
-        else decode_merge_kernel<true><<<nunits, DC_THREADS, 0, st>>>(mp);
+        mp.rpu = rows_total < 16 ? rows_total : 16;
+        const unsigned nmerge = (unsigned)(ns * sh.G * pl.nqt * mp.rpu * MG_CB);
+        if (sh.dtype == VARRATE_BF16) decode_merge_kernel<false><<<nmerge, MG_THREADS, 0, st>>>(mp);
+        else decode_merge_kernel<true><<<nmerge, MG_THREADS, 0, st>>>(mp);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
