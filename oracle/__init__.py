@@ -64,6 +64,11 @@ def lib():
                                    ctypes.POINTER(_i64)]
         L.vro_project.restype = None
         L.vro_project.argtypes = [_i64, _int, _int, _f32p, _f32p, _i32p, _int, _f32p]
+        L.vro_half_round.restype = ctypes.c_float
+        L.vro_half_round.argtypes = [ctypes.c_float]
+        L.vro_quantize.restype = None
+        L.vro_quantize.argtypes = [_i64, _int, _int, _f32p, _i32p, _int,
+                                   np.ctypeslib.ndpointer(np.int8, flags="C_CONTIGUOUS"), _f32p, _f32p]
         L.vro_decode.restype = None
         L.vro_decode.argtypes = [_i64, _i64, _int, _int, _int, _f32p, _f32p, _i32p,
                                  _f32p, _f32p, _f32p, _f32p, _f32p, _f64p]
@@ -157,6 +162,29 @@ def decode(coefK, coefV, rank, Kx, Vx, PK, PV, q, H: int) -> np.ndarray:
                      _c(rank, np.int32), _c(Kx, np.float32), _c(Vx, np.float32),
                      _c(PK, np.float32), _c(PV, np.float32), _c(q, np.float32), out)
     return out
+
+
+def half_round(x: float) -> float:
+    """Nearest IEEE binary16 value of an fp32 value (ties to even), as a float."""
+    return float(lib().vro_half_round(float(x)))
+
+
+@dataclass
+class Quantized:
+    codes: np.ndarray    # int8 [N][G][d], zero past each rank
+    scales: np.ndarray   # float32 [N][G][d/32] (binary16 values)
+    deq: np.ndarray      # float32 [N][G][d] = codes * scale of their group
+
+
+def quantize(coef: np.ndarray, rank: np.ndarray, bits: int) -> Quantized:
+    """Sec. 3.3 "Composability": group-wise symmetric b-bit codes of stored coefficients
+    (groups: one token, one head, 32 consecutive coordinates below its rank)."""
+    n, G, d = coef.shape
+    codes = np.zeros((n, G, d), np.int8)
+    scales = np.zeros((n, G, (d + 31) // 32), np.float32)
+    deq = np.zeros((n, G, d), np.float32)
+    lib().vro_quantize(n, G, d, _c(coef, np.float32), _c(rank, np.int32), int(bits), codes, scales, deq)
+    return Quantized(codes, scales, deq)
 
 
 @dataclass

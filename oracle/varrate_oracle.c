@@ -14,6 +14,7 @@
  *                          on integer ranks
  *   projection/truncation  Sec. 3.3 Eq. (6) "eq:recon", Algorithm 1 (projection step)
  *   decode                 Sec. 4.4 "Cost": reconstruct-in-place, then stock attention
+ *   coefficient quantiser  Sec. 3.3 "Composability": group-wise b-bit codes of the coefficients
  *
  * Specialisation (the data-parallel path only): per-KV-head bases P in R^{d x d} (R = d, so
  * full rank is exact), no anchors (residual mean zbar = 0), no RoPE, exact set = last w tokens.
@@ -354,4 +355,70 @@ EXPORT void vro_decode(int64_t N, int64_t n_exact, int G, int H, int d,
     free(kh);
     free(vh);
     free(x);
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Sec. 3.3 "Composability": the coefficients are themselves quantised, group-wise, to b
+ * bits, with the allocation unchanged.  Reading (the paper names only "standard group-wise
+ * b-bit quantization"): symmetric absmax groups; a group is one token's coefficients of one
+ * head and one stream (K or V) in one 32-coordinate segment [32 s, min(32 s + 32, r_t)).
+ * With Qmax = 2^(b-1) - 1 the group's scale is
+ *     sc = half(fp32(amax / Qmax))          (IEEE fp32 division, then nearest binary16)
+ * and each coefficient x of the group gets the code
+ *     k = clamp(rint(fp32(x / sc)), -Qmax, Qmax)    (IEEE fp32 division, ties to even),
+ * read back as k * sc.  A group whose scale is 0 codes every entry as 0; entries past the
+ * token's rank are 0.  The input x is the stored (storage-rounded) coefficient.            */
+
+/* Nearest IEEE 754 binary16 value (ties to even) of an fp32 value, returned as fp32:
+ * 11 significant bits for |x| >= 2^-14, a fixed quantum of 2^-24 below that (subnormals),
+ * infinity past the largest finite value 65504.                                          */
+EXPORT float vro_half_round(float x)
+{
+    if (x == 0.0f || !isfinite(x)) return x;
+    int e;
+    (void)frexp((double)x, &e);             /* |x| = m 2^e, 0.5 <= m < 1 */
+    int qexp = e - 11;                      /* quantum of an 11-bit significand */
+    if (qexp < -24) qexp = -24;             /* subnormal range */
+    double r = nearbyint(ldexp((double)x, -qexp)) ;
+    double y = ldexp(r, qexp);
+    if (fabs(y) > 65504.0) return x > 0 ? INFINITY : -INFINITY;
+    return (float)y;
+}
+
+EXPORT void vro_quantize(int64_t n_tok, int G, int d, const float *coef, const int32_t *rank,
+                         int bits, int8_t *codes, float *scales, float *deq)
+{
+    const int qmax = (1 << (bits - 1)) - 1;
+    const int nseg = (d + 31) / 32;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < n_tok; ++t) {
+        for (int g = 0; g < G; ++g) {
+            const float *x = coef + (t * G + g) * d;
+            int8_t *k = codes + (t * G + g) * d;
+            float *y = deq + (t * G + g) * d;
+            for (int j = 0; j < d; ++j) { k[j] = 0; y[j] = 0.0f; }
+            for (int sg = 0; sg < nseg; ++sg) {
+                const int lo = 32 * sg;
+                int hi = lo + 32 < rank[t] ? lo + 32 : rank[t];
+                if (hi > d) hi = d;
+                float amax = 0.0f;
+                for (int j = lo; j < hi; ++j) {
+                    const float a = fabsf(x[j]);
+                    if (a > amax) amax = a;
+                }
+                volatile float ratio = amax / (float)qmax;
+                const float sc = vro_half_round(ratio);
+                scales[(t * G + g) * nseg + sg] = sc;
+                if (sc == 0.0f) continue;
+                for (int j = lo; j < hi; ++j) {
+                    volatile float q = x[j] / sc;
+                    float r = nearbyintf(q);
+                    if (r > (float)qmax) r = (float)qmax;
+                    if (r < -(float)qmax) r = -(float)qmax;
+                    k[j] = (int8_t)r;
+                    y[j] = r * sc;
+                }
+            }
+        }
+    }
 }
