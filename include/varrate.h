@@ -196,6 +196,53 @@ VARRATE_API int varrate_decode_attn(const varrate_shape* shape, const varrate_ca
                         const void* q, int32_t Q, const float* P_K, const float* P_V,
                         void* out, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- quantised coefficients (Sec. 3.3 "Composability") -------------------------------- */
+/* The coefficients of a compressed bf16 layer quantised group-wise to b bits, the allocation
+ * (ranks, storage order, exact rows) unchanged.  A group is one stored position's
+ * coefficients of one head and stream in one 32-coordinate segment [32 s, 32 s + 32) below
+ * its rank; symmetric absmax with Qmax = 2^(b-1) - 1:
+ *     sc = binary16(fp32(amax / Qmax)),  k = clamp(rint(fp32(x / sc)), -Qmax, Qmax),
+ * fp32 divisions correctly rounded, ties to even; a group with sc = 0 codes 0; x is the
+ * stored bf16 coefficient, read back as k * sc.
+ * Layout, per head stream (K and V alike), tile by tile in the layer's storage order: tile
+ * h of chunk c (size m = its first position's rank, mq = m rounded up to a multiple of 8,
+ * KS = ceil(m / 32)) takes 2 mq b + 32 KS bytes at
+ *     code[g * q_stride + qchunk_off[c] + sum of the chunk's earlier tiles' bytes]:
+ *   K: 16 rows of mq codes, code (position i, coordinate j) at bit b (i mq + j);
+ *   V: mq rows of 16 codes, code (coordinate j, position i) at bit b (16 j + i);
+ * then the KS x 16 binary16 scales of the tile, scale (group s, position i) at entry
+ * 16 s + i.  Codes are two's complement b-bit fields packed from bit 0 of the tile upward;
+ * codes past a position's rank, and of absent positions, are 0.                           */
+typedef struct varrate_qcache {
+    void*     code_k;      /* [G][q_stride] bytes                                           */
+    void*     code_v;      /* [G][q_stride] bytes                                           */
+    uint32_t* qchunk_off;  /* [n_chunks + 1] byte offset of each chunk in a head stream     */
+    int64_t   q_stride;    /* bytes per head stream, a multiple of 16, >= varrate_qcache_bytes */
+    int32_t   bits;        /* b: 3, 4 or 8                                                  */
+    int32_t   reserved;
+} varrate_qcache;
+
+/* Bytes per head stream (q_stride) and of qchunk_off for b-bit codes of this shape's layer. */
+VARRATE_API int varrate_qcache_bytes(const varrate_shape* shape, int32_t bits, int64_t* q_stride,
+                         size_t* qchunk_off_bytes);
+
+/* Quantises the coefficients of `cache` (filled by varrate_compress or varrate_project;
+ * bf16 layers only) into `q` (q->bits, q->q_stride and the buffers set by the caller).
+ * Two launches: the chunk offsets, then the codes and scales.  EINVAL for a bad q;
+ * EUNSUPPORTED for fp32 layers or bits not in {3, 4, 8}.                                     */
+VARRATE_API int varrate_quantize(const varrate_shape* shape, const varrate_cache* cache, varrate_qcache* q,
+                     void* stream);
+
+/* varrate_decode_attn over quantised coefficients: caches[s] supplies the storage order,
+ * ranks and exact rows, qcaches[s] the codes of the same layer (all with the same bits
+ * and q_stride).  Each coded token's score is sum over its groups of sc_K (q' . k) and its
+ * value sum sc_V k, i.e. the reconstruct-in-place attention of Eq. (6) over the dequantised
+ * coefficients.  Workspace as for varrate_decode_attn.                                      */
+VARRATE_API int varrate_decode_attn_q(const varrate_shape* shape, const varrate_cache* caches,
+                          const varrate_qcache* qcaches, int32_t S, const void* q, int32_t Q,
+                          const float* P_K, const float* P_V, void* out, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc): varrate_decode_attn without a workspace.
  * The partial records go to a fixed device array of VARRATE_DECODE_SCRATCH_BYTES that the

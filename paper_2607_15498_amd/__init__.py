@@ -20,7 +20,8 @@ from . import _lib
 from ._lib import CHUNK, COEF_PAD, HEAD_DIM  # noqa: F401
 
 __all__ = ["VarRateError", "Shape", "Cache", "new_cache", "coded_budget", "salience", "allocate",
-           "project", "compress", "append_exact", "decode", "decode_noalloc", "library"]
+           "project", "compress", "append_exact", "decode", "decode_noalloc", "QCache", "new_qcache",
+           "quantize", "decode_q", "library"]
 
 
 class VarRateError(RuntimeError):
@@ -263,4 +264,57 @@ def decode_noalloc(shape: Shape, caches: Sequence[Cache], q: torch.Tensor, PK, P
                                                  _dev_ptr(PK, torch.float32, "PK"),
                                                  _dev_ptr(PV, torch.float32, "PV"),
                                                  _dev_ptr(out, shape.torch_dtype, "out"), _stream()))
+    return out[0] if single else out
+
+
+@dataclasses.dataclass
+class QCache:
+    """b-bit codes of one compressed bf16 layer (Sec. 3.3 "Composability")."""
+    code_k: torch.Tensor      # [G][q_stride] uint8
+    code_v: torch.Tensor
+    qchunk_off: torch.Tensor  # [n_chunks + 1] int32 (byte offsets)
+    q_stride: int
+    bits: int
+
+    def c(self) -> _lib.QCacheC:
+        return _lib.QCacheC(self.code_k.data_ptr(), self.code_v.data_ptr(), self.qchunk_off.data_ptr(),
+                            self.q_stride, self.bits, 0)
+
+
+def new_qcache(shape: Shape, bits: int, device="cuda") -> QCache:
+    qs, qo = ctypes.c_int64(), ctypes.c_size_t()
+    _check(library().varrate_qcache_bytes(ctypes.byref(shape.c()), int(bits), ctypes.byref(qs), ctypes.byref(qo)))
+    return QCache(code_k=torch.zeros((shape.G, qs.value), dtype=torch.uint8, device=device),
+                  code_v=torch.zeros((shape.G, qs.value), dtype=torch.uint8, device=device),
+                  qchunk_off=torch.zeros(qo.value // 4, dtype=torch.int32, device=device),
+                  q_stride=int(qs.value), bits=int(bits))
+
+
+def quantize(shape: Shape, cache: Cache, bits: int, qcache: Optional[QCache] = None) -> QCache:
+    """Group-wise b-bit codes of a compressed bf16 layer's coefficients."""
+    if qcache is None:
+        qcache = new_qcache(shape, bits, cache.coef_k.device)
+    cc, qc = cache.c(), qcache.c()
+    _check(library().varrate_quantize(ctypes.byref(shape.c()), ctypes.byref(cc), ctypes.byref(qc), _stream()))
+    return qcache
+
+
+def decode_q(shape: Shape, caches: Sequence[Cache], qcaches: Sequence[QCache], q: torch.Tensor, PK, PV,
+             out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Rank-space decode over quantised coefficients (q: [S][Q][H][d] or [Q][H][d])."""
+    single = q.dim() == 3
+    if single:
+        q = q.unsqueeze(0)
+    S, Q = int(q.shape[0]), int(q.shape[1])
+    if len(caches) != S or len(qcaches) != S:
+        raise VarRateError(_lib.VARRATE_EINVAL, f"{len(caches)} caches / {len(qcaches)} qcaches for {S} query sets")
+    if out is None:
+        out = torch.empty_like(q)
+    arr = (_lib.CacheC * S)(*[c.c() for c in caches])
+    qarr = (_lib.QCacheC * S)(*[c.c() for c in qcaches])
+    ws = workspace if workspace is not None else decode_workspace(shape, S, Q, q.device)
+    _check(library().varrate_decode_attn_q(ctypes.byref(shape.c()), arr, qarr, S, _dev_ptr(q, shape.torch_dtype, "q"),
+                                           Q, _dev_ptr(PK, torch.float32, "PK"), _dev_ptr(PV, torch.float32, "PV"),
+                                           _dev_ptr(out, shape.torch_dtype, "out"), ws.data_ptr(), ws.numel(),
+                                           _stream()))
     return out[0] if single else out

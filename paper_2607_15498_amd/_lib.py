@@ -21,7 +21,7 @@ EXPORTS = (
     "varrate_cache_bytes", "varrate_compress_workspace_bytes", "varrate_decode_workspace_bytes",
     "varrate_salience", "varrate_allocate", "varrate_project", "varrate_compress",
     "varrate_append_exact", "varrate_decode_attn", "varrate_decode_scratch_need",
-    "varrate_decode_attn_noalloc",
+    "varrate_decode_attn_noalloc", "varrate_qcache_bytes", "varrate_quantize", "varrate_decode_attn_q",
 )
 DECODE_SCRATCH_BYTES = 8 << 20
 
@@ -38,6 +38,11 @@ class CacheC(ctypes.Structure):
                 ("k_exact", ctypes.c_void_p), ("v_exact", ctypes.c_void_p),
                 ("coef_stride", ctypes.c_int64), ("cap", ctypes.c_int64), ("n_exact", ctypes.c_int64),
                 ("N", ctypes.c_int64), ("B", ctypes.c_int64)]
+
+
+class QCacheC(ctypes.Structure):
+    _fields_ = [("code_k", ctypes.c_void_p), ("code_v", ctypes.c_void_p), ("qchunk_off", ctypes.c_void_p),
+                ("q_stride", ctypes.c_int64), ("bits", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class CacheBytes(ctypes.Structure):
@@ -76,6 +81,10 @@ def load() -> ctypes.CDLL:
         "varrate_decode_attn": (ctypes.c_int, [P(Shape), P(CacheC), i32, vp, i32, vp, vp, vp, vp, sz, vp]),
         "varrate_decode_scratch_need": (sz, [P(Shape), i32, i32]),
         "varrate_decode_attn_noalloc": (ctypes.c_int, [P(Shape), P(CacheC), i32, vp, i32, vp, vp, vp, vp]),
+        "varrate_qcache_bytes": (ctypes.c_int, [P(Shape), i32, P(i64), P(sz)]),
+        "varrate_quantize": (ctypes.c_int, [P(Shape), P(CacheC), P(QCacheC), vp]),
+        "varrate_decode_attn_q": (ctypes.c_int, [P(Shape), P(CacheC), P(QCacheC), i32, vp, i32, vp, vp, vp, vp,
+                                                 sz, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)

@@ -287,6 +287,56 @@ int varrate_decode_attn(const varrate_shape* sh, const varrate_cache* caches, in
                       "decode launch");
 }
 
+int varrate_qcache_bytes(const varrate_shape* sh, int32_t bits, int64_t* q_stride, size_t* qchunk_off_bytes) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if (bits != 3 && bits != 4 && bits != 8) return fail(VARRATE_EUNSUPPORTED, "bits=%d not in {3, 4, 8}", bits);
+    if (!q_stride || !qchunk_off_bytes) return fail(VARRATE_EINVAL, "outputs must be non-NULL");
+    const int64_t N = sh->n - sh->w;
+    *q_stride = (int64_t)qcache_stride(*sh, bits);
+    *qchunk_off_bytes = (size_t)((N + VARRATE_CHUNK - 1) / VARRATE_CHUNK + 1) * 4;
+    return VARRATE_OK;
+}
+
+static int check_qcache(const varrate_shape* sh, const varrate_qcache* q) {
+    if (!q) return fail(VARRATE_EINVAL, "qcache is NULL");
+    if (sh->dtype != VARRATE_BF16) return fail(VARRATE_EUNSUPPORTED, "quantised coefficients need a bf16 layer");
+    if (q->bits != 3 && q->bits != 4 && q->bits != 8)
+        return fail(VARRATE_EUNSUPPORTED, "bits=%d not in {3, 4, 8}", q->bits);
+    if (!q->code_k || !q->code_v || !q->qchunk_off) return fail(VARRATE_EINVAL, "qcache has a NULL buffer");
+    if (!aligned16(q->code_k) || !aligned16(q->code_v)) return fail(VARRATE_EINVAL, "code buffers must be 16-byte aligned");
+    const int64_t need = (int64_t)qcache_stride(*sh, q->bits);
+    if (q->q_stride < need || (q->q_stride % 16) != 0)
+        return fail(VARRATE_EINVAL, "q_stride=%lld must be a multiple of 16 and >= %lld", (long long)q->q_stride,
+                    (long long)need);
+    return VARRATE_OK;
+}
+
+int varrate_quantize(const varrate_shape* sh, const varrate_cache* c, varrate_qcache* q, void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if ((rc = check_cache(sh, c, true))) return rc;
+    if ((rc = check_qcache(sh, q))) return rc;
+    return hip_status(launch_quantize(*sh, *c, *q, (hipStream_t)stream), "quantize launch");
+}
+
+int varrate_decode_attn_q(const varrate_shape* sh, const varrate_cache* caches, const varrate_qcache* qcaches,
+                          int32_t S, const void* q, int32_t Q, const float* PK, const float* PV, void* out,
+                          void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_decode(sh, caches, S, q, Q, PK, PV, out);
+    if (rc) return rc;
+    if (!qcaches) return fail(VARRATE_EINVAL, "qcaches is NULL");
+    for (int s = 0; s < S; ++s) {
+        if ((rc = check_qcache(sh, &qcaches[s]))) return rc;
+        if (qcaches[s].bits != qcaches[0].bits || qcaches[s].q_stride != qcaches[0].q_stride)
+            return fail(VARRATE_EINVAL, "qcaches must share bits and q_stride");
+    }
+    if ((rc = ws_check(ws, ws_bytes, decode_ws_bytes(*sh, S, Q)))) return rc;
+    return hip_status(launch_decode(*sh, caches, S, q, Q, PK, PV, out, (uint8_t*)ws, (hipStream_t)stream, false,
+                                    qcaches),
+                      "decode launch");
+}
+
 size_t varrate_decode_scratch_need(const varrate_shape* sh, int32_t S, int32_t Q) {
     if (check_shape(sh) || S < 1 || S > VARRATE_MAX_SEQS || Q < 1 ||
         (int64_t)Q * (sh->H / sh->G) > VARRATE_MAX_QROWS)

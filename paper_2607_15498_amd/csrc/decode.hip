@@ -108,6 +108,8 @@ struct DecSmem {
     uint32_t* cb;     // [DC_MAX_CPW] chunk bases (chunk_off)
     u32x4* kmask;     // [9] bf16 masks keeping the first nv elements of an 8-element row piece
     uint16_t* to;     // [cpw][DC_TO] element offset of tile h inside its chunk, h = 0..16
+    uint8_t* mq;      // [cpw][DC_TO] quantised layout: tile h's coordinate count (its rank
+                      //   rounded up to a multiple of 8)
 };
 
 __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
@@ -126,12 +128,14 @@ __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
     s.cb = reinterpret_cast<uint32_t*>(f); f += DC_MAX_CPW;
     s.kmask = reinterpret_cast<u32x4*>(f); f += 9 * 4;
     s.to = reinterpret_cast<uint16_t*>(f);
+    s.mq = reinterpret_cast<uint8_t*>(s.to + DC_MAX_CPW * DC_TO);
     return s;
 }
 
 static inline size_t decode_smem_bytes(int cpw) {
     return 4 * (size_t)(DC_STAGE_BYTES + DC_STAGE_PAD) + 4 * 2 * 64 * 16 +
-           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW + 9 * 4) * 4 + (size_t)cpw * DC_TO * 2;
+           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW + 9 * 4) * 4 + (size_t)DC_MAX_CPW * DC_TO * 2 +
+           (size_t)cpw * DC_TO;
 }
 
 // 8 consecutive bf16 at element index a of an LDS array (any 2-byte alignment): five dword
@@ -347,8 +351,142 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
     }
 }
 
-template <bool F32>
-__global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecParams p) {
+// ----------------------------------------------------------------------------------------
+// Quantised coefficients (group-wise b-bit codes, Sec. 3.3 "Composability").  A coded tile
+// of size m is stored with mq = m rounded up to a multiple of 8 coordinates and KS =
+// ceil(m / 32) groups per position: K codes (16 rows of mq codes), then K scales ([KS][16]
+// binary16), in the K stream; V codes (mq rows of 16 positions), then V scales, in the V
+// stream.  Codes are two's complement b-bit fields packed from bit 0 upward; code k of a
+// group with scale sc stands for k * sc.  Tile size in 2-byte units:
+template <int QB> __host__ __device__ constexpr uint32_t q_tile_units(uint32_t m) {
+    return m == 0 ? 0u : ((m + 7u) & ~7u) * (uint32_t)QB + 16u * ((m + 31u) / 32u);
+}
+// signed b-bit field e of a word
+template <int QB> __device__ __forceinline__ float code_f(uint32_t w, int e) {
+    return (float)((int32_t)(w << (32 - QB - QB * e)) >> (32 - QB));
+}
+__device__ __forceinline__ float half_f(uint32_t w, int hi) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)(hi ? w >> 16 : w));
+}
+
+// Value products whose B operand differs per 32-coordinate group: block b (coordinates
+// 16 b ..) uses ph[b / 2] (the softmax weights scaled by the positions' V scales of that group).
+template <int NB> __device__ __forceinline__ void acc_mfma_q(const u32x2* vh, const u32x2* ph);
+template <> __device__ __forceinline__ void acc_mfma_q<1>(const u32x2* vh, const u32x2* ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %1, a[0:3]\n\t" :: "v"(vh[0]), "v"(ph[0]) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_q<2>(const u32x2* vh, const u32x2* ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %2, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %2, a[4:7]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(ph[0]) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_q<4>(const u32x2* vh, const u32x2* ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %4, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %4, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %5, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %5, a[12:15]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(ph[0]), "v"(ph[1]) : ACC_AGPRS);
+}
+template <> __device__ __forceinline__ void acc_mfma_q<8>(const u32x2* vh, const u32x2* ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[0:3], %0, %8, a[0:3]\n\t" "v_mfma_f32_16x16x16_bf16 a[4:7], %1, %8, a[4:7]\n\t" "v_mfma_f32_16x16x16_bf16 a[8:11], %2, %9, a[8:11]\n\t" "v_mfma_f32_16x16x16_bf16 a[12:15], %3, %9, a[12:15]\n\t" "v_mfma_f32_16x16x16_bf16 a[16:19], %4, %10, a[16:19]\n\t" "v_mfma_f32_16x16x16_bf16 a[20:23], %5, %10, a[20:23]\n\t" "v_mfma_f32_16x16x16_bf16 a[24:27], %6, %11, a[24:27]\n\t" "v_mfma_f32_16x16x16_bf16 a[28:31], %7, %11, a[28:31]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(vh[4]), "v"(vh[5]), "v"(vh[6]), "v"(vh[7]), "v"(ph[0]), "v"(ph[1]), "v"(ph[2]), "v"(ph[3]) : ACC_AGPRS);
+}
+
+// One quantised coded tile (tm.base in 2-byte units of the stage, tm.m = mq).  Scores: the
+// MFMA takes the integer codes (exact in bf16) against the query fragments, one K group
+// (32 coordinates) per step, and each step's result is scaled by the K scales of the four
+// tokens a lane holds.  Values: the codes are the A operand as they are, and the scale of
+// each token's V group goes into the B operand (softmax weight x scale, one bf16 rounding).
+template <int QB, int KS, int NB>
+__device__ __forceinline__ void tile_step_q(const TileMeta& tm, bool partial, const uint16_t* sK,
+                                            const uint16_t* sV, const u32x4* qf, int lane, int grp,
+                                            float& m_run, float& l_part) {
+    const int col = lane & 15;
+    const int mq = tm.m;
+    const uint32_t* wk = reinterpret_cast<const uint32_t*>(sK + tm.base);   // 16-byte aligned
+    const uint32_t* wv = reinterpret_cast<const uint32_t*>(sV + tm.base);
+    const int sco = mq * QB;                        // scales after the codes, 2-byte units
+    // ---- scores
+    f32x4 sc = {0, 0, 0, 0};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const int c0 = 32 * s + 8 * grp;
+        const uint32_t bit = (uint32_t)(QB * (col * mq + (c0 < mq ? c0 : 0)));
+        u32x4 kh;
+        if constexpr (QB == 8) {
+            const uint32_t x0 = wk[bit >> 5], x1 = wk[(bit >> 5) + 1];
+            kh = u32x4{cvt_bf16x2(code_f<8>(x0, 0), code_f<8>(x0, 1)), cvt_bf16x2(code_f<8>(x0, 2), code_f<8>(x0, 3)),
+                       cvt_bf16x2(code_f<8>(x1, 0), code_f<8>(x1, 1)), cvt_bf16x2(code_f<8>(x1, 2), code_f<8>(x1, 3))};
+        } else {
+            uint32_t x = wk[bit >> 5];
+            if constexpr (QB == 3) x = __builtin_amdgcn_alignbit(wk[(bit >> 5) + 1], x, bit & 31);
+            kh = u32x4{cvt_bf16x2(code_f<QB>(x, 0), code_f<QB>(x, 1)), cvt_bf16x2(code_f<QB>(x, 2), code_f<QB>(x, 3)),
+                       cvt_bf16x2(code_f<QB>(x, 4), code_f<QB>(x, 5)), cvt_bf16x2(code_f<QB>(x, 6), code_f<QB>(x, 7))};
+        }
+        const uint32_t keep = c0 < mq ? 0xFFFFFFFFu : 0u;
+        kh = kh & keep;
+        const u32x4 qh = qf[(s * 2) * 64 + lane], ql = qf[(s * 2 + 1) * 64 + lane];
+        f32x4 t = {0, 0, 0, 0};
+        t = mfma(kh, qh, t);
+        t = mfma(kh, ql, t);
+        // K scales of tokens 4 grp .. 4 grp + 3 in group s (groups past the tile's: none)
+        u32x2 ks = *reinterpret_cast<const u32x2*>(sK + tm.base + sco + 16 * (32 * s < mq ? s : 0) + 4 * grp);
+        ks = 32 * s < mq ? ks : u32x2{0, 0};
+        sc[0] += t[0] * half_f(ks[0], 0);
+        sc[1] += t[1] * half_f(ks[0], 1);
+        sc[2] += t[2] * half_f(ks[1], 0);
+        sc[3] += t[3] * half_f(ks[1], 1);
+    }
+    float sv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sv[v] = sc[v];
+    if (partial) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sv[v] = tm.i0 + 4 * grp + v < tm.T ? sv[v] : -INFINITY;
+    }
+    float tmax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    tmax = xmax32(xmax16(tmax));
+    const bool jump = tmax > m_run + 8.f;
+    if (__builtin_amdgcn_ballot_w64(jump) != 0) {
+        const float m_new = jump ? tmax : m_run;
+        const float alpha = fast_exp(m_run - m_new);
+        l_part *= alpha;
+        acc_scale(alpha);
+        m_run = m_new;
+    }
+    float pv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        pv[v] = fast_exp(sv[v] - m_run);
+        l_part += pv[v];
+    }
+    // the value codes are read only now, so they are not live across the score steps
+    __builtin_amdgcn_sched_barrier(0);
+    // ---- value operands: coordinate j = 16 b + col, positions 4 grp .. 4 grp + 3
+    u32x2 vh[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        const int j = 16 * b + col;
+        // coordinates past the tile read its first row (in bounds) and are masked
+        const uint32_t bit = (uint32_t)(QB * (16 * (j < mq ? j : 0) + 4 * grp));
+        const uint32_t d0 = wv[bit >> 5];
+        uint32_t x;
+        if constexpr (QB == 3) x = __builtin_amdgcn_alignbit(wv[(bit >> 5) + 1], d0, bit & 31);
+        else x = d0 >> (bit & 31);
+        x = j < mq ? x : 0u;
+        vh[b] = u32x2{cvt_bf16x2(code_f<QB>(x, 0), code_f<QB>(x, 1)), cvt_bf16x2(code_f<QB>(x, 2), code_f<QB>(x, 3))};
+    }
+    // B operands: weights x the V scales of the same tokens, per group of 32 coordinates
+    constexpr int NG = (NB + 1) / 2;
+    u32x2 ph[NG];
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+        u32x2 vs = *reinterpret_cast<const u32x2*>(sV + tm.base + sco + 16 * (32 * s < mq ? s : 0) + 4 * grp);
+        vs = 32 * s < mq ? vs : u32x2{0, 0};
+        ph[s] = u32x2{cvt_bf16x2(pv[0] * half_f(vs[0], 0), pv[1] * half_f(vs[0], 1)),
+                      cvt_bf16x2(pv[2] * half_f(vs[1], 0), pv[3] * half_f(vs[1], 1))};
+    }
+    acc_mfma_q<NB>(vh, ph);
+}
+
+// QB = 0: coefficients stored in the layer's dtype; QB = 3, 4, 8: b-bit codes with binary16
+// group scales (bf16 layers only).
+template <bool F32, int QB>
+__global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel(DecParams p) {
+    static_assert(QB == 0 || !F32, "quantised coefficients come from bf16 layers");
     typedef typename Elem<F32>::T ET;
     constexpr int EPU = 16 / (int)sizeof(ET);               // elements per 16-byte unit
     constexpr int SE = DC_STAGE_BYTES / (int)sizeof(ET);     // staged elements per stream
@@ -415,6 +553,7 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
     const bool r_ok = !exact && tid < ncl * (CHUNK / 16);
     if (r_ok && t_r < p.N) rv = load16(S.srank + t_r);     // srank is padded to a multiple of 64
     if (!exact && tid < ncl) cbv = S.chunk_off[c_lo + tid];
+    if constexpr (QB != 0) cbv >>= 1;       // quantised chunk bases are in bytes
 
     lane = lane_now(); tid = 64 * wave + lane; grp = lane >> 4; col = lane & 15;
     // ---- 1c. offsets of the stored slots inside each chunk: local prefix sums of a
@@ -426,8 +565,10 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
         const int64_t t0 = (int64_t)(c_lo + cc) * CHUNK;
         const int T = (int)((p.N - t0) < CHUNK ? (p.N - t0) : CHUNK);
         const uint32_t mk = 16 * k < T ? (rv[0] & 0xFFu) : 0u;
-        const uint32_t incl = row_scan16(16u * mk);
-        sm.to[cc * DC_TO + k] = (uint16_t)(incl - 16u * mk);
+        const uint32_t units = QB ? q_tile_units<QB>(mk) : 16u * mk;
+        const uint32_t incl = row_scan16(units);
+        sm.to[cc * DC_TO + k] = (uint16_t)(incl - units);
+        if constexpr (QB != 0) sm.mq[cc * DC_TO + k] = (uint8_t)((mk + 7u) & ~7u);
         if (k == 15) { sm.to[cc * DC_TO + 16] = (uint16_t)incl; sm.cT[cc] = T; }
     }
     if (!exact && tid < ncl) sm.cb[tid] = cbv;
@@ -610,14 +751,24 @@ __global__ __launch_bounds__(DC_THREADS, F32 ? 2 : 4) void decode_kernel(DecPara
                 tm.i0 = (tile & 15) * 16;
                 tm.T = __builtin_amdgcn_readfirstlane(sm.cT[cc]);
                 const uint16_t* to = sm.to + cc * DC_TO + (tile & 15);
-                tm.m = __builtin_amdgcn_readfirstlane(((int)to[1] - (int)to[0]) >> 4);
+                if constexpr (QB != 0) tm.m = __builtin_amdgcn_readfirstlane((int)sm.mq[cc * DC_TO + (tile & 15)]);
+                else tm.m = __builtin_amdgcn_readfirstlane(((int)to[1] - (int)to[0]) >> 4);
                 // a tile's size bounds its 32-coefficient score steps and 16-wide value
                 // blocks, as compile-time bounds (no branches inside)
                 const bool partial = __builtin_amdgcn_readfirstlane(tm.i0 + 16 > tm.T ? 1 : 0) != 0;
-                if (tm.m <= 16) tile_step<F32, false, 1, 1>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
-                else if (tm.m <= 32) tile_step<F32, false, 1, 2>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
-                else if (tm.m <= 64) tile_step<F32, false, 2, 4>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
-                else tile_step<F32, false, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                if constexpr (QB != 0) {
+                    const uint16_t* qK = reinterpret_cast<const uint16_t*>(sK);
+                    const uint16_t* qV = reinterpret_cast<const uint16_t*>(sV);
+                    if (tm.m <= 16) tile_step_q<QB, 1, 1>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                    else if (tm.m <= 32) tile_step_q<QB, 1, 2>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                    else if (tm.m <= 64) tile_step_q<QB, 2, 4>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                    else tile_step_q<QB, 4, 8>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                } else {
+                    if (tm.m <= 16) tile_step<F32, false, 1, 1>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                    else if (tm.m <= 32) tile_step<F32, false, 1, 2>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                    else if (tm.m <= 64) tile_step<F32, false, 2, 4>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                    else tile_step<F32, false, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                }
             }
         }
         if (tbnd >= t_end) break;
@@ -867,8 +1018,16 @@ size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
 
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
                          int Q, const float* PK, const float* PV, void* out, uint8_t* ws,
-                         hipStream_t st, bool reuse_group_region) {
+                         hipStream_t st, bool reuse_group_region, const varrate_qcache* qcaches) {
     DecPlan pl = plan_decode(sh, S, Q);
+    const int qb = qcaches ? qcaches[0].bits : 0;
+    if (qb != 0 && qb != 3 && qb != 4 && qb != 8) return hipErrorInvalidValue;
+    if (qb != 0 && sh.dtype != VARRATE_BF16) return hipErrorInvalidValue;
+    const void* kfn = sh.dtype != VARRATE_BF16 ? (const void*)decode_kernel<true, 0>
+                      : qb == 3 ? (const void*)decode_kernel<false, 3>
+                      : qb == 4 ? (const void*)decode_kernel<false, 4>
+                      : qb == 8 ? (const void*)decode_kernel<false, 8>
+                                : (const void*)decode_kernel<false, 0>;
     const int hpg = sh.H / sh.G;
     const int rows_total = Q * hpg;
     const size_t units_all = (size_t)S * sh.G * pl.nqt;
@@ -878,15 +1037,18 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
     const size_t lds = decode_smem_bytes(pl.cpw);
-    hipError_t e = sh.dtype == VARRATE_BF16 ? ensure_lds_limit((const void*)decode_kernel<false>, lds)
-                                             : ensure_lds_limit((const void*)decode_kernel<true>, lds);
+    hipError_t e = ensure_lds_limit(kfn, lds);
     if (e != hipSuccess) return e;
     for (int s0 = 0; s0 < S; s0 += DC_SEQ) {
         const int ns = S - s0 < DC_SEQ ? S - s0 : DC_SEQ;
         DecParams prm;
         for (int i = 0; i < ns; ++i) {
             const varrate_cache& c = caches[s0 + i];
-            prm.seq[i] = DecSeq{c.coef_k, c.coef_v, c.srank, c.chunk_off, c.k_exact, c.v_exact,
+            // quantised: the code streams and their (byte) chunk bases replace the coefficients
+            const void* ck = qb ? qcaches[s0 + i].code_k : c.coef_k;
+            const void* cv = qb ? qcaches[s0 + i].code_v : c.coef_v;
+            const uint32_t* co = qb ? qcaches[s0 + i].qchunk_off : c.chunk_off;
+            prm.seq[i] = DecSeq{ck, cv, c.srank, co, c.k_exact, c.v_exact,
                                 (const uint8_t*)q + (s0 + i) * qstride, (uint8_t*)out + (s0 + i) * qstride,
                                 c.n_exact};
         }
@@ -897,7 +1059,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         // go to the start of the buffer (the previous group's merge has finished reading them)
         prm.part = reuse_group_region ? part : part + (size_t)s0 * sh.G * pl.nqt * (pl.n_wg + 1) * DC_REC;
         prm.N = sh.n - sh.w;
-        prm.coef_stride = caches[s0].coef_stride;
+        prm.coef_stride = qb ? qcaches[s0].q_stride / 2 : caches[s0].coef_stride;   // 2-byte units
         prm.cap = caches[s0].cap;
         prm.G = sh.G;
         prm.H = sh.H;
@@ -911,8 +1073,11 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         prm.total_tiles = pl.total_tiles;
         prm.units = ns * sh.G * pl.nqt;
         const unsigned nblk = (unsigned)(prm.units * (pl.n_wg + 1));
-        if (sh.dtype == VARRATE_BF16) decode_kernel<false><<<nblk, DC_THREADS, lds, st>>>(prm);
-        else decode_kernel<true><<<nblk, DC_THREADS, lds, st>>>(prm);
+        if (sh.dtype != VARRATE_BF16) decode_kernel<true, 0><<<nblk, DC_THREADS, lds, st>>>(prm);
+        else if (qb == 3) decode_kernel<false, 3><<<nblk, DC_THREADS, lds, st>>>(prm);
+        else if (qb == 4) decode_kernel<false, 4><<<nblk, DC_THREADS, lds, st>>>(prm);
+        else if (qb == 8) decode_kernel<false, 8><<<nblk, DC_THREADS, lds, st>>>(prm);
+        else decode_kernel<false, 0><<<nblk, DC_THREADS, lds, st>>>(prm);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         MergeParams mp;

@@ -39,9 +39,13 @@ hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V,
                           const float* PV, varrate_cache& c, hipStream_t st);
 // reuse_group_region: every launch group (DC_SEQ sequences) writes its partial records to the
 // start of `ws` instead of a region of its own (the no-allocation entry point)
+// qcaches non-NULL: the coefficients are the quantised codes of qcaches[s] (same bits)
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
                          int Q, const float* PK, const float* PV, void* out, uint8_t* ws,
-                         hipStream_t st, bool reuse_group_region = false);
+                         hipStream_t st, bool reuse_group_region = false,
+                         const varrate_qcache* qcaches = nullptr);
+size_t qcache_stride(const varrate_shape& sh, int bits);
+hipError_t launch_quantize(const varrate_shape& sh, const varrate_cache& c, varrate_qcache& q, hipStream_t st);
 // bytes of partial records one launch group needs (what the fixed scratch must hold)
 size_t decode_group_bytes(const varrate_shape& sh, int S, int Q);
 // this device's address of the fixed decode scratch array (looked up once per device)

@@ -117,7 +117,7 @@ def test_status_strings(L):
 def test_decode_accumulator_agprs_are_private():
     """The decode kernel keeps its value-product accumulators in AGPRs a0..a31 named by inline
     asm.  That is only sound if the compiler itself never places a value in an AGPR: check
-    the generated gfx950 code of both decode kernels (outside the inline asm blocks) for any
+    the generated gfx950 code of every decode kernel (outside the inline asm blocks) for any
     AGPR operand, and that every kernel that uses AGPRs declares exactly the 32."""
     import shutil
     import subprocess
@@ -134,8 +134,8 @@ def test_decode_accumulator_agprs_are_private():
         assert r.returncode == 0, r.stdout[-2000:]
         text = open(out).read()
     agpr = re.compile(r"\ba\d+\b|\ba\[\d+:\d+\]|v_accvgpr")
-    kernels = re.findall(r"^(_ZN2vr13decode_kernelILb[01]EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm", text, re.S | re.M)
-    assert len(kernels) == 2
+    kernels = re.findall(r"^(_ZN2vr13decode_kernelILb[01]ELi\d+EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm", text, re.S | re.M)
+    assert len(kernels) == 5          # fp32, bf16, and bf16 with 3-, 4- and 8-bit codes
     for name, body in kernels:
         inside = False
         for line in body.splitlines():
