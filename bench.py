@@ -65,6 +65,24 @@ def decode_bytes(shape, cache, n_queries=1):
     return coef + exact + meta + bases + qo
 
 
+def decode_bytes_q(shape, cache, bits, rank, n_queries=1):
+    """Algorithmic bytes of a decode over b-bit codes: the codes of every coefficient, one
+    binary16 scale per 32-coordinate group, plus what decode_bytes counts besides the
+    coefficients (exact slots, ranks and chunk offsets, bases, queries and outputs)."""
+    es = 2
+    groups = int(((rank.astype(np.int64) + 31) // 32).sum())
+    codes = 2 * shape.G * (cache.B * bits // 8 + 2 * groups)
+    return decode_bytes(shape, cache, n_queries) - 2 * shape.G * cache.B * es + codes
+
+
+def footprint_pct(shape, cache, coef_bytes):
+    """Stored bytes of the compressed layer (coefficients or codes + scales, exact rows,
+    ranks) as a percentage of the full bf16 K/V cache."""
+    full = 2 * shape.n * shape.G * 128 * 2
+    exact = 2 * shape.G * shape.w * 128 * 2
+    return 100.0 * (coef_bytes + exact + cache.N) / full
+
+
 def compress_bytes(shape, cache):
     """Minimum bytes of one compress: K and V read once, window queries and bases read,
     packed coefficients, ranks, layout tables and exact rows written."""
@@ -345,12 +363,45 @@ def main():
                      "unit": "GB/s", "frac": round(dbytes / (ms_dec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": decode_traffic(), "bytes_per_launch": int(dbytes)},
     }
+    # quantised coefficients (Sec. 3.3 "Composability"): every slot quantised, then decodes
+    # over the codes timed like the plain decode (24 slots per replay, medians)
+    rank_host = slots[0].rank.cpu().numpy()
+    qrows = {}
+    for bits in (4, 3):
+        qslots = [vr.quantize(shape, c, bits) for c in slots]
+        torch.cuda.synchronize()
+        gq, gz = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gq, stream=cap_stream):
+            for i in range(N_CACHE_SLOTS):
+                j = (i + N_CACHE_SLOTS // 2) % N_CACHE_SLOTS
+                vr.decode_q(shape, [slots[j]], [qslots[j]], q, PK, PV, out=out, workspace=ws_d)
+        with torch.cuda.graph(gz, stream=cap_stream):
+            for i in range(N_CACHE_SLOTS):
+                vr.quantize(shape, slots[i], bits, qslots[i])
+        torch.cuda.synchronize()
+        stq = _replay_stats(gq, 8, N_CACHE_SLOTS)
+        stz = _replay_stats(gz, 4, N_CACHE_SLOTS)
+        qbytes = decode_bytes_q(shape, slots[0], bits, rank_host)
+        coefq = 2 * shape.G * (slots[0].B * bits // 8 + 2 * int(((rank_host.astype(np.int64) + 31) // 32).sum()))
+        qrows[f"{bits}bit"] = {
+            "decode_ms": round(stq["p50"], 4), "decode_ms_p10_p90": [round(stq["p10"], 4), round(stq["p90"], 4)],
+            "decode_GBps": round(qbytes / (stq["p50"] * 1e-3) / 1e9, 2),
+            "frac": round(qbytes / (stq["p50"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "decode_bytes": int(qbytes),
+            "quantize_ms": round(stz["p50"], 4),
+            "footprint_pct_of_full_kv": round(footprint_pct(shape, slots[0], coefq), 2),
+        }
+        del gq, gz, qslots
+    result["quantized_coefficients"] = dict(
+        qrows, footprint_pct_bf16_coefficients=round(footprint_pct(shape, slots[0], 2 * shape.G * slots[0].B * 2), 2),
+        note="group-wise symmetric codes, 32-coordinate groups, binary16 scales; decode_bytes counts "
+             "codes + scales + exact rows + metadata + bases; same 32K layer and batch 1")
     if not args.no_stack:
         # the 128K end of the 32K-128K target range: the 32-layer Llama stack, decode at batch 1
         del graphs, step_graphs, slots, Ks, Vs, sbars
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
-        stk = bench_stack(args, "llama_128k_stack", emit=False)
+        stk = bench_stack(args, "llama_128k_stack", emit=False, quant_bits=4)
         result["llama_128k_stack"] = {
             "workload": stk["config"]["workload"],
             "decode_GBps": stk["value"], "pct_hbm_peak": stk["pct_hbm_peak"],
@@ -361,6 +412,7 @@ def main():
             "decode_bytes_per_step": stk["decode_bytes_per_step"],
             "compress_ms_per_32k_tokens": stk["compress_ms_per_32k_tokens"],
             "compress_ms_per_32k_tokens_all_layers": stk["compress_ms_per_32k_tokens_all_layers"],
+            "decode_4bit": stk["decode_4bit"],
         }
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, li, dbytes, {"decode_ms": ms_dec, "compress_ms": ms_comp})
@@ -395,7 +447,7 @@ def _pct(st, nd=4):
     return {k: (round(v, nd) if isinstance(v, float) else v) for k, v in st.items()}
 
 
-def bench_stack(args, config=None, emit=True):
+def bench_stack(args, config=None, emit=True, quant_bits=None):
     """Whole model stack: every layer (and sequence) drawn on the device, compressed, then
     decode steps of one query per sequence over all layers (one decode call per layer, the
     batch's caches in that call).  Compress and decode are timed from captured graphs.  The
@@ -499,6 +551,24 @@ def bench_stack(args, config=None, emit=True):
         "compress_ms_total": round(ms_comp, 3),
         "draw_s": round(t_draw, 1),
     }
+    if quant_bits:
+        # every layer's coefficients quantised to b-bit codes, then the same decode step over them
+        qcs = [[vr.quantize(shape, c, quant_bits) for c in row] for row in caches]
+        torch.cuda.synchronize()
+        g_q = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_q, stream=cap):
+            for l in range(L):
+                vr.decode_q(shape, caches[l], qcs[l], qs[l], bases[l][0], bases[l][1], out=outs[l], workspace=ws_d)
+        torch.cuda.synchronize()
+        st_q = _replay_stats(g_q, max(args.steps, 1))
+        qbytes = sum(decode_bytes_q(shape, c, quant_bits, c.rank.cpu().numpy()) for row in caches for c in row)
+        result[f"decode_{quant_bits}bit"] = {
+            "ms_per_step": round(st_q["p50"], 4), "ms_per_step_p10_p90": [round(st_q["p10"], 4), round(st_q["p90"], 4)],
+            "decode_GBps": round(qbytes / (st_q["p50"] * 1e-3) / 1e9, 2),
+            "frac": round(qbytes / (st_q["p50"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "decode_tokens_per_s": round(S / (st_q["p50"] * 1e-3), 1),
+            "decode_bytes_per_step": int(qbytes),
+        }
     if emit:
         print(json.dumps(result), flush=True)
     return result

@@ -18,13 +18,12 @@
 // at [s][position].  Tile bytes: 2 mq b + 32 KS (a multiple of 16).
 //
 // Two launches: one workgroup sums the tile sizes of every chunk and scans them into
-// qchunk_off; then one workgroup per (chunk, head, stream) writes its tiles (a wave per tile).
+// qchunk_off; then persistent waves write the tiles, one (chunk, head, stream, tile) at a time.
 #include "vr_internal.h"
 
 namespace vr {
 
 constexpr int QZ_SCAN_THREADS = 1024;
-constexpr int QZ_THREADS = 256;
 
 __host__ __device__ constexpr uint32_t qz_tile_bytes(uint32_t m, int b) {
     return m == 0 ? 0u : 2u * ((m + 7u) & ~7u) * (uint32_t)b + 32u * ((m + 31u) / 32u);
@@ -76,79 +75,132 @@ struct QzParams {
     int G, bits;
 };
 
+// Persistent waves: wave w of the grid takes the tiles (chunk, head, stream, tile) = w,
+// w + W, ... (W waves in all); one tile at a time, in four steps that only the wave's own
+// lanes share (its own LDS region, wave-scope fences): the bf16 tile rectangle into LDS, the
+// 16 x KS group scales, every code (int8, [position][coordinate] for both streams), the
+// packed dwords (each assembled by one lane from the fields it covers).  Few large
+// workgroups: dispatching one small workgroup per tile is far slower than the work.
+constexpr int QZ_WAVES = 4;
+constexpr int QZ_VS = D + 1;                      // padded LDS row stride: no bank conflicts
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int QB>
-__global__ __launch_bounds__(QZ_THREADS) void qz_kernel(QzParams p) {
+__global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total, int nwaves) {
     constexpr int QMAX = (1 << (QB - 1)) - 1;
-    __shared__ float scl[QZ_THREADS / 64][64];    // per wave: the tile's scales, [s][position]
-    const int c = blockIdx.x / (2 * p.G);
-    const int g = (blockIdx.x / 2) % p.G;
-    const int kv = blockIdx.x & 1;
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int64_t t0 = (int64_t)c * CHUNK;
-    const int T = (int)(p.N - t0 < CHUNK ? p.N - t0 : CHUNK);
-    // tile sizes of the chunk and their offsets in both layouts (every lane of every wave)
-    uint32_t m[16], eoff[16], boff[16];
-    uint32_t e = p.chunk_off[c], q = p.qchunk_off[c];
-#pragma unroll
-    for (int h = 0; h < 16; ++h) {
-        m[h] = 16 * h < T ? (uint32_t)p.srank[t0 + 16 * h] : 0u;
-        eoff[h] = e;
-        boff[h] = q;
-        e += 16u * m[h];
-        q += qz_tile_bytes(m[h], QB);
-    }
-    const uint16_t* src = p.coef[kv] + (int64_t)g * p.coef_stride;
-    uint8_t* dst = p.code[kv] + (int64_t)g * p.q_stride;
-    // every wave takes 4 tiles (16 / 4), so the workgroup barriers below match up
-    for (int h = wave; h < 16; h += QZ_THREADS / 64) {
-        const int mt = (int)m[h];                   // wave-uniform; 0: no tile
-        const int mq = (mt + 7) & ~7, ks = (mt + 31) / 32;
-        const uint16_t* tile = src + eoff[h];
-        uint8_t* out = dst + boff[h];
-        // element (position i, coordinate j) of the bf16 tile rectangle
-        auto val = [&](int i, int j) -> float {
-            if (j >= mt) return 0.f;
-            const int idx = kv == 0 ? i * mt + j : j * 16 + i;
-            return bf16_to_f32(tile[idx]);
-        };
-        // ---- scales: lane -> group (s, i) = (lane / 16, lane % 16)
-        {
-            const int s = lane >> 4, i = lane & 15;
-            float sc = 0.f;
-            if (s < ks) {
-                float amax = 0.f;
-                for (int j = 32 * s; j < 32 * s + 32; ++j) amax = fmaxf(amax, fabsf(val(i, j)));
-                const float ratio = __fdiv_rn(amax, (float)QMAX);
-                const _Float16 hs = (_Float16)ratio;           // nearest binary16, ties to even
-                sc = (float)hs;
-                reinterpret_cast<uint16_t*>(out + 2 * mq * QB)[16 * s + i] = __builtin_bit_cast(uint16_t, hs);
-            }
-            scl[wave][lane] = sc;
+    constexpr int VS = QZ_VS;
+    __shared__ float val_s[QZ_WAVES][16 * VS];    // tile values, [position][coordinate]
+    __shared__ float scl_s[QZ_WAVES][4 * 16];     // [group][position]
+    __shared__ uint16_t sclh_s[QZ_WAVES][4 * 16]; // the same as binary16 bits
+    __shared__ int8_t cod_s[QZ_WAVES][16 * VS];   // codes, [position][coordinate]
+    __shared__ uint32_t m16_s[QZ_WAVES][16];
+    const int wave = threadIdx.x >> 6, tid = threadIdx.x & 63;
+    float* val = val_s[wave];
+    float* scl = scl_s[wave];
+    uint16_t* sclh = sclh_s[wave];
+    int8_t* cod = cod_s[wave];
+    uint32_t* m16 = m16_s[wave];
+    for (int item = blockIdx.x * QZ_WAVES + wave; item < total; item += nwaves) {
+        const int h = item & 15;
+        const int kv = (item >> 4) & 1;
+        const int g = (item >> 5) % p.G;
+        const int c = (item >> 5) / p.G;
+        const int64_t t0 = (int64_t)c * CHUNK;
+        const int T = (int)(p.N - t0 < CHUNK ? p.N - t0 : CHUNK);
+        if (16 * h >= T) continue;                // absent tile (wave-uniform)
+        // offsets of tile h in both layouts: the sizes of the chunk's earlier tiles
+        if (tid < 16) m16[tid] = 16 * tid < T ? (uint32_t)p.srank[t0 + 16 * tid] : 0u;
+        wave_sync();
+        uint32_t eo = p.chunk_off[c], bo = p.qchunk_off[c];
+        for (int k = 0; k < h; ++k) {
+            eo += 16u * m16[k];
+            bo += qz_tile_bytes(m16[k], QB);
         }
-        __syncthreads();
-        // ---- codes: lane -> output bytes lane, lane + 64, ...
-        const int nbytes = 2 * mq * QB;
-        for (int B = lane; B < nbytes; B += 64) {
-            uint32_t byte = 0;
-            const int ebeg = (8 * B) / QB, eend = (8 * B + 7) / QB;
-            for (int ee = ebeg; ee <= eend; ++ee) {
+        const int mt = (int)m16[h];
+        const int mq = (mt + 7) & ~7, ks = (mt + 31) / 32;
+        const uint16_t* src = p.coef[kv] + (int64_t)g * p.coef_stride + eo;
+        uint8_t* dst = p.code[kv] + (int64_t)g * p.q_stride + bo;
+        // ---- 1. the tile rectangle (16 mt contiguous bf16: K rows of mt, or V rows of 16),
+        //          16-byte loads scattered to [position][coordinate]; zeros up to mq
+        for (int e8 = tid; e8 < 2 * mt; e8 += 64) {
+            const u32x4 w = *reinterpret_cast<const u32x4*>(src + 8 * e8);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int f = 8 * e8 + k;
                 int i, j;
-                if (kv == 0) { i = ee / mq; j = ee % mq; }
-                else { j = ee >> 4; i = ee & 15; }
-                const float sc = scl[wave][16 * (j >> 5) + i];
+                if (kv == 0) { i = f / mt; j = f - i * mt; }
+                else { j = f >> 4; i = f & 15; }
+                val[i * VS + j] = (k & 1) ? bf_hi(w[k >> 1]) : bf_lo(w[k >> 1]);
+            }
+        }
+        for (int e = tid; e < 16 * (mq - mt); e += 64) val[(e & 15) * VS + mt + (e >> 4)] = 0.f;
+        wave_sync();
+        // ---- 2. group scales: lane -> (group s, position i)
+        if (tid < 16 * ks) {
+            const int s = tid >> 4, i = tid & 15;
+            // every read issued before the max chain (entries past mq read row i's start: in
+            // bounds, then dropped)
+            float a[32];
+#pragma unroll
+            for (int u = 0; u < 32; ++u) {
+                const int j = 32 * s + u;
+                a[u] = j < mq ? fabsf(val[i * VS + j]) : 0.f;
+            }
+            float amax = 0.f;
+#pragma unroll
+            for (int u = 0; u < 32; ++u) amax = fmaxf(amax, a[u]);
+            const _Float16 hs = (_Float16)__fdiv_rn(amax, (float)QMAX);   // nearest binary16
+            scl[tid] = (float)hs;
+            sclh[tid] = __builtin_bit_cast(uint16_t, hs);
+        }
+        wave_sync();
+        // ---- 3. codes: lane -> coordinate j (and j + 64), every position
+        for (int j = tid; j < mq; j += 64) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float sc = scl[16 * (j >> 5) + i];
                 int k = 0;
                 if (sc != 0.f) {
-                    float r = __builtin_rintf(__fdiv_rn(val(i, j), sc));
-                    r = fminf(fmaxf(r, (float)-QMAX), (float)QMAX);
-                    k = (int)r;
+                    const float r = __builtin_rintf(__fdiv_rn(val[i * VS + j], sc));
+                    k = (int)fminf(fmaxf(r, (float)-QMAX), (float)QMAX);
                 }
-                const uint32_t field = (uint32_t)k & ((1u << QB) - 1u);
-                const int sh = QB * ee - 8 * B;             // field position relative to the byte
-                byte |= sh >= 0 ? (field << sh) : (field >> -sh);
+                cod[i * VS + j] = (int8_t)k;
             }
-            out[B] = (uint8_t)(byte & 0xFFu);
         }
-        __syncthreads();
+        wave_sync();
+        // ---- 4. packed dwords: K code (i, j) is field i mq + j, V code (j, i) is field
+        //          16 j + i; then the scales
+        uint32_t* dw = reinterpret_cast<uint32_t*>(dst);      // tile start: 16-byte aligned
+        const int nd = mq * QB / 2;
+        constexpr int NF = (32 + QB - 1) / QB + 1;          // fields a dword can touch
+        for (int d = tid; d < nd; d += 64) {
+            uint32_t word = 0;
+            const int ebeg = (32 * d) / QB, eend = (32 * d + 31) / QB;
+            int8_t cv[NF];
+#pragma unroll
+            for (int u = 0; u < NF; ++u) {
+                const int ee = ebeg + u <= eend ? ebeg + u : ebeg;   // in bounds; dropped below
+                int i, j;
+                if (kv == 0) { i = ee / mq; j = ee - i * mq; }
+                else { j = ee >> 4; i = ee & 15; }
+                cv[u] = cod[i * VS + j];
+            }
+#pragma unroll
+            for (int u = 0; u < NF; ++u) {
+                const int ee = ebeg + u;
+                const uint32_t field = ee <= eend ? (uint32_t)(int)cv[u] & ((1u << QB) - 1u) : 0u;
+                const int sh = QB * ee - 32 * d;
+                word |= sh >= 0 ? (field << sh) : (field >> -sh);
+            }
+            dw[d] = word;
+        }
+        if (tid < 8 * ks) dw[nd + tid] = (uint32_t)sclh[2 * tid] | ((uint32_t)sclh[2 * tid + 1] << 16);
+        wave_sync();                              // the wave's LDS is reused by its next tile
     }
 }
 
@@ -182,11 +234,21 @@ hipError_t launch_quantize(const varrate_shape& sh, const varrate_cache& c, varr
     p.q_stride = q.q_stride;
     p.G = sh.G;
     p.bits = q.bits;
-    const unsigned grid = (unsigned)(n_chunks * sh.G * 2);
+    const int total = n_chunks * sh.G * 2 * 16;                 // (chunk, head, stream, tile)
+    int blocks = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)qz_kernel<4>, 64 * QZ_WAVES, 0);
+    if (e != hipSuccess) return e;
+    int dev = 0, cus = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    int grid = (blocks > 0 ? blocks : 1) * cus;
+    const int need = (total + QZ_WAVES - 1) / QZ_WAVES;
+    grid = grid < need ? grid : need;
+    const int nwaves = grid * QZ_WAVES;
     switch (q.bits) {
-        case 3: qz_kernel<3><<<grid, QZ_THREADS, 0, st>>>(p); break;
-        case 4: qz_kernel<4><<<grid, QZ_THREADS, 0, st>>>(p); break;
-        case 8: qz_kernel<8><<<grid, QZ_THREADS, 0, st>>>(p); break;
+        case 3: qz_kernel<3><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total, nwaves); break;
+        case 4: qz_kernel<4><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total, nwaves); break;
+        case 8: qz_kernel<8><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total, nwaves); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
