@@ -69,6 +69,11 @@ def lib():
         L.vro_quantize.restype = None
         L.vro_quantize.argtypes = [_i64, _int, _int, _f32p, _i32p, _int,
                                    np.ctypeslib.ndpointer(np.int8, flags="C_CONTIGUOUS"), _f32p, _f32p]
+        L.vro_anchor_nearest.restype = None
+        L.vro_anchor_nearest.argtypes = [_i64, _int, _int, _int, _int, _f32p, _f32p, _i32p, _f64p]
+        L.vro_decode_anchor.restype = None
+        L.vro_decode_anchor.argtypes = [_i64, _i64, _i64, _int, _int, _int, _int, _f32p, _f32p, _i32p, _i32p,
+                                        _f32p, _f32p, _f32p, _f32p, _f32p, _f32p, _f32p, _f64p]
         L.vro_decode.restype = None
         L.vro_decode.argtypes = [_i64, _i64, _int, _int, _int, _f32p, _f32p, _i32p,
                                  _f32p, _f32p, _f32p, _f32p, _f32p, _f64p]
@@ -222,3 +227,97 @@ def compress(K, V, Qw, PK, PV, H: int, kappa_pct: int, r_min: int, storage: str,
     cV = project(V[:N], PV, al.rank, storage)
     return Compressed(s, sb, u, al, B, cK, cV, np.ascontiguousarray(K[N:]),
                       np.ascontiguousarray(V[N:]))
+
+
+# ---------------------------------------------------------------------------------------
+# Sec. 3.1 "Residual codec" (Eq. 2), Algorithm 1: strided anchors kept exact, every other
+# prefix token coded as its residual to the mean of its c nearest anchors.
+
+def anchor_nearest(K: np.ndarray, V: np.ndarray, N: int, delta: int, c: int):
+    """c nearest anchors (strided prefix tokens 0, delta, ... < N) of every prefix token by
+    the exact Euclidean distance over the joint vector [k (all heads); v (all heads)];
+    rows of anchors are -1.  Returns (nn [N][c] int32 anchor numbers, dist [N][c] fp64)."""
+    n, G, d = K.shape
+    nn = np.zeros((N, c), np.int32)
+    dist = np.zeros((N, c), np.float64)
+    lib().vro_anchor_nearest(N, G, d, delta, c, _c(K[:N], np.float32), _c(V[:N], np.float32), nn, dist)
+    return nn, dist
+
+
+def round_storage(x: np.ndarray, storage: str) -> np.ndarray:
+    """Nearest bf16 (ties to even) for bf16 storage, fp32 otherwise."""
+    x = np.ascontiguousarray(x, np.float32)
+    if storage != "bf16":
+        return x
+    b = x.view(np.uint32)
+    r = (b + (np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1)))) & np.uint32(0xFFFF0000)
+    return r.view(np.float32)
+
+
+@dataclass
+class AnchorCompressed:
+    coded: np.ndarray     # int64 [Nc] token index of each coded token (ascending)
+    anchors: np.ndarray   # int64 [na] token index of each anchor
+    nn: np.ndarray        # int32 [Nc][c] anchor numbers of each coded token's nearest anchors
+    dist: np.ndarray      # fp64 [Nc][c] their distances
+    sbar: np.ndarray      # fp32 [N] pooled salience over the whole prefix
+    u: np.ndarray         # uint32 [Nc] weights of the coded tokens
+    alloc: Allocation
+    B: int
+    resK: np.ndarray      # [Nc][G][d] residuals (rounded to the storage type)
+    resV: np.ndarray
+    coefK: np.ndarray     # [Nc][G][d] storage-rounded coefficients of the residuals
+    coefV: np.ndarray
+    Ka: np.ndarray        # anchor rows [na][G][d]
+    Va: np.ndarray
+    Kx: np.ndarray        # window rows [w][G][d]
+    Vx: np.ndarray
+
+
+def anchor_budget(n: int, d: int, w: int, kappa_pct: int, na: int) -> int:
+    """Eq. (3) with n_ref = |E| = na + w: floor(kappa n d / 100) - (na + w) d."""
+    return budget(n, d, w, kappa_pct) - na * d
+
+
+def compress_anchor(K, V, Qw, PK, PV, H: int, kappa_pct: int, r_min: int, storage: str,
+                    delta: int = 16, c: int = 4, sbar: np.ndarray | None = None) -> AnchorCompressed:
+    """Algorithm 1 with the residual codec (per-head bases, no RoPE): anchors every delta
+    prefix tokens and the window kept exact; salience and its pooling over the whole prefix,
+    min-max and water-filling over the coded tokens only (budget net of the anchors); each
+    coded token projected as its residual to the mean of its c nearest anchors."""
+    n, G, d = K.shape
+    w = Qw.shape[0]
+    N = n - w
+    anchors = np.arange(0, N, delta, dtype=np.int64)
+    coded = np.setdiff1d(np.arange(N, dtype=np.int64), anchors)
+    na, Nc = len(anchors), len(coded)
+    B = anchor_budget(n, d, w, kappa_pct, na)
+    sb = pool(salience(K, Qw, H)) if sbar is None else _c(sbar, np.float32)
+    u = weights(sb[coded])
+    al = allocate(u, B, r_min, d)
+    nn_all, dist_all = anchor_nearest(K, V, N, delta, c)
+    nn, dist = nn_all[coded], dist_all[coded]
+    Ka, Va = np.ascontiguousarray(K[anchors]), np.ascontiguousarray(V[anchors])
+    meanK = Ka[nn].astype(np.float64).mean(axis=1)       # [Nc][G][d]
+    meanV = Va[nn].astype(np.float64).mean(axis=1)
+    resK = round_storage(K[coded].astype(np.float64) - meanK, storage)
+    resV = round_storage(V[coded].astype(np.float64) - meanV, storage)
+    cK = project(resK, PK, al.rank, storage)
+    cV = project(resV, PV, al.rank, storage)
+    return AnchorCompressed(coded, anchors, nn, dist, sb, u, al, B, resK, resV, cK, cV, Ka, Va,
+                            np.ascontiguousarray(K[N:]), np.ascontiguousarray(V[N:]))
+
+
+def decode_anchor(ac: AnchorCompressed, PK, PV, q, H: int, Kx=None, Vx=None) -> np.ndarray:
+    """Reconstruct-in-place decode with anchors: coded tokens rebuilt as their anchor mean
+    plus the truncated projection, anchors and exact rows as stored (fp64)."""
+    Nc, G, d = ac.coefK.shape
+    Kx = ac.Kx if Kx is None else Kx
+    Vx = ac.Vx if Vx is None else Vx
+    out = np.zeros((H, d), np.float64)
+    c = ac.nn.shape[1]
+    lib().vro_decode_anchor(Nc, ac.Ka.shape[0], Kx.shape[0], G, H, d, c, _c(ac.coefK, np.float32),
+                            _c(ac.coefV, np.float32), _c(ac.alloc.rank, np.int32), _c(ac.nn, np.int32),
+                            _c(ac.Ka, np.float32), _c(ac.Va, np.float32), _c(Kx, np.float32), _c(Vx, np.float32),
+                            _c(PK, np.float32), _c(PV, np.float32), _c(q, np.float32), out)
+    return out

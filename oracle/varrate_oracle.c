@@ -15,6 +15,8 @@
  *   projection/truncation  Sec. 3.3 Eq. (6) "eq:recon", Algorithm 1 (projection step)
  *   decode                 Sec. 4.4 "Cost": reconstruct-in-place, then stock attention
  *   coefficient quantiser  Sec. 3.3 "Composability": group-wise b-bit codes of the coefficients
+ *   anchor residual codec  Sec. 3.1 "Residual codec" Eq. (2), Algorithm 1 (anchors, exact set,
+ *                          nearest-anchor mean, residual)
  *
  * Specialisation (the data-parallel path only): per-KV-head bases P in R^{d x d} (R = d, so
  * full rank is exact), no anchors (residual mean zbar = 0), no RoPE, exact set = last w tokens.
@@ -421,4 +423,121 @@ EXPORT void vro_quantize(int64_t n_tok, int G, int d, const float *coef, const i
             }
         }
     }
+}
+
+/* ------------------------------------------------------------------------------------- */
+/* Sec. 3.1 "Residual codec" (Eq. 2) and Algorithm 1 (anchors, exact set, residual).
+ * Anchors: the prefix tokens at stride delta, t = 0, delta, 2 delta, ... < N (the paper's
+ * z_1, z_{1+delta}, ... in 1-based numbering); they are kept exact, as is the window.
+ * Joint vector z_t = [k_t (all G heads); v_t (all G heads)] in R^{2 G d}.  For every other
+ * prefix token, its c nearest anchors in Euclidean distance over z (computed exactly in fp64
+ * here; ties to the lower anchor number).  anchor_of[t] = index of t in the anchor list, or
+ * -1; nn[t][0..c-1] = anchor numbers in increasing distance (rows of anchors left -1).     */
+EXPORT void vro_anchor_nearest(int64_t N, int G, int d, int delta, int c, const float *K, const float *V,
+                               int32_t *nn, double *dist)
+{
+    const int64_t na = (N + delta - 1) / delta;
+    const int64_t D = (int64_t)G * d;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int64_t t = 0; t < N; ++t) {
+        int32_t *out = nn + t * c;
+        double *od = dist + t * c;
+        for (int k = 0; k < c; ++k) { out[k] = -1; od[k] = INFINITY; }
+        if (t % delta == 0) continue;
+        for (int64_t a = 0; a < na; ++a) {
+            const int64_t ta = a * delta;
+            double s = 0.0;
+            for (int64_t i = 0; i < D; ++i) {
+                const double dk = (double)K[t * D + i] - (double)K[ta * D + i];
+                const double dv = (double)V[t * D + i] - (double)V[ta * D + i];
+                s += dk * dk + dv * dv;
+            }
+            /* insert into the sorted list (strictly smaller moves ahead: ties keep the
+             * lower anchor number, which was seen first) */
+            int pos = c;
+            while (pos > 0 && s < od[pos - 1]) --pos;
+            if (pos < c) {
+                for (int k = c - 1; k > pos; --k) { od[k] = od[k - 1]; out[k] = out[k - 1]; }
+                od[pos] = s;
+                out[pos] = (int32_t)a;
+            }
+        }
+    }
+}
+
+/* Decode with anchors (reconstruct-in-place, Eq. 6 with the anchor mean):
+ *   coded token i (token index tok[i]): k_hat = (1/c) sum_k Ka[nn[i][k]] + P_K^T (m . cK[i]),
+ *                                       v_hat likewise;
+ *   anchors (Ka, Va) and exact rows (Kx, Vx) as stored;
+ * then stock attention of q over all of them (fp64).  Layouts: coefK/coefV [Nc][G][d],
+ * nn [Nc][c] anchor numbers, Ka/Va [na][G][d], Kx/Vx [n_exact][G][d], q [H][d], out [H][d]. */
+EXPORT void vro_decode_anchor(int64_t Nc, int64_t na, int64_t n_exact, int G, int H, int d, int c,
+                              const float *coefK, const float *coefV, const int32_t *rank,
+                              const int32_t *nn, const float *Ka, const float *Va,
+                              const float *Kx, const float *Vx, const float *PK, const float *PV,
+                              const float *q, double *out)
+{
+    const int hpg = H / G;
+    const double scale = 1.0 / sqrt((double)d);
+    const int64_t T = Nc + na + n_exact;
+    double *kh = (double *)malloc(sizeof(double) * (size_t)(Nc > 0 ? Nc : 1) * d);
+    double *vh = (double *)malloc(sizeof(double) * (size_t)(Nc > 0 ? Nc : 1) * d);
+    double *x = (double *)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+    for (int g = 0; g < G; ++g) {
+        const float *Pk = PK + (int64_t)g * d * d;
+        const float *Pv = PV + (int64_t)g * d * d;
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < Nc; ++i) {
+            const float *ck = coefK + (i * G + g) * d;
+            const float *cv = coefV + (i * G + g) * d;
+            for (int e = 0; e < d; ++e) {
+                double mk = 0.0, mv = 0.0;
+                for (int k = 0; k < c; ++k) {
+                    const int64_t a = nn[i * c + k];
+                    mk += (double)Ka[(a * G + g) * d + e];
+                    mv += (double)Va[(a * G + g) * d + e];
+                }
+                double ak = mk / c, av = mv / c;
+                for (int j = 0; j < rank[i]; ++j) {
+                    ak += (double)ck[j] * (double)Pk[(int64_t)j * d + e];
+                    av += (double)cv[j] * (double)Pv[(int64_t)j * d + e];
+                }
+                kh[i * d + e] = ak;
+                vh[i * d + e] = av;
+            }
+        }
+        for (int hh = 0; hh < hpg; ++hh) {
+            const int h = g * hpg + hh;
+            const float *qh = q + (int64_t)h * d;
+            double m = -INFINITY;
+            for (int64_t t = 0; t < T; ++t) {
+                double acc = 0.0;
+                if (t < Nc) {
+                    for (int e = 0; e < d; ++e) acc += (double)qh[e] * kh[t * d + e];
+                } else if (t < Nc + na) {
+                    acc = dot_fd(qh, Ka + ((t - Nc) * G + g) * d, d);
+                } else {
+                    acc = dot_fd(qh, Kx + ((t - Nc - na) * G + g) * d, d);
+                }
+                x[t] = acc * scale;
+                if (x[t] > m) m = x[t];
+            }
+            double z = 0.0;
+            for (int64_t t = 0; t < T; ++t) { x[t] = exp(x[t] - m); z += x[t]; }
+            double *o = out + (int64_t)h * d;
+            for (int e = 0; e < d; ++e) o[e] = 0.0;
+            for (int64_t t = 0; t < T; ++t) {
+                const double a = x[t] / z;
+                if (t < Nc) {
+                    for (int e = 0; e < d; ++e) o[e] += a * vh[t * d + e];
+                } else {
+                    const float *v = t < Nc + na ? Va + ((t - Nc) * G + g) * d : Vx + ((t - Nc - na) * G + g) * d;
+                    for (int e = 0; e < d; ++e) o[e] += a * (double)v[e];
+                }
+            }
+        }
+    }
+    free(kh);
+    free(vh);
+    free(x);
 }
