@@ -74,7 +74,10 @@ typedef struct varrate_shape {
     int32_t r_min;      /* rank floor, 0 <= r_min <= 128                                    */
     int32_t kappa_pct;  /* KV budget kappa as an integer percent, 1..100                     */
     int32_t dtype;      /* VARRATE_BF16 or VARRATE_F32                                      */
-    int32_t reserved;
+    int32_t anchor_stride; /* 0: no anchors.  delta >= 2: the residual codec of Sec. 3.1 Eq. (2)
+                              (bf16 layers): prefix tokens 0, delta, 2 delta, ... < n - w are
+                              exact anchors, and every other prefix token is coded as its
+                              residual to the mean of its 4 nearest anchors (see below)        */
 } varrate_shape;
 
 /*
@@ -97,6 +100,15 @@ typedef struct varrate_shape {
  *     VARRATE_CHUNK * n_chunks (a tile's size is bounded by the ranks of the tile before it).
  *   - k_exact/v_exact hold exact rows: slot e < w is token N + e (the window); slots
  *     e >= w are tokens appended after compression (varrate_append_exact).
+ * Residual codec (shape->anchor_stride = delta > 0).  The prefix's na = ceil((n - w) / delta)
+ * anchors (tokens a delta) are exact and the coded tokens are the other N = n - w - na prefix
+ * tokens, numbered in order (coded token i is token i + i / (delta - 1) + 1); everything above
+ * (ranks, storage order, tiles, budget) is over them, with B = floor(kappa n d / 100) -
+ * (na + w) d (Eq. 3 with n_ref = na + w).  Each coded token's 4 nearest anchors are by
+ * squared Euclidean distance over z_t = [k_t of all heads; v_t of all heads] (Eq. 2), computed
+ * as ||z_a||^2 - 2 <z_a, z_t> with fp32 accumulation of exact bf16 products (ties to the
+ * lower anchor); its stored coefficients are those of its residual x_t - (1/4) sum of the
+ * anchors' rows (fp32, rounded to bf16 before the projection).
  * All pointers are device memory owned by the caller; sizes come from
  * varrate_cache_bytes().  n_exact is advanced on the host by varrate_compress (to w) and
  * varrate_append_exact.
@@ -115,12 +127,23 @@ typedef struct varrate_cache {
     int64_t   n_exact;      /* exact slots in use                                           */
     int64_t   N;            /* coded tokens                                                 */
     int64_t   B;            /* coded budget (coefficients per head stream)                  */
+    /* residual codec only (anchor_stride > 0; NULL / 0 otherwise):                          */
+    void*     k_anchor;     /* [na][G][d] dtype: the anchors' keys, exact                   */
+    void*     v_anchor;     /* [na][G][d] dtype: the anchors' values, exact                 */
+    uint16_t* snn;          /* [N][4] the 4 nearest anchors (anchor numbers, nearest first)
+                               of stored position i                                        */
+    uint32_t* inv_off;      /* [na + 1] start of each anchor's list in inv_pos              */
+    uint32_t* inv_pos;      /* [4 N] stored positions whose nearest anchors include anchor a,
+                               at inv_pos[inv_off[a] .. inv_off[a + 1])                    */
+    int64_t   na;           /* anchors                                                      */
 } varrate_cache;
 
 /* Buffer sizes (bytes) a caller must allocate for one varrate_cache. */
 typedef struct varrate_cache_bytes_t {
     int64_t N, B, n_chunks, coef_stride;
     size_t coef_k, coef_v, rank, srank, sidx, chunk_off, k_exact, v_exact;
+    int64_t na;                                      /* residual codec: anchors (else 0)       */
+    size_t k_anchor, v_anchor, snn, inv_off, inv_pos; /* residual codec buffers (else 0)       */
 } varrate_cache_bytes_t;
 
 /* ---- diagnostics ---------------------------------------------------------------------- */
@@ -182,6 +205,20 @@ VARRATE_API int varrate_compress(const varrate_shape* shape, const void* K, cons
  * (tokens generated after compression stay exact).  EINVAL when the capacity is full.       */
 VARRATE_API int varrate_append_exact(const varrate_shape* shape, varrate_cache* cache, const void* k_new,
                          const void* v_new, void* stream);
+
+/* Residual codec stages (shape->anchor_stride > 0, bf16 layers).
+ * varrate_anchor_search: the 4 nearest anchors of every coded token (coded order), nn
+ *   [N][4] anchor numbers, nearest first; K, V [n][G][d].
+ * varrate_anchor_encode: the rest of Algorithm 1 given the pooled salience of the whole
+ *   prefix (sbar [n - w] fp32) and nn (from varrate_anchor_search or any other source, [N][4]
+ *   coded order): the coded tokens' salience, the water-filling over them, residuals and their
+ *   projection, the exact window and anchor rows, and the anchor lists of the cache.
+ * varrate_compress on such a shape runs salience -> anchor search -> anchor encode.        */
+VARRATE_API int varrate_anchor_search(const varrate_shape* shape, const void* K, const void* V, uint16_t* nn,
+                          void* workspace, size_t workspace_bytes, void* stream);
+VARRATE_API int varrate_anchor_encode(const varrate_shape* shape, const void* K, const void* V, const float* sbar,
+                          const uint16_t* nn, const float* P_K, const float* P_V, varrate_cache* cache,
+                          void* workspace, size_t workspace_bytes, void* stream);
 
 /* Rank-space decode attention (the fused decode Sec. 4.4 calls for).
  * caches: host array of S compressed sequences of this shape (same layer, same bases).

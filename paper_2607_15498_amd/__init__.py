@@ -21,7 +21,7 @@ from ._lib import CHUNK, COEF_PAD, HEAD_DIM  # noqa: F401
 
 __all__ = ["VarRateError", "Shape", "Cache", "new_cache", "coded_budget", "salience", "allocate",
            "project", "compress", "append_exact", "decode", "decode_noalloc", "QCache", "new_qcache",
-           "quantize", "decode_q", "library"]
+           "quantize", "decode_q", "anchor_search", "anchor_encode", "library"]
 
 
 class VarRateError(RuntimeError):
@@ -50,18 +50,27 @@ class Shape:
     kappa_pct: int
     dtype: str = "bf16"
     d: int = HEAD_DIM
+    anchor_stride: int = 0     # > 0: the residual codec with exact anchors every anchor_stride tokens
 
     def c(self) -> _lib.Shape:
         return _lib.Shape(self.n, self.G, self.H, self.d, self.w, self.r_min, self.kappa_pct,
-                          _lib.VARRATE_BF16 if self.dtype == "bf16" else _lib.VARRATE_F32, 0)
+                          _lib.VARRATE_BF16 if self.dtype == "bf16" else _lib.VARRATE_F32,
+                          self.anchor_stride)
 
     @property
     def torch_dtype(self):
         return torch.bfloat16 if self.dtype == "bf16" else torch.float32
 
     @property
+    def na(self) -> int:
+        """Anchors of the residual codec (0 without it)."""
+        a = self.anchor_stride
+        return (self.n - self.w + a - 1) // a if a else 0
+
+    @property
     def N(self) -> int:
-        return self.n - self.w
+        """Coded tokens (the prefix minus its anchors)."""
+        return self.n - self.w - self.na
 
 
 @dataclasses.dataclass
@@ -79,15 +88,23 @@ class Cache:
     n_exact: int = 0
     N: int = 0
     B: int = 0
+    k_anchor: Optional[torch.Tensor] = None     # residual codec: [na][G][d]
+    v_anchor: Optional[torch.Tensor] = None
+    snn: Optional[torch.Tensor] = None          # [N][4] int16 anchor numbers (stored order)
+    inv_off: Optional[torch.Tensor] = None      # [na + 1] int32
+    inv_pos: Optional[torch.Tensor] = None      # [4 N] int32
+    na: int = 0
 
     def c(self) -> _lib.CacheC:
+        ptr = lambda t: t.data_ptr() if t is not None else None
         return _lib.CacheC(self.coef_k.data_ptr(), self.coef_v.data_ptr(), self.rank.data_ptr(),
                            self.srank.data_ptr(), self.sidx.data_ptr(), self.chunk_off.data_ptr(),
                            self.k_exact.data_ptr(), self.v_exact.data_ptr(), self.coef_stride,
-                           self.cap, self.n_exact, self.N, self.B)
+                           self.cap, self.n_exact, self.N, self.B, ptr(self.k_anchor), ptr(self.v_anchor),
+                           ptr(self.snn), ptr(self.inv_off), ptr(self.inv_pos), self.na)
 
     def _update(self, cc: _lib.CacheC):
-        self.n_exact, self.N, self.B = int(cc.n_exact), int(cc.N), int(cc.B)
+        self.n_exact, self.N, self.B, self.na = int(cc.n_exact), int(cc.N), int(cc.B), int(cc.na)
 
 
 def coded_budget(n: int, w: int, kappa_pct: int, d: int = HEAD_DIM) -> int:
@@ -115,7 +132,13 @@ def new_cache(shape: Shape, cap: Optional[int] = None, device="cuda") -> Cache:
         chunk_off=torch.zeros(b.n_chunks + 1, dtype=torch.int32, device=device),
         k_exact=torch.zeros((G, cap, HEAD_DIM), dtype=dt, device=device),
         v_exact=torch.zeros((G, cap, HEAD_DIM), dtype=dt, device=device),
-        coef_stride=int(b.coef_stride), cap=cap, n_exact=0, N=int(b.N), B=int(b.B))
+        coef_stride=int(b.coef_stride), cap=cap, n_exact=0, N=int(b.N), B=int(b.B),
+        k_anchor=torch.zeros((b.na, G, HEAD_DIM), dtype=dt, device=device) if b.na else None,
+        v_anchor=torch.zeros((b.na, G, HEAD_DIM), dtype=dt, device=device) if b.na else None,
+        snn=torch.zeros((b.N, 4), dtype=torch.int16, device=device) if b.na else None,
+        inv_off=torch.zeros(b.na + 1, dtype=torch.int32, device=device) if b.na else None,
+        inv_pos=torch.zeros(4 * b.N, dtype=torch.int32, device=device) if b.na else None,
+        na=int(b.na))
 
 
 class _Workspaces:
@@ -165,7 +188,7 @@ def salience(shape: Shape, K: torch.Tensor, Qw: torch.Tensor, sbar: Optional[tor
              workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Sec. 3.2 Eq. (4) + 5-tap pooling: returns sbar [N] fp32 on the device."""
     if sbar is None:
-        sbar = torch.empty(shape.N, dtype=torch.float32, device=K.device)
+        sbar = torch.empty(shape.n - shape.w, dtype=torch.float32, device=K.device)
     ws, _ = _compress_ws(shape, K.device, workspace)
     _check(library().varrate_salience(ctypes.byref(shape.c()), _dev_ptr(K, shape.torch_dtype, "K"),
                                       _dev_ptr(Qw, shape.torch_dtype, "Qw"),
@@ -318,3 +341,31 @@ def decode_q(shape: Shape, caches: Sequence[Cache], qcaches: Sequence[QCache], q
                                            _dev_ptr(out, shape.torch_dtype, "out"), ws.data_ptr(), ws.numel(),
                                            _stream()))
     return out[0] if single else out
+
+
+def anchor_search(shape: Shape, K: torch.Tensor, V: torch.Tensor, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Residual codec (Sec. 3.1 Eq. (2)): the 4 nearest anchors of every coded token,
+    [N][4] int16 anchor numbers (nearest first)."""
+    nn = torch.empty((shape.N, 4), dtype=torch.int16, device=K.device)
+    ws, _ = _compress_ws(shape, K.device, workspace)
+    _check(library().varrate_anchor_search(ctypes.byref(shape.c()), _dev_ptr(K, shape.torch_dtype, "K"),
+                                           _dev_ptr(V, shape.torch_dtype, "V"), nn.data_ptr(), ws.data_ptr(),
+                                           ws.numel(), _stream()))
+    return nn
+
+
+def anchor_encode(shape: Shape, K, V, sbar: torch.Tensor, nn: torch.Tensor, PK, PV, cache: Optional[Cache] = None,
+                  cap: Optional[int] = None, workspace: Optional[torch.Tensor] = None) -> Cache:
+    """Residual codec, given the prefix's pooled salience sbar [n - w] and the nearest
+    anchors nn [N][4]: allocation over the coded tokens, residual projection, exact rows."""
+    if cache is None:
+        cache = new_cache(shape, cap, K.device)
+    ws, _ = _compress_ws(shape, K.device, workspace)
+    cc = cache.c()
+    _check(library().varrate_anchor_encode(ctypes.byref(shape.c()), _dev_ptr(K, shape.torch_dtype, "K"),
+                                           _dev_ptr(V, shape.torch_dtype, "V"), _dev_ptr(sbar, torch.float32, "sbar"),
+                                           _dev_ptr(nn, torch.int16, "nn"), _dev_ptr(PK, torch.float32, "PK"),
+                                           _dev_ptr(PV, torch.float32, "PV"), ctypes.byref(cc), ws.data_ptr(),
+                                           ws.numel(), _stream()))
+    cache._update(cc)
+    return cache

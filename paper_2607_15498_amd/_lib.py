@@ -22,6 +22,7 @@ EXPORTS = (
     "varrate_salience", "varrate_allocate", "varrate_project", "varrate_compress",
     "varrate_append_exact", "varrate_decode_attn", "varrate_decode_scratch_need",
     "varrate_decode_attn_noalloc", "varrate_qcache_bytes", "varrate_quantize", "varrate_decode_attn_q",
+    "varrate_anchor_search", "varrate_anchor_encode",
 )
 DECODE_SCRATCH_BYTES = 8 << 20
 
@@ -29,7 +30,7 @@ DECODE_SCRATCH_BYTES = 8 << 20
 class Shape(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int64), ("G", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("d", ctypes.c_int32), ("w", ctypes.c_int32), ("r_min", ctypes.c_int32),
-                ("kappa_pct", ctypes.c_int32), ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("kappa_pct", ctypes.c_int32), ("dtype", ctypes.c_int32), ("anchor_stride", ctypes.c_int32)]
 
 
 class CacheC(ctypes.Structure):
@@ -37,7 +38,9 @@ class CacheC(ctypes.Structure):
                 ("srank", ctypes.c_void_p), ("sidx", ctypes.c_void_p), ("chunk_off", ctypes.c_void_p),
                 ("k_exact", ctypes.c_void_p), ("v_exact", ctypes.c_void_p),
                 ("coef_stride", ctypes.c_int64), ("cap", ctypes.c_int64), ("n_exact", ctypes.c_int64),
-                ("N", ctypes.c_int64), ("B", ctypes.c_int64)]
+                ("N", ctypes.c_int64), ("B", ctypes.c_int64),
+                ("k_anchor", ctypes.c_void_p), ("v_anchor", ctypes.c_void_p), ("snn", ctypes.c_void_p),
+                ("inv_off", ctypes.c_void_p), ("inv_pos", ctypes.c_void_p), ("na", ctypes.c_int64)]
 
 
 class QCacheC(ctypes.Structure):
@@ -49,7 +52,9 @@ class CacheBytes(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("B", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
                 ("coef_stride", ctypes.c_int64)] + \
                [(k, ctypes.c_size_t) for k in ("coef_k", "coef_v", "rank", "srank", "sidx",
-                                               "chunk_off", "k_exact", "v_exact")]
+                                               "chunk_off", "k_exact", "v_exact")] + \
+               [("na", ctypes.c_int64)] + \
+               [(k, ctypes.c_size_t) for k in ("k_anchor", "v_anchor", "snn", "inv_off", "inv_pos")]
 
 
 _lib = None
@@ -82,6 +87,8 @@ def load() -> ctypes.CDLL:
         "varrate_decode_scratch_need": (sz, [P(Shape), i32, i32]),
         "varrate_decode_attn_noalloc": (ctypes.c_int, [P(Shape), P(CacheC), i32, vp, i32, vp, vp, vp, vp]),
         "varrate_qcache_bytes": (ctypes.c_int, [P(Shape), i32, P(i64), P(sz)]),
+        "varrate_anchor_search": (ctypes.c_int, [P(Shape), vp, vp, vp, vp, sz, vp]),
+        "varrate_anchor_encode": (ctypes.c_int, [P(Shape), vp, vp, vp, vp, vp, vp, P(CacheC), vp, sz, vp]),
         "varrate_quantize": (ctypes.c_int, [P(Shape), P(CacheC), P(QCacheC), vp]),
         "varrate_decode_attn_q": (ctypes.c_int, [P(Shape), P(CacheC), P(QCacheC), i32, vp, i32, vp, vp, vp, vp,
                                                  sz, vp]),

@@ -72,8 +72,16 @@ int check_shape(const varrate_shape* sh) {
                     (long long)(sh->H / sh->G) * sh->w);
     if (sh->n - sh->w > MAX_CODED)
         return fail(VARRATE_EUNSUPPORTED, "N=%lld coded tokens exceeds %lld", (long long)(sh->n - sh->w), (long long)MAX_CODED);
-    const int64_t B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
-    const int64_t N = sh->n - sh->w;
+    if (sh->anchor_stride != 0) {
+        if (sh->anchor_stride < 2 || sh->anchor_stride > 4096)
+            return fail(VARRATE_EINVAL, "anchor_stride=%d outside {0} or [2, 4096]", sh->anchor_stride);
+        if (sh->dtype != VARRATE_BF16) return fail(VARRATE_EUNSUPPORTED, "the residual codec needs a bf16 layer");
+        if (anchor_count(*sh) > 65535) return fail(VARRATE_EUNSUPPORTED, "more than 65535 anchors");
+        if (anchor_count(*sh) < 4) return fail(VARRATE_EBUDGET, "fewer than 4 anchors");
+        if (coded_count(*sh) < 1) return fail(VARRATE_EBUDGET, "no coded tokens between the anchors");
+    }
+    const int64_t B = coded_budget(*sh);
+    const int64_t N = coded_count(*sh);
     if (N * sh->r_min > B || B > N * VARRATE_HEAD_DIM)
         return fail(VARRATE_EBUDGET, "budget B=%lld infeasible for N=%lld, r_min=%d, R=128", (long long)B,
                     (long long)N, sh->r_min);
@@ -82,13 +90,17 @@ int check_shape(const varrate_shape* sh) {
 
 int check_cache(const varrate_shape* sh, const varrate_cache* c, bool need_layout) {
     if (!c) return fail(VARRATE_EINVAL, "cache is NULL");
-    const int64_t B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    const int64_t B = coded_budget(*sh);
+    if (sh->anchor_stride != 0 && (!c->k_anchor || !c->v_anchor || !c->snn || !c->inv_off || !c->inv_pos))
+        return fail(VARRATE_EINVAL, "cache has a NULL anchor buffer");
+    if (sh->anchor_stride != 0 && (!aligned16(c->k_anchor) || !aligned16(c->v_anchor)))
+        return fail(VARRATE_EINVAL, "anchor buffers must be 16-byte aligned");
     if (!c->coef_k || !c->coef_v || !c->rank || !c->chunk_off || !c->k_exact || !c->v_exact ||
         (need_layout && (!c->srank || !c->sidx)))
         return fail(VARRATE_EINVAL, "cache has a NULL buffer");
     if (!aligned16(c->coef_k) || !aligned16(c->coef_v) || !aligned16(c->k_exact) || !aligned16(c->v_exact))
         return fail(VARRATE_EINVAL, "cache buffers must be 16-byte aligned");
-    const int64_t N = sh->n - sh->w;
+    const int64_t N = coded_count(*sh);
     const int64_t need = B + (int64_t)8 * VARRATE_CHUNK * ((N + VARRATE_CHUNK - 1) / VARRATE_CHUNK) + VARRATE_COEF_PAD;
     if (c->coef_stride < need || (c->coef_stride % 8) != 0)
         return fail(VARRATE_EINVAL, "coef_stride=%lld must be a multiple of 8 and >= %lld (B + 2048 per chunk + %d)",
@@ -98,6 +110,7 @@ int check_cache(const varrate_shape* sh, const varrate_cache* c, bool need_layou
 }
 
 size_t compress_ws(const varrate_shape& sh) {
+    if (sh.anchor_stride != 0) return anchor_ws_bytes(sh);
     const int64_t N = sh.n - sh.w;
     return align256(salience_ws_bytes(sh)) + align256(allocate_ws_bytes(sh)) + align256((size_t)N * 4);
 }
@@ -131,8 +144,13 @@ int varrate_cache_bytes(const varrate_shape* sh, int64_t cap, varrate_cache_byte
     if (!out) return fail(VARRATE_EINVAL, "out is NULL");
     if (cap < sh->w) return fail(VARRATE_EINVAL, "exact capacity %lld < w=%d", (long long)cap, sh->w);
     const size_t es = sh->dtype == VARRATE_BF16 ? 2 : 4;
-    out->N = sh->n - sh->w;
-    out->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
+    out->N = coded_count(*sh);
+    out->B = coded_budget(*sh);
+    out->na = anchor_count(*sh);
+    out->k_anchor = out->v_anchor = (size_t)out->na * sh->G * VARRATE_HEAD_DIM * es;
+    out->snn = out->na ? (size_t)out->N * 4 * 2 : 0;
+    out->inv_off = out->na ? (size_t)(out->na + 1) * 4 : 0;
+    out->inv_pos = out->na ? (size_t)out->N * 4 * 4 : 0;
     out->n_chunks = (out->N + VARRATE_CHUNK - 1) / VARRATE_CHUNK;
     // tile rectangles: a chunk's 16 tiles take at most its ranks + 16 x 128 elements
     const int64_t bound = out->B + (int64_t)8 * VARRATE_CHUNK * out->n_chunks;
@@ -176,6 +194,7 @@ int varrate_allocate(const varrate_shape* sh, const float* sbar, varrate_cache* 
                      size_t ws_bytes, void* stream) {
     int rc = check_shape(sh);
     if (rc) return rc;
+    if (sh->anchor_stride) return fail(VARRATE_EUNSUPPORTED, "residual codec: use varrate_anchor_encode");
     if ((rc = check_cache(sh, c, false))) return rc;
     if (!sbar) return fail(VARRATE_EINVAL, "sbar is NULL");
     if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
@@ -189,6 +208,7 @@ int varrate_project(const varrate_shape* sh, const void* K, const void* V, const
                     const float* PV, varrate_cache* c, void* ws, size_t ws_bytes, void* stream) {
     int rc = check_shape(sh);
     if (rc) return rc;
+    if (sh->anchor_stride) return fail(VARRATE_EUNSUPPORTED, "residual codec: use varrate_anchor_encode");
     if ((rc = check_cache(sh, c, true))) return rc;
     if (!K || !V || !PK || !PV) return fail(VARRATE_EINVAL, "K, V, P_K and P_V must be non-NULL");
     if (!aligned16(K) || !aligned16(V) || !aligned16(PK) || !aligned16(PV))
@@ -213,6 +233,21 @@ int varrate_compress(const varrate_shape* sh, const void* K, const void* V, cons
     if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
     if (!aligned16(K) || !aligned16(V) || !aligned16(Qw) || !aligned16(PK) || !aligned16(PV))
         return fail(VARRATE_EINVAL, "K, V, Qw, P_K, P_V must be 16-byte aligned");
+    if (sh->anchor_stride) {
+        // residual codec: salience over the whole prefix (pooled), anchor search, encode
+        hipStream_t st = (hipStream_t)stream;
+        const AnchorWs w = anchor_ws(*sh, (uint8_t*)ws);
+        float* sb = sbar_out ? sbar_out : w.sbar;
+        if ((rc = hip_status(launch_salience(*sh, K, Qw, sb, w.sal, st, true), "salience launch"))) return rc;
+        if ((rc = hip_status(launch_anchor_search(*sh, K, V, w.nn, w, st), "anchor search launch"))) return rc;
+        c->N = coded_count(*sh);
+        c->B = coded_budget(*sh);
+        c->na = anchor_count(*sh);
+        if ((rc = hip_status(launch_anchor_encode(*sh, K, V, sb, w.nn, PK, PV, *c, w, st), "anchor encode launch")))
+            return rc;
+        c->n_exact = sh->w;
+        return VARRATE_OK;
+    }
     float* sbar = sbar_out;
     if (!sbar) {
         sbar = (float*)((uint8_t*)ws + align256(salience_ws_bytes(*sh)) + align256(allocate_ws_bytes(*sh)));
@@ -229,6 +264,39 @@ int varrate_compress(const varrate_shape* sh, const void* K, const void* V, cons
     if ((rc = hip_status(launch_allocate(*sh, sbar, *c, w8, st, salience_part(*sh, w0)), "allocate launch")))
         return rc;
     if ((rc = hip_status(launch_project(*sh, K, V, PK, PV, *c, st), "project launch"))) return rc;
+    c->n_exact = sh->w;
+    return VARRATE_OK;
+}
+
+int varrate_anchor_search(const varrate_shape* sh, const void* K, const void* V, uint16_t* nn, void* ws,
+                          size_t ws_bytes, void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if (!sh->anchor_stride) return fail(VARRATE_EINVAL, "anchor_stride is 0");
+    if (!K || !V || !nn) return fail(VARRATE_EINVAL, "K, V and nn must be non-NULL");
+    if (!aligned16(K) || !aligned16(V)) return fail(VARRATE_EINVAL, "K and V must be 16-byte aligned");
+    if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
+    const AnchorWs w = anchor_ws(*sh, (uint8_t*)ws);
+    return hip_status(launch_anchor_search(*sh, K, V, nn, w, (hipStream_t)stream), "anchor search launch");
+}
+
+int varrate_anchor_encode(const varrate_shape* sh, const void* K, const void* V, const float* sbar, const uint16_t* nn,
+                          const float* PK, const float* PV, varrate_cache* c, void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_shape(sh);
+    if (rc) return rc;
+    if (!sh->anchor_stride) return fail(VARRATE_EINVAL, "anchor_stride is 0");
+    if ((rc = check_cache(sh, c, true))) return rc;
+    if (!K || !V || !sbar || !nn || !PK || !PV) return fail(VARRATE_EINVAL, "inputs must be non-NULL");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(PK) || !aligned16(PV))
+        return fail(VARRATE_EINVAL, "K, V, P_K, P_V must be 16-byte aligned");
+    if ((rc = ws_check(ws, ws_bytes, compress_ws(*sh)))) return rc;
+    const AnchorWs w = anchor_ws(*sh, (uint8_t*)ws);
+    c->N = coded_count(*sh);
+    c->B = coded_budget(*sh);
+    c->na = anchor_count(*sh);
+    if ((rc = hip_status(launch_anchor_encode(*sh, K, V, sbar, nn, PK, PV, *c, w, (hipStream_t)stream),
+                         "anchor encode launch")))
+        return rc;
     c->n_exact = sh->w;
     return VARRATE_OK;
 }
@@ -266,7 +334,7 @@ static int check_decode(const varrate_shape* sh, const varrate_cache* caches, in
         return fail(VARRATE_EINVAL, "q, P_K, P_V must be 16-byte aligned");
     for (int s = 0; s < S; ++s) {
         if ((rc = check_cache(sh, &caches[s], true))) return rc;
-        if (caches[s].N != sh->n - sh->w) return fail(VARRATE_EINVAL, "cache %d was not compressed with this shape", s);
+        if (caches[s].N != coded_count(*sh)) return fail(VARRATE_EINVAL, "cache %d was not compressed with this shape", s);
         if (caches[s].n_exact < 0 || caches[s].n_exact > caches[s].cap)
             return fail(VARRATE_EINVAL, "cache %d has n_exact outside [0, cap]", s);
         if (caches[s].coef_stride != caches[0].coef_stride || caches[s].cap != caches[0].cap)
@@ -292,7 +360,7 @@ int varrate_qcache_bytes(const varrate_shape* sh, int32_t bits, int64_t* q_strid
     if (rc) return rc;
     if (bits != 3 && bits != 4 && bits != 8) return fail(VARRATE_EUNSUPPORTED, "bits=%d not in {3, 4, 8}", bits);
     if (!q_stride || !qchunk_off_bytes) return fail(VARRATE_EINVAL, "outputs must be non-NULL");
-    const int64_t N = sh->n - sh->w;
+    const int64_t N = coded_count(*sh);
     *q_stride = (int64_t)qcache_stride(*sh, bits);
     *qchunk_off_bytes = (size_t)((N + VARRATE_CHUNK - 1) / VARRATE_CHUNK + 1) * 4;
     return VARRATE_OK;

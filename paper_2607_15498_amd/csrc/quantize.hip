@@ -206,9 +206,9 @@ __global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total
 
 // ----------------------------------------------------------------------------------------
 size_t qcache_stride(const varrate_shape& sh, int bits) {
-    const int64_t N = sh.n - sh.w;
+    const int64_t N = coded_count(sh);
     const int64_t n_chunks = (N + CHUNK - 1) / CHUNK;
-    const int64_t B = varrate_coded_budget(sh.n, sh.d, sh.w, sh.kappa_pct);
+    const int64_t B = coded_budget(sh);
     // a chunk's tile maxima sum to at most its ranks / 16 + 128, each tile pads up to 7
     // coordinates and holds at most 4 groups per position
     const int64_t bound = (int64_t)bits * B / 8 + n_chunks * (480LL * bits + 2048) + 64;
@@ -216,7 +216,7 @@ size_t qcache_stride(const varrate_shape& sh, int bits) {
 }
 
 hipError_t launch_quantize(const varrate_shape& sh, const varrate_cache& c, varrate_qcache& q, hipStream_t st) {
-    const int64_t N = sh.n - sh.w;
+    const int64_t N = coded_count(sh);
     const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
     qz_scan_kernel<<<1, QZ_SCAN_THREADS, 0, st>>>(c.srank, N, n_chunks, q.bits, q.qchunk_off);
     hipError_t e = hipGetLastError();

@@ -17,11 +17,19 @@ __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w <<
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
+// element <-> fp32 for the storage types (bf16 bits in uint16_t, or fp32)
+__device__ __forceinline__ float elem_f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+__device__ __forceinline__ float elem_f(float x) { return x; }
+
 // fp32 -> bf16 bits, round to nearest even (inputs are finite).
 __device__ __forceinline__ uint32_t f32_to_bf16(float x) {
     uint32_t u = __float_as_uint(x);
     return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
+template <typename ET> __device__ __forceinline__ ET to_elem(float x);
+template <> __device__ __forceinline__ uint16_t to_elem<uint16_t>(float x) { return (uint16_t)f32_to_bf16(x); }
+template <> __device__ __forceinline__ float to_elem<float>(float x) { return x; }
+
 // x = hi + lo to about 2^-17 relative: hi = bf16(x), lo = bf16(x - hi).
 __device__ __forceinline__ void split_bf16(float x, uint32_t& hi, uint32_t& lo) {
     hi = f32_to_bf16(x);

@@ -20,6 +20,44 @@ inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 // several devices are safe; this is the only state the library keeps across calls.
 hipError_t ensure_lds_limit(const void* fn, size_t bytes);
 
+// Residual codec: anchors are the prefix tokens 0, delta, ...; the coded tokens the rest.
+inline int64_t anchor_count(const varrate_shape& sh) {
+    return sh.anchor_stride > 0 ? (sh.n - sh.w + sh.anchor_stride - 1) / sh.anchor_stride : 0;
+}
+inline int64_t coded_count(const varrate_shape& sh) { return sh.n - sh.w - anchor_count(sh); }
+// Eq. (3) with n_ref = anchors + window
+inline int64_t coded_budget(const varrate_shape& sh) {
+    return varrate_coded_budget(sh.n, sh.d, sh.w, sh.kappa_pct) - anchor_count(sh) * sh.d;
+}
+// The shape the coded-token stages see (allocation, projection, decode): the coded tokens
+// followed by the window.  Its budget comes from the cache (cache.B), not from its kappa.
+inline varrate_shape coded_shape(const varrate_shape& sh) {
+    varrate_shape c = sh;
+    c.n = coded_count(sh) + sh.w;
+    c.anchor_stride = 0;
+    return c;
+}
+struct AnchorWs {
+    float* sbar;          // [n - w] pooled salience of the whole prefix
+    float* sbar_c;        // [N] coded tokens' salience
+    float* nrm;           // [na]
+    float* pk;            // [n_atiles][N][4]
+    uint32_t* pa;         // [n_atiles][N][4]
+    uint16_t* nn;         // [N][4]
+    void* Kr;             // [N + w][G][d] residuals, then the window rows
+    void* Vr;
+    uint32_t* cnt;        // [na]
+    uint8_t* sal;         // salience workspace
+    uint8_t* alloc;       // allocation workspace
+};
+size_t anchor_ws_bytes(const varrate_shape& sh);
+AnchorWs anchor_ws(const varrate_shape& sh, uint8_t* ws);
+hipError_t launch_anchor_search(const varrate_shape& sh, const void* K, const void* V, uint16_t* nn,
+                                const AnchorWs& w, hipStream_t st);
+hipError_t launch_anchor_encode(const varrate_shape& sh, const void* K, const void* V, const float* sbar,
+                                const uint16_t* nn, const float* PK, const float* PV, varrate_cache& c,
+                                const AnchorWs& w, hipStream_t st);
+
 size_t salience_ws_bytes(const varrate_shape& sh);
 size_t allocate_ws_bytes(const varrate_shape& sh);
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q);

@@ -33,12 +33,12 @@ def test_every_declared_symbol_is_exported(L):
 def test_struct_sizes_match_header():
     from paper_2607_15498_amd import _lib
     assert ctypes.sizeof(_lib.Shape) == 40
-    assert ctypes.sizeof(_lib.CacheC) == 8 * 8 + 5 * 8
+    assert ctypes.sizeof(_lib.CacheC) == 8 * 8 + 5 * 8 + 6 * 8
 
 
 def _shape(**kw):
     from paper_2607_15498_amd import _lib
-    base = dict(n=32768, G=8, H=32, d=128, w=32, r_min=16, kappa_pct=20, dtype=_lib.VARRATE_BF16, reserved=0)
+    base = dict(n=32768, G=8, H=32, d=128, w=32, r_min=16, kappa_pct=20, dtype=_lib.VARRATE_BF16, anchor_stride=0)
     base.update(kw)
     return _lib.Shape(**base)
 
@@ -175,3 +175,24 @@ def test_noalloc_decode_validates_and_bounds_its_scratch(L):
     rc = L.varrate_decode_attn_noalloc(ctypes.byref(sh), arr, S, fake, Q, fake, fake, fake, None)
     assert rc == -3
     assert b"scratch" in L.varrate_last_error()
+
+
+def test_residual_codec_sizes_and_validation(L):
+    """Residual codec shapes: the cache describes the coded tokens (the prefix minus its
+    anchors) with the budget net of the anchors (Eq. 3, n_ref = anchors + window)."""
+    from paper_2607_15498_amd import _lib
+    out = _lib.CacheBytes()
+    sh = _shape(anchor_stride=16)
+    assert L.varrate_cache_bytes(ctypes.byref(sh), 32, ctypes.byref(out)) == 0
+    na = (32768 - 32 + 15) // 16
+    assert out.na == na == 2046
+    assert out.N == 32768 - 32 - na
+    assert out.B == (20 * 32768 * 128) // 100 - (na + 32) * 128
+    assert out.k_anchor == na * 8 * 128 * 2 and out.snn == out.N * 8 and out.inv_pos == out.N * 16
+    assert out.inv_off == (na + 1) * 4
+    for kw, code in [(dict(anchor_stride=1), -1), (dict(anchor_stride=16, dtype=_lib.VARRATE_F32), -3),
+                     (dict(anchor_stride=16, kappa_pct=10), -2)]:
+        assert L.varrate_cache_bytes(ctypes.byref(_shape(**kw)), 32, ctypes.byref(out)) == code
+    # no anchors: the anchor buffers are empty
+    assert L.varrate_cache_bytes(ctypes.byref(_shape()), 32, ctypes.byref(out)) == 0
+    assert out.na == 0 and out.k_anchor == 0 and out.snn == 0 and out.inv_pos == 0
