@@ -416,6 +416,8 @@ int varrate_decode_attn_noalloc(const varrate_shape* sh, const varrate_cache* ca
                                 int32_t Q, const float* PK, const float* PV, void* out, void* stream) {
     int rc = check_decode(sh, caches, S, q, Q, PK, PV, out);
     if (rc) return rc;
+    if (sh->anchor_stride)
+        return fail(VARRATE_EUNSUPPORTED, "the residual codec's decode needs a workspace (varrate_decode_attn)");
     const size_t need = decode_group_bytes(*sh, S, Q);
     if (need > (size_t)VARRATE_DECODE_SCRATCH_BYTES)
         return fail(VARRATE_EUNSUPPORTED,

@@ -69,6 +69,10 @@ struct DecParams {
     float* part;
     int64_t N, coef_stride, cap;
     int G, H, hpg, nqt, rows_total, n_chunks, cpw, n_wg, tpw, total_tiles, units;
+    int nrec;                // records per unit (n_wg + 1, plus the anchor records of the residual codec)
+    const float* xbar;       // residual codec: [unit][16 total_tiles][ns] anchor-mean score terms
+    float* S;                // residual codec: [unit][16 total_tiles][ns] the coded tokens' scores
+    int ns;                  // query rows per unit those arrays hold
 };
 
 template <bool F32> struct Elem;
@@ -219,7 +223,27 @@ __device__ __forceinline__ void acc_read(f32x4 (&acc)[8]) {
 // and its size m (coded: the largest rank of the tile; exact rows: 128).
 struct TileMeta {
     int i0, T, base, m;
+    const float* xb;   // residual codec: the tile's 16 positions' anchor-mean score terms (else NULL)
+    float* sw;         // residual codec: where the tile's scores go
+    int ns;            // row stride of both
 };
+
+// Residual codec: a coded token's score also holds the mean of its anchors' scores (Eq. 2:
+// k_hat = anchor mean + P^T (m . c)); the final scores are kept for the anchors' value weights.
+__device__ __forceinline__ void anc_scores_in(const TileMeta& tm, int col, int grp, float (&xv)[4]) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) xv[v] = 0.f;
+    if (tm.xb && col < tm.ns) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) xv[v] = tm.xb[(4 * grp + v) * tm.ns + col];
+    }
+}
+__device__ __forceinline__ void anc_scores_out(const TileMeta& tm, int col, int grp, const float (&sv)[4]) {
+    if (tm.xb && col < tm.ns) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) tm.sw[(4 * grp + v) * tm.ns + col] = sv[v];
+    }
+}
 
 // One tile.  Scores S[token][row] by 16x16x32 MFMA over KS steps of 32 coefficients (A =
 // the tile's key rows, B = the query fragments); the C fragment (lane = query row, tokens
@@ -234,6 +258,8 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
                                           const u32x4* kmask, int lane, int grp, float& m_run,
                                           float& l_part) {
     const int col = lane & 15;
+    float xv[4];
+    anc_scores_in(tm, col, grp, xv);
     // K rows of a coded tile are m coordinates apart (exact rows: 128) with zeros past each
     // position's rank; a row piece past the row's end (into the next row, the pad or the LDS
     // arrays after the stage) is masked.  V blocks are coordinate-major (coded) or row-major
@@ -314,7 +340,8 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
     }
     float sv[4];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) sv[v] = sc[v];
+    for (int v = 0; v < 4; ++v) sv[v] = sc[v] + xv[v];
+    anc_scores_out(tm, col, grp, sv);
     if (partial) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) sv[v] = tm.i0 + 4 * grp + v < tm.T ? sv[v] : -INFINITY;
@@ -396,6 +423,8 @@ __device__ __forceinline__ void tile_step_q(const TileMeta& tm, bool partial, co
                                             float& m_run, float& l_part) {
     const int col = lane & 15;
     const int mq = tm.m;
+    float xv[4];
+    anc_scores_in(tm, col, grp, xv);
     const uint32_t* wk = reinterpret_cast<const uint32_t*>(sK + tm.base);   // 16-byte aligned
     const uint32_t* wv = reinterpret_cast<const uint32_t*>(sV + tm.base);
     const int sco = mq * QB;                        // scales after the codes, 2-byte units
@@ -432,7 +461,8 @@ __device__ __forceinline__ void tile_step_q(const TileMeta& tm, bool partial, co
     }
     float sv[4];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) sv[v] = sc[v];
+    for (int v = 0; v < 4; ++v) sv[v] = sc[v] + xv[v];
+    anc_scores_out(tm, col, grp, sv);
     if (partial) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) sv[v] = tm.i0 + 4 * grp + v < tm.T ? sv[v] : -INFINITY;
@@ -740,6 +770,14 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
             const int col = ln & 15, grp = ln >> 4;
             TileMeta tm;
             tm.base = __builtin_amdgcn_readfirstlane(toff(tile) - s0);
+            tm.xb = nullptr;
+            tm.sw = nullptr;
+            tm.ns = p.ns;
+            if (!exact && p.xbar) {
+                const int64_t o = ((int64_t)unit * p.total_tiles + tile) * 16 * p.ns;
+                tm.xb = p.xbar + o;
+                tm.sw = p.S + o;
+            }
             if (exact) {
                 tm.i0 = tile * 16;
                 tm.T = nexact;
@@ -818,8 +856,7 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
         }
     }
     __syncthreads();
-    const int nrec = p.n_wg + 1;
-    float* recs = p.part + (int64_t)unit * nrec * DC_REC;
+    float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
     {
         float* rec = recs + (int64_t)x * DC_REC;
         const int n4 = nr4 * D / 4;
@@ -852,6 +889,7 @@ struct MergeParams {
     void* out;              // [S][Q][H][d] of this launch's sequences
     int64_t out_seq_stride; // elements per sequence
     int G, H, hpg, nqt, rows_total, n_wg, rpu;
+    int nrec;               // records per unit; those past n_wg + 1 are original-space (anchors)
 };
 
 constexpr int MG_THREADS = 256;
@@ -875,7 +913,8 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
     const int rows = min(16, p.rows_total - 16 * qt);
     if (row >= rows) return;                      // row tiles with fewer rows (workgroup-uniform)
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int nrec = p.n_wg + 1;
+    const int nrec = p.nrec;
+    const int nrc = p.n_wg + 1;                   // records 1 .. nrc - 1 are rank-space
     const float* recs = p.part + (int64_t)unit * nrec * DC_REC;
 
     // ---- 1. issue every load: this row's max and sum of each record, its rank-space row of
@@ -895,7 +934,7 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
 #pragma unroll
     for (int u = 0; u < MG_RPT; ++u) {
         const int r = 1 + h + 2 * u;
-        a[u] = r < nrec ? recs[(int64_t)r * DC_REC + 32 + row * D + j] : 0.f;
+        a[u] = r < nrc ? recs[(int64_t)r * DC_REC + 32 + row * D + j] : 0.f;
     }
     const float* PV = p.PV + (int64_t)g * D * D + MG_COLS * cb + c;
     float pb[16];
@@ -944,9 +983,9 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
 #pragma unroll
     for (int u = 0; u < MG_RPT; ++u) {
         const int r = 1 + h + 2 * u;
-        s += (r < nrec ? wr[r] : 0.f) * a[u];
+        s += (r < nrc ? wr[r] : 0.f) * a[u];
     }
-    for (int r = 1 + h + 2 * MG_RPT; r < nrec; r += 2) s += wr[r] * recs[(int64_t)r * DC_REC + 32 + row * D + j];
+    for (int r = 1 + h + 2 * MG_RPT; r < nrc; r += 2) s += wr[r] * recs[(int64_t)r * DC_REC + 32 + row * D + j];
     accR[h][j] = s;
     __syncthreads();
 
@@ -963,7 +1002,9 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
         float t = part8[0][tid];
 #pragma unroll
         for (int k = 1; k < 8; ++k) t += part8[k][tid];
-        const float val = (t + wr[0] * ex) / L;
+        float e = wr[0] * ex;
+        for (int r = nrc; r < nrec; ++r) e += wr[r] * recs[(int64_t)r * DC_REC + 32 + row * D + MG_COLS * cb + tid];
+        const float val = (t + e) / L;
         const int qrow = 16 * qt + row;
         const int query = qrow / p.hpg, hh = qrow % p.hpg;
         ET* out = reinterpret_cast<ET*>(p.out) + (int64_t)sq * p.out_seq_stride;
@@ -973,13 +1014,209 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
     }
 }
 // ----------------------------------------------------------------------------------------
+// Residual codec (Sec. 3.1 Eq. (2)): a coded token's key is its anchors' mean plus the
+// truncated projection, so its score is the mean of its 4 anchors' scores plus the rank-space
+// product, and its value's anchor part sends a quarter of its softmax weight to each of its
+// anchors.  Three more launches around the streaming kernel:
+//   anc_qscores  X[unit][a][row] = <q_row, k_a> / sqrt(d) for every anchor (exact rows)
+//   anc_xbar     xbar[unit][pos][row] = (1/4) sum of X over the stored position's anchors, the
+//                term the streaming kernel adds to each coded score (it also writes the final
+//                scores S[unit][pos][row])
+//   anc_values   one record per (unit, block of anchors) in the original space: for its
+//                anchors, W_a = exp(X_a - F) + (1/4) sum over the positions that use a of
+//                exp(S - F) (the inverse lists), acc = sum W_a v_a, l = sum exp(X_a - F),
+//                m = F (the block's largest score); the merge combines these with the others
+//                by log-sum-exp like the exact record.
+struct AncDec {
+    const varrate_cache* seq;   // unused on the device
+    const void* q[DC_SEQ];
+    const void* ka[DC_SEQ];
+    const void* va[DC_SEQ];
+    const uint16_t* snn[DC_SEQ];
+    const uint32_t* inv_off[DC_SEQ];
+    const uint32_t* inv_pos[DC_SEQ];
+    float* X;          // [unit][na][ns]
+    float* xbar;       // [unit][16 total_tiles][ns]
+    float* S;          // [unit][16 total_tiles][ns]
+    float* part;       // records [unit][nrec][DC_REC]
+    int64_t N, na;
+    int G, H, hpg, nqt, rows_total, ns, total_tiles, nrec, rec0, ablk, n_ablk;
+};
+
+__device__ __forceinline__ void anc_unit(const AncDec& p, int unit, int& sq, int& g, int& qt, int& rows) {
+    const int per = p.G * p.nqt;
+    sq = unit / per;
+    const int gq = unit % per;
+    g = gq / p.nqt;
+    qt = gq % p.nqt;
+    rows = min(16, p.rows_total - 16 * qt);
+}
+
+// one thread per (anchor, row): 64 anchors x 4 row groups per workgroup
+__global__ __launch_bounds__(256) void anc_qscores(AncDec p) {
+    const int blocks = (int)((p.na + 63) / 64);
+    const int unit = blockIdx.x / blocks, ab = blockIdx.x % blocks;
+    int sq, g, qt, rows;
+    anc_unit(p, unit, sq, g, qt, rows);
+    const int64_t a = (int64_t)ab * 64 + (threadIdx.x >> 2);
+    const int rg = threadIdx.x & 3;
+    if (a >= p.na) return;
+    const uint16_t* ka = reinterpret_cast<const uint16_t*>(p.ka[sq]) + (a * p.G + g) * D;
+    const uint16_t* qb = reinterpret_cast<const uint16_t*>(p.q[sq]);
+    float* X = p.X + ((int64_t)unit * p.na + a) * p.ns;
+    for (int r = rg; r < p.ns; r += 4) {
+        float acc = 0.f;
+        if (r < rows) {
+            const int qrow = 16 * qt + r;
+            const uint16_t* qv = qb + ((int64_t)(qrow / p.hpg) * p.H + g * p.hpg + qrow % p.hpg) * D;
+            for (int e = 0; e < D; e += 8) {
+                const u32x4 kk = load16(ka + e), qq = load16(qv + e);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    acc = fmaf(bf_lo(kk[k]), bf_lo(qq[k]), acc);
+                    acc = fmaf(bf_hi(kk[k]), bf_hi(qq[k]), acc);
+                }
+            }
+        }
+        X[r] = acc * 0.08838834764831845f;   // 1/sqrt(128)
+    }
+}
+
+// one thread per (stored position, row group)
+__global__ __launch_bounds__(256) void anc_xbar(AncDec p) {
+    const int npos = 16 * p.total_tiles;
+    const int blocks = (npos + 63) / 64;
+    const int unit = blockIdx.x / blocks, pb = blockIdx.x % blocks;
+    int sq, g, qt, rows;
+    anc_unit(p, unit, sq, g, qt, rows);
+    const int64_t pos = (int64_t)pb * 64 + (threadIdx.x >> 2);
+    const int rg = threadIdx.x & 3;
+    if (pos >= npos) return;
+    float* xb = p.xbar + ((int64_t)unit * npos + pos) * p.ns;
+    const float* X = p.X + (int64_t)unit * p.na * p.ns;
+    if (pos >= p.N) {
+        for (int r = rg; r < p.ns; r += 4) xb[r] = 0.f;
+        return;
+    }
+    const uint16_t* nn = p.snn[sq] + pos * 4;
+    const int64_t a0 = nn[0], a1 = nn[1], a2 = nn[2], a3 = nn[3];
+    for (int r = rg; r < p.ns; r += 4)
+        xb[r] = (((X[a0 * p.ns + r] + X[a1 * p.ns + r]) + X[a2 * p.ns + r]) + X[a3 * p.ns + r]) * 0.25f;
+}
+
+// One thread per anchor (256 per workgroup), all rows at once.  The frame F[row] is an upper
+// bound of every score the block touches without a pass over the lists: the largest of its
+// anchors' own scores and of the streaming records' running maxima + 8 (each coded score
+// exceeds its workgroup's running maximum by at most 8).
+constexpr int AV_T = 256;
+__global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
+    __shared__ float F_s[16], red[AV_T / 64][16];
+    __shared__ float W[AV_T][17];
+    const int unit = blockIdx.x / p.n_ablk, ab = blockIdx.x % p.n_ablk;
+    int sq, g, qt, rows;
+    anc_unit(p, unit, sq, g, qt, rows);
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int64_t a_lo = (int64_t)ab * AV_T;
+    const int64_t a = a_lo + tid;
+    const bool live = a < p.na;
+    const int ns = p.ns;
+    const float* X = p.X + (int64_t)unit * p.na * ns;
+    const float* S = p.S + (int64_t)unit * 16 * p.total_tiles * ns;
+    const float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
+    // ---- 1. the frame
+    float xa[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) xa[r] = live && r < rows ? X[a * ns + r] : -INFINITY;
+    if (tid < 16) {
+        float m = -INFINITY;
+        for (int x = 0; x < p.rec0; ++x) m = fmaxf(m, recs[(int64_t)x * DC_REC + tid]);
+        F_s[tid] = m + 8.f;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float m = xa[r];
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+        if (lane == 0) red[wave][r] = m;
+    }
+    __syncthreads();
+    if (tid < 16) {
+        float m = F_s[tid];
+        for (int w = 0; w < AV_T / 64; ++w) m = fmaxf(m, red[w][tid]);
+        F_s[tid] = tid < rows ? m : 0.f;
+    }
+    __syncthreads();
+    // ---- 2. weights: own + a quarter of each using position's softmax weight (8 gathers in
+    //          flight per thread), and the anchors' own mass
+    float own[16], sh[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        own[r] = r < rows ? fast_exp(xa[r] - F_s[r]) : 0.f;      // exp(-inf) = 0 past the anchors
+        sh[r] = 0.f;
+    }
+    if (live) {
+        const uint32_t* inv = p.inv_pos[sq];
+        const uint32_t e0 = p.inv_off[sq][a], e1 = p.inv_off[sq][a + 1];
+        for (uint32_t e = e0; e < e1; e += 8) {
+            uint32_t pos[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) pos[u] = inv[e + u < e1 ? e + u : e0];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float* sp = S + (int64_t)pos[u] * ns;
+                const bool ok = e + u < e1;
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (r < rows) sh[r] += ok ? fast_exp(sp[r] - F_s[r]) : 0.f;
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) W[tid][r] = own[r] + 0.25f * sh[r];
+    // the anchors' own softmax mass, summed in a fixed order (lanes, then waves)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float l = own[r];
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
+        if (lane == 0) red[wave][r] = l;
+    }
+    __syncthreads();
+    // ---- 3. the value sums: thread -> column c, rows rh, rh + 2, ... (anchors in order)
+    const int c = tid & (D - 1), rh = tid >> 7;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    const uint16_t* va = reinterpret_cast<const uint16_t*>(p.va[sq]);
+    const int nact = (int)min<int64_t>(AV_T, p.na - a_lo);
+    for (int j = 0; j < nact; ++j) {
+        const float v = bf16_to_f32(va[((a_lo + j) * p.G + g) * D + c]);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[k] = fmaf(W[j][rh + 2 * k], v, acc[k]);
+    }
+    // ---- 4. the record: m = F, l = the anchors' own mass, acc in the original space
+    float* rec = p.part + ((int64_t)unit * p.nrec + p.rec0 + ab) * DC_REC;
+    if (tid < 16) {
+        float l = 0.f;
+        for (int w = 0; w < AV_T / 64; ++w) l += red[w][tid];
+        rec[tid] = tid < rows ? F_s[tid] : -INFINITY;
+        rec[16 + tid] = tid < rows ? l : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        const int r = rh + 2 * k;
+        if (r < ((rows + 3) & ~3)) rec[32 + r * D + c] = r < rows ? acc[k] : 0.f;
+    }
+}
+
+// ----------------------------------------------------------------------------------------
 struct DecPlan {
     int nqt, n_chunks, cpw, n_wg, tpw, total_tiles;
+    int nrec, n_ablk, ns;      // records per unit; residual codec: anchor records, score rows
+    int64_t na;
 };
 
 static DecPlan plan_decode(const varrate_shape& sh, int S, int Q) {
     DecPlan pl;
-    const int64_t N = sh.n - sh.w;
+    const int64_t N = coded_count(sh);
     const int rows_total = Q * (sh.H / sh.G);
     pl.nqt = (rows_total + 15) / 16;
     pl.n_chunks = (int)((N + CHUNK - 1) / CHUNK);
@@ -998,6 +1235,10 @@ static DecPlan plan_decode(const varrate_shape& sh, int S, int Q) {
     pl.tpw = (pl.total_tiles + n_wg - 1) / n_wg;
     pl.n_wg = (pl.total_tiles + pl.tpw - 1) / pl.tpw;
     pl.cpw = (pl.tpw + 15) / 16 + 1;    // chunks a tile range can touch
+    pl.na = anchor_count(sh);
+    pl.n_ablk = (int)((pl.na + AV_T - 1) / AV_T);
+    pl.nrec = pl.n_wg + 1 + pl.n_ablk;
+    pl.ns = rows_total < 16 ? (rows_total + 3) & ~3 : 16;
     return pl;
 }
 
@@ -1007,13 +1248,19 @@ size_t decode_units(const varrate_shape& sh, int S, int Q) {
 }
 
 bool decode_supported(const varrate_shape& sh, int S, int Q) {
-    return plan_decode(sh, S, Q).n_wg + 1 <= DC_MAX_REC;
+    return plan_decode(sh, S, Q).nrec <= DC_MAX_REC;
+}
+
+// Residual codec buffers after the records: X [units][na][ns], xbar and S [units][16 tiles][ns]
+static size_t anc_dec_bytes(const DecPlan& pl, size_t units) {
+    if (!pl.na) return 0;
+    return align256(units * pl.na * pl.ns * 4) + 2 * align256(units * 16 * (size_t)pl.total_tiles * pl.ns * 4);
 }
 
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
     DecPlan pl = plan_decode(sh, S, Q);
     const size_t units = (size_t)S * sh.G * pl.nqt;
-    return align256(units * (pl.n_wg + 1) * DC_REC * sizeof(float));
+    return align256(units * pl.nrec * DC_REC * sizeof(float)) + anc_dec_bytes(pl, units);
 }
 
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
@@ -1031,9 +1278,19 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     const int hpg = sh.H / sh.G;
     const int rows_total = Q * hpg;
     const size_t units_all = (size_t)S * sh.G * pl.nqt;
-    if (pl.n_wg + 1 > DC_MAX_REC) return hipErrorInvalidValue;
-    (void)units_all;
+    if (pl.nrec > DC_MAX_REC) return hipErrorInvalidValue;
     float* part = (float*)ws;
+    // residual codec: X, xbar and S after the records
+    float *Xb = nullptr, *xbarb = nullptr, *Sb = nullptr;
+    if (pl.na) {
+        if (reuse_group_region) return hipErrorInvalidValue;   // no fixed scratch for it
+        uint8_t* b = ws + align256(units_all * pl.nrec * DC_REC * sizeof(float));
+        Xb = (float*)b;
+        b += align256(units_all * pl.na * pl.ns * 4);
+        xbarb = (float*)b;
+        b += align256(units_all * 16 * (size_t)pl.total_tiles * pl.ns * 4);
+        Sb = (float*)b;
+    }
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
     const size_t lds = decode_smem_bytes(pl.cpw);
@@ -1057,8 +1314,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         prm.PV = PV;
         // launch groups run in stream order, so with reuse_group_region every group's records
         // go to the start of the buffer (the previous group's merge has finished reading them)
-        prm.part = reuse_group_region ? part : part + (size_t)s0 * sh.G * pl.nqt * (pl.n_wg + 1) * DC_REC;
-        prm.N = sh.n - sh.w;
+        prm.part = reuse_group_region ? part : part + (size_t)s0 * sh.G * pl.nqt * pl.nrec * DC_REC;
+        prm.N = coded_count(sh);
         prm.coef_stride = qb ? qcaches[s0].q_stride / 2 : caches[s0].coef_stride;   // 2-byte units
         prm.cap = caches[s0].cap;
         prm.G = sh.G;
@@ -1072,6 +1329,48 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         prm.tpw = pl.tpw;
         prm.total_tiles = pl.total_tiles;
         prm.units = ns * sh.G * pl.nqt;
+        prm.nrec = pl.nrec;
+        prm.ns = pl.ns;
+        prm.xbar = nullptr;
+        prm.S = nullptr;
+        AncDec ad;
+        if (pl.na) {
+            const size_t u0 = (size_t)s0 * sh.G * pl.nqt;
+            prm.xbar = xbarb + u0 * 16 * pl.total_tiles * pl.ns;
+            prm.S = Sb + u0 * 16 * pl.total_tiles * pl.ns;
+            ad.seq = nullptr;
+            for (int i = 0; i < DC_SEQ; ++i) {
+                const int si = s0 + (i < ns ? i : 0);
+                const varrate_cache& c = caches[si];
+                ad.q[i] = (const uint8_t*)q + si * qstride;
+                ad.ka[i] = c.k_anchor;
+                ad.va[i] = c.v_anchor;
+                ad.snn[i] = c.snn;
+                ad.inv_off[i] = c.inv_off;
+                ad.inv_pos[i] = c.inv_pos;
+            }
+            ad.X = Xb + u0 * pl.na * pl.ns;
+            ad.xbar = const_cast<float*>(prm.xbar);
+            ad.S = prm.S;
+            ad.part = prm.part;
+            ad.N = prm.N;
+            ad.na = pl.na;
+            ad.G = sh.G;
+            ad.H = sh.H;
+            ad.hpg = hpg;
+            ad.nqt = pl.nqt;
+            ad.rows_total = rows_total;
+            ad.ns = pl.ns;
+            ad.total_tiles = pl.total_tiles;
+            ad.nrec = pl.nrec;
+            ad.rec0 = pl.n_wg + 1;
+            ad.ablk = AV_T;
+            ad.n_ablk = pl.n_ablk;
+            anc_qscores<<<(unsigned)(prm.units * ((pl.na + 63) / 64)), 256, 0, st>>>(ad);
+            anc_xbar<<<(unsigned)(prm.units * ((16 * pl.total_tiles + 63) / 64)), 256, 0, st>>>(ad);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
         const unsigned nblk = (unsigned)(prm.units * (pl.n_wg + 1));
         if (sh.dtype != VARRATE_BF16) decode_kernel<true, 0><<<nblk, DC_THREADS, lds, st>>>(prm);
         else if (qb == 3) decode_kernel<false, 3><<<nblk, DC_THREADS, lds, st>>>(prm);
@@ -1080,6 +1379,11 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         else decode_kernel<false, 0><<<nblk, DC_THREADS, lds, st>>>(prm);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
+        if (pl.na) {
+            anc_values<<<(unsigned)(prm.units * pl.n_ablk), AV_T, 0, st>>>(ad);
+            e = hipGetLastError();
+            if (e != hipSuccess) return e;
+        }
         MergeParams mp;
         mp.part = prm.part;
         mp.PV = PV;
@@ -1092,6 +1396,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         mp.rows_total = rows_total;
         mp.n_wg = pl.n_wg;
         mp.rpu = rows_total < 16 ? rows_total : 16;
+        mp.nrec = pl.nrec;
         const unsigned nmerge = (unsigned)(ns * sh.G * pl.nqt * mp.rpu * MG_CB);
         if (sh.dtype == VARRATE_BF16) decode_merge_kernel<false><<<nmerge, MG_THREADS, 0, st>>>(mp);
         else decode_merge_kernel<true><<<nmerge, MG_THREADS, 0, st>>>(mp);

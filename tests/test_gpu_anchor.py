@@ -170,3 +170,86 @@ def test_anchor_encode_given_oracle_salience_and_anchors(vr, oracle_lib, name):
         say(f"  {kind}: beyond-bound {int((~ok).sum())}, identical {float((err == 0).mean()):.4f}, "
             f"max err / S_j {float((err / np.maximum(S, 1e-30)).max()):.3e}")
         assert ok.all()
+
+
+def decode_err(o_gpu, o_or):
+    return max(np.abs(o_gpu[h] - o_or[h]).max() / np.abs(o_or[h]).max() for h in range(o_or.shape[0]))
+
+
+@pytest.mark.parametrize("name,nq", [("llama_8k", 1), ("qwen_16k", 1), ("llama_ragged", 4)])
+def test_anchor_decode(vr, oracle_lib, name, nq):
+    """Decode over the residual-coded cache (anchor-mean score terms, anchor value weights
+    merged by log-sum-exp) against the oracle's reconstruct-in-place decode, the cache built
+    from the oracle's salience and nearest anchors."""
+    import torch
+    cfg, li, ac, shape, cache, PK, PV = encode_with_oracle_inputs(vr, oracle_lib, name, n_queries=nq)
+    out = host(vr.decode(shape, [cache], dev(li.q, torch.bfloat16), PK, PV))
+    torch.cuda.synchronize()
+    worst = max(decode_err(out[i], oracle_lib.decode_anchor(ac, li.PK, li.PV, li.q[i], cfg["H"])) for i in range(nq))
+    say(f"[anchor decode] {name} queries={nq}: worst rel err {worst:.3e}")
+    assert worst <= DEC_TOL_BF16
+
+
+def test_anchor_decode_multi_sequence_appended_and_quantised(vr, oracle_lib):
+    """S = 3 sequences x Q = 5 queries (two row tiles), two tokens appended after compression,
+    then the same caches with 4-bit coefficient codes."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = dict(CONFIGS["llama_32k"])
+    cfg.update(n=1300, G=2, H=8, seed=277)
+    shape = vr.Shape(n=1300, G=2, H=8, w=32, r_min=16, kappa_pct=30, dtype="bf16", anchor_stride=DELTA)
+    Q, extra = 5, 2
+    caches, acs, qs, lis = [], [], [], []
+    for s in range(3):
+        li = make_layer(cfg, seq=s, n_queries=Q, n=1300 + extra)
+        Kc, Vc = li.K[:1300], li.V[:1300]
+        ac = oracle_lib.compress_anchor(Kc, Vc, li.Qw, li.PK, li.PV, 8, 30, 16, "bf16", delta=DELTA)
+        PK, PV = dev(li.PK, torch.float32), dev(li.PV, torch.float32)
+        cache = vr.anchor_encode(shape, dev(Kc, torch.bfloat16), dev(Vc, torch.bfloat16), dev(ac.sbar, torch.float32),
+                                 dev(ac.nn.astype(np.int16), torch.int16), PK, PV, cap=32 + extra)
+        for e in range(extra):
+            vr.append_exact(shape, cache, dev(li.K[1300 + e], torch.bfloat16), dev(li.V[1300 + e], torch.bfloat16))
+        caches.append(cache)
+        acs.append(ac)
+        qs.append(li.q)
+        lis.append(li)
+    q = dev(np.stack(qs), torch.bfloat16)
+    out = host(vr.decode(shape, caches, q, PK, PV))
+    qcs = [vr.quantize(shape, c, 4) for c in caches]
+    outq = host(vr.decode_q(shape, caches, qcs, q, PK, PV))
+    torch.cuda.synchronize()
+    worst = worst_q = 0.0
+    for s in range(3):
+        li, ac = lis[s], acs[s]
+        Kx = np.concatenate([ac.Kx, li.K[1300:]])
+        Vx = np.concatenate([ac.Vx, li.V[1300:]])
+        qk = oracle_lib.quantize(ac.coefK, ac.alloc.rank, 4)
+        qv = oracle_lib.quantize(ac.coefV, ac.alloc.rank, 4)
+        import dataclasses
+        acq = dataclasses.replace(ac, coefK=qk.deq, coefV=qv.deq)
+        for i in range(Q):
+            worst = max(worst, decode_err(out[s][i], oracle_lib.decode_anchor(ac, li.PK, li.PV, li.q[i], 8, Kx, Vx)))
+            worst_q = max(worst_q, decode_err(outq[s][i], oracle_lib.decode_anchor(acq, li.PK, li.PV, li.q[i], 8, Kx, Vx)))
+    say(f"[anchor decode multi] worst rel err {worst:.3e}; 4-bit codes {worst_q:.3e}")
+    assert worst <= DEC_TOL_BF16 and worst_q <= DEC_TOL_BF16
+
+
+@pytest.mark.parametrize("name", ["llama_8k", "qwen_16k"])
+def test_anchor_end_to_end(vr, oracle_lib, name):
+    """GPU compress of the residual codec (salience, anchor search, encode) and decode, against
+    the oracle's own pipeline, fully independent."""
+    import torch
+    cfg, li, ac, shape = prepared(vr, oracle_lib, name, n_queries=2)
+    PK, PV = dev(li.PK, torch.float32), dev(li.PV, torch.float32)
+    sb = torch.empty(shape.n - shape.w, dtype=torch.float32, device="cuda")
+    cache = vr.compress(shape, dev(li.K, torch.bfloat16), dev(li.V, torch.bfloat16), dev(li.Qw, torch.bfloat16),
+                        PK, PV, sbar_out=sb)
+    out = host(vr.decode(shape, [cache], dev(li.q, torch.bfloat16), PK, PV))
+    torch.cuda.synchronize()
+    from test_gpu_parity import check_salience
+    check_salience(host(sb), ac.sbar, f"anchor {name}")
+    mism = int((host(cache.rank).astype(np.int64) != ac.alloc.rank).sum())
+    worst = max(decode_err(out[i], oracle_lib.decode_anchor(ac, li.PK, li.PV, li.q[i], cfg["H"])) for i in range(2))
+    say(f"[anchor end-to-end] {name}: rank mismatches {mism} of {shape.N}; worst decode rel err {worst:.3e}")
+    assert mism <= max(8, shape.N // 1000)
+    assert worst <= DEC_TOL_BF16
