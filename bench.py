@@ -396,6 +396,9 @@ def main():
         qrows, footprint_pct_bf16_coefficients=round(footprint_pct(shape, slots[0], 2 * shape.G * slots[0].B * 2), 2),
         note="group-wise symmetric codes, 32-coordinate groups, binary16 scales; decode_bytes counts "
              "codes + scales + exact rows + metadata + bases; same 32K layer and batch 1")
+    # residual codec (Sec. 3.1 Eq. 2): anchors every 16 tokens kept exact, the other tokens
+    # coded as residuals to their 4 nearest anchors' mean; same layer, budget and floor
+    result["residual_codec"] = bench_anchor(args, shape, Ks, Vs, Qw, q, PK, PV, out, cap_stream)
     if not args.no_stack:
         # the 128K end of the 32K-128K target range: the 32-layer Llama stack, decode at batch 1
         del graphs, step_graphs, slots, Ks, Vs, sbars
@@ -417,6 +420,68 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, li, dbytes, {"decode_ms": ms_dec, "compress_ms": ms_comp})
     print(json.dumps(result), flush=True)
+
+
+def decode_bytes_anchor(shape, cache, n_queries=1):
+    """Algorithmic bytes of a decode over the residual codec: the coded tokens' coefficients,
+    the exact anchor and window rows, ranks, chunk offsets, each stored position's anchors and
+    the anchors' inverse lists, both bases, queries and outputs."""
+    es = 2
+    G, H, d = shape.G, shape.H, 128
+    coef = 2 * G * cache.B * es
+    exact = 2 * G * (cache.n_exact + cache.na) * d * es
+    meta = cache.N + cache.chunk_off.numel() * 4 + cache.N * 8 + cache.N * 16 + (cache.na + 1) * 4
+    return coef + exact + meta + 2 * G * d * d * 4 + 2 * n_queries * H * d * es
+
+
+def bench_anchor(args, shape0, Ks, Vs, Qw, q, PK, PV, out, cap_stream, n_slots=12):
+    """The residual codec on the bench layer: compress (salience, nearest-anchor search,
+    encode) and decode, each replayed from a graph over `n_slots` caches (medians)."""
+    import ctypes
+    import torch
+
+    import paper_2607_15498_amd as vr
+    ash = vr.Shape(n=shape0.n, G=shape0.G, H=shape0.H, w=shape0.w, r_min=shape0.r_min,
+                   kappa_pct=shape0.kappa_pct, dtype=shape0.dtype, anchor_stride=16)
+    dev = Ks[0].device
+    slots = [vr.new_cache(ash, device=dev) for _ in range(n_slots)]
+    wsa = torch.zeros(vr.library().varrate_compress_workspace_bytes(ctypes.byref(ash.c())), dtype=torch.uint8,
+                      device=dev)
+    wsd = vr.decode_workspace(ash, 1, 1, dev)
+    for i, c in enumerate(slots):
+        vr.compress(ash, Ks[i % len(Ks)], Vs[i % len(Vs)], Qw, PK, PV, cache=c, workspace=wsa)
+    torch.cuda.synchronize()
+    gc, gd, gs = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gc, stream=cap_stream):
+        for i, c in enumerate(slots):
+            vr.compress(ash, Ks[i % len(Ks)], Vs[i % len(Vs)], Qw, PK, PV, cache=c, workspace=wsa)
+    with torch.cuda.graph(gd, stream=cap_stream):
+        for i in range(n_slots):
+            vr.decode(ash, [slots[(i + n_slots // 2) % n_slots]], q, PK, PV, out=out, workspace=wsd)
+    with torch.cuda.graph(gs, stream=cap_stream):
+        for i in range(n_slots):
+            vr.anchor_search(ash, Ks[i % len(Ks)], Vs[i % len(Vs)], workspace=wsa)
+    torch.cuda.synchronize()
+    stc = _replay_stats(gc, 3, n_slots)
+    std = _replay_stats(gd, 8, n_slots)
+    sts = _replay_stats(gs, 3, n_slots)
+    by = decode_bytes_anchor(ash, slots[0])
+    full = 2 * ash.n * ash.G * 128 * 2
+    stored = 2 * ash.G * slots[0].B * 2 + 2 * ash.G * (ash.w + slots[0].na) * 128 * 2 + slots[0].N * 9
+    res = {
+        "config": f"anchors every 16 prefix tokens ({slots[0].na}), {slots[0].N} coded tokens, B {slots[0].B}, "
+                  f"budget {ash.kappa_pct}%, r_min {ash.r_min}",
+        "compress_ms_per_32k_tokens": round(stc["p50"] * 32768 / ash.n, 4),
+        "anchor_search_ms": round(sts["p50"], 4),
+        "anchor_search_TFLOPs": round(2.0 * slots[0].N * slots[0].na * 2 * ash.G * 128 / (sts["p50"] * 1e-3) / 1e12, 1),
+        "decode_ms": round(std["p50"], 4), "decode_ms_p10_p90": [round(std["p10"], 4), round(std["p90"], 4)],
+        "decode_GBps": round(by / (std["p50"] * 1e-3) / 1e9, 2),
+        "frac": round(by / (std["p50"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "decode_bytes": int(by),
+        "footprint_pct_of_full_kv": round(100.0 * stored / full, 2),
+    }
+    del gc, gd, gs, slots
+    return res
 
 
 def _graph_ms(g_, reps):

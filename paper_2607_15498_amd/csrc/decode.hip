@@ -252,14 +252,14 @@ __device__ __forceinline__ void anc_scores_out(const TileMeta& tm, int col, int 
 // and the online-softmax rescale is lane-local.  KS and NB bound the tile's largest rank,
 // so every LDS read is unconditional (masked by value) and they all issue before the first
 // wait.
-template <bool F32, bool EXACT, int KS, int NB>
+template <bool F32, bool EXACT, int KS, int NB, bool ANC = false>
 __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, const typename Elem<F32>::T* sK,
                                           const typename Elem<F32>::T* sV, const u32x4* qf,
                                           const u32x4* kmask, int lane, int grp, float& m_run,
                                           float& l_part) {
     const int col = lane & 15;
-    float xv[4];
-    anc_scores_in(tm, col, grp, xv);
+    float xv[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (ANC) anc_scores_in(tm, col, grp, xv);
     // K rows of a coded tile are m coordinates apart (exact rows: 128) with zeros past each
     // position's rank; a row piece past the row's end (into the next row, the pad or the LDS
     // arrays after the stage) is masked.  V blocks are coordinate-major (coded) or row-major
@@ -341,7 +341,7 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
     float sv[4];
 #pragma unroll
     for (int v = 0; v < 4; ++v) sv[v] = sc[v] + xv[v];
-    anc_scores_out(tm, col, grp, sv);
+    if constexpr (ANC) anc_scores_out(tm, col, grp, sv);
     if (partial) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) sv[v] = tm.i0 + 4 * grp + v < tm.T ? sv[v] : -INFINITY;
@@ -417,14 +417,14 @@ template <> __device__ __forceinline__ void acc_mfma_q<8>(const u32x2* vh, const
 // (32 coordinates) per step, and each step's result is scaled by the K scales of the four
 // tokens a lane holds.  Values: the codes are the A operand as they are, and the scale of
 // each token's V group goes into the B operand (softmax weight x scale, one bf16 rounding).
-template <int QB, int KS, int NB>
+template <int QB, int KS, int NB, bool ANC>
 __device__ __forceinline__ void tile_step_q(const TileMeta& tm, bool partial, const uint16_t* sK,
                                             const uint16_t* sV, const u32x4* qf, int lane, int grp,
                                             float& m_run, float& l_part) {
     const int col = lane & 15;
     const int mq = tm.m;
-    float xv[4];
-    anc_scores_in(tm, col, grp, xv);
+    float xv[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (ANC) anc_scores_in(tm, col, grp, xv);
     const uint32_t* wk = reinterpret_cast<const uint32_t*>(sK + tm.base);   // 16-byte aligned
     const uint32_t* wv = reinterpret_cast<const uint32_t*>(sV + tm.base);
     const int sco = mq * QB;                        // scales after the codes, 2-byte units
@@ -462,7 +462,7 @@ __device__ __forceinline__ void tile_step_q(const TileMeta& tm, bool partial, co
     float sv[4];
 #pragma unroll
     for (int v = 0; v < 4; ++v) sv[v] = sc[v] + xv[v];
-    anc_scores_out(tm, col, grp, sv);
+    if constexpr (ANC) anc_scores_out(tm, col, grp, sv);
     if (partial) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) sv[v] = tm.i0 + 4 * grp + v < tm.T ? sv[v] : -INFINITY;
@@ -514,7 +514,7 @@ __device__ __forceinline__ void tile_step_q(const TileMeta& tm, bool partial, co
 
 // QB = 0: coefficients stored in the layer's dtype; QB = 3, 4, 8: b-bit codes with binary16
 // group scales (bf16 layers only).
-template <bool F32, int QB>
+template <bool F32, int QB, bool ANC>
 __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel(DecParams p) {
     static_assert(QB == 0 || !F32, "quantised coefficients come from bf16 layers");
     typedef typename Elem<F32>::T ET;
@@ -773,7 +773,7 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
             tm.xb = nullptr;
             tm.sw = nullptr;
             tm.ns = p.ns;
-            if (!exact && p.xbar) {
+            if (ANC && !exact) {
                 const int64_t o = ((int64_t)unit * p.total_tiles + tile) * 16 * p.ns;
                 tm.xb = p.xbar + o;
                 tm.sw = p.S + o;
@@ -797,15 +797,15 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
                 if constexpr (QB != 0) {
                     const uint16_t* qK = reinterpret_cast<const uint16_t*>(sK);
                     const uint16_t* qV = reinterpret_cast<const uint16_t*>(sV);
-                    if (tm.m <= 16) tile_step_q<QB, 1, 1>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
-                    else if (tm.m <= 32) tile_step_q<QB, 1, 2>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
-                    else if (tm.m <= 64) tile_step_q<QB, 2, 4>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
-                    else tile_step_q<QB, 4, 8>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                    if (tm.m <= 16) tile_step_q<QB, 1, 1, ANC>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                    else if (tm.m <= 32) tile_step_q<QB, 1, 2, ANC>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                    else if (tm.m <= 64) tile_step_q<QB, 2, 4, ANC>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
+                    else tile_step_q<QB, 4, 8, ANC>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
                 } else {
-                    if (tm.m <= 16) tile_step<F32, false, 1, 1>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
-                    else if (tm.m <= 32) tile_step<F32, false, 1, 2>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
-                    else if (tm.m <= 64) tile_step<F32, false, 2, 4>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
-                    else tile_step<F32, false, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                    if (tm.m <= 16) tile_step<F32, false, 1, 1, ANC>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                    else if (tm.m <= 32) tile_step<F32, false, 1, 2, ANC>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                    else if (tm.m <= 64) tile_step<F32, false, 2, 4, ANC>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
+                    else tile_step<F32, false, 4, 8, ANC>(tm, partial, sK, sV, sm.qf, sm.kmask, ln, grp, m_run, l_part);
                 }
             }
         }
@@ -1104,25 +1104,39 @@ __global__ __launch_bounds__(256) void anc_xbar(AncDec p) {
         xb[r] = (((X[a0 * p.ns + r] + X[a1 * p.ns + r]) + X[a2 * p.ns + r]) + X[a3 * p.ns + r]) * 0.25f;
 }
 
-// One thread per anchor (256 per workgroup), all rows at once.  The frame F[row] is an upper
-// bound of every score the block touches without a pass over the lists: the largest of its
-// anchors' own scores and of the streaming records' running maxima + 8 (each coded score
-// exceeds its workgroup's running maximum by at most 8).
+// A workgroup per (unit, block of AV_A anchors), four threads per anchor (each a quarter of
+// its list), all rows at once.  The frame F[row] is an upper bound of every score the block
+// touches without a pass over the lists: the largest of its anchors' own scores and of the
+// streaming records' running maxima + 8 (each coded score exceeds its workgroup's running
+// maximum by at most 8).  The block's value rows are staged in LDS for the value sums.
 constexpr int AV_T = 256;
+constexpr int AV_A = 64;                          // anchors per workgroup
 __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
     __shared__ float F_s[16], red[AV_T / 64][16];
-    __shared__ float W[AV_T][17];
+    __shared__ float W4[AV_T][17];                // per (anchor, quarter): partial weights
+    __shared__ float W[AV_A][17];
+    __shared__ __attribute__((aligned(16))) uint16_t vrow[AV_A][D];
     const int unit = blockIdx.x / p.n_ablk, ab = blockIdx.x % p.n_ablk;
     int sq, g, qt, rows;
     anc_unit(p, unit, sq, g, qt, rows);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int64_t a_lo = (int64_t)ab * AV_T;
-    const int64_t a = a_lo + tid;
-    const bool live = a < p.na;
+    const int slot = tid >> 2, quarter = tid & 3;
+    const int64_t a_lo = (int64_t)ab * AV_A;
+    const int nact = (int)min<int64_t>(AV_A, p.na - a_lo);
+    const int64_t a = a_lo + slot;
+    const bool live = slot < nact;
     const int ns = p.ns;
     const float* X = p.X + (int64_t)unit * p.na * ns;
     const float* S = p.S + (int64_t)unit * 16 * p.total_tiles * ns;
     const float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
+    // the block's value rows into LDS (16-byte pieces, all in flight together)
+    {
+        const uint16_t* va = reinterpret_cast<const uint16_t*>(p.va[sq]);
+        for (int k = tid; k < nact * (D / 8); k += AV_T) {
+            const int j = k / (D / 8), e = 8 * (k % (D / 8));
+            *reinterpret_cast<u32x4*>(&vrow[j][e]) = load16(va + ((a_lo + j) * p.G + g) * D + e);
+        }
+    }
     // ---- 1. the frame
     float xa[16];
 #pragma unroll
@@ -1146,25 +1160,21 @@ __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
         F_s[tid] = tid < rows ? m : 0.f;
     }
     __syncthreads();
-    // ---- 2. weights: own + a quarter of each using position's softmax weight (8 gathers in
-    //          flight per thread), and the anchors' own mass
-    float own[16], sh[16];
+    // ---- 2. weights: each quarter of the anchor's list (4 gathers in flight per thread)
+    float sh[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        own[r] = r < rows ? fast_exp(xa[r] - F_s[r]) : 0.f;      // exp(-inf) = 0 past the anchors
-        sh[r] = 0.f;
-    }
+    for (int r = 0; r < 16; ++r) sh[r] = 0.f;
     if (live) {
         const uint32_t* inv = p.inv_pos[sq];
         const uint32_t e0 = p.inv_off[sq][a], e1 = p.inv_off[sq][a + 1];
-        for (uint32_t e = e0; e < e1; e += 8) {
-            uint32_t pos[8];
+        for (uint32_t e = e0 + quarter; e < e1; e += 16) {
+            uint32_t pos[4];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) pos[u] = inv[e + u < e1 ? e + u : e0];
+            for (int u = 0; u < 4; ++u) pos[u] = inv[e + 4 * u < e1 ? e + 4 * u : e];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
+            for (int u = 0; u < 4; ++u) {
                 const float* sp = S + (int64_t)pos[u] * ns;
-                const bool ok = e + u < e1;
+                const bool ok = e + 4 * u < e1;
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     if (r < rows) sh[r] += ok ? fast_exp(sp[r] - F_s[r]) : 0.f;
@@ -1172,33 +1182,47 @@ __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
         }
     }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) W[tid][r] = own[r] + 0.25f * sh[r];
-    // the anchors' own softmax mass, summed in a fixed order (lanes, then waves)
+    for (int r = 0; r < 16; ++r) W4[tid][r] = sh[r];
+    __syncthreads();
+    // the anchor's weight: own + a quarter of the quarters' sums (fixed order); own mass
+    float own_l[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        float l = own[r];
+    for (int r = 0; r < 16; ++r) own_l[r] = 0.f;
+    if (tid < AV_A) {
+        const int j = tid;
+        const bool lv = j < nact;
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
-        if (lane == 0) red[wave][r] = l;
+        for (int r = 0; r < 16; ++r) {
+            const float own = lv && r < rows ? fast_exp(X[(a_lo + j) * ns + r] - F_s[r]) : 0.f;
+            const float shr = ((W4[4 * j][r] + W4[4 * j + 1][r]) + W4[4 * j + 2][r]) + W4[4 * j + 3][r];
+            W[j][r] = own + 0.25f * shr;
+            own_l[r] = own;
+        }
+    }
+    // the anchors' own softmax mass, summed in a fixed order (lanes of wave 0)
+    if (wave == 0) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float l = own_l[r];
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
+            if (lane == 0) red[0][r] = l;
+        }
     }
     __syncthreads();
     // ---- 3. the value sums: thread -> column c, rows rh, rh + 2, ... (anchors in order)
     const int c = tid & (D - 1), rh = tid >> 7;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    const uint16_t* va = reinterpret_cast<const uint16_t*>(p.va[sq]);
-    const int nact = (int)min<int64_t>(AV_T, p.na - a_lo);
     for (int j = 0; j < nact; ++j) {
-        const float v = bf16_to_f32(va[((a_lo + j) * p.G + g) * D + c]);
+        const float v = bf16_to_f32(vrow[j][c]);
 #pragma unroll
         for (int k = 0; k < 8; ++k) acc[k] = fmaf(W[j][rh + 2 * k], v, acc[k]);
     }
     // ---- 4. the record: m = F, l = the anchors' own mass, acc in the original space
     float* rec = p.part + ((int64_t)unit * p.nrec + p.rec0 + ab) * DC_REC;
     if (tid < 16) {
-        float l = 0.f;
-        for (int w = 0; w < AV_T / 64; ++w) l += red[w][tid];
         rec[tid] = tid < rows ? F_s[tid] : -INFINITY;
-        rec[16 + tid] = tid < rows ? l : 0.f;
+        rec[16 + tid] = tid < rows ? red[0][tid] : 0.f;
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -1236,7 +1260,7 @@ static DecPlan plan_decode(const varrate_shape& sh, int S, int Q) {
     pl.n_wg = (pl.total_tiles + pl.tpw - 1) / pl.tpw;
     pl.cpw = (pl.tpw + 15) / 16 + 1;    // chunks a tile range can touch
     pl.na = anchor_count(sh);
-    pl.n_ablk = (int)((pl.na + AV_T - 1) / AV_T);
+    pl.n_ablk = (int)((pl.na + AV_A - 1) / AV_A);
     pl.nrec = pl.n_wg + 1 + pl.n_ablk;
     pl.ns = rows_total < 16 ? (rows_total + 3) & ~3 : 16;
     return pl;
@@ -1270,11 +1294,14 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     const int qb = qcaches ? qcaches[0].bits : 0;
     if (qb != 0 && qb != 3 && qb != 4 && qb != 8) return hipErrorInvalidValue;
     if (qb != 0 && sh.dtype != VARRATE_BF16) return hipErrorInvalidValue;
-    const void* kfn = sh.dtype != VARRATE_BF16 ? (const void*)decode_kernel<true, 0>
-                      : qb == 3 ? (const void*)decode_kernel<false, 3>
-                      : qb == 4 ? (const void*)decode_kernel<false, 4>
-                      : qb == 8 ? (const void*)decode_kernel<false, 8>
-                                : (const void*)decode_kernel<false, 0>;
+    const bool anc = pl.na > 0;
+    typedef void (*DecFn)(DecParams);
+    DecFn kfn;
+    if (sh.dtype != VARRATE_BF16) kfn = decode_kernel<true, 0, false>;
+    else if (!anc) kfn = qb == 3 ? decode_kernel<false, 3, false> : qb == 4 ? decode_kernel<false, 4, false>
+                       : qb == 8 ? decode_kernel<false, 8, false> : decode_kernel<false, 0, false>;
+    else kfn = qb == 3 ? decode_kernel<false, 3, true> : qb == 4 ? decode_kernel<false, 4, true>
+             : qb == 8 ? decode_kernel<false, 8, true> : decode_kernel<false, 0, true>;
     const int hpg = sh.H / sh.G;
     const int rows_total = Q * hpg;
     const size_t units_all = (size_t)S * sh.G * pl.nqt;
@@ -1282,7 +1309,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     float* part = (float*)ws;
     // residual codec: X, xbar and S after the records
     float *Xb = nullptr, *xbarb = nullptr, *Sb = nullptr;
-    if (pl.na) {
+    if (anc) {
         if (reuse_group_region) return hipErrorInvalidValue;   // no fixed scratch for it
         uint8_t* b = ws + align256(units_all * pl.nrec * DC_REC * sizeof(float));
         Xb = (float*)b;
@@ -1294,7 +1321,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
     const size_t lds = decode_smem_bytes(pl.cpw);
-    hipError_t e = ensure_lds_limit(kfn, lds);
+    hipError_t e = ensure_lds_limit((const void*)kfn, lds);
     if (e != hipSuccess) return e;
     for (int s0 = 0; s0 < S; s0 += DC_SEQ) {
         const int ns = S - s0 < DC_SEQ ? S - s0 : DC_SEQ;
@@ -1364,7 +1391,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
             ad.total_tiles = pl.total_tiles;
             ad.nrec = pl.nrec;
             ad.rec0 = pl.n_wg + 1;
-            ad.ablk = AV_T;
+            ad.ablk = AV_A;
             ad.n_ablk = pl.n_ablk;
             anc_qscores<<<(unsigned)(prm.units * ((pl.na + 63) / 64)), 256, 0, st>>>(ad);
             anc_xbar<<<(unsigned)(prm.units * ((16 * pl.total_tiles + 63) / 64)), 256, 0, st>>>(ad);
@@ -1372,11 +1399,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
             if (e != hipSuccess) return e;
         }
         const unsigned nblk = (unsigned)(prm.units * (pl.n_wg + 1));
-        if (sh.dtype != VARRATE_BF16) decode_kernel<true, 0><<<nblk, DC_THREADS, lds, st>>>(prm);
-        else if (qb == 3) decode_kernel<false, 3><<<nblk, DC_THREADS, lds, st>>>(prm);
-        else if (qb == 4) decode_kernel<false, 4><<<nblk, DC_THREADS, lds, st>>>(prm);
-        else if (qb == 8) decode_kernel<false, 8><<<nblk, DC_THREADS, lds, st>>>(prm);
-        else decode_kernel<false, 0><<<nblk, DC_THREADS, lds, st>>>(prm);
+        kfn<<<nblk, DC_THREADS, lds, st>>>(prm);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (pl.na) {

@@ -134,8 +134,10 @@ def test_decode_accumulator_agprs_are_private():
         assert r.returncode == 0, r.stdout[-2000:]
         text = open(out).read()
     agpr = re.compile(r"\ba\d+\b|\ba\[\d+:\d+\]|v_accvgpr")
-    kernels = re.findall(r"^(_ZN2vr13decode_kernelILb[01]ELi\d+EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm", text, re.S | re.M)
-    assert len(kernels) == 5          # fp32, bf16, and bf16 with 3-, 4- and 8-bit codes
+    kernels = re.findall(r"^(_ZN2vr13decode_kernelILb[01]ELi\d+ELb[01]EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm",
+                         text, re.S | re.M)
+    # fp32; bf16 and bf16 with 3-, 4- and 8-bit codes, each with and without anchors
+    assert len(kernels) == 9
     for name, body in kernels:
         inside = False
         for line in body.splitlines():
