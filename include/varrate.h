@@ -135,6 +135,9 @@ typedef struct varrate_cache {
     uint32_t* inv_off;      /* [na + 1] start of each anchor's list in inv_pos              */
     uint32_t* inv_pos;      /* [4 N] stored positions whose nearest anchors include anchor a,
                                at inv_pos[inv_off[a] .. inv_off[a + 1])                    */
+    uint32_t* piece_off;    /* [na + 1] each anchor's list cut into pieces of 64 entries: the
+                               pieces of anchor a are piece_off[a] .. piece_off[a + 1] - 1  */
+    uint16_t* piece_anchor; /* [4 N / 64 + na] the anchor of each piece                     */
     int64_t   na;           /* anchors                                                      */
 } varrate_cache;
 
@@ -144,6 +147,7 @@ typedef struct varrate_cache_bytes_t {
     size_t coef_k, coef_v, rank, srank, sidx, chunk_off, k_exact, v_exact;
     int64_t na;                                      /* residual codec: anchors (else 0)       */
     size_t k_anchor, v_anchor, snn, inv_off, inv_pos; /* residual codec buffers (else 0)       */
+    size_t piece_off, piece_anchor;
 } varrate_cache_bytes_t;
 
 /* ---- diagnostics ---------------------------------------------------------------------- */

@@ -93,6 +93,8 @@ class Cache:
     snn: Optional[torch.Tensor] = None          # [N][4] int16 anchor numbers (stored order)
     inv_off: Optional[torch.Tensor] = None      # [na + 1] int32
     inv_pos: Optional[torch.Tensor] = None      # [4 N] int32
+    piece_off: Optional[torch.Tensor] = None    # [na + 1] int32
+    piece_anchor: Optional[torch.Tensor] = None  # [4 N / 64 + na] int16
     na: int = 0
 
     def c(self) -> _lib.CacheC:
@@ -101,7 +103,8 @@ class Cache:
                            self.srank.data_ptr(), self.sidx.data_ptr(), self.chunk_off.data_ptr(),
                            self.k_exact.data_ptr(), self.v_exact.data_ptr(), self.coef_stride,
                            self.cap, self.n_exact, self.N, self.B, ptr(self.k_anchor), ptr(self.v_anchor),
-                           ptr(self.snn), ptr(self.inv_off), ptr(self.inv_pos), self.na)
+                           ptr(self.snn), ptr(self.inv_off), ptr(self.inv_pos), ptr(self.piece_off),
+                           ptr(self.piece_anchor), self.na)
 
     def _update(self, cc: _lib.CacheC):
         self.n_exact, self.N, self.B, self.na = int(cc.n_exact), int(cc.N), int(cc.B), int(cc.na)
@@ -138,6 +141,8 @@ def new_cache(shape: Shape, cap: Optional[int] = None, device="cuda") -> Cache:
         snn=torch.zeros((b.N, 4), dtype=torch.int16, device=device) if b.na else None,
         inv_off=torch.zeros(b.na + 1, dtype=torch.int32, device=device) if b.na else None,
         inv_pos=torch.zeros(4 * b.N, dtype=torch.int32, device=device) if b.na else None,
+        piece_off=torch.zeros(b.na + 1, dtype=torch.int32, device=device) if b.na else None,
+        piece_anchor=torch.zeros(4 * b.N // 64 + b.na, dtype=torch.int16, device=device) if b.na else None,
         na=int(b.na))
 
 

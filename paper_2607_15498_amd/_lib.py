@@ -40,7 +40,8 @@ class CacheC(ctypes.Structure):
                 ("coef_stride", ctypes.c_int64), ("cap", ctypes.c_int64), ("n_exact", ctypes.c_int64),
                 ("N", ctypes.c_int64), ("B", ctypes.c_int64),
                 ("k_anchor", ctypes.c_void_p), ("v_anchor", ctypes.c_void_p), ("snn", ctypes.c_void_p),
-                ("inv_off", ctypes.c_void_p), ("inv_pos", ctypes.c_void_p), ("na", ctypes.c_int64)]
+                ("inv_off", ctypes.c_void_p), ("inv_pos", ctypes.c_void_p), ("piece_off", ctypes.c_void_p),
+                ("piece_anchor", ctypes.c_void_p), ("na", ctypes.c_int64)]
 
 
 class QCacheC(ctypes.Structure):
@@ -54,7 +55,8 @@ class CacheBytes(ctypes.Structure):
                [(k, ctypes.c_size_t) for k in ("coef_k", "coef_v", "rank", "srank", "sidx",
                                                "chunk_off", "k_exact", "v_exact")] + \
                [("na", ctypes.c_int64)] + \
-               [(k, ctypes.c_size_t) for k in ("k_anchor", "v_anchor", "snn", "inv_off", "inv_pos")]
+               [(k, ctypes.c_size_t) for k in ("k_anchor", "v_anchor", "snn", "inv_off", "inv_pos", "piece_off",
+                                               "piece_anchor")]
 
 
 _lib = None

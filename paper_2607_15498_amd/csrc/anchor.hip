@@ -17,8 +17,9 @@
 //   anc_prep     coded salience gathered from the prefix's, residuals k_t - mean, v_t - mean
 //                (fp32, stored in the layer's dtype) followed by the window rows, and the
 //                anchor rows copied to their store
-//   anc_lists    after the allocation: the anchors of each stored position, and per anchor
-//                the stored positions that use it (counts, scan, fill)
+//   anc_lists    after the allocation: the anchors of each stored position, per anchor the
+//                stored positions that use it (counts, scan, fill), and those lists cut into
+//                pieces of 64 entries (hub anchors are used by most tokens)
 #include "vr_internal.h"
 
 namespace vr {
@@ -295,6 +296,19 @@ __global__ __launch_bounds__(256) void anc_fill(const uint16_t* __restrict__ snn
     }
 }
 
+// pieces of 64 entries per anchor list (hub anchors, used by a large share of the tokens,
+// have long lists): counts, then (after a scan into piece_off) each piece's anchor
+__global__ __launch_bounds__(256) void anc_pcount(const uint32_t* __restrict__ off, int64_t na, uint32_t* __restrict__ cnt) {
+    const int64_t a = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (a < na) cnt[a] = (off[a + 1] - off[a] + 63) / 64;
+}
+__global__ __launch_bounds__(256) void anc_pfill(const uint32_t* __restrict__ poff, int64_t na,
+                                                uint16_t* __restrict__ panchor) {
+    const int64_t a = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (a >= na) return;
+    for (uint32_t k = poff[a]; k < poff[a + 1]; ++k) panchor[k] = (uint16_t)a;
+}
+
 __global__ void anc_zero(uint32_t* __restrict__ x, int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) x[i] = 0u;
@@ -372,6 +386,9 @@ hipError_t launch_anchor_encode(const varrate_shape& sh, const void* K, const vo
     anc_count<<<(unsigned)((Nc + 255) / 256), 256, 0, st>>>(c.sidx, nn, Nc, c.snn, w.cnt);
     anc_scan<<<1, 1024, 0, st>>>(w.cnt, na, c.inv_off);
     anc_fill<<<(unsigned)((Nc + 255) / 256), 256, 0, st>>>(c.snn, Nc, w.cnt, c.inv_pos);
+    anc_pcount<<<(unsigned)((na + 255) / 256), 256, 0, st>>>(c.inv_off, na, w.cnt);
+    anc_scan<<<1, 1024, 0, st>>>(w.cnt, na, c.piece_off);
+    anc_pfill<<<(unsigned)((na + 255) / 256), 256, 0, st>>>(c.piece_off, na, c.piece_anchor);
     return hipGetLastError();
 }
 

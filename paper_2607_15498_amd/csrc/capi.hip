@@ -91,7 +91,8 @@ int check_shape(const varrate_shape* sh) {
 int check_cache(const varrate_shape* sh, const varrate_cache* c, bool need_layout) {
     if (!c) return fail(VARRATE_EINVAL, "cache is NULL");
     const int64_t B = coded_budget(*sh);
-    if (sh->anchor_stride != 0 && (!c->k_anchor || !c->v_anchor || !c->snn || !c->inv_off || !c->inv_pos))
+    if (sh->anchor_stride != 0 && (!c->k_anchor || !c->v_anchor || !c->snn || !c->inv_off || !c->inv_pos ||
+                                   !c->piece_off || !c->piece_anchor))
         return fail(VARRATE_EINVAL, "cache has a NULL anchor buffer");
     if (sh->anchor_stride != 0 && (!aligned16(c->k_anchor) || !aligned16(c->v_anchor)))
         return fail(VARRATE_EINVAL, "anchor buffers must be 16-byte aligned");
@@ -151,6 +152,8 @@ int varrate_cache_bytes(const varrate_shape* sh, int64_t cap, varrate_cache_byte
     out->snn = out->na ? (size_t)out->N * 4 * 2 : 0;
     out->inv_off = out->na ? (size_t)(out->na + 1) * 4 : 0;
     out->inv_pos = out->na ? (size_t)out->N * 4 * 4 : 0;
+    out->piece_off = out->inv_off;
+    out->piece_anchor = out->na ? (size_t)(out->N * 4 / 64 + out->na) * 2 : 0;
     out->n_chunks = (out->N + VARRATE_CHUNK - 1) / VARRATE_CHUNK;
     // tile rectangles: a chunk's 16 tiles take at most its ranks + 16 x 128 elements
     const int64_t bound = out->B + (int64_t)8 * VARRATE_CHUNK * out->n_chunks;

@@ -1022,10 +1022,11 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
 //   anc_xbar     xbar[unit][pos][row] = (1/4) sum of X over the stored position's anchors, the
 //                term the streaming kernel adds to each coded score (it also writes the final
 //                scores S[unit][pos][row])
+//   anc_pieces   per piece of an anchor's list (64 entries): sum of exp(S - F)
 //   anc_values   one record per (unit, block of anchors) in the original space: for its
 //                anchors, W_a = exp(X_a - F) + (1/4) sum over the positions that use a of
-//                exp(S - F) (the inverse lists), acc = sum W_a v_a, l = sum exp(X_a - F),
-//                m = F (the block's largest score); the merge combines these with the others
+//                exp(S - F) (its pieces), acc = sum W_a v_a, l = sum exp(X_a - F), m = F
+//                (a bound of every score involved); the merge combines these with the others
 //                by log-sum-exp like the exact record.
 struct AncDec {
     const varrate_cache* seq;   // unused on the device
@@ -1035,7 +1036,12 @@ struct AncDec {
     const uint16_t* snn[DC_SEQ];
     const uint32_t* inv_off[DC_SEQ];
     const uint32_t* inv_pos[DC_SEQ];
+    const uint32_t* piece_off[DC_SEQ];
+    const uint16_t* piece_anchor[DC_SEQ];
     float* X;          // [unit][na][ns]
+    float* XM;         // [unit][ceil(na / 64)][ns] block maxima of X
+    float* PW;         // [unit][np_bound][ns] per-piece sums of exp(S - F)
+    int64_t np_bound;  // pieces per unit at most: 4 N / 64 + na
     float* xbar;       // [unit][16 total_tiles][ns]
     float* S;          // [unit][16 total_tiles][ns]
     float* part;       // records [unit][nrec][DC_REC]
@@ -1082,6 +1088,21 @@ __global__ __launch_bounds__(256) void anc_qscores(AncDec p) {
     }
 }
 
+// the block maxima of X (per row), for the frame of the anchor weights
+__global__ __launch_bounds__(256) void anc_xmax(AncDec p) {
+    const int blocks = (int)((p.na + 63) / 64);
+    const int unit = blockIdx.x / blocks, ab = blockIdx.x % blocks;
+    const int lane = threadIdx.x & 63, r = threadIdx.x >> 6;   // 4 waves: rows r, r + 4, ...
+    const int64_t a = (int64_t)ab * 64 + lane;
+    const float* X = p.X + (int64_t)unit * p.na * p.ns;
+    for (int rr = r; rr < p.ns; rr += 4) {
+        float m = a < p.na ? X[a * p.ns + rr] : -INFINITY;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+        if (lane == 0) p.XM[((int64_t)unit * blocks + ab) * p.ns + rr] = m;
+    }
+}
+
 // one thread per (stored position, row group)
 __global__ __launch_bounds__(256) void anc_xbar(AncDec p) {
     const int npos = 16 * p.total_tiles;
@@ -1104,31 +1125,85 @@ __global__ __launch_bounds__(256) void anc_xbar(AncDec p) {
         xb[r] = (((X[a0 * p.ns + r] + X[a1 * p.ns + r]) + X[a2 * p.ns + r]) + X[a3 * p.ns + r]) * 0.25f;
 }
 
-// A workgroup per (unit, block of AV_A anchors), four threads per anchor (each a quarter of
-// its list), all rows at once.  The frame F[row] is an upper bound of every score the block
-// touches without a pass over the lists: the largest of its anchors' own scores and of the
-// streaming records' running maxima + 8 (each coded score exceeds its workgroup's running
-// maximum by at most 8).  The block's value rows are staged in LDS for the value sums.
+// The frame F[row] of the anchor weights: an upper bound of every score they involve, the
+// largest of the anchors' own scores and of the streaming records' running maxima + 8 (each
+// coded score exceeds its workgroup's running maximum by at most 8).  Computed the same way
+// (same order) wherever it is needed, into F_s[16].
+__device__ __forceinline__ void anc_frame(const AncDec& p, int unit, int rows, float* F_s) {
+    const int tid = threadIdx.x;
+    if (tid < 16) {
+        const float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
+        const int xb = (int)((p.na + 63) / 64);
+        const float* XM = p.XM + (int64_t)unit * xb * p.ns;
+        float m = -INFINITY, mx = -INFINITY;
+        if (tid < rows) {
+            for (int x = 0; x < p.rec0; ++x) m = fmaxf(m, recs[(int64_t)x * DC_REC + tid]);
+            for (int b = 0; b < xb; ++b) mx = fmaxf(mx, XM[b * p.ns + tid]);
+        }
+        F_s[tid] = tid < rows ? fmaxf(m + 8.f, mx) : 0.f;
+    }
+    __syncthreads();
+}
+
+// one thread per list piece (at most 64 entries): PW = sum of exp(S - F) over the piece
+constexpr int AP_T = 256;
+__global__ __launch_bounds__(AP_T) void anc_pieces(AncDec p) {
+    __shared__ float F_s[16];
+    const int blocks = (int)((p.np_bound + AP_T - 1) / AP_T);
+    const int unit = blockIdx.x / blocks, pb = blockIdx.x % blocks;
+    int sq, g, qt, rows;
+    anc_unit(p, unit, sq, g, qt, rows);
+    anc_frame(p, unit, rows, F_s);
+    const int64_t P = (int64_t)pb * AP_T + threadIdx.x;
+    const uint32_t npieces = p.piece_off[sq][p.na];
+    if (P >= (int64_t)npieces) return;
+    const int ns = p.ns;
+    const uint32_t a = p.piece_anchor[sq][P];
+    const uint32_t j = (uint32_t)P - p.piece_off[sq][a];
+    const uint32_t e0 = p.inv_off[sq][a] + 64 * j;
+    const uint32_t e1 = min(p.inv_off[sq][a + 1], e0 + 64);
+    const uint32_t* inv = p.inv_pos[sq];
+    const float* S = p.S + (int64_t)unit * 16 * p.total_tiles * ns;
+    float sh[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sh[r] = 0.f;
+    for (uint32_t e = e0; e < e1; e += 8) {
+        uint32_t pos[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) pos[u] = inv[e + u < e1 ? e + u : e0];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const float* sp = S + (int64_t)pos[u] * ns;
+            const bool ok = e + u < e1;
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                if (r < rows) sh[r] += ok ? fast_exp(sp[r] - F_s[r]) : 0.f;
+        }
+    }
+    float* pw = p.PW + ((int64_t)unit * p.np_bound + P) * ns;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+        if (r < ns) pw[r] = sh[r];
+}
+
+// A workgroup per (unit, block of AV_A anchors): each anchor's weight W_a = exp(X_a - F) +
+// (1/4) sum of its pieces' PW (a wave per anchor: lanes take every 64th piece, then a fixed
+// butterfly), then the value sums over the block's anchors (value rows staged in LDS).
 constexpr int AV_T = 256;
 constexpr int AV_A = 64;                          // anchors per workgroup
 __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
-    __shared__ float F_s[16], red[AV_T / 64][16];
-    __shared__ float W4[AV_T][17];                // per (anchor, quarter): partial weights
+    __shared__ float F_s[16], red[16];
     __shared__ float W[AV_A][17];
+    __shared__ float own_s[AV_A][17];
     __shared__ __attribute__((aligned(16))) uint16_t vrow[AV_A][D];
     const int unit = blockIdx.x / p.n_ablk, ab = blockIdx.x % p.n_ablk;
     int sq, g, qt, rows;
     anc_unit(p, unit, sq, g, qt, rows);
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-    const int slot = tid >> 2, quarter = tid & 3;
     const int64_t a_lo = (int64_t)ab * AV_A;
     const int nact = (int)min<int64_t>(AV_A, p.na - a_lo);
-    const int64_t a = a_lo + slot;
-    const bool live = slot < nact;
     const int ns = p.ns;
     const float* X = p.X + (int64_t)unit * p.na * ns;
-    const float* S = p.S + (int64_t)unit * 16 * p.total_tiles * ns;
-    const float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
     // the block's value rows into LDS (16-byte pieces, all in flight together)
     {
         const uint16_t* va = reinterpret_cast<const uint16_t*>(p.va[sq]);
@@ -1137,80 +1212,49 @@ __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
             *reinterpret_cast<u32x4*>(&vrow[j][e]) = load16(va + ((a_lo + j) * p.G + g) * D + e);
         }
     }
-    // ---- 1. the frame
-    float xa[16];
+    anc_frame(p, unit, rows, F_s);
+    // ---- weights: wave w takes anchors w, w + 4, ...
+    const uint32_t* poff = p.piece_off[sq];
+    const float* PW = p.PW + (int64_t)unit * p.np_bound * ns;
+    for (int j = wave; j < AV_A; j += AV_T / 64) {
+        float sh[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) xa[r] = live && r < rows ? X[a * ns + r] : -INFINITY;
-    if (tid < 16) {
-        float m = -INFINITY;
-        for (int x = 0; x < p.rec0; ++x) m = fmaxf(m, recs[(int64_t)x * DC_REC + tid]);
-        F_s[tid] = m + 8.f;
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        float m = xa[r];
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-        if (lane == 0) red[wave][r] = m;
-    }
-    __syncthreads();
-    if (tid < 16) {
-        float m = F_s[tid];
-        for (int w = 0; w < AV_T / 64; ++w) m = fmaxf(m, red[w][tid]);
-        F_s[tid] = tid < rows ? m : 0.f;
-    }
-    __syncthreads();
-    // ---- 2. weights: each quarter of the anchor's list (4 gathers in flight per thread)
-    float sh[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) sh[r] = 0.f;
-    if (live) {
-        const uint32_t* inv = p.inv_pos[sq];
-        const uint32_t e0 = p.inv_off[sq][a], e1 = p.inv_off[sq][a + 1];
-        for (uint32_t e = e0 + quarter; e < e1; e += 16) {
-            uint32_t pos[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) pos[u] = inv[e + 4 * u < e1 ? e + 4 * u : e];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const float* sp = S + (int64_t)pos[u] * ns;
-                const bool ok = e + 4 * u < e1;
+        for (int r = 0; r < 16; ++r) sh[r] = 0.f;
+        if (j < nact) {
+            const int64_t a = a_lo + j;
+            for (uint32_t P = poff[a] + lane; P < poff[a + 1]; P += 64) {
+                const float* pw = PW + (int64_t)P * ns;
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    if (r < rows) sh[r] += ok ? fast_exp(sp[r] - F_s[r]) : 0.f;
+                    if (r < rows) sh[r] += pw[r];
             }
         }
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) W4[tid][r] = sh[r];
-    __syncthreads();
-    // the anchor's weight: own + a quarter of the quarters' sums (fixed order); own mass
-    float own_l[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) own_l[r] = 0.f;
-    if (tid < AV_A) {
-        const int j = tid;
-        const bool lv = j < nact;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const float own = lv && r < rows ? fast_exp(X[(a_lo + j) * ns + r] - F_s[r]) : 0.f;
-            const float shr = ((W4[4 * j][r] + W4[4 * j + 1][r]) + W4[4 * j + 2][r]) + W4[4 * j + 3][r];
-            W[j][r] = own + 0.25f * shr;
-            own_l[r] = own;
+            float v = sh[r];
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+            sh[r] = v;
         }
-    }
-    // the anchors' own softmax mass, summed in a fixed order (lanes of wave 0)
-    if (wave == 0) {
+        if (lane < 16) {
+            const int r = lane;
+            const bool ok = j < nact && r < rows;
+            const float own = ok ? fast_exp(X[(a_lo + j) * ns + r] - F_s[r]) : 0.f;
+            float shr = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float l = own_l[r];
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) l += __shfl_xor(l, o, 64);
-            if (lane == 0) red[0][r] = l;
+            for (int rr = 0; rr < 16; ++rr) shr = rr == r ? sh[rr] : shr;
+            W[j][r] = ok ? own + 0.25f * shr : 0.f;
+            own_s[j][r] = own;
         }
     }
     __syncthreads();
-    // ---- 3. the value sums: thread -> column c, rows rh, rh + 2, ... (anchors in order)
+    // the anchors' own softmax mass, in anchor order
+    if (tid < 16) {
+        float l = 0.f;
+        for (int j = 0; j < nact; ++j) l += own_s[j][tid];
+        red[tid] = l;
+    }
+    // ---- the value sums: thread -> column c, rows rh, rh + 2, ... (anchors in order)
     const int c = tid & (D - 1), rh = tid >> 7;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int j = 0; j < nact; ++j) {
@@ -1218,11 +1262,12 @@ __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
 #pragma unroll
         for (int k = 0; k < 8; ++k) acc[k] = fmaf(W[j][rh + 2 * k], v, acc[k]);
     }
-    // ---- 4. the record: m = F, l = the anchors' own mass, acc in the original space
+    __syncthreads();
+    // ---- the record: m = F, l = the anchors' own mass, acc in the original space
     float* rec = p.part + ((int64_t)unit * p.nrec + p.rec0 + ab) * DC_REC;
     if (tid < 16) {
         rec[tid] = tid < rows ? F_s[tid] : -INFINITY;
-        rec[16 + tid] = tid < rows ? red[0][tid] : 0.f;
+        rec[16 + tid] = tid < rows ? red[tid] : 0.f;
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -1276,15 +1321,17 @@ bool decode_supported(const varrate_shape& sh, int S, int Q) {
 }
 
 // Residual codec buffers after the records: X [units][na][ns], xbar and S [units][16 tiles][ns]
-static size_t anc_dec_bytes(const DecPlan& pl, size_t units) {
+static inline int64_t anc_np_bound(const DecPlan& pl, int64_t N) { return 4 * N / 64 + pl.na; }
+static size_t anc_dec_bytes(const DecPlan& pl, size_t units, int64_t N) {
     if (!pl.na) return 0;
-    return align256(units * pl.na * pl.ns * 4) + 2 * align256(units * 16 * (size_t)pl.total_tiles * pl.ns * 4);
+    return align256(units * pl.na * pl.ns * 4) + 2 * align256(units * 16 * (size_t)pl.total_tiles * pl.ns * 4) +
+           align256(units * ((pl.na + 63) / 64) * pl.ns * 4) + align256(units * anc_np_bound(pl, N) * pl.ns * 4);
 }
 
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
     DecPlan pl = plan_decode(sh, S, Q);
     const size_t units = (size_t)S * sh.G * pl.nqt;
-    return align256(units * pl.nrec * DC_REC * sizeof(float)) + anc_dec_bytes(pl, units);
+    return align256(units * pl.nrec * DC_REC * sizeof(float)) + anc_dec_bytes(pl, units, coded_count(sh));
 }
 
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
@@ -1308,7 +1355,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     if (pl.nrec > DC_MAX_REC) return hipErrorInvalidValue;
     float* part = (float*)ws;
     // residual codec: X, xbar and S after the records
-    float *Xb = nullptr, *xbarb = nullptr, *Sb = nullptr;
+    float *Xb = nullptr, *xbarb = nullptr, *Sb = nullptr, *XMb = nullptr, *PWb = nullptr;
+    const int64_t np_bound = anc_np_bound(pl, coded_count(sh));
     if (anc) {
         if (reuse_group_region) return hipErrorInvalidValue;   // no fixed scratch for it
         uint8_t* b = ws + align256(units_all * pl.nrec * DC_REC * sizeof(float));
@@ -1317,6 +1365,10 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         xbarb = (float*)b;
         b += align256(units_all * 16 * (size_t)pl.total_tiles * pl.ns * 4);
         Sb = (float*)b;
+        b += align256(units_all * 16 * (size_t)pl.total_tiles * pl.ns * 4);
+        XMb = (float*)b;
+        b += align256(units_all * ((pl.na + 63) / 64) * pl.ns * 4);
+        PWb = (float*)b;
     }
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
@@ -1375,8 +1427,13 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
                 ad.snn[i] = c.snn;
                 ad.inv_off[i] = c.inv_off;
                 ad.inv_pos[i] = c.inv_pos;
+                ad.piece_off[i] = c.piece_off;
+                ad.piece_anchor[i] = c.piece_anchor;
             }
             ad.X = Xb + u0 * pl.na * pl.ns;
+            ad.XM = XMb + u0 * ((pl.na + 63) / 64) * pl.ns;
+            ad.PW = PWb + u0 * np_bound * pl.ns;
+            ad.np_bound = np_bound;
             ad.xbar = const_cast<float*>(prm.xbar);
             ad.S = prm.S;
             ad.part = prm.part;
@@ -1394,6 +1451,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
             ad.ablk = AV_A;
             ad.n_ablk = pl.n_ablk;
             anc_qscores<<<(unsigned)(prm.units * ((pl.na + 63) / 64)), 256, 0, st>>>(ad);
+            anc_xmax<<<(unsigned)(prm.units * ((pl.na + 63) / 64)), 256, 0, st>>>(ad);
             anc_xbar<<<(unsigned)(prm.units * ((16 * pl.total_tiles + 63) / 64)), 256, 0, st>>>(ad);
             e = hipGetLastError();
             if (e != hipSuccess) return e;
@@ -1403,6 +1461,7 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (pl.na) {
+            anc_pieces<<<(unsigned)(prm.units * ((np_bound + AP_T - 1) / AP_T)), AP_T, 0, st>>>(ad);
             anc_values<<<(unsigned)(prm.units * pl.n_ablk), AV_T, 0, st>>>(ad);
             e = hipGetLastError();
             if (e != hipSuccess) return e;
