@@ -1023,11 +1023,12 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
 //                term the streaming kernel adds to each coded score (it also writes the final
 //                scores S[unit][pos][row])
 //   anc_pieces   per piece of an anchor's list (64 entries): sum of exp(S - F)
+//   anc_weights  per anchor: W_a = exp(X_a - F) + (1/4) sum over the positions that use a
+//                of exp(S - F) (its pieces)
 //   anc_values   one record per (unit, block of anchors) in the original space: for its
-//                anchors, W_a = exp(X_a - F) + (1/4) sum over the positions that use a of
-//                exp(S - F) (its pieces), acc = sum W_a v_a, l = sum exp(X_a - F), m = F
-//                (a bound of every score involved); the merge combines these with the others
-//                by log-sum-exp like the exact record.
+//                anchors, acc = sum W_a v_a, l = sum exp(X_a - F), m = F (a bound of every
+//                score involved); the merge combines these with the others by log-sum-exp
+//                like the exact record.
 struct AncDec {
     const varrate_cache* seq;   // unused on the device
     const void* q[DC_SEQ];
@@ -1041,6 +1042,8 @@ struct AncDec {
     float* X;          // [unit][na][ns]
     float* XM;         // [unit][ceil(na / 64)][ns] block maxima of X
     float* PW;         // [unit][np_bound][ns] per-piece sums of exp(S - F)
+    float* W;          // [unit][na][ns] anchor weights
+    float* F;          // [unit][16] the frame
     int64_t np_bound;  // pieces per unit at most: 4 N / 64 + na
     float* xbar;       // [unit][16 total_tiles][ns]
     float* S;          // [unit][16 total_tiles][ns]
@@ -1127,124 +1130,180 @@ __global__ __launch_bounds__(256) void anc_xbar(AncDec p) {
 
 // The frame F[row] of the anchor weights: an upper bound of every score they involve, the
 // largest of the anchors' own scores and of the streaming records' running maxima + 8 (each
-// coded score exceeds its workgroup's running maximum by at most 8).  Computed the same way
-// (same order) wherever it is needed, into F_s[16].
+// coded score exceeds its workgroup's running maximum by at most 8).  All 256 threads scan
+// (thread -> row tid % 16, every 16th record and block maximum), then a max over the 16
+// partial maxima; a maximum does not depend on the order, so every workgroup that computes
+// it gets the same F.
 __device__ __forceinline__ void anc_frame(const AncDec& p, int unit, int rows, float* F_s) {
-    const int tid = threadIdx.x;
+    __shared__ float part_m[16][17], part_x[16][17];
+    const int tid = threadIdx.x, r = tid & 15, k = tid >> 4;
+    const float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
+    const int xb = (int)((p.na + 63) / 64);
+    const float* XM = p.XM + (int64_t)unit * xb * p.ns;
+    float m = -INFINITY, mx = -INFINITY;
+    if (r < rows) {
+        for (int x = k; x < p.rec0; x += 16) m = fmaxf(m, recs[(int64_t)x * DC_REC + r]);
+        for (int b = k; b < xb; b += 16) mx = fmaxf(mx, XM[b * p.ns + r]);
+    }
+    part_m[k][r] = m;
+    part_x[k][r] = mx;
+    __syncthreads();
     if (tid < 16) {
-        const float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
-        const int xb = (int)((p.na + 63) / 64);
-        const float* XM = p.XM + (int64_t)unit * xb * p.ns;
-        float m = -INFINITY, mx = -INFINITY;
-        if (tid < rows) {
-            for (int x = 0; x < p.rec0; ++x) m = fmaxf(m, recs[(int64_t)x * DC_REC + tid]);
-            for (int b = 0; b < xb; ++b) mx = fmaxf(mx, XM[b * p.ns + tid]);
+        m = -INFINITY;
+        mx = -INFINITY;
+        for (int j = 0; j < 16; ++j) {
+            m = fmaxf(m, part_m[j][tid]);
+            mx = fmaxf(mx, part_x[j][tid]);
         }
         F_s[tid] = tid < rows ? fmaxf(m + 8.f, mx) : 0.f;
     }
     __syncthreads();
 }
 
-// one thread per list piece (at most 64 entries): PW = sum of exp(S - F) over the piece
+// Four threads per list piece (at most 64 entries, 16 each, all loads in flight), then a
+// fixed two-step butterfly: PW[P][row] = sum over the piece of exp(S - F).  The first
+// workgroup of each unit also stores F for the kernels after it.
 constexpr int AP_T = 256;
+constexpr int AP_PIECES = AP_T / 4;   // pieces per workgroup
 __global__ __launch_bounds__(AP_T) void anc_pieces(AncDec p) {
     __shared__ float F_s[16];
-    const int blocks = (int)((p.np_bound + AP_T - 1) / AP_T);
+    const int blocks = (int)((p.np_bound + AP_PIECES - 1) / AP_PIECES);
     const int unit = blockIdx.x / blocks, pb = blockIdx.x % blocks;
     int sq, g, qt, rows;
     anc_unit(p, unit, sq, g, qt, rows);
     anc_frame(p, unit, rows, F_s);
-    const int64_t P = (int64_t)pb * AP_T + threadIdx.x;
+    if (pb == 0 && threadIdx.x < 16) p.F[unit * 16 + threadIdx.x] = F_s[threadIdx.x];
+    const int64_t P = (int64_t)pb * AP_PIECES + (threadIdx.x >> 2);
+    const int sub = threadIdx.x & 3;
     const uint32_t npieces = p.piece_off[sq][p.na];
+    // whole quads leave together, so the butterfly below sees all four lanes
     if (P >= (int64_t)npieces) return;
     const int ns = p.ns;
     const uint32_t a = p.piece_anchor[sq][P];
     const uint32_t j = (uint32_t)P - p.piece_off[sq][a];
-    const uint32_t e0 = p.inv_off[sq][a] + 64 * j;
-    const uint32_t e1 = min(p.inv_off[sq][a + 1], e0 + 64);
+    const uint32_t e_end = p.inv_off[sq][a + 1];
+    const uint32_t e0 = min(p.inv_off[sq][a] + 64 * j + 16 * sub, e_end);
+    const uint32_t e1 = min(e0 + 16, e_end);
     const uint32_t* inv = p.inv_pos[sq];
     const float* S = p.S + (int64_t)unit * 16 * p.total_tiles * ns;
+    float F[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) F[r] = F_s[r];
+    uint32_t pos[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) pos[u] = e0 + u < e1 ? inv[e0 + u] : 0u;
     float sh[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) sh[r] = 0.f;
-    for (uint32_t e = e0; e < e1; e += 8) {
-        uint32_t pos[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) pos[u] = inv[e + u < e1 ? e + u : e0];
+    for (int u = 0; u < 16; ++u) {
+        const bool ok = e0 + u < e1;
+        const f32x4* sp = reinterpret_cast<const f32x4*>(S + (int64_t)pos[u] * ns);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const float* sp = S + (int64_t)pos[u] * ns;
-            const bool ok = e + u < e1;
+        for (int r4 = 0; r4 < 4; ++r4) {
+            if (4 * r4 < ns && ok) {
+                const f32x4 v = sp[r4];
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                if (r < rows) sh[r] += ok ? fast_exp(sp[r] - F_s[r]) : 0.f;
+                for (int k = 0; k < 4; ++k)
+                    if (4 * r4 + k < rows) sh[4 * r4 + k] += fast_exp(v[k] - F[4 * r4 + k]);
+            }
         }
     }
-    float* pw = p.PW + ((int64_t)unit * p.np_bound + P) * ns;
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-        if (r < ns) pw[r] = sh[r];
+    for (int r = 0; r < 16; ++r) {
+        if (r < ns) {
+            sh[r] += __shfl_xor(sh[r], 1, 64);
+            sh[r] += __shfl_xor(sh[r], 2, 64);
+        }
+    }
+    if (sub == 0) {
+        float* pw = p.PW + ((int64_t)unit * p.np_bound + P) * ns;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            if (r < ns) pw[r] = sh[r];
+    }
 }
 
-// A workgroup per (unit, block of AV_A anchors): each anchor's weight W_a = exp(X_a - F) +
-// (1/4) sum of its pieces' PW (a wave per anchor: lanes take every 64th piece, then a fixed
-// butterfly), then the value sums over the block's anchors (value rows staged in LDS).
+// A wave per anchor: W_a = exp(X_a - F) + (1/4) sum of its pieces' PW (lanes take every 64th
+// piece, then a fixed butterfly).  Writes W[unit][a][row] and the anchor's own mass
+// exp(X_a - F) over X (read only here, by the same lane).
+constexpr int AW_T = 256;
+__global__ __launch_bounds__(AW_T) void anc_weights(AncDec p) {
+    const int blocks = (int)((p.na + AW_T / 64 - 1) / (AW_T / 64));
+    const int unit = blockIdx.x / blocks, ab = blockIdx.x % blocks;
+    int sq, g, qt, rows;
+    anc_unit(p, unit, sq, g, qt, rows);
+    const int lane = threadIdx.x & 63;
+    const int64_t a = (int64_t)ab * (AW_T / 64) + (threadIdx.x >> 6);
+    if (a >= p.na) return;   // whole waves
+    const int ns = p.ns;
+    const uint32_t P0 = p.piece_off[sq][a], P1 = p.piece_off[sq][a + 1];
+    const float* PW = p.PW + (int64_t)unit * p.np_bound * ns;
+    float sh[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sh[r] = 0.f;
+    for (uint32_t P = P0 + lane; P < P1; P += 64) {
+        const f32x4* pw = reinterpret_cast<const f32x4*>(PW + (int64_t)P * ns);
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+            if (4 * r4 < ns) {
+                const f32x4 v = pw[r4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) sh[4 * r4 + k] += v[k];
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        if (r < rows) {
+            float v = sh[r];
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+            sh[r] = v;
+        }
+    }
+    if (lane < ns) {
+        const int r = lane;
+        float shr = 0.f;
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) shr = rr == r ? sh[rr] : shr;
+        float* X = p.X + ((int64_t)unit * p.na + a) * ns;
+        const float own = r < rows ? fast_exp(X[r] - p.F[unit * 16 + r]) : 0.f;
+        X[r] = own;
+        p.W[((int64_t)unit * p.na + a) * ns + r] = r < rows ? own + 0.25f * shr : 0.f;
+    }
+}
+
+// A workgroup per (unit, block of AV_A anchors): the value sums over the block's anchors
+// (value rows and weights staged in LDS) and its record.
 constexpr int AV_T = 256;
 constexpr int AV_A = 64;                          // anchors per workgroup
 __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
-    __shared__ float F_s[16], red[16];
+    __shared__ float red[16];
     __shared__ float W[AV_A][17];
     __shared__ float own_s[AV_A][17];
     __shared__ __attribute__((aligned(16))) uint16_t vrow[AV_A][D];
     const int unit = blockIdx.x / p.n_ablk, ab = blockIdx.x % p.n_ablk;
     int sq, g, qt, rows;
     anc_unit(p, unit, sq, g, qt, rows);
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x;
     const int64_t a_lo = (int64_t)ab * AV_A;
     const int nact = (int)min<int64_t>(AV_A, p.na - a_lo);
     const int ns = p.ns;
-    const float* X = p.X + (int64_t)unit * p.na * ns;
-    // the block's value rows into LDS (16-byte pieces, all in flight together)
+    // the block's value rows, weights and own masses into LDS (all loads in flight together)
     {
         const uint16_t* va = reinterpret_cast<const uint16_t*>(p.va[sq]);
         for (int k = tid; k < nact * (D / 8); k += AV_T) {
             const int j = k / (D / 8), e = 8 * (k % (D / 8));
             *reinterpret_cast<u32x4*>(&vrow[j][e]) = load16(va + ((a_lo + j) * p.G + g) * D + e);
         }
-    }
-    anc_frame(p, unit, rows, F_s);
-    // ---- weights: wave w takes anchors w, w + 4, ...
-    const uint32_t* poff = p.piece_off[sq];
-    const float* PW = p.PW + (int64_t)unit * p.np_bound * ns;
-    for (int j = wave; j < AV_A; j += AV_T / 64) {
-        float sh[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sh[r] = 0.f;
-        if (j < nact) {
-            const int64_t a = a_lo + j;
-            for (uint32_t P = poff[a] + lane; P < poff[a + 1]; P += 64) {
-                const float* pw = PW + (int64_t)P * ns;
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (r < rows) sh[r] += pw[r];
-            }
-        }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            float v = sh[r];
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-            sh[r] = v;
-        }
-        if (lane < 16) {
-            const int r = lane;
-            const bool ok = j < nact && r < rows;
-            const float own = ok ? fast_exp(X[(a_lo + j) * ns + r] - F_s[r]) : 0.f;
-            float shr = 0.f;
-#pragma unroll
-            for (int rr = 0; rr < 16; ++rr) shr = rr == r ? sh[rr] : shr;
-            W[j][r] = ok ? own + 0.25f * shr : 0.f;
-            own_s[j][r] = own;
+        const float* Wg = p.W + ((int64_t)unit * p.na + a_lo) * ns;
+        const float* Og = p.X + ((int64_t)unit * p.na + a_lo) * ns;
+        for (int k = tid; k < AV_A * 16; k += AV_T) {
+            const int j = k >> 4, r = k & 15;
+            const bool ok = j < nact && r < ns;
+            W[j][r] = ok ? Wg[j * ns + r] : 0.f;
+            own_s[j][r] = ok ? Og[j * ns + r] : 0.f;
         }
     }
     __syncthreads();
@@ -1266,7 +1325,7 @@ __global__ __launch_bounds__(AV_T) void anc_values(AncDec p) {
     // ---- the record: m = F, l = the anchors' own mass, acc in the original space
     float* rec = p.part + ((int64_t)unit * p.nrec + p.rec0 + ab) * DC_REC;
     if (tid < 16) {
-        rec[tid] = tid < rows ? F_s[tid] : -INFINITY;
+        rec[tid] = tid < rows ? p.F[unit * 16 + tid] : -INFINITY;
         rec[16 + tid] = tid < rows ? red[tid] : 0.f;
     }
 #pragma unroll
@@ -1320,12 +1379,14 @@ bool decode_supported(const varrate_shape& sh, int S, int Q) {
     return plan_decode(sh, S, Q).nrec <= DC_MAX_REC;
 }
 
-// Residual codec buffers after the records: X [units][na][ns], xbar and S [units][16 tiles][ns]
+// Residual codec buffers after the records: X [units][na][ns], xbar and S [units][16 tiles][ns],
+// XM [units][na / 64][ns], PW [units][pieces][ns], W [units][na][ns], F [units][16]
 static inline int64_t anc_np_bound(const DecPlan& pl, int64_t N) { return 4 * N / 64 + pl.na; }
 static size_t anc_dec_bytes(const DecPlan& pl, size_t units, int64_t N) {
     if (!pl.na) return 0;
-    return align256(units * pl.na * pl.ns * 4) + 2 * align256(units * 16 * (size_t)pl.total_tiles * pl.ns * 4) +
-           align256(units * ((pl.na + 63) / 64) * pl.ns * 4) + align256(units * anc_np_bound(pl, N) * pl.ns * 4);
+    return 2 * align256(units * pl.na * pl.ns * 4) + 2 * align256(units * 16 * (size_t)pl.total_tiles * pl.ns * 4) +
+           align256(units * ((pl.na + 63) / 64) * pl.ns * 4) + align256(units * anc_np_bound(pl, N) * pl.ns * 4) +
+           align256(units * 16 * 4);
 }
 
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
@@ -1355,7 +1416,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     if (pl.nrec > DC_MAX_REC) return hipErrorInvalidValue;
     float* part = (float*)ws;
     // residual codec: X, xbar and S after the records
-    float *Xb = nullptr, *xbarb = nullptr, *Sb = nullptr, *XMb = nullptr, *PWb = nullptr;
+    float *Xb = nullptr, *xbarb = nullptr, *Sb = nullptr, *XMb = nullptr, *PWb = nullptr, *Wb = nullptr,
+          *Fb = nullptr;
     const int64_t np_bound = anc_np_bound(pl, coded_count(sh));
     if (anc) {
         if (reuse_group_region) return hipErrorInvalidValue;   // no fixed scratch for it
@@ -1369,6 +1431,10 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         XMb = (float*)b;
         b += align256(units_all * ((pl.na + 63) / 64) * pl.ns * 4);
         PWb = (float*)b;
+        b += align256(units_all * np_bound * pl.ns * 4);
+        Wb = (float*)b;
+        b += align256(units_all * pl.na * pl.ns * 4);
+        Fb = (float*)b;
     }
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
@@ -1433,6 +1499,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
             ad.X = Xb + u0 * pl.na * pl.ns;
             ad.XM = XMb + u0 * ((pl.na + 63) / 64) * pl.ns;
             ad.PW = PWb + u0 * np_bound * pl.ns;
+            ad.W = Wb + u0 * pl.na * pl.ns;
+            ad.F = Fb + u0 * 16;
             ad.np_bound = np_bound;
             ad.xbar = const_cast<float*>(prm.xbar);
             ad.S = prm.S;
@@ -1461,7 +1529,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (pl.na) {
-            anc_pieces<<<(unsigned)(prm.units * ((np_bound + AP_T - 1) / AP_T)), AP_T, 0, st>>>(ad);
+            anc_pieces<<<(unsigned)(prm.units * ((np_bound + AP_PIECES - 1) / AP_PIECES)), AP_T, 0, st>>>(ad);
+            anc_weights<<<(unsigned)(prm.units * ((pl.na + AW_T / 64 - 1) / (AW_T / 64))), AW_T, 0, st>>>(ad);
             anc_values<<<(unsigned)(prm.units * pl.n_ablk), AV_T, 0, st>>>(ad);
             e = hipGetLastError();
             if (e != hipSuccess) return e;
