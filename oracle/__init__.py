@@ -25,6 +25,7 @@ _f32p = np.ctypeslib.ndpointer(np.float32, flags="C_CONTIGUOUS")
 _f64p = np.ctypeslib.ndpointer(np.float64, flags="C_CONTIGUOUS")
 _u32p = np.ctypeslib.ndpointer(np.uint32, flags="C_CONTIGUOUS")
 _i32p = np.ctypeslib.ndpointer(np.int32, flags="C_CONTIGUOUS")
+_i64p = np.ctypeslib.ndpointer(np.int64, flags="C_CONTIGUOUS")
 _i64 = ctypes.c_int64
 _int = ctypes.c_int
 
@@ -77,6 +78,11 @@ def lib():
         L.vro_decode.restype = None
         L.vro_decode.argtypes = [_i64, _i64, _int, _int, _int, _f32p, _f32p, _i32p,
                                  _f32p, _f32p, _f32p, _f32p, _f32p, _f64p]
+        L.vro_rope.restype = None
+        L.vro_rope.argtypes = [_i64, _int, _int, _f32p, _i64p, _f32p, _int, _f64p]
+        L.vro_decode_rope.restype = None
+        L.vro_decode_rope.argtypes = [_i64, _i64, _int, _int, _int, _f32p, _f32p, _i32p,
+                                      _f32p, _f32p, _f32p, _f32p, _f32p, _i64p, _f32p, _f64p]
         _lib = L
     return _lib
 
@@ -320,4 +326,59 @@ def decode_anchor(ac: AnchorCompressed, PK, PV, q, H: int, Kx=None, Vx=None) -> 
                             _c(ac.coefV, np.float32), _c(ac.alloc.rank, np.int32), _c(ac.nn, np.int32),
                             _c(ac.Ka, np.float32), _c(ac.Va, np.float32), _c(Kx, np.float32), _c(Vx, np.float32),
                             _c(PK, np.float32), _c(PV, np.float32), _c(q, np.float32), out)
+    return out
+
+
+# ---------------------------------------------------------------------------------------
+# Sec. 3.1 "Joint per-token vector", Algorithm 1 first and last steps: keys arrive with
+# rotary position embedding (post-RoPE); the codec works on the un-rotated keys and the
+# reconstruction is rotated back at each token's position.
+
+def rope(X: np.ndarray, pos, theta: np.ndarray, sign: int = 1) -> np.ndarray:
+    """Rotary embedding in the rotate-half layout (pair i = coordinates i and i + d/2) at
+    positions pos [n_tok], angle sign * pos * theta[i]; sign -1 removes it.  fp64 out."""
+    n, G, d = X.shape
+    out = np.zeros((n, G, d), np.float64)
+    lib().vro_rope(n, G, d, _c(X, np.float32), _c(np.broadcast_to(pos, (n,)), np.int64),
+                   _c(theta, np.float32), int(sign), out)
+    return out
+
+
+def compress_rope(K, V, Qw, PK, PV, H: int, kappa_pct: int, r_min: int, storage: str,
+                  theta: np.ndarray, sbar: np.ndarray | None = None) -> Compressed:
+    """Algorithm 1 with rotary keys (anchor-free, per-head bases): salience on the
+    post-RoPE keys and window queries as the model attends; each coded key is un-rotated at
+    its position t (rounded to the storage type) before the projection; the window rows stay
+    exact and post-RoPE."""
+    n, G, d = K.shape
+    w = Qw.shape[0]
+    N = n - w
+    B = budget(n, d, w, kappa_pct)
+    if sbar is None:
+        s = salience(K, Qw, H)
+        sb = pool(s)
+    else:
+        s = np.full(N, np.nan)
+        sb = _c(sbar, np.float32)
+    u = weights(sb)
+    al = allocate(u, B, r_min, d)
+    Ku = round_storage(rope(K[:N], np.arange(N, dtype=np.int64), theta, -1), storage)
+    cK = project(Ku, PK, al.rank, storage)
+    cV = project(V[:N], PV, al.rank, storage)
+    return Compressed(s, sb, u, al, B, cK, cV, np.ascontiguousarray(K[N:]),
+                      np.ascontiguousarray(V[N:]))
+
+
+def decode_rope(comp: Compressed, PK, PV, q, H: int, theta: np.ndarray, Kx=None, Vx=None) -> np.ndarray:
+    """Reconstruct-in-place decode with rotary keys: coded keys rebuilt from their
+    coefficients and re-rotated at their positions 0..N-1; exact rows and the query q [H][d]
+    post-RoPE as given.  fp64 [H][d]."""
+    N, G, d = comp.coefK.shape
+    Kx = comp.Kx if Kx is None else Kx
+    Vx = comp.Vx if Vx is None else Vx
+    out = np.zeros((H, d), np.float64)
+    lib().vro_decode_rope(N, Kx.shape[0], G, H, d, _c(comp.coefK, np.float32), _c(comp.coefV, np.float32),
+                          _c(comp.alloc.rank, np.int32), _c(Kx, np.float32), _c(Vx, np.float32),
+                          _c(PK, np.float32), _c(PV, np.float32), _c(q, np.float32),
+                          np.arange(N, dtype=np.int64), _c(theta, np.float32), out)
     return out

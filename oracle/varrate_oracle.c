@@ -289,17 +289,52 @@ EXPORT void vro_project(int64_t n_tok, int G, int d, const float *X, const float
 }
 
 /* ------------------------------------------------------------------------------------- */
+/* Sec. 3.1 "Joint per-token vector" and Algorithm 1 (first and last steps): rotary position
+ * embedding in the rotate-half layout.  Coordinates i and i + d/2 form pair i; at position p
+ * the pair turns by the angle sign * p * theta[i] (exact product, fp64):
+ *     y_i       = x_i cos(a) - x_{i+d/2} sin(a)
+ *     y_{i+d/2} = x_i sin(a) + x_{i+d/2} cos(a).
+ * sign = +1 applies the embedding (pre-RoPE -> post-RoPE), sign = -1 removes it.
+ * Layouts: X, out [n_tok][G][d]; pos [n_tok]; theta [d/2].                                */
+static void rope_row(const double *x, double *y, int d, double p, const float *theta, int sign)
+{
+    const int h = d / 2;
+    for (int i = 0; i < h; ++i) {
+        const double a = (double)sign * p * (double)theta[i];
+        const double c = cos(a), s = sin(a);
+        const double x0 = x[i], x1 = x[i + h];
+        y[i] = x0 * c - x1 * s;
+        y[i + h] = x0 * s + x1 * c;
+    }
+}
+
+EXPORT void vro_rope(int64_t n_tok, int G, int d, const float *X, const int64_t *pos,
+                     const float *theta, int sign, double *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < n_tok; ++t) {
+        double x[512];
+        for (int g = 0; g < G; ++g) {
+            for (int i = 0; i < d; ++i) x[i] = (double)X[(t * G + g) * d + i];
+            rope_row(x, out + (t * G + g) * d, d, (double)pos[t], theta, sign);
+        }
+    }
+}
+
 /* Sec. 4.4 decode, reconstruct-in-place: coded tokens are rebuilt from their stored
  * coefficients, x_hat_t = P^T (m_t . c_t) (Eq. 6 with zbar = 0); exact tokens (the window
  * and any tokens appended during decode) are used as stored.  A decode query then runs
  * stock attention over all of them:
  *     o_h = sum_t softmax_t(<q_h, k_hat_t> / sqrt(d)) v_hat_t        (fp64).
+ * With rotary embedding (pos != NULL; the last step of Algorithm 1), a coded key is
+ * re-rotated to post-RoPE at its token position pos[t] after the reconstruction; the exact
+ * rows and the query are post-RoPE already.
  * Layouts: coefK/coefV [N][G][d] (zero beyond the rank), Kx/Vx [n_exact][G][d],
  * PK/PV [G][d][d], q [H][d], out [H][d].                                                  */
-EXPORT void vro_decode(int64_t N, int64_t n_exact, int G, int H, int d,
-                       const float *coefK, const float *coefV, const int32_t *rank,
-                       const float *Kx, const float *Vx, const float *PK, const float *PV,
-                       const float *q, double *out)
+static void decode_impl(int64_t N, int64_t n_exact, int G, int H, int d,
+                        const float *coefK, const float *coefV, const int32_t *rank,
+                        const float *Kx, const float *Vx, const float *PK, const float *PV,
+                        const float *q, const int64_t *pos, const float *theta, double *out)
 {
     const int hpg = H / G;
     const double scale = 1.0 / sqrt((double)d);
@@ -315,15 +350,18 @@ EXPORT void vro_decode(int64_t N, int64_t n_exact, int G, int H, int d,
         for (int64_t t = 0; t < N; ++t) {
             const float *ck = coefK + (t * G + g) * d;
             const float *cv = coefV + (t * G + g) * d;
+            double kt[512];
             for (int c = 0; c < d; ++c) {
                 double ak = 0.0, av = 0.0;
                 for (int j = 0; j < rank[t]; ++j) {
                     ak += (double)ck[j] * (double)Pk[(int64_t)j * d + c];
                     av += (double)cv[j] * (double)Pv[(int64_t)j * d + c];
                 }
-                kh[t * d + c] = ak;
+                kt[c] = ak;
                 vh[t * d + c] = av;
             }
+            if (pos) rope_row(kt, kh + t * d, d, (double)pos[t], theta, +1);
+            else for (int c = 0; c < d; ++c) kh[t * d + c] = kt[c];
         }
         for (int hh = 0; hh < hpg; ++hh) {
             const int h = g * hpg + hh;
@@ -357,6 +395,22 @@ EXPORT void vro_decode(int64_t N, int64_t n_exact, int G, int H, int d,
     free(kh);
     free(vh);
     free(x);
+}
+
+EXPORT void vro_decode(int64_t N, int64_t n_exact, int G, int H, int d,
+                       const float *coefK, const float *coefV, const int32_t *rank,
+                       const float *Kx, const float *Vx, const float *PK, const float *PV,
+                       const float *q, double *out)
+{
+    decode_impl(N, n_exact, G, H, d, coefK, coefV, rank, Kx, Vx, PK, PV, q, NULL, NULL, out);
+}
+
+EXPORT void vro_decode_rope(int64_t N, int64_t n_exact, int G, int H, int d,
+                            const float *coefK, const float *coefV, const int32_t *rank,
+                            const float *Kx, const float *Vx, const float *PK, const float *PV,
+                            const float *q, const int64_t *pos, const float *theta, double *out)
+{
+    decode_impl(N, n_exact, G, H, d, coefK, coefV, rank, Kx, Vx, PK, PV, q, pos, theta, out);
 }
 
 /* ------------------------------------------------------------------------------------- */

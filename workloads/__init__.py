@@ -11,6 +11,7 @@ from .synth import (  # noqa: F401
     bf16_round,
     make_layer,
     make_head_model,
+    rope_theta,
     calibration_basis,
     decode_queries,
     seed_for,

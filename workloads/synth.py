@@ -10,6 +10,11 @@ Recipe (one per layer x KV head x sequence):
               decode; query-agnostic decode draws q ~ N(0, s^2 I) with s set for logit std ~2.
   * values    low-rank plus noise  v = A_g eta + 0.1 eps  (A_g in R^{128x32}, entries
               N(0, 1/32)), or, for the tiny config, the key law without planting.
+  * RoPE      (configs with rope="llama3") the drawn keys are pre-RoPE; the cache holds them
+              rotated at their positions 0..n-1 in the rotate-half layout with Llama-3.1's
+              frequencies (base 500000, long-context scaling factor 8), the window queries at
+              n-w..n-1 and the decode queries at n.  The planted direction u_g then lives on
+              the 16 slowest pairs, so planted tokens stay salient across the context.
   * basis     per (layer, KV head, K|V): eigenvectors of the uncentred second moment of 8192
               calibration draws from a disjoint seed, rows in descending-eigenvalue order,
               each row's largest-magnitude entry made positive.  The basis is an input to the
@@ -39,6 +44,10 @@ CONFIGS: Dict[str, dict] = {
                            dtype="bf16", seed=2, values="lowrank", batch=8, steps=256),
     "llama_128k_stack": dict(layers=32, G=8, H=32, d=128, n=131072, w=32, kappa=20, r_min=16,
                              dtype="bf16", seed=3, values="lowrank", batch=1),
+    "tiny_rope": dict(layers=1, G=1, H=2, d=128, n=512, w=32, kappa=20, r_min=16,
+                      dtype="f32", seed=6, values="keys", batch=1, rope="llama3"),
+    "llama_32k_rope": dict(layers=1, G=8, H=32, d=128, n=32768, w=32, kappa=20, r_min=16,
+                           dtype="bf16", seed=7, values="lowrank", batch=1, rope="llama3"),
     "agnostic_32k": dict(layers=1, G=8, H=32, d=128, n=32768, w=32, kappa=20, r_min=16,
                          dtype="bf16", seed=4, values="lowrank", batch=1, queries=64,
                          budgets=((10, 8), (20, 16), (40, 16))),
@@ -101,11 +110,44 @@ class HeadModel:
     outliers_v: np.ndarray
 
 
-def make_head_model(base: int, layer: int, head: int, d: int = 128) -> HeadModel:
+def rope_theta(kind: str, d: int = 128) -> np.ndarray:
+    """Per-pair rotary frequencies (radians per position), float32 [d/2].  "llama3": base
+    500000 with Llama-3.1's long-context scaling (factor 8, low/high frequency factors 1
+    and 4, original context 8192): slow pairs divided by 8, fast pairs kept, a linear blend
+    of the two in between."""
+    if kind != "llama3":
+        raise ValueError(kind)
+    inv = 500000.0 ** (-np.arange(0, d, 2, dtype=np.float64) / d)
+    factor, lo_f, hi_f, old = 8.0, 1.0, 4.0, 8192.0
+    wavelen = 2.0 * np.pi / inv
+    smooth = np.clip((old / wavelen - lo_f) / (hi_f - lo_f), 0.0, 1.0)
+    out = (1.0 - smooth) * inv / factor + smooth * inv
+    return out.astype(np.float32)
+
+
+def _rotate(x: np.ndarray, pos: np.ndarray, theta: np.ndarray) -> np.ndarray:
+    """x [m, ..., d] rotated at positions pos [m] (rotate-half pairs i, i + d/2), fp64."""
+    h = x.shape[-1] // 2
+    a = pos.astype(np.float64)[:, None] * theta.astype(np.float64)[None, :]
+    shape = (len(pos),) + (1,) * (x.ndim - 2) + (h,)
+    c, s = np.cos(a).reshape(shape), np.sin(a).reshape(shape)
+    x0, x1 = x[..., :h], x[..., h:]
+    return np.concatenate([x0 * c - x1 * s, x0 * s + x1 * c], axis=-1)
+
+
+ROPE_SLOW_PAIRS = 16
+
+
+def make_head_model(base: int, layer: int, head: int, d: int = 128, rope: bool = False) -> HeadModel:
     rng = _rng(base, layer, head, 0, _S_HEAD)
     M = _orthogonal(rng, d)
     outliers = rng.choice(d, size=2, replace=False)
     u = rng.standard_normal(d)
+    if rope:      # only the slowest pairs: planted logits survive the relative rotation
+        keep = np.zeros(d, bool)
+        keep[d // 2 - ROPE_SLOW_PAIRS:d // 2] = True
+        keep[d - ROPE_SLOW_PAIRS:] = True
+        u = np.where(keep, u, 0.0)
     u /= np.linalg.norm(u)
     A = rng.standard_normal((d, VALUE_RANK)) / np.sqrt(VALUE_RANK)
     rv = _rng(base, layer, head, 0, _S_VHEAD)
@@ -183,6 +225,7 @@ class LayerInputs:
     PV: np.ndarray     # [G, d, d]
     planted: list      # per KV head: planted coded-token indices
     cfg: dict
+    theta: Optional[np.ndarray] = None   # rotary frequencies [d/2] (RoPE configs), else None
 
 
 def decode_queries(cfg: dict, layer: int, seq: int, n_q: int, law: str,
@@ -210,7 +253,8 @@ def make_layer(cfg: dict, layer: int = 0, seq: int = 0, n_queries: int = 1,
     n = cfg["n"] if n is None else n
     base = cfg["seed"]
     N = n - w
-    hms = [make_head_model(base, layer, g, d) for g in range(G)]
+    rope = cfg.get("rope")
+    hms = [make_head_model(base, layer, g, d, rope=bool(rope)) for g in range(G)]
     K = np.empty((n, G, d))
     V = np.empty((n, G, d))
     planted = []
@@ -222,6 +266,12 @@ def make_layer(cfg: dict, layer: int = 0, seq: int = 0, n_queries: int = 1,
     hm_of_head = [hms[h // (H // G)] for h in range(H)]
     Qw = _window_law_queries(_rng(base, layer, 0, seq, _S_QWIN), hm_of_head, w, H, d)
     q = decode_queries(cfg, layer, seq, n_queries, query_law, hms, K)
+    theta = None
+    if rope:
+        theta = rope_theta(rope, d)
+        K = _rotate(K, np.arange(n), theta)
+        Qw = _rotate(Qw, np.arange(N, n), theta)
+        q = _rotate(q, np.full(q.shape[0], n), theta)
     rnd = bf16_round if cfg["dtype"] == "bf16" else (lambda a: a.astype(np.float32))
     K, V, Qw, q = (rnd(a.astype(np.float32)) for a in (K, V, Qw, q))
     if with_basis:
@@ -231,4 +281,4 @@ def make_layer(cfg: dict, layer: int = 0, seq: int = 0, n_queries: int = 1,
             PK[g], PV[g] = calibration_basis(base, layer, g, hms[g], d, cfg["values"])
     else:
         PK = PV = None
-    return LayerInputs(K, V, Qw, q, PK, PV, planted, cfg)
+    return LayerInputs(K, V, Qw, q, PK, PV, planted, cfg, theta)
