@@ -78,6 +78,18 @@ typedef struct varrate_shape {
                               (bf16 layers): prefix tokens 0, delta, 2 delta, ... < n - w are
                               exact anchors, and every other prefix token is coded as its
                               residual to the mean of its 4 nearest anchors (see below)        */
+    int32_t rope;       /* 0: position-free keys.  1: rotary keys (Sec. 3.1 "Joint per-token
+                           vector", Algorithm 1 first and last steps): K, the window queries,
+                           the decode queries and appended exact keys are post-RoPE, in the
+                           rotate-half layout -- coordinates i and i + 64 form pair i, turned at
+                           position p by the angle p * rope_theta[i] (radians; the exact product):
+                               y_i = x_i cos - x_{i+64} sin,  y_{i+64} = x_i sin + x_{i+64} cos.
+                           Prompt token t sits at position t.  The codec codes the un-rotated
+                           keys (rotated back by -t, rounded to dtype, then projected), the
+                           window rows stay exact and post-RoPE, and decode rebuilds each coded
+                           key from its coefficients and rotates it to its position before the
+                           score.  Not with anchors or quantised coefficients (EUNSUPPORTED).  */
+    float   rope_theta[64]; /* per-pair frequencies (finite, >= 0; any scaling already applied) */
 } varrate_shape;
 
 /*

@@ -51,11 +51,13 @@ class Shape:
     dtype: str = "bf16"
     d: int = HEAD_DIM
     anchor_stride: int = 0     # > 0: the residual codec with exact anchors every anchor_stride tokens
+    rope_theta: tuple | None = None   # rotary keys: 64 per-pair frequencies (post-RoPE inputs)
 
     def c(self) -> _lib.Shape:
+        th = (ctypes.c_float * 64)(*(self.rope_theta if self.rope_theta is not None else [0.0] * 64))
         return _lib.Shape(self.n, self.G, self.H, self.d, self.w, self.r_min, self.kappa_pct,
                           _lib.VARRATE_BF16 if self.dtype == "bf16" else _lib.VARRATE_F32,
-                          self.anchor_stride)
+                          self.anchor_stride, 1 if self.rope_theta is not None else 0, th)
 
     @property
     def torch_dtype(self):

@@ -30,7 +30,8 @@ DECODE_SCRATCH_BYTES = 8 << 20
 class Shape(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int64), ("G", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("d", ctypes.c_int32), ("w", ctypes.c_int32), ("r_min", ctypes.c_int32),
-                ("kappa_pct", ctypes.c_int32), ("dtype", ctypes.c_int32), ("anchor_stride", ctypes.c_int32)]
+                ("kappa_pct", ctypes.c_int32), ("dtype", ctypes.c_int32), ("anchor_stride", ctypes.c_int32),
+                ("rope", ctypes.c_int32), ("rope_theta", ctypes.c_float * 64)]
 
 
 class CacheC(ctypes.Structure):

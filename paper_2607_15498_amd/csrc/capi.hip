@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <cmath>
+
 #include <map>
 #include <mutex>
 #include <string>
@@ -80,6 +82,13 @@ int check_shape(const varrate_shape* sh) {
         if (anchor_count(*sh) < 4) return fail(VARRATE_EBUDGET, "fewer than 4 anchors");
         if (coded_count(*sh) < 1) return fail(VARRATE_EBUDGET, "no coded tokens between the anchors");
     }
+    if (sh->rope != 0) {
+        if (sh->rope != 1) return fail(VARRATE_EINVAL, "rope=%d outside {0, 1}", sh->rope);
+        if (sh->anchor_stride != 0) return fail(VARRATE_EUNSUPPORTED, "rotary keys with anchors");
+        for (int i = 0; i < VARRATE_HEAD_DIM / 2; ++i)
+            if (!(sh->rope_theta[i] >= 0.f) || !std::isfinite(sh->rope_theta[i]))
+                return fail(VARRATE_EINVAL, "rope_theta[%d] is negative or not finite", i);
+    }
     const int64_t B = coded_budget(*sh);
     const int64_t N = coded_count(*sh);
     if (N * sh->r_min > B || B > N * VARRATE_HEAD_DIM)
@@ -110,10 +119,27 @@ int check_cache(const varrate_shape* sh, const varrate_cache* c, bool need_layou
     return VARRATE_OK;
 }
 
-size_t compress_ws(const varrate_shape& sh) {
-    if (sh.anchor_stride != 0) return anchor_ws_bytes(sh);
+size_t compress_ws_base(const varrate_shape& sh) {
     const int64_t N = sh.n - sh.w;
     return align256(salience_ws_bytes(sh)) + align256(allocate_ws_bytes(sh)) + align256((size_t)N * 4);
+}
+
+// rotary keys: the un-rotated copy of K [n][G][d] follows the other buffers
+size_t compress_ws(const varrate_shape& sh) {
+    if (sh.anchor_stride != 0) return anchor_ws_bytes(sh);
+    const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
+    return compress_ws_base(sh) + (sh.rope ? align256((size_t)sh.n * sh.G * VARRATE_HEAD_DIM * es) : 0);
+}
+
+// Eq. (6) projection; with rotary keys, of the keys turned back to pre-RoPE (Algorithm 1,
+// first step) in the workspace
+hipError_t project_keys(const varrate_shape& sh, const void* K, const void* V, const float* PK,
+                        const float* PV, varrate_cache& c, uint8_t* ws, hipStream_t st) {
+    if (!sh.rope) return launch_project(sh, K, V, PK, PV, c, st);
+    void* Kr = ws + compress_ws_base(sh);
+    hipError_t e = launch_rope_unrotate(sh, K, Kr, st);
+    if (e != hipSuccess) return e;
+    return launch_project(sh, Kr, V, PK, PV, c, st);
 }
 
 }  // namespace
@@ -220,7 +246,7 @@ int varrate_project(const varrate_shape* sh, const void* K, const void* V, const
     c->N = sh->n - sh->w;
     c->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
     hipStream_t st = (hipStream_t)stream;
-    rc = hip_status(launch_project(*sh, K, V, PK, PV, *c, st), "project launch");
+    rc = hip_status(project_keys(*sh, K, V, PK, PV, *c, (uint8_t*)ws, st), "project launch");
     if (rc) return rc;
     c->n_exact = sh->w;
     return VARRATE_OK;
@@ -266,7 +292,7 @@ int varrate_compress(const varrate_shape* sh, const void* K, const void* V, cons
     uint8_t* w8 = w0 + align256(salience_ws_bytes(*sh));
     if ((rc = hip_status(launch_allocate(*sh, sbar, *c, w8, st, salience_part(*sh, w0)), "allocate launch")))
         return rc;
-    if ((rc = hip_status(launch_project(*sh, K, V, PK, PV, *c, st), "project launch"))) return rc;
+    if ((rc = hip_status(project_keys(*sh, K, V, PK, PV, *c, w0, st), "project launch"))) return rc;
     c->n_exact = sh->w;
     return VARRATE_OK;
 }
@@ -386,6 +412,7 @@ static int check_qcache(const varrate_shape* sh, const varrate_qcache* q) {
 int varrate_quantize(const varrate_shape* sh, const varrate_cache* c, varrate_qcache* q, void* stream) {
     int rc = check_shape(sh);
     if (rc) return rc;
+    if (sh->rope) return fail(VARRATE_EUNSUPPORTED, "quantised coefficients of rotary keys");
     if ((rc = check_cache(sh, c, true))) return rc;
     if ((rc = check_qcache(sh, q))) return rc;
     return hip_status(launch_quantize(*sh, *c, *q, (hipStream_t)stream), "quantize launch");
@@ -396,6 +423,7 @@ int varrate_decode_attn_q(const varrate_shape* sh, const varrate_cache* caches, 
                           void* ws, size_t ws_bytes, void* stream) {
     int rc = check_decode(sh, caches, S, q, Q, PK, PV, out);
     if (rc) return rc;
+    if (sh->rope) return fail(VARRATE_EUNSUPPORTED, "quantised coefficients of rotary keys");
     if (!qcaches) return fail(VARRATE_EINVAL, "qcaches is NULL");
     for (int s = 0; s < S; ++s) {
         if ((rc = check_qcache(sh, &qcaches[s]))) return rc;
@@ -419,8 +447,9 @@ int varrate_decode_attn_noalloc(const varrate_shape* sh, const varrate_cache* ca
                                 int32_t Q, const float* PK, const float* PV, void* out, void* stream) {
     int rc = check_decode(sh, caches, S, q, Q, PK, PV, out);
     if (rc) return rc;
-    if (sh->anchor_stride)
-        return fail(VARRATE_EUNSUPPORTED, "the residual codec's decode needs a workspace (varrate_decode_attn)");
+    if (sh->anchor_stride || sh->rope)
+        return fail(VARRATE_EUNSUPPORTED, "the residual codec's and rotary keys' decode need a workspace "
+                                          "(varrate_decode_attn)");
     const size_t need = decode_group_bytes(*sh, S, Q);
     if (need > (size_t)VARRATE_DECODE_SCRATCH_BYTES)
         return fail(VARRATE_EUNSUPPORTED,

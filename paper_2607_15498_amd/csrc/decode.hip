@@ -60,6 +60,7 @@ struct DecSeq {
     const void* q;
     void* out;
     int64_t n_exact;
+    const uint32_t* sidx;    // rotary keys: stored position -> token (its position)
 };
 
 struct DecParams {
@@ -73,6 +74,8 @@ struct DecParams {
     const float* xbar;       // residual codec: [unit][16 total_tiles][ns] anchor-mean score terms
     float* S;                // residual codec: [unit][16 total_tiles][ns] the coded tokens' scores
     int ns;                  // query rows per unit those arrays hold
+    const u32x4* rfrag;      // rotary keys: key-basis fragments [G][4][8][2][64] (bf16 hi, lo)
+    const float* rfreq;      // rotary keys: theta / (2 pi) per pair as (hi, lo) [128]
 };
 
 template <bool F32> struct Elem;
@@ -114,6 +117,10 @@ struct DecSmem {
     uint16_t* to;     // [cpw][DC_TO] element offset of tile h inside its chunk, h = 0..16
     uint8_t* mq;      // [cpw][DC_TO] quantised layout: tile h's coordinate count (its rank
                       //   rounded up to a multiple of 8)
+    float* rf;        // rotary keys: [128] theta / (2 pi) per pair (hi, lo)
+    u32x4* pfr;       // rotary keys: key-basis fragments [4 steps][8 blocks][hi, lo][64 lanes]
+    uint8_t* dpos;    // rotary keys: [DC_MAX_CPW][CHUNK] token of each stored position minus
+                      //   its chunk's first token
 };
 
 __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
@@ -131,15 +138,22 @@ __device__ __forceinline__ DecSmem carve(uint8_t* smem) {
     s.cT = reinterpret_cast<int*>(f); f += DC_MAX_CPW;
     s.cb = reinterpret_cast<uint32_t*>(f); f += DC_MAX_CPW;
     s.kmask = reinterpret_cast<u32x4*>(f); f += 9 * 4;
-    s.to = reinterpret_cast<uint16_t*>(f);
+    s.rf = f; f += D;
+    s.dpos = reinterpret_cast<uint8_t*>(f);
+    s.to = reinterpret_cast<uint16_t*>(s.dpos + (size_t)DC_MAX_CPW * CHUNK);
     s.mq = reinterpret_cast<uint8_t*>(s.to + DC_MAX_CPW * DC_TO);
+    s.pfr = reinterpret_cast<u32x4*>(s.mq + DC_MAX_CPW * DC_TO);   // 16-byte aligned offset
     return s;
 }
+constexpr size_t DC_RFRAG_BYTES = (size_t)4 * 8 * 2 * 64 * 16;     // 64 KB
 
-static inline size_t decode_smem_bytes(int cpw) {
+// (the small rotary tables are carved for every variant, so one layout serves all; the
+// fragments only in the rotary variant, which then runs one workgroup per CU)
+static inline size_t decode_smem_bytes(int cpw, bool rope = false) {
+    (void)cpw;
     return 4 * (size_t)(DC_STAGE_BYTES + DC_STAGE_PAD) + 4 * 2 * 64 * 16 +
-           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW + 9 * 4) * 4 + (size_t)DC_MAX_CPW * DC_TO * 2 +
-           (size_t)cpw * DC_TO;
+           (size_t)(2 * DC_WAVES * 16 + 32 + 2 * DC_MAX_CPW + 9 * 4 + D) * 4 + (size_t)DC_MAX_CPW * CHUNK +
+           (size_t)DC_MAX_CPW * DC_TO * 2 + (size_t)DC_MAX_CPW * DC_TO + (rope ? DC_RFRAG_BYTES : 0);
 }
 
 // 8 consecutive bf16 at element index a of an LDS array (any 2-byte alignment): five dword
@@ -379,6 +393,134 @@ __device__ __forceinline__ void tile_step(const TileMeta& tm, bool partial, cons
 }
 
 // ----------------------------------------------------------------------------------------
+// Rotary keys (Sec. 3.1 "Joint per-token vector"; Algorithm 1, last step).  A coded key is
+// pre-RoPE, k = P_K^T (m . c), and must be turned to its token's position p before the score,
+// so the rank-space score <P_K q, c> does not apply.  One tile:
+//   1. reconstruction by MFMA, K^T[dim][token] = sum_j P_K[j][dim] c[token][j]: A = the basis
+//      fragments (bf16 hi + lo, held in LDS for the whole workgroup), B = the tile's key rows
+//      as staged (the score A operand of the plain decode); C lane -> token col, dims
+//      16 b + 4 grp + v for blocks b = 0..7;
+//   2. rotation: dims i and i + 64 (pair i) sit in blocks b and b + 4 of the same lane, so it
+//      is lane-local; angles from rope_cs at the token's position;
+//   3. scores by 16x16x32 MFMA, A = the rotated keys (lane -> token col; step s2 takes the
+//      lane's dims of blocks 2 s2 and 2 s2 + 1 as its 8 k-values, split into bf16 hi + lo),
+//      B = the query fragments laid out in the same dim order (hi + lo).  The C fragment is
+//      that of the plain decode (lane -> query row, tokens 4 grp + v), so the online softmax
+//      and the rank-space value product follow unchanged.
+template <bool F32, int KS, int NB>
+__device__ __forceinline__ void tile_step_rope(const TileMeta& tm, bool partial, const typename Elem<F32>::T* sK,
+                                               const typename Elem<F32>::T* sV, const u32x4* qf,
+                                               const u32x4* kmask, const u32x4* pfr,
+                                               const float* rf, float pos, int lane, int grp, float& m_run,
+                                               float& l_part) {
+    const int col = lane & 15;
+    u32x2 vh[NB], vl[NB];
+    auto gather_v = [&]() {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int j = 16 * b + col;
+            if constexpr (F32) {
+                const int a = j < tm.m ? tm.base + 16 * j + 4 * grp : DC_STAGE_BYTES / 4;
+                const f32x4 t = *reinterpret_cast<const f32x4*>(sV + a);
+                const float f4[4] = {t[0], t[1], t[2], t[3]};
+                split4(f4, vh[b], vl[b]);
+            } else {
+                const int a = j < tm.m ? tm.base + 16 * j + 4 * grp : DC_ZERO_BF16;
+                vh[b] = *reinterpret_cast<const u32x2*>(sV + a);
+                vl[b] = u32x2{0, 0};
+            }
+        }
+    };
+    if constexpr (KS < 4) gather_v();
+    // 1. reconstruction
+    f32x4 kt[8];
+#pragma unroll
+    for (int b = 0; b < 8; ++b) kt[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const int c0 = 32 * s + 8 * grp;
+        int nv = tm.m - c0;
+        nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
+        const int a = tm.base + col * tm.m + c0;
+        u32x4 kh, kl;
+        if constexpr (!F32) {
+            kh = lds_row8_bf16(reinterpret_cast<const uint32_t*>(sK), a) & kmask[nv];
+            kl = u32x4{0, 0, 0, 0};
+        } else {
+            float x8[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) { const float t = sK[a + e]; x8[e] = e < nv ? t : 0.f; }
+            split8(x8, kh, kl);
+        }
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const u32x4 ph = pfr[((s * 8 + b) * 2) * 64 + lane], pl = pfr[((s * 8 + b) * 2 + 1) * 64 + lane];
+            kt[b] = mfma(ph, kh, kt[b]);
+            kt[b] = mfma(pl, kh, kt[b]);
+            if constexpr (F32) kt[b] = mfma(ph, kl, kt[b]);
+        }
+    }
+    // 2. rotation to the token's position
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int i = 16 * b + 4 * grp + v;
+            float c, sn;
+            rope_cs(pos, rf[2 * i], rf[2 * i + 1], c, sn);
+            const float x = kt[b][v], y = kt[b + 4][v];
+            kt[b][v] = x * c - y * sn;
+            kt[b + 4][v] = x * sn + y * c;
+        }
+    }
+    // 3. scores
+    f32x4 sc = {0, 0, 0, 0};
+#pragma unroll
+    for (int s2 = 0; s2 < 4; ++s2) {
+        const float x8[8] = {kt[2 * s2][0], kt[2 * s2][1], kt[2 * s2][2], kt[2 * s2][3],
+                             kt[2 * s2 + 1][0], kt[2 * s2 + 1][1], kt[2 * s2 + 1][2], kt[2 * s2 + 1][3]};
+        u32x4 kh, kl;
+        split8(x8, kh, kl);
+        const u32x4 qh = qf[(s2 * 2) * 64 + lane], ql = qf[(s2 * 2 + 1) * 64 + lane];
+        sc = mfma(kh, qh, sc);
+        sc = mfma(kh, ql, sc);
+        sc = mfma(kl, qh, sc);
+    }
+    if constexpr (KS >= 4) gather_v();
+    float sv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sv[v] = sc[v];
+    if (partial) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sv[v] = tm.i0 + 4 * grp + v < tm.T ? sv[v] : -INFINITY;
+    }
+    float tmax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    tmax = xmax32(xmax16(tmax));
+    const bool jump = tmax > m_run + 8.f;
+    if (__builtin_amdgcn_ballot_w64(jump) != 0) {
+        const float m_new = jump ? tmax : m_run;
+        const float alpha = fast_exp(m_run - m_new);
+        l_part *= alpha;
+        acc_scale(alpha);
+        m_run = m_new;
+    }
+    float pv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        pv[v] = fast_exp(sv[v] - m_run);
+        l_part += pv[v];
+    }
+    if constexpr (F32) {
+        u32x2 ph, pl;
+        split4(pv, ph, pl);
+        acc_mfma_f32<NB>(vh, vl, ph, pl);
+    } else {
+        const u32x2 ph = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
+        acc_mfma_bf16<NB>(vh, ph);
+    }
+}
+
+// ----------------------------------------------------------------------------------------
 // Quantised coefficients (group-wise b-bit codes, Sec. 3.3 "Composability").  A coded tile
 // of size m is stored with mq = m rounded up to a multiple of 8 coordinates and KS =
 // ceil(m / 32) groups per position: K codes (16 rows of mq codes), then K scales ([KS][16]
@@ -514,9 +656,10 @@ __device__ __forceinline__ void tile_step_q(const TileMeta& tm, bool partial, co
 
 // QB = 0: coefficients stored in the layer's dtype; QB = 3, 4, 8: b-bit codes with binary16
 // group scales (bf16 layers only).
-template <bool F32, int QB, bool ANC>
-__global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel(DecParams p) {
+template <bool F32, int QB, bool ANC, bool ROPE = false>
+__global__ __launch_bounds__(DC_THREADS, (F32 || QB || ROPE) ? 2 : 4) void decode_kernel(DecParams p) {
     static_assert(QB == 0 || !F32, "quantised coefficients come from bf16 layers");
+    static_assert(!ROPE || (QB == 0 && !ANC), "rotary keys: plain coefficients, no anchors");
     typedef typename Elem<F32>::T ET;
     constexpr int EPU = 16 / (int)sizeof(ET);               // elements per 16-byte unit
     constexpr int SE = DC_STAGE_BYTES / (int)sizeof(ET);     // staged elements per stream
@@ -556,7 +699,16 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
     u32x4 pa[4][2];
     u32x4 qr[4][2];
     const int qs_ = tid >> 7, qpart = (tid >> 6) & 1;   // exact: 4 steps x {hi, lo} x 64 lanes
-    if (!exact) {
+    if (ROPE && !exact) {
+        // the query dims of score step qs_ in the rotary order (dims 32 qs_ + 4 grp .. + 3
+        // and 32 qs_ + 16 + 4 grp .. + 3); the basis fragments go to LDS below
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+            const ET* src = qv + 32 * qs_ + 16 * hf + 4 * grp;
+            if constexpr (F32) qr[0][hf] = load16(src);
+            else { const u32x2 t = *reinterpret_cast<const u32x2*>(src); qr[0][hf] = u32x4{t[0], t[1], 0u, 0u}; }
+        }
+    } else if (!exact) {
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             const float* src = P + (16 * wave + col) * D + 32 * s + 8 * grp;
@@ -584,6 +736,28 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
     if (r_ok && t_r < p.N) rv = load16(S.srank + t_r);     // srank is padded to a multiple of 64
     if (!exact && tid < ncl) cbv = S.chunk_off[c_lo + tid];
     if constexpr (QB != 0) cbv >>= 1;       // quantised chunk bases are in bytes
+    // rotary keys: the basis fragments (8 per thread), the frequency table and each stored
+    // position's token offset in its chunk
+    u32x4 frv[8];
+    if (ROPE && !exact) {
+        const u32x4* fr = p.rfrag + (int64_t)g * (4 * 8 * 2 * 64);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) frv[k] = fr[k * DC_THREADS + tid];
+    }
+    float rfv = 0.f;
+    uint32_t dp[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    const bool dp_ok = ROPE && !exact && tid < ncl * (CHUNK / 8);
+    if (ROPE && !exact) {
+        if (tid < D) rfv = p.rfreq[tid];
+        if (dp_ok) {
+            const int64_t gi0 = (int64_t)c_lo * CHUNK + 8 * tid;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                const int64_t gi = gi0 + k;
+                dp[k] = gi < p.N ? S.sidx[gi] - (uint32_t)((gi / CHUNK) * CHUNK) : 0u;
+            }
+        }
+    }
 
     lane = lane_now(); tid = 64 * wave + lane; grp = lane >> 4; col = lane & 15;
     // ---- 1c. offsets of the stored slots inside each chunk: local prefix sums of a
@@ -602,6 +776,16 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
         if (k == 15) { sm.to[cc * DC_TO + 16] = (uint16_t)incl; sm.cT[cc] = T; }
     }
     if (!exact && tid < ncl) sm.cb[tid] = cbv;
+    if (ROPE && !exact) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) sm.pfr[k * DC_THREADS + tid] = frv[k];
+        if (tid < D) sm.rf[tid] = rfv;
+        if (dp_ok) {
+            const uint32_t lo4 = dp[0] | (dp[1] << 8) | (dp[2] << 16) | (dp[3] << 24);
+            const uint32_t hi4 = dp[4] | (dp[5] << 8) | (dp[6] << 16) | (dp[7] << 24);
+            *reinterpret_cast<u32x2*>(sm.dpos + 8 * tid) = u32x2{lo4, hi4};
+        }
+    }
     // the V stage's pad holds zeros (coordinates past a token's rank read them), and the
     // K-row masks: entry nv keeps the first nv bf16 elements of an 8-element piece
     if (tid < DC_STAGE_PAD / 2)     // the zeroed pad after each V buffer
@@ -699,7 +883,21 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
     //          query loads landed with the rank loads (issued before them), so nothing here
     //          waits for the direct-to-LDS loads.
     uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf);
-    if (!exact) {
+    if (ROPE && !exact) {
+        // rotary keys: fragments of q itself (scaled), k-values in the rotary dim order
+        float v8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const u32x4& w = qr[0][e >> 2];
+            float val;
+            if constexpr (F32) val = __uint_as_float(w[e & 3]);
+            else val = (e & 1) ? bf_hi(w[(e & 3) >> 1]) : bf_lo(w[(e & 3) >> 1]);
+            v8[e] = q_ok ? val * scale : 0.f;
+        }
+        u32x4 hh, ll;
+        split8(v8, hh, ll);
+        sm.qf[(qs_ * 2 + qpart) * 64 + lane] = qpart ? ll : hh;
+    } else if (!exact) {
         // q' = P_K q / sqrt(d) by MFMA; C lane -> query row col, directions 16 wave + 4 grp + v
         u32x4 qb[4][2];
 #pragma unroll
@@ -794,7 +992,14 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB) ? 2 : 4) void decode_kernel
                 // a tile's size bounds its 32-coefficient score steps and 16-wide value
                 // blocks, as compile-time bounds (no branches inside)
                 const bool partial = __builtin_amdgcn_readfirstlane(tm.i0 + 16 > tm.T ? 1 : 0) != 0;
-                if constexpr (QB != 0) {
+                if constexpr (ROPE) {
+                    const int ip = (tile & 15) * 16 + col;
+                    const float pos = (float)(((tile >> 4) * CHUNK) + (int)sm.dpos[cc * CHUNK + ip]);
+                    if (tm.m <= 16) tile_step_rope<F32, 1, 1>(tm, partial, sK, sV, sm.qf, sm.kmask, sm.pfr, sm.rf, pos, ln, grp, m_run, l_part);
+                    else if (tm.m <= 32) tile_step_rope<F32, 1, 2>(tm, partial, sK, sV, sm.qf, sm.kmask, sm.pfr, sm.rf, pos, ln, grp, m_run, l_part);
+                    else if (tm.m <= 64) tile_step_rope<F32, 2, 4>(tm, partial, sK, sV, sm.qf, sm.kmask, sm.pfr, sm.rf, pos, ln, grp, m_run, l_part);
+                    else tile_step_rope<F32, 4, 8>(tm, partial, sK, sV, sm.qf, sm.kmask, sm.pfr, sm.rf, pos, ln, grp, m_run, l_part);
+                } else if constexpr (QB != 0) {
                     const uint16_t* qK = reinterpret_cast<const uint16_t*>(sK);
                     const uint16_t* qV = reinterpret_cast<const uint16_t*>(sV);
                     if (tm.m <= 16) tile_step_q<QB, 1, 1, ANC>(tm, partial, qK, qV, sm.qf, ln, grp, m_run, l_part);
@@ -1392,7 +1597,8 @@ static size_t anc_dec_bytes(const DecPlan& pl, size_t units, int64_t N) {
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
     DecPlan pl = plan_decode(sh, S, Q);
     const size_t units = (size_t)S * sh.G * pl.nqt;
-    return align256(units * pl.nrec * DC_REC * sizeof(float)) + anc_dec_bytes(pl, units, coded_count(sh));
+    const size_t rope = sh.rope ? align256((size_t)sh.G * ROPE_FRAG_BYTES) + align256(D * sizeof(float)) : 0;
+    return align256(units * pl.nrec * DC_REC * sizeof(float)) + anc_dec_bytes(pl, units, coded_count(sh)) + rope;
 }
 
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
@@ -1405,7 +1611,10 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     const bool anc = pl.na > 0;
     typedef void (*DecFn)(DecParams);
     DecFn kfn;
-    if (sh.dtype != VARRATE_BF16) kfn = decode_kernel<true, 0, false>;
+    const bool rope = sh.rope != 0;
+    if (rope && (qb != 0 || anc)) return hipErrorInvalidValue;
+    if (rope) kfn = sh.dtype != VARRATE_BF16 ? decode_kernel<true, 0, false, true> : decode_kernel<false, 0, false, true>;
+    else if (sh.dtype != VARRATE_BF16) kfn = decode_kernel<true, 0, false>;
     else if (!anc) kfn = qb == 3 ? decode_kernel<false, 3, false> : qb == 4 ? decode_kernel<false, 4, false>
                        : qb == 8 ? decode_kernel<false, 8, false> : decode_kernel<false, 0, false>;
     else kfn = qb == 3 ? decode_kernel<false, 3, true> : qb == 4 ? decode_kernel<false, 4, true>
@@ -1436,10 +1645,24 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         b += align256(units_all * pl.na * pl.ns * 4);
         Fb = (float*)b;
     }
+    // rotary keys: the basis fragments and the frequency table after the records, prepared
+    // once per call
+    const u32x4* rfrag = nullptr;
+    const float* rfreq = nullptr;
+    hipError_t e;
+    if (rope) {
+        if (reuse_group_region) return hipErrorInvalidValue;   // no fixed scratch for it
+        uint8_t* b = ws + align256(units_all * pl.nrec * DC_REC * sizeof(float));
+        rfrag = reinterpret_cast<const u32x4*>(b);
+        float* fq = reinterpret_cast<float*>(b + align256((size_t)sh.G * ROPE_FRAG_BYTES));
+        rfreq = fq;
+        e = launch_rope_prep(sh, PK, b, fq, st);
+        if (e != hipSuccess) return e;
+    }
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
-    const size_t lds = decode_smem_bytes(pl.cpw);
-    hipError_t e = ensure_lds_limit((const void*)kfn, lds);
+    const size_t lds = decode_smem_bytes(pl.cpw, rope);
+    e = ensure_lds_limit((const void*)kfn, lds);
     if (e != hipSuccess) return e;
     for (int s0 = 0; s0 < S; s0 += DC_SEQ) {
         const int ns = S - s0 < DC_SEQ ? S - s0 : DC_SEQ;
@@ -1452,10 +1675,12 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
             const uint32_t* co = qb ? qcaches[s0 + i].qchunk_off : c.chunk_off;
             prm.seq[i] = DecSeq{ck, cv, c.srank, co, c.k_exact, c.v_exact,
                                 (const uint8_t*)q + (s0 + i) * qstride, (uint8_t*)out + (s0 + i) * qstride,
-                                c.n_exact};
+                                c.n_exact, c.sidx};
         }
         for (int i = ns; i < DC_SEQ; ++i) prm.seq[i] = prm.seq[0];
         prm.PK = PK;
+        prm.rfrag = rfrag;
+        prm.rfreq = rfreq;
         prm.PV = PV;
         // launch groups run in stream order, so with reuse_group_region every group's records
         // go to the start of the buffer (the previous group's merge has finished reading them)

@@ -123,6 +123,19 @@ __device__ __forceinline__ float xsum32(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Rotary embedding angle (Sec. 3.1 "Joint per-token vector"): cos and sin of p * theta for
+// an integer position p < 2^24, with theta / (2 pi) given as the double-float fhi + flo.  The
+// product's whole turns are removed exactly (fmaf returns p * fhi - prod exactly), and the
+// remaining fraction of a turn (|r| < 1, error ~2^-25 turns) goes to the hardware sine and
+// cosine, which take their argument in turns.
+__device__ __forceinline__ void rope_cs(float p, float fhi, float flo, float& c, float& s) {
+    const float prod = p * fhi;
+    const float err = fmaf(p, fhi, -prod);
+    const float r = (prod - rintf(prod)) + (err + p * flo);
+    s = __builtin_amdgcn_sinf(r);
+    c = __builtin_amdgcn_cosf(r);
+}
+
 // exp(x) on the hardware exp2 path (x * log2 e); -inf -> 0.
 __device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
 

@@ -58,6 +58,15 @@ hipError_t launch_anchor_encode(const varrate_shape& sh, const void* K, const vo
                                 const uint16_t* nn, const float* PK, const float* PV, varrate_cache& c,
                                 const AnchorWs& w, hipStream_t st);
 
+// Rotary keys: theta / (2 pi) per pair as a double-float (hi + lo), for the kernel arguments
+struct RopeFreq { float hi[D / 2], lo[D / 2]; };
+RopeFreq rope_freq(const varrate_shape& sh);
+// Kr [n][G][d] = K with rows t < N turned back by -t (rounded to dtype), rows >= N copied
+hipError_t launch_rope_unrotate(const varrate_shape& sh, const void* K, void* Kr, hipStream_t st);
+// decode operands: basis fragments [G][4][8][2][64] u32x4 and the frequency table [128] fp32
+constexpr size_t ROPE_FRAG_BYTES = (size_t)4 * 8 * 2 * 64 * 16;   // per KV head
+hipError_t launch_rope_prep(const varrate_shape& sh, const float* PK, void* frags, float* freq, hipStream_t st);
+
 size_t salience_ws_bytes(const varrate_shape& sh);
 size_t allocate_ws_bytes(const varrate_shape& sh);
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q);

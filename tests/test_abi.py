@@ -3,6 +3,7 @@ host-side validation returns the documented status codes before anything is enqu
 import ctypes
 import os
 import re
+import subprocess
 
 import pytest
 
@@ -30,15 +31,27 @@ def test_every_declared_symbol_is_exported(L):
         assert hasattr(L, name), name
 
 
-def test_struct_sizes_match_header():
+def test_struct_sizes_match_header(tmp_path):
+    """The ctypes mirrors have the C layout: sizes and field offsets as gcc lays out the
+    header's structs."""
     from paper_2607_15498_amd import _lib
-    assert ctypes.sizeof(_lib.Shape) == 40
+    prog = tmp_path / "probe.c"
+    prog.write_text(
+        '#include <stddef.h>\n#include <stdio.h>\n#include "varrate.h"\n'
+        'int main(void) { printf("%zu %zu %zu %zu %zu\\n", sizeof(varrate_shape), offsetof(varrate_shape, rope),'
+        ' offsetof(varrate_shape, rope_theta), sizeof(varrate_cache), sizeof(varrate_qcache)); return 0; }\n')
+    exe = tmp_path / "probe"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(prog)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], stdout=subprocess.PIPE, text=True, check=True).stdout.split()]
+    assert got == [ctypes.sizeof(_lib.Shape), _lib.Shape.rope.offset, _lib.Shape.rope_theta.offset,
+                   ctypes.sizeof(_lib.CacheC), ctypes.sizeof(_lib.QCacheC)]
     assert ctypes.sizeof(_lib.CacheC) == 8 * 8 + 5 * 8 + 8 * 8
 
 
 def _shape(**kw):
     from paper_2607_15498_amd import _lib
-    base = dict(n=32768, G=8, H=32, d=128, w=32, r_min=16, kappa_pct=20, dtype=_lib.VARRATE_BF16, anchor_stride=0)
+    base = dict(n=32768, G=8, H=32, d=128, w=32, r_min=16, kappa_pct=20, dtype=_lib.VARRATE_BF16, anchor_stride=0,
+                rope=0)
     base.update(kw)
     return _lib.Shape(**base)
 
@@ -134,10 +147,11 @@ def test_decode_accumulator_agprs_are_private():
         assert r.returncode == 0, r.stdout[-2000:]
         text = open(out).read()
     agpr = re.compile(r"\ba\d+\b|\ba\[\d+:\d+\]|v_accvgpr")
-    kernels = re.findall(r"^(_ZN2vr13decode_kernelILb[01]ELi\d+ELb[01]EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm",
+    kernels = re.findall(r"^(_ZN2vr13decode_kernelILb[01]ELi\d+ELb[01]ELb[01]EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm",
                          text, re.S | re.M)
-    # fp32; bf16 and bf16 with 3-, 4- and 8-bit codes, each with and without anchors
-    assert len(kernels) == 9
+    # fp32; bf16 and bf16 with 3-, 4- and 8-bit codes, each with and without anchors; rotary
+    # keys in fp32 and bf16
+    assert len(kernels) == 11
     for name, body in kernels:
         inside = False
         for line in body.splitlines():
@@ -198,3 +212,27 @@ def test_residual_codec_sizes_and_validation(L):
     # no anchors: the anchor buffers are empty
     assert L.varrate_cache_bytes(ctypes.byref(_shape()), 32, ctypes.byref(out)) == 0
     assert out.na == 0 and out.k_anchor == 0 and out.snn == 0 and out.inv_pos == 0
+
+
+def test_rotary_keys_validation(L):
+    """Rotary keys: flag in {0, 1}, finite non-negative frequencies, and the combinations
+    with no rotary kernels (anchors, quantised coefficients, the fixed-scratch decode) are
+    refused before anything is enqueued."""
+    from paper_2607_15498_amd import _lib
+    th = (ctypes.c_float * 64)(*([1e-3] * 64))
+    out = _lib.CacheBytes()
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(rope=1, rope_theta=th)), 64, ctypes.byref(out)) == 0
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(rope=2, rope_theta=th)), 64, ctypes.byref(out)) == -1
+    bad = (ctypes.c_float * 64)(*([1e-3] * 63 + [float("nan")]))
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(rope=1, rope_theta=bad)), 64, ctypes.byref(out)) == -1
+    neg = (ctypes.c_float * 64)(*([-1.0] + [1e-3] * 63))
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(rope=1, rope_theta=neg)), 64, ctypes.byref(out)) == -1
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(rope=1, rope_theta=th, anchor_stride=16)), 64,
+                                 ctypes.byref(out)) == -3
+    sh = _shape(rope=1, rope_theta=th)
+    # the un-rotated key copy is part of the compress workspace
+    assert L.varrate_compress_workspace_bytes(ctypes.byref(sh)) >= \
+        L.varrate_compress_workspace_bytes(ctypes.byref(_shape())) + 32768 * 8 * 128 * 2
+    cc = _lib.CacheC()
+    qc = _lib.QCacheC()
+    assert L.varrate_quantize(ctypes.byref(sh), ctypes.byref(cc), ctypes.byref(qc), None) == -3
