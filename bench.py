@@ -399,6 +399,8 @@ def main():
     # residual codec (Sec. 3.1 Eq. 2): anchors every 16 tokens kept exact, the other tokens
     # coded as residuals to their 4 nearest anchors' mean; same layer, budget and floor
     result["residual_codec"] = bench_anchor(args, shape, Ks, Vs, Qw, q, PK, PV, out, cap_stream)
+    # rotary keys: a 32K layer of the same geometry whose cache is post-RoPE
+    result["rotary_keys"] = bench_rope(args, cap_stream)
     if not args.no_stack:
         # the 128K end of the 32K-128K target range: the 32-layer Llama stack, decode at batch 1
         del graphs, step_graphs, slots, Ks, Vs, sbars
@@ -420,6 +422,62 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, li, dbytes, {"decode_ms": ms_dec, "compress_ms": ms_comp})
     print(json.dumps(result), flush=True)
+
+
+def bench_rope(args, cap_stream, n_slots=12):
+    """Rotary keys (Sec. 3.1 "Joint per-token vector"; Algorithm 1 first and last steps) on a
+    32K layer of the same geometry with Llama-3.1 frequencies: compress (salience on the
+    post-RoPE cache, un-rotation, allocation, projection) and decode (keys rebuilt by MFMA and
+    rotated to their positions), each replayed from a graph over `n_slots` caches."""
+    import ctypes
+    import torch
+
+    import paper_2607_15498_amd as vr
+    from workloads import CONFIGS, make_layer
+    cfg = CONFIGS["llama_32k_rope"]
+    li = make_layer(cfg, n_queries=1)
+    sh = vr.Shape(n=cfg["n"], G=cfg["G"], H=cfg["H"], w=cfg["w"], r_min=cfg["r_min"], kappa_pct=cfg["kappa"],
+                  dtype=cfg["dtype"], rope_theta=tuple(float(x) for x in li.theta))
+    dev = torch.device("cuda:0")
+    up = lambda a, t=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(t).to(dev)
+    Ks = [up(li.K) for _ in range(N_INPUT_COPIES)]
+    Vs = [up(li.V) for _ in range(N_INPUT_COPIES)]
+    Qw, q = up(li.Qw), up(li.q)
+    PK, PV = up(li.PK, torch.float32), up(li.PV, torch.float32)
+    out = torch.empty_like(q)
+    slots = [vr.new_cache(sh, device=dev) for _ in range(n_slots)]
+    wsc = torch.zeros(vr.library().varrate_compress_workspace_bytes(ctypes.byref(sh.c())), dtype=torch.uint8,
+                      device=dev)
+    wsd = vr.decode_workspace(sh, 1, 1, dev)
+    for i, c in enumerate(slots):
+        vr.compress(sh, Ks[i % len(Ks)], Vs[i % len(Vs)], Qw, PK, PV, cache=c, workspace=wsc)
+    torch.cuda.synchronize()
+    gc, gd = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gc, stream=cap_stream):
+        for i, c in enumerate(slots):
+            vr.compress(sh, Ks[i % len(Ks)], Vs[i % len(Vs)], Qw, PK, PV, cache=c, workspace=wsc)
+    with torch.cuda.graph(gd, stream=cap_stream):
+        for i in range(n_slots):
+            vr.decode(sh, [slots[(i + n_slots // 2) % n_slots]], q, PK, PV, out=out, workspace=wsd)
+    torch.cuda.synchronize()
+    stc = _replay_stats(gc, 3, n_slots)
+    std = _replay_stats(gd, 8, n_slots)
+    # the plain decode's bytes plus each stored position's token index (read once per KV head)
+    by = decode_bytes(sh, slots[0]) + sh.G * slots[0].N * 4
+    flops = 2.0 * sh.G * 128 * int(slots[0].rank[:slots[0].N].to(torch.int64).sum()) + 2.0 * sh.H * slots[0].N * 128
+    res = {
+        "config": f"llama_32k_rope: 1 layer, 8 KV x 32 q heads, n {sh.n}, w {sh.w}, budget {sh.kappa_pct}%, "
+                  f"r_min {sh.r_min}, Llama-3.1 rotary frequencies (base 500000, scaling 8)",
+        "compress_ms_per_32k_tokens": round(stc["p50"] * 32768 / sh.n, 4),
+        "compress_ms_p10_p90": [round(stc["p10"], 4), round(stc["p90"], 4)],
+        "decode_ms": round(std["p50"], 4), "decode_ms_p10_p90": [round(std["p10"], 4), round(std["p90"], 4)],
+        "decode_GBps": round(by / (std["p50"] * 1e-3) / 1e9, 2),
+        "frac": round(by / (std["p50"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "decode_bytes": int(by),
+        "decode_key_rebuild_GFLOP": round(flops / 1e9, 3),
+    }
+    del gc, gd, slots, Ks, Vs
+    return res
 
 
 def decode_bytes_anchor(shape, cache, n_queries=1):
