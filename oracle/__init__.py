@@ -78,6 +78,11 @@ def lib():
         L.vro_decode.restype = None
         L.vro_decode.argtypes = [_i64, _i64, _int, _int, _int, _f32p, _f32p, _i32p,
                                  _f32p, _f32p, _f32p, _f32p, _f32p, _f64p]
+        L.vro_project_joint.restype = None
+        L.vro_project_joint.argtypes = [_i64, _int, _int, _int, _f32p, _f32p, _f32p, _i32p, _int, _f32p]
+        L.vro_decode_joint.restype = None
+        L.vro_decode_joint.argtypes = [_i64, _i64, _int, _int, _int, _int, _f32p, _i32p, _f32p, _f32p,
+                                       _f32p, _f32p, _f64p]
         L.vro_rope.restype = None
         L.vro_rope.argtypes = [_i64, _int, _int, _f32p, _i64p, _f32p, _int, _f64p]
         L.vro_decode_rope.restype = None
@@ -382,3 +387,62 @@ def decode_rope(comp: Compressed, PK, PV, q, H: int, theta: np.ndarray, Kx=None,
                           _c(PK, np.float32), _c(PV, np.float32), _c(q, np.float32),
                           np.arange(N, dtype=np.int64), _c(theta, np.float32), out)
     return out
+
+
+# ---------------------------------------------------------------------------------------
+# Sec. 3.1 Eq. (1) "Joint per-token vector" and "Shared basis": one basis W in R^{R x Dz},
+# Dz = 2 G d, codes z_t = [k_t (all heads); v_t (all heads)]; a token at rank r costs r
+# scalars, so Eq. (3) is B = floor(kappa n Dz / 100) - w Dz and ranks run r_min..R.
+
+def project_joint(K: np.ndarray, V: np.ndarray, W: np.ndarray, rank: np.ndarray, storage: str) -> np.ndarray:
+    """Eq. (6) with the shared basis: c_t = W z_t truncated to rank[t], storage-rounded.
+    K, V [n][G][d]; W [R][2 G d] -> coef [n][R]."""
+    n, G, d = K.shape
+    R = W.shape[0]
+    out = np.zeros((n, R), np.float32)
+    lib().vro_project_joint(n, G, d, R, _c(K, np.float32), _c(V, np.float32), _c(W, np.float32),
+                            _c(rank, np.int32), 1 if storage == "bf16" else 0, out)
+    return out
+
+
+def decode_joint(coef, rank, Kx, Vx, W, q, H: int) -> np.ndarray:
+    """Reconstruct-in-place decode with the shared basis for one query set q [H][d] (fp64)."""
+    N, R = coef.shape
+    n_exact, G, d = Kx.shape
+    out = np.zeros((H, d), np.float64)
+    lib().vro_decode_joint(N, n_exact, G, H, d, R, _c(coef, np.float32), _c(rank, np.int32),
+                           _c(Kx, np.float32), _c(Vx, np.float32), _c(W, np.float32), _c(q, np.float32), out)
+    return out
+
+
+@dataclass
+class JointCompressed:
+    sbar: np.ndarray     # fp32 pooled salience [N]
+    u: np.ndarray        # uint32 weights [N]
+    alloc: Allocation    # ranks in 0..R (joint units)
+    B: int               # coded budget in joint units
+    coef: np.ndarray     # [N][R] storage-rounded coefficients
+    Kx: np.ndarray       # exact window rows [w][G][d]
+    Vx: np.ndarray
+
+
+def joint_budget(n: int, G: int, d: int, w: int, kappa_pct: int) -> int:
+    """Eq. (3) in joint units: floor(kappa n Dz / 100) - w Dz, Dz = 2 G d."""
+    return budget(n, 2 * G * d, w, kappa_pct)
+
+
+def compress_joint(K, V, Qw, W, H: int, kappa_pct: int, r_min: int, storage: str,
+                   sbar: np.ndarray | None = None) -> JointCompressed:
+    """Algorithm 1 with the shared cross-head basis (no anchors, no RoPE): the salience,
+    pooling and weights of the per-head codec, water-filling of the joint budget with cap
+    R = W.shape[0], one coefficient row per token for every head and both K and V."""
+    n, G, d = K.shape
+    w = Qw.shape[0]
+    N = n - w
+    R = W.shape[0]
+    B = joint_budget(n, G, d, w, kappa_pct)
+    sb = pool(salience(K, Qw, H)) if sbar is None else _c(sbar, np.float32)
+    u = weights(sb)
+    al = allocate(u, B, r_min, R)
+    coef = project_joint(K[:N], V[:N], W, al.rank, storage)
+    return JointCompressed(sb, u, al, B, coef, np.ascontiguousarray(K[N:]), np.ascontiguousarray(V[N:]))

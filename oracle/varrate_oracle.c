@@ -595,3 +595,83 @@ EXPORT void vro_decode_anchor(int64_t Nc, int64_t na, int64_t n_exact, int G, in
     free(vh);
     free(x);
 }
+
+/* ------------------------------------------------------------------------------------- */
+/* Sec. 3.1 Eq. (1) "Joint per-token vector" with one shared basis: z_t = [k_t of all G heads;
+ * v_t of all G heads] in R^Dz, Dz = 2 G d, and a basis W in R^{R x Dz} (row j = j-th
+ * direction).  Eq. (6): c_t = W z_t at full rank, the leading rank[t] coefficients kept, the
+ * rest 0, rounded to the storage type.  Layouts: K, V [n_tok][G][d]; W [R][Dz];
+ * coef [n_tok][R].                                                                         */
+EXPORT void vro_project_joint(int64_t n_tok, int G, int d, int R, const float *K, const float *V,
+                              const float *W, const int32_t *rank, int storage_bf16, float *coef)
+{
+    const int half = G * d, Dz = 2 * G * d;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < n_tok; ++t) {
+        const float *kt = K + t * half, *vt = V + t * half;
+        float *c = coef + t * R;
+        for (int j = 0; j < R; ++j) {
+            if (j >= rank[t]) { c[j] = 0.0f; continue; }
+            const float *w = W + (int64_t)j * Dz;
+            double acc = dot_fd(w, kt, half) + dot_fd(w + half, vt, half);
+            c[j] = storage_bf16 ? (float)round_bf16(acc) : (float)acc;
+        }
+    }
+}
+
+/* Sec. 4.4 decode, reconstruct-in-place, shared basis: z_hat_t = W^T (m_t . c_t) split into
+ * the keys and values of every head (Eq. 6 with zbar = 0); exact rows as stored; then stock
+ * attention per query head h over KV head h / (H / G), fp64.
+ * Layouts: coef [N][R], Kx/Vx [n_exact][G][d], W [R][Dz], q [H][d], out [H][d].            */
+EXPORT void vro_decode_joint(int64_t N, int64_t n_exact, int G, int H, int d, int R,
+                             const float *coef, const int32_t *rank, const float *Kx, const float *Vx,
+                             const float *W, const float *q, double *out)
+{
+    const int hpg = H / G, half = G * d, Dz = 2 * G * d;
+    const double scale = 1.0 / sqrt((double)d);
+    const int64_t T = N + n_exact;
+    double *zh = (double *)malloc(sizeof(double) * (size_t)(N > 0 ? N : 1) * Dz);
+    double *x = (double *)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1));
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < N; ++t) {
+        const float *c = coef + t * R;
+        double *z = zh + t * Dz;
+        for (int i = 0; i < Dz; ++i) z[i] = 0.0;
+        for (int j = 0; j < rank[t]; ++j) {
+            const float *w = W + (int64_t)j * Dz;
+            for (int i = 0; i < Dz; ++i) z[i] += (double)c[j] * (double)w[i];
+        }
+    }
+    for (int h = 0; h < H; ++h) {
+        const int g = h / hpg;
+        const float *qh = q + (int64_t)h * d;
+        double m = -INFINITY;
+        for (int64_t t = 0; t < T; ++t) {
+            double acc = 0.0;
+            if (t < N) {
+                const double *k = zh + t * Dz + (int64_t)g * d;
+                for (int i = 0; i < d; ++i) acc += (double)qh[i] * k[i];
+            } else {
+                acc = dot_fd(qh, Kx + ((t - N) * G + g) * d, d);
+            }
+            x[t] = acc * scale;
+            if (x[t] > m) m = x[t];
+        }
+        double zs = 0.0;
+        for (int64_t t = 0; t < T; ++t) { x[t] = exp(x[t] - m); zs += x[t]; }
+        double *o = out + (int64_t)h * d;
+        for (int i = 0; i < d; ++i) o[i] = 0.0;
+        for (int64_t t = 0; t < T; ++t) {
+            const double a = x[t] / zs;
+            if (t < N) {
+                const double *v = zh + t * Dz + half + (int64_t)g * d;
+                for (int i = 0; i < d; ++i) o[i] += a * v[i];
+            } else {
+                const float *v = Vx + ((t - N) * G + g) * d;
+                for (int i = 0; i < d; ++i) o[i] += a * (double)v[i];
+            }
+        }
+    }
+    free(zh);
+    free(x);
+}

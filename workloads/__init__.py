@@ -12,6 +12,7 @@ from .synth import (  # noqa: F401
     make_layer,
     make_head_model,
     rope_theta,
+    joint_calibration_basis,
     calibration_basis,
     decode_queries,
     seed_for,

@@ -48,6 +48,10 @@ CONFIGS: Dict[str, dict] = {
                       dtype="f32", seed=6, values="keys", batch=1, rope="llama3"),
     "llama_32k_rope": dict(layers=1, G=8, H=32, d=128, n=32768, w=32, kappa=20, r_min=16,
                            dtype="bf16", seed=7, values="lowrank", batch=1, rope="llama3"),
+    "tiny_joint": dict(layers=1, G=1, H=2, d=128, n=512, w=32, kappa=20, r_min=16,
+                       dtype="f32", seed=8, values="keys", batch=1, joint_R=256),
+    "llama_32k_joint": dict(layers=1, G=8, H=32, d=128, n=32768, w=32, kappa=20, r_min=16,
+                            dtype="bf16", seed=9, values="lowrank", batch=1, joint_R=1024),
     "agnostic_32k": dict(layers=1, G=8, H=32, d=128, n=32768, w=32, kappa=20, r_min=16,
                          dtype="bf16", seed=4, values="lowrank", batch=1, queries=64,
                          budgets=((10, 8), (20, 16), (40, 16))),
@@ -215,6 +219,31 @@ def calibration_basis(base: int, layer: int, head: int, hm: HeadModel, d: int,
     return out[0], out[1]
 
 
+def joint_calibration_basis(cfg: dict, layer: int, head_models, R: int) -> np.ndarray:
+    """Offline shared basis (Sec. 3.1 "Shared basis"): the top-R eigenvectors of the uncentred
+    second moment of 8192 calibration joint vectors z = [k (all heads); v (all heads)], drawn
+    from the same disjoint seeds as the per-head bases; rows in descending-eigenvalue order,
+    each row's largest-magnitude entry positive.  float32 [R][2 G d]."""
+    G, d = cfg["G"], cfg["d"]
+    base = cfg["seed"]
+    Z = np.empty((CALIB_DRAWS, 2 * G * d))
+    for g in range(G):
+        hm = head_models[g]
+        rk = _rng(base + CALIB_SEED_OFFSET, layer, g, 0, _S_KEYS)
+        rv = _rng(base + CALIB_SEED_OFFSET, layer, g, 0, _S_VALS)
+        Z[:, g * d:(g + 1) * d], _ = _draw_keys(rk, hm, CALIB_DRAWS, CALIB_DRAWS, d)
+        Z[:, (G + g) * d:(G + g + 1) * d] = _draw_values(rv, hm, CALIB_DRAWS, d, cfg["values"])
+    c = Z.T @ Z / CALIB_DRAWS
+    evals, evecs = np.linalg.eigh(c)
+    order = np.argsort(-evals, kind="stable")[:R]
+    W = evecs[:, order].T.copy()
+    for j in range(R):
+        i = int(np.argmax(np.abs(W[j])))
+        if W[j, i] < 0:
+            W[j] = -W[j]
+    return W.astype(np.float32)
+
+
 @dataclasses.dataclass
 class LayerInputs:
     K: np.ndarray      # [n, G, d] float32 (values exactly representable in the storage dtype)
@@ -226,6 +255,7 @@ class LayerInputs:
     planted: list      # per KV head: planted coded-token indices
     cfg: dict
     theta: Optional[np.ndarray] = None   # rotary frequencies [d/2] (RoPE configs), else None
+    W: Optional[np.ndarray] = None       # shared cross-head basis [R][2 G d] (joint configs), else None
 
 
 def decode_queries(cfg: dict, layer: int, seq: int, n_q: int, law: str,
@@ -248,7 +278,8 @@ def decode_queries(cfg: dict, layer: int, seq: int, n_q: int, law: str,
 def make_layer(cfg: dict, layer: int = 0, seq: int = 0, n_queries: int = 1,
                query_law: str = "aware", n: Optional[int] = None,
                with_basis: bool = True) -> LayerInputs:
-    """Draw one layer of one sequence.  ``n`` overrides the config's prompt length."""
+    """Draw one layer of one sequence.  ``n`` overrides the config's prompt length.  Configs
+    with ``joint_R`` also carry the shared cross-head basis of that many rows."""
     G, H, d, w = cfg["G"], cfg["H"], cfg["d"], cfg["w"]
     n = cfg["n"] if n is None else n
     base = cfg["seed"]
@@ -281,4 +312,5 @@ def make_layer(cfg: dict, layer: int = 0, seq: int = 0, n_queries: int = 1,
             PK[g], PV[g] = calibration_basis(base, layer, g, hms[g], d, cfg["values"])
     else:
         PK = PV = None
-    return LayerInputs(K, V, Qw, q, PK, PV, planted, cfg, theta)
+    W = joint_calibration_basis(cfg, layer, hms, cfg["joint_R"]) if with_basis and cfg.get("joint_R") else None
+    return LayerInputs(K, V, Qw, q, PK, PV, planted, cfg, theta, W)
