@@ -312,6 +312,66 @@ VARRATE_API int varrate_decode_attn_noalloc(const varrate_shape* shape, const va
                                 const void* q, int32_t Q, const float* P_K, const float* P_V,
                                 void* out, void* stream);
 
+/* ---- shared cross-head basis ------------------------------------------------------------
+ * Sec. 3.1 Eq. (1) "Joint per-token vector" and "Shared basis": every head's key and value of
+ * a token form one vector z_t = [k_t of all G heads; v_t of all G heads] of Dz = 2 G d
+ * entries, coded against ONE basis W in R^{R x Dz} (fp32, row j = j-th direction,
+ * orthonormal rows; R a multiple of 128, 128 <= R <= min(1024, Dz)).  A coded token keeps
+ * the leading r_t coefficients of c_t = W z_t (Eq. 6), one row for all heads and both K and
+ * V, so a token at rank r costs r scalars and Eq. (3) reads B = floor(kappa n Dz / 100) -
+ * w Dz, with ranks r_min <= r_t <= R (EBUDGET otherwise).  Salience, pooling and the exact
+ * water-filling are those of the per-head codec (cap R instead of 128).  Position-free
+ * keys, no anchors (shape->rope and shape->anchor_stride must be 0).
+ * Layout (original token order): token t's coefficients are coef[offset[t] .. offset[t] +
+ * rank[t]), offset = exclusive prefix sum of rank (offset[N] = B); chunk_off[c] = offset of
+ * token 256 c.  Exact rows as in varrate_cache.  Decode: every query row (query x head) is
+ * rotated into rank space once, q'_h = W_K,g q_h / sqrt(d) (W_K,g = the columns of head g's
+ * keys), scored against the shared rows, and the rank-space value sums are rotated back by
+ * W_V,g^T.  At most 32 query rows (Q H <= 32) per decode.                                    */
+typedef struct varrate_jcache {
+    void*     coef;         /* [coef_stride] dtype                                            */
+    uint16_t* rank;         /* [N], allocation padded to a multiple of 64 bytes                */
+    uint32_t* offset;       /* [N + 1]                                                        */
+    uint32_t* chunk_off;    /* [n_chunks + 1]                                                 */
+    void*     k_exact;      /* [G][cap][d] dtype                                              */
+    void*     v_exact;      /* [G][cap][d] dtype                                              */
+    int64_t   coef_stride;  /* elements, >= B + VARRATE_JOINT_PAD                             */
+    int64_t   cap;          /* exact-slot capacity, >= w                                      */
+    int64_t   n_exact;      /* exact slots in use                                             */
+    int64_t   N;            /* coded tokens                                                   */
+    int64_t   B;            /* coded budget in joint units                                    */
+    int32_t   R;            /* basis rows                                                     */
+    int32_t   reserved;
+} varrate_jcache;
+#define VARRATE_JOINT_PAD 2048  /* elements after B that decode may read (staging slack)      */
+
+typedef struct varrate_jcache_bytes_t {
+    int64_t N, B, n_chunks, coef_stride;
+    size_t coef, rank, offset, chunk_off, k_exact, v_exact;
+} varrate_jcache_bytes_t;
+
+/* Sizes of one shared-basis cache with exact capacity cap (>= w); validates the shape and
+ * the budget for R basis rows.                                                              */
+VARRATE_API int varrate_jcache_bytes(const varrate_shape* shape, int32_t R, int64_t cap,
+                                     varrate_jcache_bytes_t* out);
+VARRATE_API size_t varrate_joint_compress_workspace_bytes(const varrate_shape* shape, int32_t R);
+VARRATE_API size_t varrate_joint_decode_workspace_bytes(const varrate_shape* shape, int32_t R, int32_t S,
+                                                        int32_t Q);
+/* Algorithm 1 with the shared basis W [R][2 G d] (fp32): salience (sbar_out [N] when
+ * non-NULL), water-filling of the joint budget with cap R, projection of z_t onto W truncated
+ * to each rank.  Fills cache (R taken from cache->R) and copies the window rows.            */
+VARRATE_API int varrate_joint_compress(const varrate_shape* shape, const void* K, const void* V, const void* Qw,
+                                       const float* W, varrate_jcache* cache, float* sbar_out, void* workspace,
+                                       size_t workspace_bytes, void* stream);
+/* Decode attention over S shared-basis caches (same shape and R): q [S][Q][H][d] -> out
+ * [S][Q][H][d], Q H <= 32.                                                                   */
+VARRATE_API int varrate_joint_decode_attn(const varrate_shape* shape, const varrate_jcache* caches, int32_t S,
+                                          const void* q, int32_t Q, const float* W, void* out, void* workspace,
+                                          size_t workspace_bytes, void* stream);
+/* varrate_append_exact for a shared-basis cache.                                             */
+VARRATE_API int varrate_joint_append_exact(const varrate_shape* shape, varrate_jcache* cache, const void* k_new,
+                                           const void* v_new, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -376,3 +376,106 @@ def anchor_encode(shape: Shape, K, V, sbar: torch.Tensor, nn: torch.Tensor, PK, 
                                            ws.numel(), _stream()))
     cache._update(cc)
     return cache
+
+
+# ---------------------------------------------------------------------------------------
+# Shared cross-head basis (Sec. 3.1 Eq. (1) "Joint per-token vector" and "Shared basis"): one
+# basis W [R][2 G d] codes z_t = [k_t (all heads); v_t (all heads)], one coefficient row per
+# token for every head and both K and V, in original token order.
+
+@dataclasses.dataclass
+class JCache:
+    coef: torch.Tensor
+    rank: torch.Tensor          # [N] int16 (values 0..R)
+    offset: torch.Tensor        # [N + 1] int32
+    chunk_off: torch.Tensor
+    k_exact: torch.Tensor
+    v_exact: torch.Tensor
+    coef_stride: int
+    cap: int
+    R: int
+    n_exact: int = 0
+    N: int = 0
+    B: int = 0
+
+    def c(self) -> _lib.JCacheC:
+        return _lib.JCacheC(self.coef.data_ptr(), self.rank.data_ptr(), self.offset.data_ptr(),
+                            self.chunk_off.data_ptr(), self.k_exact.data_ptr(), self.v_exact.data_ptr(),
+                            self.coef_stride, self.cap, self.n_exact, self.N, self.B, self.R, 0)
+
+    def _update(self, cc: _lib.JCacheC):
+        self.n_exact, self.N, self.B = int(cc.n_exact), int(cc.N), int(cc.B)
+
+
+def jcache_bytes(shape: Shape, R: int, cap: int) -> _lib.JCacheBytes:
+    out = _lib.JCacheBytes()
+    _check(library().varrate_jcache_bytes(ctypes.byref(shape.c()), R, cap, ctypes.byref(out)))
+    return out
+
+
+def new_jcache(shape: Shape, R: int, cap: Optional[int] = None, device="cuda") -> JCache:
+    cap = shape.w if cap is None else cap
+    b = jcache_bytes(shape, R, cap)
+    dt = shape.torch_dtype
+    return JCache(coef=torch.zeros(b.coef_stride, dtype=dt, device=device),
+                  rank=torch.zeros(b.rank // 2, dtype=torch.int16, device=device)[: b.N],
+                  offset=torch.zeros(b.N + 1, dtype=torch.int32, device=device),
+                  chunk_off=torch.zeros(b.n_chunks + 1, dtype=torch.int32, device=device),
+                  k_exact=torch.zeros((shape.G, cap, HEAD_DIM), dtype=dt, device=device),
+                  v_exact=torch.zeros((shape.G, cap, HEAD_DIM), dtype=dt, device=device),
+                  coef_stride=int(b.coef_stride), cap=cap, R=R, N=int(b.N), B=int(b.B))
+
+
+def joint_compress(shape: Shape, K, V, Qw, W, R: Optional[int] = None, cache: Optional[JCache] = None,
+                   cap: Optional[int] = None, sbar_out: Optional[torch.Tensor] = None,
+                   workspace: Optional[torch.Tensor] = None) -> JCache:
+    """Algorithm 1 with the shared basis W [R][2 G d] (fp32)."""
+    R = int(W.shape[0]) if R is None else R
+    if cache is None:
+        cache = new_jcache(shape, R, cap, K.device)
+    need = int(library().varrate_joint_compress_workspace_bytes(ctypes.byref(shape.c()), R))
+    if need == 0:
+        _check(library().varrate_jcache_bytes(ctypes.byref(shape.c()), R, cache.cap, None))
+    ws = workspace if workspace is not None else _WS.get("jcompress", need, K.device)
+    cc = cache.c()
+    _check(library().varrate_joint_compress(ctypes.byref(shape.c()), _dev_ptr(K, shape.torch_dtype, "K"),
+                                            _dev_ptr(V, shape.torch_dtype, "V"), _dev_ptr(Qw, shape.torch_dtype, "Qw"),
+                                            _dev_ptr(W, torch.float32, "W"), ctypes.byref(cc),
+                                            _dev_ptr(sbar_out, torch.float32, "sbar_out"), ws.data_ptr(), ws.numel(),
+                                            _stream()))
+    cache._update(cc)
+    return cache
+
+
+def joint_decode_workspace(shape: Shape, R: int, S: int, Q: int, device="cuda") -> torch.Tensor:
+    need = int(library().varrate_joint_decode_workspace_bytes(ctypes.byref(shape.c()), R, S, Q))
+    return _WS.get("jdecode", need, device)
+
+
+def joint_decode(shape: Shape, caches: Sequence[JCache], q: torch.Tensor, W, out: Optional[torch.Tensor] = None,
+                 workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Decode attention over shared-basis caches.  q: [S][Q][H][d] (or [Q][H][d] for one cache)."""
+    single = q.dim() == 3
+    if single:
+        q = q.unsqueeze(0)
+    S, Q = int(q.shape[0]), int(q.shape[1])
+    if len(caches) != S:
+        raise VarRateError(_lib.VARRATE_EINVAL, f"{len(caches)} caches for {S} query sets")
+    if out is None:
+        out = torch.empty_like(q)
+    arr = (_lib.JCacheC * S)(*[c.c() for c in caches])
+    ws = workspace if workspace is not None else joint_decode_workspace(shape, caches[0].R, S, Q, q.device)
+    _check(library().varrate_joint_decode_attn(ctypes.byref(shape.c()), arr, S, _dev_ptr(q, shape.torch_dtype, "q"),
+                                               Q, _dev_ptr(W, torch.float32, "W"),
+                                               _dev_ptr(out, shape.torch_dtype, "out"), ws.data_ptr(), ws.numel(),
+                                               _stream()))
+    return out[0] if single else out
+
+
+def joint_append_exact(shape: Shape, cache: JCache, k_new: torch.Tensor, v_new: torch.Tensor) -> JCache:
+    cc = cache.c()
+    _check(library().varrate_joint_append_exact(ctypes.byref(shape.c()), ctypes.byref(cc),
+                                                _dev_ptr(k_new, shape.torch_dtype, "k_new"),
+                                                _dev_ptr(v_new, shape.torch_dtype, "v_new"), _stream()))
+    cache._update(cc)
+    return cache

@@ -23,6 +23,8 @@ EXPORTS = (
     "varrate_append_exact", "varrate_decode_attn", "varrate_decode_scratch_need",
     "varrate_decode_attn_noalloc", "varrate_qcache_bytes", "varrate_quantize", "varrate_decode_attn_q",
     "varrate_anchor_search", "varrate_anchor_encode",
+    "varrate_jcache_bytes", "varrate_joint_compress_workspace_bytes", "varrate_joint_decode_workspace_bytes",
+    "varrate_joint_compress", "varrate_joint_decode_attn", "varrate_joint_append_exact",
 )
 DECODE_SCRATCH_BYTES = 8 << 20
 
@@ -60,6 +62,19 @@ class CacheBytes(ctypes.Structure):
                                                "piece_anchor")]
 
 
+class JCacheC(ctypes.Structure):
+    _fields_ = [("coef", ctypes.c_void_p), ("rank", ctypes.c_void_p), ("offset", ctypes.c_void_p),
+                ("chunk_off", ctypes.c_void_p), ("k_exact", ctypes.c_void_p), ("v_exact", ctypes.c_void_p),
+                ("coef_stride", ctypes.c_int64), ("cap", ctypes.c_int64), ("n_exact", ctypes.c_int64),
+                ("N", ctypes.c_int64), ("B", ctypes.c_int64), ("R", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class JCacheBytes(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("B", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
+                ("coef_stride", ctypes.c_int64)] + \
+               [(k, ctypes.c_size_t) for k in ("coef", "rank", "offset", "chunk_off", "k_exact", "v_exact")]
+
+
 _lib = None
 
 
@@ -95,6 +110,12 @@ def load() -> ctypes.CDLL:
         "varrate_quantize": (ctypes.c_int, [P(Shape), P(CacheC), P(QCacheC), vp]),
         "varrate_decode_attn_q": (ctypes.c_int, [P(Shape), P(CacheC), P(QCacheC), i32, vp, i32, vp, vp, vp, vp,
                                                  sz, vp]),
+        "varrate_jcache_bytes": (ctypes.c_int, [P(Shape), i32, i64, P(JCacheBytes)]),
+        "varrate_joint_compress_workspace_bytes": (sz, [P(Shape), i32]),
+        "varrate_joint_decode_workspace_bytes": (sz, [P(Shape), i32, i32, i32]),
+        "varrate_joint_compress": (ctypes.c_int, [P(Shape), vp, vp, vp, vp, P(JCacheC), vp, vp, sz, vp]),
+        "varrate_joint_decode_attn": (ctypes.c_int, [P(Shape), P(JCacheC), i32, vp, i32, vp, vp, vp, sz, vp]),
+        "varrate_joint_append_exact": (ctypes.c_int, [P(Shape), P(JCacheC), vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)

@@ -399,10 +399,12 @@ __global__ __launch_bounds__(AK_T) void al_fine(int64_t N, int64_t B, int r_min,
 }
 
 // ---- 4. fine level; floors, keys and the first selection digit --------------------------------
+// RT: the rank type, uint8_t (per-head codec, R = 128) or uint16_t (shared basis, R <= 1024)
+template <typename RT>
 __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_min, int R,
                                                   const uint32_t* __restrict__ u_ws,
                                                   const uint32_t* __restrict__ f_cnt,
-                                                  uint8_t* __restrict__ rank, uint64_t* __restrict__ phi_ws,
+                                                  RT* __restrict__ rank, uint64_t* __restrict__ phi_ws,
                                                   uint32_t* __restrict__ d_cnt, AlCtl* __restrict__ ctl) {
     __shared__ uint32_t cnt[NDB];
     __shared__ uint32_t wt32[AK_T / 64];
@@ -509,7 +511,7 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
             base = (uint32_t)(r_min + f);
             atomicAdd(&cnt[(phi >> sh0) & (NDB - 1)], 1u);
         }
-        rank[t] = (uint8_t)base;
+        rank[t] = (RT)base;
         phi_ws[t] = phi;
         fsum += base;
     }
@@ -854,6 +856,55 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
     if (lane == 0 && c * CHUNK < N) chunk_off[c] = tile_sum;
 }
 
+// ---- 6'. shared basis: final ranks (16-bit, original order) and each chunk's rank sum ---------
+__global__ __launch_bounds__(AK_T) void al_final_joint(int64_t N, const uint32_t* __restrict__ u_ws,
+                                                       const uint64_t* __restrict__ phi_ws,
+                                                       uint16_t* __restrict__ rank, uint32_t* __restrict__ chunk_off,
+                                                       const AlCtl* __restrict__ ctl) {
+    const uint64_t T_hi = ctl->T_hi, T_lo = ctl->T_lo;
+    const bool any = ctl->any;
+    uint32_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = al_tok(k);
+        if (t >= N) continue;
+        uint32_t r = rank[t];
+        const uint64_t phi = phi_ws[t];
+        if (any && phi != CAPPED && (phi > T_hi || (phi == T_hi && lo_key(u_ws[t], t) >= T_lo))) {
+            r += 1;
+            rank[t] = (uint16_t)r;
+        }
+        sum += r;
+    }
+    sum = wave_sum(sum);
+    const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + (threadIdx.x >> 6);
+    if ((threadIdx.x & 63) == 0 && c * CHUNK < N) chunk_off[c] = sum;
+}
+
+// ---- 8. shared basis: per-token offsets = chunk offset + the chunk's earlier ranks -------------
+__global__ __launch_bounds__(AK_T) void al_offsets(int64_t N, const uint16_t* __restrict__ rank,
+                                                   const uint32_t* __restrict__ chunk_off,
+                                                   uint32_t* __restrict__ offset, int n_chunks) {
+    const int lane = threadIdx.x & 63;
+    const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + (threadIdx.x >> 6);
+    if (c * CHUNK >= N) return;
+    uint32_t pre = chunk_off[c];
+#pragma unroll
+    for (int k = 0; k < AK_PER; ++k) {
+        const int64_t t = c * CHUNK + 64 * k + lane;       // the wave's tokens, in index order
+        const uint32_t r = t < N ? rank[t] : 0u;
+        uint32_t x = r;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        if (t < N) offset[t] = pre + x - r;
+        pre += __shfl(x, 63, 64);
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) offset[N] = chunk_off[n_chunks];
+}
+
 // ---- 7. chunk offsets (in place: chunk sums -> exclusive prefix, total at [n_chunks]) --------
 constexpr int SCAN_T = 1024;
 constexpr int SCAN_PT = MAX_CODED_CHUNKS / SCAN_T;   // chunk sums per thread
@@ -895,11 +946,36 @@ hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_c
         al_minmax<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, w.clear, w.clear_words);
     al_weights<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_low, w.c_cnt, w.ctl);
     al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
-    al_floors<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
+    al_floors<uint8_t><<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
     al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
     al_select<<<1, AS_T, 0, st>>>(N, w.cand, w.ctl);
     al_final<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, c.rank, c.srank, c.sidx, c.chunk_off, w.ctl);
     al_scan<<<1, SCAN_T, 0, st>>>(c.chunk_off, n_chunks);
+    return hipGetLastError();
+}
+
+hipError_t launch_allocate_joint(const varrate_shape& sh, int R, int64_t B, const float* sbar, uint16_t* rank,
+                                 uint32_t* offset, uint32_t* chunk_off, uint8_t* ws, hipStream_t st,
+                                 const float* s_part) {
+    const int64_t N = sh.n - sh.w;
+    const int r_min = sh.r_min;
+    const int nwg = (int)((N + AK_TOK - 1) / AK_TOK);
+    const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
+    if (n_chunks > MAX_CODED_CHUNKS) return hipErrorInvalidValue;
+    const AlWs w = al_ws(ws, N);
+    if (s_part)
+        al_pool_minmax<<<nwg, AK_T, 0, st>>>(s_part, N, sh.G, salience_pool_scale(sh), const_cast<float*>(sbar),
+                                             w.mm, w.clear, w.clear_words);
+    else
+        al_minmax<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, w.clear, w.clear_words);
+    al_weights<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_low, w.c_cnt, w.ctl);
+    al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
+    al_floors<uint16_t><<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, rank, w.phi, w.d_cnt, w.ctl);
+    al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
+    al_select<<<1, AS_T, 0, st>>>(N, w.cand, w.ctl);
+    al_final_joint<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, rank, chunk_off, w.ctl);
+    al_scan<<<1, SCAN_T, 0, st>>>(chunk_off, n_chunks);
+    al_offsets<<<nwg, AK_T, 0, st>>>(N, rank, chunk_off, offset, n_chunks);
     return hipGetLastError();
 }
 

@@ -58,7 +58,7 @@ int hip_status(hipError_t e, const char* what) {
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 
-int check_shape(const varrate_shape* sh) {
+int check_shape_only(const varrate_shape* sh) {
     if (!sh) return fail(VARRATE_EINVAL, "shape is NULL");
     if (sh->d != VARRATE_HEAD_DIM) return fail(VARRATE_EUNSUPPORTED, "head dim %d != 128", sh->d);
     if (sh->G < 1 || sh->H < 1) return fail(VARRATE_EINVAL, "G=%d H=%d must be >= 1", sh->G, sh->H);
@@ -89,11 +89,56 @@ int check_shape(const varrate_shape* sh) {
             if (!(sh->rope_theta[i] >= 0.f) || !std::isfinite(sh->rope_theta[i]))
                 return fail(VARRATE_EINVAL, "rope_theta[%d] is negative or not finite", i);
     }
+    return VARRATE_OK;
+}
+
+int check_shape(const varrate_shape* sh) {
+    int rc = check_shape_only(sh);
+    if (rc) return rc;
     const int64_t B = coded_budget(*sh);
     const int64_t N = coded_count(*sh);
     if (N * sh->r_min > B || B > N * VARRATE_HEAD_DIM)
         return fail(VARRATE_EBUDGET, "budget B=%lld infeasible for N=%lld, r_min=%d, R=128", (long long)B,
                     (long long)N, sh->r_min);
+    return VARRATE_OK;
+}
+
+// shared cross-head basis: R rows, joint budget
+int64_t joint_budget(const varrate_shape& sh) {
+    return varrate_coded_budget(sh.n, 2 * sh.G * VARRATE_HEAD_DIM, sh.w, sh.kappa_pct);
+}
+
+int check_joint(const varrate_shape* sh, int R) {
+    int rc = check_shape_only(sh);
+    if (rc) return rc;
+    if (sh->rope || sh->anchor_stride)
+        return fail(VARRATE_EUNSUPPORTED, "the shared basis takes position-free keys and no anchors");
+    const int Dz = 2 * sh->G * VARRATE_HEAD_DIM;
+    if (R < 256 || R > 1024 || R % 256 != 0 || R > Dz)
+        return fail(VARRATE_EUNSUPPORTED, "R=%d: need a multiple of 256 in [256, min(1024, 2 G d = %d)]", R, Dz);
+    if (sh->r_min > R) return fail(VARRATE_EINVAL, "r_min=%d exceeds R=%d", sh->r_min, R);
+    const int64_t B = joint_budget(*sh);
+    const int64_t N = sh->n - sh->w;
+    if (N * sh->r_min > B || B > N * R)
+        return fail(VARRATE_EBUDGET, "joint budget B=%lld infeasible for N=%lld, r_min=%d, R=%d", (long long)B,
+                    (long long)N, sh->r_min, R);
+    if (B + VARRATE_JOINT_PAD > (int64_t)UINT32_MAX)
+        return fail(VARRATE_EUNSUPPORTED, "joint budget B=%lld exceeds 32-bit offsets", (long long)B);
+    return VARRATE_OK;
+}
+
+int check_jcache(const varrate_shape* sh, const varrate_jcache* c) {
+    if (!c) return fail(VARRATE_EINVAL, "jcache is NULL");
+    int rc = check_joint(sh, c->R);
+    if (rc) return rc;
+    if (!c->coef || !c->rank || !c->offset || !c->chunk_off || !c->k_exact || !c->v_exact)
+        return fail(VARRATE_EINVAL, "jcache has a NULL buffer");
+    if (!aligned16(c->coef) || !aligned16(c->k_exact) || !aligned16(c->v_exact))
+        return fail(VARRATE_EINVAL, "jcache buffers must be 16-byte aligned");
+    if (c->coef_stride < joint_budget(*sh) + VARRATE_JOINT_PAD)
+        return fail(VARRATE_EINVAL, "coef_stride %lld < B + %d", (long long)c->coef_stride, VARRATE_JOINT_PAD);
+    if (c->cap < sh->w || c->cap > 8192) return fail(VARRATE_EINVAL, "exact capacity %lld outside [w, 8192]",
+                                                     (long long)c->cap);
     return VARRATE_OK;
 }
 
@@ -434,6 +479,112 @@ int varrate_decode_attn_q(const varrate_shape* sh, const varrate_cache* caches, 
     return hip_status(launch_decode(*sh, caches, S, q, Q, PK, PV, out, (uint8_t*)ws, (hipStream_t)stream, false,
                                     qcaches),
                       "decode launch");
+}
+
+int varrate_jcache_bytes(const varrate_shape* sh, int32_t R, int64_t cap, varrate_jcache_bytes_t* out) {
+    int rc = check_joint(sh, R);
+    if (rc) return rc;
+    if (!out) return fail(VARRATE_EINVAL, "out is NULL");
+    if (cap < sh->w || cap > 8192) return fail(VARRATE_EINVAL, "exact capacity %lld outside [w, 8192]", (long long)cap);
+    const size_t es = sh->dtype == VARRATE_BF16 ? 2 : 4;
+    out->N = sh->n - sh->w;
+    out->B = joint_budget(*sh);
+    out->n_chunks = (out->N + VARRATE_CHUNK - 1) / VARRATE_CHUNK;
+    out->coef_stride = ((out->B + VARRATE_JOINT_PAD + 63) / 64) * 64;
+    out->coef = (size_t)out->coef_stride * es;
+    out->rank = (size_t)((out->N + 31) / 32) * 64;
+    out->offset = (size_t)(out->N + 1) * 4;
+    out->chunk_off = (size_t)(out->n_chunks + 1) * 4;
+    out->k_exact = out->v_exact = (size_t)sh->G * cap * VARRATE_HEAD_DIM * es;
+    return VARRATE_OK;
+}
+
+size_t varrate_joint_compress_workspace_bytes(const varrate_shape* sh, int32_t R) {
+    if (check_joint(sh, R)) return 0;
+    return compress_ws_base(*sh);
+}
+
+size_t varrate_joint_decode_workspace_bytes(const varrate_shape* sh, int32_t R, int32_t S, int32_t Q) {
+    if (check_joint(sh, R) || S < 1 || Q < 1 || (int64_t)Q * sh->H > 32) return 0;
+    return joint_decode_ws_bytes(*sh, R, S, Q);
+}
+
+int varrate_joint_compress(const varrate_shape* sh, const void* K, const void* V, const void* Qw, const float* W,
+                           varrate_jcache* c, float* sbar_out, void* ws, size_t ws_bytes, void* stream) {
+    int rc = check_jcache(sh, c);
+    if (rc) return rc;
+    if (!K || !V || !Qw || !W) return fail(VARRATE_EINVAL, "inputs must be non-NULL");
+    if (!aligned16(K) || !aligned16(V) || !aligned16(Qw) || !aligned16(W))
+        return fail(VARRATE_EINVAL, "K, V, Qw, W must be 16-byte aligned");
+    if ((rc = ws_check(ws, ws_bytes, compress_ws_base(*sh)))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    uint8_t* w0 = (uint8_t*)ws;
+    float* sbar = sbar_out ? sbar_out
+                           : (float*)(w0 + align256(salience_ws_bytes(*sh)) + align256(allocate_ws_bytes(*sh)));
+    c->N = sh->n - sh->w;
+    c->B = joint_budget(*sh);
+    if ((rc = hip_status(launch_salience(*sh, K, Qw, sbar, w0, st, false), "salience launch"))) return rc;
+    uint8_t* w8 = w0 + align256(salience_ws_bytes(*sh));
+    if ((rc = hip_status(launch_allocate_joint(*sh, c->R, c->B, sbar, c->rank, c->offset, c->chunk_off, w8, st,
+                                               salience_part(*sh, w0)),
+                         "allocate launch")))
+        return rc;
+    if ((rc = hip_status(launch_joint_project(*sh, c->R, K, V, W, c->rank, c->offset, c->coef, st), "project launch")))
+        return rc;
+    // the window rows stay exact: k_exact[g][e] = K[N + e][g]
+    const size_t es = sh->dtype == VARRATE_BF16 ? 2 : 4;
+    const size_t row = VARRATE_HEAD_DIM * es;
+    for (int kv = 0; kv < 2; ++kv) {
+        const uint8_t* src = (const uint8_t*)(kv ? V : K) + (size_t)c->N * sh->G * row;
+        uint8_t* dst = (uint8_t*)(kv ? c->v_exact : c->k_exact);
+        for (int g = 0; g < sh->G; ++g) {
+            hipError_t e = hipMemcpy2DAsync(dst + (size_t)g * c->cap * row, row, src + (size_t)g * row,
+                                            (size_t)sh->G * row, row, (size_t)sh->w, hipMemcpyDeviceToDevice, st);
+            if ((rc = hip_status(e, "window copy"))) return rc;
+        }
+    }
+    c->n_exact = sh->w;
+    return VARRATE_OK;
+}
+
+int varrate_joint_decode_attn(const varrate_shape* sh, const varrate_jcache* caches, int32_t S, const void* q,
+                              int32_t Q, const float* W, void* out, void* ws, size_t ws_bytes, void* stream) {
+    if (!caches || S < 1 || S > VARRATE_MAX_SEQS) return fail(VARRATE_EINVAL, "S=%d outside [1, %d]", S, VARRATE_MAX_SEQS);
+    int rc;
+    for (int s = 0; s < S; ++s) {
+        if ((rc = check_jcache(sh, &caches[s]))) return rc;
+        if (caches[s].N != sh->n - sh->w || caches[s].R != caches[0].R || caches[s].cap != caches[0].cap)
+            return fail(VARRATE_EINVAL, "jcache %d does not match the shape, R or cap of jcache 0", s);
+        if (caches[s].n_exact < 1 || caches[s].n_exact > caches[s].cap)
+            return fail(VARRATE_EINVAL, "jcache %d has n_exact outside [1, cap]", s);
+    }
+    if (Q < 1 || (int64_t)Q * sh->H > 32) return fail(VARRATE_EUNSUPPORTED, "Q H = %lld query rows exceed 32",
+                                                      (long long)Q * sh->H);
+    if (!q || !out || !W) return fail(VARRATE_EINVAL, "q, out and W must be non-NULL");
+    if (!aligned16(q) || !aligned16(W)) return fail(VARRATE_EINVAL, "q and W must be 16-byte aligned");
+    if ((rc = ws_check(ws, ws_bytes, joint_decode_ws_bytes(*sh, caches[0].R, S, Q)))) return rc;
+    return hip_status(launch_joint_decode(*sh, caches[0].R, caches, S, q, Q, W, out, (uint8_t*)ws,
+                                          (hipStream_t)stream),
+                      "joint decode launch");
+}
+
+int varrate_joint_append_exact(const varrate_shape* sh, varrate_jcache* c, const void* k_new, const void* v_new,
+                               void* stream) {
+    int rc = check_jcache(sh, c);
+    if (rc) return rc;
+    if (!k_new || !v_new) return fail(VARRATE_EINVAL, "k_new and v_new must be non-NULL");
+    if (c->n_exact >= c->cap) return fail(VARRATE_EINVAL, "exact capacity %lld is full", (long long)c->cap);
+    const size_t es = sh->dtype == VARRATE_BF16 ? 2 : 4;
+    const size_t row = VARRATE_HEAD_DIM * es;
+    hipStream_t st = (hipStream_t)stream;
+    for (int kv = 0; kv < 2; ++kv) {
+        uint8_t* dst = (uint8_t*)(kv ? c->v_exact : c->k_exact) + (size_t)c->n_exact * row;
+        const void* src = kv ? v_new : k_new;
+        hipError_t e = hipMemcpy2DAsync(dst, (size_t)c->cap * row, src, row, row, sh->G, hipMemcpyDeviceToDevice, st);
+        if ((rc = hip_status(e, "append copy"))) return rc;
+    }
+    c->n_exact += 1;
+    return VARRATE_OK;
 }
 
 size_t varrate_decode_scratch_need(const varrate_shape* sh, int32_t S, int32_t Q) {

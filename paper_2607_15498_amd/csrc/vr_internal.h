@@ -67,6 +67,16 @@ hipError_t launch_rope_unrotate(const varrate_shape& sh, const void* K, void* Kr
 constexpr size_t ROPE_FRAG_BYTES = (size_t)4 * 8 * 2 * 64 * 16;   // per KV head
 hipError_t launch_rope_prep(const varrate_shape& sh, const float* PK, void* frags, float* freq, hipStream_t st);
 
+// shared cross-head basis
+hipError_t launch_allocate_joint(const varrate_shape& sh, int R, int64_t B, const float* sbar, uint16_t* rank,
+                                 uint32_t* offset, uint32_t* chunk_off, uint8_t* ws, hipStream_t st,
+                                 const float* s_part);
+hipError_t launch_joint_project(const varrate_shape& sh, int R, const void* K, const void* V, const float* W,
+                                const uint16_t* rank, const uint32_t* offset, void* coef, hipStream_t st);
+size_t joint_decode_ws_bytes(const varrate_shape& sh, int R, int S, int Q);
+hipError_t launch_joint_decode(const varrate_shape& sh, int R, const varrate_jcache* caches, int S, const void* q,
+                               int Q, const float* W, void* out, uint8_t* ws, hipStream_t st);
+
 size_t salience_ws_bytes(const varrate_shape& sh);
 size_t allocate_ws_bytes(const varrate_shape& sh);
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q);

@@ -39,12 +39,14 @@ def test_struct_sizes_match_header(tmp_path):
     prog.write_text(
         '#include <stddef.h>\n#include <stdio.h>\n#include "varrate.h"\n'
         'int main(void) { printf("%zu %zu %zu %zu %zu\\n", sizeof(varrate_shape), offsetof(varrate_shape, rope),'
-        ' offsetof(varrate_shape, rope_theta), sizeof(varrate_cache), sizeof(varrate_qcache)); return 0; }\n')
+        ' offsetof(varrate_shape, rope_theta), sizeof(varrate_cache), sizeof(varrate_qcache));'
+        ' printf(" %zu %zu\\n", sizeof(varrate_jcache), sizeof(varrate_jcache_bytes_t)); return 0; }\n')
     exe = tmp_path / "probe"
     subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(prog)], check=True)
     got = [int(x) for x in subprocess.run([str(exe)], stdout=subprocess.PIPE, text=True, check=True).stdout.split()]
     assert got == [ctypes.sizeof(_lib.Shape), _lib.Shape.rope.offset, _lib.Shape.rope_theta.offset,
-                   ctypes.sizeof(_lib.CacheC), ctypes.sizeof(_lib.QCacheC)]
+                   ctypes.sizeof(_lib.CacheC), ctypes.sizeof(_lib.QCacheC), ctypes.sizeof(_lib.JCacheC),
+                   ctypes.sizeof(_lib.JCacheBytes)]
     assert ctypes.sizeof(_lib.CacheC) == 8 * 8 + 5 * 8 + 8 * 8
 
 
@@ -236,3 +238,29 @@ def test_rotary_keys_validation(L):
     cc = _lib.CacheC()
     qc = _lib.QCacheC()
     assert L.varrate_quantize(ctypes.byref(sh), ctypes.byref(cc), ctypes.byref(qc), None) == -3
+
+
+def test_shared_basis_validation(L):
+    """Shared basis: R a multiple of 256 in [256, min(1024, 2 G d)], the joint budget of
+    Eq. (3) (Dz = 2 G d units) feasible for r_min and R, exact capacity <= 8192; sizes follow
+    the joint budget."""
+    from paper_2607_15498_amd import _lib
+    out = _lib.JCacheBytes()
+    sh = _shape()
+    assert L.varrate_jcache_bytes(ctypes.byref(sh), 1024, 64, ctypes.byref(out)) == 0
+    Dz = 2 * 8 * 128
+    assert out.B == (20 * 32768 * Dz) // 100 - 32 * Dz and out.N == 32736
+    assert out.coef_stride >= out.B + 2048 and out.coef == out.coef_stride * 2
+    assert out.offset == (out.N + 1) * 4 and out.rank >= out.N * 2
+    for R in (128, 384, 2048):
+        assert L.varrate_jcache_bytes(ctypes.byref(sh), R, 64, ctypes.byref(out)) == -3
+    # 10% is feasible in joint units with r_min 16 (the per-head units are not)
+    assert L.varrate_jcache_bytes(ctypes.byref(_shape(kappa_pct=10)), 1024, 64, ctypes.byref(out)) == 0
+    assert L.varrate_cache_bytes(ctypes.byref(_shape(kappa_pct=10)), 64, ctypes.byref(_lib.CacheBytes())) == -2
+    # 60% needs more than R = 1024 per token: infeasible
+    assert L.varrate_jcache_bytes(ctypes.byref(_shape(kappa_pct=60)), 1024, 64, ctypes.byref(out)) == -2
+    assert L.varrate_jcache_bytes(ctypes.byref(sh), 1024, 9000, ctypes.byref(out)) == -1
+    th = (ctypes.c_float * 64)(*([1e-3] * 64))
+    assert L.varrate_jcache_bytes(ctypes.byref(_shape(rope=1, rope_theta=th)), 1024, 64, ctypes.byref(out)) == -3
+    assert L.varrate_joint_decode_workspace_bytes(ctypes.byref(sh), 1024, 1, 2) == 0      # 64 query rows
+    assert L.varrate_joint_decode_workspace_bytes(ctypes.byref(sh), 1024, 1, 1) > 0
