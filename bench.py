@@ -401,6 +401,8 @@ def main():
     result["residual_codec"] = bench_anchor(args, shape, Ks, Vs, Qw, q, PK, PV, out, cap_stream)
     # rotary keys: a 32K layer of the same geometry whose cache is post-RoPE
     result["rotary_keys"] = bench_rope(args, cap_stream)
+    # shared cross-head basis: one R = 1024 coefficient row per token for all heads and K, V
+    result["shared_basis"] = bench_joint(args, cap_stream)
     if not args.no_stack:
         # the 128K end of the 32K-128K target range: the 32-layer Llama stack, decode at batch 1
         del graphs, step_graphs, slots, Ks, Vs, sbars
@@ -475,6 +477,69 @@ def bench_rope(args, cap_stream, n_slots=12):
         "frac": round(by / (std["p50"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "decode_bytes": int(by),
         "decode_key_rebuild_GFLOP": round(flops / 1e9, 3),
+    }
+    del gc, gd, slots, Ks, Vs
+    return res
+
+
+def bench_joint(args, cap_stream, n_slots=12):
+    """Shared cross-head basis (Sec. 3.1 Eq. (1) "Joint per-token vector", "Shared basis") on
+    a 32K layer of the Llama geometry with R = 1024 (Dz = 2048): compress (salience, joint
+    water-filling, projection onto W) and decode, each replayed from a graph over `n_slots`
+    caches."""
+    import ctypes
+    import torch
+
+    import paper_2607_15498_amd as vr
+    from workloads import CONFIGS, make_layer
+    cfg = CONFIGS["llama_32k_joint"]
+    li = make_layer(cfg, n_queries=1)
+    R = cfg["joint_R"]
+    sh = vr.Shape(n=cfg["n"], G=cfg["G"], H=cfg["H"], w=cfg["w"], r_min=cfg["r_min"], kappa_pct=cfg["kappa"],
+                  dtype=cfg["dtype"])
+    dev = torch.device("cuda:0")
+    up = lambda a, t=torch.bfloat16: torch.from_numpy(np.ascontiguousarray(a)).to(t).to(dev)
+    Ks = [up(li.K) for _ in range(N_INPUT_COPIES)]
+    Vs = [up(li.V) for _ in range(N_INPUT_COPIES)]
+    Qw, q = up(li.Qw), up(li.q)
+    W = up(li.W, torch.float32)
+    out = torch.empty_like(q)
+    slots = [vr.new_jcache(sh, R, device=dev) for _ in range(n_slots)]
+    wsc = torch.zeros(vr.library().varrate_joint_compress_workspace_bytes(ctypes.byref(sh.c()), R),
+                      dtype=torch.uint8, device=dev)
+    wsd = vr.joint_decode_workspace(sh, R, 1, 1, dev)
+    for i, c in enumerate(slots):
+        vr.joint_compress(sh, Ks[i % len(Ks)], Vs[i % len(Vs)], Qw, W, cache=c, workspace=wsc)
+    torch.cuda.synchronize()
+    gc, gd = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gc, stream=cap_stream):
+        for i, c in enumerate(slots):
+            vr.joint_compress(sh, Ks[i % len(Ks)], Vs[i % len(Vs)], Qw, W, cache=c, workspace=wsc)
+    with torch.cuda.graph(gd, stream=cap_stream):
+        for i in range(n_slots):
+            vr.joint_decode(sh, [slots[(i + n_slots // 2) % n_slots]], q, W, out=out, workspace=wsd)
+    torch.cuda.synchronize()
+    stc = _replay_stats(gc, 3, n_slots)
+    std = _replay_stats(gd, 8, n_slots)
+    c0 = slots[0]
+    rank_sum = int(c0.rank.to(torch.int64).sum())
+    Dz = 2 * sh.G * 128
+    # coefficients, exact rows, ranks and offsets, the basis's key and value columns (fp32),
+    # queries and outputs
+    by = 2 * c0.B + 2 * sh.G * c0.n_exact * 128 * 2 + c0.N * 6 + R * Dz * 4 + 2 * sh.H * 128 * 2
+    proj_flop = 2.0 * rank_sum * Dz
+    res = {
+        "config": f"llama_32k_joint: 1 layer, 8 KV x 32 q heads, n {sh.n}, w {sh.w}, budget {sh.kappa_pct}%, "
+                  f"r_min {sh.r_min}, R {R}, Dz {Dz}, B {c0.B} (mean rank {rank_sum / c0.N:.1f})",
+        "compress_ms_per_32k_tokens": round(stc["p50"] * 32768 / sh.n, 4),
+        "compress_ms_p10_p90": [round(stc["p10"], 4), round(stc["p90"], 4)],
+        "projection_GFLOP_kept_coefficients": round(proj_flop / 1e9, 1),
+        "decode_ms": round(std["p50"], 4), "decode_ms_p10_p90": [round(std["p10"], 4), round(std["p90"], 4)],
+        "decode_GBps": round(by / (std["p50"] * 1e-3) / 1e9, 2),
+        "frac": round(by / (std["p50"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "decode_bytes": int(by),
+        "footprint_pct_of_full_kv": round(100.0 * (2 * c0.B + 2 * sh.G * sh.w * 128 * 2 + c0.N * 2)
+                                          / (2 * sh.n * sh.G * 128 * 2), 2),
     }
     del gc, gd, slots, Ks, Vs
     return res

@@ -531,18 +531,7 @@ int varrate_joint_compress(const varrate_shape* sh, const void* K, const void* V
         return rc;
     if ((rc = hip_status(launch_joint_project(*sh, c->R, K, V, W, c->rank, c->offset, c->coef, st), "project launch")))
         return rc;
-    // the window rows stay exact: k_exact[g][e] = K[N + e][g]
-    const size_t es = sh->dtype == VARRATE_BF16 ? 2 : 4;
-    const size_t row = VARRATE_HEAD_DIM * es;
-    for (int kv = 0; kv < 2; ++kv) {
-        const uint8_t* src = (const uint8_t*)(kv ? V : K) + (size_t)c->N * sh->G * row;
-        uint8_t* dst = (uint8_t*)(kv ? c->v_exact : c->k_exact);
-        for (int g = 0; g < sh->G; ++g) {
-            hipError_t e = hipMemcpy2DAsync(dst + (size_t)g * c->cap * row, row, src + (size_t)g * row,
-                                            (size_t)sh->G * row, row, (size_t)sh->w, hipMemcpyDeviceToDevice, st);
-            if ((rc = hip_status(e, "window copy"))) return rc;
-        }
-    }
+    if ((rc = hip_status(launch_joint_window(*sh, K, V, *c, st), "window copy"))) return rc;
     c->n_exact = sh->w;
     return VARRATE_OK;
 }

@@ -20,8 +20,10 @@
 //               rank-space value sum of its own slice (16x16x16 MFMA, the score fragment as
 //               B operand).  One record (m, l, acc[32][R]) per workgroup;
 //   jx_kernel   the exact rows (window and appended tokens) per query row, original space;
-//   jm1_kernel  log-sum-exp combination of the records per (row, 256 coefficients);
-//   jm2_kernel  rotation back with W_V,g^T, the exact part added, division by the sum.
+//   jm1_kernel  log-sum-exp combination of the records per (row, 64 coefficients);
+//   jm2_kernel_part  rotation back with W_V,g^T for all of head g's rows: a workgroup per
+//               (g, 32 output coordinates, 256 coefficients), 8 partial sums each;
+//   jm2_kernel  the partial sums added in order, the exact part added, division by the sum.
 #include <type_traits>
 
 #include "vr_internal.h"
@@ -504,52 +506,138 @@ __global__ __launch_bounds__(256) void jx_kernel(JDec p) {
     if (tid == 0) { xr[0] = M; xr[1] = red[0]; }
 }
 
-// combined rank-space sums per (sequence, row, 256 coefficients); workgroup 0 of a row also
-// records (M, L)
+// combined rank-space sums per (sequence, row, 64 coefficients): the records' factors
+// exp(m_x - M) once per workgroup, then 4 groups of threads over the records (fixed order
+// within a group, then the 4 groups in order); workgroup 0 of a row records (M, L)
+constexpr int JM_MAXWG = 256;      // records per sequence at most (joint_plan)
 __global__ __launch_bounds__(256) void jm1_kernel(JDec p) {
-    const int kb_n = p.R / 256;
+    __shared__ float fx[JM_MAXWG];
+    __shared__ float red[256];
+    const int kb_n = p.R / 64;
     const int s = blockIdx.x / (p.rows * kb_n), rem = blockIdx.x % (p.rows * kb_n);
     const int row = rem / kb_n, kb = rem % kb_n;
-    const int k = kb * 256 + threadIdx.x;
-    const float* rec = p.rec + (int64_t)s * p.n_wg * (JREC_HEAD + (int64_t)JROWS * p.R);
+    const int tid = threadIdx.x;
     const int64_t rs = JREC_HEAD + (int64_t)JROWS * p.R;
+    const float* rec = p.rec + (int64_t)s * p.n_wg * rs;
     const float* xr = p.xrec + ((int64_t)s * JROWS + row) * (2 + D);
-    float M = xr[0];
-    for (int x = 0; x < p.n_wg; ++x) M = fmaxf(M, rec[x * rs + row]);
-    float a = 0.f, L = xr[1] * fast_exp(xr[0] - M);
-    for (int x = 0; x < p.n_wg; ++x) {
-        const float mx = rec[x * rs + row];
-        const float f = mx == -INFINITY ? 0.f : fast_exp(mx - M);
-        a = fmaf(f, rec[x * rs + JREC_HEAD + (int64_t)row * p.R + k], a);
-        L = fmaf(f, rec[x * rs + JROWS + row], L);
+    const float mx = tid < p.n_wg ? rec[tid * rs + row] : -INFINITY;
+    const float lx = tid < p.n_wg ? rec[tid * rs + JROWS + row] : 0.f;
+    red[tid] = mx;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) red[tid] = fmaxf(red[tid], red[tid + o]);
+        __syncthreads();
     }
-    p.comb[((int64_t)s * JROWS + row) * p.R + k] = a;
-    if (kb == 0 && threadIdx.x == 0) {
+    const float M = fmaxf(red[0], xr[0]);
+    __syncthreads();
+    const float f = mx == -INFINITY ? 0.f : fast_exp(mx - M);
+    if (tid < p.n_wg) fx[tid] = f;
+    red[tid] = f * lx;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if (tid < o) red[tid] += red[tid + o];
+        __syncthreads();
+    }
+    if (kb == 0 && tid == 0) {
         p.ml[((int64_t)s * JROWS + row) * 2] = M;
-        p.ml[((int64_t)s * JROWS + row) * 2 + 1] = L;
+        p.ml[((int64_t)s * JROWS + row) * 2 + 1] = red[0] + xr[1] * fast_exp(xr[0] - M);
+    }
+    __syncthreads();
+    const int kk = tid & 63, xg = tid >> 6;
+    const float* src = rec + JREC_HEAD + (int64_t)row * p.R + kb * 64 + kk;
+    float a = 0.f;
+#pragma unroll 8
+    for (int x = xg; x < p.n_wg; x += 4) a = fmaf(fx[x], src[x * rs], a);
+    red[tid] = a;
+    __syncthreads();
+    if (tid < 64)
+        p.comb[((int64_t)s * JROWS + row) * p.R + kb * 64 + tid] = ((red[tid] + red[tid + 64]) + red[tid + 128]) + red[tid + 192];
+}
+
+// out = (W_V,g^T comb + exp(m_x - M) acc_x) / L for every query row of KV head g: a workgroup
+// per (sequence, g, 32 output coordinates), 8 groups of 32 threads over the coefficients (the
+// basis entry read once for all of g's rows), the 8 partial sums added in order
+constexpr int JM2_ROWS = JROWS;
+constexpr int JM2_KC = 256;        // coefficients per workgroup
+constexpr int JM2_NP = 8;          // partial sums per chunk (thread groups)
+__global__ __launch_bounds__(256) void jm2_kernel_part(JDec p, float* part) {
+    __shared__ float cbs[JM2_ROWS][JM2_KC];
+    __shared__ int rowof[JM2_ROWS];
+    const int nkc = p.R / JM2_KC;
+    const int s = blockIdx.x / (p.G * 4 * nkc);
+    int rem = blockIdx.x % (p.G * 4 * nkc);
+    const int g = rem / (4 * nkc);
+    rem %= 4 * nkc;
+    const int ib = rem / nkc, kc = rem % nkc;
+    const int tid = threadIdx.x, i = ib * 32 + (tid & 31), kg = tid >> 5;
+    const int Dz = 2 * p.G * D;
+    const int k0 = kc * JM2_KC;
+    const int nr = (p.rows / p.H) * p.hpg;      // head g's rows: query * H + g hpg + hh
+    // this thread's basis entries W[k0 + kg + 8 m][(G + g) d + i], all loads in flight
+    const float* w = p.W + (int64_t)(k0 + kg) * Dz + (p.G + g) * D + i;
+    float wv[JM2_KC / JM2_NP];
+#pragma unroll
+    for (int m = 0; m < JM2_KC / JM2_NP; ++m) wv[m] = w[(int64_t)(JM2_NP * m) * Dz];
+    if (tid < JM2_ROWS) rowof[tid] = tid < nr ? (tid / p.hpg) * p.H + g * p.hpg + tid % p.hpg : 0;
+    __syncthreads();
+    const float* comb = p.comb + (int64_t)s * JROWS * p.R + k0;
+    for (int e = tid; e < nr * JM2_KC; e += 256) {
+        const int r = e / JM2_KC, kk = e % JM2_KC;
+        cbs[r][kk] = comb[(int64_t)rowof[r] * p.R + kk];
+    }
+    __syncthreads();
+    float* dst = part + ((((int64_t)s * p.G + g) * (JM2_NP * nkc) + kc * JM2_NP + kg) * JM2_ROWS) * D + i;
+    for (int r = 0; r < nr; ++r) {
+        float a = 0.f;
+#pragma unroll
+        for (int m = 0; m < JM2_KC / JM2_NP; ++m) a = fmaf(wv[m], cbs[r][kg + JM2_NP * m], a);
+        dst[r * D] = a;
     }
 }
 
-// out = (W_V,g^T comb + exp(m_x - M) acc_x) / L per (sequence, row)
 template <bool F32>
-__global__ __launch_bounds__(D) void jm2_kernel(JDec p) {
+__global__ __launch_bounds__(D) void jm2_kernel(JDec p, const float* part) {
     typedef typename std::conditional<F32, float, uint16_t>::type ET;
-    __shared__ float cb[1024];
     const int s = blockIdx.x / p.rows, row = blockIdx.x % p.rows;
     const int h = row % p.H, query = row / p.H, g = h / p.hpg;
-    const float* comb = p.comb + ((int64_t)s * JROWS + row) * p.R;
-    for (int k = threadIdx.x; k < p.R; k += D) cb[k] = comb[k];
-    __syncthreads();
+    const int r = query * p.hpg + h % p.hpg;      // the row's index among head g's rows
     const int i = threadIdx.x;
-    const int Dz = 2 * p.G * D;
-    const float* w = p.W + (p.G + g) * D + i;
+    const int np = JM2_NP * (p.R / JM2_KC);
+    const float* src = part + ((((int64_t)s * p.G + g) * np) * JM2_ROWS + r) * D + i;
     float a = 0.f;
-    for (int k = 0; k < p.R; ++k) a = fmaf(w[(int64_t)k * Dz], cb[k], a);
+#pragma unroll 8
+    for (int x = 0; x < np; ++x) a += src[(int64_t)x * JM2_ROWS * D];
     const float M = p.ml[((int64_t)s * JROWS + row) * 2], L = p.ml[((int64_t)s * JROWS + row) * 2 + 1];
     const float* xr = p.xrec + ((int64_t)s * JROWS + row) * (2 + D);
     a = (a + fast_exp(xr[0] - M) * xr[2 + i]) / L;
     ET* out = reinterpret_cast<ET*>(p.seq[s].out) + ((int64_t)query * p.H + h) * D;
     out[i] = to_elem<ET>(a);
+}
+
+// the window rows stay exact: dst[g][e] = src[N + e][g] for K and V, 16 bytes per thread
+__global__ __launch_bounds__(256) void jwin_kernel(const uint8_t* __restrict__ K, const uint8_t* __restrict__ V,
+                                                   uint8_t* __restrict__ kx, uint8_t* __restrict__ vx, int64_t N,
+                                                   int G, int w, int64_t cap, int row_bytes) {
+    const int upr = row_bytes / 16;
+    const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t total = 2 * (int64_t)w * G * upr;
+    if (gid >= total) return;
+    const int kv = (int)(gid / ((int64_t)w * G * upr));
+    const int64_t r = gid % ((int64_t)w * G * upr);
+    const int e = (int)(r / (G * upr)), g = (int)((r / upr) % G), u = (int)(r % upr);
+    const uint8_t* src = (kv ? V : K) + ((N + e) * G + g) * (int64_t)row_bytes + 16 * u;
+    uint8_t* dst = (kv ? vx : kx) + ((int64_t)g * cap + e) * row_bytes + 16 * u;
+    *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+}
+
+hipError_t launch_joint_window(const varrate_shape& sh, const void* K, const void* V, varrate_jcache& c,
+                               hipStream_t st) {
+    const int row_bytes = D * (sh.dtype == VARRATE_BF16 ? 2 : 4);
+    const int64_t total = 2 * (int64_t)sh.w * sh.G * (row_bytes / 16);
+    jwin_kernel<<<(unsigned)((total + 255) / 256), 256, 0, st>>>((const uint8_t*)K, (const uint8_t*)V,
+                                                                 (uint8_t*)c.k_exact, (uint8_t*)c.v_exact,
+                                                                 sh.n - sh.w, sh.G, sh.w, c.cap, row_bytes);
+    return hipGetLastError();
 }
 
 struct JPlan { int n_wg, tpw, total_tiles; };
@@ -560,7 +648,7 @@ static JPlan joint_plan(const varrate_shape& sh, int S) {
     pl.total_tiles = (int)((N + 15) / 16);
     const int ns = S < JSEQ ? S : JSEQ;
     int want = 256 / ns;                        // about one workgroup per CU per launch
-    want = want < 1 ? 1 : want;
+    want = want < 1 ? 1 : (want > JM_MAXWG ? JM_MAXWG : want);
     pl.tpw = (pl.total_tiles + want - 1) / want;
     pl.n_wg = (pl.total_tiles + pl.tpw - 1) / pl.tpw;
     return pl;
@@ -571,7 +659,8 @@ size_t joint_decode_ws_bytes(const varrate_shape& sh, int R, int S, int Q) {
     const JPlan pl = joint_plan(sh, S);
     const size_t ns = (size_t)S;
     return align256(ns * JROWS * R * 4) + align256(ns * pl.n_wg * (JREC_HEAD + (size_t)JROWS * R) * 4) +
-           align256(ns * JROWS * (2 + D) * 4) + align256(ns * JROWS * R * 4) + align256(ns * JROWS * 2 * 4);
+           align256(ns * JROWS * (2 + D) * 4) + align256(ns * JROWS * R * 4) + align256(ns * JROWS * 2 * 4) +
+           align256(ns * sh.G * (JM2_NP * (size_t)R / JM2_KC) * JM2_ROWS * D * 4);
 }
 
 hipError_t launch_joint_decode(const varrate_shape& sh, int R, const varrate_jcache* caches, int S, const void* q,
@@ -587,7 +676,8 @@ hipError_t launch_joint_decode(const varrate_shape& sh, int R, const varrate_jca
     float* rec = (float*)b;  b += align256(ns_all * pl.n_wg * (JREC_HEAD + (size_t)JROWS * R) * 4);
     float* xrec = (float*)b; b += align256(ns_all * JROWS * (2 + D) * 4);
     float* comb = (float*)b; b += align256(ns_all * JROWS * R * 4);
-    float* ml = (float*)b;
+    float* ml = (float*)b;   b += align256(ns_all * JROWS * 2 * 4);
+    float* part = (float*)b;
     const bool f32 = sh.dtype != VARRATE_BF16;
     for (int s0 = 0; s0 < S; s0 += JSEQ) {
         const int ns = S - s0 < JSEQ ? S - s0 : JSEQ;
@@ -617,21 +707,25 @@ hipError_t launch_joint_decode(const varrate_shape& sh, int R, const varrate_jca
         const unsigned nq = (unsigned)(ns * JROWS * (R / 64));
         const unsigned nd = (unsigned)(ns * pl.n_wg);
         const unsigned nx = (unsigned)(ns * rows);
-        const unsigned n1 = (unsigned)(ns * rows * (R / 256));
+        const unsigned n1 = (unsigned)(ns * rows * (R / 64));
+        const unsigned n2 = (unsigned)(ns * sh.G * 4 * (R / JM2_KC));
+        float* pt = part + (size_t)s0 * sh.G * (JM2_NP * (size_t)R / JM2_KC) * JM2_ROWS * D;
         if (f32) {
             jq_kernel<true><<<nq, 256, 0, st>>>(p);
             if (rows > 16) jd_kernel<true, 2><<<nd, JD_T, 0, st>>>(p);
             else jd_kernel<true, 1><<<nd, JD_T, 0, st>>>(p);
             jx_kernel<true><<<nx, 256, 0, st>>>(p);
             jm1_kernel<<<n1, 256, 0, st>>>(p);
-            jm2_kernel<true><<<nx, D, 0, st>>>(p);
+            jm2_kernel_part<<<n2, 256, 0, st>>>(p, pt);
+            jm2_kernel<true><<<nx, D, 0, st>>>(p, pt);
         } else {
             jq_kernel<false><<<nq, 256, 0, st>>>(p);
             if (rows > 16) jd_kernel<false, 2><<<nd, JD_T, 0, st>>>(p);
             else jd_kernel<false, 1><<<nd, JD_T, 0, st>>>(p);
             jx_kernel<false><<<nx, 256, 0, st>>>(p);
             jm1_kernel<<<n1, 256, 0, st>>>(p);
-            jm2_kernel<false><<<nx, D, 0, st>>>(p);
+            jm2_kernel_part<<<n2, 256, 0, st>>>(p, pt);
+            jm2_kernel<false><<<nx, D, 0, st>>>(p, pt);
         }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;

@@ -74,6 +74,8 @@ hipError_t launch_allocate_joint(const varrate_shape& sh, int R, int64_t B, cons
 hipError_t launch_joint_project(const varrate_shape& sh, int R, const void* K, const void* V, const float* W,
                                 const uint16_t* rank, const uint32_t* offset, void* coef, hipStream_t st);
 size_t joint_decode_ws_bytes(const varrate_shape& sh, int R, int S, int Q);
+hipError_t launch_joint_window(const varrate_shape& sh, const void* K, const void* V, varrate_jcache& c,
+                               hipStream_t st);
 hipError_t launch_joint_decode(const varrate_shape& sh, int R, const varrate_jcache* caches, int S, const void* q,
                                int Q, const float* W, void* out, uint8_t* ws, hipStream_t st);
 
