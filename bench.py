@@ -815,8 +815,17 @@ def bench_agnostic(args):
             vr.decode(shape, [cache], q, PK, PV, out=out, workspace=ws)
         ms = _graph_ms(g_, 20)
         by = decode_bytes(shape, cache, Qn)
+        # the call's binding roof: min over HBM (its bytes at 8 TB/s) and bf16 MFMA (score and
+        # value products of every query row against every kept coefficient, 2.5 PFLOP/s)
+        rsum = int(cache.rank.to(torch.int64).sum())
+        flop = 2.0 * 2 * (Qn * hpg) * G * rsum
+        t_hbm = by / (HBM_PEAK_GBS * 1e9)
+        t_mfma = flop / 2.5e15
         rows.append({"budget_pct": kappa, "r_min": r_min, "decode_ms": round(ms, 4),
                      "decode_GBps": round(by / (ms * 1e-3) / 1e9, 1), "decode_bytes": int(by),
+                     "decode_GFLOP": round(flop / 1e9, 2),
+                     "binding_roof": "hbm" if t_hbm >= t_mfma else "mfma",
+                     "frac_of_binding_roof": round(max(t_hbm, t_mfma) / (ms * 1e-3), 4),
                      "rel_l2_err_varrate": err_v, "rel_l2_err_flat": err_f})
     main_row = next(r for r in rows if r["budget_pct"] == 20)
     result = {
