@@ -18,7 +18,7 @@
 // at [s][position].  Tile bytes: 2 mq b + 32 KS (a multiple of 16).
 //
 // Two launches: one workgroup sums the tile sizes of every chunk and scans them into
-// qchunk_off; then persistent waves write the tiles, one (chunk, head, stream, tile) at a time.
+// qchunk_off; then a workgroup per (chunk, head, stream) writes that chunk's tiles.
 #include "vr_internal.h"
 
 namespace vr {
@@ -75,12 +75,14 @@ struct QzParams {
     int G, bits;
 };
 
-// Persistent waves: wave w of the grid takes the tiles (chunk, head, stream, tile) = w,
-// w + W, ... (W waves in all); one tile at a time, in four steps that only the wave's own
-// lanes share (its own LDS region, wave-scope fences): the bf16 tile rectangle into LDS, the
-// 16 x KS group scales, every code (int8, [position][coordinate] for both streams), the
-// packed dwords (each assembled by one lane from the fields it covers).  Few large
-// workgroups: dispatching one small workgroup per tile is far slower than the work.
+// One workgroup per (chunk, head, stream), its wave w taking tiles w, w + 4, w + 8, w + 12:
+// the chunk's tile sizes are loaded once per wave and each tile runs in four steps that only the wave's own lanes share (its own LDS region,
+// wave-scope fences): the bf16 tile rectangle into LDS, the 16 x KS group scales, every code
+// (int8, [position][coordinate] for both streams), the packed dwords (each assembled by one
+// lane from the fields it covers).  Element indices of a tile of size m are split into
+// (row, column) by a float reciprocal: for f < 2048 and m <= 128, floor(f * (1/m) + 2^-10)
+// is floor(f / m) exactly (the product errs by far less than 2^-10 and the fraction of f / m
+// is at most 127/128 below an integer).
 constexpr int QZ_WAVES = 4;
 constexpr int QZ_VS = D + 1;                      // padded LDS row stride: no bank conflicts
 
@@ -90,41 +92,51 @@ __device__ __forceinline__ void wave_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+__device__ __forceinline__ int qz_div(int f, float inv) { return (int)(fmaf((float)f, inv, 0.0009765625f)); }
+
 template <int QB>
-__global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total, int nwaves) {
+__global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total) {
     constexpr int QMAX = (1 << (QB - 1)) - 1;
     constexpr int VS = QZ_VS;
     __shared__ float val_s[QZ_WAVES][16 * VS];    // tile values, [position][coordinate]
     __shared__ float scl_s[QZ_WAVES][4 * 16];     // [group][position]
     __shared__ uint16_t sclh_s[QZ_WAVES][4 * 16]; // the same as binary16 bits
     __shared__ int8_t cod_s[QZ_WAVES][16 * VS];   // codes, [position][coordinate]
-    __shared__ uint32_t m16_s[QZ_WAVES][16];
     const int wave = threadIdx.x >> 6, tid = threadIdx.x & 63;
     float* val = val_s[wave];
     float* scl = scl_s[wave];
     uint16_t* sclh = sclh_s[wave];
     int8_t* cod = cod_s[wave];
-    uint32_t* m16 = m16_s[wave];
-    for (int item = blockIdx.x * QZ_WAVES + wave; item < total; item += nwaves) {
-        const int h = item & 15;
-        const int kv = (item >> 4) & 1;
-        const int g = (item >> 5) % p.G;
-        const int c = (item >> 5) / p.G;
-        const int64_t t0 = (int64_t)c * CHUNK;
-        const int T = (int)(p.N - t0 < CHUNK ? p.N - t0 : CHUNK);
-        if (16 * h >= T) continue;                // absent tile (wave-uniform)
-        // offsets of tile h in both layouts: the sizes of the chunk's earlier tiles
-        if (tid < 16) m16[tid] = 16 * tid < T ? (uint32_t)p.srank[t0 + 16 * tid] : 0u;
-        wave_sync();
-        uint32_t eo = p.chunk_off[c], bo = p.qchunk_off[c];
-        for (int k = 0; k < h; ++k) {
-            eo += 16u * m16[k];
-            bo += qz_tile_bytes(m16[k], QB);
-        }
-        const int mt = (int)m16[h];
+    const int item = blockIdx.x;                  // (chunk, head, stream); wave w takes tiles w, w + 4, ...
+    if (item >= total) return;
+    const int kv = item & 1;
+    const int g = (item >> 1) % p.G;
+    const int c = (item >> 1) / p.G;
+    const int64_t t0 = (int64_t)c * CHUNK;
+    const int T = (int)(p.N - t0 < CHUNK ? p.N - t0 : CHUNK);
+    const int ntile = (T + 15) >> 4;
+    // the chunk's tile sizes (lane h < 16 holds tile h's) and their prefix offsets
+    const uint32_t mlane = tid < ntile ? (uint32_t)p.srank[t0 + 16 * tid] : 0u;
+    uint32_t eo = p.chunk_off[c], bo = p.qchunk_off[c];
+    const uint16_t* base_src = p.coef[kv] + (int64_t)g * p.coef_stride;
+    uint8_t* base_dst = p.code[kv] + (int64_t)g * p.q_stride;
+    for (int h = 0; h < wave; ++h) {
+        const uint32_t m = (uint32_t)__builtin_amdgcn_readlane((int)mlane, h);
+        eo += 16u * m;
+        bo += qz_tile_bytes(m, QB);
+    }
+    for (int h = wave; h < ntile; h += QZ_WAVES) {
+        const int mt = __builtin_amdgcn_readlane((int)mlane, h);
         const int mq = (mt + 7) & ~7, ks = (mt + 31) / 32;
-        const uint16_t* src = p.coef[kv] + (int64_t)g * p.coef_stride + eo;
-        uint8_t* dst = p.code[kv] + (int64_t)g * p.q_stride + bo;
+        const uint16_t* src = base_src + eo;
+        uint8_t* dst = base_dst + bo;
+        // the offsets of this wave's next tile: past tiles h .. h + 3
+        for (int k = h; k < h + QZ_WAVES && k < ntile; ++k) {
+            const uint32_t m = (uint32_t)__builtin_amdgcn_readlane((int)mlane, k);
+            eo += 16u * m;
+            bo += qz_tile_bytes(m, QB);
+        }
+        const float inv_mt = 1.0f / (float)(mt > 0 ? mt : 1), inv_mq = 1.0f / (float)(mq > 0 ? mq : 1);
         // ---- 1. the tile rectangle (16 mt contiguous bf16: K rows of mt, or V rows of 16),
         //          16-byte loads scattered to [position][coordinate]; zeros up to mq
         for (int e8 = tid; e8 < 2 * mt; e8 += 64) {
@@ -133,7 +145,7 @@ __global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total
             for (int k = 0; k < 8; ++k) {
                 const int f = 8 * e8 + k;
                 int i, j;
-                if (kv == 0) { i = f / mt; j = f - i * mt; }
+                if (kv == 0) { i = qz_div(f, inv_mt); j = f - i * mt; }
                 else { j = f >> 4; i = f & 15; }
                 val[i * VS + j] = (k & 1) ? bf_hi(w[k >> 1]) : bf_lo(w[k >> 1]);
             }
@@ -143,8 +155,6 @@ __global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total
         // ---- 2. group scales: lane -> (group s, position i)
         if (tid < 16 * ks) {
             const int s = tid >> 4, i = tid & 15;
-            // every read issued before the max chain (entries past mq read row i's start: in
-            // bounds, then dropped)
             float a[32];
 #pragma unroll
             for (int u = 0; u < 32; ++u) {
@@ -159,18 +169,16 @@ __global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total
             sclh[tid] = __builtin_bit_cast(uint16_t, hs);
         }
         wave_sync();
-        // ---- 3. codes: lane -> coordinate j (and j + 64), every position
-        for (int j = tid; j < mq; j += 64) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const float sc = scl[16 * (j >> 5) + i];
-                int k = 0;
-                if (sc != 0.f) {
-                    const float r = __builtin_rintf(__fdiv_rn(val[i * VS + j], sc));
-                    k = (int)fminf(fmaxf(r, (float)-QMAX), (float)QMAX);
-                }
-                cod[i * VS + j] = (int8_t)k;
+        // ---- 3. codes: element e -> position e & 15, coordinate e >> 4 (every lane busy)
+        for (int e = tid; e < 16 * mq; e += 64) {
+            const int i = e & 15, j = e >> 4;
+            const float sc = scl[16 * (j >> 5) + i];
+            int k = 0;
+            if (sc != 0.f) {
+                const float r = __builtin_rintf(__fdiv_rn(val[i * VS + j], sc));
+                k = (int)fminf(fmaxf(r, (float)-QMAX), (float)QMAX);
             }
+            cod[i * VS + j] = (int8_t)k;
         }
         wave_sync();
         // ---- 4. packed dwords: K code (i, j) is field i mq + j, V code (j, i) is field
@@ -186,7 +194,7 @@ __global__ __launch_bounds__(64 * QZ_WAVES) void qz_kernel(QzParams p, int total
             for (int u = 0; u < NF; ++u) {
                 const int ee = ebeg + u <= eend ? ebeg + u : ebeg;   // in bounds; dropped below
                 int i, j;
-                if (kv == 0) { i = ee / mq; j = ee - i * mq; }
+                if (kv == 0) { i = qz_div(ee, inv_mq); j = ee - i * mq; }
                 else { j = ee >> 4; i = ee & 15; }
                 cv[u] = cod[i * VS + j];
             }
@@ -234,21 +242,12 @@ hipError_t launch_quantize(const varrate_shape& sh, const varrate_cache& c, varr
     p.q_stride = q.q_stride;
     p.G = sh.G;
     p.bits = q.bits;
-    const int total = n_chunks * sh.G * 2 * 16;                 // (chunk, head, stream, tile)
-    int blocks = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, (const void*)qz_kernel<4>, 64 * QZ_WAVES, 0);
-    if (e != hipSuccess) return e;
-    int dev = 0, cus = 0;
-    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
-    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-    int grid = (blocks > 0 ? blocks : 1) * cus;
-    const int need = (total + QZ_WAVES - 1) / QZ_WAVES;
-    grid = grid < need ? grid : need;
-    const int nwaves = grid * QZ_WAVES;
+    const int total = n_chunks * sh.G * 2;                      // (chunk, head, stream)
+    const int grid = total;
     switch (q.bits) {
-        case 3: qz_kernel<3><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total, nwaves); break;
-        case 4: qz_kernel<4><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total, nwaves); break;
-        case 8: qz_kernel<8><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total, nwaves); break;
+        case 3: qz_kernel<3><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total); break;
+        case 4: qz_kernel<4><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total); break;
+        case 8: qz_kernel<8><<<grid, 64 * QZ_WAVES, 0, st>>>(p, total); break;
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
