@@ -333,10 +333,13 @@ __global__ __launch_bounds__(JD_T, 2) void jd_kernel(JDec p) {
         __syncthreads();
         const int T = (int)min((int64_t)16, p.N - 16 * (int64_t)tau);
         if (tau + 1 < tau1) fetch(tau + 1);
-        int m = 0;
-        for (int i = 0; i < T; ++i) m = max(m, to_s[i + 1] - to_s[i]);
         // ---- partial scores of this wave's slice: A = rows of token col, B = q'
         const int a_col = to_s[col], r_col = col < T ? to_s[col + 1] - to_s[col] : 0;
+        // the tile's largest rank (a max over the 16 lanes of a row, then wave-uniform)
+        int m = r_col;
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) m = max(m, __shfl_xor(m, o, 64));
+        m = __builtin_amdgcn_readfirstlane(m);
         f32x4 sc[RT];
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) sc[rt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -375,6 +378,25 @@ __global__ __launch_bounds__(JD_T, 2) void jd_kernel(JDec p) {
             rr[e] = t < T ? to_s[t + 1] - to_s[t] : 0;
             ao[e] = to_s[t < T ? t : 0];
         }
+        // value operands of the slice (lane -> coordinate slice + 16 b + col, tokens 4 grp ..
+        // 4 grp + 3), built once for every row tile
+        j_u32x2 vop[8], vopl[8];
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            vop[b] = vopl[b] = j_u32x2{0u, 0u};
+            if (b < nvb && slice + 16 * b < m) {
+                const int j = slice + 16 * b + col;
+                float v4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const bool ok = j < rr[e];
+                    const float v = elem_f(stage[ok ? ao[e] + j : 0]);
+                    v4[e] = ok ? v : 0.f;
+                }
+                if constexpr (F32) j_split4(v4, vop[b], vopl[b]);
+                else vop[b] = j_u32x2{cvt_bf16x2(v4[0], v4[1]), cvt_bf16x2(v4[2], v4[3])};
+            }
+        }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
             f32x4 sv = psc[0][rt][lane];
@@ -408,23 +430,10 @@ __global__ __launch_bounds__(JD_T, 2) void jd_kernel(JDec p) {
 #pragma unroll
             for (int b = 0; b < 8; ++b) {
                 if (b < nvb && slice + 16 * b < m) {
-                    const int j = slice + 16 * b + col;
-                    float v4[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const bool ok = j < rr[e];
-                        const float v = elem_f(stage[ok ? ao[e] + j : 0]);
-                        v4[e] = ok ? v : 0.f;
-                    }
+                    acc[rt][b] = jmfma16(vop[b], ph, acc[rt][b]);
                     if constexpr (F32) {
-                        j_u32x2 vh, vl;
-                        j_split4(v4, vh, vl);
-                        acc[rt][b] = jmfma16(vh, ph, acc[rt][b]);
-                        acc[rt][b] = jmfma16(vh, pl, acc[rt][b]);
-                        acc[rt][b] = jmfma16(vl, ph, acc[rt][b]);
-                    } else {
-                        const j_u32x2 vh{cvt_bf16x2(v4[0], v4[1]), cvt_bf16x2(v4[2], v4[3])};
-                        acc[rt][b] = jmfma16(vh, ph, acc[rt][b]);
+                        acc[rt][b] = jmfma16(vop[b], pl, acc[rt][b]);
+                        acc[rt][b] = jmfma16(vopl[b], ph, acc[rt][b]);
                     }
                 }
             }
