@@ -1095,6 +1095,8 @@ struct MergeParams {
     int64_t out_seq_stride; // elements per sequence
     int G, H, hpg, nqt, rows_total, n_wg, rpu;
     int nrec;               // records per unit; those past n_wg + 1 are original-space (anchors)
+    int xcd_m;              // > 0: XCD-aware order, each KV head's workgroups on 8 / G XCDs (G < 8)
+                            // or head g on XCD g mod 8 (G a multiple of 8); 0: plain order
 };
 
 constexpr int MG_THREADS = 256;
@@ -1109,10 +1111,34 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
     __shared__ float red[2][MG_THREADS / 64];
     __shared__ float accR[2][D];
     __shared__ float part8[8][MG_COLS];
-    const int cb = blockIdx.x % MG_CB;
-    const int row = (blockIdx.x / MG_CB) % p.rpu;
-    const int unit = blockIdx.x / (MG_CB * p.rpu);
+    // workgroup -> (unit, row, column block).  Workgroups are dispatched round-robin over the
+    // 8 XCDs (workgroup L on XCD L mod 8), so the XCD-aware order puts every workgroup of KV
+    // head g on the XCDs that ran g's streaming workgroups: the head's basis slabs and records
+    // are then fetched into those XCDs' L2 only.
+    const int P = p.rpu * MG_CB;                  // workgroups per unit
     const int units = p.G * p.nqt;
+    const int nsq = (int)(gridDim.x / (P * units));
+    int unit, wi;
+    if (p.xcd_m > 0) {
+        const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+        const int per_head = nsq * p.nqt * P;    // workgroups of one KV head
+        int gh, idx;
+        if (p.G >= 8) {                           // heads x, x + 8, ...: k-th of them in order
+            gh = x + 8 * (k / per_head);
+            idx = k % per_head;
+        } else {                                  // head x / m over m XCDs, interleaved
+            gh = x / p.xcd_m;
+            idx = k * p.xcd_m + x % p.xcd_m;
+        }
+        const int uh = idx / P;                   // (sequence, row tile) of the head
+        wi = idx % P;
+        unit = ((uh / p.nqt) * p.G + gh) * p.nqt + uh % p.nqt;
+    } else {
+        unit = blockIdx.x / P;
+        wi = blockIdx.x % P;
+    }
+    const int cb = wi % MG_CB;
+    const int row = wi / MG_CB;
     const int sq = unit / units, gq = unit % units;
     const int g = gq / p.nqt, qt = gq % p.nqt;
     const int rows = min(16, p.rows_total - 16 * qt);
@@ -1774,6 +1800,13 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         mp.rpu = rows_total < 16 ? rows_total : 16;
         mp.nrec = pl.nrec;
         const unsigned nmerge = (unsigned)(ns * sh.G * pl.nqt * mp.rpu * MG_CB);
+        {
+            // XCD-aware order when the heads spread evenly over the 8 XCDs
+            const int per_head = ns * pl.nqt * mp.rpu * MG_CB;
+            const int m = sh.G < 8 ? 8 / sh.G : 1;
+            const bool even = (sh.G % 8 == 0) || (8 % sh.G == 0 && per_head % m == 0);
+            mp.xcd_m = even && nmerge % 8 == 0 ? m : 0;
+        }
         if (sh.dtype == VARRATE_BF16) decode_merge_kernel<false><<<nmerge, MG_THREADS, 0, st>>>(mp);
         else decode_merge_kernel<true><<<nmerge, MG_THREADS, 0, st>>>(mp);
         e = hipGetLastError();
