@@ -358,7 +358,7 @@ def main():
         "stage_ms_p10_p90": {k: [round(st["p10"], 4), round(st["p90"], 4)] for k, st in stage_st.items()},
         "timing": "medians over 8 replays of a graph of 24 launches on distinct inputs/caches "
                   "(HIP events on the launching stream); p10/p90 beside them",
-        "roofline": {"kernel": "decode_kernel (rank-space decode attention)", "bound": "hbm",
+        "roofline": {"kernel": "decode_ring_kernel + decode_merge_kernel (rank-space decode attention)", "bound": "hbm",
                      "achieved": round(dbytes / (ms_dec * 1e-3) / 1e9, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(dbytes / (ms_dec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "traffic": decode_traffic(), "bytes_per_launch": int(dbytes)},

@@ -76,6 +76,8 @@ struct DecParams {
     int ns;                  // query rows per unit those arrays hold
     const u32x4* rfrag;      // rotary keys: key-basis fragments [G][4][8][2][64] (bf16 hi, lo)
     const float* rfreq;      // rotary keys: theta / (2 pi) per pair as (hi, lo) [128]
+    int wpu;                 // ring kernel: workgroups per unit
+    int n_xw;                // ring kernel: waves of the unit's last workgroup that take the exact rows
 };
 
 template <bool F32> struct Elem;
@@ -1079,6 +1081,567 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB || ROPE) ? 2 : 4) void decod
 
 
 // ----------------------------------------------------------------------------------------
+// Ring-streaming decode (bf16 coefficients, the plain codec).  One workgroup of 8 waves per
+// CU; the workgroups of a unit (sequence, KV head, row tile) share its stored tiles.  Every
+// wave owns a contiguous run of tiles, i.e. one contiguous byte range of the K stream and the
+// same range of the V stream, and streams it through a private ring in LDS (8 KB per
+// stream): 1 KB direct-to-LDS loads in stream order, as far ahead of the tile being scored as
+// the ring allows.  A wave waits only on its own load counter, so nothing in the tile loop
+// waits for another wave.  A tile that crosses the ring's end is gathered with wrapped
+// addresses.  The last n_xw waves of the unit's last workgroup attend to the exact rows in
+// the original space.  Each workgroup writes its records in the layout the merge launch
+// reads: record 0 the exact rows (last workgroup), record 1 + j the coded tiles of
+// workgroup j.
+constexpr int DR_WAVES = 8;
+constexpr int DR_THREADS = 64 * DR_WAVES;
+constexpr int DR_RING = 8192;                     // bytes per stream and wave
+constexpr int DR_RING_E = DR_RING / 2;            // bf16 elements
+constexpr int DR_UNIT = 1024;                     // one load: 64 lanes x 16 bytes
+constexpr int DR_NU = DR_RING / DR_UNIT;          // ring slots
+constexpr int DR_PAD = 64;                        // zeros after each ring (V reads past a tile's size)
+constexpr int DR_RS = DR_RING + DR_PAD;           // ring stride
+constexpr int DR_META = 4;                        // tile-offset registers per lane, 64 tiles each
+constexpr int DR_MAX_TPW = 64 * DR_META - 15;     // tiles one wave can own (from its first chunk's start)
+constexpr int DR_CUS = 256;                       // workgroups per launch: one per CU of the MI355X
+
+struct RingSmem {
+    uint8_t* ring;    // [wave][K, V][DR_RS]; after the tiles: comb [wave][16][DC_CROW] f32
+    float* comb;
+    u32x4* qf;        // [4 steps][hi, lo][64] rotated query fragments (coded tiles)
+    u32x4* qx;        // [4 steps][hi, lo][64] query fragments (exact rows)
+    u32x4* kmask;     // [9]
+    float* cm;        // [8][16]
+    float* cl;        // [8][16]
+    float* mrow;      // [coded, exact][16]
+    float* lrow;      // [coded, exact][16]
+};
+__device__ __forceinline__ RingSmem ring_carve(uint8_t* smem) {
+    RingSmem s;
+    uint8_t* b = smem;
+    s.ring = b; b += (size_t)DR_WAVES * 2 * DR_RS;
+    s.comb = reinterpret_cast<float*>(s.ring);
+    s.qf = reinterpret_cast<u32x4*>(b); b += 4 * 2 * 64 * 16;
+    s.qx = reinterpret_cast<u32x4*>(b); b += 4 * 2 * 64 * 16;
+    s.kmask = reinterpret_cast<u32x4*>(b); b += 9 * 16;
+    float* f = reinterpret_cast<float*>(b);
+    s.cm = f; f += DR_WAVES * 16;
+    s.cl = f; f += DR_WAVES * 16;
+    s.mrow = f; f += 32;
+    s.lrow = f;
+    return s;
+}
+constexpr size_t DR_SMEM = (size_t)DR_WAVES * 2 * DR_RS + 2 * 4 * 2 * 64 * 16 + 9 * 16 + (2 * DR_WAVES * 16 + 64) * 4;
+static_assert(DR_WAVES * 16 * DC_CROW * 4 <= DR_WAVES * 2 * DR_RS, "combine rows fit in the rings");
+static_assert(DR_SMEM <= 160 * 1024, "one workgroup per CU");
+
+// 8 consecutive bf16 at ring element a (any 2-byte alignment, a may run past the ring's
+// end): the dword indices are taken modulo the ring.
+__device__ __forceinline__ u32x4 lds_row8_wrap(const uint32_t* w, int a) {
+    constexpr int M = DR_RING / 4 - 1;
+    const int w0 = a >> 1;
+    const uint32_t sh = (uint32_t)(a & 1) * 16u;
+    const uint32_t d0 = w[w0 & M], d1 = w[(w0 + 1) & M], d2 = w[(w0 + 2) & M], d3 = w[(w0 + 3) & M],
+                   d4 = w[(w0 + 4) & M];
+    return u32x4{__builtin_amdgcn_alignbit(d1, d0, sh), __builtin_amdgcn_alignbit(d2, d1, sh),
+                 __builtin_amdgcn_alignbit(d3, d2, sh), __builtin_amdgcn_alignbit(d4, d3, sh)};
+}
+
+// s_waitcnt vmcnt(n) for a wave-uniform n (clamped to 0..16; a larger count waits at 16,
+// which only waits longer)
+__device__ __forceinline__ void wait_vm(int n) {
+    switch (n < 0 ? 0 : n) {
+        case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+        case 3: asm volatile("s_waitcnt vmcnt(3)" ::: "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+        case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
+        case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+        case 7: asm volatile("s_waitcnt vmcnt(7)" ::: "memory"); break;
+        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+        case 9: asm volatile("s_waitcnt vmcnt(9)" ::: "memory"); break;
+        case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+        case 11: asm volatile("s_waitcnt vmcnt(11)" ::: "memory"); break;
+        case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+        case 13: asm volatile("s_waitcnt vmcnt(13)" ::: "memory"); break;
+        case 14: asm volatile("s_waitcnt vmcnt(14)" ::: "memory"); break;
+        case 15: asm volatile("s_waitcnt vmcnt(15)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    }
+}
+
+// One tile from a wave's ring (bf16): the arithmetic of tile_step, with the tile at ring
+// element rb, the query fragments in registers and the scores in log2 units (the fragments
+// carry log2(e) / sqrt(d), so a softmax weight is exp2 of a score difference).  Coded tiles:
+// K rows m elements apart, V coordinate-major; WRAP gathers modulo the ring.  Exact tiles:
+// rows of 128 (never wrapped: 4 KB tiles from a 4 KB-aligned start).
+template <bool EXACT, bool WRAP, int KS, int NB>
+__device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool partial, const uint16_t* rK,
+                                          const uint16_t* rV, const u32x4 (&qfr)[4][2], const u32x4* kmask,
+                                          int col, int grp, float& m_run, float& l_part) {
+    u32x2 vh[NB];
+    auto gather_v = [&]() {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const int j = 16 * b + col;
+            if constexpr (EXACT) {
+                // rows past the exact slots in use hold no data: masked
+                us2 h[2];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int a = i0 + 4 * grp + e < T ? rb + (4 * grp + e) * D + j : DR_RING_E;
+                    h[e >> 1][e & 1] = rV[a];
+                }
+                vh[b] = u32x2{__builtin_bit_cast(uint32_t, h[0]), __builtin_bit_cast(uint32_t, h[1])};
+            } else {
+                // four consecutive positions at coordinate j (8-byte aligned, so never split by
+                // the ring's end); past the tile's size: the zeros after the ring
+                int a = rb + 16 * j + 4 * grp;
+                if constexpr (WRAP) a &= DR_RING_E - 1;
+                a = j < m ? a : DR_RING_E;
+                vh[b] = *reinterpret_cast<const u32x2*>(rV + a);
+            }
+        }
+    };
+    if constexpr (KS < 4) gather_v();
+    const uint32_t* rK32 = reinterpret_cast<const uint32_t*>(rK);
+    f32x4 sc = {0, 0, 0, 0};
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        if (KS >= 4 && s == 2) __builtin_amdgcn_sched_barrier(0);
+        const int c0 = 32 * s + 8 * grp;
+        const int mm = EXACT ? D : m;
+        int nv = mm - c0;
+        nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
+        const int a = rb + col * mm + c0;
+        const u32x4 kh = (WRAP ? lds_row8_wrap(rK32, a) : lds_row8_bf16(rK32, a)) & kmask[nv];
+        sc = mfma(kh, qfr[s][0], sc);
+        sc = mfma(kh, qfr[s][1], sc);
+    }
+    if constexpr (KS >= 4) {
+        __builtin_amdgcn_sched_barrier(0);
+        gather_v();
+    }
+    float sv[4] = {sc[0], sc[1], sc[2], sc[3]};
+    if (partial) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sv[v] = i0 + 4 * grp + v < T ? sv[v] : -INFINITY;
+    }
+    float tmax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    tmax = xmax32(xmax16(tmax));
+    // lazy reference, as in tile_step (here every weight stays below 2^8)
+    const bool jump = tmax > m_run + 8.f;
+    if (__builtin_amdgcn_ballot_w64(jump) != 0) {
+        const float m_new = jump ? tmax : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_part *= alpha;
+        acc_scale(alpha);
+        m_run = m_new;
+    }
+    float pv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        pv[v] = __builtin_amdgcn_exp2f(sv[v] - m_run);
+        l_part += pv[v];
+    }
+    const u32x2 ph = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
+    acc_mfma_bf16<NB>(vh, ph);
+}
+
+// Two consecutive small tiles (sizes <= 32, neither wrapped nor ragged) in one step: their
+// gathers and MFMA chains interleave, and they share one max reduction, one rescale test and
+// the loop's bookkeeping.  Same arithmetic as two ring_tile<false, false, 1, 2> calls except
+// that the reference maximum moves at most once for both.
+__device__ __forceinline__ void ring_pair(int rbA, int mA, int rbB, int mB, const uint16_t* rK, const uint16_t* rV,
+                                          const u32x4 (&qfr)[4][2], const u32x4* kmask, int col, int grp,
+                                          float& m_run, float& l_part) {
+    const uint32_t* rK32 = reinterpret_cast<const uint32_t*>(rK);
+    u32x2 va[2], vb[2];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int j = 16 * b + col;
+        const int aa = j < mA ? rbA + 16 * j + 4 * grp : DR_RING_E;
+        const int ab = j < mB ? rbB + 16 * j + 4 * grp : DR_RING_E;
+        va[b] = *reinterpret_cast<const u32x2*>(rV + aa);
+        vb[b] = *reinterpret_cast<const u32x2*>(rV + ab);
+    }
+    int nvA = mA - 8 * grp, nvB = mB - 8 * grp;
+    nvA = nvA < 0 ? 0 : (nvA > 8 ? 8 : nvA);
+    nvB = nvB < 0 ? 0 : (nvB > 8 ? 8 : nvB);
+    const u32x4 kA = lds_row8_bf16(rK32, rbA + (int)__umul24((uint32_t)col, (uint32_t)mA) + 8 * grp) & kmask[nvA];
+    const u32x4 kB = lds_row8_bf16(rK32, rbB + (int)__umul24((uint32_t)col, (uint32_t)mB) + 8 * grp) & kmask[nvB];
+    f32x4 sA = {0, 0, 0, 0}, sB = {0, 0, 0, 0};
+    sA = mfma(kA, qfr[0][0], sA);
+    sB = mfma(kB, qfr[0][0], sB);
+    sA = mfma(kA, qfr[0][1], sA);
+    sB = mfma(kB, qfr[0][1], sB);
+    float tmax = fmaxf(fmaxf(fmaxf(sA[0], sA[1]), fmaxf(sA[2], sA[3])), fmaxf(fmaxf(sB[0], sB[1]), fmaxf(sB[2], sB[3])));
+    tmax = xmax32(xmax16(tmax));
+    const bool jump = tmax > m_run + 8.f;
+    if (__builtin_amdgcn_ballot_w64(jump) != 0) {
+        const float m_new = jump ? tmax : m_run;
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_part *= alpha;
+        acc_scale(alpha);
+        m_run = m_new;
+    }
+    float pa[4], pb[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        pa[v] = __builtin_amdgcn_exp2f(sA[v] - m_run);
+        pb[v] = __builtin_amdgcn_exp2f(sB[v] - m_run);
+    }
+    l_part += ((pa[0] + pa[1]) + (pa[2] + pa[3])) + ((pb[0] + pb[1]) + (pb[2] + pb[3]));
+    const u32x2 pha = {cvt_bf16x2(pa[0], pa[1]), cvt_bf16x2(pa[2], pa[3])};
+    const u32x2 phb = {cvt_bf16x2(pb[0], pb[1]), cvt_bf16x2(pb[2], pb[3])};
+    acc_mfma_bf16<2>(va, pha);
+    acc_mfma_bf16<2>(vb, phb);
+}
+
+__global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    const int U = p.units;
+    const int L = blockIdx.x;
+    const int unit = L % U, j = L / U;          // workgroup j of the unit
+    const int sq = unit / (p.G * p.nqt), gq = unit % (p.G * p.nqt);
+    const int g = gq / p.nqt, qt = gq % p.nqt;
+    const DecSeq& S = p.seq[sq];
+    const int rows = min(16, p.rows_total - 16 * qt);
+    const int nr4 = (rows + 3) & ~3;
+    const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int lane = lane_now(), tid = 64 * wave + lane, grp = lane >> 4, col = lane & 15;
+    RingSmem sm = ring_carve(smem);
+    const float qscale = 0.12751743082459868f;  // log2(e) / sqrt(128)
+    const bool lastwg = j == p.wpu - 1;
+    const int nxw = lastwg ? p.n_xw : 0;          // exact waves of this workgroup (its last ones)
+    const bool xw = wave >= DR_WAVES - nxw;
+    const int ncw = DR_WAVES * p.wpu - p.n_xw;   // coded waves of the unit
+    const int T = p.total_tiles;
+    const int nexact = (int)S.n_exact;
+    int t0, t1;
+    if (!xw) {
+        const int k = DR_WAVES * j + wave;
+        t0 = (int)((int64_t)k * T / ncw);
+        t1 = (int)((int64_t)(k + 1) * T / ncw);
+    } else {
+        const int xi = wave - (DR_WAVES - nxw);
+        const int X = (nexact + 15) >> 4;
+        t0 = xi * X / nxw;
+        t1 = (xi + 1) * X / nxw;
+    }
+    t0 = __builtin_amdgcn_readfirstlane(t0);
+    t1 = __builtin_amdgcn_readfirstlane(t1);
+
+    // ---- 1. loads of the prologue, in this order: the first rank of every tile from the start
+    //         of this wave's first chunk to its last tile and the chunk bases (coded waves; 8
+    //         loads), then the basis rows 16 wave .. 16 wave + 15 and the query rows (12 loads:
+    //         every wave rotates its 16 directions of q' for the whole workgroup).  They are
+    //         issued in asm and waited for by load count: the metadata once the basis is the only
+    //         younger load, the basis once only the ring loads issued after it are younger.
+    //         Every lane loads a valid address; values of lanes outside the range are dropped.
+    const int c0 = t0 >> 4;
+    uint32_t mr[DR_META], cbr[DR_META];
+#pragma unroll
+    for (int b = 0; b < DR_META; ++b) {
+        const int tt = 16 * c0 + 64 * b + lane;
+        const bool in = !xw && tt < t1;
+        const uint8_t* ap = in ? S.srank + (int64_t)tt * 16 : S.srank;
+        const uint32_t* cp = in ? S.chunk_off + c0 + 4 * b + (lane >> 4) : S.chunk_off;
+        asm volatile("global_load_ubyte %0, %1, off" : "=v"(mr[b]) : "v"(ap) : "memory");
+        asm volatile("global_load_dword %0, %1, off" : "=v"(cbr[b]) : "v"(cp) : "memory");
+    }
+    const uint16_t* qsrc = reinterpret_cast<const uint16_t*>(S.q);
+    const float* P = p.PK + (int64_t)g * D * D;
+    const int qrow_l = 16 * qt + col;
+    const bool q_ok = qrow_l < p.rows_total;
+    const int query_l = q_ok ? qrow_l / p.hpg : 0, hh_l = q_ok ? qrow_l % p.hpg : 0;
+    const uint16_t* qv = qsrc + ((int64_t)query_l * p.H + g * p.hpg + hh_l) * D;
+    u32x4 pa[4][2], qr[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const float* src = P + (16 * wave + col) * D + 32 * s + 8 * grp;
+        const uint16_t* qs = qv + 32 * s + 8 * grp;     // 2-byte aligned: gfx950 serves it whole
+        asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(pa[s][0]) : "v"(src) : "memory");
+        asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(pa[s][1]) : "v"(src + 4) : "memory");
+        asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(qr[s]) : "v"(qs) : "memory");
+    }
+    asm volatile("s_waitcnt vmcnt(12)" : "+v"(mr[0]), "+v"(mr[1]), "+v"(mr[2]), "+v"(mr[3]), "+v"(cbr[0]),
+                 "+v"(cbr[1]), "+v"(cbr[2]), "+v"(cbr[3]) :: "memory");
+#pragma unroll
+    for (int b = 0; b < DR_META; ++b) {
+        const int tt = 16 * c0 + 64 * b + lane;
+        const bool in = !xw && tt < t1;
+        mr[b] = in ? mr[b] : 0u;
+        cbr[b] = in ? cbr[b] : 0u;
+    }
+    // lane i of register b: tile 16 c0 + 64 b + i (chunk c0 + 4 b + i / 16, one DPP row per
+    // chunk): element offset in the head stream = chunk base + sizes of the chunk's earlier tiles
+    uint32_t off[DR_META];
+#pragma unroll
+    for (int b = 0; b < DR_META; ++b) {
+        const uint32_t units = 16u * mr[b];
+        off[b] = cbr[b] + row_scan16(units) - units;
+    }
+    auto pick = [&](const uint32_t (&r)[DR_META], int nb) -> uint32_t {
+        return nb == 0 ? r[0] : (nb == 1 ? r[1] : (nb == 2 ? r[2] : r[3]));
+    };
+    // the wave's element range of its stream
+    uint32_t e0, e1;
+    if (xw) {
+        e0 = 16u * D * (uint32_t)t0;
+        e1 = (uint32_t)min(16 * t1, nexact) * D;
+    } else if (t1 > t0) {
+        e0 = (uint32_t)__builtin_amdgcn_readlane((int)off[0], t0 & 15);
+        const int il = t1 - 1 - 16 * c0;
+        const int nb = il >> 6;
+        const uint32_t ol = (uint32_t)__builtin_amdgcn_readlane((int)pick(off, nb), il & 63);
+        const uint32_t ml = (uint32_t)__builtin_amdgcn_readlane((int)pick(mr, nb), il & 63);
+        e1 = ol + 16u * ml;
+    } else {
+        e0 = e1 = 0;
+    }
+    e0 = __builtin_amdgcn_readfirstlane(e0);
+    e1 = __builtin_amdgcn_readfirstlane(e1);
+
+    // ---- 2. ring loads: unit u = bytes [base + 1 KB u, + 1 KB) of the wave's range (lanes past
+    //         its end masked), into ring slot u mod 8 of K and of V; two loads per unit.  The
+    //         first 8 units go out now; a range of fewer units is padded with one-lane loads of
+    //         its first bytes into the slots it leaves unused, so exactly 16 ring loads are
+    //         younger than the basis when it is waited for.
+    uint8_t* rK = sm.ring + (size_t)wave * 2 * DR_RS;
+    uint8_t* rV = rK + DR_RS;
+    const int64_t hoff = xw ? (int64_t)g * p.cap * D : (int64_t)g * p.coef_stride;
+    const uint8_t* kg = reinterpret_cast<const uint8_t*>(xw ? S.k_exact : S.coef_k) + hoff * 2;
+    const uint8_t* vg = reinterpret_cast<const uint8_t*>(xw ? S.v_exact : S.coef_v) + hoff * 2;
+    const uint32_t base = (2u * e0) & ~15u;
+    const uint32_t eb = 2u * e1;
+    const int n_units = e1 > e0 ? (int)((eb - base + DR_UNIT - 1) / DR_UNIT) : 0;
+    const uint32_t ldsK = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_u8*)rK);
+    const uint32_t ldsV = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_u8*)rV);
+    const uint32_t lane16 = 16u * (uint32_t)lane;
+    auto issue = [&](int u) {
+        const uint32_t o = base + (uint32_t)u * DR_UNIT + lane16;
+        const uint32_t sl = (uint32_t)(u & (DR_NU - 1)) * DR_UNIT;
+        if (o < eb) {     // lane 0 always is: unit u < n_units starts before the range's end
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(kg + o), "s"(ldsK + sl) : "memory", "m0");
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(vg + o), "s"(ldsV + sl) : "memory", "m0");
+        }
+    };
+    int u_iss = n_units < DR_NU ? n_units : DR_NU;
+    for (int u = 0; u < DR_NU; ++u) {
+        if (u < u_iss) {
+            issue(u);
+        } else if (lane == 0) {
+            const uint32_t sl = (uint32_t)u * DR_UNIT;
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(kg + base), "s"(ldsK + sl) : "memory", "m0");
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(vg + base), "s"(ldsV + sl) : "memory", "m0");
+        }
+    }
+    asm volatile("s_waitcnt vmcnt(16)" : "+v"(pa[0][0]), "+v"(pa[0][1]), "+v"(pa[1][0]), "+v"(pa[1][1]),
+                 "+v"(pa[2][0]), "+v"(pa[2][1]), "+v"(pa[3][0]), "+v"(pa[3][1]), "+v"(qr[0]), "+v"(qr[1]),
+                 "+v"(qr[2]), "+v"(qr[3]) :: "memory");
+
+    // ---- 3. while the ring fills: q' = P_K q log2(e) / sqrt(d) by MFMA (C lane -> query row
+    //         col, directions 16 wave + 4 grp + v) into the score fragments; the exact rows'
+    //         fragments of q itself; the V rings' zero pads and the K-row masks.  Then every wave
+    //         keeps its fragments in registers.
+    {
+        f32x4 c = {0, 0, 0, 0};
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            float a8[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { a8[e] = __uint_as_float(pa[s][0][e]); a8[4 + e] = __uint_as_float(pa[s][1][e]); }
+            u32x4 ah, al;
+            split8(a8, ah, al);
+            const u32x4 qb = q_ok ? qr[s] : u32x4{0, 0, 0, 0};
+            c = mfma(ah, qb, c);
+            c = mfma(al, qb, c);
+        }
+        uint32_t h[4], l[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) split_bf16(c[v] * qscale, h[v], l[v]);
+        uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf);
+        const int s = wave >> 1, gp = 2 * (wave & 1) + (grp >> 1), dw = 2 * (grp & 1);
+        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 0) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 1) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
+    }
+    if (lastwg && wave == DR_WAVES - 1) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            float v8[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float val = (e & 1) ? bf_hi(qr[s][e >> 1]) : bf_lo(qr[s][e >> 1]);
+                v8[e] = q_ok ? val * qscale : 0.f;
+            }
+            u32x4 hh, ll;
+            split8(v8, hh, ll);
+            sm.qx[(s * 2) * 64 + lane] = hh;
+            sm.qx[(s * 2 + 1) * 64 + lane] = ll;
+        }
+    }
+    if (lane < DR_PAD / 4) reinterpret_cast<uint32_t*>(rV + DR_RING)[lane] = 0u;
+    if (tid >= 64 && tid < 64 + 9) {
+        const int nv = tid - 64;
+        u32x4 mk;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) mk[k] = nv >= 2 * k + 2 ? 0xFFFFFFFFu : (nv == 2 * k + 1 ? 0x0000FFFFu : 0u);
+        sm.kmask[nv] = mk;
+    }
+    __syncthreads();
+    u32x4 qfr[4][2];
+    {
+        const u32x4* src = xw ? sm.qx : sm.qf;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            qfr[s][0] = src[(s * 2) * 64 + lane];
+            qfr[s][1] = src[(s * 2 + 1) * 64 + lane];
+        }
+    }
+    // allow n units (2 n loads) in flight, n rounded down to even: at most one unit more is
+    // waited for than the tile needs (and the padding loads of a short range, which are younger
+    // than all of its units)
+    auto wait_units = [&](int n) {
+        if (n < 4) {
+            if (n < 2) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+        } else {
+            if (n < 6) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+            else asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
+        }
+    };
+    // before a tile: load every unit up to 8 past its first one (their slots hold units no
+    // remaining tile needs), then wait for the units it spans
+    auto land = [&](uint32_t bs, uint32_t tbytes) {
+        const int first_u = (int)(bs >> 10);
+        const int u_lim = n_units < first_u + DR_NU ? n_units : first_u + DR_NU;
+        while (u_iss < u_lim) {
+            issue(u_iss);
+            ++u_iss;
+        }
+        if (tbytes) wait_units(u_iss - (int)((bs + tbytes - 1) >> 10) - 1);
+    };
+
+    // ---- 4. tiles
+    float m_run = -INFINITY, l_part = 0.f;
+    acc_zero();
+    const uint16_t* rK16 = reinterpret_cast<const uint16_t*>(rK);
+    const uint16_t* rV16 = reinterpret_cast<const uint16_t*>(rV);
+    if (xw) {
+        for (int t = t0; t < t1; ++t) {
+            const uint32_t bs = 2u * 16u * D * (uint32_t)t - base;
+            land(bs, 2u * 16u * D);
+            const int rb = (int)((bs & (DR_RING - 1)) >> 1);
+            ring_tile<true, false, 4, 8>(rb, D, 16 * t, nexact, 16 * t + 16 > nexact, rK16, rV16, qfr, sm.kmask,
+                                         col, grp, m_run, l_part);
+        }
+    } else {
+        // the head's last tile is the only one with fewer than 16 positions
+        const int t_part = (p.N & 15) ? T - 1 : -1;
+        for (int b = 0; b < DR_META; ++b) {
+            const int lo = max(t0, 16 * c0 + 64 * b), hi = min(t1, 16 * c0 + 64 * b + 64);
+            if (lo >= hi) break;
+            const uint32_t co = pick(off, b), cmk = pick(mr, b);
+            for (int t = lo; t < hi;) {
+                const int li = (t - 16 * c0) & 63;
+                const uint32_t tb = (uint32_t)__builtin_amdgcn_readlane((int)co, li);
+                const int mi = __builtin_amdgcn_readlane((int)cmk, li);
+                const uint32_t bs = 2u * tb - base;           // byte offset from the ring's origin
+                const int rb = (int)((bs & (DR_RING - 1)) >> 1);
+                const bool wrap = rb + 16 * mi > DR_RING_E;
+                const bool small = mi <= 32 && !wrap && t != t_part;
+                if (small && t + 1 < hi) {
+                    // the next tile follows this one in the stream
+                    const int mj = __builtin_amdgcn_readlane((int)cmk, li + 1);
+                    const int rb2 = (int)(((bs + 32u * (uint32_t)mi) & (DR_RING - 1)) >> 1);
+                    if (mj <= 32 && rb2 + 16 * mj <= DR_RING_E && t + 1 != t_part) {
+                        land(bs, 32u * (uint32_t)(mi + mj));
+                        ring_pair(rb, mi, rb2, mj, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        t += 2;
+                        continue;
+                    }
+                }
+                land(bs, 32u * (uint32_t)mi);
+                if (small) {
+                    ring_tile<false, false, 1, 2>(rb, mi, 0, CHUNK, false, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                } else {
+                    const int i0 = 16 * (t & 15);
+                    const int64_t ct = (int64_t)(t >> 4) * CHUNK;
+                    const int Tc = (int)(p.N - ct < CHUNK ? p.N - ct : CHUNK);
+                    const bool partial = t == t_part;
+                    if (!wrap) {
+                        if (mi <= 32) ring_tile<false, false, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        else if (mi <= 64) ring_tile<false, false, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        else ring_tile<false, false, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                    } else {
+                        if (mi <= 32) ring_tile<false, true, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        else if (mi <= 64) ring_tile<false, true, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        else ring_tile<false, true, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                    }
+                }
+                ++t;
+            }
+        }
+    }
+    f32x4 acc[8];
+    acc_read(acc);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+    // ---- 5. combine: the coded waves into record 1 + j, the exact waves into record 0, each
+    //         in wave order (log2 units here; the records hold the maxima in natural-log units,
+    //         as the merge reads them).  Lane (col, grp) holds query row col.
+    const float lsum = xsum32(xsum16(l_part));
+    if (lane < 16) { sm.cm[wave * 16 + col] = m_run; sm.cl[wave * 16 + col] = lsum; }
+    __syncthreads();   // also: every wave is done with its ring, which comb reuses
+    const int wc = DR_WAVES - nxw;
+    if (tid < 32) {
+        const int r = tid & 15;
+        const int w_lo = tid >= 16 ? wc : 0, w_hi = tid >= 16 ? DR_WAVES : wc;
+        float M = -INFINITY;
+        for (int w = w_lo; w < w_hi; ++w) M = fmaxf(M, sm.cm[w * 16 + r]);
+        float Ls = 0.f;
+        for (int w = w_lo; w < w_hi; ++w) {
+            const float mw = sm.cm[w * 16 + r];
+            Ls += mw == -INFINITY ? 0.f : sm.cl[w * 16 + r] * __builtin_amdgcn_exp2f(mw - M);
+        }
+        sm.mrow[tid] = M;
+        sm.lrow[tid] = Ls;
+    }
+    __syncthreads();
+    {
+        const float mref = sm.mrow[(xw ? 16 : 0) + col];
+        const float fac = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mref);
+        if (col < nr4) {
+#pragma unroll
+            for (int b = 0; b < 8; ++b)
+                *reinterpret_cast<f32x4*>(&sm.comb[(wave * 16 + col) * DC_CROW + 16 * b + 4 * grp]) = acc[b] * fac;
+        }
+    }
+    __syncthreads();
+    float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
+    const int n4 = nr4 * D / 4;
+    for (int part = 0; part < (lastwg ? 2 : 1); ++part) {
+        float* rec = recs + (int64_t)(part ? 0 : 1 + j) * DC_REC;
+        const int w_lo = part ? wc : 0, w_hi = part ? DR_WAVES : wc;
+        for (int idx = tid; idx < n4; idx += DR_THREADS) {
+            const int ci = (idx >> 5) * DC_CROW + 4 * (idx & 31);   // row idx/32, float4 idx%32
+            f32x4 s = {0.f, 0.f, 0.f, 0.f};
+            for (int w = w_lo; w < w_hi; ++w) s += *reinterpret_cast<const f32x4*>(sm.comb + w * 16 * DC_CROW + ci);
+            reinterpret_cast<f32x4*>(rec + 32)[idx] = s;
+        }
+        if (tid < 16) {
+            rec[tid] = sm.mrow[16 * part + tid] * 0.6931471805599453f;   // ln 2: log2 -> natural units
+            rec[16 + tid] = sm.lrow[16 * part + tid];
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------------------
 // Merge of the partial records of one (sequence, KV head, row tile): log-sum-exp over the
 // records (record 0 = exact slots, original space; records 1.. = coded tile ranges, rank
 // space), back-rotation of the rank-space sum with P_V^T, division by the softmax
@@ -1571,9 +2134,12 @@ struct DecPlan {
     int nqt, n_chunks, cpw, n_wg, tpw, total_tiles;
     int nrec, n_ablk, ns;      // records per unit; residual codec: anchor records, score rows
     int64_t na;
+    bool ring;                 // decode_ring_kernel (n_wg = its workgroups per unit)
 };
 
-static DecPlan plan_decode(const varrate_shape& sh, int S, int Q) {
+// allow_ring: bf16 coefficients of the plain codec go to the ring kernel when every wave's
+// tile run fits its offset registers
+static DecPlan plan_decode(const varrate_shape& sh, int S, int Q, bool allow_ring = true) {
     DecPlan pl;
     const int64_t N = coded_count(sh);
     const int rows_total = Q * (sh.H / sh.G);
@@ -1598,6 +2164,16 @@ static DecPlan plan_decode(const varrate_shape& sh, int S, int Q) {
     pl.n_ablk = (int)((pl.na + AV_A - 1) / AV_A);
     pl.nrec = pl.n_wg + 1 + pl.n_ablk;
     pl.ns = rows_total < 16 ? (rows_total + 3) & ~3 : 16;
+    pl.ring = false;
+    if (allow_ring && sh.dtype == VARRATE_BF16 && !sh.rope && pl.na == 0 && units > 0) {
+        const int wpu = DR_CUS / units > 1 ? DR_CUS / units : 1;
+        const int ncw_min = wpu == 1 ? DR_WAVES - 4 : DR_WAVES * wpu - DR_WAVES;   // n_xw at its cap
+        if ((pl.total_tiles + ncw_min - 1) / ncw_min <= DR_MAX_TPW) {
+            pl.ring = true;
+            pl.n_wg = wpu;
+            pl.nrec = wpu + 1;
+        }
+    }
     return pl;
 }
 
@@ -1607,7 +2183,7 @@ size_t decode_units(const varrate_shape& sh, int S, int Q) {
 }
 
 bool decode_supported(const varrate_shape& sh, int S, int Q) {
-    return plan_decode(sh, S, Q).nrec <= DC_MAX_REC;
+    return plan_decode(sh, S, Q, false).nrec <= DC_MAX_REC && plan_decode(sh, S, Q).nrec <= DC_MAX_REC;
 }
 
 // Residual codec buffers after the records: X [units][na][ns], xbar and S [units][16 tiles][ns],
@@ -1621,7 +2197,9 @@ static size_t anc_dec_bytes(const DecPlan& pl, size_t units, int64_t N) {
 }
 
 size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
-    DecPlan pl = plan_decode(sh, S, Q);
+    DecPlan pl = plan_decode(sh, S, Q, false);
+    const DecPlan pr = plan_decode(sh, S, Q);
+    if (pr.nrec > pl.nrec) pl.nrec = pr.nrec;     // room for either kernel's records
     const size_t units = (size_t)S * sh.G * pl.nqt;
     const size_t rope = sh.rope ? align256((size_t)sh.G * ROPE_FRAG_BYTES) + align256(D * sizeof(float)) : 0;
     return align256(units * pl.nrec * DC_REC * sizeof(float)) + anc_dec_bytes(pl, units, coded_count(sh)) + rope;
@@ -1630,8 +2208,8 @@ size_t decode_ws_bytes(const varrate_shape& sh, int S, int Q) {
 hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, int S, const void* q,
                          int Q, const float* PK, const float* PV, void* out, uint8_t* ws,
                          hipStream_t st, bool reuse_group_region, const varrate_qcache* qcaches) {
-    DecPlan pl = plan_decode(sh, S, Q);
     const int qb = qcaches ? qcaches[0].bits : 0;
+    DecPlan pl = plan_decode(sh, S, Q, qb == 0);
     if (qb != 0 && qb != 3 && qb != 4 && qb != 8) return hipErrorInvalidValue;
     if (qb != 0 && sh.dtype != VARRATE_BF16) return hipErrorInvalidValue;
     const bool anc = pl.na > 0;
@@ -1687,7 +2265,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     }
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
-    const size_t lds = decode_smem_bytes(pl.cpw, rope);
+    const size_t lds = pl.ring ? DR_SMEM : decode_smem_bytes(pl.cpw, rope);
+    if (pl.ring) kfn = decode_ring_kernel;
     e = ensure_lds_limit((const void*)kfn, lds);
     if (e != hipSuccess) return e;
     for (int s0 = 0; s0 < S; s0 += DC_SEQ) {
@@ -1775,8 +2354,24 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
             e = hipGetLastError();
             if (e != hipSuccess) return e;
         }
-        const unsigned nblk = (unsigned)(prm.units * (pl.n_wg + 1));
-        kfn<<<nblk, DC_THREADS, lds, st>>>(prm);
+        prm.wpu = pl.n_wg;
+        prm.n_xw = 0;
+        if (pl.ring) {
+            // exact waves in proportion to the exact rows' share of the streamed bytes (the coded
+            // share estimated from the budget and the tiles' measured 6% padding), at least one,
+            // at most one per exact tile and half the unit's waves when it has one workgroup
+            int64_t nx = 0;
+            for (int i = 0; i < ns; ++i) nx = caches[s0 + i].n_exact > nx ? caches[s0 + i].n_exact : nx;
+            const int X = (int)((nx + 15) / 16);
+            const double xb = (double)nx * D, cb = (double)caches[s0].B * 1.06;
+            int nxw = (int)(DR_WAVES * pl.n_wg * xb / (xb + cb) + 0.5);
+            const int cap_x = pl.n_wg == 1 ? DR_WAVES / 2 : DR_WAVES;
+            nxw = nxw > cap_x ? cap_x : nxw;
+            nxw = nxw > X ? X : nxw;
+            prm.n_xw = nxw < 1 ? 1 : nxw;
+        }
+        const unsigned nblk = (unsigned)(prm.units * (pl.ring ? pl.n_wg : pl.n_wg + 1));
+        kfn<<<nblk, pl.ring ? DR_THREADS : DC_THREADS, lds, st>>>(prm);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         if (pl.na) {
@@ -1830,9 +2425,10 @@ static std::mutex scratch_mu;
 static void* scratch_addr[SCRATCH_MAX_DEVICES];
 
 size_t decode_group_bytes(const varrate_shape& sh, int S, int Q) {
-    DecPlan pl = plan_decode(sh, S, Q);
+    const DecPlan pl = plan_decode(sh, S, Q, false), pr = plan_decode(sh, S, Q);
     const int ns = S < DC_SEQ ? S : DC_SEQ;
-    return (size_t)ns * sh.G * pl.nqt * (pl.n_wg + 1) * DC_REC * sizeof(float);
+    const int nrec = pr.n_wg + 1 > pl.n_wg + 1 ? pr.n_wg + 1 : pl.n_wg + 1;
+    return (size_t)ns * sh.G * pl.nqt * nrec * DC_REC * sizeof(float);
 }
 
 hipError_t decode_scratch(uint8_t** out) {
