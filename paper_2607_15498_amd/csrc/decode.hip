@@ -1100,7 +1100,7 @@ constexpr int DR_UNIT = 1024;                     // one load: 64 lanes x 16 byt
 constexpr int DR_NU = DR_RING / DR_UNIT;          // ring slots
 constexpr int DR_PAD = 64;                        // zeros after each ring (V reads past a tile's size)
 constexpr int DR_RS = DR_RING + DR_PAD;           // ring stride
-constexpr int DR_META = 4;                        // tile-offset registers per lane, 64 tiles each
+constexpr int DR_META = 8;                        // tile-offset registers per lane, 64 tiles each
 constexpr int DR_MAX_TPW = 64 * DR_META - 15;     // tiles one wave can own (from its first chunk's start)
 constexpr int DR_CUS = 256;                       // workgroups per launch: one per CU of the MI355X
 
@@ -1144,30 +1144,6 @@ __device__ __forceinline__ u32x4 lds_row8_wrap(const uint32_t* w, int a) {
                    d4 = w[(w0 + 4) & M];
     return u32x4{__builtin_amdgcn_alignbit(d1, d0, sh), __builtin_amdgcn_alignbit(d2, d1, sh),
                  __builtin_amdgcn_alignbit(d3, d2, sh), __builtin_amdgcn_alignbit(d4, d3, sh)};
-}
-
-// s_waitcnt vmcnt(n) for a wave-uniform n (clamped to 0..16; a larger count waits at 16,
-// which only waits longer)
-__device__ __forceinline__ void wait_vm(int n) {
-    switch (n < 0 ? 0 : n) {
-        case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-        case 1: asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); break;
-        case 2: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
-        case 3: asm volatile("s_waitcnt vmcnt(3)" ::: "memory"); break;
-        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
-        case 5: asm volatile("s_waitcnt vmcnt(5)" ::: "memory"); break;
-        case 6: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
-        case 7: asm volatile("s_waitcnt vmcnt(7)" ::: "memory"); break;
-        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-        case 9: asm volatile("s_waitcnt vmcnt(9)" ::: "memory"); break;
-        case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
-        case 11: asm volatile("s_waitcnt vmcnt(11)" ::: "memory"); break;
-        case 12: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
-        case 13: asm volatile("s_waitcnt vmcnt(13)" ::: "memory"); break;
-        case 14: asm volatile("s_waitcnt vmcnt(14)" ::: "memory"); break;
-        case 15: asm volatile("s_waitcnt vmcnt(15)" ::: "memory"); break;
-        default: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
-    }
 }
 
 // One tile from a wave's ring (bf16): the arithmetic of tile_step, with the tile at ring
@@ -1333,7 +1309,7 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
     t1 = __builtin_amdgcn_readfirstlane(t1);
 
     // ---- 1. loads of the prologue, in this order: the first rank of every tile from the start
-    //         of this wave's first chunk to its last tile and the chunk bases (coded waves; 8
+    //         of this wave's first chunk to its last tile and the chunk bases (coded waves; 16
     //         loads), then the basis rows 16 wave .. 16 wave + 15 and the query rows (12 loads:
     //         every wave rotates its 16 directions of q' for the whole workgroup).  They are
     //         issued in asm and waited for by load count: the metadata once the basis is the only
@@ -1365,8 +1341,10 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
         asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(pa[s][1]) : "v"(src + 4) : "memory");
         asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(qr[s]) : "v"(qs) : "memory");
     }
-    asm volatile("s_waitcnt vmcnt(12)" : "+v"(mr[0]), "+v"(mr[1]), "+v"(mr[2]), "+v"(mr[3]), "+v"(cbr[0]),
-                 "+v"(cbr[1]), "+v"(cbr[2]), "+v"(cbr[3]) :: "memory");
+    static_assert(DR_META == 8, "the wait below names every metadata register");
+    asm volatile("s_waitcnt vmcnt(12)" : "+v"(mr[0]), "+v"(mr[1]), "+v"(mr[2]), "+v"(mr[3]), "+v"(mr[4]), "+v"(mr[5]),
+                 "+v"(mr[6]), "+v"(mr[7]), "+v"(cbr[0]), "+v"(cbr[1]), "+v"(cbr[2]), "+v"(cbr[3]), "+v"(cbr[4]),
+                 "+v"(cbr[5]), "+v"(cbr[6]), "+v"(cbr[7]) :: "memory");
 #pragma unroll
     for (int b = 0; b < DR_META; ++b) {
         const int tt = 16 * c0 + 64 * b + lane;
@@ -1382,9 +1360,6 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
         const uint32_t units = 16u * mr[b];
         off[b] = cbr[b] + row_scan16(units) - units;
     }
-    auto pick = [&](const uint32_t (&r)[DR_META], int nb) -> uint32_t {
-        return nb == 0 ? r[0] : (nb == 1 ? r[1] : (nb == 2 ? r[2] : r[3]));
-    };
     // the wave's element range of its stream
     uint32_t e0, e1;
     if (xw) {
@@ -1392,10 +1367,18 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
         e1 = (uint32_t)min(16 * t1, nexact) * D;
     } else if (t1 > t0) {
         e0 = (uint32_t)__builtin_amdgcn_readlane((int)off[0], t0 & 15);
+        // the last tile's offset and size: read from every block, kept from block il / 64 (no
+        // register is picked by a run-time index, which would go through scratch memory)
         const int il = t1 - 1 - 16 * c0;
         const int nb = il >> 6;
-        const uint32_t ol = (uint32_t)__builtin_amdgcn_readlane((int)pick(off, nb), il & 63);
-        const uint32_t ml = (uint32_t)__builtin_amdgcn_readlane((int)pick(mr, nb), il & 63);
+        uint32_t ol = 0u, ml = 0u;
+#pragma unroll
+        for (int b = 0; b < DR_META; ++b) {
+            const uint32_t ob = (uint32_t)__builtin_amdgcn_readlane((int)off[b], il & 63);
+            const uint32_t mb = (uint32_t)__builtin_amdgcn_readlane((int)mr[b], il & 63);
+            ol = nb == b ? ob : ol;
+            ml = nb == b ? mb : ml;
+        }
         e1 = ol + 16u * ml;
     } else {
         e0 = e1 = 0;
@@ -1543,10 +1526,17 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
     } else {
         // the head's last tile is the only one with fewer than 16 positions
         const int t_part = (p.N & 15) ? T - 1 : -1;
+        // block b's offsets and sizes are always read from off[0] / mr[0]: the blocks shift
+        // down by one after each
         for (int b = 0; b < DR_META; ++b) {
             const int lo = max(t0, 16 * c0 + 64 * b), hi = min(t1, 16 * c0 + 64 * b + 64);
             if (lo >= hi) break;
-            const uint32_t co = pick(off, b), cmk = pick(mr, b);
+            const uint32_t co = off[0], cmk = mr[0];
+#pragma unroll
+            for (int k = 0; k + 1 < DR_META; ++k) {
+                off[k] = off[k + 1];
+                mr[k] = mr[k + 1];
+            }
             for (int t = lo; t < hi;) {
                 const int li = (t - 16 * c0) & 63;
                 const uint32_t tb = (uint32_t)__builtin_amdgcn_readlane((int)co, li);
@@ -1807,6 +1797,88 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
         else out[oi] = (uint16_t)f32_to_bf16(val);
     }
 }
+// The same merge for units with many query rows: one workgroup per (unit, block of 32 output
+// columns) takes every row of the unit, so the basis slab is read once per unit and column
+// block (into LDS) instead of once per row, and each record row is read by one thread.
+// Fixed-order sums throughout.
+template <bool F32>
+__global__ __launch_bounds__(MG_THREADS) void decode_merge_rows_kernel(MergeParams p) {
+    typedef typename Elem<F32>::T ET;
+    __shared__ float wgt[16][DC_MAX_REC];          // record weights exp(m_r - M) per row
+    __shared__ float Lr[16];
+    __shared__ float accR[16][D + 1];
+    __shared__ float slab[D][MG_COLS + 1];
+    const int units = p.G * p.nqt;
+    const int nsq = (int)(gridDim.x / (MG_CB * units));
+    int unit, cb;
+    if (p.xcd_m > 0) {
+        const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+        const int per_head = nsq * p.nqt * MG_CB;
+        int gh, idx;
+        if (p.G >= 8) {
+            gh = x + 8 * (k / per_head);
+            idx = k % per_head;
+        } else {
+            gh = x / p.xcd_m;
+            idx = k * p.xcd_m + x % p.xcd_m;
+        }
+        const int uh = idx / MG_CB;
+        cb = idx % MG_CB;
+        unit = ((uh / p.nqt) * p.G + gh) * p.nqt + uh % p.nqt;
+    } else {
+        unit = blockIdx.x / MG_CB;
+        cb = blockIdx.x % MG_CB;
+    }
+    const int sq = unit / units, gq = unit % units;
+    const int g = gq / p.nqt, qt = gq % p.nqt;
+    const int rows = min(16, p.rows_total - 16 * qt);
+    const int tid = threadIdx.x;
+    const int nrec = p.nrec;
+    const int nrc = p.n_wg + 1;                   // records 1 .. nrc - 1 are rank-space
+    const float* recs = p.part + (int64_t)unit * nrec * DC_REC;
+    // 1. the basis slab rows j, columns 32 cb .. 32 cb + 31
+    const float* PV = p.PV + (int64_t)g * D * D + MG_COLS * cb;
+    for (int i = tid; i < D * MG_COLS; i += MG_THREADS) slab[i / MG_COLS][i % MG_COLS] = PV[(int64_t)(i / MG_COLS) * D + i % MG_COLS];
+    // 2. per row: maximum over the records, weights, softmax denominator (thread r)
+    if (tid < rows) {
+        float M = -INFINITY;
+        for (int r = 0; r < nrec; ++r) M = fmaxf(M, recs[(int64_t)r * DC_REC + tid]);
+        float L = 0.f;
+        for (int r = 0; r < nrec; ++r) {
+            const float m = recs[(int64_t)r * DC_REC + tid];
+            const float w = m == -INFINITY ? 0.f : fast_exp(m - M);
+            wgt[tid][r] = w;
+            L += w * recs[(int64_t)r * DC_REC + 16 + tid];
+        }
+        Lr[tid] = L;
+    }
+    __syncthreads();
+    // 3. rank-space sum of every row over the coded records, in record order
+    for (int i = tid; i < rows * D; i += MG_THREADS) {
+        const int row = i / D, j = i % D;
+        float a = 0.f;
+        for (int r = 1; r < nrc; ++r) a += wgt[row][r] * recs[(int64_t)r * DC_REC + 32 + row * D + j];
+        accR[row][j] = a;
+    }
+    __syncthreads();
+    // 4. back-rotation by the slab, the original-space records, division by the denominator
+    for (int i = tid; i < rows * MG_COLS; i += MG_THREADS) {
+        const int row = i / MG_COLS, c = i % MG_COLS;
+        float o = 0.f;
+#pragma unroll 8
+        for (int j = 0; j < D; ++j) o += accR[row][j] * slab[j][c];
+        float e = wgt[row][0] * recs[32 + row * D + MG_COLS * cb + c];
+        for (int r = nrc; r < nrec; ++r) e += wgt[row][r] * recs[(int64_t)r * DC_REC + 32 + row * D + MG_COLS * cb + c];
+        const float val = (o + e) / Lr[row];
+        const int qrow = 16 * qt + row;
+        const int query = qrow / p.hpg, hh = qrow % p.hpg;
+        ET* out = reinterpret_cast<ET*>(p.out) + (int64_t)sq * p.out_seq_stride;
+        const int64_t oi = ((int64_t)query * p.H + g * p.hpg + hh) * D + MG_COLS * cb + c;
+        if constexpr (F32) out[oi] = val;
+        else out[oi] = (uint16_t)f32_to_bf16(val);
+    }
+}
+
 // ----------------------------------------------------------------------------------------
 // Residual codec (Sec. 3.1 Eq. (2)): a coded token's key is its anchors' mean plus the
 // truncated projection, so its score is the mean of its 4 anchors' scores plus the rank-space
@@ -2394,16 +2466,24 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         mp.n_wg = pl.n_wg;
         mp.rpu = rows_total < 16 ? rows_total : 16;
         mp.nrec = pl.nrec;
-        const unsigned nmerge = (unsigned)(ns * sh.G * pl.nqt * mp.rpu * MG_CB);
+        // units of more than 4 query rows: one workgroup per (unit, column block) for all rows
+        const bool by_rows = mp.rpu > 4;
+        const unsigned nmerge = (unsigned)(ns * sh.G * pl.nqt * (by_rows ? 1 : mp.rpu) * MG_CB);
         {
             // XCD-aware order when the heads spread evenly over the 8 XCDs
-            const int per_head = ns * pl.nqt * mp.rpu * MG_CB;
+            const int per_head = ns * pl.nqt * (by_rows ? 1 : mp.rpu) * MG_CB;
             const int m = sh.G < 8 ? 8 / sh.G : 1;
             const bool even = (sh.G % 8 == 0) || (8 % sh.G == 0 && per_head % m == 0);
             mp.xcd_m = even && nmerge % 8 == 0 ? m : 0;
         }
-        if (sh.dtype == VARRATE_BF16) decode_merge_kernel<false><<<nmerge, MG_THREADS, 0, st>>>(mp);
-        else decode_merge_kernel<true><<<nmerge, MG_THREADS, 0, st>>>(mp);
+        if (by_rows) {
+            if (sh.dtype == VARRATE_BF16) decode_merge_rows_kernel<false><<<nmerge, MG_THREADS, 0, st>>>(mp);
+            else decode_merge_rows_kernel<true><<<nmerge, MG_THREADS, 0, st>>>(mp);
+        } else if (sh.dtype == VARRATE_BF16) {
+            decode_merge_kernel<false><<<nmerge, MG_THREADS, 0, st>>>(mp);
+        } else {
+            decode_merge_kernel<true><<<nmerge, MG_THREADS, 0, st>>>(mp);
+        }
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
