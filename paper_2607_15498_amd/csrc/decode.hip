@@ -1146,15 +1146,42 @@ __device__ __forceinline__ u32x4 lds_row8_wrap(const uint32_t* w, int a) {
                  __builtin_amdgcn_alignbit(d3, d2, sh), __builtin_amdgcn_alignbit(d4, d3, sh)};
 }
 
+// Online softmax of the ring kernel, in log2 units (the query fragments carry log2(e) /
+// sqrt(d)).  Each lane's reference m_run (its query row's) starts every score MFMA as the
+// accumulator's initial value, so the MFMA returns score - reference directly.  The reference
+// moves lazily: only when some score exceeds it by more than 8 (every weight then stays below
+// 2^8), found from the lane's own scores; the cross-lane maximum of the row is taken only
+// then, and on the wave's first tile (first: the sums and accumulators are still zero, so
+// nothing is rescaled).  Returns through sv the scores relative to the (possibly moved)
+// reference.
+template <int NV>
+__device__ __forceinline__ void ring_softmax_ref(float (&sv)[NV], bool& first, float& m_run, float& l_part) {
+    float lmax = sv[0];
+#pragma unroll
+    for (int v = 1; v < NV; ++v) lmax = fmaxf(lmax, sv[v]);
+    if (first || __builtin_amdgcn_ballot_w64(lmax > 8.f) != 0) {
+        const float t = xmax32(xmax16(lmax));        // the row's maximum, relative
+        const float shift = first ? t : (t > 8.f ? t : 0.f);
+        if (!first) {
+            const float alpha = __builtin_amdgcn_exp2f(-shift);
+            l_part *= alpha;
+            acc_scale(alpha);
+        }
+        m_run += shift;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) sv[v] -= shift;
+        first = false;
+    }
+}
+
 // One tile from a wave's ring (bf16): the arithmetic of tile_step, with the tile at ring
-// element rb, the query fragments in registers and the scores in log2 units (the fragments
-// carry log2(e) / sqrt(d), so a softmax weight is exp2 of a score difference).  Coded tiles:
-// K rows m elements apart, V coordinate-major; WRAP gathers modulo the ring.  Exact tiles:
-// rows of 128 (never wrapped: 4 KB tiles from a 4 KB-aligned start).
+// element rb and the query fragments in registers.  Coded tiles: K rows m elements apart, V
+// coordinate-major; WRAP gathers modulo the ring.  Exact tiles: rows of 128 (never wrapped:
+// 4 KB tiles from a 4 KB-aligned start).
 template <bool EXACT, bool WRAP, int KS, int NB>
 __device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool partial, const uint16_t* rK,
                                           const uint16_t* rV, const u32x4 (&qfr)[4][2], const u32x4* kmask,
-                                          int col, int grp, float& m_run, float& l_part) {
+                                          int col, int grp, bool& first, float& m_run, float& l_part) {
     u32x2 vh[NB];
     auto gather_v = [&]() {
 #pragma unroll
@@ -1181,7 +1208,7 @@ __device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool par
     };
     if constexpr (KS < 4) gather_v();
     const uint32_t* rK32 = reinterpret_cast<const uint32_t*>(rK);
-    f32x4 sc = {0, 0, 0, 0};
+    f32x4 sc = {-m_run, -m_run, -m_run, -m_run};
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
         if (KS >= 4 && s == 2) __builtin_amdgcn_sched_barrier(0);
@@ -1189,7 +1216,7 @@ __device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool par
         const int mm = EXACT ? D : m;
         int nv = mm - c0;
         nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
-        const int a = rb + col * mm + c0;
+        const int a = rb + (int)__umul24((uint32_t)col, (uint32_t)mm) + c0;
         const u32x4 kh = (WRAP ? lds_row8_wrap(rK32, a) : lds_row8_bf16(rK32, a)) & kmask[nv];
         sc = mfma(kh, qfr[s][0], sc);
         sc = mfma(kh, qfr[s][1], sc);
@@ -1203,34 +1230,21 @@ __device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool par
 #pragma unroll
         for (int v = 0; v < 4; ++v) sv[v] = i0 + 4 * grp + v < T ? sv[v] : -INFINITY;
     }
-    float tmax = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
-    tmax = xmax32(xmax16(tmax));
-    // lazy reference, as in tile_step (here every weight stays below 2^8)
-    const bool jump = tmax > m_run + 8.f;
-    if (__builtin_amdgcn_ballot_w64(jump) != 0) {
-        const float m_new = jump ? tmax : m_run;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        l_part *= alpha;
-        acc_scale(alpha);
-        m_run = m_new;
-    }
+    ring_softmax_ref<4>(sv, first, m_run, l_part);
     float pv[4];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        pv[v] = __builtin_amdgcn_exp2f(sv[v] - m_run);
-        l_part += pv[v];
-    }
+    for (int v = 0; v < 4; ++v) pv[v] = __builtin_amdgcn_exp2f(sv[v]);
+    l_part += (pv[0] + pv[1]) + (pv[2] + pv[3]);
     const u32x2 ph = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
     acc_mfma_bf16<NB>(vh, ph);
 }
 
 // Two consecutive small tiles (sizes <= 32, neither wrapped nor ragged) in one step: their
-// gathers and MFMA chains interleave, and they share one max reduction, one rescale test and
-// the loop's bookkeeping.  Same arithmetic as two ring_tile<false, false, 1, 2> calls except
-// that the reference maximum moves at most once for both.
+// gathers and MFMA chains interleave, and they share one reference test and the loop's
+// bookkeeping.
 __device__ __forceinline__ void ring_pair(int rbA, int mA, int rbB, int mB, const uint16_t* rK, const uint16_t* rV,
                                           const u32x4 (&qfr)[4][2], const u32x4* kmask, int col, int grp,
-                                          float& m_run, float& l_part) {
+                                          bool& first, float& m_run, float& l_part) {
     const uint32_t* rK32 = reinterpret_cast<const uint32_t*>(rK);
     u32x2 va[2], vb[2];
 #pragma unroll
@@ -1246,30 +1260,19 @@ __device__ __forceinline__ void ring_pair(int rbA, int mA, int rbB, int mB, cons
     nvB = nvB < 0 ? 0 : (nvB > 8 ? 8 : nvB);
     const u32x4 kA = lds_row8_bf16(rK32, rbA + (int)__umul24((uint32_t)col, (uint32_t)mA) + 8 * grp) & kmask[nvA];
     const u32x4 kB = lds_row8_bf16(rK32, rbB + (int)__umul24((uint32_t)col, (uint32_t)mB) + 8 * grp) & kmask[nvB];
-    f32x4 sA = {0, 0, 0, 0}, sB = {0, 0, 0, 0};
-    sA = mfma(kA, qfr[0][0], sA);
-    sB = mfma(kB, qfr[0][0], sB);
+    const f32x4 minit = {-m_run, -m_run, -m_run, -m_run};
+    f32x4 sA = mfma(kA, qfr[0][0], minit);
+    f32x4 sB = mfma(kB, qfr[0][0], minit);
     sA = mfma(kA, qfr[0][1], sA);
     sB = mfma(kB, qfr[0][1], sB);
-    float tmax = fmaxf(fmaxf(fmaxf(sA[0], sA[1]), fmaxf(sA[2], sA[3])), fmaxf(fmaxf(sB[0], sB[1]), fmaxf(sB[2], sB[3])));
-    tmax = xmax32(xmax16(tmax));
-    const bool jump = tmax > m_run + 8.f;
-    if (__builtin_amdgcn_ballot_w64(jump) != 0) {
-        const float m_new = jump ? tmax : m_run;
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        l_part *= alpha;
-        acc_scale(alpha);
-        m_run = m_new;
-    }
-    float pa[4], pb[4];
+    float sv[8] = {sA[0], sA[1], sA[2], sA[3], sB[0], sB[1], sB[2], sB[3]};
+    ring_softmax_ref<8>(sv, first, m_run, l_part);
+    float pv[8];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-        pa[v] = __builtin_amdgcn_exp2f(sA[v] - m_run);
-        pb[v] = __builtin_amdgcn_exp2f(sB[v] - m_run);
-    }
-    l_part += ((pa[0] + pa[1]) + (pa[2] + pa[3])) + ((pb[0] + pb[1]) + (pb[2] + pb[3]));
-    const u32x2 pha = {cvt_bf16x2(pa[0], pa[1]), cvt_bf16x2(pa[2], pa[3])};
-    const u32x2 phb = {cvt_bf16x2(pb[0], pb[1]), cvt_bf16x2(pb[2], pb[3])};
+    for (int v = 0; v < 8; ++v) pv[v] = __builtin_amdgcn_exp2f(sv[v]);
+    l_part += ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
+    const u32x2 pha = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
+    const u32x2 phb = {cvt_bf16x2(pv[4], pv[5]), cvt_bf16x2(pv[6], pv[7])};
     acc_mfma_bf16<2>(va, pha);
     acc_mfma_bf16<2>(vb, phb);
 }
@@ -1511,7 +1514,8 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
     };
 
     // ---- 4. tiles
-    float m_run = -INFINITY, l_part = 0.f;
+    float m_run = 0.f, l_part = 0.f;    // the reference is set on the first tile
+    bool first = true;
     acc_zero();
     const uint16_t* rK16 = reinterpret_cast<const uint16_t*>(rK);
     const uint16_t* rV16 = reinterpret_cast<const uint16_t*>(rV);
@@ -1521,7 +1525,7 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
             land(bs, 2u * 16u * D);
             const int rb = (int)((bs & (DR_RING - 1)) >> 1);
             ring_tile<true, false, 4, 8>(rb, D, 16 * t, nexact, 16 * t + 16 > nexact, rK16, rV16, qfr, sm.kmask,
-                                         col, grp, m_run, l_part);
+                                         col, grp, first, m_run, l_part);
         }
     } else {
         // the head's last tile is the only one with fewer than 16 positions
@@ -1551,33 +1555,34 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
                     const int rb2 = (int)(((bs + 32u * (uint32_t)mi) & (DR_RING - 1)) >> 1);
                     if (mj <= 32 && rb2 + 16 * mj <= DR_RING_E && t + 1 != t_part) {
                         land(bs, 32u * (uint32_t)(mi + mj));
-                        ring_pair(rb, mi, rb2, mj, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        ring_pair(rb, mi, rb2, mj, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                         t += 2;
                         continue;
                     }
                 }
                 land(bs, 32u * (uint32_t)mi);
                 if (small) {
-                    ring_tile<false, false, 1, 2>(rb, mi, 0, CHUNK, false, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                    ring_tile<false, false, 1, 2>(rb, mi, 0, CHUNK, false, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                 } else {
                     const int i0 = 16 * (t & 15);
                     const int64_t ct = (int64_t)(t >> 4) * CHUNK;
                     const int Tc = (int)(p.N - ct < CHUNK ? p.N - ct : CHUNK);
                     const bool partial = t == t_part;
                     if (!wrap) {
-                        if (mi <= 32) ring_tile<false, false, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
-                        else if (mi <= 64) ring_tile<false, false, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
-                        else ring_tile<false, false, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        if (mi <= 32) ring_tile<false, false, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else if (mi <= 64) ring_tile<false, false, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else ring_tile<false, false, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                     } else {
-                        if (mi <= 32) ring_tile<false, true, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
-                        else if (mi <= 64) ring_tile<false, true, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
-                        else ring_tile<false, true, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, m_run, l_part);
+                        if (mi <= 32) ring_tile<false, true, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else if (mi <= 64) ring_tile<false, true, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else ring_tile<false, true, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                     }
                 }
                 ++t;
             }
         }
     }
+    if (first) m_run = -INFINITY;      // no tile: an empty partial
     f32x4 acc[8];
     acc_read(acc);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
