@@ -421,9 +421,57 @@ def main():
             "compress_ms_per_32k_tokens_all_layers": stk["compress_ms_per_32k_tokens_all_layers"],
             "decode_4bit": stk["decode_4bit"],
         }
+    # measured read ceiling for the same byte counts: the decode's time over the probe's
+    probe_sizes = [int(dbytes)]
+    if "llama_128k_stack" in result:
+        probe_sizes.append(int(result["llama_128k_stack"]["decode_bytes_per_step"]) // 32)
+    probe = bench_read_probe(cap_stream, probe_sizes)
+    dec_us = [ms_dec * 1e3] + ([result["llama_128k_stack"]["decode_us_per_layer"]] if len(probe_sizes) > 1 else [])
+    for (k, row), us in zip(probe.items(), dec_us):
+        row["decode_us"] = round(us, 2)
+        row["decode_over_probe_with_second_launch"] = round(us / row["with_second_launch"]["us"], 3)
+    result["read_probe"] = dict(probe, note="varrate_read_probe over 8 rotating windows (no last-level cache "
+                                            "reuse), graphs of 24 launches like the decode's, medians; keys are the byte counts of the "
+                                            "32K decode call and of one 128K layer's decode")
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(cfg, li, dbytes, {"decode_ms": ms_dec, "compress_ms": ms_comp})
     print(json.dumps(result), flush=True)
+
+
+def bench_read_probe(cap_stream, sizes, n_windows=8, per_graph=N_CACHE_SLOTS):
+    """Measured read ceiling: the library's streaming-read probe over `nbytes` (each size in
+    `sizes`), replayed from a graph of `per_graph` launches (as many as the decode graphs hold)
+    that cycles through `n_windows` distinct windows so that no launch finds its bytes in the
+    256 MB last-level cache, alone and followed by a one-element fill (a second dependent
+    launch, the shape of a decode call: streaming kernel + merge)."""
+    import torch
+
+    import paper_2607_15498_amd as vr
+    dev = torch.device("cuda:0")
+    span = max(sizes)
+    span = (span + 4095) // 4096 * 4096
+    buf = torch.ones(n_windows * span // 4, dtype=torch.int32, device=dev)
+    sink = torch.zeros(vr.PROBE_WGS, dtype=torch.int32, device=dev)
+    tiny = torch.zeros(1, dtype=torch.int32, device=dev)
+    res = {}
+    for nb in sizes:
+        nb = nb // 16 * 16
+        row = {}
+        for label, second in (("alone", False), ("with_second_launch", True)):
+            g_ = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_, stream=cap_stream):
+                for i in range(per_graph):
+                    vr.read_probe(buf[(i % n_windows) * span // 4:], nb, sink)
+                    if second:
+                        tiny.fill_(i)
+            torch.cuda.synchronize()
+            st = _replay_stats(g_, 8, per_graph)
+            row[label] = {"us": round(st["p50"] * 1e3, 2),
+                          "GBps": round(nb / (st["p50"] * 1e-3) / 1e9, 1),
+                          "frac": round(nb / (st["p50"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        res[str(nb)] = row
+    del buf
+    return res
 
 
 def bench_rope(args, cap_stream, n_slots=12):

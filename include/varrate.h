@@ -167,6 +167,15 @@ VARRATE_API const char* varrate_status_string(int status);
 VARRATE_API const char* varrate_last_error(void);   /* thread-local text of the last failure           */
 VARRATE_API int varrate_version(void);               /* ABI version (1)                                 */
 
+/* Measurement aid (not part of the codec): reads `bytes` (a multiple of 16, > 0) of device
+ * memory at `src` (16-byte aligned) with a plain streaming kernel of VARRATE_PROBE_WGS
+ * workgroups, asynchronously on `stream`, so a caller can time what reading a given number of
+ * bytes takes on this device.  `sink` is a device buffer of VARRATE_PROBE_WGS uint32 words that
+ * the kernel may write (in practice it does not); its contents are meaningless.  EINVAL for
+ * NULL or misaligned pointers or a bad size.                                                 */
+#define VARRATE_PROBE_WGS 4096
+VARRATE_API int varrate_read_probe(const void* src, size_t bytes, uint32_t* sink, void* stream);
+
 /* ---- sizing ----------------------------------------------------------------------------- */
 /* Coded budget of Sec. 3.1 Eq. (3) in per-head coefficient units, with kappa an integer
  * percent: B = floor(kappa_pct * n * d / 100) - w * d (the exact window costs w d).       */

@@ -252,6 +252,19 @@ def append_exact(shape: Shape, cache: Cache, k_new: torch.Tensor, v_new: torch.T
     return cache
 
 
+PROBE_WGS = 4096
+
+
+def read_probe(src: torch.Tensor, nbytes: int, sink: torch.Tensor) -> None:
+    """Measurement aid: a plain streaming read of the first `nbytes` bytes of `src` (device
+    memory) on the current stream; `sink` is a device int32 tensor of PROBE_WGS elements."""
+    if sink.numel() < PROBE_WGS or not sink.is_cuda or sink.element_size() != 4:
+        raise VarRateError(_lib.VARRATE_EINVAL, "sink: a device tensor of 4096 32-bit words")
+    if nbytes > src.numel() * src.element_size():
+        raise VarRateError(_lib.VARRATE_EINVAL, "nbytes past the end of src")
+    _check(library().varrate_read_probe(_dev_ptr(src), int(nbytes), _dev_ptr(sink), _stream()))
+
+
 def decode_workspace(shape: Shape, S: int, Q: int, device="cuda") -> torch.Tensor:
     need = int(library().varrate_decode_workspace_bytes(ctypes.byref(shape.c()), S, Q))
     return _WS.get(f"decode", need, device)

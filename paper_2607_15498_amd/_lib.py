@@ -25,6 +25,7 @@ EXPORTS = (
     "varrate_anchor_search", "varrate_anchor_encode",
     "varrate_jcache_bytes", "varrate_joint_compress_workspace_bytes", "varrate_joint_decode_workspace_bytes",
     "varrate_joint_compress", "varrate_joint_decode_attn", "varrate_joint_append_exact",
+    "varrate_read_probe",
 )
 DECODE_SCRATCH_BYTES = 8 << 20
 
@@ -116,6 +117,7 @@ def load() -> ctypes.CDLL:
         "varrate_joint_compress": (ctypes.c_int, [P(Shape), vp, vp, vp, vp, P(JCacheC), vp, vp, sz, vp]),
         "varrate_joint_decode_attn": (ctypes.c_int, [P(Shape), P(JCacheC), i32, vp, i32, vp, vp, vp, sz, vp]),
         "varrate_joint_append_exact": (ctypes.c_int, [P(Shape), P(JCacheC), vp, vp, vp]),
+        "varrate_read_probe": (ctypes.c_int, [vp, ctypes.c_size_t, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)

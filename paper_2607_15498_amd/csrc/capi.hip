@@ -206,6 +206,13 @@ const char* varrate_last_error(void) { return g_err.c_str(); }
 
 int varrate_version(void) { return 1; }
 
+int varrate_read_probe(const void* src, size_t bytes, uint32_t* sink, void* stream) {
+    if (!src || !sink || !aligned16(src) || bytes == 0 || bytes % 16 != 0)
+        return fail(VARRATE_EINVAL, "read probe: src and sink non-NULL, src 16-byte aligned, bytes a positive "
+                                    "multiple of 16");
+    return hip_status(launch_read_probe(src, bytes, sink, (hipStream_t)stream), "read probe launch");
+}
+
 int64_t varrate_coded_budget(int64_t n, int32_t d, int32_t w, int32_t kappa_pct) {
     return ((int64_t)kappa_pct * n * d) / 100 - (int64_t)w * d;
 }

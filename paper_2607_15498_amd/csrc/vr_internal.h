@@ -109,5 +109,7 @@ hipError_t launch_quantize(const varrate_shape& sh, const varrate_cache& c, varr
 size_t decode_group_bytes(const varrate_shape& sh, int S, int Q);
 // this device's address of the fixed decode scratch array (looked up once per device)
 hipError_t decode_scratch(uint8_t** out);
+// streaming-read probe (measurement aid)
+hipError_t launch_read_probe(const void* src, size_t bytes, uint32_t* sink, hipStream_t st);
 
 }  // namespace vr

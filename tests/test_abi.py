@@ -264,3 +264,14 @@ def test_shared_basis_validation(L):
     assert L.varrate_jcache_bytes(ctypes.byref(_shape(rope=1, rope_theta=th)), 1024, 64, ctypes.byref(out)) == -3
     assert L.varrate_joint_decode_workspace_bytes(ctypes.byref(sh), 1024, 1, 2) == 0      # 64 query rows
     assert L.varrate_joint_decode_workspace_bytes(ctypes.byref(sh), 1024, 1, 1) > 0
+
+
+def test_read_probe_validation(L):
+    # host-side checks only: NULL buffers, a misaligned source or a size that is not a
+    # positive multiple of 16 never reach a launch
+    assert L.varrate_read_probe(None, 16, None, None) == -1
+    assert L.varrate_read_probe(ctypes.c_void_p(16), 16, None, None) == -1
+    assert L.varrate_read_probe(ctypes.c_void_p(24), 16, ctypes.c_void_p(64), None) == -1
+    assert L.varrate_read_probe(ctypes.c_void_p(16), 0, ctypes.c_void_p(64), None) == -1
+    assert L.varrate_read_probe(ctypes.c_void_p(16), 24, ctypes.c_void_p(64), None) == -1
+    assert b"read probe" in L.varrate_last_error()

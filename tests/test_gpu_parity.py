@@ -590,3 +590,20 @@ def test_run_twice_bitwise_identical(vr):
         outs.append((host(sb), host(cache.rank), host(cache.coef_k), host(cache.coef_v), host(o)))
     for a, b in zip(*outs):
         assert np.array_equal(a, b)
+
+
+def test_read_probe_runs_clean(vr):
+    """The measurement probe reads the bytes it is given and leaves the sink alone (the fold
+    of an all-ones buffer is zero, never the sink's trigger value); errors come back as codes."""
+    import torch
+    say("read probe: 1 MiB + ragged 48 B tail")
+    buf = torch.ones(((1 << 20) + 48) // 4, dtype=torch.int32, device="cuda")
+    sink = torch.zeros(vr.PROBE_WGS, dtype=torch.int32, device="cuda")
+    vr.read_probe(buf, (1 << 20) + 48, sink)
+    vr.read_probe(buf, 16, sink)
+    torch.cuda.synchronize()
+    assert int(sink.abs().sum()) == 0
+    with pytest.raises(vr.VarRateError):
+        vr.read_probe(buf[1:], 16, sink)          # misaligned source
+    with pytest.raises(vr.VarRateError):
+        vr.read_probe(buf, 4 * buf.numel() + 16, sink)
