@@ -20,19 +20,21 @@
 //
 // Kernel chain.  Every pass over the tokens is a grid of 256-thread workgroups holding 1024
 // consecutive tokens each (wave w: the 256 tokens of one storage chunk, four coalesced loads
-// per lane).  The small scans between passes (4097 coarse bins, 4096 fine bins, 2048 digit
-// bins) are repeated by every workgroup of the pass that needs them, which costs less than
-// a launch of their own; workgroup 0 records the results for the later kernels.
+// per lane).  The small scans and searches between passes (4097 coarse bins, 4096 fine bins,
+// 2048 digit bins, the threshold among the candidates) are repeated by every workgroup of the
+// pass that needs them, which costs less than a launch of their own; workgroup 0 records the
+// results for the later kernels.
 //   al_minmax   per-workgroup min / max of sbar; clears the histograms and counters
 //   al_weights  u, coarse histogram of u >> 12 (count, sum of the low bits), max u
 //   al_fine     coarse scan -> the bin holding tau_lo; counts of the low bits inside it
 //   al_floors   fine scan -> tau_lo, k, Q, M; floors, keys phi, sum of floors, histogram
 //               of phi's top 11 significant bits
 //   al_gather   rho; the digit bucket holding the rho-th largest key; its candidates
-//   al_select   (one workgroup) the exact threshold among the candidates
-//   al_final    final ranks, each chunk's storage order (srank, sidx) and its size in tile
-//               rectangles (16 x the largest rank of each 16-position tile)
-//   al_scan     (one workgroup) chunk offsets
+//   al_final    the exact threshold among the candidates; final ranks, each chunk's storage
+//               order (srank, sidx) and its size in tile rectangles (16 x the largest rank of
+//               each 16-position tile)
+//   al_scan     (one workgroup; the allocation entry point only) chunk offsets.  In the
+//               compress path the projection scans the chunk sizes itself.
 #include "vr_internal.h"
 
 namespace vr {
@@ -61,7 +63,7 @@ struct AlCtl {
     long long M, kcap;
     uint32_t tau_lo;
     int sh0;                     // shift of the first selection digit
-    // selection (al_gather, then al_select)
+    // selection (al_gather, then every workgroup of al_final)
     unsigned long long pv, pm, T_hi, T_lo;
     long long need;              // rank of the threshold inside the bucket
     int done, any;
@@ -81,6 +83,7 @@ struct AlWs {
     uint32_t* u;
     uint64_t* phi;
     uint64_t* cand;              // 2 x u64 per candidate (hi = phi, lo = (u, ~t))
+    uint32_t* csum;              // each chunk's size (tile rectangles, or ranks for the shared basis)
 };
 constexpr int NCB_PAD = (NCB + 3) & ~3;
 
@@ -99,7 +102,8 @@ static AlWs al_ws(uint8_t* ws, int64_t N) {
     w.mm = (float2*)p;                p += align256((size_t)nwg * sizeof(float2));
     w.u = (uint32_t*)p;               p += align256((size_t)N * 4);
     w.phi = (uint64_t*)p;             p += align256((size_t)N * 8);
-    w.cand = (uint64_t*)p;
+    w.cand = (uint64_t*)p;            p += align256((size_t)N * 16);
+    w.csum = (uint32_t*)p;
     return w;
 }
 
@@ -108,7 +112,8 @@ size_t allocate_ws_bytes(const varrate_shape& sh) {
     const int64_t nwg = (N + AK_TOK - 1) / AK_TOK;
     size_t b = align256(NCB_PAD * 12 + NFB * 4 + NDB * 4 + ((sizeof(AlCtl) + 15) & ~(size_t)15));
     b += align256((size_t)nwg * sizeof(float2)) + align256((size_t)N * 4) + align256((size_t)N * 8);
-    return b + align256((size_t)N * 16);
+    const int64_t n_chunks = (N + CHUNK - 1) / CHUNK;
+    return b + align256((size_t)N * 16) + align256((size_t)(n_chunks + 1) * 4);
 }
 
 // ---- workgroup primitives ----------------------------------------------------------------
@@ -690,67 +695,85 @@ __global__ __launch_bounds__(AK_T) void al_gather(int64_t N, int64_t B, const ui
 
 }
 
-// The exact threshold among the bucket's candidates (one workgroup).  Up to AS_T candidates
-// (the usual case: a bucket holds about 2^-11 of the uncapped tokens) each find their
-// rank among the others directly; more go through the radix narrowing.
-constexpr int AS_T = 1024;
+// The exact threshold among the bucket's candidates, found by every workgroup of the final
+// pass from the same list with the same arithmetic, so all of them agree and no one-workgroup
+// pass sits between the gather and the final ranks.  Up to AK_T candidates (the usual case: a
+// digit bucket holds about 2^-11 of the uncapped tokens) rank one another directly, each
+// candidate's comparisons split over the workgroup; up to SEL_CAP go through the radix
+// narrowing in LDS; more (many equal weights) through the same narrowing over the list in
+// memory.
+struct AlSelSmem {
+    unsigned long long chi[SEL_CAP], clo[SEL_CAP];
+    uint32_t cnt[NDB];
+    unsigned long long wt64[AK_T / 64];
+    uint32_t wt32[AK_T / 64];
+    unsigned long long T[2];
+    SelState sel;
+};
 
-__global__ __launch_bounds__(AS_T) void al_select(int64_t N, const uint64_t* __restrict__ cand,
-                                                  AlCtl* __restrict__ ctl) {
-    __shared__ uint32_t cnt[NDB];
-    __shared__ unsigned long long chi[SEL_CAP], clo[SEL_CAP];
-    __shared__ unsigned long long wtot64[AS_T / 64];
-    __shared__ uint32_t wtot32[AS_T / 64];
-    __shared__ SelState sel;
+// (my_hi, my_lo): list entry min(threadIdx.x, N - 1), loaded by the caller ahead of time
+__device__ void al_threshold(int64_t N, const uint64_t* __restrict__ cand, const AlCtl* __restrict__ ctl,
+                             uint64_t my_hi, uint64_t my_lo, AlSelSmem& s, uint64_t& T_hi, uint64_t& T_lo) {
     const int tid = threadIdx.x;
-    // the candidates' loads issue with the state's (slots past the list hold stale keys and
-    // are not used)
-    const int64_t ti = tid < N ? tid : N - 1;
-    const uint64_t my_hi = cand[2 * ti], my_lo = cand[2 * ti + 1];
-    if (ctl->done) return;
+    if (ctl->done) {                 // nothing to take (T = ~0), or the whole bucket (T = its edge)
+        T_hi = ctl->T_hi;
+        T_lo = ctl->T_lo;
+        return;
+    }
     const int nc = (int)ctl->ncand;
     const int64_t need = ctl->need;
-    if (nc <= AS_T) {
-        if (tid < nc) { chi[tid] = my_hi; clo[tid] = my_lo; }
+    if (nc <= AK_T) {
+        if (tid < nc) { s.chi[tid] = my_hi; s.clo[tid] = my_lo; s.cnt[tid] = 0; }
         __syncthreads();
-        if (tid < nc) {
-            // keys are unique: exactly one candidate has need - 1 larger ones
-            int above = 0;
-            for (int j = 0; j < nc; ++j) {
-                const uint64_t h = chi[j], l = clo[j];
-                above += (h > my_hi || (h == my_hi && l > my_lo)) ? 1 : 0;
+        // candidate i = tid mod nc against slice tid / nc of the list (nseg slices)
+        const int nseg = AK_T / nc, per = (nc + nseg - 1) / nseg;
+        if (tid < nc * nseg) {
+            const int i = tid % nc, j0 = (tid / nc) * per;
+            const int j1 = j0 + per < nc ? j0 + per : nc;
+            const uint64_t h = s.chi[i], l = s.clo[i];
+            uint32_t above = 0;
+            for (int j = j0; j < j1; ++j) {
+                const uint64_t hj = s.chi[j], lj = s.clo[j];
+                above += (hj > h || (hj == h && lj > l)) ? 1u : 0u;
             }
-            if (above == need - 1) { ctl->T_hi = my_hi; ctl->T_lo = my_lo; }
+            if (above) atomicAdd(&s.cnt[i], above);
         }
+        __syncthreads();
+        // keys are unique: exactly one candidate has need - 1 larger ones
+        if (tid < nc && (int64_t)s.cnt[tid] == need - 1) { s.T[0] = s.chi[tid]; s.T[1] = s.clo[tid]; }
+        __syncthreads();
+        T_hi = s.T[0];
+        T_lo = s.T[1];
         return;
     }
     if (tid == 0) {
-        sel.pv = ctl->pv; sel.pm = ctl->pm; sel.need = need;
-        sel.T_hi = ~0ull; sel.T_lo = ~0ull; sel.phase = 0; sel.done = 0;
+        s.sel.pv = ctl->pv; s.sel.pm = ctl->pm; s.sel.need = need;
+        s.sel.T_hi = ~0ull; s.sel.T_lo = ~0ull; s.sel.phase = 0; s.sel.done = 0;
     }
     if (nc <= SEL_CAP) {
-        for (int i = tid; i < nc; i += AS_T) { chi[i] = cand[2 * i]; clo[i] = cand[2 * i + 1]; }
+        for (int i = tid; i < nc; i += AK_T) { s.chi[i] = cand[2 * i]; s.clo[i] = cand[2 * i + 1]; }
         __syncthreads();
-        radix_narrow<AS_T>([&](auto f) {
-            for (int i = tid; i < nc; i += AS_T) f(chi[i], clo[i]);
-        }, sel, cnt, wtot32, wtot64);
+        radix_narrow<AK_T>([&](auto f) {
+            for (int i = tid; i < nc; i += AK_T) f(s.chi[i], s.clo[i]);
+        }, s.sel, s.cnt, s.wt32, s.wt64);
     } else {
         __syncthreads();
-        radix_narrow<AS_T>([&](auto f) {
-            for (int i0 = 0; i0 < nc; i0 += 4 * AS_T) {
+        radix_narrow<AK_T>([&](auto f) {
+            for (int i0 = 0; i0 < nc; i0 += 4 * AK_T) {
                 uint64_t h[4], l[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    const int i = i0 + k * AS_T + tid;
+                    const int i = i0 + k * AK_T + tid;
                     if (i < nc) { h[k] = cand[2 * i]; l[k] = cand[2 * i + 1]; }
                 }
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
-                    if (i0 + k * AS_T + tid < nc) f(h[k], l[k]);
+                    if (i0 + k * AK_T + tid < nc) f(h[k], l[k]);
             }
-        }, sel, cnt, wtot32, wtot64);
+        }, s.sel, s.cnt, s.wt32, s.wt64);
     }
-    if (tid == 0) { ctl->T_hi = sel.T_hi; ctl->T_lo = sel.T_lo; }
+    T_hi = s.sel.T_hi;
+    T_lo = s.sel.T_lo;
 }
 
 // Stored order of one chunk per wave: rank descending, token index ascending (a stable
@@ -816,17 +839,24 @@ __device__ uint32_t chunk_order(unsigned long long (*m)[4], uint16_t* above, con
     return wave_sum(tile_sum);
 }
 
-// ---- 6. final ranks, chunk sums, storage order ----------------------------------------------------
-
+// ---- 6. threshold, final ranks, each chunk's size ------------------------------------------------
+// Per-head codec (ORDER): 8-bit ranks, each chunk's storage order (srank, sidx) and its size in
+// tile rectangles.  Shared basis: 16-bit ranks in original order and each chunk's rank sum.
+// The chunk sizes go to csum[c] (unscanned: the scan runs in whichever pass reads them next).
+template <typename RT, bool ORDER>
 __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __restrict__ u_ws,
                                                  const uint64_t* __restrict__ phi_ws,
-                                                 uint8_t* __restrict__ rank, uint8_t* __restrict__ srank,
-                                                 uint32_t* __restrict__ sidx, uint32_t* __restrict__ chunk_off,
-                                                 const AlCtl* __restrict__ ctl) {
+                                                 const uint64_t* __restrict__ cand, RT* __restrict__ rank,
+                                                 uint8_t* __restrict__ srank, uint32_t* __restrict__ sidx,
+                                                 uint32_t* __restrict__ csum, const AlCtl* __restrict__ ctl) {
+    __shared__ AlSelSmem ss;
     // storage order of each wave's chunk: per-rank 256-bit token masks, and the count of
     // tokens of higher rank per rank value
-    __shared__ unsigned long long msk[AK_T / 64][NRV][4];
-    __shared__ uint16_t above_r[AK_T / 64][NRV];
+    __shared__ unsigned long long msk[ORDER ? AK_T / 64 : 1][NRV][4];
+    __shared__ uint16_t above_r[ORDER ? AK_T / 64 : 1][NRV];
+    // every load of the pass goes out first: the tokens, one list entry per thread
+    const int64_t ti = (int64_t)threadIdx.x < N ? (int64_t)threadIdx.x : N - 1;
+    const uint64_t my_hi = cand[2 * ti], my_lo = cand[2 * ti + 1];
     uint64_t phi[AK_PER];
     uint32_t u[AK_PER], r[AK_PER];
 #pragma unroll
@@ -836,7 +866,8 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
         u[k] = u_ws[tt];
         r[k] = rank[tt];
     }
-    const uint64_t T_hi = ctl->T_hi, T_lo = ctl->T_lo;
+    uint64_t T_hi, T_lo;
+    al_threshold(N, cand, ctl, my_hi, my_lo, ss, T_hi, T_lo);
     const bool any = ctl->any;
 #pragma unroll
     for (int k = 0; k < AK_PER; ++k) {
@@ -846,49 +877,54 @@ __global__ __launch_bounds__(AK_T) void al_final(int64_t N, const uint32_t* __re
             const bool take = phi[k] > T_hi || (phi[k] == T_hi && lo_key(u[k], t) >= T_lo);
             if (take) {
                 r[k] += 1;
-                rank[t] = (uint8_t)r[k];
+                rank[t] = (RT)r[k];
             }
         }
     }
     const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + wv;
-    const uint32_t tile_sum = chunk_order(msk[wv], above_r[wv], r, c * CHUNK, N, srank, sidx);
-    if (lane == 0 && c * CHUNK < N) chunk_off[c] = tile_sum;
-}
-
-// ---- 6'. shared basis: final ranks (16-bit, original order) and each chunk's rank sum ---------
-__global__ __launch_bounds__(AK_T) void al_final_joint(int64_t N, const uint32_t* __restrict__ u_ws,
-                                                       const uint64_t* __restrict__ phi_ws,
-                                                       uint16_t* __restrict__ rank, uint32_t* __restrict__ chunk_off,
-                                                       const AlCtl* __restrict__ ctl) {
-    const uint64_t T_hi = ctl->T_hi, T_lo = ctl->T_lo;
-    const bool any = ctl->any;
-    uint32_t sum = 0;
+    uint32_t size;
+    if constexpr (ORDER) {
+        size = chunk_order(msk[wv], above_r[wv], r, c * CHUNK, N, srank, sidx);
+    } else {
+        uint32_t sum = 0;
 #pragma unroll
-    for (int k = 0; k < AK_PER; ++k) {
-        const int64_t t = al_tok(k);
-        if (t >= N) continue;
-        uint32_t r = rank[t];
-        const uint64_t phi = phi_ws[t];
-        if (any && phi != CAPPED && (phi > T_hi || (phi == T_hi && lo_key(u_ws[t], t) >= T_lo))) {
-            r += 1;
-            rank[t] = (uint16_t)r;
-        }
-        sum += r;
+        for (int k = 0; k < AK_PER; ++k)
+            if (al_tok(k) < N) sum += r[k];
+        size = wave_sum(sum);
     }
-    sum = wave_sum(sum);
-    const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + (threadIdx.x >> 6);
-    if ((threadIdx.x & 63) == 0 && c * CHUNK < N) chunk_off[c] = sum;
+    if (lane == 0 && c * CHUNK < N) csum[c] = size;
 }
 
-// ---- 8. shared basis: per-token offsets = chunk offset + the chunk's earlier ranks -------------
+// Exclusive prefix of the chunk sizes up to chunk c (c + 1 <= n_chunks) by one wave.
+// Eight independent loads per lane at a time (clamped addresses, masked values).
+__device__ __forceinline__ uint32_t chunk_prefix(const uint32_t* __restrict__ csum, int64_t c) {
+    const int lane = threadIdx.x & 63;
+    uint32_t pre = 0;
+    for (int64_t i0 = 0; i0 < c; i0 += 8 * 64) {
+        uint32_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int64_t i = i0 + 64 * j + lane;
+            v[j] = csum[i < c ? i : 0];
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pre += i0 + 64 * j + lane < c ? v[j] : 0u;
+    }
+    return wave_sum(pre);
+}
+
+// ---- 7. shared basis: chunk offsets and per-token offsets = chunk offset + the chunk's
+//         earlier ranks (one wave per chunk, which scans the chunk sums before it itself)
 __global__ __launch_bounds__(AK_T) void al_offsets(int64_t N, const uint16_t* __restrict__ rank,
-                                                   const uint32_t* __restrict__ chunk_off,
+                                                   const uint32_t* __restrict__ csum,
+                                                   uint32_t* __restrict__ chunk_off,
                                                    uint32_t* __restrict__ offset, int n_chunks) {
     const int lane = threadIdx.x & 63;
     const int64_t c = (int64_t)blockIdx.x * (AK_TOK / CHUNK) + (threadIdx.x >> 6);
     if (c * CHUNK >= N) return;
-    uint32_t pre = chunk_off[c];
+    uint32_t pre = chunk_prefix(csum, c);
+    if (lane == 0) chunk_off[c] = pre;
 #pragma unroll
     for (int k = 0; k < AK_PER; ++k) {
         const int64_t t = c * CHUNK + 64 * k + lane;       // the wave's tokens, in index order
@@ -902,21 +938,26 @@ __global__ __launch_bounds__(AK_T) void al_offsets(int64_t N, const uint16_t* __
         if (t < N) offset[t] = pre + x - r;
         pre += __shfl(x, 63, 64);
     }
-    if (blockIdx.x == 0 && threadIdx.x == 0) offset[N] = chunk_off[n_chunks];
+    if (c == n_chunks - 1 && lane == 0) {       // the totals
+        chunk_off[n_chunks] = pre;
+        offset[N] = pre;
+    }
 }
 
-// ---- 7. chunk offsets (in place: chunk sums -> exclusive prefix, total at [n_chunks]) --------
+// ---- 7'. chunk offsets for the allocation entry point (chunk sizes -> exclusive prefix,
+//          total at [n_chunks]); the compress path leaves this scan to the projection
 constexpr int SCAN_T = 1024;
 constexpr int SCAN_PT = MAX_CODED_CHUNKS / SCAN_T;   // chunk sums per thread
 
-__global__ __launch_bounds__(SCAN_T) void al_scan(uint32_t* __restrict__ chunk_off, int n_chunks) {
+__global__ __launch_bounds__(SCAN_T) void al_scan(const uint32_t* __restrict__ csum,
+                                                  uint32_t* __restrict__ chunk_off, int n_chunks) {
     __shared__ uint32_t wt32[SCAN_T / 64];
     const int per = (n_chunks + SCAN_T - 1) / SCAN_T;
     const int i0 = per * threadIdx.x;
     uint32_t v[SCAN_PT], loc = 0;
 #pragma unroll
     for (int j = 0; j < SCAN_PT; ++j) {
-        v[j] = j < per && i0 + j < n_chunks ? chunk_off[i0 + j] : 0u;
+        v[j] = j < per && i0 + j < n_chunks ? csum[i0 + j] : 0u;
         loc += v[j];
     }
     uint32_t total;
@@ -931,7 +972,7 @@ __global__ __launch_bounds__(SCAN_T) void al_scan(uint32_t* __restrict__ chunk_o
 }
 
 hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_cache& c,
-                           uint8_t* ws, hipStream_t st, const float* s_part) {
+                           uint8_t* ws, hipStream_t st, const float* s_part, const uint32_t** chunk_sizes) {
     const int64_t N = sh.n - sh.w;
     const int R = D, r_min = sh.r_min;
     const int64_t B = c.B;
@@ -948,9 +989,11 @@ hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_c
     al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
     al_floors<uint8_t><<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
     al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
-    al_select<<<1, AS_T, 0, st>>>(N, w.cand, w.ctl);
-    al_final<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, c.rank, c.srank, c.sidx, c.chunk_off, w.ctl);
-    al_scan<<<1, SCAN_T, 0, st>>>(c.chunk_off, n_chunks);
+    al_final<uint8_t, true><<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, w.cand, c.rank, c.srank, c.sidx, w.csum, w.ctl);
+    if (chunk_sizes)
+        *chunk_sizes = w.csum;
+    else
+        al_scan<<<1, SCAN_T, 0, st>>>(w.csum, c.chunk_off, n_chunks);
     return hipGetLastError();
 }
 
@@ -972,10 +1015,8 @@ hipError_t launch_allocate_joint(const varrate_shape& sh, int R, int64_t B, cons
     al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
     al_floors<uint16_t><<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, rank, w.phi, w.d_cnt, w.ctl);
     al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
-    al_select<<<1, AS_T, 0, st>>>(N, w.cand, w.ctl);
-    al_final_joint<<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, rank, chunk_off, w.ctl);
-    al_scan<<<1, SCAN_T, 0, st>>>(chunk_off, n_chunks);
-    al_offsets<<<nwg, AK_T, 0, st>>>(N, rank, chunk_off, offset, n_chunks);
+    al_final<uint16_t, false><<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, w.cand, rank, nullptr, nullptr, w.csum, w.ctl);
+    al_offsets<<<nwg, AK_T, 0, st>>>(N, rank, w.csum, chunk_off, offset, n_chunks);
     return hipGetLastError();
 }
 

@@ -380,8 +380,9 @@ hipError_t launch_anchor_encode(const varrate_shape& sh, const void* K, const vo
         (uint16_t*)w.Kr, (uint16_t*)w.Vr, (uint16_t*)c.k_anchor, (uint16_t*)c.v_anchor);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if ((e = launch_allocate(shc, w.sbar_c, c, w.alloc, st)) != hipSuccess) return e;
-    if ((e = launch_project(shc, w.Kr, w.Vr, PK, PV, c, st)) != hipSuccess) return e;
+    const uint32_t* csz = nullptr;
+    if ((e = launch_allocate(shc, w.sbar_c, c, w.alloc, st, nullptr, &csz)) != hipSuccess) return e;
+    if ((e = launch_project(shc, w.Kr, w.Vr, PK, PV, c, st, csz)) != hipSuccess) return e;
     anc_zero<<<(unsigned)((na + 255) / 256), 256, 0, st>>>(w.cnt, na);
     anc_count<<<(unsigned)((Nc + 255) / 256), 256, 0, st>>>(c.sidx, nn, Nc, c.snn, w.cnt);
     anc_scan<<<1, 1024, 0, st>>>(w.cnt, na, c.inv_off);

@@ -178,13 +178,15 @@ size_t compress_ws(const varrate_shape& sh) {
 
 // Eq. (6) projection; with rotary keys, of the keys turned back to pre-RoPE (Algorithm 1,
 // first step) in the workspace
+// chunk_sizes: as launch_project's (NULL: the cache's chunk table is already scanned)
 hipError_t project_keys(const varrate_shape& sh, const void* K, const void* V, const float* PK,
-                        const float* PV, varrate_cache& c, uint8_t* ws, hipStream_t st) {
-    if (!sh.rope) return launch_project(sh, K, V, PK, PV, c, st);
+                        const float* PV, varrate_cache& c, uint8_t* ws, hipStream_t st,
+                        const uint32_t* chunk_sizes = nullptr) {
+    if (!sh.rope) return launch_project(sh, K, V, PK, PV, c, st, chunk_sizes);
     void* Kr = ws + compress_ws_base(sh);
     hipError_t e = launch_rope_unrotate(sh, K, Kr, st);
     if (e != hipSuccess) return e;
-    return launch_project(sh, Kr, V, PK, PV, c, st);
+    return launch_project(sh, Kr, V, PK, PV, c, st, chunk_sizes);
 }
 
 }  // namespace
@@ -335,16 +337,18 @@ int varrate_compress(const varrate_shape* sh, const void* K, const void* V, cons
     }
     // salience passes, then the allocation's first pass pools sbar from the column sums
     // itself (the separate pooling launch is skipped), then the rest of the allocation and
-    // the projection: the same results as the three entry points in turn
+    // the projection, which scans the chunk sizes into the chunk table itself (the
+    // allocation's scan launch is skipped): the same results as the three entry points in turn
     hipStream_t st = (hipStream_t)stream;
     uint8_t* w0 = (uint8_t*)ws;
     if ((rc = hip_status(launch_salience(*sh, K, Qw, sbar, w0, st, false), "salience launch"))) return rc;
     c->N = sh->n - sh->w;
     c->B = varrate_coded_budget(sh->n, sh->d, sh->w, sh->kappa_pct);
     uint8_t* w8 = w0 + align256(salience_ws_bytes(*sh));
-    if ((rc = hip_status(launch_allocate(*sh, sbar, *c, w8, st, salience_part(*sh, w0)), "allocate launch")))
+    const uint32_t* csz = nullptr;
+    if ((rc = hip_status(launch_allocate(*sh, sbar, *c, w8, st, salience_part(*sh, w0), &csz), "allocate launch")))
         return rc;
-    if ((rc = hip_status(project_keys(*sh, K, V, PK, PV, *c, w0, st), "project launch"))) return rc;
+    if ((rc = hip_status(project_keys(*sh, K, V, PK, PV, *c, w0, st, csz), "project launch"))) return rc;
     c->n_exact = sh->w;
     return VARRATE_OK;
 }

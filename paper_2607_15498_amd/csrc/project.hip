@@ -35,7 +35,9 @@ constexpr int PJ_FRAGS = 8 * 4;                       // (16-row block a, 32-col
 template <bool F32> __host__ __device__ constexpr int pj_xd() { return F32 ? 2 : 3; }
 static_assert(PJ_CPW * PJ_TPC % PJ_WAVES == 0, "whole tiles per wave");
 
-static inline size_t project_smem_bytes() { return (size_t)PJ_FRAGS * 64 * 16 * 2; }
+constexpr size_t PJ_FRAG_BYTES = (size_t)PJ_FRAGS * 64 * 16 * 2;
+// the basis fragments (hi, lo), then the workgroup's chunk offsets
+static inline size_t project_smem_bytes() { return PJ_FRAG_BYTES + 64; }
 
 // Layout rows of one tile, per lane: srank of slots 4 lane .. 4 lane + 3 of the chunk, and
 // the token of slot 16 h + (lane % 16).
@@ -121,7 +123,7 @@ __device__ __forceinline__ void pj_load_x(PjX<F32>& x, const void* X, uint32_t t
 template <bool F32>
 __device__ __forceinline__ void pj_compute(PjOut<F32>& o, const PjMeta& m, const PjX<F32>& x, int k,
                                            int wave, int c0, int n_chunks, int64_t N, bool is_v,
-                                           const uint32_t* __restrict__ chunk_off,
+                                           const uint32_t* cbase,
                                            int64_t coef_stride, const u32x4* frag_hi,
                                            const u32x4* frag_lo) {
     const int lane = threadIdx.x & 63, col = lane & 15, grp = lane >> 4;
@@ -144,7 +146,7 @@ __device__ __forceinline__ void pj_compute(PjOut<F32>& o, const PjMeta& m, const
     }
     const int mt = __builtin_amdgcn_readfirstlane((int)(__shfl(quad, 4 * h, 64) & 0xFF));
     const uint32_t before = __builtin_amdgcn_readfirstlane(__shfl(incl, 4 * h, 64)) - (uint32_t)mt;
-    const uint32_t base = live ? chunk_off[c] : 0u;
+    const uint32_t base = live ? cbase[c - c0] : 0u;
     o.off = __builtin_amdgcn_readfirstlane(base + 16u * before);
     o.m = mt;
     // the tile stays inside the head's stream whatever the layout tables hold
@@ -259,11 +261,12 @@ template <bool F32, bool IS_V>
 __device__ __forceinline__ void project_body(
     const void* __restrict__ K, const void* __restrict__ V, const float* __restrict__ PK,
     const float* __restrict__ PV, int64_t N, int G, int w, const uint8_t* __restrict__ srank,
-    const uint32_t* __restrict__ sidx, const uint32_t* __restrict__ chunk_off, int n_chunks,
-    void* __restrict__ coef_k, void* __restrict__ coef_v, int64_t coef_stride,
+    const uint32_t* __restrict__ sidx, const uint32_t* __restrict__ csum, uint32_t* __restrict__ chunk_off,
+    int n_chunks, void* __restrict__ coef_k, void* __restrict__ coef_v, int64_t coef_stride,
     void* __restrict__ k_exact, void* __restrict__ v_exact, int64_t cap, uint8_t* smem) {
     u32x4* frag_hi = reinterpret_cast<u32x4*>(smem);
     u32x4* frag_lo = frag_hi + PJ_FRAGS * 64;
+    uint32_t* cbase = reinterpret_cast<uint32_t*>(smem + PJ_FRAG_BYTES);
 
     const int g = blockIdx.y, kv = IS_V ? 1 : 0;
     const void* X = kv ? V : K;
@@ -274,6 +277,21 @@ __device__ __forceinline__ void project_body(
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c0 = blockIdx.x * PJ_CPW;
+
+    // offsets of this workgroup's chunks (wave 0): read from the chunk table, or (csum given)
+    // scanned from the chunk sizes.  The sizes of the first 512 chunks are requested here, ahead
+    // of every other load (clamped addresses, masked values).
+    const int lane0 = tid & 63, cown = c0 + lane0;
+    const bool own = lane0 < PJ_CPW && cown < n_chunks;
+    uint32_t cs_v[8], cs_sz = 0;
+    if (csum && wave == 0) {
+        cs_sz = csum[own ? cown : 0];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int i = 64 * j + lane0;
+            cs_v[j] = csum[i < c0 ? i : 0];
+        }
+    }
 
     constexpr int PJ_XD = pj_xd<F32>(), PJ_MD = PJ_XD + 1;
     // ---- layout rows of the first PJ_MD tiles and the basis, all requested at once
@@ -303,6 +321,42 @@ __device__ __forceinline__ void project_body(
         for (int i = 0; i < 4; ++i) { v[i] = __uint_as_float(p0[e][i]); v[4 + i] = __uint_as_float(p1[e][i]); }
         split8(v, frag_hi[tid + e * PJ_THREADS], frag_lo[tid + e * PJ_THREADS]);
     }
+    if (wave == 0) {
+        if (csum) {
+            // every earlier chunk's size summed, the group's own scanned across lanes; the
+            // workgroups of head 0's K half write the table
+            uint32_t pre = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) pre += 64 * j + lane0 < c0 ? cs_v[j] : 0u;
+            for (int i0 = 8 * 64; i0 < c0; i0 += 8 * 64) {
+                uint32_t v[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int i = i0 + 64 * j + lane0;
+                    v[j] = csum[i < c0 ? i : 0];
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) pre += i0 + 64 * j + lane0 < c0 ? v[j] : 0u;
+            }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) pre += __shfl_xor(pre, off, 64);
+            const uint32_t sz = own ? cs_sz : 0u;
+            uint32_t incl = sz;
+#pragma unroll
+            for (int off = 1; off < PJ_CPW; off <<= 1) {
+                const uint32_t y = __shfl_up(incl, off, 64);
+                if (lane0 >= off) incl += y;
+            }
+            const uint32_t base = pre + incl - sz;
+            if (lane0 < PJ_CPW) cbase[lane0] = base;
+            if (blockIdx.y == 0 && blockIdx.z == 0 && own) {
+                chunk_off[cown] = base;
+                if (cown == n_chunks - 1) chunk_off[n_chunks] = base + sz;
+            }
+        } else if (lane0 < PJ_CPW) {
+            cbase[lane0] = own ? chunk_off[cown] : 0u;
+        }
+    }
     __syncthreads();
 
     // ---- tile loop (fully unrolled: every load count is fixed).  The top of tile k waits for
@@ -316,7 +370,7 @@ __device__ __forceinline__ void project_body(
         if (k > 0) pj_store<F32>(o, is_v, coef);                         // tile k - 1, late
         if (k + PJ_MD < PJ_ITERS) m[k + PJ_MD] = pj_load_meta(k + PJ_MD, wave, c0, n_chunks, N, srank, sidx);
         if (k + PJ_XD < PJ_ITERS) pj_load_x<F32>(x[k + PJ_XD], X, m[k + PJ_XD].tok, N, G, g);
-        pj_compute<F32>(o, m[k], x[k], k, wave, c0, n_chunks, N, is_v, chunk_off, coef_stride,
+        pj_compute<F32>(o, m[k], x[k], k, wave, c0, n_chunks, N, is_v, cbase, coef_stride,
                         frag_hi, frag_lo);
     }
     pj_store<F32>(o, is_v, coef);
@@ -342,20 +396,20 @@ template <bool F32>
 __global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
     const void* __restrict__ K, const void* __restrict__ V, const float* __restrict__ PK,
     const float* __restrict__ PV, int64_t N, int G, int w, const uint8_t* __restrict__ srank,
-    const uint32_t* __restrict__ sidx, const uint32_t* __restrict__ chunk_off, int n_chunks,
-    void* __restrict__ coef_k, void* __restrict__ coef_v, int64_t coef_stride,
+    const uint32_t* __restrict__ sidx, const uint32_t* __restrict__ csum, uint32_t* __restrict__ chunk_off,
+    int n_chunks, void* __restrict__ coef_k, void* __restrict__ coef_v, int64_t coef_stride,
     void* __restrict__ k_exact, void* __restrict__ v_exact, int64_t cap) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     if (blockIdx.z == 0)
-        project_body<F32, false>(K, V, PK, PV, N, G, w, srank, sidx, chunk_off, n_chunks, coef_k, coef_v,
+        project_body<F32, false>(K, V, PK, PV, N, G, w, srank, sidx, csum, chunk_off, n_chunks, coef_k, coef_v,
                                  coef_stride, k_exact, v_exact, cap, smem);
     else
-        project_body<F32, true>(K, V, PK, PV, N, G, w, srank, sidx, chunk_off, n_chunks, coef_k, coef_v,
+        project_body<F32, true>(K, V, PK, PV, N, G, w, srank, sidx, csum, chunk_off, n_chunks, coef_k, coef_v,
                                 coef_stride, k_exact, v_exact, cap, smem);
 }
 
 hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V, const float* PK,
-                          const float* PV, varrate_cache& c, hipStream_t st) {
+                          const float* PV, varrate_cache& c, hipStream_t st, const uint32_t* chunk_sizes) {
     const int64_t N = sh.n - sh.w;
     const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
     dim3 grid((n_chunks + PJ_CPW - 1) / PJ_CPW, sh.G, 2);
@@ -364,13 +418,13 @@ hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V,
         hipError_t e = ensure_lds_limit((const void*)project_kernel<false>, lds);
         if (e != hipSuccess) return e;
         project_kernel<false><<<grid, PJ_THREADS, lds, st>>>(
-            K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
+            K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, chunk_sizes, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
             c.coef_stride, c.k_exact, c.v_exact, c.cap);
     } else {
         hipError_t e = ensure_lds_limit((const void*)project_kernel<true>, lds);
         if (e != hipSuccess) return e;
         project_kernel<true><<<grid, PJ_THREADS, lds, st>>>(
-            K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
+            K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, chunk_sizes, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
             c.coef_stride, c.k_exact, c.v_exact, c.cap);
     }
     return hipGetLastError();

@@ -91,11 +91,18 @@ hipError_t launch_salience(const varrate_shape& sh, const void* K, const void* Q
                            uint8_t* ws, hipStream_t st, bool pool = true);
 const float* salience_part(const varrate_shape& sh, const uint8_t* ws);
 float salience_pool_scale(const varrate_shape& sh);
-// s_part non-NULL: the first pass pools sbar from the column sums (and writes it) itself
+// s_part non-NULL: the first pass pools sbar from the column sums (and writes it) itself.
+// chunk_sizes NULL: the chunk table c.chunk_off is scanned before return (the allocation entry
+// point); non-NULL: it receives the workspace array of unscanned chunk sizes and c.chunk_off is
+// left to the projection, which must then be given that array (compress path: one launch fewer)
 hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_cache& c,
-                           uint8_t* ws, hipStream_t st, const float* s_part = nullptr);
+                           uint8_t* ws, hipStream_t st, const float* s_part = nullptr,
+                           const uint32_t** chunk_sizes = nullptr);
+// chunk_sizes non-NULL: the chunk offsets are scanned from these sizes and written to
+// c.chunk_off by the projection itself
 hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V, const float* PK,
-                          const float* PV, varrate_cache& c, hipStream_t st);
+                          const float* PV, varrate_cache& c, hipStream_t st,
+                          const uint32_t* chunk_sizes = nullptr);
 // reuse_group_region: every launch group (DC_SEQ sequences) writes its partial records to the
 // start of `ws` instead of a region of its own (the no-allocation entry point)
 // qcaches non-NULL: the coefficients are the quantised codes of qcaches[s] (same bits)

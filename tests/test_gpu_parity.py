@@ -208,6 +208,11 @@ def sbar_cases(N, oracle_sbar):
         "oracle": oracle_sbar,
         "constant": np.full(N, 0.37, np.float32),
         "ties": rng.integers(0, 4, N).astype(np.float32) / 7,
+        # about N/24 and N/160 tokens per weight: the threshold's digit bucket then holds
+        # several hundred to a few thousand candidates (the LDS narrowing, and the direct
+        # ranking with one slice per candidate)
+        "ties24": rng.integers(0, 24, N).astype(np.float32) / 23,
+        "ties160": rng.integers(0, 160, N).astype(np.float32) / 159,
         "one_hot": np.where(np.arange(N) == N // 3, 1.0, 0.0).astype(np.float32),
         "random": rng.random(N).astype(np.float32),
         "spiky": (rng.random(N) ** 12).astype(np.float32),
