@@ -18,9 +18,10 @@
 // most-significant-digit radix select (11-bit digits, common-prefix skipping) over the
 // 2 x 64-bit key.  All arithmetic is integer: the ranks are bit-exact and deterministic.
 //
-// Kernel chain.  Every pass over the tokens is a grid of 256-thread workgroups holding 1024
-// consecutive tokens each (wave w: the 256 tokens of one storage chunk, four coalesced loads
-// per lane).  The small scans and searches between passes (4097 coarse bins, 4096 fine bins,
+// Kernel chain.  Every pass over the tokens is a grid of workgroups holding 1024 consecutive
+// tokens each: 256 threads (wave w: the 256 tokens of one storage chunk, four coalesced loads
+// per lane), or 1024 threads, one token each, in the passes that scan histograms (weights,
+// fine, floors).  The small scans and searches between passes (4097 coarse bins, 4096 fine bins,
 // 2048 digit bins, the threshold among the candidates) are repeated by every workgroup of the
 // pass that needs them, which costs less than a launch of their own; workgroup 0 records the
 // results for the later kernels.
@@ -50,6 +51,7 @@ constexpr int SEL_CAP = 2048;              // candidates the selection finishes 
 constexpr uint64_t CAPPED = 1ull << 63;
 constexpr int NRV = D + 1;                 // rank values 0..128
 static_assert(AK_PER * 64 == CHUNK, "a wave holds one storage chunk");
+static_assert(NFB % (4 * AK_T) == 0 && NDB % (4 * AK_T) == 0, "whole 16-byte staging loads per thread");
 
 // Device-side state of one allocation (in the workspace, cleared by al_minmax).
 struct AlCtl {
@@ -69,11 +71,14 @@ struct AlCtl {
     int done, any;
 };
 
-// Workspace: [coarse low sums (u64) | coarse counts | fine counts | digit counts | ctl]
-// (the cleared region), then partial min/max, u, phi, candidates.
+// Workspace: [coarse histogram | fine counts | digit counts | ctl] (the cleared region), then
+// partial min/max, u, phi, candidates, chunk sizes.  A coarse bin packs its count (bits 40..63)
+// and the sum of its tokens' low 12 bits (bits 0..39: at most 2^20 x 4095 < 2^40), so one
+// 64-bit atomic adds both.
+constexpr int CP_SHIFT = 40;
+constexpr unsigned long long CP_LOW = (1ull << CP_SHIFT) - 1;
 struct AlWs {
-    unsigned long long* c_low;
-    uint32_t* c_cnt;
+    unsigned long long* c_pack;
     uint32_t* f_cnt;
     uint32_t* d_cnt;
     AlCtl* ctl;
@@ -92,8 +97,7 @@ static AlWs al_ws(uint8_t* ws, int64_t N) {
     const int64_t nwg = (N + AK_TOK - 1) / AK_TOK;
     uint8_t* p = ws;
     w.clear = (uint32_t*)p;
-    w.c_low = (unsigned long long*)p; p += NCB_PAD * 8;
-    w.c_cnt = (uint32_t*)p;           p += NCB_PAD * 4;
+    w.c_pack = (unsigned long long*)p; p += NCB_PAD * 8;
     w.f_cnt = (uint32_t*)p;           p += NFB * 4;
     w.d_cnt = (uint32_t*)p;           p += NDB * 4;
     w.ctl = (AlCtl*)p;                p += (sizeof(AlCtl) + 15) & ~(size_t)15;
@@ -110,7 +114,7 @@ static AlWs al_ws(uint8_t* ws, int64_t N) {
 size_t allocate_ws_bytes(const varrate_shape& sh) {
     const int64_t N = sh.n - sh.w;
     const int64_t nwg = (N + AK_TOK - 1) / AK_TOK;
-    size_t b = align256(NCB_PAD * 12 + NFB * 4 + NDB * 4 + ((sizeof(AlCtl) + 15) & ~(size_t)15));
+    size_t b = align256(NCB_PAD * 8 + NFB * 4 + NDB * 4 + ((sizeof(AlCtl) + 15) & ~(size_t)15));
     b += align256((size_t)nwg * sizeof(float2)) + align256((size_t)N * 4) + align256((size_t)N * 8);
     const int64_t n_chunks = (N + CHUNK - 1) / CHUNK;
     return b + align256((size_t)N * 16) + align256((size_t)(n_chunks + 1) * 4);
@@ -234,7 +238,20 @@ __global__ __launch_bounds__(AK_T) void al_pool_minmax(const float* __restrict__
     const int c0 = blockIdx.x * per, c1 = c0 + per < clear_words ? c0 + per : clear_words;
     for (int i = c0 + threadIdx.x; i < c1; i += AK_T) clear[i] = 0;
     const int64_t t0 = (int64_t)blockIdx.x * AK_TOK;
-    for (int i = threadIdx.x; i < AK_TOK + 4; i += AK_T) sv[i] = pool_term(s_part, N, G, inv_wh, t0 - 2 + i);
+    // the column sums of every pooling term this thread forms, requested together
+    constexpr int SV_IT = (AK_TOK + 4 + AK_T - 1) / AK_T;
+    float part[SV_IT][POOL_MAXG];
+#pragma unroll
+    for (int it = 0; it < SV_IT; ++it) {
+        const int64_t k = t0 - 2 + threadIdx.x + it * AK_T;
+        pool_load(s_part, N, G, k >= 0 && k < N ? k : 0, part[it]);
+    }
+#pragma unroll
+    for (int it = 0; it < SV_IT; ++it) {
+        const int i = threadIdx.x + it * AK_T;
+        const int64_t k = t0 - 2 + i;
+        if (i < AK_TOK + 4) sv[i] = k >= 0 && k < N ? pool_sum(part[it], s_part, N, G, inv_wh, k) : 0.0;
+    }
     __syncthreads();
     float v[AK_PER];
 #pragma unroll
@@ -252,108 +269,112 @@ __global__ __launch_bounds__(AK_T) void al_pool_minmax(const float* __restrict__
     if (threadIdx.x == 0) mm[blockIdx.x] = make_float2(mn, mx);
 }
 
+// The histogram passes run 1024 threads, one token each (the same 1024 tokens per workgroup
+// as the other passes): their per-thread scans over the bins are then 4 to 5 bins long, with
+// four waves per SIMD to hide each other's latency.
+constexpr int AW_T = AK_TOK;
+__device__ __forceinline__ int64_t aw_tok() { return (int64_t)blockIdx.x * AK_TOK + threadIdx.x; }
+
 // Global min / max from the per-workgroup partials (exact, so any order gives the same).
+template <int NT>
 __device__ __forceinline__ float2 al_range(const float2* __restrict__ mm, int nwg, float* red) {
     float mn = INFINITY, mx = -INFINITY;
-    for (int i = threadIdx.x; i < nwg; i += AK_T) {
+    for (int i = threadIdx.x; i < nwg; i += NT) {
         const float2 p = mm[i];
         mn = fminf(mn, p.x);
         mx = fmaxf(mx, p.y);
     }
-    mn = block_reduce<AK_T>(mn, red, [](float a, float b) { return fminf(a, b); });
-    mx = block_reduce<AK_T>(mx, red, [](float a, float b) { return fmaxf(a, b); });
+    mn = block_reduce<NT>(mn, red, [](float a, float b) { return fminf(a, b); });
+    mx = block_reduce<NT>(mx, red, [](float a, float b) { return fmaxf(a, b); });
     return make_float2(mn, mx);
 }
 
 // ---- 2. weights and the coarse histogram ----------------------------------------------------
-__global__ __launch_bounds__(AK_T) void al_weights(const float* __restrict__ sbar, int64_t N,
+__global__ __launch_bounds__(AW_T) void al_weights(const float* __restrict__ sbar, int64_t N,
                                                    const float2* __restrict__ mm, int nwg,
                                                    uint32_t* __restrict__ u_ws,
-                                                   unsigned long long* __restrict__ c_low,
-                                                   uint32_t* __restrict__ c_cnt, AlCtl* __restrict__ ctl) {
+                                                   unsigned long long* __restrict__ c_pack,
+                                                   AlCtl* __restrict__ ctl) {
     __shared__ uint32_t cnt[NCB_PAD], low[NCB_PAD];
-    __shared__ float red[AK_T / 64];
-    __shared__ uint32_t redu[AK_T / 64];
-    float s[AK_PER];
-#pragma unroll
-    for (int k = 0; k < AK_PER; ++k) {
-        const int64_t t = al_tok(k);
-        s[k] = sbar[t < N ? t : N - 1];
-    }
-    for (int i = threadIdx.x; i < NCB_PAD; i += AK_T) { cnt[i] = 0; low[i] = 0; }
-    const float2 r = al_range(mm, nwg, red);     // (its barriers also order the clearing)
+    __shared__ float red[AW_T / 64];
+    __shared__ uint32_t redu[AW_T / 64];
+    const int64_t t = aw_tok();
+    const float s = sbar[t < N ? t : N - 1];
+    for (int i = threadIdx.x; i < NCB_PAD; i += AW_T) { cnt[i] = 0; low[i] = 0; }
+    const float2 r = al_range<AW_T>(mm, nwg, red);     // (its barriers also order the clearing)
     const bool flat = !(r.y > r.x);
     const double lo = (double)r.x, range = (double)r.y - lo;
     uint32_t umax = 0;
-#pragma unroll
-    for (int k = 0; k < AK_PER; ++k) {
-        const int64_t t = al_tok(k);
-        if (t < N) {
-            const uint32_t u = weight_of(s[k], flat, lo, range);
-            u_ws[t] = u;
-            umax = u > umax ? u : umax;
-            atomicAdd(&cnt[u >> CBITS], 1u);
-            atomicAdd(&low[u >> CBITS], u & ((1u << CBITS) - 1));
-        }
+    if (t < N) {
+        const uint32_t u = weight_of(s, flat, lo, range);
+        u_ws[t] = u;
+        umax = u;
+        atomicAdd(&cnt[u >> CBITS], 1u);
+        atomicAdd(&low[u >> CBITS], u & ((1u << CBITS) - 1));
     }
-    umax = block_reduce<AK_T>(umax, redu, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+    umax = block_reduce<AW_T>(umax, redu, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
     if (threadIdx.x == 0) atomicMax(&ctl->umax, umax);
-    for (int i = threadIdx.x; i < NCB; i += AK_T) {
+    for (int i = threadIdx.x; i < NCB; i += AW_T) {
         const uint32_t c = cnt[i];
-        if (c) {
-            atomicAdd(&c_cnt[i], c);
-            atomicAdd(&c_low[i], (unsigned long long)low[i]);
-        }
+        if (c) atomicAdd(&c_pack[i], ((unsigned long long)c << CP_SHIFT) | low[i]);
     }
 }
 
 // ---- 3. coarse level; fine histogram ----------------------------------------------------------
-// Thread i holds bins [CPT i, CPT i + CPT) of a scan in registers (one batch of loads).
-constexpr int CPT = (NCB + AK_T - 1) / AK_T;    // 17 coarse bins per thread
-constexpr int FPT = NFB / AK_T;                 // 16 fine bins per thread
+// Thread i holds bins [CPT i, CPT i + CPT) of a scan in registers.
+constexpr int CPT = (NCB + AW_T - 1) / AW_T;    // 5 coarse bins per thread
+constexpr int FPT = NFB / AW_T;                 // 4 fine bins per thread
+static_assert(FPT == 4, "one 16-byte load of fine counts per thread");
 
-__global__ __launch_bounds__(AK_T) void al_fine(int64_t N, int64_t B, int r_min, int R,
+__global__ __launch_bounds__(AW_T) void al_fine(int64_t N, int64_t B, int r_min, int R,
                                                 const uint32_t* __restrict__ u_ws,
-                                                const unsigned long long* __restrict__ c_low,
-                                                const uint32_t* __restrict__ c_cnt,
+                                                const unsigned long long* __restrict__ c_pack,
                                                 uint32_t* __restrict__ f_cnt, AlCtl* __restrict__ ctl) {
-    __shared__ uint32_t cnt[NFB];
-    __shared__ uint32_t wt32[AK_T / 64];
-    __shared__ unsigned long long wt64[AK_T / 64];
+    // the coarse histogram staged through LDS with coalesced loads, then the fine counts
+    __shared__ union {
+        unsigned long long bins[CPT * AW_T];
+        uint32_t cnt[NFB];
+    } sm;
+    uint32_t* cnt = sm.cnt;
+    __shared__ uint32_t wt32[AW_T / 64];
+    __shared__ unsigned long long wt64[AW_T / 64];
     __shared__ unsigned long long s_edge[2];
-    uint32_t u[AK_PER];
+    const int64_t t = aw_tok();
+    const uint32_t u = u_ws[t < N ? t : N - 1];
+    {
+        unsigned long long st[CPT];
 #pragma unroll
-    for (int k = 0; k < AK_PER; ++k) {
-        const int64_t t = al_tok(k);
-        u[k] = u_ws[t < N ? t : N - 1];
+        for (int j = 0; j < CPT; ++j) {
+            const int i = threadIdx.x + j * AW_T;
+            st[j] = c_pack[i < NCB ? i : NCB - 1];
+        }
+#pragma unroll
+        for (int j = 0; j < CPT; ++j) sm.bins[threadIdx.x + j * AW_T] = st[j];
     }
+    __syncthreads();
     const int b0 = CPT * threadIdx.x;
-    uint32_t c[CPT];
-    unsigned long long l[CPT];
-#pragma unroll
-    for (int j = 0; j < CPT; ++j) {
-        const int b = b0 + j < NCB ? b0 + j : NCB - 1;
-        c[j] = c_cnt[b];
-        l[j] = c_low[b];
-    }
-    for (int i = threadIdx.x; i < NFB; i += AK_T) cnt[i] = 0;
     const uint32_t umax = ctl->umax;
     const int nb = (int)(umax >> CBITS) + 1;
-    // bin sums and this thread's totals (bins >= nb are empty: u <= umax)
+    // bin sums and this thread's totals (bins >= nb are empty: u <= umax; bins past NCB too)
+    uint32_t c[CPT];
+    unsigned long long l[CPT];
     uint32_t lc = 0;
     unsigned long long ls = 0;
 #pragma unroll
     for (int j = 0; j < CPT; ++j) {
         const int b = b0 + j;
-        if (b >= nb) { c[j] = 0; l[j] = 0; }
-        l[j] += (unsigned long long)c[j] * ((uint64_t)b << CBITS);    // sum of u in bin b
+        const unsigned long long v = sm.bins[b];
+        c[j] = b < nb ? (uint32_t)(v >> CP_SHIFT) : 0u;
+        l[j] = b < nb ? (v & CP_LOW) + (unsigned long long)c[j] * ((uint64_t)b << CBITS) : 0ull;   // sum of u in bin b
         lc += c[j];
         ls += l[j];
     }
     uint32_t tc;
     unsigned long long ts;
-    uint32_t pc = block_exscan<AK_T, uint32_t>(lc, wt32, tc);
-    unsigned long long ps = block_exscan<AK_T, unsigned long long>(ls, wt64, ts);
+    uint32_t pc = block_exscan<AW_T, uint32_t>(lc, wt32, tc);
+    // (every thread has its bins in registers: the staging area becomes the fine counts)
+    for (int i = threadIdx.x; i < NFB; i += AW_T) cnt[i] = 0;
+    unsigned long long ps = block_exscan<AW_T, unsigned long long>(ls, wt64, ts);
     const uint64_t Dr = (uint64_t)(R - r_min);
     const uint64_t E = (uint64_t)(B - N * (int64_t)r_min);
     // the predicate at coarse edges tau_b = max(1, b << 12): c_ge = N - cnt_ex[b], s_lt = sm_ex[b]
@@ -371,7 +392,7 @@ __global__ __launch_bounds__(AK_T) void al_fine(int64_t N, int64_t B, int r_min,
             rs += l[j];
         }
     }
-    bbest = (int)block_reduce<AK_T, uint32_t>((uint32_t)bbest, wt32,
+    bbest = (int)block_reduce<AW_T, uint32_t>((uint32_t)bbest, wt32,
                                               [](uint32_t a, uint32_t b) { return a > b ? a : b; });
     {
         uint32_t rc = pc;
@@ -393,11 +414,9 @@ __global__ __launch_bounds__(AK_T) void al_fine(int64_t N, int64_t B, int r_min,
         ctl->slt_b = s_edge[1];
     }
     // fine counts of the low 12 bits inside bin bbest (every u there is (bbest << 12) + f)
-#pragma unroll
-    for (int k = 0; k < AK_PER; ++k)
-        if (al_tok(k) < N && (int)(u[k] >> CBITS) == bbest) atomicAdd(&cnt[u[k] & (NFB - 1)], 1u);
+    if (t < N && (int)(u >> CBITS) == bbest) atomicAdd(&cnt[u & (NFB - 1)], 1u);
     __syncthreads();
-    for (int i = threadIdx.x; i < NFB; i += AK_T) {
+    for (int i = threadIdx.x; i < NFB; i += AW_T) {
         const uint32_t cc = cnt[i];
         if (cc) atomicAdd(&f_cnt[i], cc);
     }
@@ -406,29 +425,24 @@ __global__ __launch_bounds__(AK_T) void al_fine(int64_t N, int64_t B, int r_min,
 // ---- 4. fine level; floors, keys and the first selection digit --------------------------------
 // RT: the rank type, uint8_t (per-head codec, R = 128) or uint16_t (shared basis, R <= 1024)
 template <typename RT>
-__global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_min, int R,
+__global__ __launch_bounds__(AW_T) void al_floors(int64_t N, int64_t B, int r_min, int R,
                                                   const uint32_t* __restrict__ u_ws,
                                                   const uint32_t* __restrict__ f_cnt,
                                                   RT* __restrict__ rank, uint64_t* __restrict__ phi_ws,
                                                   uint32_t* __restrict__ d_cnt, AlCtl* __restrict__ ctl) {
     __shared__ uint32_t cnt[NDB];
-    __shared__ uint32_t wt32[AK_T / 64];
-    __shared__ unsigned long long wt64[AK_T / 64];
+    __shared__ uint32_t wt32[AW_T / 64];
+    __shared__ unsigned long long wt64[AW_T / 64];
     __shared__ unsigned long long s_edge[2];
-    uint32_t u[AK_PER];
-#pragma unroll
-    for (int k = 0; k < AK_PER; ++k) {
-        const int64_t t = al_tok(k);
-        u[k] = u_ws[t < N ? t : N - 1];
-    }
+    const int64_t t = aw_tok();
+    const uint32_t u = u_ws[t < N ? t : N - 1];
     const int f0 = FPT * threadIdx.x;
     uint32_t c[FPT];
-#pragma unroll
-    for (int j = 0; j < FPT; j += 4) {
-        const uint4 v = *reinterpret_cast<const uint4*>(f_cnt + f0 + j);
-        c[j] = v.x; c[j + 1] = v.y; c[j + 2] = v.z; c[j + 3] = v.w;
+    {
+        const uint4 v = reinterpret_cast<const uint4*>(f_cnt)[threadIdx.x];
+        c[0] = v.x; c[1] = v.y; c[2] = v.z; c[3] = v.w;
     }
-    for (int i = threadIdx.x; i < NDB; i += AK_T) cnt[i] = 0;
+    for (int i = threadIdx.x; i < NDB; i += AW_T) cnt[i] = 0;
     const uint32_t umax = ctl->umax;
     const int bbest = ctl->bbest;
     const uint64_t cge_next = ctl->cge_next, slt_b = ctl->slt_b;
@@ -442,8 +456,8 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
     }
     uint32_t tc;
     unsigned long long ts;
-    const uint32_t pc = block_exscan<AK_T, uint32_t>(lc, wt32, tc);
-    const unsigned long long ps = block_exscan<AK_T, unsigned long long>(ls, wt64, ts);
+    const uint32_t pc = block_exscan<AW_T, uint32_t>(lc, wt32, tc);
+    const unsigned long long ps = block_exscan<AW_T, unsigned long long>(ls, wt64, ts);
     const uint64_t Dr = (uint64_t)(R - r_min);
     const uint64_t E = (uint64_t)(B - N * (int64_t)r_min);
     const uint64_t fc_total = tc;
@@ -464,7 +478,7 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
             rs += (unsigned long long)c[j] * (base_tau + (uint64_t)f);
         }
     }
-    fbest = (int)block_reduce<AK_T, uint32_t>((uint32_t)fbest, wt32,
+    fbest = (int)block_reduce<AW_T, uint32_t>((uint32_t)fbest, wt32,
                                               [](uint32_t a, uint32_t b) { return a > b ? a : b; });
     {
         uint32_t rc = pc;
@@ -495,19 +509,16 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
     }
 
     unsigned long long fsum = 0;
-#pragma unroll
-    for (int k = 0; k < AK_PER; ++k) {
-        const int64_t t = al_tok(k);
-        if (t >= N) continue;
+    if (t < N) {
         uint32_t base;
         uint64_t phi;
-        if (u[k] > tau_lo) {
+        if (u > tau_lo) {
             base = (uint32_t)R;
             phi = CAPPED;
         } else {
             // num < 2^52 and Q < 2^45 are exact in fp64; the reciprocal quotient is within
             // one unit of floor(num / Q) and the integer remainder corrects it exactly
-            const uint64_t num = (uint64_t)u[k] * (uint64_t)M;
+            const uint64_t num = (uint64_t)u * (uint64_t)M;
             int64_t f = (int64_t)((double)num * invQ);
             int64_t rem = (int64_t)num - f * (int64_t)Q;
             if (rem < 0) { f -= 1; rem += (int64_t)Q; }
@@ -518,12 +529,12 @@ __global__ __launch_bounds__(AK_T) void al_floors(int64_t N, int64_t B, int r_mi
         }
         rank[t] = (RT)base;
         phi_ws[t] = phi;
-        fsum += base;
+        fsum = base;
     }
-    fsum = block_reduce<AK_T, unsigned long long>(fsum, wt64,
+    fsum = block_reduce<AW_T, unsigned long long>(fsum, wt64,
                                                   [](unsigned long long a, unsigned long long b) { return a + b; });
     if (threadIdx.x == 0) atomicAdd(&ctl->fsum, fsum);
-    for (int i = threadIdx.x; i < NDB; i += AK_T) {
+    for (int i = threadIdx.x; i < NDB; i += AW_T) {
         const uint32_t c = cnt[i];
         if (c) atomicAdd(&d_cnt[i], c);
     }
@@ -628,6 +639,7 @@ __global__ __launch_bounds__(AK_T) void al_gather(int64_t N, int64_t B, const ui
     __shared__ uint32_t wt32[AK_T / 64];
     __shared__ int s_hit;
     __shared__ uint32_t s_above, s_hcnt, s_n, s_base;
+    __shared__ uint4 sd[NDB / 4];                 // the digit counts (coalesced loads)
     uint64_t phi[AK_PER];
     uint32_t u[AK_PER];
 #pragma unroll
@@ -641,9 +653,19 @@ __global__ __launch_bounds__(AK_T) void al_gather(int64_t N, int64_t B, const ui
     if (threadIdx.x == 0) { s_hit = -1; s_n = 0; }
     // descending digit order: thread i holds digits 2047 - 8 i .. 2040 - 8 i
     constexpr int DPT = NDB / AK_T;
+    {
+        constexpr int DL = NDB / 4 / AK_T;
+        uint4 st[DL];
+#pragma unroll
+        for (int j = 0; j < DL; ++j) st[j] = reinterpret_cast<const uint4*>(d_cnt)[threadIdx.x + j * AK_T];
+#pragma unroll
+        for (int j = 0; j < DL; ++j) sd[threadIdx.x + j * AK_T] = st[j];
+    }
+    __syncthreads();
+    const uint32_t* sdc = reinterpret_cast<const uint32_t*>(sd);
     uint32_t c[DPT], loc = 0;
 #pragma unroll
-    for (int j = 0; j < DPT; ++j) { c[j] = d_cnt[NDB - 1 - DPT * threadIdx.x - j]; loc += c[j]; }
+    for (int j = 0; j < DPT; ++j) { c[j] = sdc[NDB - 1 - DPT * threadIdx.x - j]; loc += c[j]; }
     uint32_t tot;
     uint32_t above = block_exscan<AK_T, uint32_t>(loc, wt32, tot);
     if (rho > 0) {
@@ -985,9 +1007,9 @@ hipError_t launch_allocate(const varrate_shape& sh, const float* sbar, varrate_c
                                              w.mm, w.clear, w.clear_words);
     else
         al_minmax<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, w.clear, w.clear_words);
-    al_weights<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_low, w.c_cnt, w.ctl);
-    al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
-    al_floors<uint8_t><<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
+    al_weights<<<nwg, AW_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_pack, w.ctl);
+    al_fine<<<nwg, AW_T, 0, st>>>(N, B, r_min, R, w.u, w.c_pack, w.f_cnt, w.ctl);
+    al_floors<uint8_t><<<nwg, AW_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, c.rank, w.phi, w.d_cnt, w.ctl);
     al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
     al_final<uint8_t, true><<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, w.cand, c.rank, c.srank, c.sidx, w.csum, w.ctl);
     if (chunk_sizes)
@@ -1011,9 +1033,9 @@ hipError_t launch_allocate_joint(const varrate_shape& sh, int R, int64_t B, cons
                                              w.mm, w.clear, w.clear_words);
     else
         al_minmax<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, w.clear, w.clear_words);
-    al_weights<<<nwg, AK_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_low, w.c_cnt, w.ctl);
-    al_fine<<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.c_low, w.c_cnt, w.f_cnt, w.ctl);
-    al_floors<uint16_t><<<nwg, AK_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, rank, w.phi, w.d_cnt, w.ctl);
+    al_weights<<<nwg, AW_T, 0, st>>>(sbar, N, w.mm, nwg, w.u, w.c_pack, w.ctl);
+    al_fine<<<nwg, AW_T, 0, st>>>(N, B, r_min, R, w.u, w.c_pack, w.f_cnt, w.ctl);
+    al_floors<uint16_t><<<nwg, AW_T, 0, st>>>(N, B, r_min, R, w.u, w.f_cnt, rank, w.phi, w.d_cnt, w.ctl);
     al_gather<<<nwg, AK_T, 0, st>>>(N, B, w.u, w.phi, w.d_cnt, w.cand, w.ctl);
     al_final<uint16_t, false><<<nwg, AK_T, 0, st>>>(N, w.u, w.phi, w.cand, rank, nullptr, nullptr, w.csum, w.ctl);
     al_offsets<<<nwg, AK_T, 0, st>>>(N, rank, w.csum, chunk_off, offset, n_chunks);

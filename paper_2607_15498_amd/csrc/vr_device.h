@@ -145,18 +145,29 @@ __device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp
 // Used by the pooling kernel and by the compress path's fused pooling + range pass, so both
 // produce the same bits.
 constexpr int POOL_MAXG = 16;      // heads whose loads issue together
-__device__ __forceinline__ double pool_term(const float* __restrict__ s_part, int64_t N, int G,
-                                            float inv_wh, int64_t k) {
-    if (k < 0 || k >= N) return 0.0;
-    float part[POOL_MAXG];
+// the first POOL_MAXG heads' column sums of token k (0 <= k < N), loaded by the caller; the
+// loads are unconditional (heads past G read head 0, and the sum skips them) so that they all
+// issue before the first wait
+__device__ __forceinline__ void pool_load(const float* __restrict__ s_part, int64_t N, int G, int64_t k,
+                                          float (&part)[POOL_MAXG]) {
 #pragma unroll
-    for (int gg = 0; gg < POOL_MAXG; ++gg) part[gg] = gg < G ? s_part[(int64_t)gg * N + k] : 0.f;
+    for (int gg = 0; gg < POOL_MAXG; ++gg) part[gg] = s_part[(int64_t)(gg < G ? gg : 0) * N + k];
+}
+__device__ __forceinline__ double pool_sum(const float (&part)[POOL_MAXG], const float* __restrict__ s_part,
+                                           int64_t N, int G, float inv_wh, int64_t k) {
     float s = 0.f;
 #pragma unroll
     for (int gg = 0; gg < POOL_MAXG; ++gg)
         if (gg < G) s += part[gg];
     for (int gg = POOL_MAXG; gg < G; ++gg) s += s_part[(int64_t)gg * N + k];
     return (double)(s * inv_wh);
+}
+__device__ __forceinline__ double pool_term(const float* __restrict__ s_part, int64_t N, int G,
+                                            float inv_wh, int64_t k) {
+    if (k < 0 || k >= N) return 0.0;
+    float part[POOL_MAXG];
+    pool_load(s_part, N, G, k, part);
+    return pool_sum(part, s_part, N, G, inv_wh, k);
 }
 // sv[i - 2 .. i + 2] are the terms around the token
 __device__ __forceinline__ float pool5(const double* sv, int i) {
