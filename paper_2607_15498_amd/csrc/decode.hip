@@ -2471,8 +2471,10 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
         mp.n_wg = pl.n_wg;
         mp.rpu = rows_total < 16 ? rows_total : 16;
         mp.nrec = pl.nrec;
-        // units of more than 4 query rows: one workgroup per (unit, column block) for all rows
-        const bool by_rows = mp.rpu > 4;
+        // units of more than 8 query rows (batches of queries): one workgroup per (unit, column
+        // block) for all rows; up to 8 rows the per-row spread keeps more workgroups busy
+        // (Qwen's 7 rows per KV head: 0.80 against 1.07 ms per 28-layer step)
+        const bool by_rows = mp.rpu > 8;
         const unsigned nmerge = (unsigned)(ns * sh.G * pl.nqt * (by_rows ? 1 : mp.rpu) * MG_CB);
         {
             // XCD-aware order when the heads spread evenly over the 8 XCDs

@@ -330,19 +330,39 @@ __global__ __launch_bounds__(SL_THREADS, 4) void sal_colsum(const void* __restri
     // waits for the partials (counted over its own loads only) can only over-wait.
     sl_prime<F32>(lds, K, n, G, g, b0, b1);
     {
+        // partials past the first SL_MERGE_REG of this thread (many rows x many pass-1
+        // workgroups) come in batches of SL_MERGE_REG loads issued together, in the same
+        // order as the first batch, so the sums keep one fixed order
         float mm = -INFINITY;
 #pragma unroll
         for (int i = 0; i < SL_MERGE_REG; ++i) mm = fmaxf(mm, part[i].x);
-        for (int b = h + tpr * SL_MERGE_REG; b < nw1; b += tpr) mm = fmaxf(mm, st[b].x);
+        for (int b0 = h + tpr * SL_MERGE_REG; b0 < nw1; b0 += tpr * SL_MERGE_REG) {
+            float x[SL_MERGE_REG];
+#pragma unroll
+            for (int i = 0; i < SL_MERGE_REG; ++i) {
+                const int b = b0 + tpr * i;
+                x[i] = st[b < nw1 ? b : 0].x;
+            }
+#pragma unroll
+            for (int i = 0; i < SL_MERGE_REG; ++i)
+                if (b0 + tpr * i < nw1) mm = fmaxf(mm, x[i]);
+        }
         for (int off = 1; off < tpr; off <<= 1) mm = fmaxf(mm, shfl_xor_f(mm, off));
         float ll = 0.f;
         if (mm != -INFINITY) {
 #pragma unroll
             for (int i = 0; i < SL_MERGE_REG; ++i)
                 ll += part[i].x == -INFINITY ? 0.f : part[i].y * fast_exp(part[i].x - mm);
-            for (int b = h + tpr * SL_MERGE_REG; b < nw1; b += tpr) {
-                const float2 v = st[b];
-                ll += v.x == -INFINITY ? 0.f : v.y * fast_exp(v.x - mm);
+            for (int b0 = h + tpr * SL_MERGE_REG; b0 < nw1; b0 += tpr * SL_MERGE_REG) {
+                float2 v[SL_MERGE_REG];
+#pragma unroll
+                for (int i = 0; i < SL_MERGE_REG; ++i) {
+                    const int b = b0 + tpr * i;
+                    v[i] = st[b < nw1 ? b : 0];
+                }
+#pragma unroll
+                for (int i = 0; i < SL_MERGE_REG; ++i)
+                    if (b0 + tpr * i < nw1) ll += v[i].x == -INFINITY ? 0.f : v[i].y * fast_exp(v[i].x - mm);
             }
         }
         for (int off = 1; off < tpr; off <<= 1) ll += shfl_xor_f(ll, off);
