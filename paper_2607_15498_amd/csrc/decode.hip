@@ -1804,8 +1804,10 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_kernel(MergeParams p)
 }
 // The same merge for units with many query rows: one workgroup per (unit, block of 32 output
 // columns) takes every row of the unit, so the basis slab is read once per unit and column
-// block (into LDS) instead of once per row, and each record row is read by one thread.
-// Fixed-order sums throughout.
+// block (into LDS) instead of once per row, and each record row is read by one thread.  The
+// slab's loads and the records' go out in batches before their first use; the back-rotation
+// of the 16 x 128 rank-space rows by the 128 x 32 slab runs as fp32 MFMAs (16x16x4, two waves,
+// one 16-column tile each).  Fixed-order sums throughout.
 template <bool F32>
 __global__ __launch_bounds__(MG_THREADS) void decode_merge_rows_kernel(MergeParams p) {
     typedef typename Elem<F32>::T ET;
@@ -1841,46 +1843,134 @@ __global__ __launch_bounds__(MG_THREADS) void decode_merge_rows_kernel(MergePara
     const int nrec = p.nrec;
     const int nrc = p.n_wg + 1;                   // records 1 .. nrc - 1 are rank-space
     const float* recs = p.part + (int64_t)unit * nrec * DC_REC;
-    // 1. the basis slab rows j, columns 32 cb .. 32 cb + 31
+    // 1. the basis slab rows j, columns 32 cb .. 32 cb + 31 (every load before the first store)
     const float* PV = p.PV + (int64_t)g * D * D + MG_COLS * cb;
-    for (int i = tid; i < D * MG_COLS; i += MG_THREADS) slab[i / MG_COLS][i % MG_COLS] = PV[(int64_t)(i / MG_COLS) * D + i % MG_COLS];
-    // 2. per row: maximum over the records, weights, softmax denominator (thread r)
-    if (tid < rows) {
-        float M = -INFINITY;
-        for (int r = 0; r < nrec; ++r) M = fmaxf(M, recs[(int64_t)r * DC_REC + tid]);
-        float L = 0.f;
-        for (int r = 0; r < nrec; ++r) {
-            const float m = recs[(int64_t)r * DC_REC + tid];
-            const float w = m == -INFINITY ? 0.f : fast_exp(m - M);
-            wgt[tid][r] = w;
-            L += w * recs[(int64_t)r * DC_REC + 16 + tid];
+    {
+        constexpr int SPT = D * MG_COLS / MG_THREADS;
+        float sv[SPT];
+#pragma unroll
+        for (int e = 0; e < SPT; ++e) {
+            const int i = tid + e * MG_THREADS;
+            sv[e] = PV[(int64_t)(i / MG_COLS) * D + i % MG_COLS];
         }
-        Lr[tid] = L;
+#pragma unroll
+        for (int e = 0; e < SPT; ++e) {
+            const int i = tid + e * MG_THREADS;
+            slab[i / MG_COLS][i % MG_COLS] = sv[e];
+        }
+    }
+    // the first (up to) four coded records' rows for step 3, requested ahead of step 2
+    constexpr int EPT = 16 * D / MG_THREADS;
+    const int nb0 = nrc - 1 < 4 ? nrc - 1 : 4;
+    float x0[4][EPT];
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const int i = tid + e * MG_THREADS;
+            x0[k][e] = recs[(int64_t)(1 + (k < nb0 ? k : 0)) * DC_REC + 32 + i];
+        }
+    // 2. per row: maximum over the records, weights, softmax denominator.  Thread (group q =
+    //    tid / 16, row tid % 16) takes records q, q + 16, ..; the groups' maxima and sums are
+    //    combined in group order.
+    __shared__ float gmax[MG_THREADS / 16][16], gsum[MG_THREADS / 16][16];
+    {
+        const int row = tid & 15, q = tid >> 4;
+        constexpr int NG = MG_THREADS / 16;
+        float M = -INFINITY;
+        for (int r = q; r < nrec; r += NG) M = fmaxf(M, recs[(int64_t)r * DC_REC + row]);
+        gmax[q][row] = M;
+        __syncthreads();
+        M = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < NG; ++k) M = fmaxf(M, gmax[k][row]);
+        float L = 0.f;
+        for (int r = q; r < nrec; r += NG) {
+            const float m = recs[(int64_t)r * DC_REC + row];
+            const float w = m == -INFINITY ? 0.f : fast_exp(m - M);
+            wgt[row][r] = w;
+            L += w * recs[(int64_t)r * DC_REC + 16 + row];
+        }
+        gsum[q][row] = L;
+        __syncthreads();
+        if (tid < 16) {
+            float Ls = 0.f;
+#pragma unroll
+            for (int k = 0; k < NG; ++k) Ls += gsum[k][tid];
+            Lr[tid] = Ls;
+        }
     }
     __syncthreads();
-    // 3. rank-space sum of every row over the coded records, in record order
-    for (int i = tid; i < rows * D; i += MG_THREADS) {
-        const int row = i / D, j = i % D;
-        float a = 0.f;
-        for (int r = 1; r < nrc; ++r) a += wgt[row][r] * recs[(int64_t)r * DC_REC + 32 + row * D + j];
-        accR[row][j] = a;
+    // 3. rank-space sum of every row over the coded records, in record order: each thread's
+    //    elements (row i / D, coordinate i % D), four records' loads in flight at a time;
+    //    rows past `rows` are zero
+    {
+        float a[EPT];
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) a[e] = 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int e = 0; e < EPT; ++e) {
+                const int row = (tid + e * MG_THREADS) / D;
+                if (k < nb0 && row < rows) a[e] += wgt[row][1 + k] * x0[k][e];
+            }
+        int r = 1 + nb0;
+        for (; r + 4 <= nrc; r += 4) {
+            float x[4][EPT];
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int e = 0; e < EPT; ++e) {
+                    const int i = tid + e * MG_THREADS;
+                    x[k][e] = recs[(int64_t)(r + k) * DC_REC + 32 + i];
+                }
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int e = 0; e < EPT; ++e) {
+                    const int row = (tid + e * MG_THREADS) / D;
+                    if (row < rows) a[e] += wgt[row][r + k] * x[k][e];
+                }
+        }
+        for (; r < nrc; ++r) {
+#pragma unroll
+            for (int e = 0; e < EPT; ++e) {
+                const int i = tid + e * MG_THREADS, row = i / D;
+                if (row < rows) a[e] += wgt[row][r] * recs[(int64_t)r * DC_REC + 32 + i];
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < EPT; ++e) {
+            const int i = tid + e * MG_THREADS;
+            accR[i / D][i % D] = a[e];
+        }
     }
     __syncthreads();
-    // 4. back-rotation by the slab, the original-space records, division by the denominator
-    for (int i = tid; i < rows * MG_COLS; i += MG_THREADS) {
-        const int row = i / MG_COLS, c = i % MG_COLS;
-        float o = 0.f;
+    // 4. back-rotation by the slab (wave t: output columns 16 t .. 16 t + 15 of the block), the
+    //    original-space records, division by the denominator
+    const int wave = tid >> 6, lane = tid & 63;
+    if (wave < MG_COLS / 16) {
+        const int li = lane & 15, lk = lane >> 4;
+        f32x4 o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 8
-        for (int j = 0; j < D; ++j) o += accR[row][j] * slab[j][c];
-        float e = wgt[row][0] * recs[32 + row * D + MG_COLS * cb + c];
-        for (int r = nrc; r < nrec; ++r) e += wgt[row][r] * recs[(int64_t)r * DC_REC + 32 + row * D + MG_COLS * cb + c];
-        const float val = (o + e) / Lr[row];
-        const int qrow = 16 * qt + row;
-        const int query = qrow / p.hpg, hh = qrow % p.hpg;
-        ET* out = reinterpret_cast<ET*>(p.out) + (int64_t)sq * p.out_seq_stride;
-        const int64_t oi = ((int64_t)query * p.H + g * p.hpg + hh) * D + MG_COLS * cb + c;
-        if constexpr (F32) out[oi] = val;
-        else out[oi] = (uint16_t)f32_to_bf16(val);
+        for (int s = 0; s < D / 4; ++s)
+            o = __builtin_amdgcn_mfma_f32_16x16x4f32(accR[li][4 * s + lk], slab[4 * s + lk][16 * wave + li], o, 0, 0, 0);
+        const int c = 16 * wave + li;             // C lane: column li, rows 4 lk .. 4 lk + 3
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = 4 * lk + v;
+            if (row >= rows) continue;
+            float e = wgt[row][0] * recs[32 + row * D + MG_COLS * cb + c];
+            for (int r = nrc; r < nrec; ++r) e += wgt[row][r] * recs[(int64_t)r * DC_REC + 32 + row * D + MG_COLS * cb + c];
+            const float val = (o[v] + e) / Lr[row];
+            const int qrow = 16 * qt + row;
+            const int query = qrow / p.hpg, hh = qrow % p.hpg;
+            ET* out = reinterpret_cast<ET*>(p.out) + (int64_t)sq * p.out_seq_stride;
+            const int64_t oi = ((int64_t)query * p.H + g * p.hpg + hh) * D + MG_COLS * cb + c;
+            if constexpr (F32) out[oi] = val;
+            else out[oi] = (uint16_t)f32_to_bf16(val);
+        }
     }
 }
 
