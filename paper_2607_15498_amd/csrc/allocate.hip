@@ -780,16 +780,20 @@ __device__ void al_threshold(int64_t N, const uint64_t* __restrict__ cand, const
         }, s.sel, s.cnt, s.wt32, s.wt64);
     } else {
         __syncthreads();
+        // sixteen entries per thread in flight at a time (clamped addresses, masked entries)
         radix_narrow<AK_T>([&](auto f) {
-            for (int i0 = 0; i0 < nc; i0 += 4 * AK_T) {
-                uint64_t h[4], l[4];
+            constexpr int BT = 16;
+            for (int i0 = 0; i0 < nc; i0 += BT * AK_T) {
+                uint64_t h[BT], l[BT];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
+                for (int k = 0; k < BT; ++k) {
                     const int i = i0 + k * AK_T + tid;
-                    if (i < nc) { h[k] = cand[2 * i]; l[k] = cand[2 * i + 1]; }
+                    const int ii = i < nc ? i : 0;
+                    h[k] = cand[2 * ii];
+                    l[k] = cand[2 * ii + 1];
                 }
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
+                for (int k = 0; k < BT; ++k)
                     if (i0 + k * AK_T + tid < nc) f(h[k], l[k]);
             }
         }, s.sel, s.cnt, s.wt32, s.wt64);
