@@ -1,6 +1,7 @@
 // Basis projection + nested truncation + packing (Sec. 3.3 Eq. (6), Algorithm 1), gfx950.
 //
-// One workgroup per (group of PJ_CPW chunks, KV head g, K|V), one workgroup per CU.  The
+// One workgroup per (group of CPW chunks, KV head g, K|V), one workgroup per CU: CPW = 8, or
+// 4 or 2 when that leaves fewer than 256 workgroups (short contexts, few heads).  The
 // storage order of every chunk (srank, sidx: rank descending, index ascending) comes with
 // the ranks from the allocation.
 //   1. The basis P (fp32) is split into bf16 hi + lo parts once per workgroup and kept in
@@ -25,15 +26,14 @@ namespace vr {
 
 constexpr int PJ_THREADS = 512;                       // 8 waves
 constexpr int PJ_WAVES = PJ_THREADS / 64;
-constexpr int PJ_CPW = 8;                             // chunks per workgroup
+constexpr int PJ_CPW = 8;                             // chunks per workgroup (at most)
 constexpr int PJ_HT = 16;                             // tokens per tile
 constexpr int PJ_TPC = CHUNK / PJ_HT;                 // tiles per chunk
-constexpr int PJ_ITERS = PJ_CPW * PJ_TPC / PJ_WAVES;  // tiles per wave
 constexpr int PJ_FRAGS = 8 * 4;                       // (16-row block a, 32-col step s) pairs
 // token rows are requested XD tiles ahead (fp32 rows are twice as large: one tile less),
 // layout rows one tile further
 template <bool F32> __host__ __device__ constexpr int pj_xd() { return F32 ? 2 : 3; }
-static_assert(PJ_CPW * PJ_TPC % PJ_WAVES == 0, "whole tiles per wave");
+static_assert(2 * PJ_TPC % PJ_WAVES == 0, "whole tiles per wave for 2, 4 and 8 chunks per workgroup");
 
 constexpr size_t PJ_FRAG_BYTES = (size_t)PJ_FRAGS * 64 * 16 * 2;
 // the basis fragments (hi, lo), then the workgroup's chunk offsets
@@ -257,7 +257,7 @@ __device__ __forceinline__ void pj_store(const PjOut<F32>& o, bool is_v, void* _
     }
 }
 
-template <bool F32, bool IS_V>
+template <bool F32, bool IS_V, int CPW>
 __device__ __forceinline__ void project_body(
     const void* __restrict__ K, const void* __restrict__ V, const float* __restrict__ PK,
     const float* __restrict__ PV, int64_t N, int G, int w, const uint8_t* __restrict__ srank,
@@ -276,13 +276,14 @@ __device__ __forceinline__ void project_body(
     const float* P = (kv ? PV : PK) + (int64_t)g * D * D;
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int c0 = blockIdx.x * PJ_CPW;
+    constexpr int PJ_ITERS = CPW * PJ_TPC / PJ_WAVES;   // tiles per wave
+    const int c0 = blockIdx.x * CPW;
 
     // offsets of this workgroup's chunks (wave 0): read from the chunk table, or (csum given)
     // scanned from the chunk sizes.  The sizes of the first 512 chunks are requested here, ahead
     // of every other load (clamped addresses, masked values).
     const int lane0 = tid & 63, cown = c0 + lane0;
-    const bool own = lane0 < PJ_CPW && cown < n_chunks;
+    const bool own = lane0 < CPW && cown < n_chunks;
     uint32_t cs_v[8], cs_sz = 0;
     if (csum && wave == 0) {
         cs_sz = csum[own ? cown : 0];
@@ -343,17 +344,17 @@ __device__ __forceinline__ void project_body(
             const uint32_t sz = own ? cs_sz : 0u;
             uint32_t incl = sz;
 #pragma unroll
-            for (int off = 1; off < PJ_CPW; off <<= 1) {
+            for (int off = 1; off < CPW; off <<= 1) {
                 const uint32_t y = __shfl_up(incl, off, 64);
                 if (lane0 >= off) incl += y;
             }
             const uint32_t base = pre + incl - sz;
-            if (lane0 < PJ_CPW) cbase[lane0] = base;
+            if (lane0 < CPW) cbase[lane0] = base;
             if (blockIdx.y == 0 && blockIdx.z == 0 && own) {
                 chunk_off[cown] = base;
                 if (cown == n_chunks - 1) chunk_off[n_chunks] = base + sz;
             }
-        } else if (lane0 < PJ_CPW) {
+        } else if (lane0 < CPW) {
             cbase[lane0] = own ? chunk_off[cown] : 0u;
         }
     }
@@ -392,7 +393,7 @@ __device__ __forceinline__ void project_body(
 
 // K (blockIdx.z = 0) and V (blockIdx.z = 1) in one launch; their stores differ, so each
 // half runs its own instance of the body.
-template <bool F32>
+template <bool F32, int CPW>
 __global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
     const void* __restrict__ K, const void* __restrict__ V, const float* __restrict__ PK,
     const float* __restrict__ PV, int64_t N, int G, int w, const uint8_t* __restrict__ srank,
@@ -401,33 +402,45 @@ __global__ __launch_bounds__(PJ_THREADS, 1) void project_kernel(
     void* __restrict__ k_exact, void* __restrict__ v_exact, int64_t cap) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     if (blockIdx.z == 0)
-        project_body<F32, false>(K, V, PK, PV, N, G, w, srank, sidx, csum, chunk_off, n_chunks, coef_k, coef_v,
-                                 coef_stride, k_exact, v_exact, cap, smem);
+        project_body<F32, false, CPW>(K, V, PK, PV, N, G, w, srank, sidx, csum, chunk_off, n_chunks, coef_k,
+                                      coef_v, coef_stride, k_exact, v_exact, cap, smem);
     else
-        project_body<F32, true>(K, V, PK, PV, N, G, w, srank, sidx, csum, chunk_off, n_chunks, coef_k, coef_v,
-                                coef_stride, k_exact, v_exact, cap, smem);
+        project_body<F32, true, CPW>(K, V, PK, PV, N, G, w, srank, sidx, csum, chunk_off, n_chunks, coef_k,
+                                     coef_v, coef_stride, k_exact, v_exact, cap, smem);
+}
+
+template <bool F32, int CPW>
+static hipError_t project_launch(const varrate_shape& sh, const void* K, const void* V, const float* PK,
+                                 const float* PV, varrate_cache& c, hipStream_t st, const uint32_t* chunk_sizes,
+                                 int n_chunks) {
+    const int64_t N = sh.n - sh.w;
+    const size_t lds = project_smem_bytes();
+    hipError_t e = ensure_lds_limit((const void*)project_kernel<F32, CPW>, lds);
+    if (e != hipSuccess) return e;
+    dim3 grid((n_chunks + CPW - 1) / CPW, sh.G, 2);
+    project_kernel<F32, CPW><<<grid, PJ_THREADS, lds, st>>>(
+        K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, chunk_sizes, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
+        c.coef_stride, c.k_exact, c.v_exact, c.cap);
+    return hipGetLastError();
+}
+
+template <bool F32>
+static hipError_t project_launch_cpw(const varrate_shape& sh, const void* K, const void* V, const float* PK,
+                                     const float* PV, varrate_cache& c, hipStream_t st,
+                                     const uint32_t* chunk_sizes, int n_chunks) {
+    // the most chunks per workgroup that still gives every CU a workgroup
+    auto wgs = [&](int cpw) { return (int64_t)((n_chunks + cpw - 1) / cpw) * sh.G * 2; };
+    if (wgs(8) >= 256) return project_launch<F32, 8>(sh, K, V, PK, PV, c, st, chunk_sizes, n_chunks);
+    if (wgs(4) >= 256) return project_launch<F32, 4>(sh, K, V, PK, PV, c, st, chunk_sizes, n_chunks);
+    return project_launch<F32, 2>(sh, K, V, PK, PV, c, st, chunk_sizes, n_chunks);
 }
 
 hipError_t launch_project(const varrate_shape& sh, const void* K, const void* V, const float* PK,
                           const float* PV, varrate_cache& c, hipStream_t st, const uint32_t* chunk_sizes) {
     const int64_t N = sh.n - sh.w;
     const int n_chunks = (int)((N + CHUNK - 1) / CHUNK);
-    dim3 grid((n_chunks + PJ_CPW - 1) / PJ_CPW, sh.G, 2);
-    const size_t lds = project_smem_bytes();
-    if (sh.dtype == VARRATE_BF16) {
-        hipError_t e = ensure_lds_limit((const void*)project_kernel<false>, lds);
-        if (e != hipSuccess) return e;
-        project_kernel<false><<<grid, PJ_THREADS, lds, st>>>(
-            K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, chunk_sizes, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
-            c.coef_stride, c.k_exact, c.v_exact, c.cap);
-    } else {
-        hipError_t e = ensure_lds_limit((const void*)project_kernel<true>, lds);
-        if (e != hipSuccess) return e;
-        project_kernel<true><<<grid, PJ_THREADS, lds, st>>>(
-            K, V, PK, PV, N, sh.G, sh.w, c.srank, c.sidx, chunk_sizes, c.chunk_off, n_chunks, c.coef_k, c.coef_v,
-            c.coef_stride, c.k_exact, c.v_exact, c.cap);
-    }
-    return hipGetLastError();
+    return sh.dtype == VARRATE_BF16 ? project_launch_cpw<false>(sh, K, V, PK, PV, c, st, chunk_sizes, n_chunks)
+                                    : project_launch_cpw<true>(sh, K, V, PK, PV, c, st, chunk_sizes, n_chunks);
 }
 
 }  // namespace vr
