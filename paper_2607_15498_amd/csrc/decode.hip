@@ -1281,7 +1281,19 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     const int U = p.units;
     const int L = blockIdx.x;
-    const int unit = L % U, j = L / U;          // workgroup j of the unit
+    // workgroup j of the unit.  Workgroup L runs on XCD L mod 8: with a grid of a multiple of 8
+    // workgroups, XCD x takes the x-th eighth of the unit-major order, so a unit's workgroups,
+    // and the units of one KV head (the row tiles of a batch of queries, which stream the same
+    // coefficients), share one L2.  For one sequence of 8 KV heads this is unit = L mod 8.
+    int unit, j;
+    if ((gridDim.x & 7) == 0) {
+        const int Lp = (L & 7) * (int)(gridDim.x >> 3) + (L >> 3);
+        unit = Lp / p.wpu;
+        j = Lp % p.wpu;
+    } else {
+        unit = L % U;
+        j = L / U;
+    }
     const int sq = unit / (p.G * p.nqt), gq = unit % (p.G * p.nqt);
     const int g = gq / p.nqt, qt = gq % p.nqt;
     const DecSeq& S = p.seq[sq];
