@@ -234,6 +234,40 @@ __device__ __forceinline__ void acc_read(f32x4 (&acc)[8]) {
     asm volatile("s_nop 15\n\ts_nop 7\n\t" "v_accvgpr_read_b32 %0, a0\n\t" "v_accvgpr_read_b32 %1, a1\n\t" "v_accvgpr_read_b32 %2, a2\n\t" "v_accvgpr_read_b32 %3, a3\n\t" "v_accvgpr_read_b32 %4, a4\n\t" "v_accvgpr_read_b32 %5, a5\n\t" "v_accvgpr_read_b32 %6, a6\n\t" "v_accvgpr_read_b32 %7, a7\n\t" "v_accvgpr_read_b32 %8, a8\n\t" "v_accvgpr_read_b32 %9, a9\n\t" "v_accvgpr_read_b32 %10, a10\n\t" "v_accvgpr_read_b32 %11, a11\n\t" "v_accvgpr_read_b32 %12, a12\n\t" "v_accvgpr_read_b32 %13, a13\n\t" "v_accvgpr_read_b32 %14, a14\n\t" "v_accvgpr_read_b32 %15, a15\n\t" "v_accvgpr_read_b32 %16, a16\n\t" "v_accvgpr_read_b32 %17, a17\n\t" "v_accvgpr_read_b32 %18, a18\n\t" "v_accvgpr_read_b32 %19, a19\n\t" "v_accvgpr_read_b32 %20, a20\n\t" "v_accvgpr_read_b32 %21, a21\n\t" "v_accvgpr_read_b32 %22, a22\n\t" "v_accvgpr_read_b32 %23, a23\n\t" "v_accvgpr_read_b32 %24, a24\n\t" "v_accvgpr_read_b32 %25, a25\n\t" "v_accvgpr_read_b32 %26, a26\n\t" "v_accvgpr_read_b32 %27, a27\n\t" "v_accvgpr_read_b32 %28, a28\n\t" "v_accvgpr_read_b32 %29, a29\n\t" "v_accvgpr_read_b32 %30, a30\n\t" "v_accvgpr_read_b32 %31, a31\n\t" : "=v"(acc[0][0]), "=v"(acc[0][1]), "=v"(acc[0][2]), "=v"(acc[0][3]), "=v"(acc[1][0]), "=v"(acc[1][1]), "=v"(acc[1][2]), "=v"(acc[1][3]), "=v"(acc[2][0]), "=v"(acc[2][1]), "=v"(acc[2][2]), "=v"(acc[2][3]), "=v"(acc[3][0]), "=v"(acc[3][1]), "=v"(acc[3][2]), "=v"(acc[3][3]), "=v"(acc[4][0]), "=v"(acc[4][1]), "=v"(acc[4][2]), "=v"(acc[4][3]), "=v"(acc[5][0]), "=v"(acc[5][1]), "=v"(acc[5][2]), "=v"(acc[5][3]), "=v"(acc[6][0]), "=v"(acc[6][1]), "=v"(acc[6][2]), "=v"(acc[6][3]), "=v"(acc[7][0]), "=v"(acc[7][1]), "=v"(acc[7][2]), "=v"(acc[7][3]) :: ACC_AGPRS);
 }
 
+// The second set of accumulators (a32..a63), for a wave that serves two row tiles of query
+// rows at once: the same helpers on the other registers.
+#define ACC1_AGPRS "a32", "a33", "a34", "a35", "a36", "a37", "a38", "a39", "a40", "a41", "a42", "a43", "a44", "a45", "a46", "a47", "a48", "a49", "a50", "a51", "a52", "a53", "a54", "a55", "a56", "a57", "a58", "a59", "a60", "a61", "a62", "a63"
+__device__ __forceinline__ void acc1_zero() {
+    asm volatile("v_accvgpr_write_b32 a32, 0\n\t" "v_accvgpr_write_b32 a33, 0\n\t" "v_accvgpr_write_b32 a34, 0\n\t" "v_accvgpr_write_b32 a35, 0\n\t" "v_accvgpr_write_b32 a36, 0\n\t" "v_accvgpr_write_b32 a37, 0\n\t" "v_accvgpr_write_b32 a38, 0\n\t" "v_accvgpr_write_b32 a39, 0\n\t" "v_accvgpr_write_b32 a40, 0\n\t" "v_accvgpr_write_b32 a41, 0\n\t" "v_accvgpr_write_b32 a42, 0\n\t" "v_accvgpr_write_b32 a43, 0\n\t" "v_accvgpr_write_b32 a44, 0\n\t" "v_accvgpr_write_b32 a45, 0\n\t" "v_accvgpr_write_b32 a46, 0\n\t" "v_accvgpr_write_b32 a47, 0\n\t" "v_accvgpr_write_b32 a48, 0\n\t" "v_accvgpr_write_b32 a49, 0\n\t" "v_accvgpr_write_b32 a50, 0\n\t" "v_accvgpr_write_b32 a51, 0\n\t" "v_accvgpr_write_b32 a52, 0\n\t" "v_accvgpr_write_b32 a53, 0\n\t" "v_accvgpr_write_b32 a54, 0\n\t" "v_accvgpr_write_b32 a55, 0\n\t" "v_accvgpr_write_b32 a56, 0\n\t" "v_accvgpr_write_b32 a57, 0\n\t" "v_accvgpr_write_b32 a58, 0\n\t" "v_accvgpr_write_b32 a59, 0\n\t" "v_accvgpr_write_b32 a60, 0\n\t" "v_accvgpr_write_b32 a61, 0\n\t" "v_accvgpr_write_b32 a62, 0\n\t" "v_accvgpr_write_b32 a63, 0\n\t" "s_nop 4\n\t" ::: ACC1_AGPRS);
+}
+template <int NB> __device__ __forceinline__ void acc1_mfma_bf16(const u32x2* vh, u32x2 ph);
+template <> __device__ __forceinline__ void acc1_mfma_bf16<1>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[32:35], %0, %1, a[32:35]\n\t" :: "v"(vh[0]), "v"(ph) : ACC1_AGPRS);
+}
+template <> __device__ __forceinline__ void acc1_mfma_bf16<2>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[32:35], %0, %2, a[32:35]\n\t" "v_mfma_f32_16x16x16_bf16 a[36:39], %1, %2, a[36:39]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(ph) : ACC1_AGPRS);
+}
+template <> __device__ __forceinline__ void acc1_mfma_bf16<4>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[32:35], %0, %4, a[32:35]\n\t" "v_mfma_f32_16x16x16_bf16 a[36:39], %1, %4, a[36:39]\n\t" "v_mfma_f32_16x16x16_bf16 a[40:43], %2, %4, a[40:43]\n\t" "v_mfma_f32_16x16x16_bf16 a[44:47], %3, %4, a[44:47]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(ph) : ACC1_AGPRS);
+}
+template <> __device__ __forceinline__ void acc1_mfma_bf16<8>(const u32x2* vh, u32x2 ph) {
+    asm volatile("s_nop 4\n\t" "v_mfma_f32_16x16x16_bf16 a[32:35], %0, %8, a[32:35]\n\t" "v_mfma_f32_16x16x16_bf16 a[36:39], %1, %8, a[36:39]\n\t" "v_mfma_f32_16x16x16_bf16 a[40:43], %2, %8, a[40:43]\n\t" "v_mfma_f32_16x16x16_bf16 a[44:47], %3, %8, a[44:47]\n\t" "v_mfma_f32_16x16x16_bf16 a[48:51], %4, %8, a[48:51]\n\t" "v_mfma_f32_16x16x16_bf16 a[52:55], %5, %8, a[52:55]\n\t" "v_mfma_f32_16x16x16_bf16 a[56:59], %6, %8, a[56:59]\n\t" "v_mfma_f32_16x16x16_bf16 a[60:63], %7, %8, a[60:63]\n\t" :: "v"(vh[0]), "v"(vh[1]), "v"(vh[2]), "v"(vh[3]), "v"(vh[4]), "v"(vh[5]), "v"(vh[6]), "v"(vh[7]), "v"(ph) : ACC1_AGPRS);
+}
+__device__ __forceinline__ void acc1_scale(float alpha) {
+    float t0, t1, t2, t3;
+    asm volatile("s_nop 15\n\ts_nop 7\n\t" "v_accvgpr_read_b32 %0, a32\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a32, %0\n\t" "v_accvgpr_read_b32 %1, a33\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a33, %1\n\t" "v_accvgpr_read_b32 %2, a34\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a34, %2\n\t" "v_accvgpr_read_b32 %3, a35\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a35, %3\n\t" "v_accvgpr_read_b32 %0, a36\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a36, %0\n\t" "v_accvgpr_read_b32 %1, a37\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a37, %1\n\t" "v_accvgpr_read_b32 %2, a38\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a38, %2\n\t" "v_accvgpr_read_b32 %3, a39\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a39, %3\n\t" "v_accvgpr_read_b32 %0, a40\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a40, %0\n\t" "v_accvgpr_read_b32 %1, a41\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a41, %1\n\t" "v_accvgpr_read_b32 %2, a42\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a42, %2\n\t" "v_accvgpr_read_b32 %3, a43\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a43, %3\n\t" "v_accvgpr_read_b32 %0, a44\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a44, %0\n\t" "v_accvgpr_read_b32 %1, a45\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a45, %1\n\t" "v_accvgpr_read_b32 %2, a46\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a46, %2\n\t" "v_accvgpr_read_b32 %3, a47\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a47, %3\n\t" "v_accvgpr_read_b32 %0, a48\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a48, %0\n\t" "v_accvgpr_read_b32 %1, a49\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a49, %1\n\t" "v_accvgpr_read_b32 %2, a50\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a50, %2\n\t" "v_accvgpr_read_b32 %3, a51\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a51, %3\n\t" "v_accvgpr_read_b32 %0, a52\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a52, %0\n\t" "v_accvgpr_read_b32 %1, a53\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a53, %1\n\t" "v_accvgpr_read_b32 %2, a54\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a54, %2\n\t" "v_accvgpr_read_b32 %3, a55\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a55, %3\n\t" "v_accvgpr_read_b32 %0, a56\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a56, %0\n\t" "v_accvgpr_read_b32 %1, a57\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a57, %1\n\t" "v_accvgpr_read_b32 %2, a58\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a58, %2\n\t" "v_accvgpr_read_b32 %3, a59\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a59, %3\n\t" "v_accvgpr_read_b32 %0, a60\n\tv_mul_f32 %0, %0, %4\n\tv_accvgpr_write_b32 a60, %0\n\t" "v_accvgpr_read_b32 %1, a61\n\tv_mul_f32 %1, %1, %4\n\tv_accvgpr_write_b32 a61, %1\n\t" "v_accvgpr_read_b32 %2, a62\n\tv_mul_f32 %2, %2, %4\n\tv_accvgpr_write_b32 a62, %2\n\t" "v_accvgpr_read_b32 %3, a63\n\tv_mul_f32 %3, %3, %4\n\tv_accvgpr_write_b32 a63, %3\n\t" "s_nop 4\n\t" : "=&v"(t0), "=&v"(t1), "=&v"(t2), "=&v"(t3) : "v"(alpha) : ACC1_AGPRS);
+}
+__device__ __forceinline__ void acc1_read(f32x4 (&acc)[8]) {
+    asm volatile("s_nop 15\n\ts_nop 7\n\t" "v_accvgpr_read_b32 %0, a32\n\t" "v_accvgpr_read_b32 %1, a33\n\t" "v_accvgpr_read_b32 %2, a34\n\t" "v_accvgpr_read_b32 %3, a35\n\t" "v_accvgpr_read_b32 %4, a36\n\t" "v_accvgpr_read_b32 %5, a37\n\t" "v_accvgpr_read_b32 %6, a38\n\t" "v_accvgpr_read_b32 %7, a39\n\t" "v_accvgpr_read_b32 %8, a40\n\t" "v_accvgpr_read_b32 %9, a41\n\t" "v_accvgpr_read_b32 %10, a42\n\t" "v_accvgpr_read_b32 %11, a43\n\t" "v_accvgpr_read_b32 %12, a44\n\t" "v_accvgpr_read_b32 %13, a45\n\t" "v_accvgpr_read_b32 %14, a46\n\t" "v_accvgpr_read_b32 %15, a47\n\t" "v_accvgpr_read_b32 %16, a48\n\t" "v_accvgpr_read_b32 %17, a49\n\t" "v_accvgpr_read_b32 %18, a50\n\t" "v_accvgpr_read_b32 %19, a51\n\t" "v_accvgpr_read_b32 %20, a52\n\t" "v_accvgpr_read_b32 %21, a53\n\t" "v_accvgpr_read_b32 %22, a54\n\t" "v_accvgpr_read_b32 %23, a55\n\t" "v_accvgpr_read_b32 %24, a56\n\t" "v_accvgpr_read_b32 %25, a57\n\t" "v_accvgpr_read_b32 %26, a58\n\t" "v_accvgpr_read_b32 %27, a59\n\t" "v_accvgpr_read_b32 %28, a60\n\t" "v_accvgpr_read_b32 %29, a61\n\t" "v_accvgpr_read_b32 %30, a62\n\t" "v_accvgpr_read_b32 %31, a63\n\t" : "=v"(acc[0][0]), "=v"(acc[0][1]), "=v"(acc[0][2]), "=v"(acc[0][3]), "=v"(acc[1][0]), "=v"(acc[1][1]), "=v"(acc[1][2]), "=v"(acc[1][3]), "=v"(acc[2][0]), "=v"(acc[2][1]), "=v"(acc[2][2]), "=v"(acc[2][3]), "=v"(acc[3][0]), "=v"(acc[3][1]), "=v"(acc[3][2]), "=v"(acc[3][3]), "=v"(acc[4][0]), "=v"(acc[4][1]), "=v"(acc[4][2]), "=v"(acc[4][3]), "=v"(acc[5][0]), "=v"(acc[5][1]), "=v"(acc[5][2]), "=v"(acc[5][3]), "=v"(acc[6][0]), "=v"(acc[6][1]), "=v"(acc[6][2]), "=v"(acc[6][3]), "=v"(acc[7][0]), "=v"(acc[7][1]), "=v"(acc[7][2]), "=v"(acc[7][3]) :: ACC1_AGPRS);
+}
+// Accumulator set SET (0: a0..a31, 1: a32..a63).
+template <int SET> __device__ __forceinline__ void accs_zero() { if constexpr (SET == 0) acc_zero(); else acc1_zero(); }
+template <int SET, int NB> __device__ __forceinline__ void accs_mfma_bf16(const u32x2* vh, u32x2 ph) {
+    if constexpr (SET == 0) acc_mfma_bf16<NB>(vh, ph); else acc1_mfma_bf16<NB>(vh, ph);
+}
+template <int SET> __device__ __forceinline__ void accs_scale(float alpha) { if constexpr (SET == 0) acc_scale(alpha); else acc1_scale(alpha); }
+template <int SET> __device__ __forceinline__ void accs_read(f32x4 (&acc)[8]) { if constexpr (SET == 0) acc_read(acc); else acc1_read(acc); }
+
 // One 16-position tile in the stage (wave-uniform): its first position i0 inside the chunk
 // (or the exact rows), the chunk's valid positions T, the stage offset of its first element
 // and its size m (coded: the largest rank of the tile; exact rows: 128).
@@ -1107,21 +1141,21 @@ constexpr int DR_CUS = 256;                       // workgroups per launch: one 
 struct RingSmem {
     uint8_t* ring;    // [wave][K, V][DR_RS]; after the tiles: comb [wave][16][DC_CROW] f32
     float* comb;
-    u32x4* qf;        // [4 steps][hi, lo][64] rotated query fragments (coded tiles)
-    u32x4* qx;        // [4 steps][hi, lo][64] query fragments (exact rows)
+    u32x4* qf;        // [row tile][4 steps][hi, lo][64] rotated query fragments (coded tiles)
     u32x4* kmask;     // [9]
     float* cm;        // [8][16]
     float* cl;        // [8][16]
     float* mrow;      // [coded, exact][16]
     float* lrow;      // [coded, exact][16]
 };
+constexpr int DR_QF = 4 * 2 * 64;                 // u32x4 per row tile's fragments (8 KB)
+template <int RT>
 __device__ __forceinline__ RingSmem ring_carve(uint8_t* smem) {
     RingSmem s;
     uint8_t* b = smem;
     s.ring = b; b += (size_t)DR_WAVES * 2 * DR_RS;
     s.comb = reinterpret_cast<float*>(s.ring);
-    s.qf = reinterpret_cast<u32x4*>(b); b += 4 * 2 * 64 * 16;
-    s.qx = reinterpret_cast<u32x4*>(b); b += 4 * 2 * 64 * 16;
+    s.qf = reinterpret_cast<u32x4*>(b); b += (size_t)RT * DR_QF * 16;
     s.kmask = reinterpret_cast<u32x4*>(b); b += 9 * 16;
     float* f = reinterpret_cast<float*>(b);
     s.cm = f; f += DR_WAVES * 16;
@@ -1130,9 +1164,10 @@ __device__ __forceinline__ RingSmem ring_carve(uint8_t* smem) {
     s.lrow = f;
     return s;
 }
-constexpr size_t DR_SMEM = (size_t)DR_WAVES * 2 * DR_RS + 2 * 4 * 2 * 64 * 16 + 9 * 16 + (2 * DR_WAVES * 16 + 64) * 4;
+template <int RT>
+constexpr size_t dr_smem() { return (size_t)DR_WAVES * 2 * DR_RS + (size_t)RT * DR_QF * 16 + 9 * 16 + (2 * DR_WAVES * 16 + 64) * 4; }
 static_assert(DR_WAVES * 16 * DC_CROW * 4 <= DR_WAVES * 2 * DR_RS, "combine rows fit in the rings");
-static_assert(DR_SMEM <= 160 * 1024, "one workgroup per CU");
+static_assert(dr_smem<2>() <= 160 * 1024, "one workgroup per CU");
 
 // 8 consecutive bf16 at ring element a (any 2-byte alignment, a may run past the ring's
 // end): the dword indices are taken modulo the ring.
@@ -1154,7 +1189,7 @@ __device__ __forceinline__ u32x4 lds_row8_wrap(const uint32_t* w, int a) {
 // then, and on the wave's first tile (first: the sums and accumulators are still zero, so
 // nothing is rescaled).  Returns through sv the scores relative to the (possibly moved)
 // reference.
-template <int NV>
+template <int NV, int SET>
 __device__ __forceinline__ void ring_softmax_ref(float (&sv)[NV], bool& first, float& m_run, float& l_part) {
     float lmax = sv[0];
 #pragma unroll
@@ -1165,7 +1200,7 @@ __device__ __forceinline__ void ring_softmax_ref(float (&sv)[NV], bool& first, f
         if (!first) {
             const float alpha = __builtin_amdgcn_exp2f(-shift);
             l_part *= alpha;
-            acc_scale(alpha);
+            accs_scale<SET>(alpha);
         }
         m_run += shift;
 #pragma unroll
@@ -1174,14 +1209,36 @@ __device__ __forceinline__ void ring_softmax_ref(float (&sv)[NV], bool& first, f
     }
 }
 
+// Softmax and value product of one tile for row tile R of the wave (accumulator set R):
+// scores relative to the row tile's reference in sc.
+template <int R, int NB>
+__device__ __forceinline__ void ring_finish(f32x4 sc, const u32x2 (&vh)[NB], bool partial, int i0, int T, int grp,
+                                            bool& first, float& m_run, float& l_part) {
+    float sv[4] = {sc[0], sc[1], sc[2], sc[3]};
+    if (partial) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sv[v] = i0 + 4 * grp + v < T ? sv[v] : -INFINITY;
+    }
+    ring_softmax_ref<4, R>(sv, first, m_run, l_part);
+    float pv[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) pv[v] = __builtin_amdgcn_exp2f(sv[v]);
+    l_part += (pv[0] + pv[1]) + (pv[2] + pv[3]);
+    const u32x2 ph = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
+    accs_mfma_bf16<R, NB>(vh, ph);
+}
+
 // One tile from a wave's ring (bf16): the arithmetic of tile_step, with the tile at ring
-// element rb and the query fragments in registers.  Coded tiles: K rows m elements apart, V
-// coordinate-major; WRAP gathers modulo the ring.  Exact tiles: rows of 128 (never wrapped:
-// 4 KB tiles from a 4 KB-aligned start).
-template <bool EXACT, bool WRAP, int KS, int NB>
+// element rb and the query fragments in registers, for each of the wave's RT row tiles (the
+// K and V gathers are shared; each row tile has its own scores, softmax state and
+// accumulator set).  Coded tiles: K rows m elements apart, V coordinate-major; WRAP gathers
+// modulo the ring.  Exact tiles: rows of 128 (never wrapped: 4 KB tiles from a 4 KB-aligned
+// start).
+template <bool EXACT, bool WRAP, int KS, int NB, int RT>
 __device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool partial, const uint16_t* rK,
-                                          const uint16_t* rV, const u32x4 (&qfr)[4][2], const u32x4* kmask,
-                                          int col, int grp, bool& first, float& m_run, float& l_part) {
+                                          const uint16_t* rV, const u32x4 (&qfr)[RT][4][2], const u32x4* kmask,
+                                          int col, int grp, bool (&first)[RT], float (&m_run)[RT],
+                                          float (&l_part)[RT]) {
     u32x2 vh[NB];
     auto gather_v = [&]() {
 #pragma unroll
@@ -1208,7 +1265,9 @@ __device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool par
     };
     if constexpr (KS < 4) gather_v();
     const uint32_t* rK32 = reinterpret_cast<const uint32_t*>(rK);
-    f32x4 sc = {-m_run, -m_run, -m_run, -m_run};
+    f32x4 sc[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) sc[r] = f32x4{-m_run[r], -m_run[r], -m_run[r], -m_run[r]};
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
         if (KS >= 4 && s == 2) __builtin_amdgcn_sched_barrier(0);
@@ -1218,33 +1277,43 @@ __device__ __forceinline__ void ring_tile(int rb, int m, int i0, int T, bool par
         nv = nv < 0 ? 0 : (nv > 8 ? 8 : nv);
         const int a = rb + (int)__umul24((uint32_t)col, (uint32_t)mm) + c0;
         const u32x4 kh = (WRAP ? lds_row8_wrap(rK32, a) : lds_row8_bf16(rK32, a)) & kmask[nv];
-        sc = mfma(kh, qfr[s][0], sc);
-        sc = mfma(kh, qfr[s][1], sc);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            sc[r] = mfma(kh, qfr[r][s][0], sc[r]);
+            sc[r] = mfma(kh, qfr[r][s][1], sc[r]);
+        }
     }
     if constexpr (KS >= 4) {
         __builtin_amdgcn_sched_barrier(0);
         gather_v();
     }
-    float sv[4] = {sc[0], sc[1], sc[2], sc[3]};
-    if (partial) {
+    ring_finish<0, NB>(sc[0], vh, partial, i0, T, grp, first[0], m_run[0], l_part[0]);
+    if constexpr (RT == 2) ring_finish<1, NB>(sc[RT - 1], vh, partial, i0, T, grp, first[RT - 1], m_run[RT - 1], l_part[RT - 1]);
+}
+
+// Softmax and value products of a pair of small tiles for row tile R (accumulator set R).
+template <int R>
+__device__ __forceinline__ void ring_pair_finish(f32x4 sA, f32x4 sB, const u32x2 (&va)[2], const u32x2 (&vb)[2],
+                                                 bool& first, float& m_run, float& l_part) {
+    float sv[8] = {sA[0], sA[1], sA[2], sA[3], sB[0], sB[1], sB[2], sB[3]};
+    ring_softmax_ref<8, R>(sv, first, m_run, l_part);
+    float pv[8];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) sv[v] = i0 + 4 * grp + v < T ? sv[v] : -INFINITY;
-    }
-    ring_softmax_ref<4>(sv, first, m_run, l_part);
-    float pv[4];
-#pragma unroll
-    for (int v = 0; v < 4; ++v) pv[v] = __builtin_amdgcn_exp2f(sv[v]);
-    l_part += (pv[0] + pv[1]) + (pv[2] + pv[3]);
-    const u32x2 ph = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
-    acc_mfma_bf16<NB>(vh, ph);
+    for (int v = 0; v < 8; ++v) pv[v] = __builtin_amdgcn_exp2f(sv[v]);
+    l_part += ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
+    const u32x2 pha = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
+    const u32x2 phb = {cvt_bf16x2(pv[4], pv[5]), cvt_bf16x2(pv[6], pv[7])};
+    accs_mfma_bf16<R, 2>(va, pha);
+    accs_mfma_bf16<R, 2>(vb, phb);
 }
 
 // Two consecutive small tiles (sizes <= 32, neither wrapped nor ragged) in one step: their
 // gathers and MFMA chains interleave, and they share one reference test and the loop's
 // bookkeeping.
+template <int RT>
 __device__ __forceinline__ void ring_pair(int rbA, int mA, int rbB, int mB, const uint16_t* rK, const uint16_t* rV,
-                                          const u32x4 (&qfr)[4][2], const u32x4* kmask, int col, int grp,
-                                          bool& first, float& m_run, float& l_part) {
+                                          const u32x4 (&qfr)[RT][4][2], const u32x4* kmask, int col, int grp,
+                                          bool (&first)[RT], float (&m_run)[RT], float (&l_part)[RT]) {
     const uint32_t* rK32 = reinterpret_cast<const uint32_t*>(rK);
     u32x2 va[2], vb[2];
 #pragma unroll
@@ -1260,26 +1329,90 @@ __device__ __forceinline__ void ring_pair(int rbA, int mA, int rbB, int mB, cons
     nvB = nvB < 0 ? 0 : (nvB > 8 ? 8 : nvB);
     const u32x4 kA = lds_row8_bf16(rK32, rbA + (int)__umul24((uint32_t)col, (uint32_t)mA) + 8 * grp) & kmask[nvA];
     const u32x4 kB = lds_row8_bf16(rK32, rbB + (int)__umul24((uint32_t)col, (uint32_t)mB) + 8 * grp) & kmask[nvB];
-    const f32x4 minit = {-m_run, -m_run, -m_run, -m_run};
-    f32x4 sA = mfma(kA, qfr[0][0], minit);
-    f32x4 sB = mfma(kB, qfr[0][0], minit);
-    sA = mfma(kA, qfr[0][1], sA);
-    sB = mfma(kB, qfr[0][1], sB);
-    float sv[8] = {sA[0], sA[1], sA[2], sA[3], sB[0], sB[1], sB[2], sB[3]};
-    ring_softmax_ref<8>(sv, first, m_run, l_part);
-    float pv[8];
+    f32x4 sA[RT], sB[RT];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) pv[v] = __builtin_amdgcn_exp2f(sv[v]);
-    l_part += ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
-    const u32x2 pha = {cvt_bf16x2(pv[0], pv[1]), cvt_bf16x2(pv[2], pv[3])};
-    const u32x2 phb = {cvt_bf16x2(pv[4], pv[5]), cvt_bf16x2(pv[6], pv[7])};
-    acc_mfma_bf16<2>(va, pha);
-    acc_mfma_bf16<2>(vb, phb);
+    for (int r = 0; r < RT; ++r) {
+        const f32x4 minit = {-m_run[r], -m_run[r], -m_run[r], -m_run[r]};
+        sA[r] = mfma(kA, qfr[r][0][0], minit);
+        sB[r] = mfma(kB, qfr[r][0][0], minit);
+        sA[r] = mfma(kA, qfr[r][0][1], sA[r]);
+        sB[r] = mfma(kB, qfr[r][0][1], sB[r]);
+    }
+    ring_pair_finish<0>(sA[0], sB[0], va, vb, first[0], m_run[0], l_part[0]);
+    if constexpr (RT == 2) ring_pair_finish<1>(sA[RT - 1], sB[RT - 1], va, vb, first[RT - 1], m_run[RT - 1], l_part[RT - 1]);
 }
 
+// ---- 5. combine of row tile R (accumulator set R): the coded waves into record 1 + j, the
+//         exact waves into record 0, each in wave order (log2 units here; the records hold the
+//         maxima in natural-log units, as the merge reads them).  Lane (col, grp) holds query
+//         row col.  upair: the (sequence, KV head, row-tile group) unit of the workgroup.
+template <int R, int RT>
+__device__ __forceinline__ void combine_records(const DecParams& p, const RingSmem& sm, int upair, int nqp, int j,
+                                                bool lastwg, int nxw, bool xw, int wave, int lane, int tid,
+                                                int col, int grp, bool first, float m_run, float l_part) {
+    const int sq = upair / (p.G * nqp), gq = upair % (p.G * nqp);
+    const int g = gq / nqp, qt = RT * (gq % nqp) + R;
+    if (qt >= p.nqt) return;            // (the whole workgroup: a group's second row tile past the last)
+    const int unit = (sq * p.G + g) * p.nqt + qt;
+    const int rows = min(16, p.rows_total - 16 * qt);
+    const int nr4 = (rows + 3) & ~3;
+    if (first) m_run = -INFINITY;       // no tile: an empty partial
+    f32x4 acc[8];
+    accs_read<R>(acc);
+    const float lsum = xsum32(xsum16(l_part));
+    if (lane < 16) { sm.cm[wave * 16 + col] = m_run; sm.cl[wave * 16 + col] = lsum; }
+    __syncthreads();   // also: every wave is done with its ring, which comb reuses
+    const int wc = DR_WAVES - nxw;
+    if (tid < 32) {
+        const int r = tid & 15;
+        const int w_lo = tid >= 16 ? wc : 0, w_hi = tid >= 16 ? DR_WAVES : wc;
+        float M = -INFINITY;
+        for (int w = w_lo; w < w_hi; ++w) M = fmaxf(M, sm.cm[w * 16 + r]);
+        float Ls = 0.f;
+        for (int w = w_lo; w < w_hi; ++w) {
+            const float mw = sm.cm[w * 16 + r];
+            Ls += mw == -INFINITY ? 0.f : sm.cl[w * 16 + r] * __builtin_amdgcn_exp2f(mw - M);
+        }
+        sm.mrow[tid] = M;
+        sm.lrow[tid] = Ls;
+    }
+    __syncthreads();
+    {
+        const float mref = sm.mrow[(xw ? 16 : 0) + col];
+        const float fac = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mref);
+        if (col < nr4) {
+#pragma unroll
+            for (int b = 0; b < 8; ++b)
+                *reinterpret_cast<f32x4*>(&sm.comb[(wave * 16 + col) * DC_CROW + 16 * b + 4 * grp]) = acc[b] * fac;
+        }
+    }
+    __syncthreads();
+    float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
+    const int n4 = nr4 * D / 4;
+    for (int part = 0; part < (lastwg ? 2 : 1); ++part) {
+        float* rec = recs + (int64_t)(part ? 0 : 1 + j) * DC_REC;
+        const int w_lo = part ? wc : 0, w_hi = part ? DR_WAVES : wc;
+        for (int idx = tid; idx < n4; idx += DR_THREADS) {
+            const int ci = (idx >> 5) * DC_CROW + 4 * (idx & 31);   // row idx/32, float4 idx%32
+            f32x4 s = {0.f, 0.f, 0.f, 0.f};
+            for (int w = w_lo; w < w_hi; ++w) s += *reinterpret_cast<const f32x4*>(sm.comb + w * 16 * DC_CROW + ci);
+            reinterpret_cast<f32x4*>(rec + 32)[idx] = s;
+        }
+        if (tid < 16) {
+            rec[tid] = sm.mrow[16 * part + tid] * 0.6931471805599453f;   // ln 2: log2 -> natural units
+            rec[16 + tid] = sm.lrow[16 * part + tid];
+        }
+    }
+}
+
+// RT = 2: every wave serves two row tiles of the same (sequence, KV head) (a batch of query
+// rows): the ring, the K and V gathers and the loop's bookkeeping are shared, the scores,
+// softmax states, accumulator sets (a0..a31, a32..a63) and records are the row tiles' own.
+template <int RT>
 __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
-    const int U = p.units;
+    const int nqp = (p.nqt + RT - 1) / RT;       // groups of RT row tiles
+    const int U = p.units / p.nqt * nqp;          // (sequence, KV head, row-tile group) units
     const int L = blockIdx.x;
     // workgroup j of the unit.  Workgroup L runs on XCD L mod 8: with a grid of a multiple of 8
     // workgroups, XCD x takes the x-th eighth of the unit-major order, so a unit's workgroups,
@@ -1294,14 +1427,12 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
         unit = L % U;
         j = L / U;
     }
-    const int sq = unit / (p.G * p.nqt), gq = unit % (p.G * p.nqt);
-    const int g = gq / p.nqt, qt = gq % p.nqt;
+    const int sq = unit / (p.G * nqp), gq = unit % (p.G * nqp);
+    const int g = gq / nqp, qp = gq % nqp;
     const DecSeq& S = p.seq[sq];
-    const int rows = min(16, p.rows_total - 16 * qt);
-    const int nr4 = (rows + 3) & ~3;
     const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int lane = lane_now(), tid = 64 * wave + lane, grp = lane >> 4, col = lane & 15;
-    RingSmem sm = ring_carve(smem);
+    RingSmem sm = ring_carve<RT>(smem);
     const float qscale = 0.12751743082459868f;  // log2(e) / sqrt(128)
     const bool lastwg = j == p.wpu - 1;
     const int nxw = lastwg ? p.n_xw : 0;          // exact waves of this workgroup (its last ones)
@@ -1325,8 +1456,8 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
 
     // ---- 1. loads of the prologue, in this order: the first rank of every tile from the start
     //         of this wave's first chunk to its last tile and the chunk bases (coded waves; 16
-    //         loads), then the basis rows 16 wave .. 16 wave + 15 and the query rows (12 loads:
-    //         every wave rotates its 16 directions of q' for the whole workgroup).  They are
+    //         loads), then the basis rows 16 wave .. 16 wave + 15 and the query rows (8 + 4 RT
+    //         loads: every wave rotates its 16 directions of q' for the whole workgroup).  They are
     //         issued in asm and waited for by load count: the metadata once the basis is the only
     //         younger load, the basis once only the ring loads issued after it are younger.
     //         Every lane loads a valid address; values of lanes outside the range are dropped.
@@ -1343,23 +1474,36 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
     }
     const uint16_t* qsrc = reinterpret_cast<const uint16_t*>(S.q);
     const float* P = p.PK + (int64_t)g * D * D;
-    const int qrow_l = 16 * qt + col;
-    const bool q_ok = qrow_l < p.rows_total;
-    const int query_l = q_ok ? qrow_l / p.hpg : 0, hh_l = q_ok ? qrow_l % p.hpg : 0;
-    const uint16_t* qv = qsrc + ((int64_t)query_l * p.H + g * p.hpg + hh_l) * D;
-    u32x4 pa[4][2], qr[4];
+    bool q_ok[RT];
+    u32x4 pa[4][2], qr[RT][4];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        const int qrow_l = 16 * (RT * qp + r) + col;
+        q_ok[r] = qrow_l < p.rows_total;
+    }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
         const float* src = P + (16 * wave + col) * D + 32 * s + 8 * grp;
-        const uint16_t* qs = qv + 32 * s + 8 * grp;     // 2-byte aligned: gfx950 serves it whole
         asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(pa[s][0]) : "v"(src) : "memory");
         asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(pa[s][1]) : "v"(src + 4) : "memory");
-        asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(qr[s]) : "v"(qs) : "memory");
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            const int qrow_l = 16 * (RT * qp + r) + col;
+            const int query_l = q_ok[r] ? qrow_l / p.hpg : 0, hh_l = q_ok[r] ? qrow_l % p.hpg : 0;
+            // 2-byte aligned: gfx950 serves it whole
+            const uint16_t* qs = qsrc + ((int64_t)query_l * p.H + g * p.hpg + hh_l) * D + 32 * s + 8 * grp;
+            asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(qr[r][s]) : "v"(qs) : "memory");
+        }
     }
-    static_assert(DR_META == 8, "the wait below names every metadata register");
-    asm volatile("s_waitcnt vmcnt(12)" : "+v"(mr[0]), "+v"(mr[1]), "+v"(mr[2]), "+v"(mr[3]), "+v"(mr[4]), "+v"(mr[5]),
-                 "+v"(mr[6]), "+v"(mr[7]), "+v"(cbr[0]), "+v"(cbr[1]), "+v"(cbr[2]), "+v"(cbr[3]), "+v"(cbr[4]),
-                 "+v"(cbr[5]), "+v"(cbr[6]), "+v"(cbr[7]) :: "memory");
+    static_assert(DR_META == 8, "the waits below name every metadata register");
+    if constexpr (RT == 1)
+        asm volatile("s_waitcnt vmcnt(12)" : "+v"(mr[0]), "+v"(mr[1]), "+v"(mr[2]), "+v"(mr[3]), "+v"(mr[4]), "+v"(mr[5]),
+                     "+v"(mr[6]), "+v"(mr[7]), "+v"(cbr[0]), "+v"(cbr[1]), "+v"(cbr[2]), "+v"(cbr[3]), "+v"(cbr[4]),
+                     "+v"(cbr[5]), "+v"(cbr[6]), "+v"(cbr[7]) :: "memory");
+    else
+        asm volatile("s_waitcnt vmcnt(16)" : "+v"(mr[0]), "+v"(mr[1]), "+v"(mr[2]), "+v"(mr[3]), "+v"(mr[4]), "+v"(mr[5]),
+                     "+v"(mr[6]), "+v"(mr[7]), "+v"(cbr[0]), "+v"(cbr[1]), "+v"(cbr[2]), "+v"(cbr[3]), "+v"(cbr[4]),
+                     "+v"(cbr[5]), "+v"(cbr[6]), "+v"(cbr[7]) :: "memory");
 #pragma unroll
     for (int b = 0; b < DR_META; ++b) {
         const int tt = 16 * c0 + 64 * b + lane;
@@ -1440,15 +1584,20 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
         }
     }
     asm volatile("s_waitcnt vmcnt(16)" : "+v"(pa[0][0]), "+v"(pa[0][1]), "+v"(pa[1][0]), "+v"(pa[1][1]),
-                 "+v"(pa[2][0]), "+v"(pa[2][1]), "+v"(pa[3][0]), "+v"(pa[3][1]), "+v"(qr[0]), "+v"(qr[1]),
-                 "+v"(qr[2]), "+v"(qr[3]) :: "memory");
+                 "+v"(pa[2][0]), "+v"(pa[2][1]), "+v"(pa[3][0]), "+v"(pa[3][1]), "+v"(qr[0][0]), "+v"(qr[0][1]),
+                 "+v"(qr[0][2]), "+v"(qr[0][3]) :: "memory");
+    if constexpr (RT == 2)      // (already landed: the wait above covers every older load)
+        asm volatile("" : "+v"(qr[RT - 1][0]), "+v"(qr[RT - 1][1]), "+v"(qr[RT - 1][2]), "+v"(qr[RT - 1][3]) :: "memory");
 
     // ---- 3. while the ring fills: q' = P_K q log2(e) / sqrt(d) by MFMA (C lane -> query row
-    //         col, directions 16 wave + 4 grp + v) into the score fragments; the exact rows'
-    //         fragments of q itself; the V rings' zero pads and the K-row masks.  Then every wave
-    //         keeps its fragments in registers.
+    //         col, directions 16 wave + 4 grp + v) into the score fragments, for each row tile;
+    //         the V rings' zero pads and the K-row masks.  Then every coded wave keeps its
+    //         fragments in registers; the exact waves form theirs from q itself, which every
+    //         wave holds in the fragment layout.
     {
-        f32x4 c = {0, 0, 0, 0};
+        f32x4 c[RT];
+#pragma unroll
+        for (int r = 0; r < RT; ++r) c[r] = f32x4{0, 0, 0, 0};
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
             float a8[8];
@@ -1456,31 +1605,22 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
             for (int e = 0; e < 4; ++e) { a8[e] = __uint_as_float(pa[s][0][e]); a8[4 + e] = __uint_as_float(pa[s][1][e]); }
             u32x4 ah, al;
             split8(a8, ah, al);
-            const u32x4 qb = q_ok ? qr[s] : u32x4{0, 0, 0, 0};
-            c = mfma(ah, qb, c);
-            c = mfma(al, qb, c);
-        }
-        uint32_t h[4], l[4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) split_bf16(c[v] * qscale, h[v], l[v]);
-        uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf);
-        const int s = wave >> 1, gp = 2 * (wave & 1) + (grp >> 1), dw = 2 * (grp & 1);
-        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 0) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
-        *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 1) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
-    }
-    if (lastwg && wave == DR_WAVES - 1) {
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            float v8[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float val = (e & 1) ? bf_hi(qr[s][e >> 1]) : bf_lo(qr[s][e >> 1]);
-                v8[e] = q_ok ? val * qscale : 0.f;
+            for (int r = 0; r < RT; ++r) {
+                const u32x4 qb = q_ok[r] ? qr[r][s] : u32x4{0, 0, 0, 0};
+                c[r] = mfma(ah, qb, c[r]);
+                c[r] = mfma(al, qb, c[r]);
             }
-            u32x4 hh, ll;
-            split8(v8, hh, ll);
-            sm.qx[(s * 2) * 64 + lane] = hh;
-            sm.qx[(s * 2 + 1) * 64 + lane] = ll;
+        }
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            uint32_t h[4], l[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) split_bf16(c[r][v] * qscale, h[v], l[v]);
+            uint32_t* qf32 = reinterpret_cast<uint32_t*>(sm.qf + r * DR_QF);
+            const int s = wave >> 1, gp = 2 * (wave & 1) + (grp >> 1), dw = 2 * (grp & 1);
+            *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 0) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(h[0], h[1]), pack2(h[2], h[3])};
+            *reinterpret_cast<u32x2*>(qf32 + ((s * 2 + 1) * 64 + gp * 16 + col) * 4 + dw) = u32x2{pack2(l[0], l[1]), pack2(l[2], l[3])};
         }
     }
     if (lane < DR_PAD / 4) reinterpret_cast<uint32_t*>(rV + DR_RING)[lane] = 0u;
@@ -1492,14 +1632,29 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
         sm.kmask[nv] = mk;
     }
     __syncthreads();
-    u32x4 qfr[4][2];
-    {
-        const u32x4* src = xw ? sm.qx : sm.qf;
+    u32x4 qfr[RT][4][2];
+    if (!xw) {
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
-            qfr[s][0] = src[(s * 2) * 64 + lane];
-            qfr[s][1] = src[(s * 2 + 1) * 64 + lane];
-        }
+        for (int r = 0; r < RT; ++r)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                qfr[r][s][0] = sm.qf[r * DR_QF + (s * 2) * 64 + lane];
+                qfr[r][s][1] = sm.qf[r * DR_QF + (s * 2 + 1) * 64 + lane];
+            }
+    } else {
+        // the exact rows' fragments: q itself (lane: query row col, elements 32 s + 8 grp ..)
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                float v8[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float val = (e & 1) ? bf_hi(qr[r][s][e >> 1]) : bf_lo(qr[r][s][e >> 1]);
+                    v8[e] = q_ok[r] ? val * qscale : 0.f;
+                }
+                split8(v8, qfr[r][s][0], qfr[r][s][1]);
+            }
     }
     // allow n units (2 n loads) in flight, n rounded down to even: at most one unit more is
     // waited for than the tile needs (and the padding loads of a short range, which are younger
@@ -1526,9 +1681,12 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
     };
 
     // ---- 4. tiles
-    float m_run = 0.f, l_part = 0.f;    // the reference is set on the first tile
-    bool first = true;
-    acc_zero();
+    float m_run[RT], l_part[RT];        // the reference is set on the first tile
+    bool first[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) { m_run[r] = 0.f; l_part[r] = 0.f; first[r] = true; }
+    accs_zero<0>();
+    if constexpr (RT == 2) accs_zero<RT - 1>();
     const uint16_t* rK16 = reinterpret_cast<const uint16_t*>(rK);
     const uint16_t* rV16 = reinterpret_cast<const uint16_t*>(rV);
     if (xw) {
@@ -1536,8 +1694,8 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
             const uint32_t bs = 2u * 16u * D * (uint32_t)t - base;
             land(bs, 2u * 16u * D);
             const int rb = (int)((bs & (DR_RING - 1)) >> 1);
-            ring_tile<true, false, 4, 8>(rb, D, 16 * t, nexact, 16 * t + 16 > nexact, rK16, rV16, qfr, sm.kmask,
-                                         col, grp, first, m_run, l_part);
+            ring_tile<true, false, 4, 8, RT>(rb, D, 16 * t, nexact, 16 * t + 16 > nexact, rK16, rV16, qfr, sm.kmask,
+                                             col, grp, first, m_run, l_part);
         }
     } else {
         // the head's last tile is the only one with fewer than 16 positions
@@ -1567,87 +1725,41 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
                     const int rb2 = (int)(((bs + 32u * (uint32_t)mi) & (DR_RING - 1)) >> 1);
                     if (mj <= 32 && rb2 + 16 * mj <= DR_RING_E && t + 1 != t_part) {
                         land(bs, 32u * (uint32_t)(mi + mj));
-                        ring_pair(rb, mi, rb2, mj, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        ring_pair<RT>(rb, mi, rb2, mj, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                         t += 2;
                         continue;
                     }
                 }
                 land(bs, 32u * (uint32_t)mi);
                 if (small) {
-                    ring_tile<false, false, 1, 2>(rb, mi, 0, CHUNK, false, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                    ring_tile<false, false, 1, 2, RT>(rb, mi, 0, CHUNK, false, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                 } else {
                     const int i0 = 16 * (t & 15);
                     const int64_t ct = (int64_t)(t >> 4) * CHUNK;
                     const int Tc = (int)(p.N - ct < CHUNK ? p.N - ct : CHUNK);
                     const bool partial = t == t_part;
                     if (!wrap) {
-                        if (mi <= 32) ring_tile<false, false, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
-                        else if (mi <= 64) ring_tile<false, false, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
-                        else ring_tile<false, false, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        if (mi <= 32) ring_tile<false, false, 1, 2, RT>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else if (mi <= 64) ring_tile<false, false, 2, 4, RT>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else ring_tile<false, false, 4, 8, RT>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                     } else {
-                        if (mi <= 32) ring_tile<false, true, 1, 2>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
-                        else if (mi <= 64) ring_tile<false, true, 2, 4>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
-                        else ring_tile<false, true, 4, 8>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        if (mi <= 32) ring_tile<false, true, 1, 2, RT>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else if (mi <= 64) ring_tile<false, true, 2, 4, RT>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
+                        else ring_tile<false, true, 4, 8, RT>(rb, mi, i0, Tc, partial, rK16, rV16, qfr, sm.kmask, col, grp, first, m_run, l_part);
                     }
                 }
                 ++t;
             }
         }
     }
-    if (first) m_run = -INFINITY;      // no tile: an empty partial
-    f32x4 acc[8];
-    acc_read(acc);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-    // ---- 5. combine: the coded waves into record 1 + j, the exact waves into record 0, each
-    //         in wave order (log2 units here; the records hold the maxima in natural-log units,
-    //         as the merge reads them).  Lane (col, grp) holds query row col.
-    const float lsum = xsum32(xsum16(l_part));
-    if (lane < 16) { sm.cm[wave * 16 + col] = m_run; sm.cl[wave * 16 + col] = lsum; }
-    __syncthreads();   // also: every wave is done with its ring, which comb reuses
-    const int wc = DR_WAVES - nxw;
-    if (tid < 32) {
-        const int r = tid & 15;
-        const int w_lo = tid >= 16 ? wc : 0, w_hi = tid >= 16 ? DR_WAVES : wc;
-        float M = -INFINITY;
-        for (int w = w_lo; w < w_hi; ++w) M = fmaxf(M, sm.cm[w * 16 + r]);
-        float Ls = 0.f;
-        for (int w = w_lo; w < w_hi; ++w) {
-            const float mw = sm.cm[w * 16 + r];
-            Ls += mw == -INFINITY ? 0.f : sm.cl[w * 16 + r] * __builtin_amdgcn_exp2f(mw - M);
-        }
-        sm.mrow[tid] = M;
-        sm.lrow[tid] = Ls;
-    }
-    __syncthreads();
-    {
-        const float mref = sm.mrow[(xw ? 16 : 0) + col];
-        const float fac = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mref);
-        if (col < nr4) {
-#pragma unroll
-            for (int b = 0; b < 8; ++b)
-                *reinterpret_cast<f32x4*>(&sm.comb[(wave * 16 + col) * DC_CROW + 16 * b + 4 * grp]) = acc[b] * fac;
-        }
-    }
-    __syncthreads();
-    float* recs = p.part + (int64_t)unit * p.nrec * DC_REC;
-    const int n4 = nr4 * D / 4;
-    for (int part = 0; part < (lastwg ? 2 : 1); ++part) {
-        float* rec = recs + (int64_t)(part ? 0 : 1 + j) * DC_REC;
-        const int w_lo = part ? wc : 0, w_hi = part ? DR_WAVES : wc;
-        for (int idx = tid; idx < n4; idx += DR_THREADS) {
-            const int ci = (idx >> 5) * DC_CROW + 4 * (idx & 31);   // row idx/32, float4 idx%32
-            f32x4 s = {0.f, 0.f, 0.f, 0.f};
-            for (int w = w_lo; w < w_hi; ++w) s += *reinterpret_cast<const f32x4*>(sm.comb + w * 16 * DC_CROW + ci);
-            reinterpret_cast<f32x4*>(rec + 32)[idx] = s;
-        }
-        if (tid < 16) {
-            rec[tid] = sm.mrow[16 * part + tid] * 0.6931471805599453f;   // ln 2: log2 -> natural units
-            rec[16 + tid] = sm.lrow[16 * part + tid];
-        }
+    combine_records<0, RT>(p, sm, unit, nqp, j, lastwg, nxw, xw, wave, lane, tid, col, grp, first[0], m_run[0], l_part[0]);
+    if constexpr (RT == 2) {
+        __syncthreads();   // every wave is done with the first row tile's combine area
+        combine_records<RT - 1, RT>(p, sm, unit, nqp, j, lastwg, nxw, xw, wave, lane, tid, col, grp, first[RT - 1],
+                                    m_run[RT - 1], l_part[RT - 1]);
     }
 }
-
 // ----------------------------------------------------------------------------------------
 // Merge of the partial records of one (sequence, KV head, row tile): log-sum-exp over the
 // records (record 0 = exact slots, original space; records 1.. = coded tile ranges, rank
@@ -2314,6 +2426,7 @@ struct DecPlan {
     int nrec, n_ablk, ns;      // records per unit; residual codec: anchor records, score rows
     int64_t na;
     bool ring;                 // decode_ring_kernel (n_wg = its workgroups per unit)
+    int rt;                    // ring kernel: row tiles per wave (2 for a batch of query rows)
 };
 
 // allow_ring: bf16 coefficients of the plain codec go to the ring kernel when every wave's
@@ -2344,8 +2457,11 @@ static DecPlan plan_decode(const varrate_shape& sh, int S, int Q, bool allow_rin
     pl.nrec = pl.n_wg + 1 + pl.n_ablk;
     pl.ns = rows_total < 16 ? (rows_total + 3) & ~3 : 16;
     pl.ring = false;
+    pl.rt = pl.nqt >= 2 ? 2 : 1;
     if (allow_ring && sh.dtype == VARRATE_BF16 && !sh.rope && pl.na == 0 && units > 0) {
-        const int wpu = DR_CUS / units > 1 ? DR_CUS / units : 1;
+        // the ring kernel's units: (sequence, KV head, group of rt row tiles)
+        const int ru = units / pl.nqt * ((pl.nqt + pl.rt - 1) / pl.rt);
+        const int wpu = DR_CUS / ru > 1 ? DR_CUS / ru : 1;
         const int ncw_min = wpu == 1 ? DR_WAVES - 4 : DR_WAVES * wpu - DR_WAVES;   // n_xw at its cap
         if ((pl.total_tiles + ncw_min - 1) / ncw_min <= DR_MAX_TPW) {
             pl.ring = true;
@@ -2444,8 +2560,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
     }
     const size_t es = sh.dtype == VARRATE_BF16 ? 2 : 4;
     const size_t qstride = (size_t)Q * sh.H * D * es;
-    const size_t lds = pl.ring ? DR_SMEM : decode_smem_bytes(pl.cpw, rope);
-    if (pl.ring) kfn = decode_ring_kernel;
+    const size_t lds = pl.ring ? (pl.rt == 2 ? dr_smem<2>() : dr_smem<1>()) : decode_smem_bytes(pl.cpw, rope);
+    if (pl.ring) kfn = pl.rt == 2 ? decode_ring_kernel<2> : decode_ring_kernel<1>;
     e = ensure_lds_limit((const void*)kfn, lds);
     if (e != hipSuccess) return e;
     for (int s0 = 0; s0 < S; s0 += DC_SEQ) {
@@ -2549,7 +2665,8 @@ hipError_t launch_decode(const varrate_shape& sh, const varrate_cache* caches, i
             nxw = nxw > X ? X : nxw;
             prm.n_xw = nxw < 1 ? 1 : nxw;
         }
-        const unsigned nblk = (unsigned)(prm.units * (pl.ring ? pl.n_wg : pl.n_wg + 1));
+        const unsigned nblk = pl.ring ? (unsigned)(prm.units / pl.nqt * ((pl.nqt + pl.rt - 1) / pl.rt) * pl.n_wg)
+                                      : (unsigned)(prm.units * (pl.n_wg + 1));
         kfn<<<nblk, pl.ring ? DR_THREADS : DC_THREADS, lds, st>>>(prm);
         e = hipGetLastError();
         if (e != hipSuccess) return e;

@@ -168,6 +168,30 @@ def test_decode_accumulator_agprs_are_private():
         m = re.search(r"\.set " + re.escape(name) + r"\.num_agpr, (\d+)", text)
         if m:
             assert int(m.group(1)) == 32
+    # the ring kernel: one row tile per wave keeps a0..a31 to itself as above; two row tiles
+    # (a32..a63 for the second) may leave the compiler AGPRs for its own values, but only
+    # above a63, never in the accumulators' registers
+    rings = {rt: body for _, rt, body in
+             re.findall(r"^(_ZN2vr18decode_ring_kernelILi([12])EEEvNS_9DecParamsE):[^\n]*\n(.*?)s_endpgm",
+                        text, re.S | re.M)}
+    assert sorted(rings) == ["1", "2"]
+    for rt, body in rings.items():
+        inside = False
+        used = []
+        for line in body.splitlines():
+            if ";;#ASMSTART" in line:
+                inside = True
+                continue
+            if ";;#ASMEND" in line:
+                inside = False
+                continue
+            code = line.split(";")[0]
+            if inside or not agpr.search(code):
+                continue
+            used += [int(x) for x in re.findall(r"\ba(\d+)\b", code)]
+            for lo, hi in re.findall(r"\ba\[(\d+):(\d+)\]", code):
+                used += list(range(int(lo), int(hi) + 1))
+            assert rt == "2" and used and min(used) >= 64, f"ring kernel RT={rt}: compiler AGPR use: {line.strip()}"
 
 
 def test_noalloc_decode_validates_and_bounds_its_scratch(L):

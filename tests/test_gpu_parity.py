@@ -447,6 +447,34 @@ def test_end_to_end(vr, oracle_lib, name):
     assert max(errs) <= DEC_TOL_BF16
 
 
+@pytest.mark.parametrize("Q", [8, 9, 13])
+def test_decode_row_tile_pairs(vr, oracle_lib, Q):
+    """Batches of query rows decode two row tiles per wave: Q = 8 (32 rows per KV head, one
+    pair of full row tiles), 9 (36 rows: a pair, then a row tile whose partner is past the
+    last) and 13 (52 rows: two pairs, the second one's partner holding 4 rows), two sequences;
+    every query against the oracle."""
+    import torch
+    from workloads import CONFIGS, make_layer
+    cfg = dict(CONFIGS["llama_32k"])
+    cfg.update(n=1300, G=2, H=8, seed=91)
+    shape = vr.Shape(n=1300, G=2, H=8, w=32, r_min=16, kappa_pct=20, dtype="bf16")
+    say(f"[row tile pairs] Q={Q}")
+    caches, qs, refs = [], [], []
+    for s in range(2):
+        li = make_layer(cfg, seq=s, n_queries=Q, n=1300)
+        oc = oracle_lib.compress(li.K, li.V, li.Qw, li.PK, li.PV, 8, 20, 16, "bf16")
+        cache, _, PK, PV = gpu_compress(vr, shape, li, sbar=oc.sbar)
+        caches.append(cache)
+        qs.append(li.q)
+        refs.append([oracle_lib.decode(oc.coefK, oc.coefV, oc.alloc.rank, oc.Kx, oc.Vx, li.PK, li.PV, li.q[i], 8)
+                     for i in range(Q)])
+    out = host(vr.decode(shape, caches, dev(np.stack(qs), torch.bfloat16), PK, PV))
+    torch.cuda.synchronize()
+    worst = max(decode_err(out[s][i], refs[s][i]) for s in range(2) for i in range(Q))
+    say(f"  worst decode rel err {worst:.3e}")
+    assert worst <= DEC_TOL_BF16
+
+
 def test_decode_multi_sequence_many_queries_appended(vr, oracle_lib):
     """S = 3 independent sequences, Q = 5 queries each (20 query rows per KV head: two row
     tiles), ragged last chunk, and 3 exact tokens appended after compression."""
