@@ -72,12 +72,25 @@ __device__ __forceinline__ void top4_push(Top4& t, float k, uint32_t a) {
     }
 }
 
-// ---- distance GEMM + per-tile top 4.  Workgroup: 4 waves, 128 anchors (A operand, staged in
-// LDS in fragment order, shared) x 128 tokens (B operand, wave w: tokens 32 w .. 32 w + 31 as
-// two 16-token column tiles, loaded straight from memory).  C[anchor][token]: lane -> token
-// column (lane % 16) and anchors 4 (lane / 16) + v of each 16-anchor row tile.  Workgroups are
-// mapped so that all anchor tiles of one token tile run on the same XCD (its token rows stay
-// in that XCD's L2).
+// ---- distance GEMM + per-tile top 4.  Workgroup: 4 waves, 128 anchors x 128 tokens; wave
+// (wa, wt) = (wave / 2, wave % 2) computes anchors 64 wa .. 64 wa + 63 (four 16-row tiles, A
+// operand) against tokens 64 wt .. 64 wt + 63 (four 16-column tiles, B operand): 16 MFMA
+// 16x16x32 per step of 32 elements of z.  Both operands are staged in LDS in fragment order by
+// direct-to-LDS loads: one 1 KB load per 16-row (or 16-column) tile and step, lane l bringing
+// row l % 16's elements 8 (l / 16) .. + 7, so every fragment read is one conflict-free 16-byte
+// read per lane.  AS_NS stages of 16 KB rotate (each wave issues 4 loads per stage and waits
+// on its own load count); a step's barrier also frees the buffer the next issue reuses.  Three
+// stages measured best: 0.53 ms for the 32K layer against 0.61 with four and 0.82 with eight
+// (one workgroup per CU then), and 0.65 ms for the earlier form (one step of lookahead, the
+// token operand loaded straight into registers).
+// C[anchor][token]: lane -> token column (lane % 16) and anchors 4 (lane / 16) + v of each
+// 16-anchor row tile.  Workgroups are mapped so that all anchor tiles of one token tile run on
+// the same XCD (its token rows stay in that XCD's L2).
+constexpr int AS_NS = 3;                                 // stages in the ring (three workgroups per CU)
+constexpr int AS_STAGE = (AN_TA / 16 + AN_TT / 16) * 1024;   // bytes per stage (A then B tiles)
+constexpr size_t AS_LDS = (size_t)AS_NS * AS_STAGE;      // 48 KB
+static_assert(AN_TA == 128 && AN_TT == 128, "one 1 KB load per 16-row tile; 16 loads per stage");
+
 struct AnSearch {
     const uint16_t* K;
     const uint16_t* V;
@@ -94,76 +107,83 @@ __device__ __forceinline__ const uint16_t* anc_zrow(const AnSearch& p, int64_t t
 }
 
 __global__ __launch_bounds__(256) void anc_search(AnSearch p) {
-    __shared__ u32x4 afrag[2][AN_TA / 16][64];      // [buffer][row tile][lane]: 16 KB
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
     const int col = lane & 15, grp = lane >> 4;
+    const int wa = wave >> 1, wt = wave & 1;
     // XCD-aware order: the 8 XCDs take consecutive workgroup ids in turn
     const int b = blockIdx.x;
     const int xcd = b & 7, k = b >> 3;
     const int tt = xcd + 8 * (k / p.n_atiles), at = k % p.n_atiles;
     if (tt >= p.n_ttiles) return;
-    const int64_t i0 = (int64_t)tt * AN_TT + 32 * wave;       // this wave's first coded token
+    const int64_t i0 = (int64_t)tt * AN_TT;
     const int64_t a0 = (int64_t)at * AN_TA;
-    // token rows of the wave's two column tiles (clamped: rows past Nc are dropped later)
-    int64_t trow[2];
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2) {
-        int64_t i = i0 + 16 * c2 + col;
-        i = i < p.Nc ? i : p.Nc - 1;
-        trow[c2] = anc_token(i, p.delta);
-    }
-    // anchor pieces this thread stages: 2 of the 512 (anchor, group) pieces of a K-step
-    int64_t arow[2];
-    int aj[2], al[2];
+    // this wave's loads of a stage: A row tiles 2 wave, 2 wave + 1 and B column tiles 2 wave,
+    // 2 wave + 1; lane row l % 16, elements 8 (l / 16) .. + 7 of the step (rows clamped: rows
+    // past the anchors or tokens are dropped later)
+    int64_t lrow[4];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-        const int piece = tid + 256 * u;                     // anchor piece (a16 tile, lane)
-        aj[u] = piece >> 6;                                  // row tile
-        al[u] = piece & 63;                                  // fragment lane
-        int64_t a = a0 + 16 * aj[u] + (al[u] & 15);
+        int64_t a = a0 + 16 * (2 * wave + u) + col;
         a = a < p.na ? a : p.na - 1;
-        arow[u] = a * p.delta;
+        lrow[u] = a * p.delta;
+        int64_t i = i0 + 16 * (2 * wave + u) + col;
+        i = i < p.Nc ? i : p.Nc - 1;
+        lrow[2 + u] = anc_token(i, p.delta);
     }
-    f32x4 acc[2][AN_TA / 16];
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-        for (int j = 0; j < AN_TA / 16; ++j) acc[c2][j] = f32x4{0, 0, 0, 0};
+    const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(__attribute__((address_space(3))) uint8_t*)smem);
     const int steps = 2 * p.GD / 32;
-    u32x4 an[2], tk[2];
-    auto load_step = [&](int s) {
-        const int kk = 32 * s;
+    auto issue = [&](int s) {
+        const int kk = 32 * s + 8 * grp;
+        const uint32_t st = lds0 + (uint32_t)(s % AS_NS) * AS_STAGE;
 #pragma unroll
-        for (int u = 0; u < 2; ++u) an[u] = load16(anc_zrow(p, arow[u], kk + 8 * (al[u] >> 4)));
-#pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2) tk[c2] = load16(anc_zrow(p, trow[c2], kk + 8 * grp));
-    };
-    load_step(0);
-    for (int s = 0; s < steps; ++s) {
-        const int buf = s & 1;
-#pragma unroll
-        for (int u = 0; u < 2; ++u) afrag[buf][aj[u]][al[u]] = an[u];
-        const u32x4 t0 = tk[0], t1 = tk[1];
-        __syncthreads();
-        if (s + 1 < steps) load_step(s + 1);                // next step's loads fly meanwhile
-#pragma unroll
-        for (int j = 0; j < AN_TA / 16; ++j) {
-            const u32x4 a = afrag[buf][j][lane];
-            acc[0][j] = mfma(a, t0, acc[0][j]);
-            acc[1][j] = mfma(a, t1, acc[1][j]);
+        for (int u = 0; u < 4; ++u) {
+            // tile index in the stage: A tiles 0..7, then B tiles 8..15
+            const uint32_t dst = st + 1024u * (uint32_t)((u < 2 ? 0 : 8) + 2 * wave + (u & 1));
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                         :: "v"(anc_zrow(p, lrow[u], kk)), "s"(dst) : "memory", "m0");
         }
-    }
-    // ---- keys and the 4 best per token: per lane, then over the 4 lanes of a token
+    };
+    f32x4 acc[4][4];                          // [row tile][column tile] of this wave
 #pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2) {
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[j][c] = f32x4{0, 0, 0, 0};
+    for (int s = 0; s < AS_NS - 1 && s < steps; ++s) issue(s);
+    for (int s = 0; s < steps; ++s) {
+        // stage s has landed when at most the loads of the stages after it are in flight
+        static_assert(AS_NS == 3, "the wait below leaves one later stage (4 loads) in flight");
+        if (s + AS_NS - 2 < steps) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();                      // every wave's part of stage s; stage s - 1 is free
+        if (s + AS_NS - 1 < steps) issue(s + AS_NS - 1);
+        const u32x4* sa = reinterpret_cast<const u32x4*>(smem + (size_t)(s % AS_NS) * AS_STAGE);
+        const u32x4* sb = sa + 8 * 64;
+        u32x4 fa[4], fb[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) fa[j] = sa[(4 * wa + j) * 64 + lane];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) fb[c] = sb[(4 * wt + c) * 64 + lane];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) acc[j][c] = mfma(fa[j], fb[c], acc[j][c]);
+    }
+    // ---- keys and the 4 best per token of this wave's 64 anchors: per lane, then over the 4
+    //      lanes of a token; then the two anchor halves of the workgroup through LDS
+    __syncthreads();                          // every wave is done with the stages
+    float* xk = reinterpret_cast<float*>(smem);                  // [wt][4 col tiles][16][4]
+    uint32_t* xa = reinterpret_cast<uint32_t*>(smem + 2 * 4 * 16 * AN_C * 4);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
         Top4 t;
         top4_init(t);
 #pragma unroll
-        for (int j = 0; j < AN_TA / 16; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int64_t a = a0 + 16 * j + 4 * grp + v;
-                if (a < p.na) top4_push(t, p.nrm[a] - 2.f * acc[c2][j][v], (uint32_t)a);
+                const int64_t a = a0 + 64 * wa + 16 * j + 4 * grp + v;
+                if (a < p.na) top4_push(t, p.nrm[a] - 2.f * acc[j][c][v], (uint32_t)a);
             }
 #pragma unroll
         for (int m = 16; m <= 32; m <<= 1) {
@@ -177,11 +197,21 @@ __global__ __launch_bounds__(256) void anc_search(AnSearch p) {
 #pragma unroll
             for (int q = 0; q < AN_C; ++q) top4_push(t, ok[q], oa[q]);
         }
-        const int64_t i = i0 + 16 * c2 + col;
-        if (grp == 0 && i < p.Nc) {
-            const int64_t o = ((int64_t)at * p.Nc + i) * AN_C;
+        const int slot = ((wt * 4 + c) * 16 + col) * AN_C;
+        if (wa == 1 && grp == 0) {
 #pragma unroll
-            for (int q = 0; q < AN_C; ++q) { p.pk[o + q] = t.k[q]; p.pa[o + q] = t.a[q]; }
+            for (int q = 0; q < AN_C; ++q) { xk[slot + q] = t.k[q]; xa[slot + q] = t.a[q]; }
+        }
+        __syncthreads();
+        if (wa == 0) {
+#pragma unroll
+            for (int q = 0; q < AN_C; ++q) top4_push(t, xk[slot + q], xa[slot + q]);
+            const int64_t i = i0 + 64 * wt + 16 * c + col;
+            if (grp == 0 && i < p.Nc) {
+                const int64_t o = ((int64_t)at * p.Nc + i) * AN_C;
+#pragma unroll
+                for (int q = 0; q < AN_C; ++q) { p.pk[o + q] = t.k[q]; p.pa[o + q] = t.a[q]; }
+            }
         }
     }
 }
@@ -364,7 +394,9 @@ hipError_t launch_anchor_search(const varrate_shape& sh, const void* K, const vo
     p.n_atiles = anc_atiles(sh);
     // 8 XCDs, each with ceil(n_ttiles / 8) token tiles x n_atiles anchor tiles
     const int64_t per_xcd = (int64_t)((p.n_ttiles + 7) / 8) * p.n_atiles;
-    anc_search<<<(unsigned)(8 * per_xcd), 256, 0, st>>>(p);
+    hipError_t e = ensure_lds_limit((const void*)anc_search, AS_LDS);
+    if (e != hipSuccess) return e;
+    anc_search<<<(unsigned)(8 * per_xcd), 256, AS_LDS, st>>>(p);
     anc_merge<<<(unsigned)((Nc + 255) / 256), 256, 0, st>>>(w.pk, w.pa, Nc, p.n_atiles, nn);
     return hipGetLastError();
 }
