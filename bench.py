@@ -48,7 +48,8 @@ def parse():
                     help="default run only: skip the 32-layer 128K stack that the line also reports")
     ap.add_argument("--mode", choices=("bench", "pmc"), default="bench",
                     help="pmc: a short run for hardware-counter passes (eager decodes on distinct "
-                         "cache slots, then plain 64 MiB device copies that calibrate the byte counters)")
+                         "cache slots, then plain 64 MiB device copies that calibrate the byte counters; "
+                         "with --config agnostic_32k: eight eager batch-64 decodes of the 20%% cache)")
     return ap.parse_args()
 
 
@@ -841,6 +842,20 @@ def bench_agnostic(args):
         e = e.flatten().cpu().numpy()
         return {"mean": round(float(e.mean()), 5), "p95": round(float(np.percentile(e, 95)), 5),
                 "max": round(float(e.max()), 5)}
+
+    if args.mode == "pmc":
+        # Counter passes: the 20% cache decoded eagerly 8 times as one batch of 64 queries.
+        kappa, r_min = next(b for b in cfg["budgets"] if b[0] == 20)
+        shape = vr.Shape(n=n, G=G, H=H, w=w, r_min=r_min, kappa_pct=kappa, dtype="bf16")
+        cache = vr.compress(shape, dl.K, dl.V, Qw, PK, PV)
+        ws = vr.decode_workspace(shape, 1, Qn, dev)
+        out = torch.empty_like(q)
+        for _ in range(8):
+            vr.decode(shape, [cache], q, PK, PV, out=out, workspace=ws)
+        torch.cuda.synchronize()
+        print(json.dumps({"mode": "pmc", "config": args.config, "decode_launches": 8,
+                          "decode_bytes": int(decode_bytes(shape, cache, Qn))}), flush=True)
+        return
 
     rows = []
     for kappa, r_min in cfg["budgets"]:

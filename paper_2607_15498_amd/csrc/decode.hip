@@ -887,7 +887,8 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB || ROPE) ? 2 : 4) void decod
     //          V.  Every wave issues exactly DC_LPR loads per round, whatever the round holds
     //          (lanes and blocks past its units reload its last unit into the unused tail of
     //          the buffer), so a wait for "all but the next round's DC_LPR loads" is exact.
-    //          Issued in asm, so the compiler adds no wait of its own for them.
+    //          Issued in asm, so the compiler adds no wait of its own for them; non-temporal, so
+    //          the streamed coefficients leave L2 before the bases and metadata do.
     auto issue = [&](const Round& r, int buf) {
         const uint8_t* kr = kg + (size_t)r.s0 * sizeof(ET);     // wave-uniform round bases
         const uint8_t* vr = vg + (size_t)r.s0 * sizeof(ET);
@@ -904,9 +905,9 @@ __global__ __launch_bounds__(DC_THREADS, (F32 || QB || ROPE) ? 2 : 4) void decod
             const uint8_t* srcv = vr + 16u * uu;
             const uint32_t dk = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_u8*)(bk + 1024 * m));
             const uint32_t dv = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_u8*)(bv + 1024 * m));
-            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
                          :: "v"(srck), "s"(dk) : "memory", "m0");
-            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
                          :: "v"(srcv), "s"(dv) : "memory", "m0");
         }
     };
@@ -1549,7 +1550,9 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
     //         its end masked), into ring slot u mod 8 of K and of V; two loads per unit.  The
     //         first 8 units go out now; a range of fewer units is padded with one-lane loads of
     //         its first bytes into the slots it leaves unused, so exactly 16 ring loads are
-    //         younger than the basis when it is waited for.
+    //         younger than the basis when it is waited for.  The coefficients are read once per
+    //         call, so the loads carry the non-temporal hint: their lines leave L2 first, and the
+    //         small data every call reuses (bases, ranks, chunk table, records) stays there.
     uint8_t* rK = sm.ring + (size_t)wave * 2 * DR_RS;
     uint8_t* rV = rK + DR_RS;
     const int64_t hoff = xw ? (int64_t)g * p.cap * D : (int64_t)g * p.coef_stride;
@@ -1565,9 +1568,9 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
         const uint32_t o = base + (uint32_t)u * DR_UNIT + lane16;
         const uint32_t sl = (uint32_t)(u & (DR_NU - 1)) * DR_UNIT;
         if (o < eb) {     // lane 0 always is: unit u < n_units starts before the range's end
-            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
                          :: "v"(kg + o), "s"(ldsK + sl) : "memory", "m0");
-            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
                          :: "v"(vg + o), "s"(ldsV + sl) : "memory", "m0");
         }
     };
@@ -1577,9 +1580,9 @@ __global__ __launch_bounds__(DR_THREADS, 1) void decode_ring_kernel(DecParams p)
             issue(u);
         } else if (lane == 0) {
             const uint32_t sl = (uint32_t)u * DR_UNIT;
-            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
                          :: "v"(kg + base), "s"(ldsK + sl) : "memory", "m0");
-            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+            asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
                          :: "v"(vg + base), "s"(ldsV + sl) : "memory", "m0");
         }
     }
