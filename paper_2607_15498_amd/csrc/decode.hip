@@ -1365,15 +1365,23 @@ __device__ __forceinline__ void combine_records(const DecParams& p, const RingSm
     __syncthreads();   // also: every wave is done with its ring, which comb reuses
     const int wc = DR_WAVES - nxw;
     if (tid < 32) {
+        // every wave's entries are read at once (fixed trip count, waves outside [w_lo, w_hi)
+        // predicated off), then folded in wave order
         const int r = tid & 15;
         const int w_lo = tid >= 16 ? wc : 0, w_hi = tid >= 16 ? DR_WAVES : wc;
-        float M = -INFINITY;
-        for (int w = w_lo; w < w_hi; ++w) M = fmaxf(M, sm.cm[w * 16 + r]);
-        float Ls = 0.f;
-        for (int w = w_lo; w < w_hi; ++w) {
-            const float mw = sm.cm[w * 16 + r];
-            Ls += mw == -INFINITY ? 0.f : sm.cl[w * 16 + r] * __builtin_amdgcn_exp2f(mw - M);
+        float mw[DR_WAVES], lw[DR_WAVES];
+#pragma unroll
+        for (int w = 0; w < DR_WAVES; ++w) {
+            mw[w] = sm.cm[w * 16 + r];
+            lw[w] = sm.cl[w * 16 + r];
         }
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < DR_WAVES; ++w) M = w >= w_lo && w < w_hi ? fmaxf(M, mw[w]) : M;
+        float Ls = 0.f;
+#pragma unroll
+        for (int w = 0; w < DR_WAVES; ++w)
+            if (w >= w_lo && w < w_hi) Ls += mw[w] == -INFINITY ? 0.f : lw[w] * __builtin_amdgcn_exp2f(mw[w] - M);
         sm.mrow[tid] = M;
         sm.lrow[tid] = Ls;
     }
@@ -1395,8 +1403,13 @@ __device__ __forceinline__ void combine_records(const DecParams& p, const RingSm
         const int w_lo = part ? wc : 0, w_hi = part ? DR_WAVES : wc;
         for (int idx = tid; idx < n4; idx += DR_THREADS) {
             const int ci = (idx >> 5) * DC_CROW + 4 * (idx & 31);   // row idx/32, float4 idx%32
+            f32x4 cw[DR_WAVES];
+#pragma unroll
+            for (int w = 0; w < DR_WAVES; ++w) cw[w] = *reinterpret_cast<const f32x4*>(sm.comb + w * 16 * DC_CROW + ci);
             f32x4 s = {0.f, 0.f, 0.f, 0.f};
-            for (int w = w_lo; w < w_hi; ++w) s += *reinterpret_cast<const f32x4*>(sm.comb + w * 16 * DC_CROW + ci);
+#pragma unroll
+            for (int w = 0; w < DR_WAVES; ++w)
+                if (w >= w_lo && w < w_hi) s += cw[w];
             reinterpret_cast<f32x4*>(rec + 32)[idx] = s;
         }
         if (tid < 16) {
