@@ -262,22 +262,19 @@ __global__ __launch_bounds__(SL_THREADS, 4) void sal_rowstats(const void* __rest
     for (int j = 0; j < SL_MAX_RT; ++j) {
         const int rt = wave + SL_WAVES * j;
         if (rt >= nrt) continue;
-        // combine the 16 lanes (keys) that share a row (lane bits 0..3), in natural-log units
+        // combine the 16 lanes (keys) that share a row (lane bits 0..3), in natural-log units:
+        // the row's maximum over the lanes, then each lane's sum rescaled to it once and the
+        // sums added over the lanes
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            float mm = m[j][v] * 0.6931471805599453f, ll = l[j][v];
+            const float mm = m[j][v] * 0.6931471805599453f;
+            const float M = wave_max16(mm);
+            float ll = mm == -INFINITY ? 0.f : l[j][v] * fast_exp(mm - M);
 #pragma unroll
-            for (int off = 1; off < 16; off <<= 1) {
-                const float mo = shfl_xor_f(mm, off), lo = shfl_xor_f(ll, off);
-                const float mn = fmaxf(mm, mo);
-                const float a = mm == -INFINITY ? 0.f : ll * fast_exp(mm - mn);
-                const float b = mo == -INFINITY ? 0.f : lo * fast_exp(mo - mn);
-                mm = mn;
-                ll = a + b;
-            }
+            for (int off = 1; off < 16; off <<= 1) ll += shfl_xor_f(ll, off);
             const int rho = rt * 16 + (lane >> 4) * 4 + v;
             if ((lane & 15) == 0 && rho < rows)
-                stats[((int64_t)g * rows + rho) * nw + wgi] = make_float2(mm, ll);
+                stats[((int64_t)g * rows + rho) * nw + wgi] = make_float2(M, ll);
         }
     }
 }
