@@ -193,7 +193,7 @@ def cpu_baseline(cfg, li, dbytes, gpu, decode_reps=24, qwen_layers=4, llama128_l
 # passes of `bench.py --mode pmc`, scaled by a 64 MiB copy kernel (FETCH x 2.0, WRITE x 1.0).
 # They hold for the decode source they were taken on (SHA-256 prefix of the files below);
 # after any change to it, traffic is reported as null until the counters are taken again.
-DECODE_TRAFFIC = {"source_sha256": "210297cefe320ae9", "bytes": 31468339}
+DECODE_TRAFFIC = {"source_sha256": "7bfcb5b3f285c259", "bytes": 31487296}
 DECODE_SOURCES = ("paper_2607_15498_amd/csrc/decode.hip", "paper_2607_15498_amd/csrc/vr_device.h")
 
 
